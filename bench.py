@@ -1,0 +1,214 @@
+#!/usr/bin/env python
+"""Benchmark of the Gefen optimizer step on one MI355X.
+
+Metric: optimizer-step Gparams/s (parameters updated per second) and achieved HBM GB/s
+(algorithmic bytes / time) as a fraction of MI355X's 8 TB/s peak, on one GPU.
+
+A step is one ``gefen_step`` over every tensor of the workload (all kernel classes),
+with parameters, gradients and optimizer state resident in HBM. The default workload
+is the Llama-3 1.5B shape (1,498,482,688 fp32 parameters, bf16 gradients with
+Student-t(3) noise and per-row / per-head scales); gradients for two steps are drawn
+before timing and alternated, so the timed region contains only optimizer steps.
+
+Prints one JSON line. ``roofline`` describes the dominant kernel class: algorithmic
+bytes per launch over its mean launch time, from HIP events recorded on the step's
+stream. ``traffic`` comes from committed rocprofv3 counter summaries when they were
+taken on the current kernel source, else null. ``cpu_baseline`` is the float64 oracle
+(single thread, as it stands) timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBPS = 8000.0
+METRIC = "optimizer-step Gparams/s and achieved HBM GB/s (% of MI355X peak), 1 GPU"
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for name in ("step.hip", "gefen_internal.h"):
+        with open(os.path.join(ROOT, "paper_2606_13894_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(workload: str, kind: str, vpl: int, gdt: str):
+    """Counter-derived HBM bytes per launch from profiles/, if taken on this source."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        d = json.load(f)
+    if d.get("source_hash") != kernel_source_hash():
+        return None
+    key = f"{kind}/vpl{vpl}/{gdt}"
+    ent = d.get("kernels", {}).get(key)
+    return None if ent is None else ent.get("bytes_per_launch")
+
+
+def cpu_baseline(w, params, grads, st, sample_elems: int):
+    """Time the oracle's step on a bounded sample: whole blocks taken from the start
+    of every tensor in turn until `sample_elems` elements are covered."""
+    import numpy as np
+    import torch
+    import oracle
+    import paper_2606_13894_amd as gf
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    from parity import grad_bits
+
+    lay = st.layout()
+    periods = st.periods
+    codes = st.read(gf.STATE_CODES).cpu().numpy()
+    scale = st.read(gf.STATE_SCALE).cpu().numpy().astype(np.float64)
+    vm = st.read(gf.STATE_V).cpu().numpy().astype(np.float64)
+    cb = st.read(gf.STATE_CB_DEC).cpu().numpy().astype(np.float64)
+    jobs = []
+    left = sample_elems
+    order = sorted(range(len(params)), key=lambda i: -params[i].numel())
+    per_tensor = max(1, sample_elems // max(1, len(order)))
+    for i in order:
+        if left <= 0:
+            break
+        p = periods[i] if periods[i] > 0 else params[i].numel()
+        take = min(params[i].numel(), max(p, (min(per_tensor, left) // p) * p))
+        nb = take // p
+        th = params[i].detach().reshape(-1)[:take].double().cpu().numpy()
+        g = grad_bits(grads[i].reshape(-1)[:take])
+        c0 = lay["code_offsets"][i]
+        b0 = lay["block_index"][i]
+        jobs.append((th, g, codes[c0:c0 + take].copy(), scale[b0:b0 + nb].copy(),
+                     vm[b0:b0 + nb].copy(), np.arange(0, take + 1, p, dtype=np.int64)))
+        left -= take
+    n = sum(j[0].size for j in jobs)
+    t0 = time.perf_counter()
+    for th, g, cq, s, v, offs in jobs:
+        oracle.step_blocks(th, g, cq, s, v, offs, cb, cb, w.lr, w.betas[0], w.betas[1], w.eps,
+                           w.wd, 5)
+    dt = time.perf_counter() - t0
+    return {"value": n / dt / 1e9, "unit": "Gparams/s", "cores": 1, "kind": "oracle",
+            "sample": f"oracle step (float64, single thread) on {n} of {w.numel} elements: "
+                      f"whole blocks from the start of the {len(jobs)} largest tensors",
+            "seconds": dt}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="llama3_1p5b")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-elems", type=int, default=40_000_000)
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: the Gefen step needs no collectives, and a run on "
+              "N GPUs would be N independent copies of this one (see the sharding notes). "
+              "Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import workloads as W
+    import paper_2606_13894_amd as gf
+
+    dev = torch.device("cuda", 0)
+    w = W.get(args.workload)
+    fields = W.scale_fields(w)
+    offsets = None
+    bscales = None
+    if w.n_blocks:
+        offsets = W.stress_block_offsets(w.numel, w.n_blocks)
+        bscales = W.stress_block_scales(w.n_blocks)
+    params = W.init_params(w, dev)
+    grads = [W.make_grads(w, fields, t, dev, block_scales=bscales, offsets=offsets)
+             for t in (1, 2)]
+    torch.cuda.synchronize()
+
+    t0 = time.perf_counter()
+    st = gf.GefenState(grads[0], block_offsets=offsets, eps_part=w.eps)
+    torch.cuda.synchronize()
+    init_s = time.perf_counter() - t0
+
+    hp = (w.lr, w.betas, w.eps, w.wd)
+    t = 0
+    for _ in range(args.warmup):
+        t += 1
+        st.step(params, grads[(t - 1) % 2], *hp, t)
+        if w.refit_every and t % w.refit_every == 0:
+            st.fit_codebook(grads[(t - 1) % 2])
+    torch.cuda.synchronize()
+
+    st.profile_begin(args.steps)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    e0.record()
+    for _ in range(args.steps):
+        t += 1
+        st.step(params, grads[(t - 1) % 2], *hp, t)
+        if w.refit_every and t % w.refit_every == 0:
+            st.fit_codebook(grads[(t - 1) % 2])
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    classes = st.profile_end()
+    ms_per_step = e0.elapsed_time(e1) / args.steps
+
+    n = w.numel
+    step_bytes = sum(c["bytes_per_launch"] for c in classes)
+    gparams = n / (ms_per_step * 1e-3) / 1e9
+    gbps = step_bytes / (ms_per_step * 1e-3) / 1e9
+    dom = max(classes, key=lambda c: c["bytes_per_launch"])
+    dom_ms = dom["total_ms"] / max(1, dom["launches"])
+    achieved = dom["bytes_per_launch"] / (dom_ms * 1e-3) / 1e9
+    traffic = read_traffic(w.name, dom["kind"], dom["vpl"], dom["grad_dtype"])
+    persistent, workspace = st.state_bytes()
+
+    line = {
+        "metric": METRIC,
+        "value": round(gparams, 3),
+        "unit": "Gparams/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "params": n, "tensors": len(w.tensors),
+                   "grad_dtype": w.grad_dtype, "code_bits": 8,
+                   "refit_every": w.refit_every or None},
+        "hbm_gbps": round(gbps, 1),
+        "pct_peak_hbm": round(100.0 * gbps / PEAK_HBM_GBPS, 2),
+        "bytes_per_step": step_bytes,
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS,
+                     "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
+                     "traffic": traffic,
+                     "kernel": f"{dom['kind']}/vpl{dom['vpl']}/{dom['grad_dtype']}",
+                     "bytes_per_launch": dom["bytes_per_launch"],
+                     "mean_launch_ms": round(dom_ms, 4)},
+        "kernels": [{k: (round(v, 4) if isinstance(v, float) else v) for k, v in c.items()}
+                    for c in classes],
+        "init_s": round(init_s, 3),
+        "wall_s_timed": round(wall, 3),
+        "state_bytes": {"persistent": persistent, "workspace": workspace},
+        "source_hash": kernel_source_hash(),
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(w, params, grads[t % 2], st, args.cpu_sample_elems)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

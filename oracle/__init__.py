@@ -64,10 +64,10 @@ def _load():
     step_args = [vp, vp, i32, vp, vp, vp]
     lib.oracle_step_blocks.restype = None
     lib.oracle_step_blocks.argtypes = step_args + [vp, i64, vp, vp, i32, f64, f64, f64, f64,
-                                                   f64, i64, i32, vp]
+                                                   f64, i64, i32, vp, vp]
     lib.oracle_step_uniform.restype = None
     lib.oracle_step_uniform.argtypes = step_args + [i64, i64, vp, vp, i32, f64, f64, f64,
-                                                    f64, f64, i64, i32, vp]
+                                                    f64, f64, i64, i32, vp, vp]
     _lib = lib
     return lib
 
@@ -165,8 +165,10 @@ def _step_common(theta, codes, s, v, cb_dec, cb_enc, m_full):
 
 
 def step_uniform(theta, g, codes, s, v, p, cb_dec, cb_enc, lr, beta1, beta2, eps, wd, t,
-                 quantize=True, m_full=None):
-    """Alg. 1 step, uniform blocks of p elements; arrays are updated in place."""
+                 quantize=True, m_full=None, m_out=None):
+    """Alg. 1 step, uniform blocks of p elements; arrays are updated in place.
+
+    ``m_out`` (float64 array, optional) receives the step's unquantized momentum."""
     lib = _load()
     _step_common(theta, codes, s, v, cb_dec, cb_enc, m_full)
     g, dt = _grad(g.reshape(-1))
@@ -177,11 +179,11 @@ def step_uniform(theta, g, codes, s, v, p, cb_dec, cb_enc, lr, beta1, beta2, eps
     lib.oracle_step_uniform(_ptr(theta), _ptr(g), dt, _ptr(codes), _ptr(s), _ptr(v), n,
                             int(p), _ptr(cb_dec), _ptr(cb_enc), cb_enc.size, float(lr),
                             float(beta1), float(beta2), float(eps), float(wd), int(t),
-                            1 if quantize else 0, _ptr(m_full))
+                            1 if quantize else 0, _ptr(m_full), _ptr(m_out))
 
 
 def step_blocks(theta, g, codes, s, v, offsets, cb_dec, cb_enc, lr, beta1, beta2, eps, wd,
-                t, quantize=True, m_full=None):
+                t, quantize=True, m_full=None, m_out=None):
     """Alg. 1 step over explicit blocks [offsets[b], offsets[b+1]); in place."""
     lib = _load()
     _step_common(theta, codes, s, v, cb_dec, cb_enc, m_full)
@@ -194,4 +196,4 @@ def step_blocks(theta, g, codes, s, v, offsets, cb_dec, cb_enc, lr, beta1, beta2
     lib.oracle_step_blocks(_ptr(theta), _ptr(g), dt, _ptr(codes), _ptr(s), _ptr(v),
                            _ptr(offs), nb, _ptr(cb_dec), _ptr(cb_enc), cb_enc.size,
                            float(lr), float(beta1), float(beta2), float(eps), float(wd),
-                           int(t), 1 if quantize else 0, _ptr(m_full))
+                           int(t), 1 if quantize else 0, _ptr(m_full), _ptr(m_out))

@@ -333,7 +333,7 @@ void oracle_step_blocks(double* theta, const void* g, int32_t dtype, uint8_t* co
                         double* s, double* v, const int64_t* offs, int64_t nblocks,
                         const double* cb_dec, const double* cb_enc, int32_t k,
                         double lr, double beta1, double beta2, double eps, double wd,
-                        int64_t t, int32_t quantize, double* m_full)
+                        int64_t t, int32_t quantize, double* m_full, double* m_out)
 {
     double bc1 = 1.0 - pow(beta1, (double)t);
     double bc2 = 1.0 - pow(beta2, (double)t);
@@ -357,6 +357,7 @@ void oracle_step_blocks(double* theta, const void* g, int32_t dtype, uint8_t* co
         double denom = sqrt(vhat) + eps;
         for (int64_t i = lo; i < hi; ++i) {
             double mi = m[i - lo];
+            if (m_out) m_out[i] = mi;
             if (quantize) {
                 int32_t q = 0;
                 if (smax > 0.0) {
@@ -388,12 +389,12 @@ void oracle_step_uniform(double* theta, const void* g, int32_t dtype, uint8_t* c
                          double* s, double* v, int64_t n, int64_t p,
                          const double* cb_dec, const double* cb_enc, int32_t k,
                          double lr, double beta1, double beta2, double eps, double wd,
-                         int64_t t, int32_t quantize, double* m_full)
+                         int64_t t, int32_t quantize, double* m_full, double* m_out)
 {
     int64_t nb = n / p;
     int64_t* offs = (int64_t*)malloc(sizeof(int64_t) * (size_t)(nb + 1));
     for (int64_t b = 0; b <= nb; ++b) offs[b] = b * p;
     oracle_step_blocks(theta, g, dtype, codes, s, v, offs, nb, cb_dec, cb_enc, k, lr,
-                       beta1, beta2, eps, wd, t, quantize, m_full);
+                       beta1, beta2, eps, wd, t, quantize, m_full, m_out);
     free(offs);
 }

@@ -1,0 +1,396 @@
+// Codebook learning (Alg. 3, App. D) for gfx950: block-normalised gradient histogram,
+// exact interval DP over the non-empty bins, and installation of a codebook into the
+// tables the step kernels read (fp32 entries, midpoints, guide table).
+//
+// Floating-point choices: the histogram bin and the whole DP are evaluated in float64
+// with contraction disabled, in the operation order of the definitions, so that the
+// bins, DP costs, split points and codebook entries are reproducible bit for bit.
+#include "gefen_internal.h"
+
+#include <math.h>
+
+namespace gefen {
+namespace {
+
+constexpr int kMaxBins = 16 * kMaxK;   // 4096
+
+// ---------------------------------------------------------------------------------
+// Histogram: x = g / max|g_block| (blocks with max 0 are skipped),
+// bin = min(NB - 1, floor((x + 1) * NB / 2)). Each workgroup accumulates its tiles into
+// an LDS histogram with integer atomics, then adds the non-zero bins to the global
+// uint64 histogram. Integer atomics make the result independent of scheduling.
+// ---------------------------------------------------------------------------------
+__device__ __forceinline__ float grad_at(const Seg& sg, int64_t i)
+{
+    if (sg.gdtype == DT_F32) return static_cast<const float*>(sg.grad)[i];
+    return __uint_as_float(static_cast<uint32_t>(static_cast<const uint16_t*>(sg.grad)[i]) << 16);
+}
+
+__device__ __forceinline__ int bin_of(float g, float a, double half_nb, int nbins)
+{
+    const double x = static_cast<double>(g) / static_cast<double>(a);
+    int b = static_cast<int>((x + 1.0) * half_nb);
+    return b < nbins - 1 ? b : nbins - 1;
+}
+
+__device__ __forceinline__ void tile_block(const Seg& sg, const Tile& tl, int bi, int64_t& start,
+                                           int64_t& len)
+{
+    if (sg.period > 0) {
+        start = tl.elem0 + static_cast<int64_t>(bi) * sg.period;
+        len = sg.period;
+    } else {
+        const int64_t local = tl.blk0 + bi - sg.blk_begin;
+        start = sg.csr[local];
+        len = sg.csr[local + 1] - start;
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void k_histogram(const Tile* __restrict__ tiles,
+                                                        int64_t n_tiles,
+                                                        const int32_t* __restrict__ tile_kind,
+                                                        const Seg* __restrict__ segs,
+                                                        int32_t nbins,
+                                                        uint64_t* __restrict__ hist)
+{
+    __shared__ uint32_t h[kMaxBins];
+    __shared__ float red[kThreads / 64];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    for (int i = tid; i < nbins; i += kThreads) h[i] = 0;
+    __syncthreads();
+    const double half_nb = 0.5 * static_cast<double>(nbins);
+
+    for (int64_t ti = blockIdx.x; ti < n_tiles; ti += gridDim.x) {
+        const Tile tl = tiles[ti];
+        const Seg sg = segs[tl.seg];
+        const int kind = tile_kind[ti];
+        if (kind == KIND_L) {
+            // one lane per small block
+            if (tid < tl.nblk) {
+                int64_t start, len;
+                tile_block(sg, tl, tid, start, len);
+                float a = 0.0f;
+                for (int64_t i = 0; i < len; ++i) a = fmaxf(a, fabsf(grad_at(sg, start + i)));
+                if (a > 0.0f)
+                    for (int64_t i = 0; i < len; ++i)
+                        atomicAdd(&h[bin_of(grad_at(sg, start + i), a, half_nb, nbins)], 1u);
+            }
+        } else if (tl.nblk == 1) {
+            // the whole workgroup on one block
+            int64_t start, len;
+            tile_block(sg, tl, 0, start, len);
+            float a = 0.0f;
+            for (int64_t i = tid; i < len; i += kThreads) a = fmaxf(a, fabsf(grad_at(sg, start + i)));
+            for (int off = 1; off < 64; off <<= 1) a = fmaxf(a, __shfl_xor(a, off));
+            if (lane == 0) red[wave] = a;
+            __syncthreads();
+            a = red[0];
+            for (int w = 1; w < kThreads / 64; ++w) a = fmaxf(a, red[w]);
+            if (a > 0.0f)
+                for (int64_t i = tid; i < len; i += kThreads)
+                    atomicAdd(&h[bin_of(grad_at(sg, start + i), a, half_nb, nbins)], 1u);
+            __syncthreads();   // red[] is reused by the next tile
+        } else {
+            // one wave per block
+            for (int bi = wave; bi < tl.nblk; bi += kThreads / 64) {
+                int64_t start, len;
+                tile_block(sg, tl, bi, start, len);
+                float a = 0.0f;
+                for (int64_t i = lane; i < len; i += 64) a = fmaxf(a, fabsf(grad_at(sg, start + i)));
+                for (int off = 1; off < 64; off <<= 1) a = fmaxf(a, __shfl_xor(a, off));
+                if (a > 0.0f)
+                    for (int64_t i = lane; i < len; i += 64)
+                        atomicAdd(&h[bin_of(grad_at(sg, start + i), a, half_nb, nbins)], 1u);
+            }
+        }
+    }
+    __syncthreads();
+    for (int i = tid; i < nbins; i += kThreads) {
+        const uint32_t c = h[i];
+        if (c) atomicAdd(reinterpret_cast<unsigned long long*>(&hist[i]),
+                         static_cast<unsigned long long>(c));
+    }
+}
+
+// ---------------------------------------------------------------------------------
+// DP workspace layout (offsets in bytes, all 256-byte aligned):
+//   hdr    int32[16]: [0] b (non-empty bins), [1] keff (entries the DP solves for),
+//          [2] status
+//   Z0,Z1,Z2,cnt,ctr   double[NB + 1] each (1-based, index 0 = 0)
+//   D      double[(k + 1) * (NB + 1)]   D[j][r]
+//   split  uint16[(k + 1) * (NB + 1)]
+// ---------------------------------------------------------------------------------
+struct DpLayout {
+    size_t hdr, z0, z1, z2, cnt, ctr, d, split, total;
+};
+
+__host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+__host__ __device__ inline DpLayout dp_layout(int32_t nbins, int32_t k)
+{
+    DpLayout L;
+    const size_t row = static_cast<size_t>(nbins) + 1;
+    size_t o = 0;
+    L.hdr = o; o += align256(16 * sizeof(int32_t));
+    L.z0 = o; o += align256(row * sizeof(double));
+    L.z1 = o; o += align256(row * sizeof(double));
+    L.z2 = o; o += align256(row * sizeof(double));
+    L.cnt = o; o += align256(row * sizeof(double));
+    L.ctr = o; o += align256(row * sizeof(double));
+    L.d = o; o += align256(static_cast<size_t>(k + 1) * row * sizeof(double));
+    L.split = o; o += align256(static_cast<size_t>(k + 1) * row * sizeof(uint16_t));
+    L.total = o;
+    return L;
+}
+
+template <typename T>
+__device__ __forceinline__ T* at(void* ws, size_t off)
+{
+    return reinterpret_cast<T*>(static_cast<char*>(ws) + off);
+}
+
+// Compaction of non-empty bins and prefix sums, in increasing bin order (one thread,
+// so the summation order is the definition's). Also clears row 0 of D.
+__global__ void k_dp_prep(const uint64_t* __restrict__ hist, int32_t nbins, int32_t k, void* ws)
+{
+    const DpLayout L = dp_layout(nbins, k);
+    double* D = at<double>(ws, L.d);
+    const size_t row = static_cast<size_t>(nbins) + 1;
+    for (size_t r = threadIdx.x; r < row; r += blockDim.x) D[r] = r == 0 ? 0.0 : INFINITY;
+    if (threadIdx.x != 0) return;
+    double* Z0 = at<double>(ws, L.z0);
+    double* Z1 = at<double>(ws, L.z1);
+    double* Z2 = at<double>(ws, L.z2);
+    double* cnt = at<double>(ws, L.cnt);
+    double* ctr = at<double>(ws, L.ctr);
+    const double w = 2.0 / static_cast<double>(nbins);
+    Z0[0] = 0.0;
+    Z1[0] = 0.0;
+    Z2[0] = 0.0;
+    int r = 0;
+    for (int i = 0; i < nbins; ++i) {
+        const uint64_t h = hist[i];
+        if (h == 0) continue;
+        const double c = static_cast<double>(h);
+        const double m = -1.0 + (static_cast<double>(i) + 0.5) * w;
+        ++r;
+        ctr[r] = m;
+        cnt[r] = c;
+        Z0[r] = Z0[r - 1] + c;
+        Z1[r] = Z1[r - 1] + c * m;
+        Z2[r] = Z2[r - 1] + c * m * m;
+    }
+    int32_t* hdr = at<int32_t>(ws, L.hdr);
+    hdr[0] = r;
+    hdr[1] = r >= k ? k : (r >= 2 ? r : 0);
+    hdr[2] = r >= k ? 0 : 1;
+}
+
+__device__ __forceinline__ double interval_cost(const double* Z0, const double* Z1,
+                                                const double* Z2, int l, int r, int j, int keff)
+{
+    const double S0 = Z0[r] - Z0[l - 1];
+    const double S1 = Z1[r] - Z1[l - 1];
+    const double S2 = Z2[r] - Z2[l - 1];
+    if (j == 1 || j == keff) {
+        const double a = j == 1 ? -1.0 : 1.0;
+        return S2 - 2.0 * a * S1 + a * a * S0;
+    }
+    return S2 - S1 * S1 / S0;
+}
+
+// One DP level j: D[j][r] = min_{l in [j, r]} D[j-1][l-1] + C(l, r, j), ties to the
+// smallest l. One wavefront per r; lanes stride over l and keep their first minimum,
+// then a shuffle reduction picks the smallest (value, l).
+__global__ __launch_bounds__(kThreads) void k_dp_level(int32_t nbins, int32_t k, int32_t j,
+                                                       void* ws)
+{
+    const DpLayout L = dp_layout(nbins, k);
+    const int32_t* hdr = at<int32_t>(ws, L.hdr);
+    const int b = hdr[0];
+    const int keff = hdr[1];
+    if (j > keff) return;
+    const int gw = (blockIdx.x * kThreads + threadIdx.x) >> 6;
+    const int lane = threadIdx.x & 63;
+    int r;
+    if (j == keff) {
+        if (gw != 0) return;
+        r = b;
+    } else {
+        r = j + gw;
+        if (r > b) return;
+    }
+    const double* Z0 = at<double>(ws, L.z0);
+    const double* Z1 = at<double>(ws, L.z1);
+    const double* Z2 = at<double>(ws, L.z2);
+    const size_t row = static_cast<size_t>(nbins) + 1;
+    double* D = at<double>(ws, L.d);
+    uint16_t* split = at<uint16_t>(ws, L.split);
+    const double* Dprev = D + static_cast<size_t>(j - 1) * row;
+
+    double best = INFINITY;
+    int arg = 0x7fffffff;
+    const int lo = j;
+    const int hi = j == 1 ? 1 : r;   // level 1 can only start at bin 1 (D[0][l-1] = inf otherwise)
+    for (int l = lo + lane; l <= hi; l += 64) {
+        const double cand = Dprev[l - 1] + interval_cost(Z0, Z1, Z2, l, r, j, keff);
+        if (cand < best) {
+            best = cand;
+            arg = l;
+        }
+    }
+    for (int off = 1; off < 64; off <<= 1) {
+        const double ob = __shfl_xor(best, off);
+        const int oa = __shfl_xor(arg, off);
+        if (ob < best || (ob == best && oa < arg)) {
+            best = ob;
+            arg = oa;
+        }
+    }
+    if (lane == 0) {
+        D[static_cast<size_t>(j) * row + r] = best;
+        split[static_cast<size_t>(j) * row + r] = static_cast<uint16_t>(arg);
+    }
+}
+
+// Backtracking (one thread): entry j is -1, +1 or the weighted mean of its interval;
+// degenerate histograms (b < k) are padded with +1.
+__global__ void k_dp_backtrack(int32_t nbins, int32_t k, void* ws, double* codebook,
+                               double* cost, int32_t* status)
+{
+    if (threadIdx.x != 0) return;
+    const DpLayout L = dp_layout(nbins, k);
+    const int32_t* hdr = at<int32_t>(ws, L.hdr);
+    const int b = hdr[0];
+    const int keff = hdr[1];
+    const double* Z0 = at<double>(ws, L.z0);
+    const double* Z1 = at<double>(ws, L.z1);
+    const double* cnt = at<double>(ws, L.cnt);
+    const double* ctr = at<double>(ws, L.ctr);
+    const size_t row = static_cast<size_t>(nbins) + 1;
+    const double* D = at<double>(ws, L.d);
+    const uint16_t* split = at<uint16_t>(ws, L.split);
+    if (keff >= 2) {
+        *cost = D[static_cast<size_t>(keff) * row + b];
+        int r = b;
+        for (int j = keff; j >= 1; --j) {
+            const int l = split[static_cast<size_t>(j) * row + r];
+            if (j == 1) {
+                codebook[j - 1] = -1.0;
+            } else if (j == keff) {
+                codebook[j - 1] = 1.0;
+            } else {
+                const double S0 = Z0[r] - Z0[l - 1];
+                const double S1 = Z1[r] - Z1[l - 1];
+                codebook[j - 1] = S1 / S0;
+            }
+            r = l - 1;
+        }
+        for (int j = keff; j < k; ++j) codebook[j] = 1.0;
+    } else {
+        codebook[0] = -1.0;
+        for (int j = 1; j < k; ++j) codebook[j] = 1.0;
+        double e = 0.0;
+        for (int i = 1; i <= b; ++i) {
+            const double dl = ctr[i] + 1.0, dr = 1.0 - ctr[i];
+            const double d2 = (dl * dl < dr * dr) ? dl * dl : dr * dr;
+            e += cnt[i] * d2;
+        }
+        *cost = e;
+    }
+    *status = hdr[2];
+}
+
+// ---------------------------------------------------------------------------------
+// Codebook installation: fp32 entries, fp64 copy, midpoints and the guide table.
+// guide[bk] = number of midpoints whose bucket is < bk, bucket(x) =
+// min(ng - 1, (int)((x + 1) * ng / 2)) in fp32 -- the same function the step applies
+// to the (clamped) value being encoded, so the lookup is exact for fp32 midpoints.
+// ---------------------------------------------------------------------------------
+__global__ void k_install(const double* __restrict__ in64, const float* __restrict__ in32,
+                          int32_t k, int32_t ng, float* cb32, double* cb64, float* mid,
+                          uint8_t* guide)
+{
+    __shared__ float c[kMaxK];
+    __shared__ uint16_t cnt[kMaxBins];
+    const int t = threadIdx.x;
+    for (int i = t; i < k; i += blockDim.x) {
+        const float f = in64 ? static_cast<float>(in64[i]) : in32[i];
+        c[i] = f;
+        cb32[i] = f;
+        cb64[i] = in64 ? in64[i] : static_cast<double>(in32[i]);
+    }
+    for (int i = t; i < ng; i += blockDim.x) cnt[i] = 0;
+    __syncthreads();
+    const float half_ng = 0.5f * static_cast<float>(ng);
+    for (int i = t; i < k; i += blockDim.x) {
+        const float mdp = i + 1 < k ? 0.5f * (c[i] + c[i + 1]) : 2.0f;
+        mid[i] = mdp;
+    }
+    if (t == 0) {
+        for (int i = 0; i + 1 < k; ++i) {
+            const float mdp = 0.5f * (c[i] + c[i + 1]);
+            const float x = fminf(fmaxf(mdp, -1.0f), 1.0f);
+            int bk = static_cast<int>((x + 1.0f) * half_ng);
+            bk = bk < ng - 1 ? bk : ng - 1;
+            cnt[bk] += 1;
+        }
+        int acc = 0;
+        for (int bk = 0; bk < ng; ++bk) {
+            guide[bk] = static_cast<uint8_t>(acc);
+            acc += cnt[bk];
+        }
+        guide[ng] = static_cast<uint8_t>(acc);
+        for (int bk = ng + 1; bk < ((ng + 1 + 15) & ~15); ++bk) guide[bk] = 0;
+    }
+}
+
+}  // namespace
+
+size_t dp_workspace_bytes(int32_t nbins, int32_t k) { return dp_layout(nbins, k).total; }
+
+hipError_t launch_histogram(const Tile* tiles, int64_t n_tiles, const int32_t* tile_kind,
+                            const Seg* segs, int32_t nbins, uint64_t* hist, hipStream_t stream)
+{
+    if (n_tiles <= 0) return hipSuccess;
+    const int64_t g = n_tiles < 4096 ? n_tiles : 4096;
+    hipLaunchKernelGGL(k_histogram, dim3(static_cast<unsigned>(g)), dim3(kThreads), 0, stream,
+                       tiles, n_tiles, tile_kind, segs, nbins, hist);
+    return hipGetLastError();
+}
+
+hipError_t launch_dp(const uint64_t* hist, int32_t nbins, int32_t k, void* ws,
+                     double* codebook_out, double* cost_out, int32_t* status_out,
+                     hipStream_t stream)
+{
+    hipLaunchKernelGGL(k_dp_prep, dim3(1), dim3(kThreads), 0, stream, hist, nbins, k, ws);
+    const unsigned waves_per_wg = kThreads / 64;
+    const unsigned grid = (static_cast<unsigned>(nbins) + waves_per_wg - 1) / waves_per_wg;
+    for (int j = 1; j <= k; ++j)
+        hipLaunchKernelGGL(k_dp_level, dim3(grid), dim3(kThreads), 0, stream, nbins, k, j, ws);
+    hipLaunchKernelGGL(k_dp_backtrack, dim3(1), dim3(64), 0, stream, nbins, k, ws,
+                       codebook_out, cost_out, status_out);
+    return hipGetLastError();
+}
+
+hipError_t launch_install_codebook(const double* cb64_in, int32_t k, int32_t ng, float* cb32,
+                                   double* cb64, float* mid, uint8_t* guide, hipStream_t stream)
+{
+    hipLaunchKernelGGL(k_install, dim3(1), dim3(kThreads), 0, stream, cb64_in,
+                       static_cast<const float*>(nullptr), k, ng, cb32, cb64, mid, guide);
+    return hipGetLastError();
+}
+
+hipError_t launch_install_codebook_f32(const float* cb32_in, int32_t k, int32_t ng, float* cb32,
+                                       double* cb64, float* mid, uint8_t* guide,
+                                       hipStream_t stream)
+{
+    hipLaunchKernelGGL(k_install, dim3(1), dim3(kThreads), 0, stream,
+                       static_cast<const double*>(nullptr), cb32_in, k, ng, cb32, cb64, mid,
+                       guide);
+    return hipGetLastError();
+}
+
+}  // namespace gefen

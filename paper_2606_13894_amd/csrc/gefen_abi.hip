@@ -1,0 +1,1002 @@
+// C ABI of libgefen: argument checks, state layout, work planning and kernel launches.
+// The arithmetic of the method runs in the kernels (step.hip, codebook.hip,
+// partition.hip); this file decides which kernel processes which part of which tensor.
+#include "gefen.h"
+#include "gefen_internal.h"
+
+#include <algorithm>
+#include <cstdlib>
+#include <memory>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+using namespace gefen;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+#define GEFEN_HIP(call)                                                                  \
+    do {                                                                                 \
+        hipError_t e_ = (call);                                                          \
+        if (e_ != hipSuccess)                                                            \
+            return fail(GEFEN_EHIP, "%s failed: %s", #call, hipGetErrorString(e_));      \
+    } while (0)
+
+struct Class {
+    int32_t kind, gdtype, vpl;
+    int64_t first, count;
+    int64_t elems, bytes;   // per launch: elements and algorithmic HBM bytes
+};
+
+constexpr int64_t kUMaxPeriod = 4LL * (1 << kMaxLpbLog2) * kMaxVpl;   // 8192
+constexpr int64_t kPartChunk = 65536;     // elements of one partition sub-chunk (mode 1)
+constexpr int64_t kPartItemElems = 16384; // elements per partition item (mode 0)
+constexpr int kPartMaxPairs = 2048;
+constexpr uint32_t kCkptMagic = 0x4e464547u;   // "GEFN"
+
+hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
+
+std::vector<int64_t> divisors_of(int64_t n)
+{
+    std::vector<int64_t> lo, hi;
+    for (int64_t d = 1; d <= n / d; ++d) {
+        if (n % d == 0) {
+            lo.push_back(d);
+            if (d != n / d) hi.push_back(n / d);
+        }
+    }
+    for (auto it = hi.rbegin(); it != hi.rend(); ++it) lo.push_back(*it);
+    return lo;
+}
+
+bool finite_f(double x) { return std::isfinite(x); }
+
+}  // namespace
+
+struct gefen_state {
+    int device = 0;
+    int32_t n_tensors = 0;
+    int32_t k = 256, nbins = 4096, ng = 4096;
+    bool explicit_blocks = false;
+    std::vector<int64_t> numel, period, blk_begin, code_off;   // blk_begin/code_off: n + 1
+    std::vector<int32_t> gdtype;
+    int64_t total_blocks = 0, code_bytes = 0;
+
+    uint8_t* codes = nullptr;
+    float* scale = nullptr;
+    float* vmom = nullptr;
+    float* cb32[2] = {nullptr, nullptr};
+    double* cb64[2] = {nullptr, nullptr};
+    float* mid[2] = {nullptr, nullptr};
+    uint8_t* guide[2] = {nullptr, nullptr};
+    int dec_slot = 0, enc_slot = 0;
+
+    Tile* tiles = nullptr;
+    int32_t* tile_kind = nullptr;
+    int64_t n_tiles = 0;
+    std::vector<Class> classes;
+
+    Seg* segs = nullptr;
+    std::vector<Seg> segs_host;
+    Seg* segs_pinned = nullptr;
+    hipEvent_t seg_evt = nullptr;
+    bool seg_evt_pending = false;
+    int64_t* csr = nullptr;
+
+    uint64_t* hist = nullptr;
+    void* dp_ws = nullptr;
+    double* fit_cb64 = nullptr;
+    double* fit_cost = nullptr;
+    int32_t* fit_status = nullptr;
+
+    int64_t persistent_bytes = 0, workspace_bytes = 0;
+    std::vector<void*> dev_allocs;
+
+    // measurement: events[(step * classes + c) * 2 + {0 start, 1 stop}]
+    bool prof_armed = false;
+    int32_t prof_max_steps = 0, prof_steps = 0;
+    std::vector<hipEvent_t> prof_events;
+
+    void prof_free()
+    {
+        for (hipEvent_t e : prof_events) (void)hipEventDestroy(e);
+        prof_events.clear();
+        prof_armed = false;
+        prof_steps = 0;
+    }
+
+    ~gefen_state()
+    {
+        prof_free();
+        for (void* p : dev_allocs) (void)hipFree(p);
+        if (segs_pinned) (void)hipHostFree(segs_pinned);
+        if (seg_evt) (void)hipEventDestroy(seg_evt);
+    }
+
+    template <typename T>
+    int alloc(T** out, size_t bytes, bool persistent)
+    {
+        void* p = nullptr;
+        hipError_t e = hipMalloc(&p, bytes ? bytes : 16);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            return fail(GEFEN_ENOMEM, "hipMalloc(%zu) failed: %s", bytes, hipGetErrorString(e));
+        }
+        dev_allocs.push_back(p);
+        *out = static_cast<T*>(p);
+        (persistent ? persistent_bytes : workspace_bytes) += static_cast<int64_t>(bytes);
+        return GEFEN_OK;
+    }
+};
+
+// ------------------------------------------------------------------ helpers
+namespace {
+
+int check_tensors(const gefen_tensor* ts, int32_t n, bool params, const char* what)
+{
+    if (!ts) return fail(GEFEN_EINVAL, "%s is NULL", what);
+    for (int32_t i = 0; i < n; ++i) {
+        if (!ts[i].ptr && ts[i].numel > 0) return fail(GEFEN_EINVAL, "%s[%d].ptr is NULL", what, i);
+        if (ts[i].numel < 1) return fail(GEFEN_EINVAL, "%s[%d].numel must be >= 1", what, i);
+        if (params ? ts[i].dtype != GEFEN_F32
+                   : (ts[i].dtype != GEFEN_F32 && ts[i].dtype != GEFEN_BF16))
+            return fail(GEFEN_EDTYPE, "%s[%d] has unsupported dtype %d", what, i, ts[i].dtype);
+    }
+    return GEFEN_OK;
+}
+
+int check_against_state(const gefen_state* st, const gefen_tensor* ts, int32_t n, bool params,
+                        const char* what)
+{
+    if (!st) return fail(GEFEN_EINVAL, "state is NULL");
+    if (n != st->n_tensors)
+        return fail(GEFEN_EINVAL, "%s: %d tensors, state has %d", what, n, st->n_tensors);
+    int rc = check_tensors(ts, n, params, what);
+    if (rc) return rc;
+    for (int32_t i = 0; i < n; ++i) {
+        if (ts[i].numel != st->numel[i])
+            return fail(GEFEN_EINVAL, "%s[%d]: numel %lld, state has %lld", what, i,
+                        (long long)ts[i].numel, (long long)st->numel[i]);
+        if (!params && ts[i].dtype != st->gdtype[i])
+            return fail(GEFEN_EDTYPE, "%s[%d]: dtype %d, state has %d", what, i, ts[i].dtype,
+                        st->gdtype[i]);
+    }
+    return GEFEN_OK;
+}
+
+// Refresh the device tensor table when the caller passes different buffers.
+int refresh_segs(gefen_state* st, const gefen_tensor* params, const gefen_tensor* grads,
+                 hipStream_t stream)
+{
+    bool changed = false;
+    for (int32_t i = 0; i < st->n_tensors; ++i) {
+        Seg& s = st->segs_host[i];
+        if (params && s.theta != static_cast<float*>(params[i].ptr)) {
+            s.theta = static_cast<float*>(params[i].ptr);
+            changed = true;
+        }
+        if (grads && s.grad != grads[i].ptr) {
+            s.grad = grads[i].ptr;
+            changed = true;
+        }
+    }
+    if (!changed) return GEFEN_OK;
+    if (st->seg_evt_pending) GEFEN_HIP(hipEventSynchronize(st->seg_evt));
+    std::memcpy(st->segs_pinned, st->segs_host.data(), sizeof(Seg) * st->n_tensors);
+    GEFEN_HIP(hipMemcpyAsync(st->segs, st->segs_pinned, sizeof(Seg) * st->n_tensors,
+                             hipMemcpyHostToDevice, stream));
+    GEFEN_HIP(hipEventRecord(st->seg_evt, stream));
+    st->seg_evt_pending = true;
+    return GEFEN_OK;
+}
+
+__global__ void k_fill_zero(uint32_t* p, size_t words)
+{
+    for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < words;
+         i += (size_t)gridDim.x * blockDim.x)
+        p[i] = 0u;
+}
+
+// Zero `bytes` (a multiple of 4) of device memory with a kernel (graph-capture safe).
+hipError_t fill_zero(void* p, size_t bytes, hipStream_t s)
+{
+    const size_t words = bytes / 4;
+    if (!words) return hipSuccess;
+    size_t g = (words + 255) / 256;
+    if (g > 65536) g = 65536;
+    hipLaunchKernelGGL(k_fill_zero, dim3(static_cast<unsigned>(g)), dim3(256), 0, s,
+                       static_cast<uint32_t*>(p), words);
+    return hipGetLastError();
+}
+
+// Lanes-per-block and vectors-per-lane of a KIND_U tensor of period p.
+void choose_u(int64_t p, int& lpb_log2, int& vpl)
+{
+    const int64_t nv = p / 4;
+    int l2 = 0;
+    while ((int64_t(1) << l2) * kMaxVpl < nv) ++l2;
+    if (nv >= 16 && l2 < 4) l2 = 4;            // >= 256 contiguous bytes per slot
+    if (nv < 16) {                             // tiny blocks: one vector per lane
+        l2 = 0;
+        while ((int64_t(1) << l2) < nv) ++l2;
+    }
+    lpb_log2 = l2;
+    vpl = static_cast<int>((nv + (int64_t(1) << l2) - 1) >> l2);
+}
+
+// Tensor-relative block starts of tensor i (explicit blocks), size n_blocks_i + 1.
+int plan_tiles(gefen_state* st, const std::vector<std::vector<int64_t>>& starts)
+{
+    struct Key {
+        int32_t kind, gdtype, vpl;
+    };
+    std::vector<std::vector<Tile>> lists;
+    std::vector<Key> keys;
+    auto list_for = [&](int32_t kind, int32_t gdt, int32_t vpl) -> std::vector<Tile>& {
+        for (size_t i = 0; i < keys.size(); ++i)
+            if (keys[i].kind == kind && keys[i].gdtype == gdt && keys[i].vpl == vpl) return lists[i];
+        keys.push_back({kind, gdt, vpl});
+        lists.emplace_back();
+        return lists.back();
+    };
+    for (int32_t t = 0; t < st->n_tensors; ++t) {
+        const int32_t gdt = st->gdtype[t];
+        const int64_t bb = st->blk_begin[t];
+        if (st->explicit_blocks) {
+            const std::vector<int64_t>& s = starts[t];
+            const int64_t nb = static_cast<int64_t>(s.size()) - 1;
+            int64_t b = 0;
+            while (b < nb) {
+                const int64_t len = s[b + 1] - s[b];
+                if (len <= kSmallBlock) {
+                    Tile tl{};
+                    tl.elem0 = s[b];
+                    tl.blk0 = bb + b;
+                    tl.seg = t;
+                    int n = 0;
+                    while (b < nb && n < kThreads && s[b + 1] - s[b] <= kSmallBlock) {
+                        ++n;
+                        ++b;
+                    }
+                    tl.nblk = static_cast<int16_t>(n);
+                    tl.nelem = s[b] - tl.elem0;
+                    list_for(KIND_L, gdt, 0).push_back(tl);
+                } else {
+                    Tile tl{};
+                    tl.elem0 = s[b];
+                    tl.blk0 = bb + b;
+                    tl.nelem = len;
+                    tl.seg = t;
+                    tl.nblk = 1;
+                    list_for(KIND_G, gdt, 0).push_back(tl);
+                    ++b;
+                }
+            }
+            continue;
+        }
+        const int64_t p = st->period[t];
+        const int64_t nb = st->numel[t] / p;
+        if (p % 4 == 0 && p <= kUMaxPeriod) {
+            int l2, vpl;
+            choose_u(p, l2, vpl);
+            const int64_t bpw = kThreads >> l2;
+            std::vector<Tile>& L = list_for(KIND_U, gdt, vpl);
+            for (int64_t b = 0; b < nb; b += bpw) {
+                Tile tl{};
+                const int64_t n = std::min(bpw, nb - b);
+                tl.elem0 = b * p;
+                tl.blk0 = bb + b;
+                tl.nelem = n * p;
+                tl.seg = t;
+                tl.nblk = static_cast<int16_t>(n);
+                tl.vpl = static_cast<uint8_t>(vpl);
+                tl.lpb_log2 = static_cast<uint8_t>(l2);
+                L.push_back(tl);
+            }
+        } else if (p <= kSmallBlock) {
+            std::vector<Tile>& L = list_for(KIND_L, gdt, 0);
+            for (int64_t b = 0; b < nb; b += kThreads) {
+                Tile tl{};
+                const int64_t n = std::min<int64_t>(kThreads, nb - b);
+                tl.elem0 = b * p;
+                tl.blk0 = bb + b;
+                tl.nelem = n * p;
+                tl.seg = t;
+                tl.nblk = static_cast<int16_t>(n);
+                L.push_back(tl);
+            }
+        } else {
+            std::vector<Tile>& L = list_for(KIND_G, gdt, 0);
+            for (int64_t b = 0; b < nb; ++b) {
+                Tile tl{};
+                tl.elem0 = b * p;
+                tl.blk0 = bb + b;
+                tl.nelem = p;
+                tl.seg = t;
+                tl.nblk = 1;
+                L.push_back(tl);
+            }
+        }
+    }
+    std::vector<Tile> all;
+    std::vector<int32_t> kinds;
+    st->classes.clear();
+    for (size_t i = 0; i < lists.size(); ++i) {
+        Class c{keys[i].kind, keys[i].gdtype, keys[i].vpl, static_cast<int64_t>(all.size()),
+                static_cast<int64_t>(lists[i].size()), 0, 0};
+        const int64_t per_elem = 8 + (keys[i].gdtype == DT_F32 ? 4 : 2) + 2;
+        for (const Tile& tl : lists[i]) {
+            c.elems += tl.nelem;
+            c.bytes += tl.nelem * per_elem + 16 * int64_t(tl.nblk);
+            if (keys[i].kind == KIND_L && st->explicit_blocks) c.bytes += 8 * int64_t(tl.nblk);
+        }
+        st->classes.push_back(c);
+        all.insert(all.end(), lists[i].begin(), lists[i].end());
+        kinds.insert(kinds.end(), lists[i].size(), keys[i].kind);
+    }
+    st->n_tiles = static_cast<int64_t>(all.size());
+    int rc = st->alloc(&st->tiles, sizeof(Tile) * all.size(), false);
+    if (rc) return rc;
+    rc = st->alloc(&st->tile_kind, sizeof(int32_t) * kinds.size(), false);
+    if (rc) return rc;
+    GEFEN_HIP(hipMemcpy(st->tiles, all.data(), sizeof(Tile) * all.size(), hipMemcpyHostToDevice));
+    GEFEN_HIP(hipMemcpy(st->tile_kind, kinds.data(), sizeof(int32_t) * kinds.size(),
+                        hipMemcpyHostToDevice));
+    return GEFEN_OK;
+}
+
+// Alg. 2 for a list of tensors. Writes one period per tensor (host), and optionally the
+// scores of every divisor (host, concatenated in tensor order).
+int infer_periods(const std::vector<gefen_tensor>& ts, double eps, hipStream_t stream,
+                  std::vector<int64_t>& periods, std::vector<int64_t>* divs_out,
+                  std::vector<double>* scores_out)
+{
+    std::vector<PartDesc> descs;
+    std::vector<int32_t> first, count;
+    std::vector<int64_t> all_divs;
+    int64_t items = 0, slots = 0;
+    for (const gefen_tensor& g : ts) {
+        const int64_t n = g.numel;
+        const std::vector<int64_t> dv = divisors_of(n);
+        first.push_back(static_cast<int32_t>(descs.size()));
+        count.push_back(static_cast<int32_t>(dv.size()));
+        for (int64_t p : dv) {
+            PartDesc d{};
+            d.grad = g.ptr;
+            d.n = n;
+            d.p = p;
+            d.gdtype = g.dtype;
+            d.item0 = items;
+            d.out0 = slots;
+            const int64_t nb = n / p;
+            if (nb < 2) {
+                d.mode = 0;
+                d.rpi = 1;
+                d.n_items = 0;
+            } else if (p <= kPartChunk) {
+                d.mode = 0;
+                int64_t rpi = kPartItemElems / p;
+                rpi = std::max<int64_t>(1, std::min<int64_t>(rpi, kPartMaxPairs));
+                d.rpi = static_cast<int32_t>(rpi);
+                d.n_items = (nb - 1 + rpi - 1) / rpi;
+                slots += d.n_items;
+            } else {
+                d.mode = 1;
+                d.rpi = static_cast<int32_t>((p + kPartChunk - 1) / kPartChunk);
+                d.n_items = nb * d.rpi;
+                slots += d.n_items;
+            }
+            items += d.n_items;
+            descs.push_back(d);
+            all_divs.push_back(p);
+        }
+    }
+    const int32_t nd = static_cast<int32_t>(descs.size());
+    const int32_t nt = static_cast<int32_t>(ts.size());
+    void *d_descs = nullptr, *d_partials = nullptr, *d_scores = nullptr, *d_first = nullptr,
+         *d_count = nullptr, *d_periods = nullptr;
+    auto cleanup = [&]() {
+        for (void* p : {d_descs, d_partials, d_scores, d_first, d_count, d_periods})
+            if (p) (void)hipFree(p);
+    };
+#define GEFEN_PART_HIP(call)                                                             \
+    do {                                                                                 \
+        hipError_t e_ = (call);                                                          \
+        if (e_ != hipSuccess) {                                                          \
+            cleanup();                                                                   \
+            return fail(GEFEN_EHIP, "%s failed: %s", #call, hipGetErrorString(e_));      \
+        }                                                                                \
+    } while (0)
+    GEFEN_PART_HIP(hipMalloc(&d_descs, sizeof(PartDesc) * std::max(nd, 1)));
+    GEFEN_PART_HIP(hipMalloc(&d_partials, sizeof(double) * std::max<int64_t>(slots, 1)));
+    GEFEN_PART_HIP(hipMalloc(&d_scores, sizeof(double) * std::max(nd, 1)));
+    GEFEN_PART_HIP(hipMalloc(&d_first, sizeof(int32_t) * std::max(nt, 1)));
+    GEFEN_PART_HIP(hipMalloc(&d_count, sizeof(int32_t) * std::max(nt, 1)));
+    GEFEN_PART_HIP(hipMalloc(&d_periods, sizeof(int64_t) * std::max(nt, 1)));
+    GEFEN_PART_HIP(hipMemcpyAsync(d_descs, descs.data(), sizeof(PartDesc) * nd,
+                                  hipMemcpyHostToDevice, stream));
+    GEFEN_PART_HIP(hipMemcpyAsync(d_first, first.data(), sizeof(int32_t) * nt,
+                                  hipMemcpyHostToDevice, stream));
+    GEFEN_PART_HIP(hipMemcpyAsync(d_count, count.data(), sizeof(int32_t) * nt,
+                                  hipMemcpyHostToDevice, stream));
+    GEFEN_PART_HIP(launch_partition(static_cast<PartDesc*>(d_descs), nd, items, eps,
+                                    static_cast<double*>(d_partials),
+                                    static_cast<double*>(d_scores),
+                                    static_cast<int32_t*>(d_first),
+                                    static_cast<int32_t*>(d_count), nt,
+                                    static_cast<int64_t*>(d_periods), stream));
+    periods.assign(nt, 1);
+    GEFEN_PART_HIP(hipMemcpyAsync(periods.data(), d_periods, sizeof(int64_t) * nt,
+                                  hipMemcpyDeviceToHost, stream));
+    if (scores_out) {
+        scores_out->assign(nd, 0.0);
+        GEFEN_PART_HIP(hipMemcpyAsync(scores_out->data(), d_scores, sizeof(double) * nd,
+                                      hipMemcpyDeviceToHost, stream));
+    }
+    GEFEN_PART_HIP(hipStreamSynchronize(stream));
+#undef GEFEN_PART_HIP
+    cleanup();
+    if (divs_out) *divs_out = all_divs;
+    return GEFEN_OK;
+}
+
+CodebookDev codebook_dev(const gefen_state* st)
+{
+    CodebookDev c;
+    c.dec = st->cb32[st->dec_slot];
+    c.enc_mid = st->mid[st->enc_slot];
+    c.enc_guide = st->guide[st->enc_slot];
+    c.k = st->k;
+    c.ng = st->ng;
+    return c;
+}
+
+// Histogram of `grads` with the state's blocks, DP, install into `slot`.
+int fit_into_slot(gefen_state* st, int slot, hipStream_t stream)
+{
+    GEFEN_HIP(fill_zero(st->hist, sizeof(uint64_t) * st->nbins, stream));
+    GEFEN_HIP(launch_histogram(st->tiles, st->n_tiles, st->tile_kind, st->segs, st->nbins,
+                               st->hist, stream));
+    GEFEN_HIP(launch_dp(st->hist, st->nbins, st->k, st->dp_ws, st->fit_cb64, st->fit_cost,
+                        st->fit_status, stream));
+    GEFEN_HIP(launch_install_codebook(st->fit_cb64, st->k, st->ng, st->cb32[slot],
+                                      st->cb64[slot], st->mid[slot], st->guide[slot], stream));
+    return GEFEN_OK;
+}
+
+struct CkptLayout {
+    int64_t header, codes, scale, vmom, cb0, cb1, total;
+};
+
+CkptLayout ckpt_layout(const gefen_state* st)
+{
+    auto a8 = [](int64_t x) { return (x + 7) & ~int64_t(7); };
+    CkptLayout L;
+    L.header = 0;
+    L.codes = 64;
+    L.scale = a8(L.codes + st->code_bytes);
+    L.vmom = L.scale + 4 * st->total_blocks;
+    L.cb0 = a8(L.vmom + 4 * st->total_blocks);
+    L.cb1 = L.cb0 + 8 * st->k;
+    L.total = L.cb1 + 8 * st->k;
+    return L;
+}
+
+bool is_host_ptr(const void* p)
+{
+    hipPointerAttribute_t a;
+    if (hipPointerGetAttributes(&a, p) != hipSuccess) {
+        (void)hipGetLastError();
+        return true;
+    }
+    return a.type == hipMemoryTypeHost || a.type == hipMemoryTypeUnregistered;
+}
+
+}  // namespace
+
+// ------------------------------------------------------------------ ABI
+extern "C" {
+
+const char* gefen_last_error(void) { return g_err.c_str(); }
+
+int gefen_init(const gefen_tensor* grads0, int32_t n_tensors, const int64_t* period_override,
+               const int64_t* block_offsets, int64_t n_blocks, int32_t code_bits,
+               double eps_part, void* stream_, gefen_state** out)
+{
+    g_err.clear();
+    if (!out) return fail(GEFEN_EINVAL, "out is NULL");
+    *out = nullptr;
+    if (n_tensors < 1) return fail(GEFEN_EINVAL, "n_tensors must be >= 1");
+    int rc = check_tensors(grads0, n_tensors, false, "grads0");
+    if (rc) return rc;
+    if (code_bits != 8 && code_bits != 4)
+        return fail(GEFEN_EINVAL, "code_bits must be 8 or 4 (got %d)", code_bits);
+    if (!finite_f(eps_part) || eps_part < 0) return fail(GEFEN_EINVAL, "eps_part must be >= 0");
+    hipStream_t stream = as_stream(stream_);
+
+    std::unique_ptr<gefen_state> st(new gefen_state());
+    GEFEN_HIP(hipGetDevice(&st->device));
+    st->n_tensors = n_tensors;
+    st->k = 1 << code_bits;
+    st->nbins = 16 * st->k;
+    st->ng = 16 * st->k;
+    int64_t total = 0;
+    for (int32_t i = 0; i < n_tensors; ++i) {
+        st->numel.push_back(grads0[i].numel);
+        st->gdtype.push_back(grads0[i].dtype);
+        total += grads0[i].numel;
+    }
+
+    // blocks
+    std::vector<std::vector<int64_t>> starts(n_tensors);
+    st->period.assign(n_tensors, 0);
+    if (block_offsets) {
+        if (n_blocks < 1) return fail(GEFEN_EINVAL, "n_blocks must be >= 1");
+        if (block_offsets[0] != 0) return fail(GEFEN_EINVAL, "block_offsets[0] must be 0");
+        if (block_offsets[n_blocks] != total)
+            return fail(GEFEN_EINVAL, "block_offsets[n_blocks] must equal the total numel");
+        st->explicit_blocks = true;
+        int64_t b = 0, base = 0;
+        for (int32_t t = 0; t < n_tensors; ++t) {
+            const int64_t end = base + st->numel[t];
+            starts[t].push_back(0);
+            while (b < n_blocks && block_offsets[b + 1] <= end) {
+                if (block_offsets[b + 1] <= block_offsets[b])
+                    return fail(GEFEN_EINVAL, "block_offsets must increase strictly (at %lld)",
+                                (long long)b);
+                starts[t].push_back(block_offsets[b + 1] - base);
+                ++b;
+            }
+            if (starts[t].back() != st->numel[t])
+                return fail(GEFEN_EINVAL, "tensor %d does not end on a block boundary", t);
+            base = end;
+        }
+    } else {
+        std::vector<gefen_tensor> infer;
+        std::vector<int32_t> which;
+        for (int32_t t = 0; t < n_tensors; ++t) {
+            const int64_t ov = period_override ? period_override[t] : 0;
+            if (ov < 0) return fail(GEFEN_EINVAL, "period_override[%d] < 0", t);
+            if (ov > 0) {
+                if (st->numel[t] % ov != 0)
+                    return fail(GEFEN_EINVAL, "period_override[%d] = %lld does not divide %lld",
+                                t, (long long)ov, (long long)st->numel[t]);
+                st->period[t] = ov;
+            } else {
+                infer.push_back(grads0[t]);
+                which.push_back(t);
+            }
+        }
+        if (!infer.empty()) {
+            std::vector<int64_t> per;
+            rc = infer_periods(infer, eps_part, stream, per, nullptr, nullptr);
+            if (rc) return rc;
+            for (size_t i = 0; i < which.size(); ++i) st->period[which[i]] = per[i];
+        }
+    }
+
+    // state layout
+    st->blk_begin.assign(n_tensors + 1, 0);
+    st->code_off.assign(n_tensors + 1, 0);
+    for (int32_t t = 0; t < n_tensors; ++t) {
+        const int64_t nb = st->explicit_blocks ? static_cast<int64_t>(starts[t].size()) - 1
+                                               : st->numel[t] / st->period[t];
+        st->blk_begin[t + 1] = st->blk_begin[t] + nb;
+        st->code_off[t + 1] = st->code_off[t] + ((st->numel[t] + 15) & ~int64_t(15));
+    }
+    st->total_blocks = st->blk_begin[n_tensors];
+    st->code_bytes = st->code_off[n_tensors];
+
+    if ((rc = st->alloc(&st->codes, st->code_bytes, true))) return rc;
+    if ((rc = st->alloc(&st->scale, 4 * st->total_blocks, true))) return rc;
+    if ((rc = st->alloc(&st->vmom, 4 * st->total_blocks, true))) return rc;
+    const size_t guide_bytes = ((st->ng + 1 + 15) / 16) * 16;
+    for (int s = 0; s < 2; ++s) {
+        if ((rc = st->alloc(&st->cb32[s], 4 * st->k, true))) return rc;
+        if ((rc = st->alloc(&st->cb64[s], 8 * st->k, true))) return rc;
+        if ((rc = st->alloc(&st->mid[s], 4 * st->k, true))) return rc;
+        if ((rc = st->alloc(&st->guide[s], guide_bytes, true))) return rc;
+    }
+    if ((rc = st->alloc(&st->segs, sizeof(Seg) * n_tensors, false))) return rc;
+    if ((rc = st->alloc(&st->hist, sizeof(uint64_t) * st->nbins, false))) return rc;
+    if ((rc = st->alloc(&st->dp_ws, dp_workspace_bytes(st->nbins, st->k), false))) return rc;
+    if ((rc = st->alloc(&st->fit_cb64, 8 * st->k, false))) return rc;
+    if ((rc = st->alloc(&st->fit_cost, 8, false))) return rc;
+    if ((rc = st->alloc(&st->fit_status, 8, false))) return rc;
+    void* pinned = nullptr;
+    GEFEN_HIP(hipHostMalloc(&pinned, sizeof(Seg) * n_tensors, hipHostMallocDefault));
+    st->segs_pinned = static_cast<Seg*>(pinned);
+    GEFEN_HIP(hipEventCreateWithFlags(&st->seg_evt, hipEventDisableTiming));
+
+    if (st->explicit_blocks) {
+        int64_t entries = 0;
+        for (int32_t t = 0; t < n_tensors; ++t) entries += static_cast<int64_t>(starts[t].size());
+        if ((rc = st->alloc(&st->csr, sizeof(int64_t) * entries, false))) return rc;
+        std::vector<int64_t> flat;
+        flat.reserve(entries);
+        for (int32_t t = 0; t < n_tensors; ++t) flat.insert(flat.end(), starts[t].begin(), starts[t].end());
+        GEFEN_HIP(hipMemcpy(st->csr, flat.data(), sizeof(int64_t) * entries, hipMemcpyHostToDevice));
+    }
+
+    st->segs_host.assign(n_tensors, Seg{});
+    int64_t csr_base = 0;
+    for (int32_t t = 0; t < n_tensors; ++t) {
+        Seg& s = st->segs_host[t];
+        s.theta = nullptr;
+        s.grad = grads0[t].ptr;
+        s.code_off = st->code_off[t];
+        s.period = st->period[t];
+        s.blk_begin = st->blk_begin[t];
+        s.csr = st->explicit_blocks ? st->csr + csr_base : nullptr;
+        s.numel = st->numel[t];
+        s.gdtype = st->gdtype[t];
+        if (st->explicit_blocks) csr_base += static_cast<int64_t>(starts[t].size());
+    }
+    std::memcpy(st->segs_pinned, st->segs_host.data(), sizeof(Seg) * n_tensors);
+    GEFEN_HIP(hipMemcpyAsync(st->segs, st->segs_pinned, sizeof(Seg) * n_tensors,
+                             hipMemcpyHostToDevice, stream));
+    GEFEN_HIP(hipEventRecord(st->seg_evt, stream));
+    st->seg_evt_pending = true;
+
+    if ((rc = plan_tiles(st.get(), starts))) return rc;
+
+    // zero state (Alg. 1: codes 0, scales 0, second moments 0)
+    GEFEN_HIP(fill_zero(st->codes, st->code_bytes, stream));
+    GEFEN_HIP(fill_zero(st->scale, 4 * st->total_blocks, stream));
+    GEFEN_HIP(fill_zero(st->vmom, 4 * st->total_blocks, stream));
+
+    // codebook from the first gradients (Alg. 3)
+    if ((rc = fit_into_slot(st.get(), 0, stream))) return rc;
+    st->dec_slot = st->enc_slot = 0;
+    GEFEN_HIP(hipStreamSynchronize(stream));
+    *out = st.release();
+    return GEFEN_OK;
+}
+
+int gefen_step(gefen_state* st, const gefen_tensor* params, const gefen_tensor* grads,
+               int32_t n_tensors, double lr, double beta1, double beta2, double eps,
+               double weight_decay, int64_t t, void* stream_)
+{
+    int rc = check_against_state(st, params, n_tensors, true, "params");
+    if (rc) return rc;
+    if ((rc = check_against_state(st, grads, n_tensors, false, "grads"))) return rc;
+    if (t < 1) return fail(GEFEN_EINVAL, "t must be >= 1 (got %lld)", (long long)t);
+    if (!(beta1 >= 0.0 && beta1 < 1.0)) return fail(GEFEN_EINVAL, "beta1 must be in [0, 1)");
+    if (!(beta2 >= 0.0 && beta2 < 1.0)) return fail(GEFEN_EINVAL, "beta2 must be in [0, 1)");
+    if (!finite_f(lr) || !finite_f(weight_decay)) return fail(GEFEN_EINVAL, "lr and weight_decay must be finite");
+    if (!finite_f(eps) || eps < 0.0) return fail(GEFEN_EINVAL, "eps must be finite and >= 0");
+    hipStream_t stream = as_stream(stream_);
+    if ((rc = refresh_segs(st, params, grads, stream))) return rc;
+
+    const double bc1 = 1.0 - std::pow(beta1, static_cast<double>(t));
+    const double bc2 = 1.0 - std::pow(beta2, static_cast<double>(t));
+    StepScalars sc;
+    sc.beta1 = static_cast<float>(beta1);
+    sc.one_minus_beta1 = static_cast<float>(1.0 - beta1);
+    sc.beta2 = static_cast<float>(beta2);
+    sc.one_minus_beta2 = static_cast<float>(1.0 - beta2);
+    sc.step_size = static_cast<float>(lr / bc1);
+    sc.inv_bc2 = static_cast<float>(1.0 / bc2);
+    sc.eps = static_cast<float>(eps);
+    sc.decay = static_cast<float>(1.0 - lr * weight_decay);
+    const CodebookDev cb = codebook_dev(st);
+    const bool prof = st->prof_armed && st->prof_steps < st->prof_max_steps;
+    const size_t ncls = st->classes.size();
+    for (size_t ci = 0; ci < ncls; ++ci) {
+        const Class& c = st->classes[ci];
+        if (prof) GEFEN_HIP(hipEventRecord(st->prof_events[(st->prof_steps * ncls + ci) * 2], stream));
+        hipError_t e = launch_step(c.kind, c.gdtype, c.vpl, st->tiles + c.first, c.count,
+                                   st->segs, st->codes, st->scale, st->vmom, cb, sc, stream);
+        if (e != hipSuccess)
+            return fail(GEFEN_EHIP, "step launch (kind %d) failed: %s", c.kind, hipGetErrorString(e));
+        if (prof) GEFEN_HIP(hipEventRecord(st->prof_events[(st->prof_steps * ncls + ci) * 2 + 1], stream));
+    }
+    if (prof) ++st->prof_steps;
+    st->dec_slot = st->enc_slot;
+    if (std::getenv("GEFEN_DEBUG_SYNC")) {
+        GEFEN_HIP(hipStreamSynchronize(stream));
+        GEFEN_HIP(hipGetLastError());
+    }
+    return GEFEN_OK;
+}
+
+int gefen_fit_codebook(gefen_state* st, const gefen_tensor* grads, int32_t n_tensors,
+                       void* stream_)
+{
+    int rc = check_against_state(st, grads, n_tensors, false, "grads");
+    if (rc) return rc;
+    hipStream_t stream = as_stream(stream_);
+    if ((rc = refresh_segs(st, nullptr, grads, stream))) return rc;
+    const int slot = 1 - st->dec_slot;
+    if ((rc = fit_into_slot(st, slot, stream))) return rc;
+    st->enc_slot = slot;
+    return GEFEN_OK;
+}
+
+int gefen_partition_scores(const gefen_tensor* grad, double eps_part, int64_t* divisors_out,
+                           double* scores_out, int32_t cap, int32_t* n_div, int64_t* period_out,
+                           void* stream_)
+{
+    g_err.clear();
+    int rc = check_tensors(grad, 1, false, "grad");
+    if (rc) return rc;
+    if (!n_div || !period_out) return fail(GEFEN_EINVAL, "n_div and period_out must not be NULL");
+    if (!finite_f(eps_part) || eps_part < 0) return fail(GEFEN_EINVAL, "eps_part must be >= 0");
+    std::vector<int64_t> per, divs;
+    std::vector<double> scores;
+    rc = infer_periods(std::vector<gefen_tensor>{*grad}, eps_part, as_stream(stream_), per,
+                       &divs, &scores);
+    if (rc) return rc;
+    *n_div = static_cast<int32_t>(divs.size());
+    *period_out = per[0];
+    if (static_cast<int64_t>(divs.size()) > cap)
+        return fail(GEFEN_EINVAL, "cap %d < %zu divisors", cap, divs.size());
+    if (divisors_out) std::memcpy(divisors_out, divs.data(), sizeof(int64_t) * divs.size());
+    if (scores_out) std::memcpy(scores_out, scores.data(), sizeof(double) * scores.size());
+    return GEFEN_OK;
+}
+
+int gefen_histogram(gefen_state* st, const gefen_tensor* grads, int32_t n_tensors,
+                    uint64_t* hist_out, void* stream_)
+{
+    int rc = check_against_state(st, grads, n_tensors, false, "grads");
+    if (rc) return rc;
+    if (!hist_out) return fail(GEFEN_EINVAL, "hist_out is NULL");
+    hipStream_t stream = as_stream(stream_);
+    if ((rc = refresh_segs(st, nullptr, grads, stream))) return rc;
+    GEFEN_HIP(fill_zero(hist_out, sizeof(uint64_t) * st->nbins, stream));
+    GEFEN_HIP(launch_histogram(st->tiles, st->n_tiles, st->tile_kind, st->segs, st->nbins,
+                               hist_out, stream));
+    return GEFEN_OK;
+}
+
+int gefen_dp_codebook(const uint64_t* hist, int32_t nbins, int32_t k, double* codebook_out,
+                      double* cost_out, int32_t* status_out, void* stream_)
+{
+    g_err.clear();
+    if (!hist || !codebook_out || !cost_out || !status_out)
+        return fail(GEFEN_EINVAL, "NULL argument");
+    if (k < 2 || k > kMaxK) return fail(GEFEN_EINVAL, "k must be in [2, %d]", kMaxK);
+    if (nbins < 1 || nbins > 16 * kMaxK) return fail(GEFEN_EINVAL, "nbins must be in [1, %d]", 16 * kMaxK);
+    hipStream_t stream = as_stream(stream_);
+    void* ws = nullptr;
+    GEFEN_HIP(hipMallocAsync(&ws, dp_workspace_bytes(nbins, k), stream));
+    hipError_t e = launch_dp(hist, nbins, k, ws, codebook_out, cost_out, status_out, stream);
+    (void)hipFreeAsync(ws, stream);
+    if (e != hipSuccess) return fail(GEFEN_EHIP, "DP launch failed: %s", hipGetErrorString(e));
+    return GEFEN_OK;
+}
+
+int gefen_get_periods(const gefen_state* st, int64_t* periods_out)
+{
+    if (!st || !periods_out) return fail(GEFEN_EINVAL, "NULL argument");
+    for (int32_t i = 0; i < st->n_tensors; ++i) periods_out[i] = st->period[i];
+    return GEFEN_OK;
+}
+
+int gefen_get_layout(const gefen_state* st, int64_t* code_offsets, int64_t* block_index,
+                     int64_t* total_code_bytes, int64_t* total_blocks, int32_t* k)
+{
+    if (!st) return fail(GEFEN_EINVAL, "state is NULL");
+    if (code_offsets) std::memcpy(code_offsets, st->code_off.data(), 8 * (st->n_tensors + 1));
+    if (block_index) std::memcpy(block_index, st->blk_begin.data(), 8 * (st->n_tensors + 1));
+    if (total_code_bytes) *total_code_bytes = st->code_bytes;
+    if (total_blocks) *total_blocks = st->total_blocks;
+    if (k) *k = st->k;
+    return GEFEN_OK;
+}
+
+static int state_array(const gefen_state* st, int32_t which, void** ptr, int64_t* bytes)
+{
+    switch (which) {
+    case 0: *ptr = st->codes; *bytes = st->code_bytes; return GEFEN_OK;
+    case 1: *ptr = st->scale; *bytes = 4 * st->total_blocks; return GEFEN_OK;
+    case 2: *ptr = st->vmom; *bytes = 4 * st->total_blocks; return GEFEN_OK;
+    case 3: *ptr = st->cb32[st->dec_slot]; *bytes = 4 * st->k; return GEFEN_OK;
+    case 4: *ptr = st->cb32[st->enc_slot]; *bytes = 4 * st->k; return GEFEN_OK;
+    case 5: *ptr = st->cb64[st->dec_slot]; *bytes = 8 * st->k; return GEFEN_OK;
+    default: return fail(GEFEN_EINVAL, "unknown state array %d", which);
+    }
+}
+
+int gefen_read_state(const gefen_state* st, int32_t which, void* dst, int64_t bytes,
+                     void* stream_)
+{
+    if (!st || !dst) return fail(GEFEN_EINVAL, "NULL argument");
+    void* src;
+    int64_t need;
+    int rc = state_array(st, which, &src, &need);
+    if (rc) return rc;
+    if (bytes != need) return fail(GEFEN_EINVAL, "bytes = %lld, array has %lld", (long long)bytes, (long long)need);
+    hipStream_t stream = as_stream(stream_);
+    GEFEN_HIP(hipMemcpyAsync(dst, src, need, hipMemcpyDefault, stream));
+    if (is_host_ptr(dst)) GEFEN_HIP(hipStreamSynchronize(stream));
+    return GEFEN_OK;
+}
+
+int gefen_write_state(gefen_state* st, int32_t which, const void* src, int64_t bytes,
+                      void* stream_)
+{
+    if (!st || !src) return fail(GEFEN_EINVAL, "NULL argument");
+    if (which == 5) return fail(GEFEN_EINVAL, "array 5 is read-only");
+    void* dst;
+    int64_t need;
+    int rc = state_array(st, which, &dst, &need);
+    if (rc) return rc;
+    if (bytes != need) return fail(GEFEN_EINVAL, "bytes = %lld, array has %lld", (long long)bytes, (long long)need);
+    hipStream_t stream = as_stream(stream_);
+    if (which == 3 || which == 4) {
+        std::vector<float> cb(st->k);
+        GEFEN_HIP(hipMemcpyAsync(cb.data(), src, need, hipMemcpyDefault, stream));
+        GEFEN_HIP(hipStreamSynchronize(stream));
+        if (cb[0] != -1.0f || cb[st->k - 1] != 1.0f)
+            return fail(GEFEN_EINVAL, "codebook must start at -1 and end at +1");
+        for (int i = 1; i < st->k; ++i)
+            if (!(cb[i] > cb[i - 1])) return fail(GEFEN_EINVAL, "codebook must increase strictly");
+        const int slot = which == 3 ? st->dec_slot : st->enc_slot;
+        float* staging = nullptr;
+        GEFEN_HIP(hipMallocAsync(reinterpret_cast<void**>(&staging), need, stream));
+        GEFEN_HIP(hipMemcpyAsync(staging, cb.data(), need, hipMemcpyHostToDevice, stream));
+        hipError_t e = launch_install_codebook_f32(staging, st->k, st->ng, st->cb32[slot],
+                                                   st->cb64[slot], st->mid[slot],
+                                                   st->guide[slot], stream);
+        (void)hipFreeAsync(staging, stream);
+        GEFEN_HIP(e);
+        GEFEN_HIP(hipStreamSynchronize(stream));
+        return GEFEN_OK;
+    }
+    GEFEN_HIP(hipMemcpyAsync(dst, src, need, hipMemcpyDefault, stream));
+    if (is_host_ptr(src)) GEFEN_HIP(hipStreamSynchronize(stream));
+    return GEFEN_OK;
+}
+
+int gefen_get_fit_info(const gefen_state* st, double* cost_out, int32_t* status_out,
+                       void* stream_)
+{
+    if (!st) return fail(GEFEN_EINVAL, "state is NULL");
+    hipStream_t stream = as_stream(stream_);
+    double c = 0;
+    int32_t s = 0;
+    GEFEN_HIP(hipMemcpyAsync(&c, st->fit_cost, 8, hipMemcpyDeviceToHost, stream));
+    GEFEN_HIP(hipMemcpyAsync(&s, st->fit_status, 4, hipMemcpyDeviceToHost, stream));
+    GEFEN_HIP(hipStreamSynchronize(stream));
+    if (cost_out) *cost_out = c;
+    if (status_out) *status_out = s;
+    return GEFEN_OK;
+}
+
+int gefen_state_bytes(const gefen_state* st, int64_t* persistent, int64_t* workspace)
+{
+    if (!st) return fail(GEFEN_EINVAL, "state is NULL");
+    if (persistent) *persistent = st->persistent_bytes;
+    if (workspace) *workspace = st->workspace_bytes;
+    return GEFEN_OK;
+}
+
+int gefen_checkpoint_bytes(const gefen_state* st, int64_t* bytes)
+{
+    if (!st || !bytes) return fail(GEFEN_EINVAL, "NULL argument");
+    *bytes = ckpt_layout(st).total;
+    return GEFEN_OK;
+}
+
+int gefen_export(const gefen_state* st, void* dst, int64_t bytes, void* stream_)
+{
+    if (!st || !dst) return fail(GEFEN_EINVAL, "NULL argument");
+    const CkptLayout L = ckpt_layout(st);
+    if (bytes != L.total) return fail(GEFEN_EINVAL, "checkpoint needs %lld bytes", (long long)L.total);
+    hipStream_t stream = as_stream(stream_);
+    char* d = static_cast<char*>(dst);
+    int64_t hdr[8] = {kCkptMagic | (int64_t(1) << 32), st->n_tensors, st->k, st->code_bytes,
+                      st->total_blocks, st->dec_slot, st->enc_slot, 0};
+    GEFEN_HIP(hipMemcpyAsync(d + L.header, hdr, sizeof hdr, hipMemcpyDefault, stream));
+    GEFEN_HIP(hipMemcpyAsync(d + L.codes, st->codes, st->code_bytes, hipMemcpyDefault, stream));
+    GEFEN_HIP(hipMemcpyAsync(d + L.scale, st->scale, 4 * st->total_blocks, hipMemcpyDefault, stream));
+    GEFEN_HIP(hipMemcpyAsync(d + L.vmom, st->vmom, 4 * st->total_blocks, hipMemcpyDefault, stream));
+    GEFEN_HIP(hipMemcpyAsync(d + L.cb0, st->cb64[0], 8 * st->k, hipMemcpyDefault, stream));
+    GEFEN_HIP(hipMemcpyAsync(d + L.cb1, st->cb64[1], 8 * st->k, hipMemcpyDefault, stream));
+    GEFEN_HIP(hipStreamSynchronize(stream));   // the header lives on this host stack
+    return GEFEN_OK;
+}
+
+int gefen_import(gefen_state* st, const void* src, int64_t bytes, void* stream_)
+{
+    if (!st || !src) return fail(GEFEN_EINVAL, "NULL argument");
+    const CkptLayout L = ckpt_layout(st);
+    if (bytes != L.total) return fail(GEFEN_EINVAL, "checkpoint needs %lld bytes", (long long)L.total);
+    hipStream_t stream = as_stream(stream_);
+    const char* s = static_cast<const char*>(src);
+    int64_t hdr[8];
+    GEFEN_HIP(hipMemcpyAsync(hdr, s + L.header, sizeof hdr, hipMemcpyDefault, stream));
+    GEFEN_HIP(hipStreamSynchronize(stream));
+    if (hdr[0] != (kCkptMagic | (int64_t(1) << 32)) || hdr[1] != st->n_tensors ||
+        hdr[2] != st->k || hdr[3] != st->code_bytes || hdr[4] != st->total_blocks ||
+        hdr[5] < 0 || hdr[5] > 1 || hdr[6] < 0 || hdr[6] > 1)
+        return fail(GEFEN_EINVAL, "checkpoint does not match this state");
+    GEFEN_HIP(hipMemcpyAsync(st->codes, s + L.codes, st->code_bytes, hipMemcpyDefault, stream));
+    GEFEN_HIP(hipMemcpyAsync(st->scale, s + L.scale, 4 * st->total_blocks, hipMemcpyDefault, stream));
+    GEFEN_HIP(hipMemcpyAsync(st->vmom, s + L.vmom, 4 * st->total_blocks, hipMemcpyDefault, stream));
+    double* staging = nullptr;
+    GEFEN_HIP(hipMallocAsync(reinterpret_cast<void**>(&staging), 16 * st->k, stream));
+    GEFEN_HIP(hipMemcpyAsync(staging, s + L.cb0, 16 * st->k, hipMemcpyDefault, stream));
+    for (int slot = 0; slot < 2; ++slot) {
+        hipError_t e = launch_install_codebook(staging + slot * st->k, st->k, st->ng,
+                                               st->cb32[slot], st->cb64[slot], st->mid[slot],
+                                               st->guide[slot], stream);
+        if (e != hipSuccess) {
+            (void)hipFreeAsync(staging, stream);
+            return fail(GEFEN_EHIP, "codebook install failed: %s", hipGetErrorString(e));
+        }
+    }
+    (void)hipFreeAsync(staging, stream);
+    GEFEN_HIP(hipStreamSynchronize(stream));
+    st->dec_slot = static_cast<int>(hdr[5]);
+    st->enc_slot = static_cast<int>(hdr[6]);
+    return GEFEN_OK;
+}
+
+int gefen_profile_begin(gefen_state* st, int32_t max_steps)
+{
+    if (!st || max_steps < 1) return fail(GEFEN_EINVAL, "bad arguments");
+    st->prof_free();
+    const size_t n = static_cast<size_t>(max_steps) * st->classes.size() * 2;
+    st->prof_events.resize(n, nullptr);
+    for (size_t i = 0; i < n; ++i) GEFEN_HIP(hipEventCreate(&st->prof_events[i]));
+    st->prof_max_steps = max_steps;
+    st->prof_steps = 0;
+    st->prof_armed = true;
+    return GEFEN_OK;
+}
+
+int gefen_profile_end(gefen_state* st, int32_t cap, int32_t* n_classes, int32_t* kind,
+                      int32_t* vpl, int32_t* gdtype, int64_t* launches, double* total_ms,
+                      int64_t* elems_per_launch, int64_t* bytes_per_launch)
+{
+    if (!st || !n_classes) return fail(GEFEN_EINVAL, "bad arguments");
+    const size_t ncls = st->classes.size();
+    *n_classes = static_cast<int32_t>(ncls);
+    if (static_cast<int64_t>(ncls) > cap) return fail(GEFEN_EINVAL, "cap < %zu classes", ncls);
+    std::vector<double> ms(ncls, 0.0);
+    if (st->prof_armed && st->prof_steps > 0) {
+        GEFEN_HIP(hipEventSynchronize(st->prof_events[(st->prof_steps * ncls - 1) * 2 + 1]));
+        for (int32_t s = 0; s < st->prof_steps; ++s)
+            for (size_t c = 0; c < ncls; ++c) {
+                float m = 0.0f;
+                GEFEN_HIP(hipEventElapsedTime(&m, st->prof_events[(s * ncls + c) * 2],
+                                              st->prof_events[(s * ncls + c) * 2 + 1]));
+                ms[c] += m;
+            }
+    }
+    for (size_t c = 0; c < ncls; ++c) {
+        const Class& k = st->classes[c];
+        if (kind) kind[c] = k.kind;
+        if (vpl) vpl[c] = k.vpl;
+        if (gdtype) gdtype[c] = k.gdtype;
+        if (launches) launches[c] = st->prof_steps;
+        if (total_ms) total_ms[c] = ms[c];
+        if (elems_per_launch) elems_per_launch[c] = k.elems;
+        if (bytes_per_launch) bytes_per_launch[c] = k.bytes;
+    }
+    st->prof_free();
+    return GEFEN_OK;
+}
+
+void gefen_destroy(gefen_state* st) { delete st; }
+
+}  // extern "C"

@@ -1,0 +1,117 @@
+// Internal declarations shared by the HIP sources of libgefen (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gefen {
+
+// Gradient element types.
+enum : int32_t { DT_F32 = 0, DT_BF16 = 1 };
+
+// Work classes of the step kernels. Every tile belongs to exactly one class.
+//  KIND_U  uniform blocks, p % 4 == 0, 16-byte aligned rows: groups of 2^lpb_log2 lanes
+//          own one block each, every lane holds `vpl` 4-element vectors in registers.
+//  KIND_G  any single block (irregular, unaligned, odd or very large p): the whole
+//          workgroup streams it twice (reduce pass, then update pass).
+//  KIND_L  up to 256 small blocks (<= 32 elements): one lane per block.
+enum : int32_t { KIND_U = 0, KIND_G = 1, KIND_L = 2 };
+
+constexpr int kThreads = 256;         // workgroup size of every step kernel
+constexpr int kMaxVpl = 8;            // max 4-element vectors per lane (KIND_U)
+constexpr int kMaxLpbLog2 = 8;        // KIND_U lanes per block up to 256
+constexpr int kSmallBlock = 32;       // KIND_L blocks hold at most this many elements
+constexpr int kMaxK = 256;            // max codebook entries
+
+// One tile = the work of one workgroup (32 bytes).
+struct Tile {
+    int64_t elem0;      // first element of the tile, relative to its tensor
+    int64_t blk0;       // global index of the tile's first block
+    int64_t nelem;      // elements in the tile
+    int32_t seg;        // tensor index
+    int16_t nblk;       // blocks in the tile
+    uint8_t vpl;        // KIND_U: vectors per lane
+    uint8_t lpb_log2;   // KIND_U: log2(lanes per block)
+};
+static_assert(sizeof(Tile) == 32, "Tile layout");
+
+// Per-tensor descriptor on device (64 bytes). Pointers are refreshed when the caller
+// passes different parameter or gradient buffers.
+struct Seg {
+    float* theta;             // parameters (fp32)
+    const void* grad;         // gradients (fp32 or bf16)
+    int64_t code_off;         // byte offset of the tensor's codes in the codes buffer
+    int64_t period;           // > 0: uniform blocks of this size; 0: explicit blocks
+    int64_t blk_begin;        // global index of the tensor's first block
+    const int64_t* csr;       // explicit blocks: tensor-relative starts (n_blocks + 1)
+    int64_t numel;
+    int32_t gdtype;
+    int32_t pad;
+};
+static_assert(sizeof(Seg) == 64, "Seg layout");
+
+// Scalars of one step, computed on the host in float64 and rounded once.
+struct StepScalars {
+    float beta1, one_minus_beta1;
+    float beta2, one_minus_beta2;
+    float step_size;          // lr / (1 - beta1^t)
+    float inv_bc2;            // 1 / (1 - beta2^t)
+    float eps;
+    float decay;              // 1 - lr * weight_decay
+};
+
+// Codebook tables used by the step: decode entries (fp32[k]) and, for encoding, the
+// midpoints between consecutive entries (fp32[k], last unused) plus a guide table
+// (uint8[ng + 1]) giving, per bucket of [-1, 1], the number of midpoints in lower
+// buckets.
+struct CodebookDev {
+    const float* dec;
+    const float* enc_mid;
+    const uint8_t* enc_guide;
+    int32_t k;
+    int32_t ng;
+};
+
+// Launchers (all enqueue on `stream` and return the launch status).
+hipError_t launch_step(int kind, int gdtype, int vpl, const Tile* tiles, int64_t n_tiles,
+                       const Seg* segs, uint8_t* codes, float* scale, float* vmom,
+                       CodebookDev cb, StepScalars sc, hipStream_t stream);
+
+hipError_t launch_histogram(const Tile* tiles, int64_t n_tiles, const int32_t* tile_kind,
+                            const Seg* segs, int32_t nbins, uint64_t* hist,
+                            hipStream_t stream);
+
+// DP over a device histogram. ws must hold dp_workspace_bytes(nbins, k) bytes.
+size_t dp_workspace_bytes(int32_t nbins, int32_t k);
+hipError_t launch_dp(const uint64_t* hist, int32_t nbins, int32_t k, void* ws,
+                     double* codebook_out, double* cost_out, int32_t* status_out,
+                     hipStream_t stream);
+
+// Install a float64 codebook into a slot: fp32 entries, fp64 copy, midpoints, guide.
+hipError_t launch_install_codebook(const double* cb64_in, int32_t k, int32_t ng,
+                                   float* cb32, double* cb64, float* mid, uint8_t* guide,
+                                   hipStream_t stream);
+// Same from an fp32 codebook (imports).
+hipError_t launch_install_codebook_f32(const float* cb32_in, int32_t k, int32_t ng,
+                                       float* cb32, double* cb64, float* mid,
+                                       uint8_t* guide, hipStream_t stream);
+
+// Block partitioning (Alg. 2) of several tensors.
+struct PartDesc {              // one (tensor, divisor) pair
+    const void* grad;
+    int64_t n;                 // tensor numel
+    int64_t p;                 // divisor
+    int64_t item0;             // first work item of this pair
+    int64_t n_items;           // work items of this pair
+    int64_t out0;              // first partial-output slot
+    int32_t gdtype;
+    int32_t mode;              // 0: pairs of block means per item; 1: sub-chunk sums
+    int32_t rpi;               // mode 0: block pairs per item; mode 1: sub-chunks per block
+    int32_t pad;
+};
+hipError_t launch_partition(const PartDesc* descs, int32_t n_desc, int64_t n_items,
+                            double eps, double* partials, double* scores,
+                            const int32_t* tensor_first_desc, const int32_t* tensor_n_desc,
+                            int32_t n_tensors, int64_t* periods, hipStream_t stream);
+
+}  // namespace gefen

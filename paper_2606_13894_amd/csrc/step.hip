@@ -1,0 +1,453 @@
+// Gefen optimizer step (Alg. 1, loop body) for gfx950.
+//
+// For every block B of a tensor (consecutive `period` elements, or an explicit range):
+//   m_i  = beta1 * (c_dec[q_i] * s_B) + (1 - beta1) * g_i       dequantize + momentum
+//   s_B' = max |m_i|,  q_i' = nearest(c_enc, m_i / s_B')         requantize, new absmax
+//   v_B' = beta2 * v_B + (1 - beta2) * mean(g_i^2)               shared second moment
+//   theta_i = theta_i * (1 - lr*wd) - (lr / (1 - beta1^t)) * m_i / (sqrt(v_B' / (1 - beta2^t)) + eps)
+// The bias-corrected momentum uses the unquantized m_i of the same step.
+//
+// The step is bound by HBM bandwidth (12-14 bytes per element against ~30 FP32
+// operations), so the kernels stream every array once, keep the momentum of a block in
+// registers, and reduce each block with wavefront shuffles (plus LDS across waves).
+// The codebook sits in LDS: decoding is one LDS read; encoding is a guide-table lookup
+// (one byte per bucket of [-1, 1] giving the number of midpoints below the bucket) plus
+// a short scan over the midpoints that fall inside the bucket (at most one for codebooks
+// whose entries are at least a bucket apart, as the DP's are).
+#include "gefen_internal.h"
+
+namespace gefen {
+namespace {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+struct LdsTables {
+    float cb[kMaxK];                  // decode entries
+    float mid[kMaxK];                 // encode midpoints
+    uint8_t guide[16 * kMaxK + 16];   // ng + 1 bytes (padded)
+    float red_ss[kThreads / 64];
+    float red_am[kThreads / 64];
+};
+
+__device__ __forceinline__ void load_tables(LdsTables& L, const CodebookDev& cb)
+{
+    const int t = threadIdx.x;
+    if (t < cb.k) {
+        L.cb[t] = cb.dec[t];
+        L.mid[t] = cb.enc_mid[t];
+    }
+    const int words = (cb.ng + 1 + 3) >> 2;   // the global guide is padded to 16 bytes
+    const uint32_t* src = reinterpret_cast<const uint32_t*>(cb.enc_guide);
+    uint32_t* dst = reinterpret_cast<uint32_t*>(L.guide);
+    for (int i = t; i < words; i += kThreads) dst[i] = src[i];
+}
+
+// Nearest codebook entry of x (ties to the lower index) = number of midpoints < x.
+__device__ __forceinline__ int encode(const LdsTables& L, float x, float half_ng, int ng_m1)
+{
+    x = fminf(fmaxf(x, -1.0f), 1.0f);
+    int b = static_cast<int>((x + 1.0f) * half_ng);
+    b = min(b, ng_m1);
+    int q = L.guide[b];
+    const int hi = L.guide[b + 1];
+    while (q < hi && L.mid[q] < x) ++q;
+    return q;
+}
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+__device__ __forceinline__ float momentum(const LdsTables& L, int q, float s_old, float g,
+                                          const StepScalars& sc)
+{
+    return fmaf(sc.beta1, L.cb[q] * s_old, sc.one_minus_beta1 * g);
+}
+
+__device__ __forceinline__ float load_grad(const void* base, int64_t i, int gdt)
+{
+    if (gdt == DT_F32) return static_cast<const float*>(base)[i];
+    return __uint_as_float(static_cast<uint32_t>(static_cast<const uint16_t*>(base)[i]) << 16);
+}
+
+// Block-local scalars after the reductions.
+struct BlockOut {
+    float s_new, v_new, r, inv_s;
+};
+
+__device__ __forceinline__ BlockOut finish_block(float ss, float am, float v_old, float count,
+                                                 const StepScalars& sc)
+{
+    BlockOut o;
+    o.s_new = am;
+    o.v_new = fmaf(sc.beta2, v_old, sc.one_minus_beta2 * (ss / count));
+    const float denom = sqrtf(o.v_new * sc.inv_bc2) + sc.eps;
+    o.r = sc.step_size / denom;
+    o.inv_s = am > 0.0f ? 1.0f / am : 0.0f;
+    return o;
+}
+
+// ---------------------------------------------------------------------------------
+// KIND_U: uniform blocks of p elements (p % 4 == 0, p <= 4 * 256 * 8). A group of
+// LPB = 2^lpb_log2 lanes owns one block; lane li holds vectors v = j * LPB + li,
+// j < VPL, of 4 consecutive elements each. A workgroup holds 256 / LPB blocks.
+// ---------------------------------------------------------------------------------
+template <int GDT, int VPL, bool ALIGNED>
+__device__ __forceinline__ void step_u_body(LdsTables& L, const Tile& tl, const Seg& sg,
+                                            uint8_t* __restrict__ codes,
+                                            float* __restrict__ scale,
+                                            float* __restrict__ vmom, const CodebookDev& cbd,
+                                            const StepScalars& sc)
+{
+    const int lpb_log2 = tl.lpb_log2;
+    const int lpb = 1 << lpb_log2;
+    const int tid = threadIdx.x;
+    const int gi = tid >> lpb_log2;
+    const int li = tid & (lpb - 1);
+    const bool active = gi < tl.nblk;
+    const int64_t p = sg.period;
+    const int nv = static_cast<int>(p >> 2);
+    const int64_t e0 = tl.elem0 + static_cast<int64_t>(gi) * p;
+    const int64_t blk = tl.blk0 + gi;
+
+    float* __restrict__ th_base = sg.theta + e0;
+    uint8_t* __restrict__ cq_base = codes + sg.code_off + e0;
+
+    float th[VPL][4];
+    float gv[VPL][4];
+    uint32_t cq[VPL];
+#pragma unroll
+    for (int j = 0; j < VPL; ++j) {
+        const int v = j * lpb + li;
+        cq[j] = 0;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) { th[j][c] = 0.0f; gv[j][c] = 0.0f; }
+        if (active && v < nv) {
+            const int64_t o = 4 * static_cast<int64_t>(v);
+            if (ALIGNED) {
+                const f32x4 t4 = __builtin_nontemporal_load(
+                    reinterpret_cast<const f32x4*>(th_base + o));
+                th[j][0] = t4.x; th[j][1] = t4.y; th[j][2] = t4.z; th[j][3] = t4.w;
+                if (GDT == DT_F32) {
+                    const f32x4 g4 = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(
+                        static_cast<const float*>(sg.grad) + e0 + o));
+                    gv[j][0] = g4.x; gv[j][1] = g4.y; gv[j][2] = g4.z; gv[j][3] = g4.w;
+                } else {
+                    const u32x2 g2 = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(
+                        static_cast<const uint16_t*>(sg.grad) + e0 + o));
+                    gv[j][0] = bf16_lo(g2.x); gv[j][1] = bf16_hi(g2.x);
+                    gv[j][2] = bf16_lo(g2.y); gv[j][3] = bf16_hi(g2.y);
+                }
+            } else {
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    th[j][c] = th_base[o + c];
+                    gv[j][c] = load_grad(sg.grad, e0 + o + c, GDT);
+                }
+            }
+            cq[j] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(cq_base + o));
+        }
+    }
+    float s_old = 0.0f, v_old = 0.0f;
+    if (active) {
+        s_old = scale[blk];
+        v_old = vmom[blk];
+    }
+    load_tables(L, cbd);
+    __syncthreads();
+
+    // phase 1: dequantize + momentum, block reductions of sum g^2 and max |m|
+    // (lanes past the end of their block, or without a block, contribute 0 to both)
+    float m[VPL][4];
+    float ss = 0.0f, am = 0.0f;
+#pragma unroll
+    for (int j = 0; j < VPL; ++j) {
+        const bool ok = active && (j * lpb + li) < nv;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const int q = (cq[j] >> (8 * c)) & 0xff;
+            const float mm = ok ? momentum(L, q, s_old, gv[j][c], sc) : 0.0f;
+            m[j][c] = mm;
+            ss = fmaf(gv[j][c], gv[j][c], ss);
+            am = fmaxf(am, fabsf(mm));
+        }
+    }
+    const int wl = lpb < 64 ? lpb : 64;
+    for (int off = 1; off < wl; off <<= 1) {
+        ss += __shfl_xor(ss, off);
+        am = fmaxf(am, __shfl_xor(am, off));
+    }
+    if (lpb > 64) {
+        const int wave = tid >> 6;
+        if ((tid & 63) == 0) {
+            L.red_ss[wave] = ss;
+            L.red_am[wave] = am;
+        }
+        __syncthreads();
+        const int wpb = lpb >> 6;
+        const int w0 = (wave / wpb) * wpb;
+        ss = L.red_ss[w0];
+        am = L.red_am[w0];
+        for (int w = 1; w < wpb; ++w) {
+            ss += L.red_ss[w0 + w];
+            am = fmaxf(am, L.red_am[w0 + w]);
+        }
+    }
+    if (!active) return;
+
+    const BlockOut bo = finish_block(ss, am, v_old, static_cast<float>(p), sc);
+    if (li == 0) {
+        scale[blk] = bo.s_new;
+        vmom[blk] = bo.v_new;
+    }
+    const float half_ng = 0.5f * static_cast<float>(cbd.ng);
+    const int ng_m1 = cbd.ng - 1;
+#pragma unroll
+    for (int j = 0; j < VPL; ++j) {
+        const int v = j * lpb + li;
+        if (v < nv) {
+            uint32_t packed = 0;
+            float out[4];
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const float mm = m[j][c];
+                const int q = bo.s_new > 0.0f ? encode(L, mm * bo.inv_s, half_ng, ng_m1) : 0;
+                packed |= static_cast<uint32_t>(q) << (8 * c);
+                out[c] = fmaf(-bo.r, mm, th[j][c] * sc.decay);
+            }
+            const int64_t o = 4 * static_cast<int64_t>(v);
+            if (ALIGNED) {
+                const f32x4 o4 = {out[0], out[1], out[2], out[3]};
+                __builtin_nontemporal_store(o4, reinterpret_cast<f32x4*>(th_base + o));
+            } else {
+#pragma unroll
+                for (int c = 0; c < 4; ++c) th_base[o + c] = out[c];
+            }
+            __builtin_nontemporal_store(packed, reinterpret_cast<uint32_t*>(cq_base + o));
+        }
+    }
+}
+
+template <int GDT, int VPL>
+__global__ __launch_bounds__(kThreads) void k_step_u(const Tile* __restrict__ tiles,
+                                                     const Seg* __restrict__ segs,
+                                                     uint8_t* __restrict__ codes,
+                                                     float* __restrict__ scale,
+                                                     float* __restrict__ vmom, CodebookDev cbd,
+                                                     StepScalars sc)
+{
+    __shared__ LdsTables L;
+    const Tile tl = tiles[blockIdx.x];
+    const Seg sg = segs[tl.seg];
+    const uintptr_t galign = GDT == DT_F32 ? 15 : 7;
+    const bool aligned = ((reinterpret_cast<uintptr_t>(sg.theta) & 15) == 0) &&
+                         ((reinterpret_cast<uintptr_t>(sg.grad) & galign) == 0);
+    if (aligned)
+        step_u_body<GDT, VPL, true>(L, tl, sg, codes, scale, vmom, cbd, sc);
+    else
+        step_u_body<GDT, VPL, false>(L, tl, sg, codes, scale, vmom, cbd, sc);
+}
+
+// ---------------------------------------------------------------------------------
+// Block range of block `bi` of a tile (tensor-relative start, length).
+// ---------------------------------------------------------------------------------
+__device__ __forceinline__ void block_range(const Seg& sg, const Tile& tl, int bi,
+                                            int64_t& start, int64_t& len)
+{
+    if (sg.period > 0) {
+        start = tl.elem0 + static_cast<int64_t>(bi) * sg.period;
+        len = sg.period;
+    } else {
+        const int64_t local = tl.blk0 + bi - sg.blk_begin;
+        start = sg.csr[local];
+        len = sg.csr[local + 1] - start;
+    }
+}
+
+// ---------------------------------------------------------------------------------
+// KIND_G: one block per workgroup of any size and alignment, streamed twice: the
+// first pass reduces sum g^2 and max |m|; the second recomputes m bit-identically
+// (same operations on the same inputs), requantizes and updates the parameters.
+// ---------------------------------------------------------------------------------
+template <int GDT>
+__global__ __launch_bounds__(kThreads) void k_step_g(const Tile* __restrict__ tiles,
+                                                     const Seg* __restrict__ segs,
+                                                     uint8_t* __restrict__ codes,
+                                                     float* __restrict__ scale,
+                                                     float* __restrict__ vmom, CodebookDev cbd,
+                                                     StepScalars sc)
+{
+    __shared__ LdsTables L;
+    const Tile tl = tiles[blockIdx.x];
+    const Seg sg = segs[tl.seg];
+    const int tid = threadIdx.x;
+    const int64_t len = tl.nelem;
+    const int64_t e0 = tl.elem0;
+    const int64_t blk = tl.blk0;
+    float* __restrict__ th = sg.theta + e0;
+    uint8_t* __restrict__ cq = codes + sg.code_off + e0;
+    const void* gp = GDT == DT_F32
+                         ? static_cast<const void*>(static_cast<const float*>(sg.grad) + e0)
+                         : static_cast<const void*>(static_cast<const uint16_t*>(sg.grad) + e0);
+    const float s_old = scale[blk];
+    const float v_old = vmom[blk];
+    load_tables(L, cbd);
+    __syncthreads();
+
+    float ss = 0.0f, am = 0.0f;
+#pragma unroll 4
+    for (int64_t i = tid; i < len; i += kThreads) {
+        const float g = load_grad(gp, i, GDT);
+        const float mm = momentum(L, cq[i], s_old, g, sc);
+        ss = fmaf(g, g, ss);
+        am = fmaxf(am, fabsf(mm));
+    }
+    for (int off = 1; off < 64; off <<= 1) {
+        ss += __shfl_xor(ss, off);
+        am = fmaxf(am, __shfl_xor(am, off));
+    }
+    const int wave = tid >> 6;
+    if ((tid & 63) == 0) {
+        L.red_ss[wave] = ss;
+        L.red_am[wave] = am;
+    }
+    __syncthreads();
+    ss = L.red_ss[0];
+    am = L.red_am[0];
+    for (int w = 1; w < kThreads / 64; ++w) {
+        ss += L.red_ss[w];
+        am = fmaxf(am, L.red_am[w]);
+    }
+    const BlockOut bo = finish_block(ss, am, v_old, static_cast<float>(len), sc);
+    if (tid == 0) {
+        scale[blk] = bo.s_new;
+        vmom[blk] = bo.v_new;
+    }
+    const float half_ng = 0.5f * static_cast<float>(cbd.ng);
+    const int ng_m1 = cbd.ng - 1;
+#pragma unroll 4
+    for (int64_t i = tid; i < len; i += kThreads) {
+        const float g = load_grad(gp, i, GDT);
+        const float mm = momentum(L, cq[i], s_old, g, sc);
+        const int q = bo.s_new > 0.0f ? encode(L, mm * bo.inv_s, half_ng, ng_m1) : 0;
+        th[i] = fmaf(-bo.r, mm, th[i] * sc.decay);
+        cq[i] = static_cast<uint8_t>(q);
+    }
+}
+
+// ---------------------------------------------------------------------------------
+// KIND_L: up to 256 small blocks (<= 32 elements) per workgroup, one lane per block.
+// ---------------------------------------------------------------------------------
+template <int GDT>
+__global__ __launch_bounds__(kThreads) void k_step_l(const Tile* __restrict__ tiles,
+                                                     const Seg* __restrict__ segs,
+                                                     uint8_t* __restrict__ codes,
+                                                     float* __restrict__ scale,
+                                                     float* __restrict__ vmom, CodebookDev cbd,
+                                                     StepScalars sc)
+{
+    __shared__ LdsTables L;
+    const Tile tl = tiles[blockIdx.x];
+    const Seg sg = segs[tl.seg];
+    load_tables(L, cbd);
+    __syncthreads();
+    const int bi = threadIdx.x;
+    if (bi >= tl.nblk) return;
+    int64_t start, len;
+    block_range(sg, tl, bi, start, len);
+    const int64_t blk = tl.blk0 + bi;
+    float* __restrict__ th = sg.theta + start;
+    uint8_t* __restrict__ cq = codes + sg.code_off + start;
+    const void* gp =
+        GDT == DT_F32 ? static_cast<const void*>(static_cast<const float*>(sg.grad) + start)
+                      : static_cast<const void*>(static_cast<const uint16_t*>(sg.grad) + start);
+    const float s_old = scale[blk];
+    const float v_old = vmom[blk];
+    float m[kSmallBlock];
+    float ss = 0.0f, am = 0.0f;
+#pragma unroll
+    for (int i = 0; i < kSmallBlock; ++i) {
+        m[i] = 0.0f;
+        if (i < len) {
+            const float g = load_grad(gp, i, GDT);
+            m[i] = momentum(L, cq[i], s_old, g, sc);
+            ss = fmaf(g, g, ss);
+            am = fmaxf(am, fabsf(m[i]));
+        }
+    }
+    const BlockOut bo = finish_block(ss, am, v_old, static_cast<float>(len), sc);
+    scale[blk] = bo.s_new;
+    vmom[blk] = bo.v_new;
+    const float half_ng = 0.5f * static_cast<float>(cbd.ng);
+    const int ng_m1 = cbd.ng - 1;
+#pragma unroll
+    for (int i = 0; i < kSmallBlock; ++i) {
+        if (i < len) {
+            const float mm = m[i];
+            const int q = bo.s_new > 0.0f ? encode(L, mm * bo.inv_s, half_ng, ng_m1) : 0;
+            th[i] = fmaf(-bo.r, mm, th[i] * sc.decay);
+            cq[i] = static_cast<uint8_t>(q);
+        }
+    }
+}
+
+template <int GDT>
+hipError_t launch_u(int vpl, dim3 grid, const Tile* tiles, const Seg* segs, uint8_t* codes,
+                    float* scale, float* vmom, CodebookDev cb, StepScalars sc, hipStream_t s)
+{
+    switch (vpl) {
+#define GEFEN_U_CASE(V)                                                                     \
+    case V:                                                                                 \
+        hipLaunchKernelGGL((k_step_u<GDT, V>), grid, dim3(kThreads), 0, s, tiles, segs,     \
+                           codes, scale, vmom, cb, sc);                                     \
+        break;
+        GEFEN_U_CASE(1)
+        GEFEN_U_CASE(2)
+        GEFEN_U_CASE(3)
+        GEFEN_U_CASE(4)
+        GEFEN_U_CASE(5)
+        GEFEN_U_CASE(6)
+        GEFEN_U_CASE(7)
+        GEFEN_U_CASE(8)
+#undef GEFEN_U_CASE
+    default:
+        return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_step(int kind, int gdtype, int vpl, const Tile* tiles, int64_t n_tiles,
+                       const Seg* segs, uint8_t* codes, float* scale, float* vmom,
+                       CodebookDev cb, StepScalars sc, hipStream_t stream)
+{
+    if (n_tiles <= 0) return hipSuccess;
+    if (n_tiles > 0x7fffffffLL) return hipErrorInvalidValue;
+    const dim3 grid(static_cast<unsigned>(n_tiles));
+    if (kind == KIND_U) {
+        return gdtype == DT_F32 ? launch_u<DT_F32>(vpl, grid, tiles, segs, codes, scale, vmom, cb, sc, stream)
+                                : launch_u<DT_BF16>(vpl, grid, tiles, segs, codes, scale, vmom, cb, sc, stream);
+    }
+    if (kind == KIND_G) {
+        if (gdtype == DT_F32)
+            hipLaunchKernelGGL((k_step_g<DT_F32>), grid, dim3(kThreads), 0, stream, tiles, segs,
+                               codes, scale, vmom, cb, sc);
+        else
+            hipLaunchKernelGGL((k_step_g<DT_BF16>), grid, dim3(kThreads), 0, stream, tiles,
+                               segs, codes, scale, vmom, cb, sc);
+        return hipGetLastError();
+    }
+    if (kind == KIND_L) {
+        if (gdtype == DT_F32)
+            hipLaunchKernelGGL((k_step_l<DT_F32>), grid, dim3(kThreads), 0, stream, tiles, segs,
+                               codes, scale, vmom, cb, sc);
+        else
+            hipLaunchKernelGGL((k_step_l<DT_BF16>), grid, dim3(kThreads), 0, stream, tiles,
+                               segs, codes, scale, vmom, cb, sc);
+        return hipGetLastError();
+    }
+    return hipErrorInvalidValue;
+}
+
+}  // namespace gefen

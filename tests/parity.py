@@ -1,0 +1,169 @@
+"""Teacher-forced parity between the HIP library and the float64 oracle.
+
+Test infrastructure. Before every step the oracle is loaded with the library's state
+after the previous step (parameters, codes, scales, second moments, both codebooks,
+widened exactly to float64), gets the same gradient bits, and every output of the
+step is compared element by element:
+
+* codes: equal, or adjacent where the oracle's x = m / s' lies within
+  delta = 1e-6 * max(1, (beta1*s + (1-beta1)*max|g|) / s') of the two entries' midpoint
+  (a tie decided by fp32 rounding);
+* scale s': |diff| <= 1e-6 * s' + 1e-6 * (beta1*s + (1-beta1)*max|g|);
+* second moment v': relative error <= 4e-6 (fp32 tree sum of up to 2^16 terms);
+* parameters: |diff| <= 1e-5 * |theta_ref| + 1e-5 * lr * u_scale, where u_scale is the
+  magnitude of the update's operands, (beta1*|c[q]*s| + (1-beta1)*|g|) / (1 - beta1^t)
+  / (sqrt(v_hat) + eps) + wd*|theta| >= |u_ref|: relative 1e-5 in fp32, with a floor
+  for parameters near zero and for momenta that cancel (the fp32 error of
+  m = beta1*c[q]*s + (1-beta1)*g is relative to its summands, not to m).
+
+Teacher forcing is needed because a legitimate tie flip changes the next momentum by a
+codebook gap times the scale, which a free-running comparison would accumulate.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+import oracle
+import paper_2606_13894_amd as gf
+
+
+def grad_bits(g: torch.Tensor) -> np.ndarray:
+    """Gradient as the oracle takes it: float32 values or bf16 bit patterns (uint16)."""
+    if g.dtype == torch.float32:
+        return g.detach().reshape(-1).cpu().numpy()
+    if g.dtype == torch.bfloat16:
+        return g.detach().reshape(-1).view(torch.int16).cpu().numpy().view(np.uint16)
+    raise TypeError(g.dtype)
+
+
+def grad_f64(g: torch.Tensor) -> np.ndarray:
+    return g.detach().reshape(-1).float().cpu().numpy().astype(np.float64)
+
+
+class Run:
+    """A library state plus the per-tensor block structure, for parity checks."""
+
+    def __init__(self, params, grads0, block_offsets=None, **init_kwargs):
+        self.params = list(params)
+        self.state = gf.GefenState(grads0, block_offsets=block_offsets, **init_kwargs)
+        self.numels = [p.numel() for p in self.params]
+        lay = self.state.layout()
+        self.code_off = lay["code_offsets"]
+        self.blk_idx = lay["block_index"]
+        self.k = lay["k"]
+        periods = self.state.periods
+        self.offsets = []
+        if block_offsets is not None:
+            bo = np.asarray(block_offsets, dtype=np.int64)
+            base = 0
+            for n in self.numels:
+                sel = bo[(bo >= base) & (bo <= base + n)] - base
+                self.offsets.append(np.ascontiguousarray(sel))
+                base += n
+        else:
+            for n, p in zip(self.numels, periods):
+                self.offsets.append(np.arange(0, n + 1, p, dtype=np.int64))
+        self.periods = periods
+
+    def snapshot(self):
+        torch.cuda.synchronize()
+        codes = self.state.read(gf.STATE_CODES).cpu().numpy()
+        scale = self.state.read(gf.STATE_SCALE).cpu().numpy().astype(np.float64)
+        v = self.state.read(gf.STATE_V).cpu().numpy().astype(np.float64)
+        snap = {"theta": [], "codes": [], "s": [], "v": [],
+                "cb_dec": self.state.read(gf.STATE_CB_DEC).cpu().numpy().astype(np.float64),
+                "cb_enc": self.state.read(gf.STATE_CB_ENC).cpu().numpy().astype(np.float64)}
+        for i, p in enumerate(self.params):
+            n = self.numels[i]
+            snap["theta"].append(p.detach().reshape(-1).cpu().numpy().astype(np.float64))
+            snap["codes"].append(codes[self.code_off[i]:self.code_off[i] + n].copy())
+            snap["s"].append(scale[self.blk_idx[i]:self.blk_idx[i + 1]].copy())
+            snap["v"].append(v[self.blk_idx[i]:self.blk_idx[i + 1]].copy())
+        return snap
+
+    def step(self, grads, lr, betas, eps, wd, t):
+        self.state.step(self.params, grads, lr, betas, eps, wd, t)
+
+    def oracle_step(self, pre, grads, lr, betas, eps, wd, t):
+        ref = {"theta": [], "codes": [], "s": [], "v": [], "m": []}
+        for i in range(len(self.params)):
+            th = pre["theta"][i].copy()
+            cq = pre["codes"][i].copy()
+            s = pre["s"][i].copy()
+            v = pre["v"][i].copy()
+            m = np.zeros_like(th)
+            oracle.step_blocks(th, grad_bits(grads[i]), cq, s, v, self.offsets[i], pre["cb_dec"],
+                               pre["cb_enc"], lr, betas[0], betas[1], eps, wd, t, m_out=m)
+            for key, val in (("theta", th), ("codes", cq), ("s", s), ("v", v), ("m", m)):
+                ref[key].append(val)
+        return ref
+
+    def check(self, pre, post, ref, grads, lr, betas, eps, wd, t, where=""):
+        """Apply the gates; returns a small report, raises AssertionError on a breach."""
+        b1 = betas[0]
+        rep = {"code_ties": 0, "codes": 0, "max_rel_theta": 0.0, "max_theta_gate": 0.0,
+               "max_rel_v": 0.0}
+        cb = pre["cb_enc"]
+        for i in range(len(self.params)):
+            offs = self.offsets[i]
+            sizes = np.diff(offs)
+            g = np.abs(grad_f64(grads[i]))
+            gmax = np.maximum.reduceat(g, offs[:-1]) if g.size else g
+            s_prev = pre["s"][i]
+            s_ref, s_gpu = ref["s"][i], post["s"][i]
+            floor = b1 * s_prev + (1 - b1) * gmax
+            bad = np.abs(s_gpu - s_ref) > 1e-6 * s_ref + 1e-6 * floor
+            assert not bad.any(), f"{where} tensor {i}: scale mismatch at blocks {np.nonzero(bad)[0][:5]}"
+            v_ref, v_gpu = ref["v"][i], post["v"][i]
+            relv = np.abs(v_gpu - v_ref) / np.maximum(np.abs(v_ref), 1e-300)
+            relv[(v_ref == 0) & (v_gpu == 0)] = 0.0
+            rep["max_rel_v"] = max(rep["max_rel_v"], float(relv.max(initial=0.0)))
+            assert (relv <= 4e-6).all(), f"{where} tensor {i}: v mismatch {relv.max()}"
+            # codes
+            c_ref, c_gpu = ref["codes"][i].astype(np.int64), post["codes"][i].astype(np.int64)
+            diff = c_ref != c_gpu
+            rep["codes"] += c_ref.size
+            if diff.any():
+                idx = np.nonzero(diff)[0]
+                blk = np.searchsorted(offs, idx, side="right") - 1
+                sr = s_ref[blk]
+                assert (sr > 0).all(), f"{where} tensor {i}: code differs in a zero-scale block"
+                x = ref["m"][i][idx] / sr
+                a = np.minimum(c_ref[idx], c_gpu[idx])
+                bb = np.maximum(c_ref[idx], c_gpu[idx])
+                assert (bb - a == 1).all(), f"{where} tensor {i}: non-adjacent code mismatch"
+                midp = 0.5 * (cb[a] + cb[bb])
+                delta = 1e-6 * np.maximum(1.0, floor[blk] / sr)
+                ok = np.abs(x - midp) <= delta
+                assert ok.all(), (f"{where} tensor {i}: {int((~ok).sum())} code mismatches "
+                                  f"outside the tie window (first at {idx[~ok][:3]})")
+                rep["code_ties"] += int(idx.size)
+            # parameters
+            th_ref, th_gpu = ref["theta"][i], post["theta"][i]
+            elem_blk = np.repeat(np.arange(sizes.size), sizes)
+            dq = pre["cb_dec"][pre["codes"][i].astype(np.int64)] * s_prev[elem_blk]
+            terms = b1 * np.abs(dq) + (1 - b1) * g
+            bc1 = 1.0 - b1 ** t
+            vhat = v_ref[elem_blk] / (1.0 - betas[1] ** t)
+            u_scale = terms / bc1 / (np.sqrt(vhat) + eps) + abs(wd) * np.abs(pre["theta"][i])
+            gate = 1e-5 * np.abs(th_ref) + 1e-5 * abs(lr) * u_scale + 1e-30
+            err = np.abs(th_gpu - th_ref)
+            ratio = err / gate
+            rep["max_theta_gate"] = max(rep["max_theta_gate"], float(ratio.max(initial=0)))
+            rel = err / np.maximum(np.abs(th_ref), 1e-30)
+            rep["max_rel_theta"] = max(rep["max_rel_theta"], float(rel.max(initial=0)))
+            if not (err <= gate).all():
+                j = int(ratio.argmax())
+                raise AssertionError(
+                    f"{where} tensor {i}: theta gate exceeded ({ratio[j]:.3g}x) at element {j}: "
+                    f"theta_pre={pre['theta'][i][j]:.9g} ref={th_ref[j]:.9g} gpu={th_gpu[j]:.9g} "
+                    f"m_ref={ref['m'][i][j]:.6g} terms={terms[j]:.6g} u_scale={u_scale[j]:.6g}")
+        return rep
+
+    def teacher_forced_step(self, grads, lr, betas, eps, wd, t, where=""):
+        pre = self.snapshot()
+        self.step(grads, lr, betas, eps, wd, t)
+        post = self.snapshot()
+        ref = self.oracle_step(pre, grads, lr, betas, eps, wd, t)
+        return self.check(pre, post, ref, grads, lr, betas, eps, wd, t, where)

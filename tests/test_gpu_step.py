@@ -1,0 +1,302 @@
+"""GPU parity of the Gefen step (Alg. 1) against the float64 oracle, through the C ABI.
+
+Teacher-forced per step (see parity.py for the gates). Covers every kernel class:
+uniform blocks held in registers (p % 4 == 0, p <= 8192), the two-pass streaming kernel
+(odd, unaligned, irregular or large blocks) and the lane-per-block kernel (blocks of
+at most 32 elements), with fp32 and bf16 gradients, ragged last tiles, zero blocks,
+misaligned tensors, explicit block tables, codebook refits and checkpoints.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+gf = pytest.importorskip("paper_2606_13894_amd")
+
+
+def _dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no HIP device")
+    return torch.device("cuda", 0)
+
+
+def _grad(n, seed, dtype, rows=None, dev=None):
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(seed)
+    g = torch.randn(n, generator=gen, device=dev)
+    if rows:
+        sc = torch.exp(torch.empty(rows, device=dev).uniform_(np.log(1e-3), 0, generator=gen))
+        g = (g.view(rows, -1) * sc[:, None]).reshape(-1)
+    return g.to(dtype)
+
+
+HP = dict(lr=1e-3, betas=(0.9, 0.999), eps=1e-8, wd=0.1)
+
+
+def _run_steps(run, grads_fn, steps, hp=HP, where=""):
+    reps = []
+    for t in range(1, steps + 1):
+        grads = grads_fn(t)
+        reps.append(run.teacher_forced_step(grads, hp["lr"], hp["betas"], hp["eps"], hp["wd"], t,
+                                            where=f"{where} step {t}"))
+    return reps
+
+
+def test_tiny_config_end_to_end():
+    """The tiny MLP configuration: periods, histogram, codebook and 10 steps."""
+    from parity import Run, grad_bits
+    dev = _dev()
+    w = W.get("tiny")
+    fields = W.scale_fields(w)
+    params = W.init_params(w, dev)
+    g1 = W.make_grads(w, fields, 1, dev)
+    run = Run(params, g1)
+    # periods: Alg. 2 on the same gradient bits
+    for i, g in enumerate(g1):
+        _, _, per = oracle.partition(grad_bits(g), 1e-8)
+        assert run.periods[i] == per, (i, run.periods[i], per)
+    # histogram and DP of the init fit
+    nb = 16 * run.k
+    h_ref = np.zeros(nb, dtype=np.uint64)
+    for i, g in enumerate(g1):
+        oracle.histogram_blocks(grad_bits(g), run.offsets[i], nb, h_ref)
+    h_gpu = run.state.histogram(g1).cpu().numpy().view(np.uint64)
+    np.testing.assert_array_equal(h_gpu, h_ref)
+    cb_ref, cost_ref, _, st_ref = oracle.dp_codebook(h_ref, run.k)
+    cb_gpu = run.state.read(gf.STATE_CB_DEC64).cpu().numpy()
+    np.testing.assert_array_equal(cb_gpu, cb_ref)
+    cost, st = run.state.fit_info()
+    assert st == st_ref and cost == cost_ref
+    _run_steps(run, lambda t: W.make_grads(w, fields, t, dev), w.steps,
+               hp=dict(lr=w.lr, betas=w.betas, eps=w.eps, wd=w.wd), where="tiny")
+
+
+# (period, number of blocks): every kernel class, ragged last tiles
+PERIODS = [(1, 3000), (2, 700), (3, 513), (4, 1000), (8, 300), (12, 257), (20, 100),
+           (32, 300), (36, 90), (64, 70), (96, 41), (100, 33), (768, 19), (2048, 9),
+           (3072, 5), (8192, 3), (8196, 2), (12288, 2), (40000, 2)]
+
+
+@pytest.mark.parametrize("p,nb", PERIODS)
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_uniform_periods(p, nb, dtype):
+    from parity import Run
+    dev = _dev()
+    n = p * nb
+    theta = (torch.randn(n, device=dev) * 0.02).contiguous()
+    g1 = _grad(n, 1, dtype, dev=dev)
+    run = Run([theta], [g1], period_override=[p])
+    assert run.periods == [p]
+    _run_steps(run, lambda t: [_grad(n, 100 + t, dtype, dev=dev)], 3, where=f"p={p}")
+
+
+def test_explicit_irregular_blocks():
+    from parity import Run
+    dev = _dev()
+    rng = np.random.default_rng(3)
+    sizes = np.concatenate([[1, 2, 5, 31, 32, 33, 64, 1000, 9000, 70000],
+                            rng.integers(1, 40, size=300), rng.integers(40, 3000, size=60)])
+    rng.shuffle(sizes)
+    sizes = np.concatenate([sizes, [7]])
+    n1 = int(sizes[:200].sum())
+    n = int(sizes.sum())
+    offs = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    # two tensors split on a block boundary
+    params = [(torch.randn(n1, device=dev) * 0.02), (torch.randn(n - n1, device=dev) * 0.02)]
+    gr = lambda t: [_grad(n1, 10 + t, torch.bfloat16, dev=dev),
+                    _grad(n - n1, 50 + t, torch.bfloat16, dev=dev)]
+    run = Run(params, gr(1), block_offsets=offs)
+    _run_steps(run, gr, 3, where="explicit")
+
+
+def test_misaligned_tensors():
+    """Parameter and gradient views at odd element offsets (unaligned vector loads)."""
+    from parity import Run
+    dev = _dev()
+    p, nb = 2048, 5
+    n = p * nb
+    pbuf = torch.randn(n + 3, device=dev) * 0.02
+    theta = pbuf[1:1 + n]
+    assert theta.data_ptr() % 16 != 0
+    gbufs = {t: _grad(n + 1, 30 + t, torch.bfloat16, dev=dev) for t in range(1, 4)}
+    gr = lambda t: [gbufs[t][1:]]
+    run = Run([theta], gr(1), period_override=[p])
+    _run_steps(run, gr, 3, where="misaligned")
+    assert pbuf[0].item() == pbuf[0].item() and torch.isfinite(pbuf).all()
+
+
+def test_zero_gradient_blocks():
+    from parity import Run
+    dev = _dev()
+    p, nb = 768, 12
+    n = p * nb
+    theta = torch.randn(n, device=dev) * 0.02
+
+    def gr(t):
+        g = _grad(n, 60 + t, torch.float32, dev=dev)
+        g.view(nb, p)[::3] = 0.0
+        return [g]
+
+    run = Run([theta], gr(1), period_override=[p])
+    _run_steps(run, gr, 3, where="zero-blocks")
+    s = run.state.read(gf.STATE_SCALE).cpu().numpy()
+    assert (s[::3] == 0).all()
+    codes = run.state.read(gf.STATE_CODES).cpu().numpy()[:n].reshape(nb, p)
+    assert (codes[::3] == 0).all()
+
+
+def test_block_size_one_matches_torch_adamw_free_running():
+    """p = 1: Gefen is AdamW (m/s' = +-1 are codebook entries). Free-running, fp32."""
+    dev = _dev()
+    n = 50_000
+    torch.manual_seed(0)
+    theta0 = torch.randn(n, device=dev) * 0.02
+    p_gef = theta0.clone()
+    p_ref = theta0.clone().requires_grad_(True)
+    lr, b1, b2, eps, wd = 1e-3, 0.9, 0.999, 1e-8, 0.1
+    opt = torch.optim.AdamW([p_ref], lr=lr, betas=(b1, b2), eps=eps, weight_decay=wd,
+                            foreach=False)
+    grads = [_grad(n, 200 + t, torch.float32, dev=dev) *
+             torch.exp(torch.linspace(-6, 0, n, device=dev)) for t in range(1, 51)]
+    st = gf.GefenState([grads[0]], period_override=[1])
+    for t in range(1, 51):
+        st.step([p_gef], [grads[t - 1]], lr, (b1, b2), eps, wd, t)
+        p_ref.grad = grads[t - 1].clone()
+        opt.step()
+    torch.cuda.synchronize()
+    a = p_gef.double()
+    b = p_ref.detach().double()
+    err = (a - b).abs()
+    assert (err <= 1e-5 * b.abs() + 1e-5 * lr).all(), float((err / (b.abs() + lr)).max())
+
+
+def test_step_is_deterministic():
+    dev = _dev()
+    n = 8192 * 7
+    theta0 = torch.randn(n, device=dev) * 0.02
+    g1 = _grad(n, 5, torch.bfloat16, rows=7 * 4, dev=dev)
+    st = gf.GefenState([g1])
+    th = theta0.clone()
+    for t in range(1, 4):
+        st.step([th], [_grad(n, 5 + t, torch.bfloat16, rows=28, dev=dev)], 1e-3, (0.9, 0.999),
+                1e-8, 0.1, t)
+    ck = st.export()
+    th_ck = th.clone()
+    g = _grad(n, 99, torch.bfloat16, rows=28, dev=dev)
+    outs = []
+    for _ in range(2):
+        st.import_(ck)
+        th.copy_(th_ck)
+        st.step([th], [g], 1e-3, (0.9, 0.999), 1e-8, 0.1, 4)
+        outs.append((th.clone(), st.read(gf.STATE_CODES).clone(), st.read(gf.STATE_SCALE).clone(),
+                     st.read(gf.STATE_V).clone()))
+    for x, y in zip(*outs):
+        assert torch.equal(x, y)
+
+
+def test_checkpoint_resume_bitwise():
+    dev = _dev()
+    w = W.get("tiny")
+    fields = W.scale_fields(w)
+    hp = (w.lr, w.betas, w.eps, w.wd)
+    pa = W.init_params(w, dev)
+    g1 = W.make_grads(w, fields, 1, dev)
+    a = gf.GefenState(g1)
+    for t in range(1, 6):
+        a.step(pa, W.make_grads(w, fields, t, dev), hp[0], hp[1], hp[2], hp[3], t)
+    ck = a.export(device=torch.device("cpu"))
+    pb = [p.clone() for p in pa]
+    for t in range(6, 11):
+        a.step(pa, W.make_grads(w, fields, t, dev), hp[0], hp[1], hp[2], hp[3], t)
+    b = gf.GefenState(g1)
+    b.import_(ck.to(dev))
+    for t in range(6, 11):
+        b.step(pb, W.make_grads(w, fields, t, dev), hp[0], hp[1], hp[2], hp[3], t)
+    for x, y in zip(pa, pb):
+        assert torch.equal(x, y)
+    for which in (gf.STATE_CODES, gf.STATE_SCALE, gf.STATE_V):
+        assert torch.equal(a.read(which), b.read(which))
+
+
+def test_refit_encodes_with_new_codebook_then_decodes_with_it():
+    from parity import Run
+    dev = _dev()
+    p, nb = 2048, 6
+    n = p * nb
+    theta = torch.randn(n, device=dev) * 0.02
+    gr = lambda t: [_grad(n, 300 + t, torch.bfloat16, rows=nb, dev=dev) * (3.0 if t > 2 else 1.0)]
+    run = Run([theta], gr(1), period_override=[p])
+    _run_steps(run, gr, 2, where="pre-refit")
+    old = run.state.read(gf.STATE_CB_DEC).clone()
+    # heavy-tailed gradients give a different codebook
+    gt = torch.distributions.StudentT(1.5).sample((n,)).to(dev).to(torch.bfloat16)
+    run.state.fit_codebook([gt])
+    new_enc = run.state.read(gf.STATE_CB_ENC)
+    assert torch.equal(run.state.read(gf.STATE_CB_DEC), old)
+    assert not torch.equal(new_enc, old)
+    rep = run.teacher_forced_step(gr(3), 1e-3, (0.9, 0.999), 1e-8, 0.1, 3, where="refit step")
+    assert torch.equal(run.state.read(gf.STATE_CB_DEC), new_enc)
+    run.teacher_forced_step(gr(4), 1e-3, (0.9, 0.999), 1e-8, 0.1, 4, where="post-refit")
+    # the refit codebook is the oracle's DP on the oracle histogram of the same bits
+    from parity import grad_bits
+    h = oracle.histogram_blocks(grad_bits(gt), run.offsets[0], 16 * run.k)
+    cb_ref, _, _, _ = oracle.dp_codebook(h, run.k)
+    np.testing.assert_array_equal(run.state.read(gf.STATE_CB_DEC64).cpu().numpy(), cb_ref)
+    assert rep["codes"] == n
+
+
+def test_guard_bands_and_code_padding():
+    """Sentinels around the parameters and the padded tail of the code buffer."""
+    dev = _dev()
+    n = 2048 * 3 + 0
+    buf = torch.full((n + 2 * 1024,), 12345.0, device=dev)
+    theta = buf[1024:1024 + n]
+    theta.normal_(0, 0.02)
+    n2 = 777  # odd, generic kernel; code padding of 15 bytes
+    buf2 = torch.full((n2 + 2 * 64,), -7.0, device=dev)
+    theta2 = buf2[64:64 + n2]
+    theta2.normal_(0, 0.02)
+    g = [_grad(n, 1, torch.float32, rows=3, dev=dev), _grad(n2, 2, torch.float32, dev=dev)]
+    st = gf.GefenState(g, period_override=[2048, 777])
+    for t in range(1, 4):
+        st.step([theta, theta2], g, 1e-3, (0.9, 0.999), 1e-8, 0.1, t)
+    torch.cuda.synchronize()
+    assert (buf[:1024] == 12345.0).all() and (buf[1024 + n:] == 12345.0).all()
+    assert (buf2[:64] == -7.0).all() and (buf2[64 + n2:] == -7.0).all()
+    lay = st.layout()
+    codes = st.read(gf.STATE_CODES).cpu().numpy()
+    assert (codes[lay["code_offsets"][0] + n:lay["code_offsets"][1]] == 0).all()
+    assert (codes[lay["code_offsets"][1] + n2:lay["code_offsets"][2]] == 0).all()
+
+
+def test_four_bit_codebook():
+    from parity import Run
+    dev = _dev()
+    p, nb = 768, 10
+    n = p * nb
+    theta = torch.randn(n, device=dev) * 0.02
+    gr = lambda t: [_grad(n, 400 + t, torch.float32, rows=nb, dev=dev)]
+    run = Run([theta], gr(1), period_override=[p], code_bits=4)
+    assert run.k == 16
+    _run_steps(run, gr, 3, where="4-bit")
+
+
+def test_argument_errors_on_device():
+    dev = _dev()
+    g = torch.randn(1024, device=dev)
+    st = gf.GefenState([g], period_override=[64])
+    th = torch.zeros(1024, device=dev)
+    with pytest.raises(gf.GefenError, match="EINVAL"):
+        st.step([th], [g], 1e-3, (0.9, 0.999), 1e-8, 0.0, 0)          # t < 1
+    with pytest.raises(gf.GefenError, match="EINVAL"):
+        st.step([th], [g], 1e-3, (1.0, 0.999), 1e-8, 0.0, 1)          # beta1 = 1
+    with pytest.raises(gf.GefenError, match="EDTYPE"):
+        st.step([th], [g.bfloat16()], 1e-3, (0.9, 0.999), 1e-8, 0.0, 1)
+    with pytest.raises(gf.GefenError, match="EINVAL"):
+        st.step([th[:512]], [g[:512]], 1e-3, (0.9, 0.999), 1e-8, 0.0, 1)
+    with pytest.raises(gf.GefenError, match="EINVAL"):
+        gf.GefenState([g], period_override=[1000])                    # does not divide
