@@ -106,7 +106,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama3_1p5b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-elems", type=int, default=40_000_000)
+    ap.add_argument("--cpu-sample-elems", type=int, default=100_000_000)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run only a plain device-to-device copy of a known byte count "
+                         "(scales rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -120,6 +123,15 @@ def main():
     import paper_2606_13894_amd as gf
 
     dev = torch.device("cuda", 0)
+    if args.copy_calibration:
+        nbytes = 1 << 30
+        src = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_per_launch": nbytes, "launches": 3}), flush=True)
+        return
     w = W.get(args.workload)
     fields = W.scale_fields(w)
     offsets = None

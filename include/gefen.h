@@ -205,8 +205,8 @@ int gefen_import(gefen_state* st, const void* src, int64_t bytes, void* stream);
  * stream around every step-kernel launch (one launch per kernel class: KIND 0 =
  * uniform blocks in registers, 1 = one streamed block per workgroup, 2 = one small
  * block per lane). gefen_profile_end synchronises those events and returns, for each
- * class (host arrays of `cap` entries): kind, vectors per lane (kind 0), gradient
- * dtype, number of timed launches, summed kernel time in milliseconds, elements per
+ * class (host arrays of `cap` entries): kind, vectors per lane (kind 0), workgroup
+ * size, gradient dtype, number of timed launches, summed kernel time in milliseconds, elements per
  * launch and algorithmic HBM bytes per launch (per element: 8 for the parameter
  * read and write, 4 or 2 for the gradient, 2 for the code read and write; per
  * block: 16 for scale and second moment read and write, plus 8 for an explicit block
@@ -214,8 +214,8 @@ int gefen_import(gefen_state* st, const void* src, int64_t bytes, void* stream);
  * ---------------------------------------------------------------------------- */
 int gefen_profile_begin(gefen_state* st, int32_t max_steps);
 int gefen_profile_end(gefen_state* st, int32_t cap, int32_t* n_classes, int32_t* kind,
-                      int32_t* vpl, int32_t* gdtype, int64_t* launches, double* total_ms,
-                      int64_t* elems_per_launch, int64_t* bytes_per_launch);
+                      int32_t* vpl, int32_t* threads, int32_t* gdtype, int64_t* launches,
+                      double* total_ms, int64_t* elems_per_launch, int64_t* bytes_per_launch);
 
 /* Free the state and every device buffer it owns. NULL is a no-op. */
 void gefen_destroy(gefen_state* st);

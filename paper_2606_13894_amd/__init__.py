@@ -80,7 +80,7 @@ def load_library(path: str = LIB_PATH):
     lib.gefen_export.argtypes = [vp, vp, i64, vp]
     lib.gefen_import.argtypes = [vp, vp, i64, vp]
     lib.gefen_profile_begin.argtypes = [vp, i32]
-    lib.gefen_profile_end.argtypes = [vp, i32, P(i32), vp, vp, vp, vp, vp, vp, vp]
+    lib.gefen_profile_end.argtypes = [vp, i32, P(i32), vp, vp, vp, vp, vp, vp, vp, vp]
     lib.gefen_destroy.argtypes = [vp]
     lib.gefen_destroy.restype = None
     lib.gefen_last_error.argtypes = []
@@ -277,16 +277,17 @@ class GefenState:
         and algorithmic bytes per launch (HIP events on the step's stream)."""
         cap = 64
         n = ctypes.c_int32()
-        arrs = [(ctypes.c_int32 * cap)() for _ in range(3)]
+        arrs = [(ctypes.c_int32 * cap)() for _ in range(4)]
         launches = (ctypes.c_int64 * cap)()
         ms = (ctypes.c_double * cap)()
         elems = (ctypes.c_int64 * cap)()
         nbytes = (ctypes.c_int64 * cap)()
         _check(_lib.gefen_profile_end(self._h, cap, ctypes.byref(n), arrs[0], arrs[1], arrs[2],
-                                      launches, ms, elems, nbytes))
-        names = {0: "uniform_registers", 1: "streamed_block", 2: "lane_per_block"}
-        return [{"kind": names[arrs[0][i]], "vpl": arrs[1][i],
-                 "grad_dtype": "f32" if arrs[2][i] == F32 else "bf16",
+                                      arrs[3], launches, ms, elems, nbytes))
+        names = {0: "uniform_registers", 1: "streamed_block", 2: "lane_per_block",
+                 3: "split_block"}
+        return [{"kind": names[arrs[0][i]], "vpl": arrs[1][i], "threads": arrs[2][i],
+                 "grad_dtype": "f32" if arrs[3][i] == F32 else "bf16",
                  "launches": launches[i], "total_ms": ms[i], "elems_per_launch": elems[i],
                  "bytes_per_launch": nbytes[i]} for i in range(n.value)]
 

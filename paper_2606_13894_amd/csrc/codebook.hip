@@ -46,9 +46,33 @@ __device__ __forceinline__ void tile_block(const Seg& sg, const Tile& tl, int bi
     }
 }
 
+// Absolute maximum of |g| over one chunk of a huge block.
+__global__ __launch_bounds__(kThreads) void k_hist_h_absmax(const Tile* __restrict__ tiles,
+                                                            const HTile* __restrict__ htiles,
+                                                            const Seg* __restrict__ segs,
+                                                            float* __restrict__ am_partials)
+{
+    __shared__ float red[kThreads / 64];
+    const Tile tl = tiles[blockIdx.x];
+    const HTile ht = htiles[blockIdx.x];
+    const Seg sg = segs[tl.seg];
+    float a = 0.0f;
+    for (int64_t i = threadIdx.x; i < tl.nelem; i += kThreads)
+        a = fmaxf(a, fabsf(grad_at(sg, tl.elem0 + i)));
+    for (int off = 1; off < 64; off <<= 1) a = fmaxf(a, __shfl_xor(a, off));
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = a;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int w = 1; w < kThreads / 64; ++w) a = fmaxf(a, red[w]);
+        am_partials[ht.first + ht.chunk] = fmaxf(a, red[0]);
+    }
+}
+
 __global__ __launch_bounds__(kThreads) void k_histogram(const Tile* __restrict__ tiles,
                                                         int64_t n_tiles,
                                                         const int32_t* __restrict__ tile_kind,
+                                                        const HTile* __restrict__ htiles,
+                                                        const float* __restrict__ am_partials,
                                                         const Seg* __restrict__ segs,
                                                         int32_t nbins,
                                                         uint64_t* __restrict__ hist)
@@ -77,6 +101,14 @@ __global__ __launch_bounds__(kThreads) void k_histogram(const Tile* __restrict__
                     for (int64_t i = 0; i < len; ++i)
                         atomicAdd(&h[bin_of(grad_at(sg, start + i), a, half_nb, nbins)], 1u);
             }
+        } else if (kind == KIND_H) {
+            // one chunk of a huge block: block absmax from the chunk maxima
+            const HTile ht = htiles[ti];
+            float a = 0.0f;
+            for (int c = 0; c < ht.nchunk; ++c) a = fmaxf(a, am_partials[ht.first + c]);
+            if (a > 0.0f)
+                for (int64_t i = tid; i < tl.nelem; i += kThreads)
+                    atomicAdd(&h[bin_of(grad_at(sg, tl.elem0 + i), a, half_nb, nbins)], 1u);
         } else if (tl.nblk == 1) {
             // the whole workgroup on one block
             int64_t start, len;
@@ -351,13 +383,24 @@ __global__ void k_install(const double* __restrict__ in64, const float* __restri
 
 size_t dp_workspace_bytes(int32_t nbins, int32_t k) { return dp_layout(nbins, k).total; }
 
+hipError_t launch_hist_h_absmax(const Tile* tiles, const HTile* htiles, int64_t n_tiles,
+                                const Seg* segs, float* am_partials, hipStream_t stream)
+{
+    if (n_tiles <= 0) return hipSuccess;
+    if (n_tiles > 0x7fffffffLL) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_hist_h_absmax, dim3(static_cast<unsigned>(n_tiles)), dim3(kThreads), 0,
+                       stream, tiles, htiles, segs, am_partials);
+    return hipGetLastError();
+}
+
 hipError_t launch_histogram(const Tile* tiles, int64_t n_tiles, const int32_t* tile_kind,
-                            const Seg* segs, int32_t nbins, uint64_t* hist, hipStream_t stream)
+                            const HTile* htiles, const float* am_partials, const Seg* segs,
+                            int32_t nbins, uint64_t* hist, hipStream_t stream)
 {
     if (n_tiles <= 0) return hipSuccess;
     const int64_t g = n_tiles < 4096 ? n_tiles : 4096;
     hipLaunchKernelGGL(k_histogram, dim3(static_cast<unsigned>(g)), dim3(kThreads), 0, stream,
-                       tiles, n_tiles, tile_kind, segs, nbins, hist);
+                       tiles, n_tiles, tile_kind, htiles, am_partials, segs, nbins, hist);
     return hipGetLastError();
 }
 

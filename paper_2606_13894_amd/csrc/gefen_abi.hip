@@ -39,12 +39,14 @@ int fail(int code, const char* fmt, ...)
     } while (0)
 
 struct Class {
-    int32_t kind, gdtype, vpl;
+    int32_t kind, gdtype, vpl, bs;
     int64_t first, count;
     int64_t elems, bytes;   // per launch: elements and algorithmic HBM bytes
 };
 
-constexpr int64_t kUMaxPeriod = 4LL * (1 << kMaxLpbLog2) * kMaxVpl;   // 8192
+constexpr int64_t kUMaxPeriod = 8192;          // longest period held in registers (KIND_U)
+constexpr int64_t kHugeBlock = 65536;         // longer blocks are always split (KIND_H)
+constexpr int64_t kMinStreamedBlocks = 4096;  // fewer blocks > kUMaxPeriod: split them too
 constexpr int64_t kPartChunk = 65536;     // elements of one partition sub-chunk (mode 1)
 constexpr int64_t kPartItemElems = 16384; // elements per partition item (mode 0)
 constexpr int kPartMaxPairs = 2048;
@@ -89,7 +91,11 @@ struct gefen_state {
 
     Tile* tiles = nullptr;
     int32_t* tile_kind = nullptr;
-    int64_t n_tiles = 0;
+    HTile* htiles = nullptr;        // parallel to tiles (KIND_H entries only)
+    float2* h_partials = nullptr;   // parallel to tiles: per-chunk (sum g^2, max |m|)
+    float* h_absmax = nullptr;      // parallel to tiles: per-chunk max |g| (histogram)
+    float2* h_old = nullptr;        // per huge block: (s, v) before the step
+    int64_t n_tiles = 0, n_hblocks = 0;
     std::vector<Class> classes;
 
     Seg* segs = nullptr;
@@ -225,36 +231,102 @@ hipError_t fill_zero(void* p, size_t bytes, hipStream_t s)
     return hipGetLastError();
 }
 
-// Lanes-per-block and vectors-per-lane of a KIND_U tensor of period p.
-void choose_u(int64_t p, int& lpb_log2, int& vpl)
+// KIND_U shape for period p (p % 4 == 0, p <= kUMaxPeriod): vectors per lane v and a
+// power-of-two lane group per block leaving at most 1/8 of the lanes idle, in a
+// workgroup of `threads` lanes (threads / lanes blocks per workgroup). Measured on the
+// MI355X for the Llama-3 1.5B shape (p = 2048 and 8192, bf16 gradients): 1024 threads
+// with v = 2 (about 8K elements per workgroup) reach 5.76 TB/s; v = 1 (4K elements)
+// 4.82 TB/s, v = 4 (16K elements) 4.11 TB/s, 512 threads 4.55 TB/s, 256 threads
+// 4.38 TB/s -- the per-workgroup start (descriptor loads, LDS tables, barrier) needs
+// ~8K elements to amortise, while larger tiles lose memory-level parallelism. So v = 2
+// is tried first, then 1, 3, 4; 256-thread workgroups (up to 8 vectors) are the
+// fallback. Tunables for measurement: GEFEN_U_THREADS (256, 512, 1024) and GEFEN_U_VPL
+// (force v).
+struct UShape {
+    int lpb_log2, vpl, bs;
+};
+
+int env_int(const char* name, int dflt)
+{
+    const char* v = std::getenv(name);
+    return v && *v ? std::atoi(v) : dflt;
+}
+
+UShape choose_u(int64_t p)
 {
     const int64_t nv = p / 4;
-    int l2 = 0;
-    while ((int64_t(1) << l2) * kMaxVpl < nv) ++l2;
-    if (nv >= 16 && l2 < 4) l2 = 4;            // >= 256 contiguous bytes per slot
-    if (nv < 16) {                             // tiny blocks: one vector per lane
-        l2 = 0;
-        while ((int64_t(1) << l2) < nv) ++l2;
+    int pref = env_int("GEFEN_U_THREADS", 1024);
+    if (pref != 256 && pref != 512 && pref != 1024) pref = 1024;
+    const int force = env_int("GEFEN_U_VPL", 0);
+    constexpr int kMaxVplBig = 4;   // instances of the 512/1024-thread kernels
+    static const int kOrderBig[kMaxVplBig] = {2, 1, 3, 4};
+    static const int kOrderSmall[kMaxVpl] = {2, 1, 3, 4, 5, 6, 7, 8};
+    for (int pass = 0; pass < 2; ++pass) {
+        const int bs = pass == 0 ? pref : 256;
+        const int vmax = bs > 256 ? kMaxVplBig : kMaxVpl;
+        for (int vi = 0; vi < vmax; ++vi) {
+            const int v = bs > 256 ? kOrderBig[vi] : kOrderSmall[vi];
+            if (force && pass == 0 && v != force) continue;
+            const int64_t need = (nv + v - 1) / v;
+            int l2 = 0;
+            while ((int64_t(1) << l2) < need) ++l2;
+            if ((1 << l2) > bs) continue;
+            const int64_t waste = (int64_t(1) << l2) * v - nv;
+            if (8 * waste <= nv || v == vmax || (pass == 1 && v == kMaxVpl))
+                return UShape{l2, v, bs};
+        }
     }
-    lpb_log2 = l2;
-    vpl = static_cast<int>((nv + (int64_t(1) << l2) - 1) >> l2);
+    // not reached for p <= 8192: 256 lanes x 8 vectors x 4 = 8192
+    return UShape{8, kMaxVpl, 256};
 }
 
 // Tensor-relative block starts of tensor i (explicit blocks), size n_blocks_i + 1.
 int plan_tiles(gefen_state* st, const std::vector<std::vector<int64_t>>& starts)
 {
     struct Key {
-        int32_t kind, gdtype, vpl;
+        int32_t kind, gdtype, vpl, bs;
     };
     std::vector<std::vector<Tile>> lists;
     std::vector<Key> keys;
-    auto list_for = [&](int32_t kind, int32_t gdt, int32_t vpl) -> std::vector<Tile>& {
+    auto list_for = [&](int32_t kind, int32_t gdt, int32_t vpl,
+                        int32_t bs = kThreads) -> std::vector<Tile>& {
         for (size_t i = 0; i < keys.size(); ++i)
-            if (keys[i].kind == kind && keys[i].gdtype == gdt && keys[i].vpl == vpl) return lists[i];
-        keys.push_back({kind, gdt, vpl});
+            if (keys[i].kind == kind && keys[i].gdtype == gdt && keys[i].vpl == vpl &&
+                keys[i].bs == bs)
+                return lists[i];
+        keys.push_back({kind, gdt, vpl, bs});
         lists.emplace_back();
         return lists.back();
     };
+    // huge blocks: chunk tiles, bookkeeping completed once tiles are concatenated
+    std::vector<std::vector<HTile>> hlists;   // parallel to lists
+    auto add_huge = [&](int32_t t, int32_t gdt, int64_t start, int64_t len, int64_t blk) {
+        std::vector<Tile>& L = list_for(KIND_H, gdt, 0);
+        hlists.resize(lists.size());
+        size_t li = 0;
+        while (&lists[li] != &L) ++li;
+        std::vector<HTile>& H = hlists[li];
+        const int64_t nchunk = (len + kHChunk - 1) / kHChunk;
+        const int64_t first_rel = static_cast<int64_t>(L.size());
+        for (int64_t c = 0; c < nchunk; ++c) {
+            Tile tl{};
+            tl.elem0 = start + c * kHChunk;
+            tl.blk0 = blk;
+            tl.nelem = std::min(kHChunk, len - c * kHChunk);
+            tl.seg = t;
+            tl.nblk = 1;
+            L.push_back(tl);
+            HTile ht{};
+            ht.blk_len = len;
+            ht.first = first_rel;   // made absolute below
+            ht.nchunk = static_cast<int32_t>(nchunk);
+            ht.chunk = static_cast<int32_t>(c);
+            ht.hb = static_cast<int32_t>(st->n_hblocks);
+            H.push_back(ht);
+        }
+        ++st->n_hblocks;
+    };
+    st->n_hblocks = 0;
     for (int32_t t = 0; t < st->n_tensors; ++t) {
         const int32_t gdt = st->gdtype[t];
         const int64_t bb = st->blk_begin[t];
@@ -264,7 +336,10 @@ int plan_tiles(gefen_state* st, const std::vector<std::vector<int64_t>>& starts)
             int64_t b = 0;
             while (b < nb) {
                 const int64_t len = s[b + 1] - s[b];
-                if (len <= kSmallBlock) {
+                if (len > kHugeBlock) {
+                    add_huge(t, gdt, s[b], len, bb + b);
+                    ++b;
+                } else if (len <= kSmallBlock) {
                     Tile tl{};
                     tl.elem0 = s[b];
                     tl.blk0 = bb + b;
@@ -293,10 +368,10 @@ int plan_tiles(gefen_state* st, const std::vector<std::vector<int64_t>>& starts)
         const int64_t p = st->period[t];
         const int64_t nb = st->numel[t] / p;
         if (p % 4 == 0 && p <= kUMaxPeriod) {
-            int l2, vpl;
-            choose_u(p, l2, vpl);
-            const int64_t bpw = kThreads >> l2;
-            std::vector<Tile>& L = list_for(KIND_U, gdt, vpl);
+            const UShape u = choose_u(p);
+            const int l2 = u.lpb_log2, vpl = u.vpl, bs = u.bs;
+            const int64_t bpw = bs >> l2;
+            std::vector<Tile>& L = list_for(KIND_U, gdt, vpl, bs);
             for (int64_t b = 0; b < nb; b += bpw) {
                 Tile tl{};
                 const int64_t n = std::min(bpw, nb - b);
@@ -321,6 +396,8 @@ int plan_tiles(gefen_state* st, const std::vector<std::vector<int64_t>>& starts)
                 tl.nblk = static_cast<int16_t>(n);
                 L.push_back(tl);
             }
+        } else if (p > kHugeBlock || (p > kUMaxPeriod && nb < kMinStreamedBlocks)) {
+            for (int64_t b = 0; b < nb; ++b) add_huge(t, gdt, b * p, p, bb + b);
         } else {
             std::vector<Tile>& L = list_for(KIND_G, gdt, 0);
             for (int64_t b = 0; b < nb; ++b) {
@@ -336,10 +413,21 @@ int plan_tiles(gefen_state* st, const std::vector<std::vector<int64_t>>& starts)
     }
     std::vector<Tile> all;
     std::vector<int32_t> kinds;
+    std::vector<HTile> hall;
+    hlists.resize(lists.size());
     st->classes.clear();
     for (size_t i = 0; i < lists.size(); ++i) {
-        Class c{keys[i].kind, keys[i].gdtype, keys[i].vpl, static_cast<int64_t>(all.size()),
-                static_cast<int64_t>(lists[i].size()), 0, 0};
+        const int64_t base = static_cast<int64_t>(all.size());
+        if (keys[i].kind == KIND_H) {
+            for (HTile h : hlists[i]) {
+                h.first += base;
+                hall.push_back(h);
+            }
+        } else {
+            hall.insert(hall.end(), lists[i].size(), HTile{});
+        }
+        Class c{keys[i].kind, keys[i].gdtype, keys[i].vpl, keys[i].bs,
+                static_cast<int64_t>(all.size()), static_cast<int64_t>(lists[i].size()), 0, 0};
         const int64_t per_elem = 8 + (keys[i].gdtype == DT_F32 ? 4 : 2) + 2;
         for (const Tile& tl : lists[i]) {
             c.elems += tl.nelem;
@@ -358,6 +446,14 @@ int plan_tiles(gefen_state* st, const std::vector<std::vector<int64_t>>& starts)
     GEFEN_HIP(hipMemcpy(st->tiles, all.data(), sizeof(Tile) * all.size(), hipMemcpyHostToDevice));
     GEFEN_HIP(hipMemcpy(st->tile_kind, kinds.data(), sizeof(int32_t) * kinds.size(),
                         hipMemcpyHostToDevice));
+    if (st->n_hblocks > 0) {
+        if ((rc = st->alloc(&st->htiles, sizeof(HTile) * hall.size(), false))) return rc;
+        if ((rc = st->alloc(&st->h_partials, sizeof(float2) * all.size(), false))) return rc;
+        if ((rc = st->alloc(&st->h_absmax, sizeof(float) * all.size(), false))) return rc;
+        if ((rc = st->alloc(&st->h_old, sizeof(float2) * st->n_hblocks, false))) return rc;
+        GEFEN_HIP(hipMemcpy(st->htiles, hall.data(), sizeof(HTile) * hall.size(),
+                            hipMemcpyHostToDevice));
+    }
     return GEFEN_OK;
 }
 
@@ -467,12 +563,24 @@ CodebookDev codebook_dev(const gefen_state* st)
     return c;
 }
 
+// Histogram with the state's blocks into `hist` (already zeroed).
+int run_histogram(gefen_state* st, uint64_t* hist, hipStream_t stream)
+{
+    for (const Class& c : st->classes)
+        if (c.kind == KIND_H)
+            GEFEN_HIP(launch_hist_h_absmax(st->tiles + c.first, st->htiles + c.first, c.count,
+                                           st->segs, st->h_absmax, stream));
+    GEFEN_HIP(launch_histogram(st->tiles, st->n_tiles, st->tile_kind, st->htiles, st->h_absmax,
+                               st->segs, st->nbins, hist, stream));
+    return GEFEN_OK;
+}
+
 // Histogram of `grads` with the state's blocks, DP, install into `slot`.
 int fit_into_slot(gefen_state* st, int slot, hipStream_t stream)
 {
     GEFEN_HIP(fill_zero(st->hist, sizeof(uint64_t) * st->nbins, stream));
-    GEFEN_HIP(launch_histogram(st->tiles, st->n_tiles, st->tile_kind, st->segs, st->nbins,
-                               st->hist, stream));
+    int rc = run_histogram(st, st->hist, stream);
+    if (rc) return rc;
     GEFEN_HIP(launch_dp(st->hist, st->nbins, st->k, st->dp_ws, st->fit_cb64, st->fit_cost,
                         st->fit_status, stream));
     GEFEN_HIP(launch_install_codebook(st->fit_cb64, st->k, st->ng, st->cb32[slot],
@@ -701,8 +809,13 @@ int gefen_step(gefen_state* st, const gefen_tensor* params, const gefen_tensor* 
     for (size_t ci = 0; ci < ncls; ++ci) {
         const Class& c = st->classes[ci];
         if (prof) GEFEN_HIP(hipEventRecord(st->prof_events[(st->prof_steps * ncls + ci) * 2], stream));
-        hipError_t e = launch_step(c.kind, c.gdtype, c.vpl, st->tiles + c.first, c.count,
-                                   st->segs, st->codes, st->scale, st->vmom, cb, sc, stream);
+        hipError_t e =
+            c.kind == KIND_H
+                ? launch_step_h(c.gdtype, st->tiles + c.first, st->htiles + c.first, c.count,
+                                st->segs, st->codes, st->scale, st->vmom, cb, sc,
+                                st->h_partials, st->h_old, stream)
+                : launch_step(c.kind, c.gdtype, c.vpl, c.bs, st->tiles + c.first, c.count,
+                              st->segs, st->codes, st->scale, st->vmom, cb, sc, stream);
         if (e != hipSuccess)
             return fail(GEFEN_EHIP, "step launch (kind %d) failed: %s", c.kind, hipGetErrorString(e));
         if (prof) GEFEN_HIP(hipEventRecord(st->prof_events[(st->prof_steps * ncls + ci) * 2 + 1], stream));
@@ -761,9 +874,7 @@ int gefen_histogram(gefen_state* st, const gefen_tensor* grads, int32_t n_tensor
     hipStream_t stream = as_stream(stream_);
     if ((rc = refresh_segs(st, nullptr, grads, stream))) return rc;
     GEFEN_HIP(fill_zero(hist_out, sizeof(uint64_t) * st->nbins, stream));
-    GEFEN_HIP(launch_histogram(st->tiles, st->n_tiles, st->tile_kind, st->segs, st->nbins,
-                               hist_out, stream));
-    return GEFEN_OK;
+    return run_histogram(st, hist_out, stream);
 }
 
 int gefen_dp_codebook(const uint64_t* hist, int32_t nbins, int32_t k, double* codebook_out,
@@ -965,8 +1076,8 @@ int gefen_profile_begin(gefen_state* st, int32_t max_steps)
 }
 
 int gefen_profile_end(gefen_state* st, int32_t cap, int32_t* n_classes, int32_t* kind,
-                      int32_t* vpl, int32_t* gdtype, int64_t* launches, double* total_ms,
-                      int64_t* elems_per_launch, int64_t* bytes_per_launch)
+                      int32_t* vpl, int32_t* threads, int32_t* gdtype, int64_t* launches,
+                      double* total_ms, int64_t* elems_per_launch, int64_t* bytes_per_launch)
 {
     if (!st || !n_classes) return fail(GEFEN_EINVAL, "bad arguments");
     const size_t ncls = st->classes.size();
@@ -987,6 +1098,7 @@ int gefen_profile_end(gefen_state* st, int32_t cap, int32_t* n_classes, int32_t*
         const Class& k = st->classes[c];
         if (kind) kind[c] = k.kind;
         if (vpl) vpl[c] = k.vpl;
+        if (threads) threads[c] = k.bs;
         if (gdtype) gdtype[c] = k.gdtype;
         if (launches) launches[c] = st->prof_steps;
         if (total_ms) total_ms[c] = ms[c];

@@ -15,13 +15,18 @@ enum : int32_t { DT_F32 = 0, DT_BF16 = 1 };
 //  KIND_G  any single block (irregular, unaligned, odd or very large p): the whole
 //          workgroup streams it twice (reduce pass, then update pass).
 //  KIND_L  up to 256 small blocks (<= 32 elements): one lane per block.
-enum : int32_t { KIND_U = 0, KIND_G = 1, KIND_L = 2 };
+//  KIND_H  one chunk of a huge block: a reduce kernel writes per-chunk partials, an
+//          update kernel combines the partials of the block (same fixed order in every
+//          chunk) and updates its chunk, so a huge block spreads over many workgroups.
+enum : int32_t { KIND_U = 0, KIND_G = 1, KIND_L = 2, KIND_H = 3 };
 
-constexpr int kThreads = 256;         // workgroup size of every step kernel
+constexpr int kThreads = 256;         // workgroup size of the streaming kernels
+constexpr int kMaxThreads = 1024;     // largest KIND_U workgroup
 constexpr int kMaxVpl = 8;            // max 4-element vectors per lane (KIND_U)
-constexpr int kMaxLpbLog2 = 8;        // KIND_U lanes per block up to 256
+constexpr int kMaxLpbLog2 = 10;       // KIND_U lanes per block up to 1024
 constexpr int kSmallBlock = 32;       // KIND_L blocks hold at most this many elements
 constexpr int kMaxK = 256;            // max codebook entries
+constexpr int64_t kHChunk = 8192;     // KIND_H chunk length
 
 // One tile = the work of one workgroup (32 bytes).
 struct Tile {
@@ -31,9 +36,21 @@ struct Tile {
     int32_t seg;        // tensor index
     int16_t nblk;       // blocks in the tile
     uint8_t vpl;        // KIND_U: vectors per lane
-    uint8_t lpb_log2;   // KIND_U: log2(lanes per block)
+    uint8_t lpb_log2;   // KIND_U: log2(lanes per block); workgroup size is a class property
 };
 static_assert(sizeof(Tile) == 32, "Tile layout");
+
+// KIND_H bookkeeping, one entry per tile (parallel to the tile array).
+struct HTile {
+    int64_t blk_len;     // elements of the whole block
+    int64_t first;       // absolute tile index of the block's chunk 0 (chunks are
+                         // consecutive tiles; partial arrays are indexed absolutely)
+    int32_t nchunk;      // chunks of the block
+    int32_t chunk;       // this tile's chunk index
+    int32_t hb;          // index of the block among huge blocks (workspace slot)
+    int32_t pad;
+};
+static_assert(sizeof(HTile) == 32, "HTile layout");
 
 // Per-tensor descriptor on device (64 bytes). Pointers are refreshed when the caller
 // passes different parameter or gradient buffers.
@@ -73,13 +90,25 @@ struct CodebookDev {
 };
 
 // Launchers (all enqueue on `stream` and return the launch status).
-hipError_t launch_step(int kind, int gdtype, int vpl, const Tile* tiles, int64_t n_tiles,
-                       const Seg* segs, uint8_t* codes, float* scale, float* vmom,
-                       CodebookDev cb, StepScalars sc, hipStream_t stream);
+// `bs` is the KIND_U workgroup size (256, 512 or 1024); other kinds use kThreads.
+hipError_t launch_step(int kind, int gdtype, int vpl, int bs, const Tile* tiles,
+                       int64_t n_tiles, const Seg* segs, uint8_t* codes, float* scale,
+                       float* vmom, CodebookDev cb, StepScalars sc, hipStream_t stream);
 
+// KIND_H needs `htiles` (parallel to `tiles`), `partials` (float2 per tile) and
+// `ws_old` (float2 per huge block).
+hipError_t launch_step_h(int gdtype, const Tile* tiles, const HTile* htiles, int64_t n_tiles,
+                         const Seg* segs, uint8_t* codes, float* scale, float* vmom,
+                         CodebookDev cb, StepScalars sc, float2* partials, float2* ws_old,
+                         hipStream_t stream);
+
+// Histogram over all tiles. KIND_H tiles need their block absmax first:
+// launch_hist_h_absmax over each KIND_H class range writes am_partials[first + chunk].
+hipError_t launch_hist_h_absmax(const Tile* tiles, const HTile* htiles, int64_t n_tiles,
+                                const Seg* segs, float* am_partials, hipStream_t stream);
 hipError_t launch_histogram(const Tile* tiles, int64_t n_tiles, const int32_t* tile_kind,
-                            const Seg* segs, int32_t nbins, uint64_t* hist,
-                            hipStream_t stream);
+                            const HTile* htiles, const float* am_partials, const Seg* segs,
+                            int32_t nbins, uint64_t* hist, hipStream_t stream);
 
 // DP over a device histogram. ws must hold dp_workspace_bytes(nbins, k) bytes.
 size_t dp_workspace_bytes(int32_t nbins, int32_t k);

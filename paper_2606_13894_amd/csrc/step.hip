@@ -26,10 +26,11 @@ struct LdsTables {
     float cb[kMaxK];                  // decode entries
     float mid[kMaxK];                 // encode midpoints
     uint8_t guide[16 * kMaxK + 16];   // ng + 1 bytes (padded)
-    float red_ss[kThreads / 64];
-    float red_am[kThreads / 64];
+    float red_ss[kMaxThreads / 64];
+    float red_am[kMaxThreads / 64];
 };
 
+template <int BS = kThreads>
 __device__ __forceinline__ void load_tables(LdsTables& L, const CodebookDev& cb)
 {
     const int t = threadIdx.x;
@@ -40,7 +41,7 @@ __device__ __forceinline__ void load_tables(LdsTables& L, const CodebookDev& cb)
     const int words = (cb.ng + 1 + 3) >> 2;   // the global guide is padded to 16 bytes
     const uint32_t* src = reinterpret_cast<const uint32_t*>(cb.enc_guide);
     uint32_t* dst = reinterpret_cast<uint32_t*>(L.guide);
-    for (int i = t; i < words; i += kThreads) dst[i] = src[i];
+    for (int i = t; i < words; i += BS) dst[i] = src[i];
 }
 
 // Nearest codebook entry of x (ties to the lower index) = number of midpoints < x.
@@ -88,11 +89,13 @@ __device__ __forceinline__ BlockOut finish_block(float ss, float am, float v_old
 }
 
 // ---------------------------------------------------------------------------------
-// KIND_U: uniform blocks of p elements (p % 4 == 0, p <= 4 * 256 * 8). A group of
+// KIND_U: uniform blocks of p elements (p % 4 == 0, p <= 8192). A group of
 // LPB = 2^lpb_log2 lanes owns one block; lane li holds vectors v = j * LPB + li,
-// j < VPL, of 4 consecutive elements each. A workgroup holds 256 / LPB blocks.
+// j < VPL, of 4 consecutive elements each. A workgroup of BS threads holds BS / LPB
+// blocks. Small tiles (one block per workgroup, one or two vectors per lane) keep
+// the most independent streams in flight, which is what saturates HBM here.
 // ---------------------------------------------------------------------------------
-template <int GDT, int VPL, bool ALIGNED>
+template <int GDT, int VPL, int BS, bool ALIGNED>
 __device__ __forceinline__ void step_u_body(LdsTables& L, const Tile& tl, const Seg& sg,
                                             uint8_t* __restrict__ codes,
                                             float* __restrict__ scale,
@@ -153,7 +156,7 @@ __device__ __forceinline__ void step_u_body(LdsTables& L, const Tile& tl, const 
         s_old = scale[blk];
         v_old = vmom[blk];
     }
-    load_tables(L, cbd);
+    load_tables<BS>(L, cbd);
     __syncthreads();
 
     // phase 1: dequantize + momentum, block reductions of sum g^2 and max |m|
@@ -228,8 +231,8 @@ __device__ __forceinline__ void step_u_body(LdsTables& L, const Tile& tl, const 
     }
 }
 
-template <int GDT, int VPL>
-__global__ __launch_bounds__(kThreads) void k_step_u(const Tile* __restrict__ tiles,
+template <int GDT, int VPL, int BS>
+__global__ __launch_bounds__(BS) void k_step_u(const Tile* __restrict__ tiles,
                                                      const Seg* __restrict__ segs,
                                                      uint8_t* __restrict__ codes,
                                                      float* __restrict__ scale,
@@ -243,9 +246,9 @@ __global__ __launch_bounds__(kThreads) void k_step_u(const Tile* __restrict__ ti
     const bool aligned = ((reinterpret_cast<uintptr_t>(sg.theta) & 15) == 0) &&
                          ((reinterpret_cast<uintptr_t>(sg.grad) & galign) == 0);
     if (aligned)
-        step_u_body<GDT, VPL, true>(L, tl, sg, codes, scale, vmom, cbd, sc);
+        step_u_body<GDT, VPL, BS, true>(L, tl, sg, codes, scale, vmom, cbd, sc);
     else
-        step_u_body<GDT, VPL, false>(L, tl, sg, codes, scale, vmom, cbd, sc);
+        step_u_body<GDT, VPL, BS, false>(L, tl, sg, codes, scale, vmom, cbd, sc);
 }
 
 // ---------------------------------------------------------------------------------
@@ -391,43 +394,183 @@ __global__ __launch_bounds__(kThreads) void k_step_l(const Tile* __restrict__ ti
     }
 }
 
-template <int GDT>
-hipError_t launch_u(int vpl, dim3 grid, const Tile* tiles, const Seg* segs, uint8_t* codes,
-                    float* scale, float* vmom, CodebookDev cb, StepScalars sc, hipStream_t s)
+// ---------------------------------------------------------------------------------
+// KIND_H: chunks of huge blocks. Reduce: per-chunk (sum g^2, max |m|); chunk 0 also
+// saves the block's old (s, v) so the update kernel can decode while chunk 0 of the
+// update overwrites the state. Update: every chunk combines all partials of its block
+// in chunk order (identical result in every chunk), recomputes m bit-identically and
+// updates its chunk.
+// ---------------------------------------------------------------------------------
+__device__ __forceinline__ void wg_reduce(float& ss, float& am, LdsTables& L)
 {
-    switch (vpl) {
-#define GEFEN_U_CASE(V)                                                                     \
-    case V:                                                                                 \
-        hipLaunchKernelGGL((k_step_u<GDT, V>), grid, dim3(kThreads), 0, s, tiles, segs,     \
-                           codes, scale, vmom, cb, sc);                                     \
-        break;
-        GEFEN_U_CASE(1)
-        GEFEN_U_CASE(2)
-        GEFEN_U_CASE(3)
-        GEFEN_U_CASE(4)
-        GEFEN_U_CASE(5)
-        GEFEN_U_CASE(6)
-        GEFEN_U_CASE(7)
-        GEFEN_U_CASE(8)
-#undef GEFEN_U_CASE
-    default:
-        return hipErrorInvalidValue;
+    for (int off = 1; off < 64; off <<= 1) {
+        ss += __shfl_xor(ss, off);
+        am = fmaxf(am, __shfl_xor(am, off));
     }
-    return hipGetLastError();
+    const int wave = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) {
+        L.red_ss[wave] = ss;
+        L.red_am[wave] = am;
+    }
+    __syncthreads();
+    ss = L.red_ss[0];
+    am = L.red_am[0];
+    for (int w = 1; w < kThreads / 64; ++w) {
+        ss += L.red_ss[w];
+        am = fmaxf(am, L.red_am[w]);
+    }
+    __syncthreads();
+}
+
+template <int GDT>
+__global__ __launch_bounds__(kThreads) void k_step_h_reduce(
+    const Tile* __restrict__ tiles, const HTile* __restrict__ htiles, const Seg* __restrict__ segs,
+    const uint8_t* __restrict__ codes, const float* __restrict__ scale,
+    const float* __restrict__ vmom, CodebookDev cbd, StepScalars sc, float2* __restrict__ partials,
+    float2* __restrict__ ws_old)
+{
+    __shared__ LdsTables L;
+    const Tile tl = tiles[blockIdx.x];
+    const HTile ht = htiles[blockIdx.x];
+    const Seg sg = segs[tl.seg];
+    const int tid = threadIdx.x;
+    const int64_t len = tl.nelem;
+    const int64_t e0 = tl.elem0;
+    const uint8_t* __restrict__ cq = codes + sg.code_off + e0;
+    const void* gp = GDT == DT_F32
+                         ? static_cast<const void*>(static_cast<const float*>(sg.grad) + e0)
+                         : static_cast<const void*>(static_cast<const uint16_t*>(sg.grad) + e0);
+    const float s_old = scale[tl.blk0];
+    load_tables(L, cbd);
+    __syncthreads();
+    float ss = 0.0f, am = 0.0f;
+#pragma unroll 4
+    for (int64_t i = tid; i < len; i += kThreads) {
+        const float g = load_grad(gp, i, GDT);
+        const float mm = momentum(L, cq[i], s_old, g, sc);
+        ss = fmaf(g, g, ss);
+        am = fmaxf(am, fabsf(mm));
+    }
+    wg_reduce(ss, am, L);
+    if (tid == 0) {
+        partials[ht.first + ht.chunk] = make_float2(ss, am);
+        if (ht.chunk == 0) ws_old[ht.hb] = make_float2(s_old, vmom[tl.blk0]);
+    }
+}
+
+template <int GDT>
+__global__ __launch_bounds__(kThreads) void k_step_h_update(
+    const Tile* __restrict__ tiles, const HTile* __restrict__ htiles, const Seg* __restrict__ segs,
+    uint8_t* __restrict__ codes, float* __restrict__ scale, float* __restrict__ vmom,
+    CodebookDev cbd, StepScalars sc, const float2* __restrict__ partials,
+    const float2* __restrict__ ws_old)
+{
+    __shared__ LdsTables L;
+    const Tile tl = tiles[blockIdx.x];
+    const HTile ht = htiles[blockIdx.x];
+    const Seg sg = segs[tl.seg];
+    const int tid = threadIdx.x;
+    const int64_t len = tl.nelem;
+    const int64_t e0 = tl.elem0;
+    float* __restrict__ th = sg.theta + e0;
+    uint8_t* __restrict__ cq = codes + sg.code_off + e0;
+    const void* gp = GDT == DT_F32
+                         ? static_cast<const void*>(static_cast<const float*>(sg.grad) + e0)
+                         : static_cast<const void*>(static_cast<const uint16_t*>(sg.grad) + e0);
+    const float2 old = ws_old[ht.hb];
+    load_tables(L, cbd);
+    // partials of the whole block, fixed order: thread t takes chunks t, t + 256, ...
+    float ss = 0.0f, am = 0.0f;
+    for (int c = tid; c < ht.nchunk; c += kThreads) {
+        const float2 pa = partials[ht.first + c];
+        ss += pa.x;
+        am = fmaxf(am, pa.y);
+    }
+    __syncthreads();
+    wg_reduce(ss, am, L);
+    const BlockOut bo = finish_block(ss, am, old.y, static_cast<float>(ht.blk_len), sc);
+    if (tid == 0 && ht.chunk == 0) {
+        scale[tl.blk0] = bo.s_new;
+        vmom[tl.blk0] = bo.v_new;
+    }
+    const float half_ng = 0.5f * static_cast<float>(cbd.ng);
+    const int ng_m1 = cbd.ng - 1;
+#pragma unroll 4
+    for (int64_t i = tid; i < len; i += kThreads) {
+        const float g = load_grad(gp, i, GDT);
+        const float mm = momentum(L, cq[i], old.x, g, sc);
+        const int q = bo.s_new > 0.0f ? encode(L, mm * bo.inv_s, half_ng, ng_m1) : 0;
+        th[i] = fmaf(-bo.r, mm, th[i] * sc.decay);
+        cq[i] = static_cast<uint8_t>(q);
+    }
+}
+
+template <int GDT>
+hipError_t launch_u(int vpl, int bs, dim3 grid, const Tile* tiles, const Seg* segs,
+                    uint8_t* codes, float* scale, float* vmom, CodebookDev cb, StepScalars sc,
+                    hipStream_t s)
+{
+#define GEFEN_U_CASE(V, B)                                                                  \
+    if (vpl == V && bs == B) {                                                              \
+        hipLaunchKernelGGL((k_step_u<GDT, V, B>), grid, dim3(B), 0, s, tiles, segs, codes,  \
+                           scale, vmom, cb, sc);                                            \
+        return hipGetLastError();                                                           \
+    }
+    GEFEN_U_CASE(1, 256)
+    GEFEN_U_CASE(2, 256)
+    GEFEN_U_CASE(3, 256)
+    GEFEN_U_CASE(4, 256)
+    GEFEN_U_CASE(5, 256)
+    GEFEN_U_CASE(6, 256)
+    GEFEN_U_CASE(7, 256)
+    GEFEN_U_CASE(8, 256)
+    GEFEN_U_CASE(1, 512)
+    GEFEN_U_CASE(2, 512)
+    GEFEN_U_CASE(3, 512)
+    GEFEN_U_CASE(4, 512)
+    GEFEN_U_CASE(1, 1024)
+    GEFEN_U_CASE(2, 1024)
+    GEFEN_U_CASE(3, 1024)
+    GEFEN_U_CASE(4, 1024)
+#undef GEFEN_U_CASE
+    return hipErrorInvalidValue;
 }
 
 }  // namespace
 
-hipError_t launch_step(int kind, int gdtype, int vpl, const Tile* tiles, int64_t n_tiles,
-                       const Seg* segs, uint8_t* codes, float* scale, float* vmom,
-                       CodebookDev cb, StepScalars sc, hipStream_t stream)
+hipError_t launch_step_h(int gdtype, const Tile* tiles, const HTile* htiles, int64_t n_tiles,
+                         const Seg* segs, uint8_t* codes, float* scale, float* vmom,
+                         CodebookDev cb, StepScalars sc, float2* partials, float2* ws_old,
+                         hipStream_t stream)
+{
+    if (n_tiles <= 0) return hipSuccess;
+    if (n_tiles > 0x7fffffffLL) return hipErrorInvalidValue;
+    const dim3 grid(static_cast<unsigned>(n_tiles));
+    if (gdtype == DT_F32) {
+        hipLaunchKernelGGL((k_step_h_reduce<DT_F32>), grid, dim3(kThreads), 0, stream, tiles,
+                           htiles, segs, codes, scale, vmom, cb, sc, partials, ws_old);
+        hipLaunchKernelGGL((k_step_h_update<DT_F32>), grid, dim3(kThreads), 0, stream, tiles,
+                           htiles, segs, codes, scale, vmom, cb, sc, partials, ws_old);
+    } else {
+        hipLaunchKernelGGL((k_step_h_reduce<DT_BF16>), grid, dim3(kThreads), 0, stream, tiles,
+                           htiles, segs, codes, scale, vmom, cb, sc, partials, ws_old);
+        hipLaunchKernelGGL((k_step_h_update<DT_BF16>), grid, dim3(kThreads), 0, stream, tiles,
+                           htiles, segs, codes, scale, vmom, cb, sc, partials, ws_old);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_step(int kind, int gdtype, int vpl, int bs, const Tile* tiles,
+                       int64_t n_tiles, const Seg* segs, uint8_t* codes, float* scale,
+                       float* vmom, CodebookDev cb, StepScalars sc, hipStream_t stream)
 {
     if (n_tiles <= 0) return hipSuccess;
     if (n_tiles > 0x7fffffffLL) return hipErrorInvalidValue;
     const dim3 grid(static_cast<unsigned>(n_tiles));
     if (kind == KIND_U) {
-        return gdtype == DT_F32 ? launch_u<DT_F32>(vpl, grid, tiles, segs, codes, scale, vmom, cb, sc, stream)
-                                : launch_u<DT_BF16>(vpl, grid, tiles, segs, codes, scale, vmom, cb, sc, stream);
+        return gdtype == DT_F32
+                   ? launch_u<DT_F32>(vpl, bs, grid, tiles, segs, codes, scale, vmom, cb, sc, stream)
+                   : launch_u<DT_BF16>(vpl, bs, grid, tiles, segs, codes, scale, vmom, cb, sc, stream);
     }
     if (kind == KIND_G) {
         if (gdtype == DT_F32)

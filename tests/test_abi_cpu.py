@@ -1,0 +1,120 @@
+"""C ABI checks that need no GPU: the library loads, exports every function that
+include/gefen.h declares, and rejects bad arguments before touching the device."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gefen.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gefen_[a-z_0-9]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import paper_2606_13894_amd as gf
+    if not os.path.exists(gf.LIB_PATH):
+        pytest.skip("libgefen.so is not built (run __graft_entry__.build())")
+    return gf.load_library()
+
+
+def test_header_declares_the_abi():
+    names = _declared()
+    for must in ("gefen_init", "gefen_step", "gefen_fit_codebook", "gefen_partition_scores",
+                 "gefen_histogram", "gefen_dp_codebook", "gefen_destroy", "gefen_last_error"):
+        assert must in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in _declared():
+        assert hasattr(lib, name), name
+
+
+def test_binding_lists_every_declared_symbol():
+    import paper_2606_13894_amd as gf
+    assert sorted(gf.SYMBOLS) == _declared()
+
+
+def _tensor(ptr=0x1000, numel=16, dtype=0):
+    import paper_2606_13894_amd as gf
+    t = (gf.gefen_tensor * 1)()
+    t[0].ptr = ptr
+    t[0].numel = numel
+    t[0].dtype = dtype
+    return t
+
+
+def test_init_argument_errors(lib):
+    out = ctypes.c_void_p()
+    assert lib.gefen_init(_tensor(), 1, None, None, 0, 8, 1e-8, None, None) == -1
+    assert b"out" in lib.gefen_last_error()
+    assert lib.gefen_init(_tensor(), 0, None, None, 0, 8, 1e-8, None, ctypes.byref(out)) == -1
+    assert lib.gefen_init(None, 1, None, None, 0, 8, 1e-8, None, ctypes.byref(out)) == -1
+    assert lib.gefen_init(_tensor(ptr=0), 1, None, None, 0, 8, 1e-8, None,
+                          ctypes.byref(out)) == -1
+    assert lib.gefen_init(_tensor(numel=0), 1, None, None, 0, 8, 1e-8, None,
+                          ctypes.byref(out)) == -1
+    assert lib.gefen_init(_tensor(dtype=7), 1, None, None, 0, 8, 1e-8, None,
+                          ctypes.byref(out)) == -2
+    assert b"dtype" in lib.gefen_last_error()
+    assert lib.gefen_init(_tensor(), 1, None, None, 0, 5, 1e-8, None, ctypes.byref(out)) == -1
+    assert b"code_bits" in lib.gefen_last_error()
+    assert lib.gefen_init(_tensor(), 1, None, None, 0, 8, -1.0, None, ctypes.byref(out)) == -1
+    assert out.value is None
+
+
+def test_step_and_queries_reject_null_state(lib):
+    t = _tensor()
+    assert lib.gefen_step(None, t, t, 1, 1e-3, 0.9, 0.999, 1e-8, 0.0, 1, None) == -1
+    assert b"state" in lib.gefen_last_error()
+    assert lib.gefen_fit_codebook(None, t, 1, None) == -1
+    assert lib.gefen_get_periods(None, None) == -1
+    n = ctypes.c_int64()
+    assert lib.gefen_checkpoint_bytes(None, ctypes.byref(n)) == -1
+    lib.gefen_destroy(None)
+
+
+def test_dp_argument_errors(lib):
+    cb = ctypes.c_void_p(0x1000)
+    assert lib.gefen_dp_codebook(cb, 4096, 1, cb, cb, cb, None) == -1      # k < 2
+    assert lib.gefen_dp_codebook(cb, 4096, 512, cb, cb, cb, None) == -1    # k > 256
+    assert lib.gefen_dp_codebook(cb, 0, 16, cb, cb, cb, None) == -1        # no bins
+    assert lib.gefen_dp_codebook(None, 256, 16, cb, cb, cb, None) == -1
+
+
+def test_binding_refuses_missing_library(monkeypatch, tmp_path):
+    import paper_2606_13894_amd as gf
+    monkeypatch.setattr(gf, "_lib", None)
+    with pytest.raises(ImportError):
+        gf.load_library(str(tmp_path / "nope.so"))
+
+
+def test_workload_shapes_and_counts():
+    import workloads as W
+    counts = {"tiny": (4, 262_912), "gpt2_125m": (148, 124_439_808),
+              "gpt2_1b": (292, 1_313_626_112), "llama3_1p5b": (147, 1_498_482_688),
+              "stress_4b": (1, 4_000_000_000)}
+    for name, (nt, n) in counts.items():
+        w = W.get(name)
+        assert (len(w.tensors), w.numel) == (nt, n), name
+    # AdamW keeps 8 bytes per parameter: 11.16 GiB for the Llama-3 1.5B shape
+    assert abs(8 * W.get("llama3_1p5b").numel / 2**30 - 11.16) < 0.01
+
+
+def test_stress_block_recipe():
+    import workloads as W
+    offs = W.stress_block_offsets()
+    sizes = np.diff(offs)
+    assert offs[0] == 0 and offs[-1] == 4_000_000_000 and sizes.size == 1_000_000
+    assert sizes.min() == 64 and sizes.max() <= 65536
+    assert abs(sizes.mean() - 4000) < 1e-9
+    seq = W.stress_block_offsets(n=10_000_000, variant="sequential")
+    s2 = np.diff(seq)
+    assert seq[-1] == 10_000_000 and s2[:-1].min() >= 64 and s2.max() <= 65536

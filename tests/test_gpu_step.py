@@ -78,7 +78,9 @@ def test_tiny_config_end_to_end():
 # (period, number of blocks): every kernel class, ragged last tiles
 PERIODS = [(1, 3000), (2, 700), (3, 513), (4, 1000), (8, 300), (12, 257), (20, 100),
            (32, 300), (36, 90), (64, 70), (96, 41), (100, 33), (768, 19), (2048, 9),
-           (3072, 5), (8192, 3), (8196, 2), (12288, 2), (40000, 2)]
+           (1024, 11), (3072, 5), (4096, 6), (6144, 3), (8192, 3), (999, 40), (5003, 9),
+           (8196, 2), (12288, 2), (40000, 2),
+           (200000, 2)]
 
 
 @pytest.mark.parametrize("p,nb", PERIODS)
