@@ -104,8 +104,11 @@ int gefen_init(const gefen_tensor* grads0, int32_t n_tensors,
  *          kernels use (beta1, 1 - beta1, beta2, 1 - beta2, lr / (1 - beta1^t),
  *          1 / (1 - beta2^t), eps, 1 - lr * weight_decay) are formed in float64 and
  *          rounded once to fp32.
- * Asynchronous: enqueues kernels on `stream` only; no host synchronisation and no
- * allocation. The decode codebook is the current one; after gefen_fit_codebook the
+ * Asynchronous: enqueues kernels on `stream` only; no allocation. The state keeps
+ * device tables of tensor addresses for the last four parameter/gradient buffer sets
+ * it was given; a call with another set first enqueues a small host-to-device copy of
+ * its table (the host waits only if that slot's previous copy is still pending).
+ * The decode codebook is the current one; after gefen_fit_codebook the
  * next step encodes with the new codebook, and later steps decode with it too.
  * NaN or Inf in gradients propagate into parameters and state as in AdamW.
  * Errors: EINVAL, EDTYPE, EHIP (launch failure). Kernel faults surface at the next
@@ -204,7 +207,9 @@ int gefen_import(gefen_state* st, const void* src, int64_t bytes, void* stream);
  * `max_steps` calls of gefen_step: a pair of HIP events is recorded on the step's
  * stream around every step-kernel launch (one launch per kernel class: KIND 0 =
  * uniform blocks in registers, 1 = one streamed block per workgroup, 2 = one small
- * block per lane). gefen_profile_end synchronises those events and returns, for each
+ * block per lane, 3 = blocks over 65536 elements split across workgroups (two
+ * kernels, timed together), 4 = the leftover small tiles of all other classes in one
+ * generic launch). gefen_profile_end synchronises those events and returns, for each
  * class (host arrays of `cap` entries): kind, vectors per lane (kind 0), workgroup
  * size, gradient dtype, number of timed launches, summed kernel time in milliseconds, elements per
  * launch and algorithmic HBM bytes per launch (per element: 8 for the parameter

@@ -56,6 +56,12 @@ def load_library(path: str = LIB_PATH):
     global _lib
     if _lib is not None:
         return _lib
+    # Load PyTorch's HIP runtime first, so that the library binds to the same runtime
+    # instance torch uses (a second copy would see no device from torch's context).
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     if not os.path.exists(path):
         raise ImportError(f"libgefen.so not found at {path}; build it with "
                           "`python -m paper_2606_13894_amd.build`")
@@ -285,7 +291,7 @@ class GefenState:
         _check(_lib.gefen_profile_end(self._h, cap, ctypes.byref(n), arrs[0], arrs[1], arrs[2],
                                       arrs[3], launches, ms, elems, nbytes))
         names = {0: "uniform_registers", 1: "streamed_block", 2: "lane_per_block",
-                 3: "split_block"}
+                 3: "split_block", 4: "small_any"}
         return [{"kind": names[arrs[0][i]], "vpl": arrs[1][i], "threads": arrs[2][i],
                  "grad_dtype": "f32" if arrs[3][i] == F32 else "bf16",
                  "launches": launches[i], "total_ms": ms[i], "elems_per_launch": elems[i],

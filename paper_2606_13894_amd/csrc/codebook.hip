@@ -33,6 +33,82 @@ __device__ __forceinline__ int bin_of(float g, float a, double half_nb, int nbin
     return b < nbins - 1 ? b : nbins - 1;
 }
 
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// Four gradient elements at vector index v (16-byte fp32 or 8-byte bf16 load).
+__device__ __forceinline__ void grad4_at(const Seg& sg, int64_t v, float g[4])
+{
+    if (sg.gdtype == DT_F32) {
+        const f32x4 x = reinterpret_cast<const f32x4*>(sg.grad)[v];
+        g[0] = x.x; g[1] = x.y; g[2] = x.z; g[3] = x.w;
+    } else {
+        const u32x2 x = reinterpret_cast<const u32x2*>(sg.grad)[v];
+        g[0] = __uint_as_float(x.x << 16); g[1] = __uint_as_float(x.x & 0xffff0000u);
+        g[2] = __uint_as_float(x.y << 16); g[3] = __uint_as_float(x.y & 0xffff0000u);
+    }
+}
+
+// Range [start, start + len) split into an aligned vector body [vb, ve) (vector units)
+// and element-wise head/tail, when the gradient pointer is aligned for vector loads.
+struct GSpan {
+    int64_t vb, ve, start, nh, tail0, nt;
+};
+
+__device__ __forceinline__ GSpan grad_span(const Seg& sg, int64_t start, int64_t len)
+{
+    const int64_t end = start + len;
+    const uintptr_t al = sg.gdtype == DT_F32 ? 15 : 7;
+    int64_t b = end, e = end;
+    if ((reinterpret_cast<uintptr_t>(sg.grad) & al) == 0) {
+        b = (start + 3) & ~int64_t(3);
+        e = end & ~int64_t(3);
+        if (b > end) b = end;
+        if (e < b) e = b;
+    }
+    GSpan s;
+    s.vb = b >> 2;
+    s.ve = e >> 2;
+    s.start = start;
+    s.nh = b - start;
+    s.tail0 = e;
+    s.nt = end - e;
+    return s;
+}
+
+// Workgroup-wide absmax over a span (per-thread partial; caller reduces).
+__device__ __forceinline__ float span_absmax(const Seg& sg, const GSpan& sp)
+{
+    float a = 0.0f;
+#pragma unroll 2
+    for (int64_t v = sp.vb + threadIdx.x; v < sp.ve; v += kThreads) {
+        float g[4];
+        grad4_at(sg, v, g);
+        a = fmaxf(a, fmaxf(fmaxf(fabsf(g[0]), fabsf(g[1])), fmaxf(fabsf(g[2]), fabsf(g[3]))));
+    }
+    for (int64_t i = threadIdx.x; i < sp.nh + sp.nt; i += kThreads) {
+        const int64_t e = i < sp.nh ? sp.start + i : sp.tail0 + (i - sp.nh);
+        a = fmaxf(a, fabsf(grad_at(sg, e)));
+    }
+    return a;
+}
+
+__device__ __forceinline__ void span_bins(const Seg& sg, const GSpan& sp, float a, double half_nb,
+                                          int nbins, uint32_t* h)
+{
+#pragma unroll 2
+    for (int64_t v = sp.vb + threadIdx.x; v < sp.ve; v += kThreads) {
+        float g[4];
+        grad4_at(sg, v, g);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) atomicAdd(&h[bin_of(g[c], a, half_nb, nbins)], 1u);
+    }
+    for (int64_t i = threadIdx.x; i < sp.nh + sp.nt; i += kThreads) {
+        const int64_t e = i < sp.nh ? sp.start + i : sp.tail0 + (i - sp.nh);
+        atomicAdd(&h[bin_of(grad_at(sg, e), a, half_nb, nbins)], 1u);
+    }
+}
+
 __device__ __forceinline__ void tile_block(const Seg& sg, const Tile& tl, int bi, int64_t& start,
                                            int64_t& len)
 {
@@ -56,9 +132,7 @@ __global__ __launch_bounds__(kThreads) void k_hist_h_absmax(const Tile* __restri
     const Tile tl = tiles[blockIdx.x];
     const HTile ht = htiles[blockIdx.x];
     const Seg sg = segs[tl.seg];
-    float a = 0.0f;
-    for (int64_t i = threadIdx.x; i < tl.nelem; i += kThreads)
-        a = fmaxf(a, fabsf(grad_at(sg, tl.elem0 + i)));
+    float a = span_absmax(sg, grad_span(sg, tl.elem0, tl.nelem));
     for (int off = 1; off < 64; off <<= 1) a = fmaxf(a, __shfl_xor(a, off));
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = a;
     __syncthreads();
@@ -106,23 +180,19 @@ __global__ __launch_bounds__(kThreads) void k_histogram(const Tile* __restrict__
             const HTile ht = htiles[ti];
             float a = 0.0f;
             for (int c = 0; c < ht.nchunk; ++c) a = fmaxf(a, am_partials[ht.first + c]);
-            if (a > 0.0f)
-                for (int64_t i = tid; i < tl.nelem; i += kThreads)
-                    atomicAdd(&h[bin_of(grad_at(sg, tl.elem0 + i), a, half_nb, nbins)], 1u);
+            if (a > 0.0f) span_bins(sg, grad_span(sg, tl.elem0, tl.nelem), a, half_nb, nbins, h);
         } else if (tl.nblk == 1) {
             // the whole workgroup on one block
             int64_t start, len;
             tile_block(sg, tl, 0, start, len);
-            float a = 0.0f;
-            for (int64_t i = tid; i < len; i += kThreads) a = fmaxf(a, fabsf(grad_at(sg, start + i)));
+            const GSpan sp = grad_span(sg, start, len);
+            float a = span_absmax(sg, sp);
             for (int off = 1; off < 64; off <<= 1) a = fmaxf(a, __shfl_xor(a, off));
             if (lane == 0) red[wave] = a;
             __syncthreads();
             a = red[0];
             for (int w = 1; w < kThreads / 64; ++w) a = fmaxf(a, red[w]);
-            if (a > 0.0f)
-                for (int64_t i = tid; i < len; i += kThreads)
-                    atomicAdd(&h[bin_of(grad_at(sg, start + i), a, half_nb, nbins)], 1u);
+            if (a > 0.0f) span_bins(sg, sp, a, half_nb, nbins, h);
             __syncthreads();   // red[] is reused by the next tile
         } else {
             // one wave per block
@@ -184,13 +254,18 @@ __device__ __forceinline__ T* at(void* ws, size_t off)
 }
 
 // Compaction of non-empty bins and prefix sums, in increasing bin order (one thread,
-// so the summation order is the definition's). Also clears row 0 of D.
-__global__ void k_dp_prep(const uint64_t* __restrict__ hist, int32_t nbins, int32_t k, void* ws)
+// so the summation order is the definition's; the histogram is staged in LDS first so
+// the sequential loop does not wait on global loads). Also clears row 0 of D.
+__global__ __launch_bounds__(kThreads) void k_dp_prep(const uint64_t* __restrict__ hist,
+                                                      int32_t nbins, int32_t k, void* ws)
 {
+    __shared__ uint64_t h[kMaxBins];
     const DpLayout L = dp_layout(nbins, k);
     double* D = at<double>(ws, L.d);
     const size_t row = static_cast<size_t>(nbins) + 1;
     for (size_t r = threadIdx.x; r < row; r += blockDim.x) D[r] = r == 0 ? 0.0 : INFINITY;
+    for (int i = threadIdx.x; i < nbins; i += blockDim.x) h[i] = hist[i];
+    __syncthreads();
     if (threadIdx.x != 0) return;
     double* Z0 = at<double>(ws, L.z0);
     double* Z1 = at<double>(ws, L.z1);
@@ -198,21 +273,25 @@ __global__ void k_dp_prep(const uint64_t* __restrict__ hist, int32_t nbins, int3
     double* cnt = at<double>(ws, L.cnt);
     double* ctr = at<double>(ws, L.ctr);
     const double w = 2.0 / static_cast<double>(nbins);
+    double z0 = 0.0, z1 = 0.0, z2 = 0.0;
     Z0[0] = 0.0;
     Z1[0] = 0.0;
     Z2[0] = 0.0;
     int r = 0;
     for (int i = 0; i < nbins; ++i) {
-        const uint64_t h = hist[i];
-        if (h == 0) continue;
-        const double c = static_cast<double>(h);
+        const uint64_t hv = h[i];
+        if (hv == 0) continue;
+        const double c = static_cast<double>(hv);
         const double m = -1.0 + (static_cast<double>(i) + 0.5) * w;
         ++r;
         ctr[r] = m;
         cnt[r] = c;
-        Z0[r] = Z0[r - 1] + c;
-        Z1[r] = Z1[r - 1] + c * m;
-        Z2[r] = Z2[r - 1] + c * m * m;
+        z0 = z0 + c;
+        z1 = z1 + c * m;
+        z2 = z2 + c * m * m;
+        Z0[r] = z0;
+        Z1[r] = z1;
+        Z2[r] = z2;
     }
     int32_t* hdr = at<int32_t>(ws, L.hdr);
     hdr[0] = r;
@@ -220,39 +299,31 @@ __global__ void k_dp_prep(const uint64_t* __restrict__ hist, int32_t nbins, int3
     hdr[2] = r >= k ? 0 : 1;
 }
 
-__device__ __forceinline__ double interval_cost(const double* Z0, const double* Z1,
-                                                const double* Z2, int l, int r, int j, int keff)
-{
-    const double S0 = Z0[r] - Z0[l - 1];
-    const double S1 = Z1[r] - Z1[l - 1];
-    const double S2 = Z2[r] - Z2[l - 1];
-    if (j == 1 || j == keff) {
-        const double a = j == 1 ? -1.0 : 1.0;
-        return S2 - 2.0 * a * S1 + a * a * S0;
-    }
-    return S2 - S1 * S1 / S0;
-}
-
 // One DP level j: D[j][r] = min_{l in [j, r]} D[j-1][l-1] + C(l, r, j), ties to the
-// smallest l. One wavefront per r; lanes stride over l and keep their first minimum,
-// then a shuffle reduction picks the smallest (value, l).
-__global__ __launch_bounds__(kThreads) void k_dp_level(int32_t nbins, int32_t k, int32_t j,
-                                                       void* ws)
+// smallest l. A workgroup owns kDpRows consecutive right boundaries r, one per wave; it
+// stages the prefix sums and row j-1 of D over the index range it needs in LDS, so the
+// O(b) candidates per r read LDS instead of L2. Lanes stride over l keeping their first
+// minimum; a shuffle reduction then picks the smallest (value, l).
+constexpr int kDpThreads = 1024;
+constexpr int kDpRows = kDpThreads / 64;
+
+__global__ __launch_bounds__(kDpThreads) void k_dp_level(int32_t nbins, int32_t k, int32_t j,
+                                                         void* ws)
 {
+    __shared__ double sh[4 * (kMaxBins + 1)];
     const DpLayout L = dp_layout(nbins, k);
     const int32_t* hdr = at<int32_t>(ws, L.hdr);
     const int b = hdr[0];
     const int keff = hdr[1];
     if (j > keff) return;
-    const int gw = (blockIdx.x * kThreads + threadIdx.x) >> 6;
-    const int lane = threadIdx.x & 63;
-    int r;
+    int r0, r1;
     if (j == keff) {
-        if (gw != 0) return;
-        r = b;
+        if (blockIdx.x != 0) return;
+        r0 = r1 = b;
     } else {
-        r = j + gw;
-        if (r > b) return;
+        r0 = j + static_cast<int>(blockIdx.x) * kDpRows;
+        if (r0 > b) return;
+        r1 = r0 + kDpRows - 1 < b ? r0 + kDpRows - 1 : b;
     }
     const double* Z0 = at<double>(ws, L.z0);
     const double* Z1 = at<double>(ws, L.z1);
@@ -261,13 +332,40 @@ __global__ __launch_bounds__(kThreads) void k_dp_level(int32_t nbins, int32_t k,
     double* D = at<double>(ws, L.d);
     uint16_t* split = at<uint16_t>(ws, L.split);
     const double* Dprev = D + static_cast<size_t>(j - 1) * row;
-
+    // indices base .. r1 of Z0, Z1, Z2 and base .. r1 - 1 of D[j-1]
+    const int base = j - 1;
+    const int span = r1 - base + 1;
+    double* sZ0 = sh;
+    double* sZ1 = sh + span;
+    double* sZ2 = sh + 2 * span;
+    double* sD = sh + 3 * span;
+    for (int i = threadIdx.x; i < span; i += kDpThreads) {
+        sZ0[i] = Z0[base + i];
+        sZ1[i] = Z1[base + i];
+        sZ2[i] = Z2[base + i];
+        sD[i] = base + i <= r1 - 1 ? Dprev[base + i] : 0.0;
+    }
+    __syncthreads();
+    const int r = r0 + static_cast<int>(threadIdx.x >> 6);
+    if (r > r1) return;
+    const int lane = threadIdx.x & 63;
+    const double zr0 = sZ0[r - base], zr1 = sZ1[r - base], zr2 = sZ2[r - base];
     double best = INFINITY;
     int arg = 0x7fffffff;
-    const int lo = j;
     const int hi = j == 1 ? 1 : r;   // level 1 can only start at bin 1 (D[0][l-1] = inf otherwise)
-    for (int l = lo + lane; l <= hi; l += 64) {
-        const double cand = Dprev[l - 1] + interval_cost(Z0, Z1, Z2, l, r, j, keff);
+    for (int l = j + lane; l <= hi; l += 64) {
+        const int o = l - 1 - base;
+        const double S0 = zr0 - sZ0[o];
+        const double S1 = zr1 - sZ1[o];
+        const double S2 = zr2 - sZ2[o];
+        double c;
+        if (j == 1 || j == keff) {
+            const double a = j == 1 ? -1.0 : 1.0;
+            c = S2 - 2.0 * a * S1 + a * a * S0;
+        } else {
+            c = S2 - S1 * S1 / S0;
+        }
+        const double cand = sD[o] + c;
         if (cand < best) {
             best = cand;
             arg = l;
@@ -409,10 +507,9 @@ hipError_t launch_dp(const uint64_t* hist, int32_t nbins, int32_t k, void* ws,
                      hipStream_t stream)
 {
     hipLaunchKernelGGL(k_dp_prep, dim3(1), dim3(kThreads), 0, stream, hist, nbins, k, ws);
-    const unsigned waves_per_wg = kThreads / 64;
-    const unsigned grid = (static_cast<unsigned>(nbins) + waves_per_wg - 1) / waves_per_wg;
+    const unsigned grid = (static_cast<unsigned>(nbins) + kDpRows - 1) / kDpRows;
     for (int j = 1; j <= k; ++j)
-        hipLaunchKernelGGL(k_dp_level, dim3(grid), dim3(kThreads), 0, stream, nbins, k, j, ws);
+        hipLaunchKernelGGL(k_dp_level, dim3(grid), dim3(kDpThreads), 0, stream, nbins, k, j, ws);
     hipLaunchKernelGGL(k_dp_backtrack, dim3(1), dim3(64), 0, stream, nbins, k, ws,
                        codebook_out, cost_out, status_out);
     return hipGetLastError();

@@ -46,6 +46,7 @@ struct Class {
 
 constexpr int64_t kUMaxPeriod = 8192;          // longest period held in registers (KIND_U)
 constexpr int64_t kHugeBlock = 65536;         // longer blocks are always split (KIND_H)
+constexpr int kSegSlots = 4;                 // device tensor tables cached per state
 constexpr int64_t kMinStreamedBlocks = 4096;  // fewer blocks > kUMaxPeriod: split them too
 constexpr int64_t kPartChunk = 65536;     // elements of one partition sub-chunk (mode 1)
 constexpr int64_t kPartItemElems = 16384; // elements per partition item (mode 0)
@@ -98,11 +99,19 @@ struct gefen_state {
     int64_t n_tiles = 0, n_hblocks = 0;
     std::vector<Class> classes;
 
+    // Device tensor tables: kSegSlots of them, each keyed by the buffers it points to, so
+    // that a caller cycling through a few parameter/gradient buffer sets uploads nothing
+    // in steady state.  `segs` points at the table the next launches read.
     Seg* segs = nullptr;
-    std::vector<Seg> segs_host;
-    Seg* segs_pinned = nullptr;
-    hipEvent_t seg_evt = nullptr;
-    bool seg_evt_pending = false;
+    Seg* seg_slots = nullptr;
+    std::vector<Seg> segs_host;     // the table wanted by the current call
+    Seg* segs_pinned = nullptr;     // upload staging, one table per slot
+    hipEvent_t seg_evt[kSegSlots] = {};
+    bool seg_evt_pending[kSegSlots] = {};
+    std::vector<const void*> slot_key[kSegSlots];   // (theta, grad) per tensor; empty = free
+    uint64_t slot_used[kSegSlots] = {};
+    uint64_t seg_clock = 0;
+    int cur_slot = -1;
     int64_t* csr = nullptr;
 
     uint64_t* hist = nullptr;
@@ -132,7 +141,8 @@ struct gefen_state {
         prof_free();
         for (void* p : dev_allocs) (void)hipFree(p);
         if (segs_pinned) (void)hipHostFree(segs_pinned);
-        if (seg_evt) (void)hipEventDestroy(seg_evt);
+        for (hipEvent_t e : seg_evt)
+            if (e) (void)hipEventDestroy(e);
     }
 
     template <typename T>
@@ -186,29 +196,54 @@ int check_against_state(const gefen_state* st, const gefen_tensor* ts, int32_t n
     return GEFEN_OK;
 }
 
-// Refresh the device tensor table when the caller passes different buffers.
+bool slot_matches(const gefen_state* st, int k)
+{
+    const std::vector<const void*>& key = st->slot_key[k];
+    if (key.size() != 2 * static_cast<size_t>(st->n_tensors)) return false;
+    for (int32_t i = 0; i < st->n_tensors; ++i)
+        if (key[2 * i] != st->segs_host[i].theta || key[2 * i + 1] != st->segs_host[i].grad)
+            return false;
+    return true;
+}
+
+// Point `segs` at a device table holding the caller's buffers: reuse a slot whose table
+// already matches, else upload into the least recently used slot.  Overwriting a slot is
+// ordered after earlier launches that read it by the stream; calls on one state are
+// stream-ordered by the caller.
 int refresh_segs(gefen_state* st, const gefen_tensor* params, const gefen_tensor* grads,
                  hipStream_t stream)
 {
-    bool changed = false;
     for (int32_t i = 0; i < st->n_tensors; ++i) {
         Seg& s = st->segs_host[i];
-        if (params && s.theta != static_cast<float*>(params[i].ptr)) {
-            s.theta = static_cast<float*>(params[i].ptr);
-            changed = true;
-        }
-        if (grads && s.grad != grads[i].ptr) {
-            s.grad = grads[i].ptr;
-            changed = true;
+        if (params) s.theta = static_cast<float*>(params[i].ptr);
+        if (grads) s.grad = grads[i].ptr;
+    }
+    const size_t n = static_cast<size_t>(st->n_tensors);
+    int hit = -1;
+    if (st->cur_slot >= 0 && slot_matches(st, st->cur_slot)) hit = st->cur_slot;
+    for (int k = 0; hit < 0 && k < kSegSlots; ++k)
+        if (slot_matches(st, k)) hit = k;
+    if (hit < 0) {
+        hit = 0;
+        for (int k = 1; k < kSegSlots; ++k)
+            if (st->slot_used[k] < st->slot_used[hit]) hit = k;
+        Seg* staging = st->segs_pinned + hit * n;
+        if (st->seg_evt_pending[hit]) GEFEN_HIP(hipEventSynchronize(st->seg_evt[hit]));
+        std::memcpy(staging, st->segs_host.data(), sizeof(Seg) * n);
+        GEFEN_HIP(hipMemcpyAsync(st->seg_slots + hit * n, staging, sizeof(Seg) * n,
+                                 hipMemcpyHostToDevice, stream));
+        GEFEN_HIP(hipEventRecord(st->seg_evt[hit], stream));
+        st->seg_evt_pending[hit] = true;
+        std::vector<const void*>& key = st->slot_key[hit];
+        key.resize(2 * n);
+        for (size_t i = 0; i < n; ++i) {
+            key[2 * i] = st->segs_host[i].theta;
+            key[2 * i + 1] = st->segs_host[i].grad;
         }
     }
-    if (!changed) return GEFEN_OK;
-    if (st->seg_evt_pending) GEFEN_HIP(hipEventSynchronize(st->seg_evt));
-    std::memcpy(st->segs_pinned, st->segs_host.data(), sizeof(Seg) * st->n_tensors);
-    GEFEN_HIP(hipMemcpyAsync(st->segs, st->segs_pinned, sizeof(Seg) * st->n_tensors,
-                             hipMemcpyHostToDevice, stream));
-    GEFEN_HIP(hipEventRecord(st->seg_evt, stream));
-    st->seg_evt_pending = true;
+    st->slot_used[hit] = ++st->seg_clock;
+    st->cur_slot = hit;
+    st->segs = st->seg_slots + hit * n;
     return GEFEN_OK;
 }
 
@@ -327,6 +362,46 @@ int plan_tiles(gefen_state* st, const std::vector<std::vector<int64_t>>& starts)
         ++st->n_hblocks;
     };
     st->n_hblocks = 0;
+    // Register-resident shapes: each eligible tensor's own best shape, then every tensor
+    // that fits the dominant shape's kernel (its vectors per lane and workgroup size; the
+    // kernel masks vectors past a block's end and reads lanes-per-block from the tile)
+    // is re-planned onto it, so one launch covers them on the fast path.
+    std::vector<UShape> ushape(st->n_tensors, UShape{-1, 0, 0});
+    {
+        std::vector<std::pair<std::pair<int, int>, int64_t>> tally;
+        for (int32_t t = 0; t < st->n_tensors; ++t) {
+            const int64_t p = st->period[t];
+            if (st->explicit_blocks || p % 4 != 0 || p > kUMaxPeriod) continue;
+            ushape[t] = choose_u(p);
+            const std::pair<int, int> key{ushape[t].vpl, ushape[t].bs};
+            bool found = false;
+            for (auto& e : tally)
+                if (e.first == key) {
+                    e.second += st->numel[t];
+                    found = true;
+                }
+            if (!found) tally.push_back({key, st->numel[t]});
+        }
+        int dom_vpl = 0, dom_bs = 0;
+        int64_t best = -1;
+        for (auto& e : tally)
+            if (e.second > best) {
+                best = e.second;
+                dom_vpl = e.first.first;
+                dom_bs = e.first.second;
+            }
+        if (best >= 0 && env_int("GEFEN_FOLD", 1)) {
+            for (int32_t t = 0; t < st->n_tensors; ++t) {
+                if (ushape[t].lpb_log2 < 0) continue;
+                if (ushape[t].vpl == dom_vpl && ushape[t].bs == dom_bs) continue;
+                const int64_t nv = st->period[t] / 4;
+                const int64_t need = (nv + dom_vpl - 1) / dom_vpl;
+                int l2 = 0;
+                while ((int64_t(1) << l2) < need) ++l2;
+                if ((1 << l2) <= dom_bs) ushape[t] = UShape{l2, dom_vpl, dom_bs};
+            }
+        }
+    }
     for (int32_t t = 0; t < st->n_tensors; ++t) {
         const int32_t gdt = st->gdtype[t];
         const int64_t bb = st->blk_begin[t];
@@ -367,8 +442,8 @@ int plan_tiles(gefen_state* st, const std::vector<std::vector<int64_t>>& starts)
         }
         const int64_t p = st->period[t];
         const int64_t nb = st->numel[t] / p;
-        if (p % 4 == 0 && p <= kUMaxPeriod) {
-            const UShape u = choose_u(p);
+        if (ushape[t].lpb_log2 >= 0) {
+            const UShape u = ushape[t];
             const int l2 = u.lpb_log2, vpl = u.vpl, bs = u.bs;
             const int64_t bpw = bs >> l2;
             std::vector<Tile>& L = list_for(KIND_U, gdt, vpl, bs);
@@ -411,12 +486,71 @@ int plan_tiles(gefen_state* st, const std::vector<std::vector<int64_t>>& starts)
             }
         }
     }
+    hlists.resize(lists.size());
+    // Fold every class other than the largest register-resident one (and the split
+    // huge-block classes, which need two kernels) into that one's launch: its kernel
+    // runs those tiles on a generic path (tile.vpl = 0). Tile kinds are kept for the
+    // histogram kernel.
+    std::vector<std::vector<int32_t>> tile_kinds(lists.size());
+    for (size_t i = 0; i < lists.size(); ++i) tile_kinds[i].assign(lists[i].size(), keys[i].kind);
+    {
+        int dom = -1;
+        int64_t dom_elems = -1;
+        for (size_t i = 0; i < lists.size(); ++i) {
+            if (keys[i].kind != KIND_U) continue;
+            int64_t e = 0;
+            for (const Tile& tl : lists[i]) e += tl.nelem;
+            if (e > dom_elems) {
+                dom_elems = e;
+                dom = static_cast<int>(i);
+            }
+        }
+        if (dom >= 0 && env_int("GEFEN_FOLD", 1)) {
+            // only small classes: a folded tile runs the slower generic path
+            const int64_t fold_max = std::max<int64_t>(int64_t(1) << 21, dom_elems / 64);
+            std::vector<Tile> front;
+            std::vector<int32_t> front_kinds;
+            int32_t any_dtype = -1;
+            for (size_t i = 0; i < lists.size(); ++i) {
+                if (static_cast<int>(i) == dom || keys[i].kind == KIND_H || lists[i].empty())
+                    continue;
+                int64_t e = 0;
+                for (const Tile& tl : lists[i]) e += tl.nelem;
+                if (e > fold_max) continue;
+                for (Tile tl : lists[i]) {
+                    tl.vpl = 0;
+                    tl.lpb_log2 = 0;
+                    front.push_back(tl);
+                }
+                front_kinds.insert(front_kinds.end(), tile_kinds[i].begin(), tile_kinds[i].end());
+                any_dtype = keys[i].gdtype;
+                lists[i].clear();
+                tile_kinds[i].clear();
+            }
+            if (!front.empty()) {
+                std::vector<Tile>& A = list_for(KIND_ANY, any_dtype, 0);
+                A.insert(A.end(), front.begin(), front.end());
+                hlists.resize(lists.size());
+                tile_kinds.resize(lists.size());
+                tile_kinds.back().insert(tile_kinds.back().end(), front_kinds.begin(),
+                                         front_kinds.end());
+            }
+        }
+    }
     std::vector<Tile> all;
     std::vector<int32_t> kinds;
     std::vector<HTile> hall;
-    hlists.resize(lists.size());
     st->classes.clear();
-    for (size_t i = 0; i < lists.size(); ++i) {
+    // The small generic class launches first: it is short and leaves the machine to the
+    // long launches after it (measured faster than running it beside them on a second
+    // stream, whose fork and join cost more than it saves).
+    std::vector<size_t> order;
+    for (size_t i = 0; i < lists.size(); ++i)
+        if (keys[i].kind == KIND_ANY) order.push_back(i);
+    for (size_t i = 0; i < lists.size(); ++i)
+        if (keys[i].kind != KIND_ANY) order.push_back(i);
+    for (size_t i : order) {
+        if (lists[i].empty()) continue;
         const int64_t base = static_cast<int64_t>(all.size());
         if (keys[i].kind == KIND_H) {
             for (HTile h : hlists[i]) {
@@ -428,15 +562,16 @@ int plan_tiles(gefen_state* st, const std::vector<std::vector<int64_t>>& starts)
         }
         Class c{keys[i].kind, keys[i].gdtype, keys[i].vpl, keys[i].bs,
                 static_cast<int64_t>(all.size()), static_cast<int64_t>(lists[i].size()), 0, 0};
-        const int64_t per_elem = 8 + (keys[i].gdtype == DT_F32 ? 4 : 2) + 2;
-        for (const Tile& tl : lists[i]) {
+        for (size_t j = 0; j < lists[i].size(); ++j) {
+            const Tile& tl = lists[i][j];
+            const int64_t per_elem = 8 + (st->gdtype[tl.seg] == DT_F32 ? 4 : 2) + 2;
             c.elems += tl.nelem;
             c.bytes += tl.nelem * per_elem + 16 * int64_t(tl.nblk);
-            if (keys[i].kind == KIND_L && st->explicit_blocks) c.bytes += 8 * int64_t(tl.nblk);
+            if (tile_kinds[i][j] == KIND_L && st->explicit_blocks) c.bytes += 8 * int64_t(tl.nblk);
         }
         st->classes.push_back(c);
         all.insert(all.end(), lists[i].begin(), lists[i].end());
-        kinds.insert(kinds.end(), lists[i].size(), keys[i].kind);
+        kinds.insert(kinds.end(), tile_kinds[i].begin(), tile_kinds[i].end());
     }
     st->n_tiles = static_cast<int64_t>(all.size());
     int rc = st->alloc(&st->tiles, sizeof(Tile) * all.size(), false);
@@ -721,16 +856,16 @@ int gefen_init(const gefen_tensor* grads0, int32_t n_tensors, const int64_t* per
         if ((rc = st->alloc(&st->mid[s], 4 * st->k, true))) return rc;
         if ((rc = st->alloc(&st->guide[s], guide_bytes, true))) return rc;
     }
-    if ((rc = st->alloc(&st->segs, sizeof(Seg) * n_tensors, false))) return rc;
+    if ((rc = st->alloc(&st->seg_slots, sizeof(Seg) * n_tensors * kSegSlots, false))) return rc;
     if ((rc = st->alloc(&st->hist, sizeof(uint64_t) * st->nbins, false))) return rc;
     if ((rc = st->alloc(&st->dp_ws, dp_workspace_bytes(st->nbins, st->k), false))) return rc;
     if ((rc = st->alloc(&st->fit_cb64, 8 * st->k, false))) return rc;
     if ((rc = st->alloc(&st->fit_cost, 8, false))) return rc;
     if ((rc = st->alloc(&st->fit_status, 8, false))) return rc;
     void* pinned = nullptr;
-    GEFEN_HIP(hipHostMalloc(&pinned, sizeof(Seg) * n_tensors, hipHostMallocDefault));
+    GEFEN_HIP(hipHostMalloc(&pinned, sizeof(Seg) * n_tensors * kSegSlots, hipHostMallocDefault));
     st->segs_pinned = static_cast<Seg*>(pinned);
-    GEFEN_HIP(hipEventCreateWithFlags(&st->seg_evt, hipEventDisableTiming));
+    for (hipEvent_t& e : st->seg_evt) GEFEN_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
 
     if (st->explicit_blocks) {
         int64_t entries = 0;
@@ -756,11 +891,7 @@ int gefen_init(const gefen_tensor* grads0, int32_t n_tensors, const int64_t* per
         s.gdtype = st->gdtype[t];
         if (st->explicit_blocks) csr_base += static_cast<int64_t>(starts[t].size());
     }
-    std::memcpy(st->segs_pinned, st->segs_host.data(), sizeof(Seg) * n_tensors);
-    GEFEN_HIP(hipMemcpyAsync(st->segs, st->segs_pinned, sizeof(Seg) * n_tensors,
-                             hipMemcpyHostToDevice, stream));
-    GEFEN_HIP(hipEventRecord(st->seg_evt, stream));
-    st->seg_evt_pending = true;
+    if ((rc = refresh_segs(st.get(), nullptr, nullptr, stream))) return rc;
 
     if ((rc = plan_tiles(st.get(), starts))) return rc;
 

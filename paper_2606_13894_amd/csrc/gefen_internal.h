@@ -18,7 +18,8 @@ enum : int32_t { DT_F32 = 0, DT_BF16 = 1 };
 //  KIND_H  one chunk of a huge block: a reduce kernel writes per-chunk partials, an
 //          update kernel combines the partials of the block (same fixed order in every
 //          chunk) and updates its chunk, so a huge block spreads over many workgroups.
-enum : int32_t { KIND_U = 0, KIND_G = 1, KIND_L = 2, KIND_H = 3 };
+//  KIND_ANY small leftover tiles of any of the shapes above, one generic launch.
+enum : int32_t { KIND_U = 0, KIND_G = 1, KIND_L = 2, KIND_H = 3, KIND_ANY = 4 };
 
 constexpr int kThreads = 256;         // workgroup size of the streaming kernels
 constexpr int kMaxThreads = 1024;     // largest KIND_U workgroup

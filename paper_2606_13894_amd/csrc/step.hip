@@ -22,6 +22,21 @@ namespace {
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
+// Pointers read from the tensor table are generic to the compiler, which then emits
+// flat accesses (counted against both the memory and the LDS wait counters); these
+// casts state that they point to global memory.
+#define GEFEN_GLOBAL __attribute__((address_space(1)))
+template <typename T>
+__device__ __forceinline__ const GEFEN_GLOBAL T* gl(const void* p)
+{
+    return (const GEFEN_GLOBAL T*)p;
+}
+template <typename T>
+__device__ __forceinline__ GEFEN_GLOBAL T* glw(void* p)
+{
+    return (GEFEN_GLOBAL T*)p;
+}
+
 struct LdsTables {
     float cb[kMaxK];                  // decode entries
     float mid[kMaxK];                 // encode midpoints
@@ -128,16 +143,15 @@ __device__ __forceinline__ void step_u_body(LdsTables& L, const Tile& tl, const 
         if (active && v < nv) {
             const int64_t o = 4 * static_cast<int64_t>(v);
             if (ALIGNED) {
-                const f32x4 t4 = __builtin_nontemporal_load(
-                    reinterpret_cast<const f32x4*>(th_base + o));
+                const f32x4 t4 = __builtin_nontemporal_load(gl<f32x4>(th_base + o));
                 th[j][0] = t4.x; th[j][1] = t4.y; th[j][2] = t4.z; th[j][3] = t4.w;
                 if (GDT == DT_F32) {
-                    const f32x4 g4 = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(
-                        static_cast<const float*>(sg.grad) + e0 + o));
+                    const f32x4 g4 = __builtin_nontemporal_load(
+                        gl<f32x4>(static_cast<const float*>(sg.grad) + e0 + o));
                     gv[j][0] = g4.x; gv[j][1] = g4.y; gv[j][2] = g4.z; gv[j][3] = g4.w;
                 } else {
-                    const u32x2 g2 = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(
-                        static_cast<const uint16_t*>(sg.grad) + e0 + o));
+                    const u32x2 g2 = __builtin_nontemporal_load(
+                        gl<u32x2>(static_cast<const uint16_t*>(sg.grad) + e0 + o));
                     gv[j][0] = bf16_lo(g2.x); gv[j][1] = bf16_hi(g2.x);
                     gv[j][2] = bf16_lo(g2.y); gv[j][3] = bf16_hi(g2.y);
                 }
@@ -221,7 +235,7 @@ __device__ __forceinline__ void step_u_body(LdsTables& L, const Tile& tl, const 
             const int64_t o = 4 * static_cast<int64_t>(v);
             if (ALIGNED) {
                 const f32x4 o4 = {out[0], out[1], out[2], out[3]};
-                __builtin_nontemporal_store(o4, reinterpret_cast<f32x4*>(th_base + o));
+                __builtin_nontemporal_store(o4, glw<f32x4>(th_base + o));
             } else {
 #pragma unroll
                 for (int c = 0; c < 4; ++c) th_base[o + c] = out[c];
@@ -229,6 +243,164 @@ __device__ __forceinline__ void step_u_body(LdsTables& L, const Tile& tl, const 
             __builtin_nontemporal_store(packed, reinterpret_cast<uint32_t*>(cq_base + o));
         }
     }
+}
+
+// ---------------------------------------------------------------------------------
+// Block range of block `bi` of a tile (tensor-relative start, length).
+// ---------------------------------------------------------------------------------
+__device__ __forceinline__ void block_range(const Seg& sg, const Tile& tl, int bi,
+                                            int64_t& start, int64_t& len)
+{
+    if (sg.period > 0) {
+        start = tl.elem0 + static_cast<int64_t>(bi) * sg.period;
+        len = sg.period;
+    } else {
+        const int64_t local = tl.blk0 + bi - sg.blk_begin;
+        start = sg.csr[local];
+        len = sg.csr[local + 1] - start;
+    }
+}
+
+// ---------------------------------------------------------------------------------
+// KIND_ANY: the leftover small tiles of every shape in one launch (generic path, kept
+// out of the KIND_U kernel, whose fast path measurably slows down when this code is
+// compiled into it): two streaming passes per block, by the whole workgroup for a
+// single block, one lane per block for blocks of at most 32 elements, else one wave
+// per block.
+// ---------------------------------------------------------------------------------
+template <int BS>
+__device__ void foreign_tile(LdsTables& L, const Tile& tl, const Seg& sg,
+                             uint8_t* __restrict__ codes, float* __restrict__ scale,
+                             float* __restrict__ vmom, const CodebookDev& cbd,
+                             const StepScalars& sc)
+{
+    load_tables<BS>(L, cbd);
+    __syncthreads();
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int gdt = sg.gdtype;
+    const float half_ng = 0.5f * static_cast<float>(cbd.ng);
+    const int ng_m1 = cbd.ng - 1;
+    if (tl.nblk == 1) {
+        int64_t start, len;
+        block_range(sg, tl, 0, start, len);
+        const int64_t blk = tl.blk0;
+        const float s_old = scale[blk];
+        const float v_old = vmom[blk];
+        float* __restrict__ th = sg.theta + start;
+        uint8_t* __restrict__ cq = codes + sg.code_off + start;
+        float ss = 0.0f, am = 0.0f;
+        for (int64_t i = tid; i < len; i += BS) {
+            const float g = load_grad(sg.grad, start + i, gdt);
+            const float mm = momentum(L, cq[i], s_old, g, sc);
+            ss = fmaf(g, g, ss);
+            am = fmaxf(am, fabsf(mm));
+        }
+        for (int off = 1; off < 64; off <<= 1) {
+            ss += __shfl_xor(ss, off);
+            am = fmaxf(am, __shfl_xor(am, off));
+        }
+        if (lane == 0) {
+            L.red_ss[wave] = ss;
+            L.red_am[wave] = am;
+        }
+        __syncthreads();
+        ss = L.red_ss[0];
+        am = L.red_am[0];
+        for (int w = 1; w < BS / 64; ++w) {
+            ss += L.red_ss[w];
+            am = fmaxf(am, L.red_am[w]);
+        }
+        const BlockOut bo = finish_block(ss, am, v_old, static_cast<float>(len), sc);
+        if (tid == 0) {
+            scale[blk] = bo.s_new;
+            vmom[blk] = bo.v_new;
+        }
+        for (int64_t i = tid; i < len; i += BS) {
+            const float g = load_grad(sg.grad, start + i, gdt);
+            const float mm = momentum(L, cq[i], s_old, g, sc);
+            const int q = bo.s_new > 0.0f ? encode(L, mm * bo.inv_s, half_ng, ng_m1) : 0;
+            th[i] = fmaf(-bo.r, mm, th[i] * sc.decay);
+            cq[i] = static_cast<uint8_t>(q);
+        }
+        return;
+    }
+    if (sg.period > 0 ? sg.period <= kSmallBlock : true) {
+        // small blocks (uniform p <= 32, or an explicit small-block tile): lane per block
+        for (int bi = tid; bi < tl.nblk; bi += BS) {
+            int64_t start, len;
+            block_range(sg, tl, bi, start, len);
+            const int64_t blk = tl.blk0 + bi;
+            const float s_old = scale[blk];
+            const float v_old = vmom[blk];
+            float* __restrict__ th = sg.theta + start;
+            uint8_t* __restrict__ cq = codes + sg.code_off + start;
+            float ss = 0.0f, am = 0.0f;
+            for (int64_t i = 0; i < len; ++i) {
+                const float g = load_grad(sg.grad, start + i, gdt);
+                const float mm = momentum(L, cq[i], s_old, g, sc);
+                ss = fmaf(g, g, ss);
+                am = fmaxf(am, fabsf(mm));
+            }
+            const BlockOut bo = finish_block(ss, am, v_old, static_cast<float>(len), sc);
+            scale[blk] = bo.s_new;
+            vmom[blk] = bo.v_new;
+            for (int64_t i = 0; i < len; ++i) {
+                const float g = load_grad(sg.grad, start + i, gdt);
+                const float mm = momentum(L, cq[i], s_old, g, sc);
+                const int q = bo.s_new > 0.0f ? encode(L, mm * bo.inv_s, half_ng, ng_m1) : 0;
+                th[i] = fmaf(-bo.r, mm, th[i] * sc.decay);
+                cq[i] = static_cast<uint8_t>(q);
+            }
+        }
+        return;
+    }
+    for (int bi = wave; bi < tl.nblk; bi += BS / 64) {
+        int64_t start, len;
+        block_range(sg, tl, bi, start, len);
+        const int64_t blk = tl.blk0 + bi;
+        const float s_old = scale[blk];
+        const float v_old = vmom[blk];
+        float* __restrict__ th = sg.theta + start;
+        uint8_t* __restrict__ cq = codes + sg.code_off + start;
+        float ss = 0.0f, am = 0.0f;
+        for (int64_t i = lane; i < len; i += 64) {
+            const float g = load_grad(sg.grad, start + i, gdt);
+            const float mm = momentum(L, cq[i], s_old, g, sc);
+            ss = fmaf(g, g, ss);
+            am = fmaxf(am, fabsf(mm));
+        }
+        for (int off = 1; off < 64; off <<= 1) {
+            ss += __shfl_xor(ss, off);
+            am = fmaxf(am, __shfl_xor(am, off));
+        }
+        const BlockOut bo = finish_block(ss, am, v_old, static_cast<float>(len), sc);
+        if (lane == 0) {
+            scale[blk] = bo.s_new;
+            vmom[blk] = bo.v_new;
+        }
+        for (int64_t i = lane; i < len; i += 64) {
+            const float g = load_grad(sg.grad, start + i, gdt);
+            const float mm = momentum(L, cq[i], s_old, g, sc);
+            const int q = bo.s_new > 0.0f ? encode(L, mm * bo.inv_s, half_ng, ng_m1) : 0;
+            th[i] = fmaf(-bo.r, mm, th[i] * sc.decay);
+            cq[i] = static_cast<uint8_t>(q);
+        }
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void k_step_any(const Tile* __restrict__ tiles,
+                                                       const Seg* __restrict__ segs,
+                                                       uint8_t* __restrict__ codes,
+                                                       float* __restrict__ scale,
+                                                       float* __restrict__ vmom, CodebookDev cbd,
+                                                       StepScalars sc)
+{
+    __shared__ LdsTables L;
+    const Tile tl = tiles[blockIdx.x];
+    const Seg sg = segs[tl.seg];
+    foreign_tile<kThreads>(L, tl, sg, codes, scale, vmom, cbd, sc);
 }
 
 template <int GDT, int VPL, int BS>
@@ -252,26 +424,150 @@ __global__ __launch_bounds__(BS) void k_step_u(const Tile* __restrict__ tiles,
 }
 
 // ---------------------------------------------------------------------------------
-// Block range of block `bi` of a tile (tensor-relative start, length).
+// Streaming passes over an element range [start, start + len) of one block (KIND_G:
+// the whole block; KIND_H: one chunk). When the tensor's parameter and gradient
+// pointers allow it, the 4-element-aligned body of the range moves with 128-bit
+// (parameters, fp32 gradients), 64-bit (bf16 gradients) and 32-bit (4 codes) accesses;
+// the head and tail (at most 3 elements each) go element by element. The reduce pass
+// uses ordinary loads so that the update pass finds gradient and code lines in cache.
+// Both passes evaluate the momentum with the same operations, so they agree bit for bit.
 // ---------------------------------------------------------------------------------
-__device__ __forceinline__ void block_range(const Seg& sg, const Tile& tl, int bi,
-                                            int64_t& start, int64_t& len)
+template <int GDT>
+__device__ __forceinline__ bool vector_ok(const Seg& sg)
 {
-    if (sg.period > 0) {
-        start = tl.elem0 + static_cast<int64_t>(bi) * sg.period;
-        len = sg.period;
+    const uintptr_t galign = GDT == DT_F32 ? 15 : 7;
+    return ((reinterpret_cast<uintptr_t>(sg.theta) & 15) == 0) &&
+           ((reinterpret_cast<uintptr_t>(sg.grad) & galign) == 0);
+}
+
+template <int GDT>
+__device__ __forceinline__ void load_grad4(const Seg& sg, int64_t v, float g[4])
+{
+    if (GDT == DT_F32) {
+        const f32x4 x = gl<f32x4>(sg.grad)[v];
+        g[0] = x.x; g[1] = x.y; g[2] = x.z; g[3] = x.w;
     } else {
-        const int64_t local = tl.blk0 + bi - sg.blk_begin;
-        start = sg.csr[local];
-        len = sg.csr[local + 1] - start;
+        const u32x2 x = gl<u32x2>(sg.grad)[v];
+        g[0] = bf16_lo(x.x); g[1] = bf16_hi(x.x); g[2] = bf16_lo(x.y); g[3] = bf16_hi(x.y);
     }
 }
 
-// ---------------------------------------------------------------------------------
-// KIND_G: one block per workgroup of any size and alignment, streamed twice: the
-// first pass reduces sum g^2 and max |m|; the second recomputes m bit-identically
-// (same operations on the same inputs), requantizes and updates the parameters.
-// ---------------------------------------------------------------------------------
+struct Span {
+    int64_t vb, ve;   // vector body [vb, ve) in vector units (4 elements)
+    int64_t start, nh, hb_end, tail0, nt;
+};
+
+template <int GDT>
+__device__ __forceinline__ Span make_span(const Seg& sg, int64_t start, int64_t len)
+{
+    const int64_t end = start + len;
+    int64_t b = end, e = end;
+    if (vector_ok<GDT>(sg)) {
+        b = (start + 3) & ~int64_t(3);
+        e = end & ~int64_t(3);
+        if (b > end) b = end;
+        if (e < b) e = b;
+    }
+    Span sp;
+    sp.vb = b >> 2;
+    sp.ve = e >> 2;
+    sp.start = start;
+    sp.nh = b - start;
+    sp.tail0 = e;
+    sp.nt = end - e;
+    sp.hb_end = b;
+    return sp;
+}
+
+template <int GDT, int BS>
+__device__ __forceinline__ void pass_reduce(const LdsTables& L, const Seg& sg,
+                                            const uint8_t* __restrict__ cq, const Span& sp,
+                                            float s_old, const StepScalars& sc, float& ss,
+                                            float& am)
+{
+    const int tid = threadIdx.x;
+#pragma unroll 2
+    for (int64_t v = sp.vb + tid; v < sp.ve; v += BS) {
+        float g[4];
+        load_grad4<GDT>(sg, v, g);
+        const uint32_t q4 = reinterpret_cast<const uint32_t*>(cq)[v];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const float mm = momentum(L, (q4 >> (8 * c)) & 0xff, s_old, g[c], sc);
+            ss = fmaf(g[c], g[c], ss);
+            am = fmaxf(am, fabsf(mm));
+        }
+    }
+    for (int64_t i = tid; i < sp.nh + sp.nt; i += BS) {
+        const int64_t e = i < sp.nh ? sp.start + i : sp.tail0 + (i - sp.nh);
+        const float g = load_grad(sg.grad, e, GDT);
+        const float mm = momentum(L, cq[e], s_old, g, sc);
+        ss = fmaf(g, g, ss);
+        am = fmaxf(am, fabsf(mm));
+    }
+}
+
+template <int GDT, int BS>
+__device__ __forceinline__ void pass_update(const LdsTables& L, const Seg& sg,
+                                            uint8_t* __restrict__ cq, const Span& sp,
+                                            float s_old, const BlockOut& bo,
+                                            const StepScalars& sc, float half_ng, int ng_m1)
+{
+    const int tid = threadIdx.x;
+    float* __restrict__ th = sg.theta;
+#pragma unroll 2
+    for (int64_t v = sp.vb + tid; v < sp.ve; v += BS) {
+        float g[4];
+        load_grad4<GDT>(sg, v, g);
+        const uint32_t q4 = reinterpret_cast<const uint32_t*>(cq)[v];
+        const f32x4 t4 = __builtin_nontemporal_load(gl<f32x4>(th) + v);
+        const float tv[4] = {t4.x, t4.y, t4.z, t4.w};
+        float out[4];
+        uint32_t packed = 0;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const float mm = momentum(L, (q4 >> (8 * c)) & 0xff, s_old, g[c], sc);
+            const int q = bo.s_new > 0.0f ? encode(L, mm * bo.inv_s, half_ng, ng_m1) : 0;
+            packed |= static_cast<uint32_t>(q) << (8 * c);
+            out[c] = fmaf(-bo.r, mm, tv[c] * sc.decay);
+        }
+        const f32x4 o4 = {out[0], out[1], out[2], out[3]};
+        __builtin_nontemporal_store(o4, glw<f32x4>(th) + v);
+        __builtin_nontemporal_store(packed, reinterpret_cast<uint32_t*>(cq) + v);
+    }
+    for (int64_t i = tid; i < sp.nh + sp.nt; i += BS) {
+        const int64_t e = i < sp.nh ? sp.start + i : sp.tail0 + (i - sp.nh);
+        const float g = load_grad(sg.grad, e, GDT);
+        const float mm = momentum(L, cq[e], s_old, g, sc);
+        const int q = bo.s_new > 0.0f ? encode(L, mm * bo.inv_s, half_ng, ng_m1) : 0;
+        th[e] = fmaf(-bo.r, mm, th[e] * sc.decay);
+        cq[e] = static_cast<uint8_t>(q);
+    }
+}
+
+template <int BS>
+__device__ __forceinline__ void wg_reduce(float& ss, float& am, LdsTables& L)
+{
+    for (int off = 1; off < 64; off <<= 1) {
+        ss += __shfl_xor(ss, off);
+        am = fmaxf(am, __shfl_xor(am, off));
+    }
+    const int wave = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) {
+        L.red_ss[wave] = ss;
+        L.red_am[wave] = am;
+    }
+    __syncthreads();
+    ss = L.red_ss[0];
+    am = L.red_am[0];
+    for (int w = 1; w < BS / 64; ++w) {
+        ss += L.red_ss[w];
+        am = fmaxf(am, L.red_am[w]);
+    }
+    __syncthreads();
+}
+
+// KIND_G: one block per workgroup, any size and alignment: reduce pass, update pass.
 template <int GDT>
 __global__ __launch_bounds__(kThreads) void k_step_g(const Tile* __restrict__ tiles,
                                                      const Seg* __restrict__ segs,
@@ -283,59 +579,23 @@ __global__ __launch_bounds__(kThreads) void k_step_g(const Tile* __restrict__ ti
     __shared__ LdsTables L;
     const Tile tl = tiles[blockIdx.x];
     const Seg sg = segs[tl.seg];
-    const int tid = threadIdx.x;
-    const int64_t len = tl.nelem;
-    const int64_t e0 = tl.elem0;
     const int64_t blk = tl.blk0;
-    float* __restrict__ th = sg.theta + e0;
-    uint8_t* __restrict__ cq = codes + sg.code_off + e0;
-    const void* gp = GDT == DT_F32
-                         ? static_cast<const void*>(static_cast<const float*>(sg.grad) + e0)
-                         : static_cast<const void*>(static_cast<const uint16_t*>(sg.grad) + e0);
+    uint8_t* __restrict__ cq = codes + sg.code_off;
+    const Span sp = make_span<GDT>(sg, tl.elem0, tl.nelem);
     const float s_old = scale[blk];
     const float v_old = vmom[blk];
     load_tables(L, cbd);
     __syncthreads();
-
     float ss = 0.0f, am = 0.0f;
-#pragma unroll 4
-    for (int64_t i = tid; i < len; i += kThreads) {
-        const float g = load_grad(gp, i, GDT);
-        const float mm = momentum(L, cq[i], s_old, g, sc);
-        ss = fmaf(g, g, ss);
-        am = fmaxf(am, fabsf(mm));
-    }
-    for (int off = 1; off < 64; off <<= 1) {
-        ss += __shfl_xor(ss, off);
-        am = fmaxf(am, __shfl_xor(am, off));
-    }
-    const int wave = tid >> 6;
-    if ((tid & 63) == 0) {
-        L.red_ss[wave] = ss;
-        L.red_am[wave] = am;
-    }
-    __syncthreads();
-    ss = L.red_ss[0];
-    am = L.red_am[0];
-    for (int w = 1; w < kThreads / 64; ++w) {
-        ss += L.red_ss[w];
-        am = fmaxf(am, L.red_am[w]);
-    }
-    const BlockOut bo = finish_block(ss, am, v_old, static_cast<float>(len), sc);
-    if (tid == 0) {
+    pass_reduce<GDT, kThreads>(L, sg, cq, sp, s_old, sc, ss, am);
+    wg_reduce<kThreads>(ss, am, L);
+    const BlockOut bo = finish_block(ss, am, v_old, static_cast<float>(tl.nelem), sc);
+    if (threadIdx.x == 0) {
         scale[blk] = bo.s_new;
         vmom[blk] = bo.v_new;
     }
-    const float half_ng = 0.5f * static_cast<float>(cbd.ng);
-    const int ng_m1 = cbd.ng - 1;
-#pragma unroll 4
-    for (int64_t i = tid; i < len; i += kThreads) {
-        const float g = load_grad(gp, i, GDT);
-        const float mm = momentum(L, cq[i], s_old, g, sc);
-        const int q = bo.s_new > 0.0f ? encode(L, mm * bo.inv_s, half_ng, ng_m1) : 0;
-        th[i] = fmaf(-bo.r, mm, th[i] * sc.decay);
-        cq[i] = static_cast<uint8_t>(q);
-    }
+    pass_update<GDT, kThreads>(L, sg, cq, sp, s_old, bo, sc, 0.5f * static_cast<float>(cbd.ng),
+                               cbd.ng - 1);
 }
 
 // ---------------------------------------------------------------------------------
@@ -401,27 +661,6 @@ __global__ __launch_bounds__(kThreads) void k_step_l(const Tile* __restrict__ ti
 // in chunk order (identical result in every chunk), recomputes m bit-identically and
 // updates its chunk.
 // ---------------------------------------------------------------------------------
-__device__ __forceinline__ void wg_reduce(float& ss, float& am, LdsTables& L)
-{
-    for (int off = 1; off < 64; off <<= 1) {
-        ss += __shfl_xor(ss, off);
-        am = fmaxf(am, __shfl_xor(am, off));
-    }
-    const int wave = threadIdx.x >> 6;
-    if ((threadIdx.x & 63) == 0) {
-        L.red_ss[wave] = ss;
-        L.red_am[wave] = am;
-    }
-    __syncthreads();
-    ss = L.red_ss[0];
-    am = L.red_am[0];
-    for (int w = 1; w < kThreads / 64; ++w) {
-        ss += L.red_ss[w];
-        am = fmaxf(am, L.red_am[w]);
-    }
-    __syncthreads();
-}
-
 template <int GDT>
 __global__ __launch_bounds__(kThreads) void k_step_h_reduce(
     const Tile* __restrict__ tiles, const HTile* __restrict__ htiles, const Seg* __restrict__ segs,
@@ -433,26 +672,15 @@ __global__ __launch_bounds__(kThreads) void k_step_h_reduce(
     const Tile tl = tiles[blockIdx.x];
     const HTile ht = htiles[blockIdx.x];
     const Seg sg = segs[tl.seg];
-    const int tid = threadIdx.x;
-    const int64_t len = tl.nelem;
-    const int64_t e0 = tl.elem0;
-    const uint8_t* __restrict__ cq = codes + sg.code_off + e0;
-    const void* gp = GDT == DT_F32
-                         ? static_cast<const void*>(static_cast<const float*>(sg.grad) + e0)
-                         : static_cast<const void*>(static_cast<const uint16_t*>(sg.grad) + e0);
+    const uint8_t* __restrict__ cq = codes + sg.code_off;
+    const Span sp = make_span<GDT>(sg, tl.elem0, tl.nelem);
     const float s_old = scale[tl.blk0];
     load_tables(L, cbd);
     __syncthreads();
     float ss = 0.0f, am = 0.0f;
-#pragma unroll 4
-    for (int64_t i = tid; i < len; i += kThreads) {
-        const float g = load_grad(gp, i, GDT);
-        const float mm = momentum(L, cq[i], s_old, g, sc);
-        ss = fmaf(g, g, ss);
-        am = fmaxf(am, fabsf(mm));
-    }
-    wg_reduce(ss, am, L);
-    if (tid == 0) {
+    pass_reduce<GDT, kThreads>(L, sg, cq, sp, s_old, sc, ss, am);
+    wg_reduce<kThreads>(ss, am, L);
+    if (threadIdx.x == 0) {
         partials[ht.first + ht.chunk] = make_float2(ss, am);
         if (ht.chunk == 0) ws_old[ht.hb] = make_float2(s_old, vmom[tl.blk0]);
     }
@@ -470,13 +698,8 @@ __global__ __launch_bounds__(kThreads) void k_step_h_update(
     const HTile ht = htiles[blockIdx.x];
     const Seg sg = segs[tl.seg];
     const int tid = threadIdx.x;
-    const int64_t len = tl.nelem;
-    const int64_t e0 = tl.elem0;
-    float* __restrict__ th = sg.theta + e0;
-    uint8_t* __restrict__ cq = codes + sg.code_off + e0;
-    const void* gp = GDT == DT_F32
-                         ? static_cast<const void*>(static_cast<const float*>(sg.grad) + e0)
-                         : static_cast<const void*>(static_cast<const uint16_t*>(sg.grad) + e0);
+    uint8_t* __restrict__ cq = codes + sg.code_off;
+    const Span sp = make_span<GDT>(sg, tl.elem0, tl.nelem);
     const float2 old = ws_old[ht.hb];
     load_tables(L, cbd);
     // partials of the whole block, fixed order: thread t takes chunks t, t + 256, ...
@@ -487,22 +710,14 @@ __global__ __launch_bounds__(kThreads) void k_step_h_update(
         am = fmaxf(am, pa.y);
     }
     __syncthreads();
-    wg_reduce(ss, am, L);
+    wg_reduce<kThreads>(ss, am, L);
     const BlockOut bo = finish_block(ss, am, old.y, static_cast<float>(ht.blk_len), sc);
     if (tid == 0 && ht.chunk == 0) {
         scale[tl.blk0] = bo.s_new;
         vmom[tl.blk0] = bo.v_new;
     }
-    const float half_ng = 0.5f * static_cast<float>(cbd.ng);
-    const int ng_m1 = cbd.ng - 1;
-#pragma unroll 4
-    for (int64_t i = tid; i < len; i += kThreads) {
-        const float g = load_grad(gp, i, GDT);
-        const float mm = momentum(L, cq[i], old.x, g, sc);
-        const int q = bo.s_new > 0.0f ? encode(L, mm * bo.inv_s, half_ng, ng_m1) : 0;
-        th[i] = fmaf(-bo.r, mm, th[i] * sc.decay);
-        cq[i] = static_cast<uint8_t>(q);
-    }
+    pass_update<GDT, kThreads>(L, sg, cq, sp, old.x, bo, sc, 0.5f * static_cast<float>(cbd.ng),
+                               cbd.ng - 1);
 }
 
 template <int GDT>
@@ -579,6 +794,11 @@ hipError_t launch_step(int kind, int gdtype, int vpl, int bs, const Tile* tiles,
         else
             hipLaunchKernelGGL((k_step_g<DT_BF16>), grid, dim3(kThreads), 0, stream, tiles,
                                segs, codes, scale, vmom, cb, sc);
+        return hipGetLastError();
+    }
+    if (kind == KIND_ANY) {
+        hipLaunchKernelGGL(k_step_any, grid, dim3(kThreads), 0, stream, tiles, segs, codes, scale,
+                           vmom, cb, sc);
         return hipGetLastError();
     }
     if (kind == KIND_L) {

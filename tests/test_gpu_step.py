@@ -200,6 +200,35 @@ def test_step_is_deterministic():
         assert torch.equal(x, y)
 
 
+def test_buffer_cycling_matches_fixed_buffers():
+    """The library caches a few device tensor tables keyed by buffer addresses; cycling
+    through more parameter/gradient buffer sets than it caches (and back) gives results
+    bit-identical to one fixed set of buffers that is refilled each step."""
+    dev = _dev()
+    w = W.get("tiny")
+    fields = W.scale_fields(w)
+    hp = (w.lr, w.betas, w.eps, w.wd)
+    pa = W.init_params(w, dev)
+    pb = [p.clone() for p in pa]
+    g1 = W.make_grads(w, fields, 1, dev)
+    grad_sets = [W.make_grads(w, fields, t, dev) for t in range(1, 8)]
+    order = [0, 1, 2, 3, 4, 5, 6, 0, 1, 6, 5, 0, 0, 3]
+    a = gf.GefenState(g1)
+    b = gf.GefenState(g1)
+    fixed = [g.clone() for g in g1]
+    for t, k in enumerate(order, start=1):
+        a.step(pa, grad_sets[k], *hp, t)
+        for f, g in zip(fixed, grad_sets[k]):
+            f.copy_(g)
+        b.step(pb, fixed, *hp, t)
+        if t == 9:                      # a histogram on an older buffer set in between
+            assert torch.equal(a.histogram(grad_sets[2]), b.histogram(grad_sets[2]))
+    for x, y in zip(pa, pb):
+        assert torch.equal(x, y)
+    for which in (gf.STATE_CODES, gf.STATE_SCALE, gf.STATE_V):
+        assert torch.equal(a.read(which), b.read(which))
+
+
 def test_checkpoint_resume_bitwise():
     dev = _dev()
     w = W.get("tiny")
@@ -302,3 +331,23 @@ def test_argument_errors_on_device():
         st.step([th[:512]], [g[:512]], 1e-3, (0.9, 0.999), 1e-8, 0.0, 1)
     with pytest.raises(gf.GefenError, match="EINVAL"):
         gf.GefenState([g], period_override=[1000])                    # does not divide
+
+
+def test_mixed_tensors_share_one_launch():
+    """Tensors of several periods and both gradient dtypes in one state: tiles of the
+    smaller classes run inside the largest class's launch (generic path)."""
+    from parity import Run
+    dev = _dev()
+    specs = [(2048, 12, torch.bfloat16), (768, 7, torch.float32), (12, 300, torch.bfloat16),
+             (3, 500, torch.float32), (999, 6, torch.bfloat16), (40000, 2, torch.float32),
+             (64, 100, torch.float32)]
+    params = [torch.randn(p * nb, device=dev) * 0.02 for p, nb, _ in specs]
+    gr = lambda t: [_grad(p * nb, 700 + 10 * i + t, dt, dev=dev)
+                    for i, (p, nb, dt) in enumerate(specs)]
+    run = Run(params, gr(1), period_override=[p for p, _, _ in specs])
+    _run_steps(run, gr, 3, where="mixed")
+    st = run.state
+    st.profile_begin(1)
+    st.step(params, gr(4), 1e-3, (0.9, 0.999), 1e-8, 0.1, 4)
+    kinds = [c["kind"] for c in st.profile_end()]
+    assert kinds.count("uniform_registers") == 1 and "split_block" in kinds, kinds
