@@ -10,6 +10,11 @@ is the Llama-3 1.5B shape (1,498,482,688 fp32 parameters, bf16 gradients with
 Student-t(3) noise and per-row / per-head scales); gradients for two steps are drawn
 before timing and alternated, so the timed region contains only optimizer steps.
 
+Per-step times come from HIP events between steps (median / mean / min over the steps
+without a refit; with codebook refits, the refit step and the amortised step time
+separately). ``ceiling`` is torch's device copy and two-input add on the same GPU,
+the practical streaming ceiling that the step kernel is compared against.
+
 Prints one JSON line. ``roofline`` describes the dominant kernel class: algorithmic
 bytes per launch over its mean launch time, from HIP events recorded on the step's
 stream. ``traffic`` comes from committed rocprofv3 counter summaries when they were
@@ -22,6 +27,7 @@ import argparse
 import hashlib
 import json
 import os
+import statistics
 import sys
 import time
 
@@ -40,7 +46,7 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def read_traffic(workload: str, kind: str, vpl: int, gdt: str):
+def read_traffic(workload: str, kind: str, vpl: int, gdt: str, code_bits: int = 8):
     """Counter-derived HBM bytes per launch from profiles/, if taken on this source."""
     path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
     if not os.path.exists(path):
@@ -49,7 +55,7 @@ def read_traffic(workload: str, kind: str, vpl: int, gdt: str):
         d = json.load(f)
     if d.get("source_hash") != kernel_source_hash():
         return None
-    key = f"{kind}/vpl{vpl}/{gdt}"
+    key = f"{kind}/vpl{vpl}/{gdt}" + ("" if code_bits == 8 else f"/cb{code_bits}")
     ent = d.get("kernels", {}).get(key)
     return None if ent is None else ent.get("bytes_per_launch")
 
@@ -62,11 +68,11 @@ def cpu_baseline(w, params, grads, st, sample_elems: int):
     import oracle
     import paper_2606_13894_amd as gf
     sys.path.insert(0, os.path.join(ROOT, "tests"))
-    from parity import grad_bits
+    from parity import grad_bits, unpack_codes
 
     lay = st.layout()
     periods = st.periods
-    codes = st.read(gf.STATE_CODES).cpu().numpy()
+    codes = unpack_codes(st.read(gf.STATE_CODES).cpu().numpy(), st.k)
     scale = st.read(gf.STATE_SCALE).cpu().numpy().astype(np.float64)
     vm = st.read(gf.STATE_V).cpu().numpy().astype(np.float64)
     cb = st.read(gf.STATE_CB_DEC).cpu().numpy().astype(np.float64)
@@ -99,13 +105,83 @@ def cpu_baseline(w, params, grads, st, sample_elems: int):
             "seconds": dt}
 
 
+def adamw_comparator(torch, w, params, grads, steps: int, gefen_state_bytes: int,
+                     gefen_ms: float):
+    """torch.optim.AdamW (fused) on the same parameters and gradients: step time, state
+    bytes and algorithmic bytes per element (parameter read + write 8, fp32 gradient 4,
+    m and v read + write 16). Fused AdamW takes gradients in the parameter dtype, so
+    bf16 gradients are widened to fp32 once, outside the timed loop."""
+    ps = [torch.nn.Parameter(p.detach().clone()) for p in params]
+    g32 = [[g.float() for g in gs] for gs in grads]
+    torch.cuda.synchronize()
+    base = torch.cuda.memory_allocated()
+    opt = torch.optim.AdamW(ps, lr=w.lr, betas=w.betas, eps=w.eps, weight_decay=w.wd,
+                            fused=True)
+    for p, g in zip(ps, g32[0]):
+        p.grad = g
+    opt.step()
+    torch.cuda.synchronize()
+    state_bytes = torch.cuda.memory_allocated() - base
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(steps):
+        for p, g in zip(ps, g32[i % 2]):
+            p.grad = g
+        opt.step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    n = w.numel
+    bytes_step = 28 * n
+    out = {"optimizer": "torch.optim.AdamW(fused=True)", "ms_per_step": round(ms, 4),
+           "gparams_per_s": round(n / (ms * 1e-3) / 1e9, 3),
+           "hbm_gbps": round(bytes_step / (ms * 1e-3) / 1e9, 1),
+           "bytes_per_elem": 28, "state_bytes": state_bytes,
+           "gefen_state_bytes": gefen_state_bytes,
+           "state_ratio": round(state_bytes / gefen_state_bytes, 3),
+           "gefen_speedup": round(ms / gefen_ms, 3)}
+    del opt, ps, g32
+    torch.cuda.empty_cache()
+    return out
+
+
+def copy_ceiling(torch, dev, nbytes: int = 4 << 30, reps: int = 10):
+    """Practical streaming ceiling on this GPU: torch's device copy (one read, one write)
+    and an add of two tensors (two reads, one write) over `nbytes` per tensor."""
+    n = nbytes // 4
+    a = torch.ones(n, dtype=torch.float32, device=dev)
+    b = torch.empty_like(a)
+    c = torch.empty_like(a)
+    out = {}
+    for name, fn, moved in (("copy_gbps", lambda: b.copy_(a), 2 * nbytes),
+                            ("add_gbps", lambda: torch.add(a, b, out=c), 3 * nbytes)):
+        fn()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        out[name] = round(moved * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9, 1)
+    del a, b, c
+    torch.cuda.empty_cache()
+    out["bytes_per_tensor"] = nbytes
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama3_1p5b")
+    ap.add_argument("--code-bits", type=int, default=8, choices=(8, 4),
+                    help="momentum code width: 8 (k = 256) or 4 (k = 16, two codes per byte)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-adamw", action="store_true",
+                    help="skip the torch AdamW comparison (always skipped for explicit blocks)")
     ap.add_argument("--cpu-sample-elems", type=int, default=100_000_000)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain device-to-device copy of a known byte count "
@@ -145,7 +221,8 @@ def main():
     torch.cuda.synchronize()
 
     t0 = time.perf_counter()
-    st = gf.GefenState(grads[0], block_offsets=offsets, eps_part=w.eps)
+    st = gf.GefenState(grads[0], block_offsets=offsets, eps_part=w.eps,
+                       code_bits=args.code_bits)
     torch.cuda.synchronize()
     init_s = time.perf_counter() - t0
 
@@ -159,21 +236,31 @@ def main():
     torch.cuda.synchronize()
 
     st.profile_begin(args.steps)
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    refit_at = []
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
-    e0.record()
-    for _ in range(args.steps):
+    marks[0].record()
+    for i in range(args.steps):
         t += 1
         st.step(params, grads[(t - 1) % 2], *hp, t)
         if w.refit_every and t % w.refit_every == 0:
             st.fit_codebook(grads[(t - 1) % 2])
-    e1.record()
+            refit_at.append(i)
+        marks[i + 1].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     classes = st.profile_end()
-    ms_per_step = e0.elapsed_time(e1) / args.steps
+    ms_per_step = marks[0].elapsed_time(marks[-1]) / args.steps
+    per_step = [marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps)]
+    plain = [x for i, x in enumerate(per_step) if i not in refit_at]
+    step_stats = {"median_ms": round(statistics.median(plain), 4),
+                  "mean_ms": round(statistics.fmean(plain), 4), "min_ms": round(min(plain), 4),
+                  "amortised_ms": round(ms_per_step, 4)}
+    if refit_at:
+        step_stats["refit_step_ms"] = round(statistics.fmean(per_step[i] for i in refit_at), 4)
+        step_stats["refits_timed"] = len(refit_at)
+    ceiling = copy_ceiling(torch, dev)
 
     n = w.numel
     step_bytes = sum(c["bytes_per_launch"] for c in classes)
@@ -182,7 +269,7 @@ def main():
     dom = max(classes, key=lambda c: c["bytes_per_launch"])
     dom_ms = dom["total_ms"] / max(1, dom["launches"])
     achieved = dom["bytes_per_launch"] / (dom_ms * 1e-3) / 1e9
-    traffic = read_traffic(w.name, dom["kind"], dom["vpl"], dom["grad_dtype"])
+    traffic = read_traffic(w.name, dom["kind"], dom["vpl"], dom["grad_dtype"], args.code_bits)
     persistent, workspace = st.state_bytes()
 
     line = {
@@ -199,10 +286,13 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": w.name, "params": n, "tensors": len(w.tensors),
-                   "grad_dtype": w.grad_dtype, "code_bits": 8,
+                   "grad_dtype": w.grad_dtype, "code_bits": args.code_bits,
                    "refit_every": w.refit_every or None},
         "hbm_gbps": round(gbps, 1),
         "pct_peak_hbm": round(100.0 * gbps / PEAK_HBM_GBPS, 2),
+        "step_ms": step_stats,
+        "ceiling": dict(ceiling, dominant_kernel_pct_of_copy=round(
+            100.0 * achieved / ceiling["copy_gbps"], 1)),
         "bytes_per_step": step_bytes,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS,
                      "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
@@ -217,6 +307,9 @@ def main():
         "state_bytes": {"persistent": persistent, "workspace": workspace},
         "source_hash": kernel_source_hash(),
     }
+    if not args.no_adamw and not w.n_blocks:
+        line["adamw"] = adamw_comparator(torch, w, params, grads, min(args.steps, 20),
+                                         persistent, ms_per_step)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, params, grads[t % 2], st, args.cpu_sample_elems)
     print(json.dumps(line), flush=True)

@@ -74,8 +74,9 @@ typedef struct gefen_state gefen_state;   /* opaque, library-owned */
  *                  elements [block_offsets[b], block_offsets[b+1]). Must start at 0,
  *                  increase strictly, end at the total numel, and have a boundary at
  *                  every tensor boundary. Overrides inference and period_override.
- *  code_bits       bits per momentum code: 8 (k = 256 entries) or 4 (k = 16, one
- *                  code still stored per byte).
+ *  code_bits       bits per momentum code: 8 (k = 256 entries, 16k = 4096 histogram
+ *                  bins, one code per byte) or 4 (k = 16, 256 bins, two codes per
+ *                  byte; the paper's 4-bit variant, Sec. 6 ablation).
  *  eps_part        eps inside log(g^2 + eps) of the partition score (>= 0; the
  *                  paper leaves it open -- the optimizer eps, 1e-8, is the default).
  *  stream          stream for all work; synchronised once (the inferred periods
@@ -165,9 +166,12 @@ int gefen_dp_codebook(const uint64_t* hist, int32_t nbins, int32_t k, double* co
 int gefen_get_periods(const gefen_state* st, int64_t* periods_out);
 
 /* Layout of the state buffers (host int64 arrays of n_tensors + 1 entries each):
- * tensor i's codes occupy bytes [code_offsets[i], code_offsets[i] + numel_i) of the
- * codes buffer, and its blocks are global block indices
- * [block_index[i], block_index[i+1]). Either pointer may be NULL. */
+ * element e of tensor i has code index j = code_offsets[i] + e (code_offsets are
+ * multiples of 32, so every tensor starts on a 16-byte boundary). With 8-bit codes,
+ * code j is byte j of the codes buffer; with 4-bit codes it is the low (j even) or high
+ * (j odd) nibble of byte j / 2. Tensor i's blocks are global block indices
+ * [block_index[i], block_index[i+1]). total_code_bytes is the codes buffer's size.
+ * Any output pointer may be NULL. */
 int gefen_get_layout(const gefen_state* st, int64_t* code_offsets, int64_t* block_index,
                      int64_t* total_code_bytes, int64_t* total_blocks, int32_t* k);
 
@@ -213,7 +217,8 @@ int gefen_import(gefen_state* st, const void* src, int64_t bytes, void* stream);
  * class (host arrays of `cap` entries): kind, vectors per lane (kind 0), workgroup
  * size, gradient dtype, number of timed launches, summed kernel time in milliseconds, elements per
  * launch and algorithmic HBM bytes per launch (per element: 8 for the parameter
- * read and write, 4 or 2 for the gradient, 2 for the code read and write; per
+ * read and write, 4 or 2 for the gradient, 2 (8-bit) or 1 (4-bit) for the code read
+ * and write; per
  * block: 16 for scale and second moment read and write, plus 8 for an explicit block
  * offset read by the small-block kernel). It then disarms and frees the events.
  * ---------------------------------------------------------------------------- */

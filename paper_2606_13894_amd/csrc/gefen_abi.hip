@@ -76,6 +76,7 @@ struct gefen_state {
     int device = 0;
     int32_t n_tensors = 0;
     int32_t k = 256, nbins = 4096, ng = 4096;
+    int32_t code_bits = 8;
     bool explicit_blocks = false;
     std::vector<int64_t> numel, period, blk_begin, code_off;   // blk_begin/code_off: n + 1
     std::vector<int32_t> gdtype;
@@ -564,7 +565,8 @@ int plan_tiles(gefen_state* st, const std::vector<std::vector<int64_t>>& starts)
                 static_cast<int64_t>(all.size()), static_cast<int64_t>(lists[i].size()), 0, 0};
         for (size_t j = 0; j < lists[i].size(); ++j) {
             const Tile& tl = lists[i][j];
-            const int64_t per_elem = 8 + (st->gdtype[tl.seg] == DT_F32 ? 4 : 2) + 2;
+            const int64_t per_elem =
+                8 + (st->gdtype[tl.seg] == DT_F32 ? 4 : 2) + (st->code_bits == 4 ? 1 : 2);
             c.elems += tl.nelem;
             c.bytes += tl.nelem * per_elem + 16 * int64_t(tl.nblk);
             if (tile_kinds[i][j] == KIND_L && st->explicit_blocks) c.bytes += 8 * int64_t(tl.nblk);
@@ -776,6 +778,7 @@ int gefen_init(const gefen_tensor* grads0, int32_t n_tensors, const int64_t* per
     std::unique_ptr<gefen_state> st(new gefen_state());
     GEFEN_HIP(hipGetDevice(&st->device));
     st->n_tensors = n_tensors;
+    st->code_bits = code_bits;
     st->k = 1 << code_bits;
     st->nbins = 16 * st->k;
     st->ng = 16 * st->k;
@@ -841,10 +844,11 @@ int gefen_init(const gefen_tensor* grads0, int32_t n_tensors, const int64_t* per
         const int64_t nb = st->explicit_blocks ? static_cast<int64_t>(starts[t].size()) - 1
                                                : st->numel[t] / st->period[t];
         st->blk_begin[t + 1] = st->blk_begin[t] + nb;
-        st->code_off[t + 1] = st->code_off[t] + ((st->numel[t] + 15) & ~int64_t(15));
+        // every tensor's codes start on a 16-byte boundary (32 codes at 4 bits)
+        st->code_off[t + 1] = st->code_off[t] + ((st->numel[t] + 31) & ~int64_t(31));
     }
     st->total_blocks = st->blk_begin[n_tensors];
-    st->code_bytes = st->code_off[n_tensors];
+    st->code_bytes = st->code_off[n_tensors] * code_bits / 8;
 
     if ((rc = st->alloc(&st->codes, st->code_bytes, true))) return rc;
     if ((rc = st->alloc(&st->scale, 4 * st->total_blocks, true))) return rc;
@@ -942,10 +946,10 @@ int gefen_step(gefen_state* st, const gefen_tensor* params, const gefen_tensor* 
         if (prof) GEFEN_HIP(hipEventRecord(st->prof_events[(st->prof_steps * ncls + ci) * 2], stream));
         hipError_t e =
             c.kind == KIND_H
-                ? launch_step_h(c.gdtype, st->tiles + c.first, st->htiles + c.first, c.count,
+                ? launch_step_h(c.gdtype, st->code_bits, st->tiles + c.first, st->htiles + c.first, c.count,
                                 st->segs, st->codes, st->scale, st->vmom, cb, sc,
                                 st->h_partials, st->h_old, stream)
-                : launch_step(c.kind, c.gdtype, c.vpl, c.bs, st->tiles + c.first, c.count,
+                : launch_step(c.kind, c.gdtype, st->code_bits, c.vpl, c.bs, st->tiles + c.first, c.count,
                               st->segs, st->codes, st->scale, st->vmom, cb, sc, stream);
         if (e != hipSuccess)
             return fail(GEFEN_EHIP, "step launch (kind %d) failed: %s", c.kind, hipGetErrorString(e));

@@ -58,7 +58,7 @@ static_assert(sizeof(HTile) == 32, "HTile layout");
 struct Seg {
     float* theta;             // parameters (fp32)
     const void* grad;         // gradients (fp32 or bf16)
-    int64_t code_off;         // byte offset of the tensor's codes in the codes buffer
+    int64_t code_off;         // code index of the tensor's first code (a multiple of 32)
     int64_t period;           // > 0: uniform blocks of this size; 0: explicit blocks
     int64_t blk_begin;        // global index of the tensor's first block
     const int64_t* csr;       // explicit blocks: tensor-relative starts (n_blocks + 1)
@@ -92,16 +92,18 @@ struct CodebookDev {
 
 // Launchers (all enqueue on `stream` and return the launch status).
 // `bs` is the KIND_U workgroup size (256, 512 or 1024); other kinds use kThreads.
-hipError_t launch_step(int kind, int gdtype, int vpl, int bs, const Tile* tiles,
+// `code_bits` is 8 (one code per byte) or 4 (two codes per byte, low nibble first);
+// codes are addressed by code index Seg::code_off + element index.
+hipError_t launch_step(int kind, int gdtype, int code_bits, int vpl, int bs, const Tile* tiles,
                        int64_t n_tiles, const Seg* segs, uint8_t* codes, float* scale,
                        float* vmom, CodebookDev cb, StepScalars sc, hipStream_t stream);
 
 // KIND_H needs `htiles` (parallel to `tiles`), `partials` (float2 per tile) and
 // `ws_old` (float2 per huge block).
-hipError_t launch_step_h(int gdtype, const Tile* tiles, const HTile* htiles, int64_t n_tiles,
-                         const Seg* segs, uint8_t* codes, float* scale, float* vmom,
-                         CodebookDev cb, StepScalars sc, float2* partials, float2* ws_old,
-                         hipStream_t stream);
+hipError_t launch_step_h(int gdtype, int code_bits, const Tile* tiles, const HTile* htiles,
+                         int64_t n_tiles, const Seg* segs, uint8_t* codes, float* scale,
+                         float* vmom, CodebookDev cb, StepScalars sc, float2* partials,
+                         float2* ws_old, hipStream_t stream);
 
 // Histogram over all tiles. KIND_H tiles need their block absmax first:
 // launch_hist_h_absmax over each KIND_H class range writes am_partials[first + chunk].

@@ -74,6 +74,54 @@ __device__ __forceinline__ int encode(const LdsTables& L, float x, float half_ng
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
+// Momentum codes of CB bits (8 or 4), addressed by code index j = the tensor's code
+// offset + element index. CB = 8: byte j. CB = 4: nibble j, i.e. byte j / 2, low half
+// for even j, so four consecutive codes from j % 4 == 0 form one 16-bit word.
+template <int CB>
+__device__ __forceinline__ int code_ld(const uint8_t* codes, int64_t j)
+{
+    if (CB == 8) return codes[j];
+    return (codes[j >> 1] >> (4 * (j & 1))) & 0xf;
+}
+
+// Scalar store of code j whose current value is `old`. With 4-bit codes the byte can be
+// shared with a neighbouring block that another lane or workgroup updates at the same
+// time, so the nibble changes by one atomic XOR (old ^ q) of its 32-bit word, which
+// leaves every other nibble of the word as it is.
+template <int CB>
+__device__ __forceinline__ void code_st(uint8_t* codes, int64_t j, int old, int q)
+{
+    if (CB == 8) {
+        codes[j] = static_cast<uint8_t>(q);
+    } else if (old != q) {
+        atomicXor(reinterpret_cast<unsigned int*>(codes) + (j >> 3),
+                  static_cast<unsigned int>(old ^ q) << (4 * (j & 7)));
+    }
+}
+
+// Codes j .. j + 3 (j % 4 == 0) packed CB bits apiece, lowest index in the lowest bits.
+template <int CB>
+__device__ __forceinline__ uint32_t code_ld4(const uint8_t* codes, int64_t j)
+{
+    if (CB == 8) return *gl<uint32_t>(codes + j);
+    return *gl<uint16_t>(codes + (j >> 1));
+}
+
+template <int CB>
+__device__ __forceinline__ void code_st4(uint8_t* codes, int64_t j, uint32_t w)
+{
+    if (CB == 8)
+        __builtin_nontemporal_store(w, glw<uint32_t>(codes + j));
+    else
+        __builtin_nontemporal_store(static_cast<uint16_t>(w), glw<uint16_t>(codes + (j >> 1)));
+}
+
+template <int CB>
+__device__ __forceinline__ int code_get(uint32_t w, int c)
+{
+    return static_cast<int>((w >> (CB * c)) & ((1u << CB) - 1));
+}
+
 __device__ __forceinline__ float momentum(const LdsTables& L, int q, float s_old, float g,
                                           const StepScalars& sc)
 {
@@ -110,7 +158,7 @@ __device__ __forceinline__ BlockOut finish_block(float ss, float am, float v_old
 // blocks. Small tiles (one block per workgroup, one or two vectors per lane) keep
 // the most independent streams in flight, which is what saturates HBM here.
 // ---------------------------------------------------------------------------------
-template <int GDT, int VPL, int BS, bool ALIGNED>
+template <int GDT, int VPL, int BS, bool ALIGNED, int CB>
 __device__ __forceinline__ void step_u_body(LdsTables& L, const Tile& tl, const Seg& sg,
                                             uint8_t* __restrict__ codes,
                                             float* __restrict__ scale,
@@ -129,7 +177,7 @@ __device__ __forceinline__ void step_u_body(LdsTables& L, const Tile& tl, const 
     const int64_t blk = tl.blk0 + gi;
 
     float* __restrict__ th_base = sg.theta + e0;
-    uint8_t* __restrict__ cq_base = codes + sg.code_off + e0;
+    const int64_t cj0 = sg.code_off + e0;   // code index of the block's first element
 
     float th[VPL][4];
     float gv[VPL][4];
@@ -162,7 +210,10 @@ __device__ __forceinline__ void step_u_body(LdsTables& L, const Tile& tl, const 
                     gv[j][c] = load_grad(sg.grad, e0 + o + c, GDT);
                 }
             }
-            cq[j] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(cq_base + o));
+            if (CB == 8)
+                cq[j] = __builtin_nontemporal_load(gl<uint32_t>(codes + cj0 + o));
+            else
+                cq[j] = __builtin_nontemporal_load(gl<uint16_t>(codes + ((cj0 + o) >> 1)));
         }
     }
     float s_old = 0.0f, v_old = 0.0f;
@@ -182,7 +233,7 @@ __device__ __forceinline__ void step_u_body(LdsTables& L, const Tile& tl, const 
         const bool ok = active && (j * lpb + li) < nv;
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
-            const int q = (cq[j] >> (8 * c)) & 0xff;
+            const int q = code_get<CB>(cq[j], c);
             const float mm = ok ? momentum(L, q, s_old, gv[j][c], sc) : 0.0f;
             m[j][c] = mm;
             ss = fmaf(gv[j][c], gv[j][c], ss);
@@ -229,7 +280,7 @@ __device__ __forceinline__ void step_u_body(LdsTables& L, const Tile& tl, const 
             for (int c = 0; c < 4; ++c) {
                 const float mm = m[j][c];
                 const int q = bo.s_new > 0.0f ? encode(L, mm * bo.inv_s, half_ng, ng_m1) : 0;
-                packed |= static_cast<uint32_t>(q) << (8 * c);
+                packed |= static_cast<uint32_t>(q) << (CB * c);
                 out[c] = fmaf(-bo.r, mm, th[j][c] * sc.decay);
             }
             const int64_t o = 4 * static_cast<int64_t>(v);
@@ -240,7 +291,7 @@ __device__ __forceinline__ void step_u_body(LdsTables& L, const Tile& tl, const 
 #pragma unroll
                 for (int c = 0; c < 4; ++c) th_base[o + c] = out[c];
             }
-            __builtin_nontemporal_store(packed, reinterpret_cast<uint32_t*>(cq_base + o));
+            code_st4<CB>(codes, cj0 + o, packed);
         }
     }
 }
@@ -268,7 +319,7 @@ __device__ __forceinline__ void block_range(const Seg& sg, const Tile& tl, int b
 // single block, one lane per block for blocks of at most 32 elements, else one wave
 // per block.
 // ---------------------------------------------------------------------------------
-template <int BS>
+template <int BS, int CB>
 __device__ void foreign_tile(LdsTables& L, const Tile& tl, const Seg& sg,
                              uint8_t* __restrict__ codes, float* __restrict__ scale,
                              float* __restrict__ vmom, const CodebookDev& cbd,
@@ -289,11 +340,11 @@ __device__ void foreign_tile(LdsTables& L, const Tile& tl, const Seg& sg,
         const float s_old = scale[blk];
         const float v_old = vmom[blk];
         float* __restrict__ th = sg.theta + start;
-        uint8_t* __restrict__ cq = codes + sg.code_off + start;
+        const int64_t cj = sg.code_off + start;
         float ss = 0.0f, am = 0.0f;
         for (int64_t i = tid; i < len; i += BS) {
             const float g = load_grad(sg.grad, start + i, gdt);
-            const float mm = momentum(L, cq[i], s_old, g, sc);
+            const float mm = momentum(L, code_ld<CB>(codes, cj + i), s_old, g, sc);
             ss = fmaf(g, g, ss);
             am = fmaxf(am, fabsf(mm));
         }
@@ -319,10 +370,11 @@ __device__ void foreign_tile(LdsTables& L, const Tile& tl, const Seg& sg,
         }
         for (int64_t i = tid; i < len; i += BS) {
             const float g = load_grad(sg.grad, start + i, gdt);
-            const float mm = momentum(L, cq[i], s_old, g, sc);
+            const int q0 = code_ld<CB>(codes, cj + i);
+            const float mm = momentum(L, q0, s_old, g, sc);
             const int q = bo.s_new > 0.0f ? encode(L, mm * bo.inv_s, half_ng, ng_m1) : 0;
             th[i] = fmaf(-bo.r, mm, th[i] * sc.decay);
-            cq[i] = static_cast<uint8_t>(q);
+            code_st<CB>(codes, cj + i, q0, q);
         }
         return;
     }
@@ -335,11 +387,11 @@ __device__ void foreign_tile(LdsTables& L, const Tile& tl, const Seg& sg,
             const float s_old = scale[blk];
             const float v_old = vmom[blk];
             float* __restrict__ th = sg.theta + start;
-            uint8_t* __restrict__ cq = codes + sg.code_off + start;
+            const int64_t cj = sg.code_off + start;
             float ss = 0.0f, am = 0.0f;
             for (int64_t i = 0; i < len; ++i) {
                 const float g = load_grad(sg.grad, start + i, gdt);
-                const float mm = momentum(L, cq[i], s_old, g, sc);
+                const float mm = momentum(L, code_ld<CB>(codes, cj + i), s_old, g, sc);
                 ss = fmaf(g, g, ss);
                 am = fmaxf(am, fabsf(mm));
             }
@@ -348,10 +400,11 @@ __device__ void foreign_tile(LdsTables& L, const Tile& tl, const Seg& sg,
             vmom[blk] = bo.v_new;
             for (int64_t i = 0; i < len; ++i) {
                 const float g = load_grad(sg.grad, start + i, gdt);
-                const float mm = momentum(L, cq[i], s_old, g, sc);
+                const int q0 = code_ld<CB>(codes, cj + i);
+                const float mm = momentum(L, q0, s_old, g, sc);
                 const int q = bo.s_new > 0.0f ? encode(L, mm * bo.inv_s, half_ng, ng_m1) : 0;
                 th[i] = fmaf(-bo.r, mm, th[i] * sc.decay);
-                cq[i] = static_cast<uint8_t>(q);
+                code_st<CB>(codes, cj + i, q0, q);
             }
         }
         return;
@@ -363,11 +416,11 @@ __device__ void foreign_tile(LdsTables& L, const Tile& tl, const Seg& sg,
         const float s_old = scale[blk];
         const float v_old = vmom[blk];
         float* __restrict__ th = sg.theta + start;
-        uint8_t* __restrict__ cq = codes + sg.code_off + start;
+        const int64_t cj = sg.code_off + start;
         float ss = 0.0f, am = 0.0f;
         for (int64_t i = lane; i < len; i += 64) {
             const float g = load_grad(sg.grad, start + i, gdt);
-            const float mm = momentum(L, cq[i], s_old, g, sc);
+            const float mm = momentum(L, code_ld<CB>(codes, cj + i), s_old, g, sc);
             ss = fmaf(g, g, ss);
             am = fmaxf(am, fabsf(mm));
         }
@@ -382,14 +435,16 @@ __device__ void foreign_tile(LdsTables& L, const Tile& tl, const Seg& sg,
         }
         for (int64_t i = lane; i < len; i += 64) {
             const float g = load_grad(sg.grad, start + i, gdt);
-            const float mm = momentum(L, cq[i], s_old, g, sc);
+            const int q0 = code_ld<CB>(codes, cj + i);
+            const float mm = momentum(L, q0, s_old, g, sc);
             const int q = bo.s_new > 0.0f ? encode(L, mm * bo.inv_s, half_ng, ng_m1) : 0;
             th[i] = fmaf(-bo.r, mm, th[i] * sc.decay);
-            cq[i] = static_cast<uint8_t>(q);
+            code_st<CB>(codes, cj + i, q0, q);
         }
     }
 }
 
+template <int CB>
 __global__ __launch_bounds__(kThreads) void k_step_any(const Tile* __restrict__ tiles,
                                                        const Seg* __restrict__ segs,
                                                        uint8_t* __restrict__ codes,
@@ -400,10 +455,10 @@ __global__ __launch_bounds__(kThreads) void k_step_any(const Tile* __restrict__ 
     __shared__ LdsTables L;
     const Tile tl = tiles[blockIdx.x];
     const Seg sg = segs[tl.seg];
-    foreign_tile<kThreads>(L, tl, sg, codes, scale, vmom, cbd, sc);
+    foreign_tile<kThreads, CB>(L, tl, sg, codes, scale, vmom, cbd, sc);
 }
 
-template <int GDT, int VPL, int BS>
+template <int GDT, int VPL, int BS, int CB>
 __global__ __launch_bounds__(BS) void k_step_u(const Tile* __restrict__ tiles,
                                                      const Seg* __restrict__ segs,
                                                      uint8_t* __restrict__ codes,
@@ -418,9 +473,9 @@ __global__ __launch_bounds__(BS) void k_step_u(const Tile* __restrict__ tiles,
     const bool aligned = ((reinterpret_cast<uintptr_t>(sg.theta) & 15) == 0) &&
                          ((reinterpret_cast<uintptr_t>(sg.grad) & galign) == 0);
     if (aligned)
-        step_u_body<GDT, VPL, BS, true>(L, tl, sg, codes, scale, vmom, cbd, sc);
+        step_u_body<GDT, VPL, BS, true, CB>(L, tl, sg, codes, scale, vmom, cbd, sc);
     else
-        step_u_body<GDT, VPL, BS, false>(L, tl, sg, codes, scale, vmom, cbd, sc);
+        step_u_body<GDT, VPL, BS, false, CB>(L, tl, sg, codes, scale, vmom, cbd, sc);
 }
 
 // ---------------------------------------------------------------------------------
@@ -479,21 +534,22 @@ __device__ __forceinline__ Span make_span(const Seg& sg, int64_t start, int64_t 
     return sp;
 }
 
-template <int GDT, int BS>
+template <int GDT, int BS, int CB>
 __device__ __forceinline__ void pass_reduce(const LdsTables& L, const Seg& sg,
-                                            const uint8_t* __restrict__ cq, const Span& sp,
+                                            const uint8_t* __restrict__ codes, const Span& sp,
                                             float s_old, const StepScalars& sc, float& ss,
                                             float& am)
 {
     const int tid = threadIdx.x;
+    const int64_t cj = sg.code_off;
 #pragma unroll 2
     for (int64_t v = sp.vb + tid; v < sp.ve; v += BS) {
         float g[4];
         load_grad4<GDT>(sg, v, g);
-        const uint32_t q4 = reinterpret_cast<const uint32_t*>(cq)[v];
+        const uint32_t q4 = code_ld4<CB>(codes, cj + 4 * v);
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
-            const float mm = momentum(L, (q4 >> (8 * c)) & 0xff, s_old, g[c], sc);
+            const float mm = momentum(L, code_get<CB>(q4, c), s_old, g[c], sc);
             ss = fmaf(g[c], g[c], ss);
             am = fmaxf(am, fabsf(mm));
         }
@@ -501,47 +557,49 @@ __device__ __forceinline__ void pass_reduce(const LdsTables& L, const Seg& sg,
     for (int64_t i = tid; i < sp.nh + sp.nt; i += BS) {
         const int64_t e = i < sp.nh ? sp.start + i : sp.tail0 + (i - sp.nh);
         const float g = load_grad(sg.grad, e, GDT);
-        const float mm = momentum(L, cq[e], s_old, g, sc);
+        const float mm = momentum(L, code_ld<CB>(codes, cj + e), s_old, g, sc);
         ss = fmaf(g, g, ss);
         am = fmaxf(am, fabsf(mm));
     }
 }
 
-template <int GDT, int BS>
+template <int GDT, int BS, int CB>
 __device__ __forceinline__ void pass_update(const LdsTables& L, const Seg& sg,
-                                            uint8_t* __restrict__ cq, const Span& sp,
+                                            uint8_t* __restrict__ codes, const Span& sp,
                                             float s_old, const BlockOut& bo,
                                             const StepScalars& sc, float half_ng, int ng_m1)
 {
     const int tid = threadIdx.x;
     float* __restrict__ th = sg.theta;
+    const int64_t cj = sg.code_off;
 #pragma unroll 2
     for (int64_t v = sp.vb + tid; v < sp.ve; v += BS) {
         float g[4];
         load_grad4<GDT>(sg, v, g);
-        const uint32_t q4 = reinterpret_cast<const uint32_t*>(cq)[v];
+        const uint32_t q4 = code_ld4<CB>(codes, cj + 4 * v);
         const f32x4 t4 = __builtin_nontemporal_load(gl<f32x4>(th) + v);
         const float tv[4] = {t4.x, t4.y, t4.z, t4.w};
         float out[4];
         uint32_t packed = 0;
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
-            const float mm = momentum(L, (q4 >> (8 * c)) & 0xff, s_old, g[c], sc);
+            const float mm = momentum(L, code_get<CB>(q4, c), s_old, g[c], sc);
             const int q = bo.s_new > 0.0f ? encode(L, mm * bo.inv_s, half_ng, ng_m1) : 0;
-            packed |= static_cast<uint32_t>(q) << (8 * c);
+            packed |= static_cast<uint32_t>(q) << (CB * c);
             out[c] = fmaf(-bo.r, mm, tv[c] * sc.decay);
         }
         const f32x4 o4 = {out[0], out[1], out[2], out[3]};
         __builtin_nontemporal_store(o4, glw<f32x4>(th) + v);
-        __builtin_nontemporal_store(packed, reinterpret_cast<uint32_t*>(cq) + v);
+        code_st4<CB>(codes, cj + 4 * v, packed);
     }
     for (int64_t i = tid; i < sp.nh + sp.nt; i += BS) {
         const int64_t e = i < sp.nh ? sp.start + i : sp.tail0 + (i - sp.nh);
         const float g = load_grad(sg.grad, e, GDT);
-        const float mm = momentum(L, cq[e], s_old, g, sc);
+        const int q0 = code_ld<CB>(codes, cj + e);
+        const float mm = momentum(L, q0, s_old, g, sc);
         const int q = bo.s_new > 0.0f ? encode(L, mm * bo.inv_s, half_ng, ng_m1) : 0;
         th[e] = fmaf(-bo.r, mm, th[e] * sc.decay);
-        cq[e] = static_cast<uint8_t>(q);
+        code_st<CB>(codes, cj + e, q0, q);
     }
 }
 
@@ -568,7 +626,7 @@ __device__ __forceinline__ void wg_reduce(float& ss, float& am, LdsTables& L)
 }
 
 // KIND_G: one block per workgroup, any size and alignment: reduce pass, update pass.
-template <int GDT>
+template <int GDT, int CB>
 __global__ __launch_bounds__(kThreads) void k_step_g(const Tile* __restrict__ tiles,
                                                      const Seg* __restrict__ segs,
                                                      uint8_t* __restrict__ codes,
@@ -580,28 +638,27 @@ __global__ __launch_bounds__(kThreads) void k_step_g(const Tile* __restrict__ ti
     const Tile tl = tiles[blockIdx.x];
     const Seg sg = segs[tl.seg];
     const int64_t blk = tl.blk0;
-    uint8_t* __restrict__ cq = codes + sg.code_off;
     const Span sp = make_span<GDT>(sg, tl.elem0, tl.nelem);
     const float s_old = scale[blk];
     const float v_old = vmom[blk];
     load_tables(L, cbd);
     __syncthreads();
     float ss = 0.0f, am = 0.0f;
-    pass_reduce<GDT, kThreads>(L, sg, cq, sp, s_old, sc, ss, am);
+    pass_reduce<GDT, kThreads, CB>(L, sg, codes, sp, s_old, sc, ss, am);
     wg_reduce<kThreads>(ss, am, L);
     const BlockOut bo = finish_block(ss, am, v_old, static_cast<float>(tl.nelem), sc);
     if (threadIdx.x == 0) {
         scale[blk] = bo.s_new;
         vmom[blk] = bo.v_new;
     }
-    pass_update<GDT, kThreads>(L, sg, cq, sp, s_old, bo, sc, 0.5f * static_cast<float>(cbd.ng),
-                               cbd.ng - 1);
+    pass_update<GDT, kThreads, CB>(L, sg, codes, sp, s_old, bo, sc,
+                                   0.5f * static_cast<float>(cbd.ng), cbd.ng - 1);
 }
 
 // ---------------------------------------------------------------------------------
 // KIND_L: up to 256 small blocks (<= 32 elements) per workgroup, one lane per block.
 // ---------------------------------------------------------------------------------
-template <int GDT>
+template <int GDT, int CB>
 __global__ __launch_bounds__(kThreads) void k_step_l(const Tile* __restrict__ tiles,
                                                      const Seg* __restrict__ segs,
                                                      uint8_t* __restrict__ codes,
@@ -620,7 +677,7 @@ __global__ __launch_bounds__(kThreads) void k_step_l(const Tile* __restrict__ ti
     block_range(sg, tl, bi, start, len);
     const int64_t blk = tl.blk0 + bi;
     float* __restrict__ th = sg.theta + start;
-    uint8_t* __restrict__ cq = codes + sg.code_off + start;
+    const int64_t cj = sg.code_off + start;
     const void* gp =
         GDT == DT_F32 ? static_cast<const void*>(static_cast<const float*>(sg.grad) + start)
                       : static_cast<const void*>(static_cast<const uint16_t*>(sg.grad) + start);
@@ -633,7 +690,7 @@ __global__ __launch_bounds__(kThreads) void k_step_l(const Tile* __restrict__ ti
         m[i] = 0.0f;
         if (i < len) {
             const float g = load_grad(gp, i, GDT);
-            m[i] = momentum(L, cq[i], s_old, g, sc);
+            m[i] = momentum(L, code_ld<CB>(codes, cj + i), s_old, g, sc);
             ss = fmaf(g, g, ss);
             am = fmaxf(am, fabsf(m[i]));
         }
@@ -649,7 +706,7 @@ __global__ __launch_bounds__(kThreads) void k_step_l(const Tile* __restrict__ ti
             const float mm = m[i];
             const int q = bo.s_new > 0.0f ? encode(L, mm * bo.inv_s, half_ng, ng_m1) : 0;
             th[i] = fmaf(-bo.r, mm, th[i] * sc.decay);
-            cq[i] = static_cast<uint8_t>(q);
+            code_st<CB>(codes, cj + i, code_ld<CB>(codes, cj + i), q);
         }
     }
 }
@@ -661,7 +718,7 @@ __global__ __launch_bounds__(kThreads) void k_step_l(const Tile* __restrict__ ti
 // in chunk order (identical result in every chunk), recomputes m bit-identically and
 // updates its chunk.
 // ---------------------------------------------------------------------------------
-template <int GDT>
+template <int GDT, int CB>
 __global__ __launch_bounds__(kThreads) void k_step_h_reduce(
     const Tile* __restrict__ tiles, const HTile* __restrict__ htiles, const Seg* __restrict__ segs,
     const uint8_t* __restrict__ codes, const float* __restrict__ scale,
@@ -672,13 +729,12 @@ __global__ __launch_bounds__(kThreads) void k_step_h_reduce(
     const Tile tl = tiles[blockIdx.x];
     const HTile ht = htiles[blockIdx.x];
     const Seg sg = segs[tl.seg];
-    const uint8_t* __restrict__ cq = codes + sg.code_off;
     const Span sp = make_span<GDT>(sg, tl.elem0, tl.nelem);
     const float s_old = scale[tl.blk0];
     load_tables(L, cbd);
     __syncthreads();
     float ss = 0.0f, am = 0.0f;
-    pass_reduce<GDT, kThreads>(L, sg, cq, sp, s_old, sc, ss, am);
+    pass_reduce<GDT, kThreads, CB>(L, sg, codes, sp, s_old, sc, ss, am);
     wg_reduce<kThreads>(ss, am, L);
     if (threadIdx.x == 0) {
         partials[ht.first + ht.chunk] = make_float2(ss, am);
@@ -686,7 +742,7 @@ __global__ __launch_bounds__(kThreads) void k_step_h_reduce(
     }
 }
 
-template <int GDT>
+template <int GDT, int CB>
 __global__ __launch_bounds__(kThreads) void k_step_h_update(
     const Tile* __restrict__ tiles, const HTile* __restrict__ htiles, const Seg* __restrict__ segs,
     uint8_t* __restrict__ codes, float* __restrict__ scale, float* __restrict__ vmom,
@@ -698,7 +754,6 @@ __global__ __launch_bounds__(kThreads) void k_step_h_update(
     const HTile ht = htiles[blockIdx.x];
     const Seg sg = segs[tl.seg];
     const int tid = threadIdx.x;
-    uint8_t* __restrict__ cq = codes + sg.code_off;
     const Span sp = make_span<GDT>(sg, tl.elem0, tl.nelem);
     const float2 old = ws_old[ht.hb];
     load_tables(L, cbd);
@@ -716,19 +771,19 @@ __global__ __launch_bounds__(kThreads) void k_step_h_update(
         scale[tl.blk0] = bo.s_new;
         vmom[tl.blk0] = bo.v_new;
     }
-    pass_update<GDT, kThreads>(L, sg, cq, sp, old.x, bo, sc, 0.5f * static_cast<float>(cbd.ng),
-                               cbd.ng - 1);
+    pass_update<GDT, kThreads, CB>(L, sg, codes, sp, old.x, bo, sc,
+                                   0.5f * static_cast<float>(cbd.ng), cbd.ng - 1);
 }
 
-template <int GDT>
+template <int GDT, int CB>
 hipError_t launch_u(int vpl, int bs, dim3 grid, const Tile* tiles, const Seg* segs,
                     uint8_t* codes, float* scale, float* vmom, CodebookDev cb, StepScalars sc,
                     hipStream_t s)
 {
 #define GEFEN_U_CASE(V, B)                                                                  \
     if (vpl == V && bs == B) {                                                              \
-        hipLaunchKernelGGL((k_step_u<GDT, V, B>), grid, dim3(B), 0, s, tiles, segs, codes,  \
-                           scale, vmom, cb, sc);                                            \
+        hipLaunchKernelGGL((k_step_u<GDT, V, B, CB>), grid, dim3(B), 0, s, tiles, segs,     \
+                           codes, scale, vmom, cb, sc);                                     \
         return hipGetLastError();                                                           \
     }
     GEFEN_U_CASE(1, 256)
@@ -751,66 +806,92 @@ hipError_t launch_u(int vpl, int bs, dim3 grid, const Tile* tiles, const Seg* se
     return hipErrorInvalidValue;
 }
 
+template <int GDT, int CB>
+hipError_t launch_h(dim3 grid, const Tile* tiles, const HTile* htiles, const Seg* segs,
+                    uint8_t* codes, float* scale, float* vmom, CodebookDev cb, StepScalars sc,
+                    float2* partials, float2* ws_old, hipStream_t stream)
+{
+    hipLaunchKernelGGL((k_step_h_reduce<GDT, CB>), grid, dim3(kThreads), 0, stream, tiles,
+                       htiles, segs, codes, scale, vmom, cb, sc, partials, ws_old);
+    hipLaunchKernelGGL((k_step_h_update<GDT, CB>), grid, dim3(kThreads), 0, stream, tiles,
+                       htiles, segs, codes, scale, vmom, cb, sc, partials, ws_old);
+    return hipGetLastError();
+}
+
+template <int GDT, int CB>
+hipError_t launch_kind(int kind, int vpl, int bs, dim3 grid, const Tile* tiles,
+                       const Seg* segs, uint8_t* codes, float* scale, float* vmom,
+                       CodebookDev cb, StepScalars sc, hipStream_t stream)
+{
+    switch (kind) {
+    case KIND_U:
+        return launch_u<GDT, CB>(vpl, bs, grid, tiles, segs, codes, scale, vmom, cb, sc, stream);
+    case KIND_G:
+        hipLaunchKernelGGL((k_step_g<GDT, CB>), grid, dim3(kThreads), 0, stream, tiles, segs,
+                           codes, scale, vmom, cb, sc);
+        return hipGetLastError();
+    case KIND_L:
+        hipLaunchKernelGGL((k_step_l<GDT, CB>), grid, dim3(kThreads), 0, stream, tiles, segs,
+                           codes, scale, vmom, cb, sc);
+        return hipGetLastError();
+    default:
+        return hipErrorInvalidValue;
+    }
+}
+
 }  // namespace
 
-hipError_t launch_step_h(int gdtype, const Tile* tiles, const HTile* htiles, int64_t n_tiles,
-                         const Seg* segs, uint8_t* codes, float* scale, float* vmom,
-                         CodebookDev cb, StepScalars sc, float2* partials, float2* ws_old,
-                         hipStream_t stream)
+hipError_t launch_step_h(int gdtype, int code_bits, const Tile* tiles, const HTile* htiles,
+                         int64_t n_tiles, const Seg* segs, uint8_t* codes, float* scale,
+                         float* vmom, CodebookDev cb, StepScalars sc, float2* partials,
+                         float2* ws_old, hipStream_t stream)
 {
     if (n_tiles <= 0) return hipSuccess;
     if (n_tiles > 0x7fffffffLL) return hipErrorInvalidValue;
     const dim3 grid(static_cast<unsigned>(n_tiles));
-    if (gdtype == DT_F32) {
-        hipLaunchKernelGGL((k_step_h_reduce<DT_F32>), grid, dim3(kThreads), 0, stream, tiles,
-                           htiles, segs, codes, scale, vmom, cb, sc, partials, ws_old);
-        hipLaunchKernelGGL((k_step_h_update<DT_F32>), grid, dim3(kThreads), 0, stream, tiles,
-                           htiles, segs, codes, scale, vmom, cb, sc, partials, ws_old);
-    } else {
-        hipLaunchKernelGGL((k_step_h_reduce<DT_BF16>), grid, dim3(kThreads), 0, stream, tiles,
-                           htiles, segs, codes, scale, vmom, cb, sc, partials, ws_old);
-        hipLaunchKernelGGL((k_step_h_update<DT_BF16>), grid, dim3(kThreads), 0, stream, tiles,
-                           htiles, segs, codes, scale, vmom, cb, sc, partials, ws_old);
-    }
-    return hipGetLastError();
+    if (code_bits == 8)
+        return gdtype == DT_F32
+                   ? launch_h<DT_F32, 8>(grid, tiles, htiles, segs, codes, scale, vmom, cb, sc,
+                                         partials, ws_old, stream)
+                   : launch_h<DT_BF16, 8>(grid, tiles, htiles, segs, codes, scale, vmom, cb, sc,
+                                          partials, ws_old, stream);
+    if (code_bits == 4)
+        return gdtype == DT_F32
+                   ? launch_h<DT_F32, 4>(grid, tiles, htiles, segs, codes, scale, vmom, cb, sc,
+                                         partials, ws_old, stream)
+                   : launch_h<DT_BF16, 4>(grid, tiles, htiles, segs, codes, scale, vmom, cb, sc,
+                                          partials, ws_old, stream);
+    return hipErrorInvalidValue;
 }
 
-hipError_t launch_step(int kind, int gdtype, int vpl, int bs, const Tile* tiles,
+hipError_t launch_step(int kind, int gdtype, int code_bits, int vpl, int bs, const Tile* tiles,
                        int64_t n_tiles, const Seg* segs, uint8_t* codes, float* scale,
                        float* vmom, CodebookDev cb, StepScalars sc, hipStream_t stream)
 {
     if (n_tiles <= 0) return hipSuccess;
     if (n_tiles > 0x7fffffffLL) return hipErrorInvalidValue;
+    if (code_bits != 8 && code_bits != 4) return hipErrorInvalidValue;
     const dim3 grid(static_cast<unsigned>(n_tiles));
-    if (kind == KIND_U) {
-        return gdtype == DT_F32
-                   ? launch_u<DT_F32>(vpl, bs, grid, tiles, segs, codes, scale, vmom, cb, sc, stream)
-                   : launch_u<DT_BF16>(vpl, bs, grid, tiles, segs, codes, scale, vmom, cb, sc, stream);
-    }
-    if (kind == KIND_G) {
-        if (gdtype == DT_F32)
-            hipLaunchKernelGGL((k_step_g<DT_F32>), grid, dim3(kThreads), 0, stream, tiles, segs,
-                               codes, scale, vmom, cb, sc);
-        else
-            hipLaunchKernelGGL((k_step_g<DT_BF16>), grid, dim3(kThreads), 0, stream, tiles,
-                               segs, codes, scale, vmom, cb, sc);
-        return hipGetLastError();
-    }
     if (kind == KIND_ANY) {
-        hipLaunchKernelGGL(k_step_any, grid, dim3(kThreads), 0, stream, tiles, segs, codes, scale,
-                           vmom, cb, sc);
-        return hipGetLastError();
-    }
-    if (kind == KIND_L) {
-        if (gdtype == DT_F32)
-            hipLaunchKernelGGL((k_step_l<DT_F32>), grid, dim3(kThreads), 0, stream, tiles, segs,
+        if (code_bits == 8)
+            hipLaunchKernelGGL(k_step_any<8>, grid, dim3(kThreads), 0, stream, tiles, segs,
                                codes, scale, vmom, cb, sc);
         else
-            hipLaunchKernelGGL((k_step_l<DT_BF16>), grid, dim3(kThreads), 0, stream, tiles,
-                               segs, codes, scale, vmom, cb, sc);
+            hipLaunchKernelGGL(k_step_any<4>, grid, dim3(kThreads), 0, stream, tiles, segs,
+                               codes, scale, vmom, cb, sc);
         return hipGetLastError();
     }
-    return hipErrorInvalidValue;
+    if (code_bits == 8)
+        return gdtype == DT_F32
+                   ? launch_kind<DT_F32, 8>(kind, vpl, bs, grid, tiles, segs, codes, scale, vmom,
+                                            cb, sc, stream)
+                   : launch_kind<DT_BF16, 8>(kind, vpl, bs, grid, tiles, segs, codes, scale,
+                                             vmom, cb, sc, stream);
+    return gdtype == DT_F32
+               ? launch_kind<DT_F32, 4>(kind, vpl, bs, grid, tiles, segs, codes, scale, vmom, cb,
+                                        sc, stream)
+               : launch_kind<DT_BF16, 4>(kind, vpl, bs, grid, tiles, segs, codes, scale, vmom,
+                                         cb, sc, stream);
 }
 
 }  // namespace gefen

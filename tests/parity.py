@@ -37,6 +37,18 @@ def grad_bits(g: torch.Tensor) -> np.ndarray:
     raise TypeError(g.dtype)
 
 
+def unpack_codes(raw: np.ndarray, k: int) -> np.ndarray:
+    """Codes by code index from the library's code buffer: one per byte for k = 256,
+    two per byte (low nibble = even index) for k = 16."""
+    raw = np.asarray(raw, dtype=np.uint8)
+    if k == 256:
+        return raw
+    out = np.empty(2 * raw.size, dtype=np.uint8)
+    out[0::2] = raw & 0xF
+    out[1::2] = raw >> 4
+    return out
+
+
 def grad_f64(g: torch.Tensor) -> np.ndarray:
     return g.detach().reshape(-1).float().cpu().numpy().astype(np.float64)
 
@@ -68,7 +80,7 @@ class Run:
 
     def snapshot(self):
         torch.cuda.synchronize()
-        codes = self.state.read(gf.STATE_CODES).cpu().numpy()
+        codes = unpack_codes(self.state.read(gf.STATE_CODES).cpu().numpy(), self.k)
         scale = self.state.read(gf.STATE_SCALE).cpu().numpy().astype(np.float64)
         v = self.state.read(gf.STATE_V).cpu().numpy().astype(np.float64)
         snap = {"theta": [], "codes": [], "s": [], "v": [],

@@ -63,7 +63,9 @@ class Sampled:
 
     def snapshot(self):
         torch.cuda.synchronize()
-        codes = self.st.read(gf.STATE_CODES)
+        from parity import unpack_codes
+        codes = torch.from_numpy(unpack_codes(self.st.read(gf.STATE_CODES).cpu().numpy(),
+                                              self.st.k))
         scale = self.st.read(gf.STATE_SCALE)
         v = self.st.read(gf.STATE_V)
         snap = {"theta": [], "codes": [], "s": [], "v": [],
@@ -73,7 +75,7 @@ class Sampled:
             ei = torch.from_numpy(self.elem_idx[i]).to(p.device)
             bi = torch.from_numpy(np.asarray(self.blocks[i], dtype=np.int64)).to(p.device)
             snap["theta"].append(p.reshape(-1)[ei].double().cpu().numpy())
-            snap["codes"].append(codes[self.code_off[i] + ei].cpu().numpy())
+            snap["codes"].append(codes[self.code_off[i] + ei.cpu()].numpy())
             snap["s"].append(scale[self.blk_idx[i] + bi].double().cpu().numpy())
             snap["v"].append(v[self.blk_idx[i] + bi].double().cpu().numpy())
         del codes, scale, v
