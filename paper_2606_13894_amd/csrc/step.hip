@@ -458,6 +458,21 @@ __global__ __launch_bounds__(kThreads) void k_step_any(const Tile* __restrict__ 
     foreign_tile<kThreads, CB>(L, tl, sg, codes, scale, vmom, cbd, sc);
 }
 
+// XCD-aware tile order. Workgroups are dispatched round-robin over the 8 XCDs, so
+// workgroup b runs on XCD b % 8. Within every group of 8 * kXcdRun workgroups, XCD x
+// takes kXcdRun consecutive tiles instead of every 8th one: four 32-byte descriptors
+// share an L2 line and each XCD streams longer contiguous runs, while the round-robin
+// over groups keeps every XCD's share of the work balanced. The trailing partial
+// group keeps the identity order. A bijection on [0, n).
+constexpr uint32_t kXcdRun = 8;
+__device__ __forceinline__ uint32_t xcd_tile(uint32_t b, uint32_t n)
+{
+    constexpr uint32_t G = 8 * kXcdRun;
+    if (b >= (n / G) * G) return b;
+    const uint32_t base = (b / G) * G, r = b - base;
+    return base + (r % 8) * kXcdRun + r / 8;
+}
+
 template <int GDT, int VPL, int BS, int CB>
 __global__ __launch_bounds__(BS) void k_step_u(const Tile* __restrict__ tiles,
                                                      const Seg* __restrict__ segs,
@@ -467,7 +482,7 @@ __global__ __launch_bounds__(BS) void k_step_u(const Tile* __restrict__ tiles,
                                                      StepScalars sc)
 {
     __shared__ LdsTables L;
-    const Tile tl = tiles[blockIdx.x];
+    const Tile tl = tiles[xcd_tile(blockIdx.x, gridDim.x)];
     const Seg sg = segs[tl.seg];
     const uintptr_t galign = GDT == DT_F32 ? 15 : 7;
     const bool aligned = ((reinterpret_cast<uintptr_t>(sg.theta) & 15) == 0) &&
