@@ -488,10 +488,9 @@ int plan_tiles(gefen_state* st, const std::vector<std::vector<int64_t>>& starts)
         }
     }
     hlists.resize(lists.size());
-    // Fold every class other than the largest register-resident one (and the split
-    // huge-block classes, which need two kernels) into that one's launch: its kernel
-    // runs those tiles on a generic path (tile.vpl = 0). Tile kinds are kept for the
-    // histogram kernel.
+    // Fold the small classes other than the largest register-resident one (and the
+    // split huge-block classes, which need two kernels) into one generic launch
+    // (KIND_ANY, tile.vpl = 0). Tile kinds are kept for the histogram kernel.
     std::vector<std::vector<int32_t>> tile_kinds(lists.size());
     for (size_t i = 0; i < lists.size(); ++i) tile_kinds[i].assign(lists[i].size(), keys[i].kind);
     {
