@@ -12,6 +12,11 @@ Each wrapper cites the paper passage that the C routine follows:
   block-absmax-normalised gradients over [-1, 1].
 * :func:`dp_codebook` -- Alg. 3 and App. D (exact interval DP with forced +-1 ends).
 * :func:`step_uniform`, :func:`step_blocks` -- Alg. 1, one optimizer step.
+* :func:`muon_codec_blocks`, :func:`newton_schulz`, :func:`muon_step` -- appendix
+  "Gefen-Muon": Muon's momentum held in Gefen's quantized form, then Muon's
+  Newton-Schulz orthogonalisation and update. The paper runs the orthogonalisation of
+  the official PyTorch Muon, in bfloat16; :func:`newton_schulz` takes the same steps
+  with every tensor-valued result rounded to bfloat16 (``bf16=True``), or in float64.
 
 Gradients are numpy ``float32`` arrays, or ``uint16`` arrays holding bf16 bit patterns.
 """
@@ -65,6 +70,9 @@ def _load():
     lib.oracle_step_blocks.restype = None
     lib.oracle_step_blocks.argtypes = step_args + [vp, i64, vp, vp, i32, f64, f64, f64, f64,
                                                    f64, i64, i32, vp, vp]
+    lib.oracle_muon_codec_blocks.restype = None
+    lib.oracle_muon_codec_blocks.argtypes = [vp, i32, vp, vp, vp, i64, vp, vp, i32, f64, i32,
+                                             vp]
     lib.oracle_step_uniform.restype = None
     lib.oracle_step_uniform.argtypes = step_args + [i64, i64, vp, vp, i32, f64, f64, f64,
                                                     f64, f64, i64, i32, vp, vp]
@@ -197,3 +205,76 @@ def step_blocks(theta, g, codes, s, v, offsets, cb_dec, cb_enc, lr, beta1, beta2
                            _ptr(offs), nb, _ptr(cb_dec), _ptr(cb_enc), cb_enc.size,
                            float(lr), float(beta1), float(beta2), float(eps), float(wd),
                            int(t), 1 if quantize else 0, _ptr(m_full), _ptr(m_out))
+
+
+# ---------------------------------------------------------------------------- Gefen-Muon
+MUON_NS_COEFFS = (3.4445, -4.7750, 2.0315)   # Muon's quintic Newton-Schulz coefficients
+MUON_NS_STEPS = 5
+MUON_EPS = 1e-7
+
+
+def muon_codec_blocks(g, codes, s, offsets, cb_dec, cb_enc, mu, nesterov=True):
+    """Gefen-Muon momentum codec over explicit blocks (the C routine's comment gives
+    the equations). Updates codes and s in place; returns u (float64), the matrix that
+    Muon orthogonalises."""
+    lib = _load()
+    g, dt = _grad(np.asarray(g).reshape(-1))
+    offs = np.ascontiguousarray(offsets, dtype=np.int64)
+    cb_dec = np.ascontiguousarray(cb_dec, dtype=np.float64)
+    cb_enc = np.ascontiguousarray(cb_enc, dtype=np.float64)
+    assert codes.dtype == np.uint8 and codes.flags.c_contiguous and codes.size == g.size
+    assert s.dtype == np.float64 and s.flags.c_contiguous and s.size == offs.size - 1
+    u = np.zeros(g.size, dtype=np.float64)
+    lib.oracle_muon_codec_blocks(_ptr(g), dt, _ptr(codes), _ptr(s), _ptr(offs), offs.size - 1,
+                                 _ptr(cb_dec), _ptr(cb_enc), cb_enc.size, float(mu),
+                                 int(bool(nesterov)), _ptr(u))
+    return u
+
+
+def to_bf16(x):
+    """Round to bfloat16 as a float32 accumulator is rounded to a bfloat16 result:
+    float64 -> float32 -> bfloat16, both round-to-nearest-even. Returns float64."""
+    f = np.ascontiguousarray(np.asarray(x, dtype=np.float64).astype(np.float32))
+    u = f.view(np.uint32).astype(np.uint64)
+    r = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16) << 16
+    return r.astype(np.uint32).view(np.float32).astype(np.float64)
+
+
+def newton_schulz(u, rows, cols, steps=MUON_NS_STEPS, coeffs=MUON_NS_COEFFS, eps=MUON_EPS,
+                  bf16=True):
+    """Muon's orthogonalisation of a rows x cols matrix: work on the wide orientation
+    (transpose when rows > cols), divide by the Frobenius norm (at least eps), then
+    `steps` times X <- a X + (b A + c A^2) X with A = X X^T; transpose back.
+    With bf16, the input, the norm and every matrix result are rounded to bfloat16,
+    as the implementation the paper uses does. Returns a float64 rows x cols array."""
+    a, b, c = coeffs
+    r = to_bf16 if bf16 else (lambda z: np.asarray(z, dtype=np.float64))
+    x = r(np.asarray(u, dtype=np.float64).reshape(rows, cols))
+    transposed = rows > cols
+    if transposed:
+        x = x.T
+    norm = float(r(np.array([np.sqrt(np.sum(x * x))]))[0])
+    x = r(x / max(norm, float(r(np.array([eps]))[0])))
+    for _ in range(steps):
+        gram = r(x @ x.T)
+        poly = r(b * gram + c * (gram @ gram))
+        x = r(a * x + poly @ x)
+    return np.ascontiguousarray(x.T if transposed else x)
+
+
+def muon_lr_scale(rows, cols):
+    """Muon's shape-dependent learning-rate factor, sqrt(max(1, rows / cols))."""
+    return float(np.sqrt(max(1.0, rows / cols)))
+
+
+def muon_step(theta, g, codes, s, offsets, rows, cols, cb_dec, cb_enc, lr, mu, wd,
+              nesterov=True, steps=MUON_NS_STEPS, coeffs=MUON_NS_COEFFS, eps=MUON_EPS,
+              bf16=True):
+    """One Gefen-Muon step of a rows x cols parameter (float64 theta, updated in place):
+    codec, orthogonalisation, then theta <- theta (1 - lr wd) - lr sqrt(max(1, rows/cols)) O.
+    Returns (u, O)."""
+    u = muon_codec_blocks(g, codes, s, offsets, cb_dec, cb_enc, mu, nesterov)
+    o = newton_schulz(u, rows, cols, steps, coeffs, eps, bf16).reshape(-1)
+    theta *= 1.0 - lr * wd
+    theta -= lr * muon_lr_scale(rows, cols) * o
+    return u, o

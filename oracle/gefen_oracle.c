@@ -28,6 +28,9 @@
  *       whose new scale is 0 stores code 0 for every element.
  *   R9  the bias-corrected momentum uses the unquantized m_t of the same step.
  *   R10 per-block second moment uses the mean of g^2 over the block's elements.
+ *   R11 Gefen-Muon: the quantized buffer is Muon's momentum (no second moment); the
+ *       matrix that is orthogonalised is formed from the unquantized momentum of the
+ *       same step (as R9), with Muon's Nesterov interpolation when enabled.
  */
 #include <math.h>
 #include <stdint.h>
@@ -397,4 +400,54 @@ void oracle_step_uniform(double* theta, const void* g, int32_t dtype, uint8_t* c
     oracle_step_blocks(theta, g, dtype, codes, s, v, offs, nb, cb_dec, cb_enc, k, lr,
                        beta1, beta2, eps, wd, t, quantize, m_full, m_out);
     free(offs);
+}
+
+/* ------------------------------------------------------------------------------
+ * Gefen-Muon momentum codec (appendix "Gefen-Muon"): Muon keeps one momentum buffer
+ * per matrix and orthogonalises it; Gefen-Muon stores that buffer in Gefen's form
+ * (per-element codes, one scale per block) and leaves the orthogonalisation as in
+ * Muon. Over blocks [offs[b], offs[b+1]):
+ *
+ *   m_i  = mu * (c_dec[q_i] * s) + (1 - mu) * g_i        Muon's momentum EMA, decoded
+ *   s'   = max_i |m_i|;  q'_i = nearest(c_enc, m_i / s')  requantize (R8)
+ *   u_i  = nesterov ? (1 - mu) * g_i + mu * m_i : m_i     the matrix handed to the
+ *                                                         orthogonalisation (R11)
+ *
+ * The Nesterov form follows Muon's: the update interpolates from the gradient towards
+ * the new momentum by mu. Codes and s are updated in place; u is written (float64).
+ * ---------------------------------------------------------------------------- */
+void oracle_muon_codec_blocks(const void* g, int32_t dtype, uint8_t* codes, double* s,
+                              const int64_t* offs, int64_t nblocks, const double* cb_dec,
+                              const double* cb_enc, int32_t k, double mu, int32_t nesterov,
+                              double* u)
+{
+    for (int64_t b = 0; b < nblocks; ++b) {
+        int64_t lo = offs[b], hi = offs[b + 1];
+        if (hi <= lo) continue;
+        double smax = 0.0;
+        for (int64_t i = lo; i < hi; ++i) {
+            double gi = grad_at(g, dtype, i);
+            double mi = mu * (cb_dec[codes[i]] * s[b]) + (1.0 - mu) * gi;
+            u[i] = mi;
+            if (fabs(mi) > smax) smax = fabs(mi);
+        }
+        for (int64_t i = lo; i < hi; ++i) {
+            double mi = u[i];
+            int32_t q = 0;
+            if (smax > 0.0) {
+                double x = mi / smax;
+                double bd = fabs(x - cb_enc[0]);
+                for (int32_t j = 1; j < k; ++j) {
+                    double d = fabs(x - cb_enc[j]);
+                    if (d < bd) {
+                        bd = d;
+                        q = j;
+                    }
+                }
+            }
+            codes[i] = (uint8_t)q;
+            if (nesterov) u[i] = (1.0 - mu) * grad_at(g, dtype, i) + mu * mi;
+        }
+        s[b] = smax;
+    }
 }

@@ -1,0 +1,143 @@
+"""Pins of the Gefen-Muon oracle (appendix "Gefen-Muon") against facts fixed outside it.
+
+* bfloat16 rounding: torch's float32 -> bfloat16 conversion (a library routine).
+* Newton-Schulz in float64: the iteration X <- a X + (b X X^T + c (X X^T)^2) X keeps the
+  singular vectors and maps every normalised singular value through the odd quintic
+  p(s) = a s + b s^3 + c s^5, so the result is U diag(p^k(s / ||X||_F)) V^T (SVD by
+  numpy). A transposed operand, a coefficient in the wrong place or a dropped term
+  breaks this on both the wide and the tall path.
+* Codec with one element per block: m / s' = +-1 are the forced end entries, so the
+  codes are lossless and the quantized buffer follows Muon's plain momentum recursion.
+* Codec against the Gefen step oracle: both compute the same momentum, scale and codes
+  (the step's codes are pinned separately).
+* Whole step with lossless codes against torch.optim.Muon (CPU), within bfloat16
+  rounding of the orthogonalised update.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+
+
+def test_bf16_rounding_matches_torch():
+    rng = np.random.default_rng(0)
+    x = np.concatenate([rng.standard_normal(20000) * 10.0 ** rng.uniform(-8, 8, 20000),
+                        [0.0, -0.0, 1.0, 1.00390625, 1.01171875, -1.00390625, 65504.0, 1e-40]])
+    x32 = x.astype(np.float32)
+    ref = torch.from_numpy(x32).to(torch.bfloat16).float().numpy().astype(np.float64)
+    np.testing.assert_array_equal(oracle.to_bf16(x32.astype(np.float64)), ref)
+
+
+def _svd_closed_form(x, steps, coeffs):
+    a, b, c = coeffs
+    u, sv, vt = np.linalg.svd(x, full_matrices=False)
+    s = sv / np.sqrt(np.sum(x * x))
+    for _ in range(steps):
+        s = a * s + b * s ** 3 + c * s ** 5
+    return (u * s) @ vt
+
+
+@pytest.mark.parametrize("rows,cols", [(8, 24), (24, 8), (16, 16), (1, 40), (40, 1), (33, 65)])
+def test_newton_schulz_float64_is_the_singular_value_polynomial(rows, cols):
+    rng = np.random.default_rng(rows * 100 + cols)
+    x = rng.standard_normal((rows, cols)) * rng.uniform(0.1, 3.0, (rows, 1))
+    for steps in (1, 2, 5):
+        got = oracle.newton_schulz(x, rows, cols, steps=steps, bf16=False)
+        ref = _svd_closed_form(x, steps, oracle.MUON_NS_COEFFS)
+        np.testing.assert_allclose(got, ref, rtol=0, atol=1e-12 * max(1.0, np.abs(ref).max()))
+
+
+def test_newton_schulz_bf16_stays_near_float64():
+    rng = np.random.default_rng(7)
+    rows, cols = 48, 96
+    x = rng.standard_normal((rows, cols))
+    o64 = oracle.newton_schulz(x, rows, cols, bf16=False)
+    o16 = oracle.newton_schulz(x, rows, cols, bf16=True)
+    assert np.all(o16 == oracle.to_bf16(o16))                 # results are bfloat16 values
+    assert np.abs(o16 - o64).max() < 0.05 * np.abs(o64).max()
+
+
+def test_newton_schulz_zero_matrix():
+    o = oracle.newton_schulz(np.zeros(12), 3, 4)
+    assert np.all(o == 0)
+
+
+def _lossless_codebook(k=256):
+    cb = np.linspace(-1.0, 1.0, k)
+    return cb
+
+
+@pytest.mark.parametrize("nesterov", [False, True])
+def test_codec_block_size_one_is_muon_momentum(nesterov):
+    """p = 1: every m / s' is +-1, so the stored buffer is exact and u follows Muon."""
+    rng = np.random.default_rng(3)
+    n, mu = 500, 0.95
+    cb = _lossless_codebook()
+    codes = np.zeros(n, dtype=np.uint8)
+    s = np.zeros(n, dtype=np.float64)
+    offs = np.arange(n + 1, dtype=np.int64)
+    buf = np.zeros(n)
+    for t in range(6):
+        g = rng.standard_normal(n).astype(np.float32)
+        gd = g.astype(np.float64)
+        u = oracle.muon_codec_blocks(g, codes, s, offs, cb, cb, mu, nesterov)
+        buf = mu * buf + (1.0 - mu) * gd
+        ref = (1.0 - mu) * gd + mu * buf if nesterov else buf
+        np.testing.assert_allclose(u, ref, rtol=1e-13, atol=1e-300)
+        np.testing.assert_allclose(s, np.abs(buf), rtol=1e-13)
+        assert set(np.unique(codes)) <= {0, 255}
+
+
+def test_codec_matches_the_step_oracle():
+    """Same momentum, scale and codes as the Gefen step with beta1 = mu."""
+    rng = np.random.default_rng(4)
+    p, nb, mu = 64, 30, 0.9
+    n = p * nb
+    offs = np.arange(0, n + 1, p, dtype=np.int64)
+    h = np.zeros(4096, dtype=np.uint64)
+    g0 = (rng.standard_normal(n) * np.repeat(np.exp(rng.uniform(-5, 0, nb)), p)).astype(np.float32)
+    oracle.histogram_blocks(g0, offs, 4096, h)
+    cb, _, _, _ = oracle.dp_codebook(h, 256)
+    c1 = np.zeros(n, dtype=np.uint8)
+    s1 = np.zeros(nb)
+    c2 = c1.copy()
+    s2 = s1.copy()
+    v2 = np.zeros(nb)
+    for t in range(1, 4):
+        g = (rng.standard_normal(n) * np.repeat(np.exp(rng.uniform(-5, 0, nb)), p)).astype(np.float32)
+        u = oracle.muon_codec_blocks(g, c1, s1, offs, cb, cb, mu, nesterov=False)
+        m = np.zeros(n)
+        oracle.step_blocks(np.zeros(n), g, c2, s2, v2, offs, cb, cb, 1e-3, mu, 0.999, 1e-8, 0.0,
+                           t, m_out=m)
+        np.testing.assert_array_equal(c1, c2)
+        np.testing.assert_array_equal(s1, s2)
+        np.testing.assert_array_equal(u, m)
+
+
+@pytest.mark.parametrize("rows,cols", [(32, 48), (48, 32)])
+def test_lossless_step_matches_torch_muon(rows, cols):
+    """Block size 1 with nesterov: Gefen-Muon is Muon; compare with torch.optim.Muon on
+    the CPU over three steps, within bfloat16 rounding of the orthogonalised update."""
+    rng = np.random.default_rng(rows)
+    n = rows * cols
+    lr, mu, wd = 0.02, 0.95, 0.01
+    theta0 = rng.standard_normal(n) * 0.02
+    theta = theta0.copy()
+    p_ref = torch.nn.Parameter(torch.tensor(theta0.reshape(rows, cols), dtype=torch.float32))
+    opt = torch.optim.Muon([p_ref], lr=lr, momentum=mu, weight_decay=wd, nesterov=True)
+    cb = _lossless_codebook()
+    codes = np.zeros(n, dtype=np.uint8)
+    s = np.zeros(n)
+    offs = np.arange(n + 1, dtype=np.int64)
+    scale = lr * oracle.muon_lr_scale(rows, cols)
+    for _ in range(3):
+        g = rng.standard_normal(n).astype(np.float32)
+        oracle.muon_step(theta, g, codes, s, offs, rows, cols, cb, cb, lr, mu, wd, nesterov=True)
+        p_ref.grad = torch.from_numpy(g.reshape(rows, cols).copy())
+        opt.step()
+    ref = p_ref.detach().double().numpy().reshape(-1)
+    # each step's update is lr * scale * O with |O| <= ~1.2; the two bfloat16 pipelines
+    # round differently (accumulation order and width), measured up to 0.8 % of one step
+    assert np.abs(theta - ref).max() < 0.02 * scale
+    assert np.abs(theta - theta0).max() > 10 * np.abs(theta - ref).max()
