@@ -178,7 +178,9 @@ int gefen_get_layout(const gefen_state* st, int64_t* code_offsets, int64_t* bloc
 /* Copy state arrays to `dst` (host or device memory; stream-ordered). which:
  * 0 = codes (uint8[total_code_bytes]), 1 = scales (float[total_blocks]),
  * 2 = second moments (float[total_blocks]), 3 = decode codebook (float[k]),
- * 4 = encode codebook (float[k]), 5 = decode codebook in double (double[k]).
+ * 4 = encode codebook (float[k]), 5 = decode codebook in double (double[k]),
+ * 6 = the Gefen-Muon bfloat16 momentum matrix (uint16[code index count], after
+ * gefen_muon_init; read-only, as is 5).
  * `bytes` must equal the array size. Synchronises `stream` when dst is host memory. */
 int gefen_read_state(const gefen_state* st, int32_t which, void* dst, int64_t bytes,
                      void* stream);
@@ -226,6 +228,45 @@ int gefen_profile_begin(gefen_state* st, int32_t max_steps);
 int gefen_profile_end(gefen_state* st, int32_t cap, int32_t* n_classes, int32_t* kind,
                       int32_t* vpl, int32_t* threads, int32_t* gdtype, int64_t* launches,
                       double* total_ms, int64_t* elems_per_launch, int64_t* bytes_per_launch);
+
+/* ------------------------------------------------------------------------------
+ * Gefen-Muon (appendix "Gefen-Muon"): Muon's momentum buffer held in Gefen's quantized
+ * form (the state's codes, per-block scales and codebooks; its second moments are not
+ * used), followed by Muon's Newton-Schulz orthogonalisation of each matrix.
+ *
+ * gefen_muon_init -- prepare a state made by gefen_init (same tensors, its inferred or
+ * explicit blocks) for gefen_muon_step.
+ *  rows    host int64[n_tensors]: tensor i is the rows[i] x (numel_i / rows[i]) matrix,
+ *          row-major (a 1-D tensor is 1 x numel). rows[i] must divide numel_i.
+ * Allocates the bfloat16 momentum matrix (2 bytes per parameter), the Newton-Schulz
+ * buffers for the largest group of equal-shape tensors, and a rocBLAS handle whose
+ * workspace is sized here; synchronises `stream`. Call once per state.
+ * Errors: EINVAL (NULL, count mismatch, rows, second call), ENOMEM, EHIP.
+ * ---------------------------------------------------------------------------- */
+int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, void* stream);
+
+/* ------------------------------------------------------------------------------
+ * gefen_muon_step -- one Gefen-Muon step. Per block B of the quantized buffer:
+ *   m_i = mu * c_dec[q_i] * s_B + (1 - mu) * g_i;  s_B' = max_B |m_i|;
+ *   q_i' = nearest entry of c_enc to m_i / s_B'   (ties to the lower index)
+ * per tensor (a rows x cols matrix):
+ *   U = nesterov ? (1 - mu) * G + mu * M : M, rounded to bfloat16
+ *   X = bf16(U / max(bf16(||U||_F), bf16(ns_eps))), transposed if rows > cols
+ *   ns_steps times: A = X X^T; B = ns_b A + ns_c A A; X = ns_a X + B X
+ *       (bfloat16 matrices, float32 accumulation, as Muon's PyTorch implementation)
+ *   theta = theta * (1 - lr * weight_decay) - lr * sqrt(max(1, rows / cols)) * X^(T)
+ *  params, grads  as for gefen_step; momentum in [0, 1); ns_steps in [0, 100];
+ *  ns_eps > 0. Muon's defaults: ns_steps 5, (ns_a, ns_b, ns_c) =
+ *  (3.4445, -4.7750, 2.0315), ns_eps 1e-7, nesterov 1.
+ * Asynchronous on `stream`; no allocation. Refits (gefen_fit_codebook) apply as for
+ * gefen_step. The bfloat16 momentum matrix of the last step can be read as array 6 of
+ * gefen_read_state (uint16 bit patterns at each element's code index).
+ * Errors: EINVAL (arguments, gefen_muon_init not called), EDTYPE, EHIP.
+ * ---------------------------------------------------------------------------- */
+int gefen_muon_step(gefen_state* st, const gefen_tensor* params, const gefen_tensor* grads,
+                    int32_t n_tensors, double lr, double momentum, double weight_decay,
+                    int32_t nesterov, int32_t ns_steps, double ns_a, double ns_b, double ns_c,
+                    double ns_eps, void* stream);
 
 /* Free the state and every device buffer it owns. NULL is a no-op. */
 void gefen_destroy(gefen_state* st);

@@ -33,7 +33,8 @@ SYMBOLS = [
     "gefen_histogram", "gefen_dp_codebook", "gefen_get_periods", "gefen_get_layout",
     "gefen_read_state", "gefen_write_state", "gefen_get_fit_info", "gefen_state_bytes",
     "gefen_checkpoint_bytes", "gefen_export", "gefen_import", "gefen_profile_begin",
-    "gefen_profile_end", "gefen_destroy", "gefen_last_error",
+    "gefen_profile_end", "gefen_destroy", "gefen_last_error", "gefen_muon_init",
+    "gefen_muon_step",
 ]
 
 
@@ -87,6 +88,9 @@ def load_library(path: str = LIB_PATH):
     lib.gefen_import.argtypes = [vp, vp, i64, vp]
     lib.gefen_profile_begin.argtypes = [vp, i32]
     lib.gefen_profile_end.argtypes = [vp, i32, P(i32), vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.gefen_muon_init.argtypes = [vp, vp, i32, vp]
+    lib.gefen_muon_step.argtypes = [vp, P(gefen_tensor), P(gefen_tensor), i32, f64, f64, f64,
+                                    i32, i32, f64, f64, f64, f64, vp]
     lib.gefen_destroy.argtypes = [vp]
     lib.gefen_destroy.restype = None
     lib.gefen_last_error.argtypes = []
@@ -145,6 +149,8 @@ def _i64_array(vals):
 
 
 STATE_CODES, STATE_SCALE, STATE_V, STATE_CB_DEC, STATE_CB_ENC, STATE_CB_DEC64 = range(6)
+STATE_MUON_U = 6          # Gefen-Muon bfloat16 momentum matrix (after muon_init)
+MUON_NS_COEFFS = (3.4445, -4.7750, 2.0315)
 
 
 class GefenState:
@@ -193,6 +199,22 @@ class GefenState:
                                float(betas[1]), float(eps), float(weight_decay), int(t),
                                _stream(stream)))
 
+    def muon_init(self, rows: Sequence[int], stream=None):
+        """Prepare Gefen-Muon steps; tensor i is rows[i] x (numel / rows[i])."""
+        a = (ctypes.c_int64 * self._n)(*[int(r) for r in rows])
+        _check(_lib.gefen_muon_init(self._h, a, self._n, _stream(stream)))
+
+    def muon_step(self, params: Sequence, grads: Sequence, lr: float, momentum: float = 0.95,
+                  weight_decay: float = 0.0, nesterov: bool = True, ns_steps: int = 5,
+                  ns_coefficients=MUON_NS_COEFFS, ns_eps: float = 1e-7, stream=None):
+        pt = _tensors(params, "params")
+        gt = _tensors(grads, "grads")
+        a, b, c = ns_coefficients
+        _check(_lib.gefen_muon_step(self._h, pt, gt, self._n, float(lr), float(momentum),
+                                    float(weight_decay), int(bool(nesterov)), int(ns_steps),
+                                    float(a), float(b), float(c), float(ns_eps),
+                                    _stream(stream)))
+
     def fit_codebook(self, grads: Sequence, stream=None):
         _check(_lib.gefen_fit_codebook(self._h, _tensors(grads, "grads"), self._n,
                                        _stream(stream)))
@@ -233,7 +255,8 @@ class GefenState:
                 STATE_V: (torch.float32, lay["total_blocks"]),
                 STATE_CB_DEC: (torch.float32, lay["k"]),
                 STATE_CB_ENC: (torch.float32, lay["k"]),
-                STATE_CB_DEC64: (torch.float64, lay["k"])}[which]
+                STATE_CB_DEC64: (torch.float64, lay["k"]),
+                STATE_MUON_U: (torch.int16, lay["code_offsets"][-1])}[which]
         dev = device if device is not None else torch.device("cuda", torch.cuda.current_device())
         out = torch.empty(spec[1], dtype=spec[0], device=dev)
         nbytes = out.numel() * out.element_size()

@@ -4,6 +4,8 @@
 #include "gefen.h"
 #include "gefen_internal.h"
 
+#include <rocblas/rocblas.h>
+
 #include <algorithm>
 #include <cstdlib>
 #include <memory>
@@ -124,6 +126,26 @@ struct gefen_state {
     int64_t persistent_bytes = 0, workspace_bytes = 0;
     std::vector<void*> dev_allocs;
 
+    // Gefen-Muon (gefen_muon_init): codec tiles over every block, the bfloat16 momentum
+    // matrix per code index, tensors grouped by shape for batched Newton-Schulz GEMMs.
+    struct MuonGroup {
+        int64_t rows, cols;
+        int32_t first, count;   // muon_tensor_of[first .. first + count)
+    };
+    bool muon_ready = false;
+    Tile* muon_tiles = nullptr;
+    int64_t muon_n_tiles = 0;
+    int64_t* muon_tile_first = nullptr;   // n_tensors + 1
+    float* muon_tile_ss = nullptr;
+    float* muon_norm = nullptr;
+    uint16_t* muon_u = nullptr;
+    int32_t* muon_tensor_of = nullptr;
+    std::vector<MuonGroup> muon_groups;
+    uint16_t* muon_x[2] = {nullptr, nullptr};
+    uint16_t* muon_a = nullptr;
+    uint16_t* muon_b = nullptr;
+    rocblas_handle blas = nullptr;
+
     // measurement: events[(step * classes + c) * 2 + {0 start, 1 stop}]
     bool prof_armed = false;
     int32_t prof_max_steps = 0, prof_steps = 0;
@@ -140,6 +162,7 @@ struct gefen_state {
     ~gefen_state()
     {
         prof_free();
+        if (blas) (void)rocblas_destroy_handle(blas);
         for (void* p : dev_allocs) (void)hipFree(p);
         if (segs_pinned) (void)hipHostFree(segs_pinned);
         for (hipEvent_t e : seg_evt)
@@ -1056,6 +1079,11 @@ static int state_array(const gefen_state* st, int32_t which, void** ptr, int64_t
     case 3: *ptr = st->cb32[st->dec_slot]; *bytes = 4 * st->k; return GEFEN_OK;
     case 4: *ptr = st->cb32[st->enc_slot]; *bytes = 4 * st->k; return GEFEN_OK;
     case 5: *ptr = st->cb64[st->dec_slot]; *bytes = 8 * st->k; return GEFEN_OK;
+    case 6:
+        if (!st->muon_ready) return fail(GEFEN_EINVAL, "array 6 needs gefen_muon_init");
+        *ptr = st->muon_u;
+        *bytes = 2 * st->code_off[st->n_tensors];
+        return GEFEN_OK;
     default: return fail(GEFEN_EINVAL, "unknown state array %d", which);
     }
 }
@@ -1079,7 +1107,7 @@ int gefen_write_state(gefen_state* st, int32_t which, const void* src, int64_t b
                       void* stream_)
 {
     if (!st || !src) return fail(GEFEN_EINVAL, "NULL argument");
-    if (which == 5) return fail(GEFEN_EINVAL, "array 5 is read-only");
+    if (which == 5 || which == 6) return fail(GEFEN_EINVAL, "array %d is read-only", which);
     void* dst;
     int64_t need;
     int rc = state_array(st, which, &dst, &need);
@@ -1244,5 +1272,219 @@ int gefen_profile_end(gefen_state* st, int32_t cap, int32_t* n_classes, int32_t*
 }
 
 void gefen_destroy(gefen_state* st) { delete st; }
+
+
+// ------------------------------------------------------------------ Gefen-Muon
+namespace {
+
+uint16_t host_bf16(float x)
+{
+    uint32_t b;
+    std::memcpy(&b, &x, 4);
+    return static_cast<uint16_t>((b + 0x7FFFu + ((b >> 16) & 1u)) >> 16);
+}
+
+float host_bf16_value(float x)
+{
+    const uint32_t b = static_cast<uint32_t>(host_bf16(x)) << 16;
+    float f;
+    std::memcpy(&f, &b, 4);
+    return f;
+}
+
+#define GEFEN_BLAS(call)                                                                 \
+    do {                                                                                 \
+        rocblas_status s_ = (call);                                                      \
+        if (s_ != rocblas_status_success)                                                \
+            return fail(GEFEN_EHIP, "%s failed: %s", #call, rocblas_status_to_string(s_)); \
+    } while (0)
+
+// One Newton-Schulz iteration on a batch of wide m x n row-major matrices (m <= n):
+// A = X X^T; B = b A + c A A; X' = a X + B X, all bfloat16 with float32 accumulation.
+// rocBLAS is column-major: the row-major m x n X is the column-major n x m X^T.
+int ns_iteration(gefen_state* st, const gefen_state::MuonGroup& g, const uint16_t* x,
+                 uint16_t* xo, float a, float b, float c)
+{
+    const int64_t m = std::min(g.rows, g.cols), n = std::max(g.rows, g.cols);
+    const rocblas_int mi = static_cast<rocblas_int>(m), ni = static_cast<rocblas_int>(n);
+    const rocblas_stride sx = m * n, sa = m * m;
+    const float one = 1.0f, zero = 0.0f;
+    const rocblas_datatype bf = rocblas_datatype_bf16_r, f32 = rocblas_datatype_f32_r;
+    GEFEN_BLAS(rocblas_gemm_strided_batched_ex(
+        st->blas, rocblas_operation_transpose, rocblas_operation_none, mi, mi, ni, &one, x, bf,
+        ni, sx, x, bf, ni, sx, &zero, st->muon_a, bf, mi, sa, st->muon_a, bf, mi, sa, g.count,
+        f32, rocblas_gemm_algo_standard, 0, 0));
+    GEFEN_BLAS(rocblas_gemm_strided_batched_ex(
+        st->blas, rocblas_operation_none, rocblas_operation_none, mi, mi, mi, &c, st->muon_a, bf,
+        mi, sa, st->muon_a, bf, mi, sa, &b, st->muon_a, bf, mi, sa, st->muon_b, bf, mi, sa,
+        g.count, f32, rocblas_gemm_algo_standard, 0, 0));
+    GEFEN_BLAS(rocblas_gemm_strided_batched_ex(
+        st->blas, rocblas_operation_none, rocblas_operation_none, ni, mi, mi, &one, x, bf, ni, sx,
+        st->muon_b, bf, mi, sa, &a, x, bf, ni, sx, xo, bf, ni, sx, g.count, f32,
+        rocblas_gemm_algo_standard, 0, 0));
+    return GEFEN_OK;
+}
+
+}  // namespace
+
+int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, void* stream_)
+{
+    if (!st || !rows) return fail(GEFEN_EINVAL, "NULL argument");
+    if (n_tensors != st->n_tensors)
+        return fail(GEFEN_EINVAL, "n_tensors = %d, state has %d", n_tensors, st->n_tensors);
+    if (st->muon_ready) return fail(GEFEN_EINVAL, "gefen_muon_init was already called");
+    const int32_t n = n_tensors;
+    for (int32_t t = 0; t < n; ++t)
+        if (rows[t] < 1 || st->numel[t] % rows[t] != 0)
+            return fail(GEFEN_EINVAL, "rows[%d] = %lld does not divide numel %lld", t,
+                        (long long)rows[t], (long long)st->numel[t]);
+    hipStream_t stream = as_stream(stream_);
+
+    // block starts on the host (explicit blocks: from the device table)
+    std::vector<int64_t> csr_host;
+    if (st->explicit_blocks) {
+        csr_host.resize(static_cast<size_t>(st->total_blocks + n));
+        GEFEN_HIP(hipMemcpy(csr_host.data(), st->csr, 8 * csr_host.size(), hipMemcpyDeviceToHost));
+    }
+    // codec tiles: mode 1 (lane per block) for blocks of <= 32 elements, mode 2 (wave per
+    // block, up to 4) for <= 2048, else mode 0 (the workgroup on one block)
+    std::vector<Tile> tiles;
+    std::vector<int64_t> tile_first(n + 1, 0);
+    int64_t csr_base = 0;
+    for (int32_t t = 0; t < n; ++t) {
+        tile_first[t] = static_cast<int64_t>(tiles.size());
+        const int64_t nb = st->blk_begin[t + 1] - st->blk_begin[t];
+        const int64_t bb = st->blk_begin[t];
+        auto start = [&](int64_t b) {
+            return st->explicit_blocks ? csr_host[csr_base + b] : b * st->period[t];
+        };
+        auto mode_of = [](int64_t len) { return len <= kSmallBlock ? 1 : (len <= 2048 ? 2 : 0); };
+        int64_t b = 0;
+        while (b < nb) {
+            const int mode = mode_of(start(b + 1) - start(b));
+            const int cap = mode == 1 ? kThreads : (mode == 2 ? kThreads / 64 : 1);
+            Tile tl{};
+            tl.elem0 = start(b);
+            tl.blk0 = bb + b;
+            tl.seg = t;
+            int cnt = 0;
+            while (b < nb && cnt < cap && mode_of(start(b + 1) - start(b)) == mode) {
+                ++cnt;
+                ++b;
+            }
+            tl.nblk = static_cast<int16_t>(cnt);
+            tl.nelem = start(b) - tl.elem0;
+            tl.vpl = static_cast<uint8_t>(mode);
+            tiles.push_back(tl);
+        }
+        if (st->explicit_blocks) csr_base += nb + 1;
+    }
+    tile_first[n] = static_cast<int64_t>(tiles.size());
+
+    // shape groups, in order of first appearance
+    std::vector<int32_t> order;
+    st->muon_groups.clear();
+    for (int32_t t = 0; t < n; ++t) {
+        const int64_t R = rows[t], C = st->numel[t] / rows[t];
+        bool found = false;
+        for (const auto& g : st->muon_groups) found = found || (g.rows == R && g.cols == C);
+        if (found) continue;
+        gefen_state::MuonGroup g{R, C, static_cast<int32_t>(order.size()), 0};
+        for (int32_t u = t; u < n; ++u)
+            if (rows[u] == R && st->numel[u] / rows[u] == C) {
+                order.push_back(u);
+                ++g.count;
+            }
+        st->muon_groups.push_back(g);
+    }
+    int64_t max_x = 0, max_a = 0;
+    for (const auto& g : st->muon_groups) {
+        const int64_t m = std::min(g.rows, g.cols);
+        if (std::max(g.rows, g.cols) > 0x7fffffffLL)
+            return fail(GEFEN_EINVAL, "a matrix side exceeds 2^31 - 1");
+        max_x = std::max(max_x, g.count * g.rows * g.cols);
+        max_a = std::max(max_a, g.count * m * m);
+    }
+
+    int rc;
+    st->muon_n_tiles = static_cast<int64_t>(tiles.size());
+    if ((rc = st->alloc(&st->muon_tiles, sizeof(Tile) * tiles.size(), false))) return rc;
+    if ((rc = st->alloc(&st->muon_tile_first, 8 * tile_first.size(), false))) return rc;
+    if ((rc = st->alloc(&st->muon_tile_ss, 4 * tiles.size(), false))) return rc;
+    if ((rc = st->alloc(&st->muon_norm, 4 * static_cast<size_t>(n), false))) return rc;
+    if ((rc = st->alloc(&st->muon_tensor_of, 4 * order.size(), false))) return rc;
+    if ((rc = st->alloc(&st->muon_u, 2 * static_cast<size_t>(st->code_off[n]), false))) return rc;
+    for (auto& x : st->muon_x)
+        if ((rc = st->alloc(&x, 2 * static_cast<size_t>(max_x), false))) return rc;
+    if ((rc = st->alloc(&st->muon_a, 2 * static_cast<size_t>(max_a), false))) return rc;
+    if ((rc = st->alloc(&st->muon_b, 2 * static_cast<size_t>(max_a), false))) return rc;
+    GEFEN_HIP(hipMemcpy(st->muon_tiles, tiles.data(), sizeof(Tile) * tiles.size(), hipMemcpyHostToDevice));
+    GEFEN_HIP(hipMemcpy(st->muon_tile_first, tile_first.data(), 8 * tile_first.size(), hipMemcpyHostToDevice));
+    GEFEN_HIP(hipMemcpy(st->muon_tensor_of, order.data(), 4 * order.size(), hipMemcpyHostToDevice));
+
+    // rocBLAS handle with its workspace sized now, so that steps allocate nothing
+    GEFEN_BLAS(rocblas_create_handle(&st->blas));
+    GEFEN_BLAS(rocblas_set_stream(st->blas, stream));
+    GEFEN_BLAS(rocblas_start_device_memory_size_query(st->blas));
+    for (const auto& g : st->muon_groups)
+        if ((rc = ns_iteration(st, g, st->muon_x[0], st->muon_x[1], 1.0f, 1.0f, 1.0f))) {
+            size_t ignored;
+            (void)rocblas_stop_device_memory_size_query(st->blas, &ignored);
+            return rc;
+        }
+    size_t blas_bytes = 0;
+    GEFEN_BLAS(rocblas_stop_device_memory_size_query(st->blas, &blas_bytes));
+    if (blas_bytes) GEFEN_BLAS(rocblas_set_device_memory_size(st->blas, blas_bytes));
+    st->workspace_bytes += static_cast<int64_t>(blas_bytes);
+    GEFEN_HIP(hipStreamSynchronize(stream));
+    st->muon_ready = true;
+    return GEFEN_OK;
+}
+
+int gefen_muon_step(gefen_state* st, const gefen_tensor* params, const gefen_tensor* grads,
+                    int32_t n_tensors, double lr, double momentum, double weight_decay,
+                    int32_t nesterov, int32_t ns_steps, double ns_a, double ns_b, double ns_c,
+                    double ns_eps, void* stream_)
+{
+    int rc = check_against_state(st, params, n_tensors, true, "params");
+    if (rc) return rc;
+    if ((rc = check_against_state(st, grads, n_tensors, false, "grads"))) return rc;
+    if (!st->muon_ready) return fail(GEFEN_EINVAL, "call gefen_muon_init first");
+    if (!(momentum >= 0.0 && momentum < 1.0)) return fail(GEFEN_EINVAL, "momentum must be in [0, 1)");
+    if (!finite_f(lr) || !finite_f(weight_decay)) return fail(GEFEN_EINVAL, "lr and weight_decay must be finite");
+    if (ns_steps < 0 || ns_steps > 100) return fail(GEFEN_EINVAL, "ns_steps must be in [0, 100]");
+    if (!finite_f(ns_a) || !finite_f(ns_b) || !finite_f(ns_c))
+        return fail(GEFEN_EINVAL, "Newton-Schulz coefficients must be finite");
+    if (!finite_f(ns_eps) || ns_eps <= 0.0) return fail(GEFEN_EINVAL, "ns_eps must be finite and > 0");
+    hipStream_t stream = as_stream(stream_);
+    if ((rc = refresh_segs(st, params, grads, stream))) return rc;
+    GEFEN_BLAS(rocblas_set_stream(st->blas, stream));
+
+    GEFEN_HIP(launch_muon_codec(st->code_bits, st->muon_tiles, st->muon_n_tiles, st->segs,
+                                st->codes, st->scale, codebook_dev(st),
+                                static_cast<float>(momentum), static_cast<float>(1.0 - momentum),
+                                nesterov ? 1 : 0, st->muon_u, st->muon_tile_ss, stream));
+    GEFEN_HIP(launch_muon_norm(st->muon_tile_ss, st->muon_tile_first, st->n_tensors,
+                               host_bf16_value(static_cast<float>(ns_eps)), st->muon_norm, stream));
+    const float decay = static_cast<float>(1.0 - lr * weight_decay);
+    for (const auto& g : st->muon_groups) {
+        GEFEN_HIP(launch_muon_prep(st->muon_u, st->segs, st->muon_tensor_of + g.first, g.count,
+                                   st->muon_norm, g.rows, g.cols, st->muon_x[0], stream));
+        int cur = 0;
+        for (int32_t it = 0; it < ns_steps; ++it) {
+            if ((rc = ns_iteration(st, g, st->muon_x[cur], st->muon_x[1 - cur],
+                                   static_cast<float>(ns_a), static_cast<float>(ns_b),
+                                   static_cast<float>(ns_c))))
+                return rc;
+            cur ^= 1;
+        }
+        const double scale = std::sqrt(std::max(1.0, static_cast<double>(g.rows) / g.cols));
+        GEFEN_HIP(launch_muon_update(st->muon_x[cur], st->segs, st->muon_tensor_of + g.first,
+                                     g.count, g.rows, g.cols, decay,
+                                     static_cast<float>(lr * scale), stream));
+    }
+    st->dec_slot = st->enc_slot;
+    return GEFEN_OK;
+}
 
 }  // extern "C"

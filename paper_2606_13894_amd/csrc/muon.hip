@@ -1,0 +1,160 @@
+// Gefen-Muon (appendix "Gefen-Muon"), the parts around the orthogonalisation: the
+// Frobenius norm of each momentum matrix, its normalised bfloat16 copy in the wide
+// orientation (the Newton-Schulz input), and the parameter update from the result.
+// The momentum codec itself lives with the step kernels; the Newton-Schulz matrix
+// products are plain bfloat16 GEMMs (rocBLAS), driven from the host.
+#include "gefen_internal.h"
+
+namespace gefen {
+namespace {
+
+__device__ __forceinline__ float bf16_val(uint16_t b)
+{
+    return __uint_as_float(static_cast<uint32_t>(b) << 16);
+}
+
+__device__ __forceinline__ uint16_t to_bf16(float x)
+{
+    const uint32_t b = __float_as_uint(x);
+    return static_cast<uint16_t>((b + 0x7FFFu + ((b >> 16) & 1u)) >> 16);
+}
+
+// One workgroup per tensor: norm = bf16(sqrt(sum of its tiles' u^2)), clamped below by
+// bf16(eps), summed in a fixed order (float64).
+__global__ __launch_bounds__(256) void k_muon_norm(const float* __restrict__ tile_ss,
+                                                   const int64_t* __restrict__ tile_first,
+                                                   float eps_bf16, float* __restrict__ norm)
+{
+    __shared__ double red[256];
+    const int t = blockIdx.x;
+    const int64_t a = tile_first[t], b = tile_first[t + 1];
+    double acc = 0.0;
+    for (int64_t i = a + threadIdx.x; i < b; i += 256) acc += static_cast<double>(tile_ss[i]);
+    red[threadIdx.x] = acc;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+        if (static_cast<int>(threadIdx.x) < w) red[threadIdx.x] += red[threadIdx.x + w];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        const float nv = bf16_val(to_bf16(static_cast<float>(sqrt(red[0]))));
+        norm[t] = fmaxf(nv, eps_bf16);
+    }
+}
+
+constexpr int kT = 64;   // transpose tile edge
+
+// X[batch] (m x n row-major, m = min(R, C)) = bf16(U_t / norm_t), with U_t the tensor's
+// R x C momentum matrix; transposed when R > C. 64 x 64 tiles through LDS so both the
+// read and the write are coalesced.
+__global__ __launch_bounds__(256) void k_muon_prep(const uint16_t* __restrict__ u,
+                                                   const Seg* __restrict__ segs,
+                                                   const int32_t* __restrict__ tensor_of,
+                                                   const float* __restrict__ norm, int64_t R,
+                                                   int64_t C, int transposed,
+                                                   uint16_t* __restrict__ x)
+{
+    __shared__ uint16_t tile[kT][kT + 2];
+    const int b = blockIdx.z;
+    const int t = tensor_of[b];
+    const uint16_t* __restrict__ src = u + segs[t].code_off;
+    uint16_t* __restrict__ dst = x + static_cast<int64_t>(b) * R * C;
+    const float nrm = norm[t];
+    const int64_t r0 = static_cast<int64_t>(blockIdx.y) * kT;
+    const int64_t c0 = static_cast<int64_t>(blockIdx.x) * kT;
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+    for (int i = ty; i < kT; i += 4) {
+        const int64_t r = r0 + i, c = c0 + tx;
+        uint16_t v = 0;
+        if (r < R && c < C) v = to_bf16(bf16_val(src[r * C + c]) / nrm);
+        tile[i][tx] = v;
+    }
+    __syncthreads();
+    if (!transposed) {
+        for (int i = ty; i < kT; i += 4) {
+            const int64_t r = r0 + i, c = c0 + tx;
+            if (r < R && c < C) dst[r * C + c] = tile[i][tx];
+        }
+    } else {
+        // X is C x R: X[c][r] = U[r][c]
+        for (int i = ty; i < kT; i += 4) {
+            const int64_t c = c0 + i, r = r0 + tx;
+            if (r < R && c < C) dst[c * R + r] = tile[tx][i];
+        }
+    }
+}
+
+// theta_t (R x C) = theta_t * decay - step * O, O the orthogonalised matrix of batch
+// entry b (m x n row-major, transposed back when R > C).
+__global__ __launch_bounds__(256) void k_muon_update(const uint16_t* __restrict__ o,
+                                                     const Seg* __restrict__ segs,
+                                                     const int32_t* __restrict__ tensor_of,
+                                                     int64_t R, int64_t C, int transposed,
+                                                     float decay, float step)
+{
+    __shared__ uint16_t tile[kT][kT + 2];
+    const int b = blockIdx.z;
+    const int t = tensor_of[b];
+    float* __restrict__ th = segs[t].theta;
+    const uint16_t* __restrict__ src = o + static_cast<int64_t>(b) * R * C;
+    const int64_t r0 = static_cast<int64_t>(blockIdx.y) * kT;
+    const int64_t c0 = static_cast<int64_t>(blockIdx.x) * kT;
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+    if (transposed) {
+        // O is C x R: stage O[c0 .. c0 + 64)[r0 .. r0 + 64) with coalesced reads along r
+        for (int i = ty; i < kT; i += 4) {
+            const int64_t c = c0 + i, r = r0 + tx;
+            tile[i][tx] = (r < R && c < C) ? src[c * R + r] : 0;
+        }
+        __syncthreads();
+    }
+    for (int i = ty; i < kT; i += 4) {
+        const int64_t r = r0 + i, c = c0 + tx;
+        if (r < R && c < C) {
+            const uint16_t ob = transposed ? tile[tx][i] : src[r * C + c];
+            const int64_t e = r * C + c;
+            th[e] = fmaf(-step, bf16_val(ob), th[e] * decay);
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_muon_norm(const float* tile_ss, const int64_t* tile_first, int32_t n_tensors,
+                            float eps_bf16, float* norm, hipStream_t stream)
+{
+    if (n_tensors <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_muon_norm, dim3(n_tensors), dim3(256), 0, stream, tile_ss, tile_first,
+                       eps_bf16, norm);
+    return hipGetLastError();
+}
+
+static dim3 tile_grid(int64_t R, int64_t C, int batch)
+{
+    return dim3(static_cast<unsigned>((C + kT - 1) / kT), static_cast<unsigned>((R + kT - 1) / kT),
+                static_cast<unsigned>(batch));
+}
+
+hipError_t launch_muon_prep(const uint16_t* u, const Seg* segs, const int32_t* tensor_of,
+                            int32_t batch, const float* norm, int64_t R, int64_t C,
+                            uint16_t* x, hipStream_t stream)
+{
+    if (batch <= 0) return hipSuccess;
+    if ((R + kT - 1) / kT > 65535 || batch > 65535) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_muon_prep, tile_grid(R, C, batch), dim3(256), 0, stream, u, segs,
+                       tensor_of, norm, R, C, R > C ? 1 : 0, x);
+    return hipGetLastError();
+}
+
+hipError_t launch_muon_update(const uint16_t* o, const Seg* segs, const int32_t* tensor_of,
+                              int32_t batch, int64_t R, int64_t C, float decay, float step,
+                              hipStream_t stream)
+{
+    if (batch <= 0) return hipSuccess;
+    if ((R + kT - 1) / kT > 65535 || batch > 65535) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_muon_update, tile_grid(R, C, batch), dim3(256), 0, stream, o, segs,
+                       tensor_of, R, C, R > C ? 1 : 0, decay, step);
+    return hipGetLastError();
+}
+
+}  // namespace gefen

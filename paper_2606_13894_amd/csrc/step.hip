@@ -821,6 +821,137 @@ hipError_t launch_u(int vpl, int bs, dim3 grid, const Tile* tiles, const Seg* se
     return hipErrorInvalidValue;
 }
 
+// ---------------------------------------------------------------------------------
+// Gefen-Muon codec (appendix "Gefen-Muon"): Muon's momentum held in Gefen's quantized
+// form. Per block: m = mu * c_dec[q] * s + (1 - mu) * g, s' = max |m|,
+// q' = nearest(c_enc, m / s'); the matrix handed to the orthogonalisation is
+// u = nesterov ? (1 - mu) * g + mu * m : m, written as bfloat16 at the code index of
+// each element, and each tile's sum of u^2 (of the bfloat16 values) goes to tile_ss.
+// Tile mode in Tile::vpl: 0 = the workgroup on one block, 1 = one lane per block,
+// 2 = one wave per block.
+// ---------------------------------------------------------------------------------
+__device__ __forceinline__ uint16_t bf16_rne(float x)
+{
+    const uint32_t b = __float_as_uint(x);
+    return static_cast<uint16_t>((b + 0x7FFFu + ((b >> 16) & 1u)) >> 16);
+}
+
+struct MuonOut {
+    uint16_t* u;
+    float mu, one_minus_mu;
+    int nesterov;
+};
+
+// Second pass over one block: encode, write u, return the block's sum of u^2.
+template <int CB>
+__device__ __forceinline__ float muon_block_out(const LdsTables& L, const Seg& sg,
+                                                uint8_t* __restrict__ codes, int64_t start,
+                                                int64_t len, int64_t i0, int64_t di,
+                                                float s_old, float s_new,
+                                                const StepScalars& sc, const MuonOut& mo,
+                                                float half_ng, int ng_m1)
+{
+    const float inv_s = s_new > 0.0f ? 1.0f / s_new : 0.0f;
+    const int64_t cj = sg.code_off + start;
+    float uss = 0.0f;
+    for (int64_t i = i0; i < len; i += di) {
+        const float g = load_grad(sg.grad, start + i, sg.gdtype);
+        const int q0 = code_ld<CB>(codes, cj + i);
+        const float mm = momentum(L, q0, s_old, g, sc);
+        const int q = s_new > 0.0f ? encode(L, mm * inv_s, half_ng, ng_m1) : 0;
+        code_st<CB>(codes, cj + i, q0, q);
+        const float uu = mo.nesterov ? fmaf(mo.mu, mm, mo.one_minus_mu * g) : mm;
+        const uint16_t ub = bf16_rne(uu);
+        mo.u[cj + i] = ub;
+        const float ur = __uint_as_float(static_cast<uint32_t>(ub) << 16);
+        uss = fmaf(ur, ur, uss);
+    }
+    return uss;
+}
+
+template <int CB>
+__global__ __launch_bounds__(kThreads) void k_muon_codec(const Tile* __restrict__ tiles,
+                                                         const Seg* __restrict__ segs,
+                                                         uint8_t* __restrict__ codes,
+                                                         float* __restrict__ scale,
+                                                         CodebookDev cbd, StepScalars sc,
+                                                         MuonOut mo, float* __restrict__ tile_ss)
+{
+    __shared__ LdsTables L;
+    const Tile tl = tiles[blockIdx.x];
+    const Seg sg = segs[tl.seg];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    load_tables<kThreads>(L, cbd);
+    __syncthreads();
+    const float half_ng = 0.5f * static_cast<float>(cbd.ng);
+    const int ng_m1 = cbd.ng - 1;
+    float uss = 0.0f;
+    if (tl.vpl == 0) {
+        int64_t start, len;
+        block_range(sg, tl, 0, start, len);
+        const float s_old = scale[tl.blk0];
+        const int64_t cj = sg.code_off + start;
+        float am = 0.0f;
+        for (int64_t i = tid; i < len; i += kThreads) {
+            const float g = load_grad(sg.grad, start + i, sg.gdtype);
+            am = fmaxf(am, fabsf(momentum(L, code_ld<CB>(codes, cj + i), s_old, g, sc)));
+        }
+        for (int off = 1; off < 64; off <<= 1) am = fmaxf(am, __shfl_xor(am, off));
+        if (lane == 0) L.red_am[wave] = am;
+        __syncthreads();
+        am = L.red_am[0];
+        for (int w = 1; w < kThreads / 64; ++w) am = fmaxf(am, L.red_am[w]);
+        __syncthreads();   // red_am is reused for the tile sum below
+        if (tid == 0) scale[tl.blk0] = am;
+        uss = muon_block_out<CB>(L, sg, codes, start, len, tid, kThreads, s_old, am, sc, mo,
+                                 half_ng, ng_m1);
+    } else if (tl.vpl == 1) {
+        if (tid < tl.nblk) {
+            int64_t start, len;
+            block_range(sg, tl, tid, start, len);
+            const int64_t blk = tl.blk0 + tid;
+            const float s_old = scale[blk];
+            const int64_t cj = sg.code_off + start;
+            float am = 0.0f;
+            for (int64_t i = 0; i < len; ++i) {
+                const float g = load_grad(sg.grad, start + i, sg.gdtype);
+                am = fmaxf(am, fabsf(momentum(L, code_ld<CB>(codes, cj + i), s_old, g, sc)));
+            }
+            scale[blk] = am;
+            uss = muon_block_out<CB>(L, sg, codes, start, len, 0, 1, s_old, am, sc, mo, half_ng,
+                                     ng_m1);
+        }
+    } else {
+        if (wave < tl.nblk) {
+            int64_t start, len;
+            block_range(sg, tl, wave, start, len);
+            const int64_t blk = tl.blk0 + wave;
+            const float s_old = scale[blk];
+            const int64_t cj = sg.code_off + start;
+            float am = 0.0f;
+            for (int64_t i = lane; i < len; i += 64) {
+                const float g = load_grad(sg.grad, start + i, sg.gdtype);
+                am = fmaxf(am, fabsf(momentum(L, code_ld<CB>(codes, cj + i), s_old, g, sc)));
+            }
+            for (int off = 1; off < 64; off <<= 1) am = fmaxf(am, __shfl_xor(am, off));
+            if (lane == 0) scale[blk] = am;
+            uss = muon_block_out<CB>(L, sg, codes, start, len, lane, 64, s_old, am, sc, mo,
+                                     half_ng, ng_m1);
+        }
+    }
+    // the tile's sum of u^2, fixed order
+    for (int off = 1; off < 64; off <<= 1) uss += __shfl_xor(uss, off);
+    if (lane == 0) L.red_ss[wave] = uss;
+    __syncthreads();
+    if (tid == 0) {
+        float t = L.red_ss[0];
+        for (int w = 1; w < kThreads / 64; ++w) t += L.red_ss[w];
+        tile_ss[blockIdx.x] = t;
+    }
+}
+
 template <int GDT, int CB>
 hipError_t launch_h(dim3 grid, const Tile* tiles, const HTile* htiles, const Seg* segs,
                     uint8_t* codes, float* scale, float* vmom, CodebookDev cb, StepScalars sc,
@@ -907,6 +1038,29 @@ hipError_t launch_step(int kind, int gdtype, int code_bits, int vpl, int bs, con
                                         sc, stream)
                : launch_kind<DT_BF16, 4>(kind, vpl, bs, grid, tiles, segs, codes, scale, vmom,
                                          cb, sc, stream);
+}
+
+hipError_t launch_muon_codec(int code_bits, const Tile* tiles, int64_t n_tiles, const Seg* segs,
+                             uint8_t* codes, float* scale, CodebookDev cb, float mu,
+                             float one_minus_mu, int nesterov, uint16_t* u, float* tile_ss,
+                             hipStream_t stream)
+{
+    if (n_tiles <= 0) return hipSuccess;
+    if (n_tiles > 0x7fffffffLL) return hipErrorInvalidValue;
+    StepScalars sc{};
+    sc.beta1 = mu;
+    sc.one_minus_beta1 = one_minus_mu;
+    MuonOut mo{u, mu, one_minus_mu, nesterov};
+    const dim3 grid(static_cast<unsigned>(n_tiles));
+    if (code_bits == 8)
+        hipLaunchKernelGGL(k_muon_codec<8>, grid, dim3(kThreads), 0, stream, tiles, segs, codes,
+                           scale, cb, sc, mo, tile_ss);
+    else if (code_bits == 4)
+        hipLaunchKernelGGL(k_muon_codec<4>, grid, dim3(kThreads), 0, stream, tiles, segs, codes,
+                           scale, cb, sc, mo, tile_ss);
+    else
+        return hipErrorInvalidValue;
+    return hipGetLastError();
 }
 
 }  // namespace gefen

@@ -1,0 +1,214 @@
+"""Gefen-Muon (appendix "Gefen-Muon") on the GPU against the oracle, through the C ABI.
+
+Teacher-forced per step: before each step the oracle takes the library's codes, scales,
+codebooks and parameters. Three stages are checked:
+
+* codec: codes and scales with the gates of the Gefen step (ties at midpoints excepted);
+* the bfloat16 momentum matrix U (state array 6): within one bfloat16 rounding of the
+  oracle's float64 value, plus a cancellation floor for the float32 momentum;
+* orthogonalisation and update: the library's O (recovered from the parameter change,
+  O = (theta * decay - theta') / (lr * scale)) against the oracle's bfloat16
+  Newton-Schulz of the library's own U. Both pipelines round every matrix product to
+  bfloat16 but accumulate differently (rocBLAS float32 tiles against float64), so the
+  gate is 3 % of max |O| per element and 0.5 % on average; the float64 oracle against
+  torch.optim.Muon on the CPU differs by up to 0.8 % (see the oracle pins).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+
+pytestmark = pytest.mark.gpu
+
+gf = pytest.importorskip("paper_2606_13894_amd")
+
+
+def _dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no HIP device")
+    return torch.device("cuda", 0)
+
+
+def _grad(rows, cols, seed, dtype, dev):
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(seed)
+    g = torch.randn(rows, cols, generator=gen, device=dev)
+    sc = torch.exp(torch.empty(rows, 1, device=dev).uniform_(np.log(1e-3), 0, generator=gen))
+    return (g * sc).reshape(-1).to(dtype)
+
+
+class MuonRun:
+    def __init__(self, shapes, dtype, dev, seed=0, code_bits=8, block_offsets=None,
+                 period_override=None):
+        from parity import Run
+        self.shapes = shapes
+        self.dtype = dtype
+        self.dev = dev
+        self.seed = seed
+        self.params = [torch.randn(r * c, device=dev) * 0.02 for r, c in shapes]
+        g1 = self.grads(0)
+        self.run = Run(self.params, g1, block_offsets=block_offsets, code_bits=code_bits,
+                       period_override=period_override)
+        self.st = self.run.state
+        self.st.muon_init([r for r, _ in shapes])
+
+    def grads(self, t):
+        return [_grad(r, c, self.seed + 1000 * i + t, self.dtype, self.dev)
+                for i, (r, c) in enumerate(self.shapes)]
+
+    def step(self, t, lr=0.02, mu=0.95, wd=0.01, nesterov=True, where=""):
+        from parity import grad_bits, unpack_codes
+        run = self.run
+        grads = self.grads(t)
+        pre = run.snapshot()
+        self.st.muon_step(self.params, grads, lr, mu, wd, nesterov)
+        post = run.snapshot()
+        u_all = self.st.read(gf.STATE_MUON_U).cpu().numpy().view(np.uint16)
+        u_all = (u_all.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+        cb_dec, cb_enc = pre["cb_dec"], pre["cb_enc"]
+        worst = {"o_max": 0.0, "o_mean": 0.0, "ties": 0}
+        for i, (R, C) in enumerate(self.shapes):
+            n = R * C
+            offs = run.offsets[i]
+            codes = pre["codes"][i].copy()
+            s = pre["s"][i].copy()
+            g = grad_bits(grads[i])
+            u_ref = oracle.muon_codec_blocks(g, codes, s, offs, cb_dec, cb_enc, mu, nesterov)
+            # codec: scales and codes
+            gd = grads[i].double().cpu().numpy()
+            sizes = np.diff(offs)
+            blk = np.repeat(np.arange(sizes.size), sizes)
+            prev = np.abs(cb_dec[pre["codes"][i]] * pre["s"][i][blk])
+            mag = mu * prev + (1 - mu) * np.abs(gd)
+            bmag = np.zeros(sizes.size)
+            np.maximum.at(bmag, blk, mag)
+            ds = np.abs(post["s"][i] - s)
+            assert (ds <= 1e-6 * s + 1e-6 * bmag).all(), f"{where} tensor {i}: scale"
+            bad = np.nonzero(post["codes"][i] != codes)[0]
+            if bad.size:
+                m_ref = oracle.muon_codec_blocks(g, pre["codes"][i].copy(), pre["s"][i].copy(),
+                                                 offs, cb_dec, cb_enc, mu, False)
+                x = m_ref[bad] / np.where(s[blk[bad]] > 0, s[blk[bad]], 1.0)
+                a, b = post["codes"][i][bad].astype(int), codes[bad].astype(int)
+                assert (np.abs(a - b) == 1).all(), f"{where} tensor {i}: non-adjacent code"
+                midp = 0.5 * (cb_enc[np.minimum(a, b)] + cb_enc[np.maximum(a, b)])
+                delta = 1e-6 * np.maximum(1.0, bmag[blk[bad]] / np.where(s[blk[bad]] > 0,
+                                                                          s[blk[bad]], 1.0))
+                assert (np.abs(x - midp) <= delta).all(), f"{where} tensor {i}: code"
+                worst["ties"] += bad.size
+            # bfloat16 momentum matrix
+            c0 = run.code_off[i]
+            u_gpu = u_all[c0:c0 + n]
+            tol_u = 2.0 ** -8 * np.abs(u_ref) + 2e-6 * (mag + np.abs(gd))
+            assert (np.abs(u_gpu - u_ref) <= tol_u).all(), f"{where} tensor {i}: U"
+            # orthogonalisation + update
+            o_ref = oracle.newton_schulz(u_gpu, R, C).reshape(-1)
+            decay = 1.0 - lr * wd
+            step = lr * oracle.muon_lr_scale(R, C)
+            th_pre = pre["theta"][i]
+            o_gpu = (th_pre * decay - post["theta"][i]) / step
+            scale_o = max(np.abs(o_ref).max(), 1e-30)
+            d = np.abs(o_gpu - o_ref)
+            noise = 4e-7 * (np.abs(th_pre) + np.abs(post["theta"][i])) / step
+            assert (d <= 0.03 * scale_o + noise).all(), (where, i, d.max() / scale_o)
+            assert d.mean() <= 0.005 * scale_o + noise.mean(), (where, i, d.mean() / scale_o)
+            worst["o_max"] = max(worst["o_max"], d.max() / scale_o)
+            worst["o_mean"] = max(worst["o_mean"], d.mean() / scale_o)
+        return worst
+
+
+SHAPES = [[(64, 192)], [(192, 64)], [(128, 128)], [(1, 300)], [(300, 1)], [(3, 5)],
+          [(64, 128), (128, 64), (64, 128), (1, 77), (64, 128), (128, 64), (96, 96)]]
+
+
+@pytest.mark.parametrize("shapes", SHAPES, ids=lambda s: "+".join(f"{r}x{c}" for r, c in s))
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_muon_parity_shapes(shapes, dtype):
+    dev = _dev()
+    mr = MuonRun(shapes, dtype, dev, seed=len(shapes))
+    for t in range(1, 4):
+        mr.step(t, where=f"t={t}")
+
+
+@pytest.mark.parametrize("code_bits", [8, 4])
+@pytest.mark.parametrize("nesterov", [True, False])
+def test_muon_code_widths_and_nesterov(code_bits, nesterov):
+    dev = _dev()
+    mr = MuonRun([(96, 160), (160, 96), (1, 160)], torch.bfloat16, dev, seed=5,
+                 code_bits=code_bits)
+    for t in range(1, 4):
+        mr.step(t, nesterov=nesterov, where=f"cb{code_bits} nesterov={nesterov} t={t}")
+
+
+def test_muon_explicit_blocks_and_refit():
+    dev = _dev()
+    rng = np.random.default_rng(9)
+    shapes = [(48, 100), (100, 48)]
+    n = sum(r * c for r, c in shapes)
+    sizes = np.concatenate([rng.integers(1, 40, 60), rng.integers(40, 600, 14)])
+    sizes = sizes[np.cumsum(sizes) < n - 4800]
+    bounds = np.concatenate([[0], np.cumsum(sizes)])
+    bounds = np.unique(np.concatenate([bounds, [4800, n]]))
+    mr = MuonRun(shapes, torch.float32, dev, seed=9, block_offsets=bounds.astype(np.int64))
+    mr.step(1, where="explicit t=1")
+    mr.step(2, where="explicit t=2")
+    mr.st.fit_codebook(mr.grads(2))
+    mr.step(3, where="explicit after refit")
+    mr.step(4, where="explicit t=4")
+
+
+def test_muon_gpt2_mlp_shape():
+    """One GPT-2 small MLP pair at full size (768 x 3072 and 3072 x 768)."""
+    dev = _dev()
+    mr = MuonRun([(768, 3072), (3072, 768)], torch.float32, dev, seed=11)
+    w = mr.step(1, where="gpt2 mlp t=1")
+    w = mr.step(2, where="gpt2 mlp t=2")
+    print("worst O deviation (max, mean) / max|O|:", w)
+
+
+def test_muon_lossless_block_size_one_matches_torch_muon():
+    """Block size 1: the stored momentum is exact, so Gefen-Muon is Muon; free-running
+    against torch.optim.Muon on the GPU (both bfloat16 Newton-Schulz)."""
+    dev = _dev()
+    R, C = 96, 256
+    torch.manual_seed(3)
+    theta0 = torch.randn(R * C, device=dev) * 0.02
+    p_gef = theta0.clone()
+    p_ref = torch.nn.Parameter(theta0.clone().reshape(R, C))
+    lr, mu, wd = 0.02, 0.95, 0.01
+    opt = torch.optim.Muon([p_ref], lr=lr, momentum=mu, weight_decay=wd, nesterov=True)
+    gs = [torch.randn(R * C, device=dev) for _ in range(4)]
+    st = gf.GefenState([gs[0]], period_override=[1])
+    st.muon_init([R])
+    for g in gs:
+        st.muon_step([p_gef], [g], lr, mu, wd, True)
+        p_ref.grad = g.reshape(R, C).clone()
+        opt.step()
+    torch.cuda.synchronize()
+    step = lr * oracle.muon_lr_scale(R, C)
+    diff = (p_gef - p_ref.detach().reshape(-1)).abs().max().item()
+    moved = (p_gef - theta0).abs().max().item()
+    assert diff < 0.03 * step, (diff / step)
+    assert moved > 10 * diff
+
+
+def test_muon_argument_errors():
+    dev = _dev()
+    g = torch.randn(12 * 8, device=dev)
+    p = torch.zeros_like(g)
+    st = gf.GefenState([g])
+    with pytest.raises(gf.GefenError, match="EINVAL"):
+        st.muon_step([p], [g], 0.02)                      # before muon_init
+    with pytest.raises(gf.GefenError, match="EINVAL"):
+        st.muon_init([5])                                 # 5 does not divide 96
+    st.muon_init([12])
+    with pytest.raises(gf.GefenError, match="EINVAL"):
+        st.muon_init([12])                                # second call
+    with pytest.raises(gf.GefenError, match="EINVAL"):
+        st.muon_step([p], [g], 0.02, momentum=1.0)
+    with pytest.raises(gf.GefenError, match="EINVAL"):
+        st.muon_step([p], [g], 0.02, ns_eps=0.0)
+    st.muon_step([p], [g], 0.02)
+    torch.cuda.synchronize()
+    assert torch.isfinite(p).all()
