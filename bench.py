@@ -146,6 +146,114 @@ def adamw_comparator(torch, w, params, grads, steps: int, gefen_state_bytes: int
     return out
 
 
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+
+
+def muon_ns_flops(w, steps: int) -> int:
+    """Newton-Schulz FLOPs of one Gefen-Muon step: per tensor (m = min side, n = max
+    side) and iteration, X X^T (2 m^2 n), A A (2 m^3) and B X (2 m^2 n)."""
+    total = 0
+    for t in w.tensors:
+        r = t.rows
+        c = t.numel // r
+        m, n = min(r, c), max(r, c)
+        total += steps * (4 * m * m * n + 2 * m * m * m)
+    return total
+
+
+def bench_muon(args, torch, w, dev):
+    """Gefen-Muon steps (quantized Muon momentum + bf16 Newton-Schulz + update) on the
+    workload's tensors as matrices (1-D tensors as 1 x n), against torch.optim.Muon."""
+    import workloads as W
+    import paper_2606_13894_amd as gf
+    fields = W.scale_fields(w)
+    params = W.init_params(w, dev)
+    grads = [W.make_grads(w, fields, t, dev) for t in (1, 2)]
+    rows = [t.rows for t in w.tensors]
+    lr, mu, wd, ns_steps = 1e-3, 0.95, 0.1, 5
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    st = gf.GefenState(grads[0], eps_part=w.eps, code_bits=args.code_bits)
+    st.muon_init(rows)
+    torch.cuda.synchronize()
+    init_s = time.perf_counter() - t0
+    for i in range(args.warmup):
+        st.muon_step(params, grads[i % 2], lr, mu, wd, True, ns_steps)
+    torch.cuda.synchronize()
+    st.profile_begin(args.steps)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(args.steps):
+        st.muon_step(params, grads[i % 2], lr, mu, wd, True, ns_steps)
+    e1.record()
+    torch.cuda.synchronize()
+    prof = st.muon_profile_end()
+    ms = e0.elapsed_time(e1) / args.steps
+    flops = muon_ns_flops(w, ns_steps)
+    ns_ms = prof["ns_ms"] / max(1, prof["steps"])
+    codec_ms = prof["codec_ms"] / max(1, prof["steps"])
+    gb = 2 if w.grad_dtype == "bf16" else 4
+    codec_bytes = w.numel * (gb + (2 if args.code_bits == 8 else 1) + 2)
+    persistent, workspace = st.state_bytes()
+    # torch.optim.Muon on the same matrices
+    ps = [torch.nn.Parameter(p.detach().clone().view(r, p.numel() // r))
+          for p, r in zip(params, rows)]
+    gm = [[g.float().view(r, g.numel() // r) for g, r in zip(gs, rows)] for gs in grads]
+    torch.cuda.synchronize()
+    base = torch.cuda.memory_allocated()
+    opt = torch.optim.Muon(ps, lr=lr, momentum=mu, weight_decay=wd, nesterov=True,
+                           ns_steps=ns_steps)
+    for p, g in zip(ps, gm[0]):
+        p.grad = g
+    opt.step()
+    torch.cuda.synchronize()
+    muon_state = torch.cuda.memory_allocated() - base
+    m0 = torch.cuda.Event(enable_timing=True)
+    m1 = torch.cuda.Event(enable_timing=True)
+    reps = min(args.steps, 10)
+    m0.record()
+    for i in range(reps):
+        for p, g in zip(ps, gm[i % 2]):
+            p.grad = g
+        opt.step()
+    m1.record()
+    torch.cuda.synchronize()
+    muon_ms = m0.elapsed_time(m1) / reps
+    achieved = flops / (ns_ms * 1e-3) / 1e12
+    return {
+        "metric": METRIC + " (Gefen-Muon)",
+        "value": round(w.numel / (ms * 1e-3) / 1e9, 3),
+        "unit": "Gparams/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "optimizer": "gefen_muon", "params": w.numel,
+                   "tensors": len(w.tensors), "grad_dtype": w.grad_dtype,
+                   "code_bits": args.code_bits, "ns_steps": ns_steps, "nesterov": True},
+        "phases_ms": {"codec": round(codec_ms, 4), "newton_schulz": round(ns_ms, 4),
+                      "prep_update": round(prof["rest_ms"] / max(1, prof["steps"]), 4)},
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": None, "kernel": "Newton-Schulz bf16 GEMMs (rocBLAS)",
+                     "flops_per_step": flops},
+        "codec": {"bytes_per_step": codec_bytes,
+                  "gbps": round(codec_bytes / (codec_ms * 1e-3) / 1e9, 1)},
+        "torch_muon": {"ms_per_step": round(muon_ms, 4), "state_bytes": muon_state,
+                       "gefen_muon_persistent_bytes": persistent,
+                       "gefen_muon_workspace_bytes": workspace,
+                       "state_ratio": round(muon_state / persistent, 3),
+                       "gefen_speedup": round(muon_ms / ms, 3)},
+        "init_s": round(init_s, 3),
+    }
+
+
 def copy_ceiling(torch, dev, nbytes: int = 4 << 30, reps: int = 10):
     """Practical streaming ceiling on this GPU: torch's device copy (one read, one write)
     and an add of two tensors (two reads, one write) over `nbytes` per tensor."""
@@ -176,10 +284,14 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="llama3_1p5b")
+    ap.add_argument("--workload", default=None,
+                    help="llama3_1p5b for gefen, gpt2_125m for gefen_muon by default")
     ap.add_argument("--code-bits", type=int, default=8, choices=(8, 4),
                     help="momentum code width: 8 (k = 256) or 4 (k = 16, two codes per byte)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--optimizer", default="gefen", choices=("gefen", "gefen_muon"),
+                    help="gefen (the default, Alg. 1) or gefen_muon (quantized Muon momentum "
+                         "with Newton-Schulz; default workload gpt2_125m)")
     ap.add_argument("--no-adamw", action="store_true",
                     help="skip the torch AdamW comparison (always skipped for explicit blocks)")
     ap.add_argument("--cpu-sample-elems", type=int, default=100_000_000)
@@ -208,7 +320,21 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes_per_launch": nbytes, "launches": 3}), flush=True)
         return
+    if args.workload is None:
+        args.workload = "gpt2_125m" if args.optimizer == "gefen_muon" else "llama3_1p5b"
     w = W.get(args.workload)
+    if args.optimizer == "gefen_muon":
+        if w.n_blocks:
+            print("gefen_muon needs matrix-shaped tensors", file=sys.stderr)
+            sys.exit(2)
+        import paper_2606_13894_amd as gf
+        try:
+            line = bench_muon(args, torch, w, dev)
+        except gf.GefenError as e:
+            print(f"gefen_muon on {w.name}: {e}", file=sys.stderr)
+            sys.exit(2)
+        print(json.dumps(line), flush=True)
+        return
     fields = W.scale_fields(w)
     offsets = None
     bscales = None

@@ -240,8 +240,10 @@ int gefen_profile_end(gefen_state* st, int32_t cap, int32_t* n_classes, int32_t*
  *          row-major (a 1-D tensor is 1 x numel). rows[i] must divide numel_i.
  * Allocates the bfloat16 momentum matrix (2 bytes per parameter), the Newton-Schulz
  * buffers for the largest group of equal-shape tensors, and a rocBLAS handle whose
- * workspace is sized here; synchronises `stream`. Call once per state.
- * Errors: EINVAL (NULL, count mismatch, rows, second call), ENOMEM, EHIP.
+ * workspace is sized here; synchronises `stream`. Call once per state. Tensors of one
+ * shape are orthogonalised together; a shape group of more than 2^27 elements is
+ * refused (EINVAL).
+ * Errors: EINVAL (NULL, count mismatch, rows, second call, group size), ENOMEM, EHIP.
  * ---------------------------------------------------------------------------- */
 int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, void* stream);
 
@@ -267,6 +269,14 @@ int gefen_muon_step(gefen_state* st, const gefen_tensor* params, const gefen_ten
                     int32_t n_tensors, double lr, double momentum, double weight_decay,
                     int32_t nesterov, int32_t ns_steps, double ns_a, double ns_b, double ns_c,
                     double ns_eps, void* stream);
+
+/* Measurement of Gefen-Muon steps (after gefen_muon_init and gefen_profile_begin):
+ * sums over the profiled steps of the codec time (codec and norms), the Newton-Schulz
+ * GEMM time (all shape groups) and the rest (normalise/transpose and update kernels),
+ * in milliseconds, from HIP events on the step's stream; then disarms like
+ * gefen_profile_end. */
+int gefen_muon_profile_end(gefen_state* st, int32_t* steps, double* codec_ms, double* ns_ms,
+                           double* rest_ms);
 
 /* Free the state and every device buffer it owns. NULL is a no-op. */
 void gefen_destroy(gefen_state* st);

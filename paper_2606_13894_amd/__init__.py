@@ -34,7 +34,7 @@ SYMBOLS = [
     "gefen_read_state", "gefen_write_state", "gefen_get_fit_info", "gefen_state_bytes",
     "gefen_checkpoint_bytes", "gefen_export", "gefen_import", "gefen_profile_begin",
     "gefen_profile_end", "gefen_destroy", "gefen_last_error", "gefen_muon_init",
-    "gefen_muon_step",
+    "gefen_muon_step", "gefen_muon_profile_end",
 ]
 
 
@@ -91,6 +91,7 @@ def load_library(path: str = LIB_PATH):
     lib.gefen_muon_init.argtypes = [vp, vp, i32, vp]
     lib.gefen_muon_step.argtypes = [vp, P(gefen_tensor), P(gefen_tensor), i32, f64, f64, f64,
                                     i32, i32, f64, f64, f64, f64, vp]
+    lib.gefen_muon_profile_end.argtypes = [vp, P(i32), P(f64), P(f64), P(f64)]
     lib.gefen_destroy.argtypes = [vp]
     lib.gefen_destroy.restype = None
     lib.gefen_last_error.argtypes = []
@@ -214,6 +215,14 @@ class GefenState:
                                     float(weight_decay), int(bool(nesterov)), int(ns_steps),
                                     float(a), float(b), float(c), float(ns_eps),
                                     _stream(stream)))
+
+    def muon_profile_end(self):
+        """Profiled Gefen-Muon steps: {steps, codec_ms, ns_ms, rest_ms} (sums)."""
+        n = ctypes.c_int32()
+        a, b, c = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+        _check(_lib.gefen_muon_profile_end(self._h, ctypes.byref(n), ctypes.byref(a),
+                                           ctypes.byref(b), ctypes.byref(c)))
+        return {"steps": n.value, "codec_ms": a.value, "ns_ms": b.value, "rest_ms": c.value}
 
     def fit_codebook(self, grads: Sequence, stream=None):
         _check(_lib.gefen_fit_codebook(self._h, _tensors(grads, "grads"), self._n,

@@ -49,6 +49,8 @@ struct Class {
 constexpr int64_t kUMaxPeriod = 8192;          // longest period held in registers (KIND_U)
 constexpr int64_t kHugeBlock = 65536;         // longer blocks are always split (KIND_H)
 constexpr int kSegSlots = 4;                 // device tensor tables cached per state
+constexpr size_t kBlasWorkspace = size_t(512) << 20;   // rocBLAS workspace (Gefen-Muon)
+constexpr int64_t kMuonMaxGroup = int64_t(1) << 27;    // elements per Gefen-Muon shape group
 constexpr int64_t kMinStreamedBlocks = 4096;  // fewer blocks > kUMaxPeriod: split them too
 constexpr int64_t kPartChunk = 65536;     // elements of one partition sub-chunk (mode 1)
 constexpr int64_t kPartItemElems = 16384; // elements per partition item (mode 0)
@@ -150,13 +152,22 @@ struct gefen_state {
     bool prof_armed = false;
     int32_t prof_max_steps = 0, prof_steps = 0;
     std::vector<hipEvent_t> prof_events;
+    // Gefen-Muon steps: per step, events [codec start, codec end, (NS start, NS end) per
+    // shape group, step end]
+    int32_t muon_prof_steps = 0;
+    std::vector<hipEvent_t> muon_prof_events;
+
+    size_t muon_prof_stride() const { return 3 + 2 * muon_groups.size(); }
 
     void prof_free()
     {
         for (hipEvent_t e : prof_events) (void)hipEventDestroy(e);
+        for (hipEvent_t e : muon_prof_events) (void)hipEventDestroy(e);
         prof_events.clear();
+        muon_prof_events.clear();
         prof_armed = false;
         prof_steps = 0;
+        muon_prof_steps = 0;
     }
 
     ~gefen_state()
@@ -1231,6 +1242,11 @@ int gefen_profile_begin(gefen_state* st, int32_t max_steps)
     const size_t n = static_cast<size_t>(max_steps) * st->classes.size() * 2;
     st->prof_events.resize(n, nullptr);
     for (size_t i = 0; i < n; ++i) GEFEN_HIP(hipEventCreate(&st->prof_events[i]));
+    if (st->muon_ready) {
+        const size_t nm = static_cast<size_t>(max_steps) * st->muon_prof_stride();
+        st->muon_prof_events.resize(nm, nullptr);
+        for (size_t i = 0; i < nm; ++i) GEFEN_HIP(hipEventCreate(&st->muon_prof_events[i]));
+    }
     st->prof_max_steps = max_steps;
     st->prof_steps = 0;
     st->prof_armed = true;
@@ -1405,6 +1421,13 @@ int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, voi
         max_x = std::max(max_x, g.count * g.rows * g.cols);
         max_a = std::max(max_a, g.count * m * m);
     }
+    // Shape groups above kMuonMaxGroup elements are refused: a state of that size (the
+    // GPT-2 1B shapes, 4e8 elements in one group) failed with a device memory fault in
+    // this initialisation, whose cause has not been found.
+    if (max_x > kMuonMaxGroup)
+        return fail(GEFEN_EINVAL, "a group of equal-shape tensors holds %lld elements; "
+                    "Gefen-Muon supports at most %lld per group",
+                    (long long)max_x, (long long)kMuonMaxGroup);
 
     int rc;
     st->muon_n_tiles = static_cast<int64_t>(tiles.size());
@@ -1422,20 +1445,17 @@ int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, voi
     GEFEN_HIP(hipMemcpy(st->muon_tile_first, tile_first.data(), 8 * tile_first.size(), hipMemcpyHostToDevice));
     GEFEN_HIP(hipMemcpy(st->muon_tensor_of, order.data(), 4 * order.size(), hipMemcpyHostToDevice));
 
-    // rocBLAS handle with its workspace sized now, so that steps allocate nothing
+    // rocBLAS handle with a fixed workspace, set before any product runs, so that steps
+    // allocate nothing; a product that would need more returns an error status. One
+    // Newton-Schulz iteration per group on zeroed matrices loads and checks every GEMM
+    // the steps use.
     GEFEN_BLAS(rocblas_create_handle(&st->blas));
     GEFEN_BLAS(rocblas_set_stream(st->blas, stream));
-    GEFEN_BLAS(rocblas_start_device_memory_size_query(st->blas));
+    GEFEN_BLAS(rocblas_set_device_memory_size(st->blas, kBlasWorkspace));
+    st->workspace_bytes += static_cast<int64_t>(kBlasWorkspace);
+    GEFEN_HIP(fill_zero(st->muon_x[0], 2 * static_cast<size_t>(max_x), stream));
     for (const auto& g : st->muon_groups)
-        if ((rc = ns_iteration(st, g, st->muon_x[0], st->muon_x[1], 1.0f, 1.0f, 1.0f))) {
-            size_t ignored;
-            (void)rocblas_stop_device_memory_size_query(st->blas, &ignored);
-            return rc;
-        }
-    size_t blas_bytes = 0;
-    GEFEN_BLAS(rocblas_stop_device_memory_size_query(st->blas, &blas_bytes));
-    if (blas_bytes) GEFEN_BLAS(rocblas_set_device_memory_size(st->blas, blas_bytes));
-    st->workspace_bytes += static_cast<int64_t>(blas_bytes);
+        if ((rc = ns_iteration(st, g, st->muon_x[0], st->muon_x[1], 1.0f, 1.0f, 1.0f))) return rc;
     GEFEN_HIP(hipStreamSynchronize(stream));
     st->muon_ready = true;
     return GEFEN_OK;
@@ -1459,6 +1479,11 @@ int gefen_muon_step(gefen_state* st, const gefen_tensor* params, const gefen_ten
     hipStream_t stream = as_stream(stream_);
     if ((rc = refresh_segs(st, params, grads, stream))) return rc;
     GEFEN_BLAS(rocblas_set_stream(st->blas, stream));
+    const bool prof = st->prof_armed && st->muon_prof_steps < st->prof_max_steps &&
+                      !st->muon_prof_events.empty();
+    hipEvent_t* ev = prof ? &st->muon_prof_events[st->muon_prof_steps * st->muon_prof_stride()]
+                          : nullptr;
+    if (prof) GEFEN_HIP(hipEventRecord(ev[0], stream));
 
     GEFEN_HIP(launch_muon_codec(st->code_bits, st->muon_tiles, st->muon_n_tiles, st->segs,
                                 st->codes, st->scale, codebook_dev(st),
@@ -1466,10 +1491,13 @@ int gefen_muon_step(gefen_state* st, const gefen_tensor* params, const gefen_ten
                                 nesterov ? 1 : 0, st->muon_u, st->muon_tile_ss, stream));
     GEFEN_HIP(launch_muon_norm(st->muon_tile_ss, st->muon_tile_first, st->n_tensors,
                                host_bf16_value(static_cast<float>(ns_eps)), st->muon_norm, stream));
+    if (prof) GEFEN_HIP(hipEventRecord(ev[1], stream));
     const float decay = static_cast<float>(1.0 - lr * weight_decay);
-    for (const auto& g : st->muon_groups) {
+    for (size_t gi = 0; gi < st->muon_groups.size(); ++gi) {
+        const auto& g = st->muon_groups[gi];
         GEFEN_HIP(launch_muon_prep(st->muon_u, st->segs, st->muon_tensor_of + g.first, g.count,
                                    st->muon_norm, g.rows, g.cols, st->muon_x[0], stream));
+        if (prof) GEFEN_HIP(hipEventRecord(ev[2 + 2 * gi], stream));
         int cur = 0;
         for (int32_t it = 0; it < ns_steps; ++it) {
             if ((rc = ns_iteration(st, g, st->muon_x[cur], st->muon_x[1 - cur],
@@ -1478,12 +1506,47 @@ int gefen_muon_step(gefen_state* st, const gefen_tensor* params, const gefen_ten
                 return rc;
             cur ^= 1;
         }
+        if (prof) GEFEN_HIP(hipEventRecord(ev[3 + 2 * gi], stream));
         const double scale = std::sqrt(std::max(1.0, static_cast<double>(g.rows) / g.cols));
         GEFEN_HIP(launch_muon_update(st->muon_x[cur], st->segs, st->muon_tensor_of + g.first,
                                      g.count, g.rows, g.cols, decay,
                                      static_cast<float>(lr * scale), stream));
     }
+    if (prof) {
+        GEFEN_HIP(hipEventRecord(ev[st->muon_prof_stride() - 1], stream));
+        ++st->muon_prof_steps;
+    }
     st->dec_slot = st->enc_slot;
+    return GEFEN_OK;
+}
+
+int gefen_muon_profile_end(gefen_state* st, int32_t* steps, double* codec_ms, double* ns_ms,
+                           double* rest_ms)
+{
+    if (!st || !steps || !codec_ms || !ns_ms || !rest_ms) return fail(GEFEN_EINVAL, "NULL argument");
+    *steps = 0;
+    *codec_ms = *ns_ms = *rest_ms = 0.0;
+    const size_t k = st->muon_prof_stride();
+    if (st->prof_armed && st->muon_prof_steps > 0) {
+        GEFEN_HIP(hipEventSynchronize(st->muon_prof_events[st->muon_prof_steps * k - 1]));
+        for (int32_t s = 0; s < st->muon_prof_steps; ++s) {
+            hipEvent_t* ev = &st->muon_prof_events[s * k];
+            float a = 0.0f, total = 0.0f;
+            GEFEN_HIP(hipEventElapsedTime(&a, ev[0], ev[1]));
+            GEFEN_HIP(hipEventElapsedTime(&total, ev[0], ev[k - 1]));
+            double ns = 0.0;
+            for (size_t gi = 0; gi < st->muon_groups.size(); ++gi) {
+                float b = 0.0f;
+                GEFEN_HIP(hipEventElapsedTime(&b, ev[2 + 2 * gi], ev[3 + 2 * gi]));
+                ns += b;
+            }
+            *codec_ms += a;
+            *ns_ms += ns;
+            *rest_ms += total - a - ns;
+        }
+        *steps = st->muon_prof_steps;
+    }
+    st->prof_free();
     return GEFEN_OK;
 }
 

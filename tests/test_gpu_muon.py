@@ -212,3 +212,38 @@ def test_muon_argument_errors():
     st.muon_step([p], [g], 0.02)
     torch.cuda.synchronize()
     assert torch.isfinite(p).all()
+
+
+def test_muon_large_k_embedding_shape():
+    """A GPT-2 1B token-embedding shape (2048 x 50257: the Gram product has K = 50257,
+    where the GEMM library picks split-K solutions that need workspace). Lossless codes
+    (block size 1); against torch.optim.Muon on the GPU for two steps."""
+    dev = _dev()
+    R, C = 50257, 2048
+    torch.manual_seed(5)
+    theta0 = torch.randn(R * C, device=dev) * 0.02
+    p_gef = theta0.clone()
+    p_ref = torch.nn.Parameter(theta0.clone().reshape(R, C))
+    lr, mu, wd = 0.02, 0.95, 0.01
+    opt = torch.optim.Muon([p_ref], lr=lr, momentum=mu, weight_decay=wd, nesterov=True)
+    gs = [torch.randn(R * C, device=dev) for _ in range(2)]
+    st = gf.GefenState([gs[0]], period_override=[1])
+    st.muon_init([R])
+    for g in gs:
+        st.muon_step([p_gef], [g], lr, mu, wd, True)
+        p_ref.grad = g.reshape(R, C).clone()
+        opt.step()
+    torch.cuda.synchronize()
+    step = lr * oracle.muon_lr_scale(R, C)
+    diff = (p_gef - p_ref.detach().reshape(-1)).abs().max().item()
+    assert torch.isfinite(p_gef).all()
+    assert diff < 0.03 * step, (diff / step)
+
+
+def test_muon_refuses_groups_over_the_limit():
+    """A shape group of more than 2^27 elements is refused before any allocation."""
+    dev = _dev()
+    gs = [torch.zeros(8192 * 8192, device=dev, dtype=torch.bfloat16) for _ in range(3)]
+    st = gf.GefenState(gs, period_override=[8192] * 3)
+    with pytest.raises(gf.GefenError, match="per group"):
+        st.muon_init([8192] * 3)
