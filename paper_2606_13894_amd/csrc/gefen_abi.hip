@@ -133,6 +133,7 @@ struct gefen_state {
     struct MuonGroup {
         int64_t rows, cols;
         int32_t first, count;   // muon_tensor_of[first .. first + count)
+        int32_t splits;         // K-chunks of the Gram product (1 = one GEMM)
     };
     bool muon_ready = false;
     Tile* muon_tiles = nullptr;
@@ -146,6 +147,7 @@ struct gefen_state {
     uint16_t* muon_x[2] = {nullptr, nullptr};
     uint16_t* muon_a = nullptr;
     uint16_t* muon_b = nullptr;
+    float* muon_partial = nullptr;   // split-K partial Gram products (float32)
     rocblas_handle blas = nullptr;
 
     // measurement: events[(step * classes + c) * 2 + {0 start, 1 stop}]
@@ -1315,6 +1317,13 @@ float host_bf16_value(float x)
             return fail(GEFEN_EHIP, "%s failed: %s", #call, rocblas_status_to_string(s_)); \
     } while (0)
 
+hipStream_t rocblas_get_stream_for(gefen_state* st)
+{
+    hipStream_t s = nullptr;
+    (void)rocblas_get_stream(st->blas, &s);
+    return s;
+}
+
 // One Newton-Schulz iteration on a batch of wide m x n row-major matrices (m <= n):
 // A = X X^T; B = b A + c A A; X' = a X + B X, all bfloat16 with float32 accumulation.
 // rocBLAS is column-major: the row-major m x n X is the column-major n x m X^T.
@@ -1326,10 +1335,33 @@ int ns_iteration(gefen_state* st, const gefen_state::MuonGroup& g, const uint16_
     const rocblas_stride sx = m * n, sa = m * m;
     const float one = 1.0f, zero = 0.0f;
     const rocblas_datatype bf = rocblas_datatype_bf16_r, f32 = rocblas_datatype_f32_r;
-    GEFEN_BLAS(rocblas_gemm_strided_batched_ex(
-        st->blas, rocblas_operation_transpose, rocblas_operation_none, mi, mi, ni, &one, x, bf,
-        ni, sx, x, bf, ni, sx, &zero, st->muon_a, bf, mi, sa, st->muon_a, bf, mi, sa, g.count,
-        f32, rocblas_gemm_algo_standard, 0, 0));
+    if (g.splits > 1) {
+        // tall-skinny Gram product (one matrix, long K): float32 partial products of
+        // K-chunks, summed in chunk order and rounded once
+        const int64_t kc = (n + g.splits - 1) / g.splits;
+        const int64_t full = n / kc;               // chunks of length kc
+        const int64_t rest = n - full * kc;
+        if (full > 0)
+            GEFEN_BLAS(rocblas_gemm_strided_batched_ex(
+                st->blas, rocblas_operation_transpose, rocblas_operation_none, mi, mi,
+                static_cast<rocblas_int>(kc), &one, x, bf, ni, kc, x, bf, ni, kc, &zero,
+                st->muon_partial, f32, mi, sa, st->muon_partial, f32, mi, sa,
+                static_cast<rocblas_int>(full), f32, rocblas_gemm_algo_standard, 0, 0));
+        if (rest > 0)
+            GEFEN_BLAS(rocblas_gemm_ex(
+                st->blas, rocblas_operation_transpose, rocblas_operation_none, mi, mi,
+                static_cast<rocblas_int>(rest), &one, x + full * kc, bf, ni, x + full * kc, bf,
+                ni, &zero, st->muon_partial + full * sa, f32, mi, st->muon_partial + full * sa,
+                f32, mi, f32, rocblas_gemm_algo_standard, 0, 0));
+        GEFEN_HIP(launch_muon_splitk_sum(st->muon_partial,
+                                         static_cast<int32_t>(full + (rest > 0 ? 1 : 0)), sa,
+                                         st->muon_a, rocblas_get_stream_for(st)));
+    } else {
+        GEFEN_BLAS(rocblas_gemm_strided_batched_ex(
+            st->blas, rocblas_operation_transpose, rocblas_operation_none, mi, mi, ni, &one, x,
+            bf, ni, sx, x, bf, ni, sx, &zero, st->muon_a, bf, mi, sa, st->muon_a, bf, mi, sa,
+            g.count, f32, rocblas_gemm_algo_standard, 0, 0));
+    }
     GEFEN_BLAS(rocblas_gemm_strided_batched_ex(
         st->blas, rocblas_operation_none, rocblas_operation_none, mi, mi, mi, &c, st->muon_a, bf,
         mi, sa, st->muon_a, bf, mi, sa, &b, st->muon_a, bf, mi, sa, st->muon_b, bf, mi, sa,
@@ -1405,13 +1437,25 @@ int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, voi
         bool found = false;
         for (const auto& g : st->muon_groups) found = found || (g.rows == R && g.cols == C);
         if (found) continue;
-        gefen_state::MuonGroup g{R, C, static_cast<int32_t>(order.size()), 0};
+        gefen_state::MuonGroup g{R, C, static_cast<int32_t>(order.size()), 0, 1};
         for (int32_t u = t; u < n; ++u)
             if (rows[u] == R && st->numel[u] / rows[u] == C) {
                 order.push_back(u);
                 ++g.count;
             }
         st->muon_groups.push_back(g);
+    }
+    // Split the Gram product of a lone tall-skinny matrix over K when its m x m output
+    // has too few 128 x 128 tiles to occupy the GPU.
+    int64_t max_partial = 0;
+    for (auto& g : st->muon_groups) {
+        const int64_t m = std::min(g.rows, g.cols), n = std::max(g.rows, g.cols);
+        const int64_t tiles = ((m + 127) / 128) * ((m + 127) / 128);
+        if (g.count == 1 && m > 1 && tiles < 128 && n >= 8 * m) {
+            g.splits = static_cast<int32_t>(std::min<int64_t>(16, n / (4 * m)));
+            if (g.splits < 2) g.splits = 1;
+        }
+        if (g.splits > 1) max_partial = std::max(max_partial, g.splits * m * m);
     }
     int64_t max_x = 0, max_a = 0;
     for (const auto& g : st->muon_groups) {
@@ -1441,6 +1485,7 @@ int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, voi
         if ((rc = st->alloc(&x, 2 * static_cast<size_t>(max_x), false))) return rc;
     if ((rc = st->alloc(&st->muon_a, 2 * static_cast<size_t>(max_a), false))) return rc;
     if ((rc = st->alloc(&st->muon_b, 2 * static_cast<size_t>(max_a), false))) return rc;
+    if ((rc = st->alloc(&st->muon_partial, 4 * static_cast<size_t>(max_partial), false))) return rc;
     GEFEN_HIP(hipMemcpy(st->muon_tiles, tiles.data(), sizeof(Tile) * tiles.size(), hipMemcpyHostToDevice));
     GEFEN_HIP(hipMemcpy(st->muon_tile_first, tile_first.data(), 8 * tile_first.size(), hipMemcpyHostToDevice));
     GEFEN_HIP(hipMemcpy(st->muon_tensor_of, order.data(), 4 * order.size(), hipMemcpyHostToDevice));
@@ -1455,7 +1500,9 @@ int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, voi
     st->workspace_bytes += static_cast<int64_t>(kBlasWorkspace);
     GEFEN_HIP(fill_zero(st->muon_x[0], 2 * static_cast<size_t>(max_x), stream));
     for (const auto& g : st->muon_groups)
-        if ((rc = ns_iteration(st, g, st->muon_x[0], st->muon_x[1], 1.0f, 1.0f, 1.0f))) return rc;
+        if (std::min(g.rows, g.cols) > 1 &&
+            (rc = ns_iteration(st, g, st->muon_x[0], st->muon_x[1], 1.0f, 1.0f, 1.0f)))
+            return rc;
     GEFEN_HIP(hipStreamSynchronize(stream));
     st->muon_ready = true;
     return GEFEN_OK;
@@ -1499,12 +1546,19 @@ int gefen_muon_step(gefen_state* st, const gefen_tensor* params, const gefen_ten
                                    st->muon_norm, g.rows, g.cols, st->muon_x[0], stream));
         if (prof) GEFEN_HIP(hipEventRecord(ev[2 + 2 * gi], stream));
         int cur = 0;
-        for (int32_t it = 0; it < ns_steps; ++it) {
-            if ((rc = ns_iteration(st, g, st->muon_x[cur], st->muon_x[1 - cur],
-                                   static_cast<float>(ns_a), static_cast<float>(ns_b),
-                                   static_cast<float>(ns_c))))
-                return rc;
-            cur ^= 1;
+        if (std::min(g.rows, g.cols) == 1) {
+            GEFEN_HIP(launch_muon_ns_vec(st->muon_x[0], g.count, std::max(g.rows, g.cols),
+                                         ns_steps, static_cast<float>(ns_a),
+                                         static_cast<float>(ns_b), static_cast<float>(ns_c),
+                                         stream));
+        } else {
+            for (int32_t it = 0; it < ns_steps; ++it) {
+                if ((rc = ns_iteration(st, g, st->muon_x[cur], st->muon_x[1 - cur],
+                                       static_cast<float>(ns_a), static_cast<float>(ns_b),
+                                       static_cast<float>(ns_c))))
+                    return rc;
+                cur ^= 1;
+            }
         }
         if (prof) GEFEN_HIP(hipEventRecord(ev[3 + 2 * gi], stream));
         const double scale = std::sqrt(std::max(1.0, static_cast<double>(g.rows) / g.cols));

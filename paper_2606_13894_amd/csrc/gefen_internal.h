@@ -160,6 +160,12 @@ hipError_t launch_muon_norm(const float* tile_ss, const int64_t* tile_first, int
 hipError_t launch_muon_prep(const uint16_t* u, const Seg* segs, const int32_t* tensor_of,
                             int32_t batch, const float* norm, int64_t R, int64_t C,
                             uint16_t* x, hipStream_t stream);
+// a (mm bfloat16) = bf16(sum of `splits` float32 partial products, in order)
+hipError_t launch_muon_splitk_sum(const float* partial, int32_t splits, int64_t mm,
+                                  uint16_t* a, hipStream_t stream);
+// `steps` Newton-Schulz iterations in place on `batch` 1 x n bfloat16 rows
+hipError_t launch_muon_ns_vec(uint16_t* x, int32_t batch, int64_t n, int32_t steps, float a,
+                              float b, float c, hipStream_t stream);
 // theta of tensor_of[b] = theta * decay - step * o[b] (o in the orientation of x)
 hipError_t launch_muon_update(const uint16_t* o, const Seg* segs, const int32_t* tensor_of,
                               int32_t batch, int64_t R, int64_t C, float decay, float step,

@@ -118,6 +118,51 @@ __global__ __launch_bounds__(256) void k_muon_update(const uint16_t* __restrict_
     }
 }
 
+// Split-K Gram: A = bf16(sum over s of P[s]), the float32 partial products of K-chunks,
+// added in chunk order.
+__global__ __launch_bounds__(256) void k_muon_splitk_sum(const float* __restrict__ partial,
+                                                         int32_t splits, int64_t mm,
+                                                         uint16_t* __restrict__ a)
+{
+    for (int64_t i = blockIdx.x * 256LL + threadIdx.x; i < mm; i += 256LL * gridDim.x) {
+        float acc = partial[i];
+        for (int32_t s = 1; s < splits; ++s) acc += partial[s * mm + i];
+        a[i] = to_bf16(acc);
+    }
+}
+
+// Newton-Schulz on 1 x n matrices (one workgroup per batch entry): the Gram matrix is
+// the scalar s = x x^T, so every iteration is x <- bf16(a x + bf16(b s + c s^2) x), with
+// s = bf16(x x^T) accumulated in float32 -- the same rounding points as the GEMM form.
+__global__ __launch_bounds__(256) void k_muon_ns_vec(uint16_t* __restrict__ x, int64_t n,
+                                                     int32_t steps, float ca, float cb,
+                                                     float cc)
+{
+    __shared__ float red[256];
+    uint16_t* __restrict__ v = x + static_cast<int64_t>(blockIdx.x) * n;
+    for (int32_t it = 0; it < steps; ++it) {
+        float acc = 0.0f;
+        for (int64_t i = threadIdx.x; i < n; i += 256) {
+            const float e = bf16_val(v[i]);
+            acc = fmaf(e, e, acc);
+        }
+        red[threadIdx.x] = acc;
+        __syncthreads();
+        for (int w = 128; w > 0; w >>= 1) {
+            if (static_cast<int>(threadIdx.x) < w) red[threadIdx.x] += red[threadIdx.x + w];
+            __syncthreads();
+        }
+        const float gram = bf16_val(to_bf16(red[0]));
+        const float poly = bf16_val(to_bf16(fmaf(cc, gram * gram, cb * gram)));
+        __syncthreads();   // red[0] is read by every thread before the next iteration
+        for (int64_t i = threadIdx.x; i < n; i += 256) {
+            const float e = bf16_val(v[i]);
+            v[i] = to_bf16(fmaf(poly, e, ca * e));
+        }
+        __syncthreads();
+    }
+}
+
 }  // namespace
 
 hipError_t launch_muon_norm(const float* tile_ss, const int64_t* tile_first, int32_t n_tensors,
@@ -154,6 +199,26 @@ hipError_t launch_muon_update(const uint16_t* o, const Seg* segs, const int32_t*
     if ((R + kT - 1) / kT > 65535 || batch > 65535) return hipErrorInvalidValue;
     hipLaunchKernelGGL(k_muon_update, tile_grid(R, C, batch), dim3(256), 0, stream, o, segs,
                        tensor_of, R, C, R > C ? 1 : 0, decay, step);
+    return hipGetLastError();
+}
+
+hipError_t launch_muon_splitk_sum(const float* partial, int32_t splits, int64_t mm,
+                                  uint16_t* a, hipStream_t stream)
+{
+    if (mm <= 0) return hipSuccess;
+    int64_t g = (mm + 255) / 256;
+    if (g > 65536) g = 65536;
+    hipLaunchKernelGGL(k_muon_splitk_sum, dim3(static_cast<unsigned>(g)), dim3(256), 0, stream,
+                       partial, splits, mm, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_muon_ns_vec(uint16_t* x, int32_t batch, int64_t n, int32_t steps, float a,
+                              float b, float c, hipStream_t stream)
+{
+    if (batch <= 0 || steps <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_muon_ns_vec, dim3(static_cast<unsigned>(batch)), dim3(256), 0, stream,
+                       x, n, steps, a, b, c);
     return hipGetLastError();
 }
 

@@ -119,7 +119,10 @@ class MuonRun:
 
 
 SHAPES = [[(64, 192)], [(192, 64)], [(128, 128)], [(1, 300)], [(300, 1)], [(3, 5)],
-          [(64, 128), (128, 64), (64, 128), (1, 77), (64, 128), (128, 64), (96, 96)]]
+          [(64, 128), (128, 64), (64, 128), (1, 77), (64, 128), (128, 64), (96, 96)],
+          # lone tall-skinny matrices: the Gram product is split over K (even chunks; a
+          # remainder chunk)
+          [(64, 4096)], [(5000, 48)]]
 
 
 @pytest.mark.parametrize("shapes", SHAPES, ids=lambda s: "+".join(f"{r}x{c}" for r, c in s))
