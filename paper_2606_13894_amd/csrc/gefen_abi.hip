@@ -138,7 +138,8 @@ struct gefen_state {
     bool muon_ready = false;
     Tile* muon_tiles = nullptr;
     int64_t muon_n_tiles = 0;
-    int64_t* muon_tile_first = nullptr;   // n_tensors + 1
+    int64_t* muon_tile_range = nullptr;   // [first, end) tile of each tensor
+    int64_t muon_dt_first[2] = {0, 0}, muon_dt_count[2] = {0, 0};   // tiles per grad dtype
     float* muon_tile_ss = nullptr;
     float* muon_norm = nullptr;
     uint16_t* muon_u = nullptr;
@@ -1396,11 +1397,18 @@ int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, voi
     }
     // codec tiles: mode 1 (lane per block) for blocks of <= 32 elements, mode 2 (wave per
     // block, up to 4) for <= 2048, else mode 0 (the workgroup on one block)
+    // (tiles of fp32-gradient tensors first, then bf16: one codec launch per dtype)
     std::vector<Tile> tiles;
-    std::vector<int64_t> tile_first(n + 1, 0);
-    int64_t csr_base = 0;
+    std::vector<int64_t> tile_range(2 * static_cast<size_t>(n), 0);
+    std::vector<int64_t> csr_at(n + 1, 0);
+    for (int32_t t = 0; t < n; ++t)
+        csr_at[t + 1] = csr_at[t] + (st->explicit_blocks
+                                          ? st->blk_begin[t + 1] - st->blk_begin[t] + 1 : 0);
+    for (int32_t pass = 0; pass < 2; ++pass)
     for (int32_t t = 0; t < n; ++t) {
-        tile_first[t] = static_cast<int64_t>(tiles.size());
+        if (st->gdtype[t] != (pass == 0 ? DT_F32 : DT_BF16)) continue;
+        const int64_t csr_base = csr_at[t];
+        tile_range[2 * t] = static_cast<int64_t>(tiles.size());
         const int64_t nb = st->blk_begin[t + 1] - st->blk_begin[t];
         const int64_t bb = st->blk_begin[t];
         auto start = [&](int64_t b) {
@@ -1425,9 +1433,10 @@ int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, voi
             tl.vpl = static_cast<uint8_t>(mode);
             tiles.push_back(tl);
         }
-        if (st->explicit_blocks) csr_base += nb + 1;
+        tile_range[2 * t + 1] = static_cast<int64_t>(tiles.size());
+        st->muon_dt_count[pass] = static_cast<int64_t>(tiles.size()) - st->muon_dt_first[pass];
+        if (pass == 0) st->muon_dt_first[1] = static_cast<int64_t>(tiles.size());
     }
-    tile_first[n] = static_cast<int64_t>(tiles.size());
 
     // shape groups, in order of first appearance
     std::vector<int32_t> order;
@@ -1476,7 +1485,7 @@ int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, voi
     int rc;
     st->muon_n_tiles = static_cast<int64_t>(tiles.size());
     if ((rc = st->alloc(&st->muon_tiles, sizeof(Tile) * tiles.size(), false))) return rc;
-    if ((rc = st->alloc(&st->muon_tile_first, 8 * tile_first.size(), false))) return rc;
+    if ((rc = st->alloc(&st->muon_tile_range, 8 * tile_range.size(), false))) return rc;
     if ((rc = st->alloc(&st->muon_tile_ss, 4 * tiles.size(), false))) return rc;
     if ((rc = st->alloc(&st->muon_norm, 4 * static_cast<size_t>(n), false))) return rc;
     if ((rc = st->alloc(&st->muon_tensor_of, 4 * order.size(), false))) return rc;
@@ -1487,7 +1496,7 @@ int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, voi
     if ((rc = st->alloc(&st->muon_b, 2 * static_cast<size_t>(max_a), false))) return rc;
     if ((rc = st->alloc(&st->muon_partial, 4 * static_cast<size_t>(max_partial), false))) return rc;
     GEFEN_HIP(hipMemcpy(st->muon_tiles, tiles.data(), sizeof(Tile) * tiles.size(), hipMemcpyHostToDevice));
-    GEFEN_HIP(hipMemcpy(st->muon_tile_first, tile_first.data(), 8 * tile_first.size(), hipMemcpyHostToDevice));
+    GEFEN_HIP(hipMemcpy(st->muon_tile_range, tile_range.data(), 8 * tile_range.size(), hipMemcpyHostToDevice));
     GEFEN_HIP(hipMemcpy(st->muon_tensor_of, order.data(), 4 * order.size(), hipMemcpyHostToDevice));
 
     // rocBLAS handle with a fixed workspace, set before any product runs, so that steps
@@ -1532,11 +1541,14 @@ int gefen_muon_step(gefen_state* st, const gefen_tensor* params, const gefen_ten
                           : nullptr;
     if (prof) GEFEN_HIP(hipEventRecord(ev[0], stream));
 
-    GEFEN_HIP(launch_muon_codec(st->code_bits, st->muon_tiles, st->muon_n_tiles, st->segs,
-                                st->codes, st->scale, codebook_dev(st),
-                                static_cast<float>(momentum), static_cast<float>(1.0 - momentum),
-                                nesterov ? 1 : 0, st->muon_u, st->muon_tile_ss, stream));
-    GEFEN_HIP(launch_muon_norm(st->muon_tile_ss, st->muon_tile_first, st->n_tensors,
+    for (int d = 0; d < 2; ++d)
+        GEFEN_HIP(launch_muon_codec(st->code_bits, d == 0 ? DT_F32 : DT_BF16,
+                                    st->muon_tiles + st->muon_dt_first[d], st->muon_dt_count[d],
+                                    st->segs, st->codes, st->scale, codebook_dev(st),
+                                    static_cast<float>(momentum),
+                                    static_cast<float>(1.0 - momentum), nesterov ? 1 : 0,
+                                    st->muon_u, st->muon_tile_ss + st->muon_dt_first[d], stream));
+    GEFEN_HIP(launch_muon_norm(st->muon_tile_ss, st->muon_tile_range, st->n_tensors,
                                host_bf16_value(static_cast<float>(ns_eps)), st->muon_norm, stream));
     if (prof) GEFEN_HIP(hipEventRecord(ev[1], stream));
     const float decay = static_cast<float>(1.0 - lr * weight_decay);

@@ -149,12 +149,14 @@ hipError_t launch_partition(const PartDesc* descs, int32_t n_desc, int64_t n_ite
 // Gefen-Muon. Codec tiles carry their mode in Tile::vpl (0: the workgroup on one block,
 // 1: one lane per block, 2: one wave per block). u: bfloat16 momentum matrix at each
 // element's code index; tile_ss: per-tile sum of u^2.
-hipError_t launch_muon_codec(int code_bits, const Tile* tiles, int64_t n_tiles, const Seg* segs,
+// All tiles must belong to tensors whose gradients have dtype gdtype.
+hipError_t launch_muon_codec(int code_bits, int gdtype, const Tile* tiles, int64_t n_tiles,
+                             const Seg* segs,
                              uint8_t* codes, float* scale, CodebookDev cb, float mu,
                              float one_minus_mu, int nesterov, uint16_t* u, float* tile_ss,
                              hipStream_t stream);
-// norm[t] = max(bf16(sqrt(sum of tile_ss over tensor t's tiles)), eps_bf16)
-hipError_t launch_muon_norm(const float* tile_ss, const int64_t* tile_first, int32_t n_tensors,
+// norm[t] = max(bf16(sqrt(sum of tile_ss over [tile_range[2t], tile_range[2t+1]))), eps_bf16)
+hipError_t launch_muon_norm(const float* tile_ss, const int64_t* tile_range, int32_t n_tensors,
                             float eps_bf16, float* norm, hipStream_t stream);
 // x[b] = bf16(u of tensor tensor_of[b] / norm), R x C, transposed to C x R when R > C
 hipError_t launch_muon_prep(const uint16_t* u, const Seg* segs, const int32_t* tensor_of,

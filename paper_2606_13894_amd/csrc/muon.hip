@@ -19,15 +19,15 @@ __device__ __forceinline__ uint16_t to_bf16(float x)
     return static_cast<uint16_t>((b + 0x7FFFu + ((b >> 16) & 1u)) >> 16);
 }
 
-// One workgroup per tensor: norm = bf16(sqrt(sum of its tiles' u^2)), clamped below by
-// bf16(eps), summed in a fixed order (float64).
+// One workgroup per tensor: norm = bf16(sqrt(sum of u^2 over its tiles [tile_range[2t],
+// tile_range[2t+1]))), clamped below by bf16(eps), summed in a fixed order (float64).
 __global__ __launch_bounds__(256) void k_muon_norm(const float* __restrict__ tile_ss,
-                                                   const int64_t* __restrict__ tile_first,
+                                                   const int64_t* __restrict__ tile_range,
                                                    float eps_bf16, float* __restrict__ norm)
 {
     __shared__ double red[256];
     const int t = blockIdx.x;
-    const int64_t a = tile_first[t], b = tile_first[t + 1];
+    const int64_t a = tile_range[2 * t], b = tile_range[2 * t + 1];
     double acc = 0.0;
     for (int64_t i = a + threadIdx.x; i < b; i += 256) acc += static_cast<double>(tile_ss[i]);
     red[threadIdx.x] = acc;
@@ -81,6 +81,68 @@ __global__ __launch_bounds__(256) void k_muon_prep(const uint16_t* __restrict__ 
             const int64_t c = c0 + i, r = r0 + tx;
             if (r < R && c < C) dst[c * R + r] = tile[tx][i];
         }
+    }
+}
+
+// Untransposed orientation (R <= C): the same copy and update as flat element loops,
+// eight bfloat16 (prep) or four parameters (update) per thread where sizes and pointers
+// are aligned, element by element otherwise.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
+typedef float f32x4v __attribute__((ext_vector_type(4)));
+
+__global__ __launch_bounds__(256) void k_muon_prep_flat(const uint16_t* __restrict__ u,
+                                                        const Seg* __restrict__ segs,
+                                                        const int32_t* __restrict__ tensor_of,
+                                                        const float* __restrict__ norm,
+                                                        int64_t n, uint16_t* __restrict__ x)
+{
+    const int b = blockIdx.y;
+    const int t = tensor_of[b];
+    const uint16_t* __restrict__ src = u + segs[t].code_off;
+    uint16_t* __restrict__ dst = x + static_cast<int64_t>(b) * n;
+    const float nrm = norm[t];
+    const int64_t stride = 256LL * gridDim.x;
+    if ((n & 7) == 0) {
+        for (int64_t v = blockIdx.x * 256LL + threadIdx.x; v < n / 8; v += stride) {
+            const u32x4 w = reinterpret_cast<const u32x4*>(src)[v];
+            u32x4 o;
+            for (int c = 0; c < 4; ++c) {
+                const uint32_t lo = to_bf16(bf16_val(static_cast<uint16_t>(w[c] & 0xffffu)) / nrm);
+                const uint32_t hi = to_bf16(bf16_val(static_cast<uint16_t>(w[c] >> 16)) / nrm);
+                o[c] = lo | (hi << 16);
+            }
+            reinterpret_cast<u32x4*>(dst)[v] = o;
+        }
+    } else {
+        for (int64_t i = blockIdx.x * 256LL + threadIdx.x; i < n; i += stride)
+            dst[i] = to_bf16(bf16_val(src[i]) / nrm);
+    }
+}
+
+__global__ __launch_bounds__(256) void k_muon_update_flat(const uint16_t* __restrict__ o,
+                                                          const Seg* __restrict__ segs,
+                                                          const int32_t* __restrict__ tensor_of,
+                                                          int64_t n, float decay, float step)
+{
+    const int b = blockIdx.y;
+    const int t = tensor_of[b];
+    float* __restrict__ th = segs[t].theta;
+    const uint16_t* __restrict__ src = o + static_cast<int64_t>(b) * n;
+    const int64_t stride = 256LL * gridDim.x;
+    if ((n & 3) == 0 && (reinterpret_cast<uintptr_t>(th) & 15) == 0) {
+        for (int64_t v = blockIdx.x * 256LL + threadIdx.x; v < n / 4; v += stride) {
+            const u32x2v w = reinterpret_cast<const u32x2v*>(src)[v];
+            f32x4v tv = reinterpret_cast<const f32x4v*>(th)[v];
+            tv.x = fmaf(-step, bf16_val(static_cast<uint16_t>(w.x & 0xffffu)), tv.x * decay);
+            tv.y = fmaf(-step, bf16_val(static_cast<uint16_t>(w.x >> 16)), tv.y * decay);
+            tv.z = fmaf(-step, bf16_val(static_cast<uint16_t>(w.y & 0xffffu)), tv.z * decay);
+            tv.w = fmaf(-step, bf16_val(static_cast<uint16_t>(w.y >> 16)), tv.w * decay);
+            reinterpret_cast<f32x4v*>(th)[v] = tv;
+        }
+    } else {
+        for (int64_t i = blockIdx.x * 256LL + threadIdx.x; i < n; i += stride)
+            th[i] = fmaf(-step, bf16_val(src[i]), th[i] * decay);
     }
 }
 
@@ -165,11 +227,11 @@ __global__ __launch_bounds__(256) void k_muon_ns_vec(uint16_t* __restrict__ x, i
 
 }  // namespace
 
-hipError_t launch_muon_norm(const float* tile_ss, const int64_t* tile_first, int32_t n_tensors,
+hipError_t launch_muon_norm(const float* tile_ss, const int64_t* tile_range, int32_t n_tensors,
                             float eps_bf16, float* norm, hipStream_t stream)
 {
     if (n_tensors <= 0) return hipSuccess;
-    hipLaunchKernelGGL(k_muon_norm, dim3(n_tensors), dim3(256), 0, stream, tile_ss, tile_first,
+    hipLaunchKernelGGL(k_muon_norm, dim3(n_tensors), dim3(256), 0, stream, tile_ss, tile_range,
                        eps_bf16, norm);
     return hipGetLastError();
 }
@@ -180,11 +242,25 @@ static dim3 tile_grid(int64_t R, int64_t C, int batch)
                 static_cast<unsigned>(batch));
 }
 
+static dim3 flat_grid(int64_t n, int batch)
+{
+    int64_t g = (n + 2047) / 2048;
+    if (g > 4096) g = 4096;
+    if (g < 1) g = 1;
+    return dim3(static_cast<unsigned>(g), static_cast<unsigned>(batch));
+}
+
 hipError_t launch_muon_prep(const uint16_t* u, const Seg* segs, const int32_t* tensor_of,
                             int32_t batch, const float* norm, int64_t R, int64_t C,
                             uint16_t* x, hipStream_t stream)
 {
     if (batch <= 0) return hipSuccess;
+    if (batch > 65535) return hipErrorInvalidValue;
+    if (R <= C) {
+        hipLaunchKernelGGL(k_muon_prep_flat, flat_grid(R * C, batch), dim3(256), 0, stream, u,
+                           segs, tensor_of, norm, R * C, x);
+        return hipGetLastError();
+    }
     if ((R + kT - 1) / kT > 65535 || batch > 65535) return hipErrorInvalidValue;
     hipLaunchKernelGGL(k_muon_prep, tile_grid(R, C, batch), dim3(256), 0, stream, u, segs,
                        tensor_of, norm, R, C, R > C ? 1 : 0, x);
@@ -196,6 +272,12 @@ hipError_t launch_muon_update(const uint16_t* o, const Seg* segs, const int32_t*
                               hipStream_t stream)
 {
     if (batch <= 0) return hipSuccess;
+    if (batch > 65535) return hipErrorInvalidValue;
+    if (R <= C) {
+        hipLaunchKernelGGL(k_muon_update_flat, flat_grid(R * C, batch), dim3(256), 0, stream, o,
+                           segs, tensor_of, R * C, decay, step);
+        return hipGetLastError();
+    }
     if ((R + kT - 1) / kT > 65535 || batch > 65535) return hipErrorInvalidValue;
     hipLaunchKernelGGL(k_muon_update, tile_grid(R, C, batch), dim3(256), 0, stream, o, segs,
                        tensor_of, R, C, R > C ? 1 : 0, decay, step);

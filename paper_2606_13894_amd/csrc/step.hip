@@ -842,34 +842,93 @@ struct MuonOut {
     int nesterov;
 };
 
-// Second pass over one block: encode, write u, return the block's sum of u^2.
+// One element of the output pass: encode, write u, return u^2 (of the bfloat16 value).
 template <int CB>
-__device__ __forceinline__ float muon_block_out(const LdsTables& L, const Seg& sg,
-                                                uint8_t* __restrict__ codes, int64_t start,
-                                                int64_t len, int64_t i0, int64_t di,
-                                                float s_old, float s_new,
-                                                const StepScalars& sc, const MuonOut& mo,
-                                                float half_ng, int ng_m1)
+__device__ __forceinline__ float muon_elem_out(const LdsTables& L, uint8_t* __restrict__ codes,
+                                               int64_t j, float g, float s_old, float s_new,
+                                               float inv_s, const StepScalars& sc,
+                                               const MuonOut& mo, float half_ng, int ng_m1)
 {
+    const int q0 = code_ld<CB>(codes, j);
+    const float mm = momentum(L, q0, s_old, g, sc);
+    const int q = s_new > 0.0f ? encode(L, mm * inv_s, half_ng, ng_m1) : 0;
+    code_st<CB>(codes, j, q0, q);
+    const float uu = mo.nesterov ? fmaf(mo.mu, mm, mo.one_minus_mu * g) : mm;
+    const uint16_t ub = bf16_rne(uu);
+    mo.u[j] = ub;
+    const float ur = __uint_as_float(static_cast<uint32_t>(ub) << 16);
+    return ur * ur;
+}
+
+// Both passes of a block by BS threads (a wave or the workgroup; tid = index among them)
+// over the Span layout of the streamed step: 4-element vectors over the aligned body
+// (16- or 8-byte gradient loads, one code word, one 8-byte store of four bfloat16 u),
+// elements at the head and tail. absmax_pass returns the thread's max |m|.
+template <int GDT, int BS, int CB>
+__device__ __forceinline__ float muon_absmax_pass(const LdsTables& L, const Seg& sg,
+                                                  const uint8_t* __restrict__ codes,
+                                                  const Span& sp, float s_old,
+                                                  const StepScalars& sc, int tid)
+{
+    const int64_t cj = sg.code_off;
+    float am = 0.0f;
+#pragma unroll 2
+    for (int64_t v = sp.vb + tid; v < sp.ve; v += BS) {
+        float g[4];
+        load_grad4<GDT>(sg, v, g);
+        const uint32_t q4 = code_ld4<CB>(codes, cj + 4 * v);
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+            am = fmaxf(am, fabsf(momentum(L, code_get<CB>(q4, c), s_old, g[c], sc)));
+    }
+    for (int64_t i = tid; i < sp.nh + sp.nt; i += BS) {
+        const int64_t e = i < sp.nh ? sp.start + i : sp.tail0 + (i - sp.nh);
+        const float g = load_grad(sg.grad, e, GDT);
+        am = fmaxf(am, fabsf(momentum(L, code_ld<CB>(codes, cj + e), s_old, g, sc)));
+    }
+    return am;
+}
+
+template <int GDT, int BS, int CB>
+__device__ __forceinline__ float muon_out_pass(const LdsTables& L, const Seg& sg,
+                                               uint8_t* __restrict__ codes, const Span& sp,
+                                               float s_old, float s_new, const StepScalars& sc,
+                                               const MuonOut& mo, float half_ng, int ng_m1,
+                                               int tid)
+{
+    const int64_t cj = sg.code_off;
     const float inv_s = s_new > 0.0f ? 1.0f / s_new : 0.0f;
-    const int64_t cj = sg.code_off + start;
     float uss = 0.0f;
-    for (int64_t i = i0; i < len; i += di) {
-        const float g = load_grad(sg.grad, start + i, sg.gdtype);
-        const int q0 = code_ld<CB>(codes, cj + i);
-        const float mm = momentum(L, q0, s_old, g, sc);
-        const int q = s_new > 0.0f ? encode(L, mm * inv_s, half_ng, ng_m1) : 0;
-        code_st<CB>(codes, cj + i, q0, q);
-        const float uu = mo.nesterov ? fmaf(mo.mu, mm, mo.one_minus_mu * g) : mm;
-        const uint16_t ub = bf16_rne(uu);
-        mo.u[cj + i] = ub;
-        const float ur = __uint_as_float(static_cast<uint32_t>(ub) << 16);
-        uss = fmaf(ur, ur, uss);
+#pragma unroll 2
+    for (int64_t v = sp.vb + tid; v < sp.ve; v += BS) {
+        float g[4];
+        load_grad4<GDT>(sg, v, g);
+        const uint32_t q4 = code_ld4<CB>(codes, cj + 4 * v);
+        uint32_t packed = 0;
+        uint32_t ub[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const float mm = momentum(L, code_get<CB>(q4, c), s_old, g[c], sc);
+            const int q = s_new > 0.0f ? encode(L, mm * inv_s, half_ng, ng_m1) : 0;
+            packed |= static_cast<uint32_t>(q) << (CB * c);
+            const float uu = mo.nesterov ? fmaf(mo.mu, mm, mo.one_minus_mu * g[c]) : mm;
+            ub[c] = bf16_rne(uu);
+            const float ur = __uint_as_float(ub[c] << 16);
+            uss = fmaf(ur, ur, uss);
+        }
+        code_st4<CB>(codes, cj + 4 * v, packed);
+        const u32x2 w = {ub[0] | (ub[1] << 16), ub[2] | (ub[3] << 16)};
+        *glw<u32x2>(mo.u + cj + 4 * v) = w;
+    }
+    for (int64_t i = tid; i < sp.nh + sp.nt; i += BS) {
+        const int64_t e = i < sp.nh ? sp.start + i : sp.tail0 + (i - sp.nh);
+        uss += muon_elem_out<CB>(L, codes, cj + e, load_grad(sg.grad, e, GDT), s_old, s_new,
+                                 inv_s, sc, mo, half_ng, ng_m1);
     }
     return uss;
 }
 
-template <int CB>
+template <int GDT, int CB>
 __global__ __launch_bounds__(kThreads) void k_muon_codec(const Tile* __restrict__ tiles,
                                                          const Seg* __restrict__ segs,
                                                          uint8_t* __restrict__ codes,
@@ -892,21 +951,16 @@ __global__ __launch_bounds__(kThreads) void k_muon_codec(const Tile* __restrict_
         int64_t start, len;
         block_range(sg, tl, 0, start, len);
         const float s_old = scale[tl.blk0];
-        const int64_t cj = sg.code_off + start;
-        float am = 0.0f;
-        for (int64_t i = tid; i < len; i += kThreads) {
-            const float g = load_grad(sg.grad, start + i, sg.gdtype);
-            am = fmaxf(am, fabsf(momentum(L, code_ld<CB>(codes, cj + i), s_old, g, sc)));
-        }
+        const Span sp = make_span<GDT>(sg, start, len);
+        float am = muon_absmax_pass<GDT, kThreads, CB>(L, sg, codes, sp, s_old, sc, tid);
         for (int off = 1; off < 64; off <<= 1) am = fmaxf(am, __shfl_xor(am, off));
         if (lane == 0) L.red_am[wave] = am;
         __syncthreads();
         am = L.red_am[0];
         for (int w = 1; w < kThreads / 64; ++w) am = fmaxf(am, L.red_am[w]);
-        __syncthreads();   // red_am is reused for the tile sum below
         if (tid == 0) scale[tl.blk0] = am;
-        uss = muon_block_out<CB>(L, sg, codes, start, len, tid, kThreads, s_old, am, sc, mo,
-                                 half_ng, ng_m1);
+        uss = muon_out_pass<GDT, kThreads, CB>(L, sg, codes, sp, s_old, am, sc, mo, half_ng,
+                                               ng_m1, tid);
     } else if (tl.vpl == 1) {
         if (tid < tl.nblk) {
             int64_t start, len;
@@ -916,12 +970,14 @@ __global__ __launch_bounds__(kThreads) void k_muon_codec(const Tile* __restrict_
             const int64_t cj = sg.code_off + start;
             float am = 0.0f;
             for (int64_t i = 0; i < len; ++i) {
-                const float g = load_grad(sg.grad, start + i, sg.gdtype);
+                const float g = load_grad(sg.grad, start + i, GDT);
                 am = fmaxf(am, fabsf(momentum(L, code_ld<CB>(codes, cj + i), s_old, g, sc)));
             }
             scale[blk] = am;
-            uss = muon_block_out<CB>(L, sg, codes, start, len, 0, 1, s_old, am, sc, mo, half_ng,
-                                     ng_m1);
+            const float inv_s = am > 0.0f ? 1.0f / am : 0.0f;
+            for (int64_t i = 0; i < len; ++i)
+                uss += muon_elem_out<CB>(L, codes, cj + i, load_grad(sg.grad, start + i, GDT),
+                                         s_old, am, inv_s, sc, mo, half_ng, ng_m1);
         }
     } else {
         if (wave < tl.nblk) {
@@ -929,19 +985,15 @@ __global__ __launch_bounds__(kThreads) void k_muon_codec(const Tile* __restrict_
             block_range(sg, tl, wave, start, len);
             const int64_t blk = tl.blk0 + wave;
             const float s_old = scale[blk];
-            const int64_t cj = sg.code_off + start;
-            float am = 0.0f;
-            for (int64_t i = lane; i < len; i += 64) {
-                const float g = load_grad(sg.grad, start + i, sg.gdtype);
-                am = fmaxf(am, fabsf(momentum(L, code_ld<CB>(codes, cj + i), s_old, g, sc)));
-            }
+            const Span sp = make_span<GDT>(sg, start, len);
+            float am = muon_absmax_pass<GDT, 64, CB>(L, sg, codes, sp, s_old, sc, lane);
             for (int off = 1; off < 64; off <<= 1) am = fmaxf(am, __shfl_xor(am, off));
             if (lane == 0) scale[blk] = am;
-            uss = muon_block_out<CB>(L, sg, codes, start, len, lane, 64, s_old, am, sc, mo,
-                                     half_ng, ng_m1);
+            uss = muon_out_pass<GDT, 64, CB>(L, sg, codes, sp, s_old, am, sc, mo, half_ng, ng_m1,
+                                             lane);
         }
     }
-    // the tile's sum of u^2, fixed order
+    // the tile's sum of u^2, fixed order (red_ss is not used above)
     for (int off = 1; off < 64; off <<= 1) uss += __shfl_xor(uss, off);
     if (lane == 0) L.red_ss[wave] = uss;
     __syncthreads();
@@ -1040,7 +1092,8 @@ hipError_t launch_step(int kind, int gdtype, int code_bits, int vpl, int bs, con
                                          cb, sc, stream);
 }
 
-hipError_t launch_muon_codec(int code_bits, const Tile* tiles, int64_t n_tiles, const Seg* segs,
+hipError_t launch_muon_codec(int code_bits, int gdtype, const Tile* tiles, int64_t n_tiles,
+                             const Seg* segs,
                              uint8_t* codes, float* scale, CodebookDev cb, float mu,
                              float one_minus_mu, int nesterov, uint16_t* u, float* tile_ss,
                              hipStream_t stream)
@@ -1052,14 +1105,16 @@ hipError_t launch_muon_codec(int code_bits, const Tile* tiles, int64_t n_tiles, 
     sc.one_minus_beta1 = one_minus_mu;
     MuonOut mo{u, mu, one_minus_mu, nesterov};
     const dim3 grid(static_cast<unsigned>(n_tiles));
-    if (code_bits == 8)
-        hipLaunchKernelGGL(k_muon_codec<8>, grid, dim3(kThreads), 0, stream, tiles, segs, codes,
-                           scale, cb, sc, mo, tile_ss);
-    else if (code_bits == 4)
-        hipLaunchKernelGGL(k_muon_codec<4>, grid, dim3(kThreads), 0, stream, tiles, segs, codes,
-                           scale, cb, sc, mo, tile_ss);
-    else
-        return hipErrorInvalidValue;
+#define GEFEN_MC(G, C)                                                                      \
+    hipLaunchKernelGGL((k_muon_codec<G, C>), grid, dim3(kThreads), 0, stream, tiles, segs,  \
+                       codes, scale, cb, sc, mo, tile_ss)
+    if (code_bits != 8 && code_bits != 4) return hipErrorInvalidValue;
+    if (gdtype == DT_F32) {
+        if (code_bits == 8) GEFEN_MC(DT_F32, 8); else GEFEN_MC(DT_F32, 4);
+    } else {
+        if (code_bits == 8) GEFEN_MC(DT_BF16, 8); else GEFEN_MC(DT_BF16, 4);
+    }
+#undef GEFEN_MC
     return hipGetLastError();
 }
 
