@@ -76,17 +76,18 @@ __device__ __forceinline__ GSpan grad_span(const Seg& sg, int64_t start, int64_t
     return s;
 }
 
-// Workgroup-wide absmax over a span (per-thread partial; caller reduces).
-__device__ __forceinline__ float span_absmax(const Seg& sg, const GSpan& sp)
+// Absmax over a span by `stride` threads, this one being `tid` (per-thread partial; the
+// caller reduces).
+__device__ __forceinline__ float span_absmax(const Seg& sg, const GSpan& sp, int tid, int stride)
 {
     float a = 0.0f;
 #pragma unroll 2
-    for (int64_t v = sp.vb + threadIdx.x; v < sp.ve; v += kThreads) {
+    for (int64_t v = sp.vb + tid; v < sp.ve; v += stride) {
         float g[4];
         grad4_at(sg, v, g);
         a = fmaxf(a, fmaxf(fmaxf(fabsf(g[0]), fabsf(g[1])), fmaxf(fabsf(g[2]), fabsf(g[3]))));
     }
-    for (int64_t i = threadIdx.x; i < sp.nh + sp.nt; i += kThreads) {
+    for (int64_t i = tid; i < sp.nh + sp.nt; i += stride) {
         const int64_t e = i < sp.nh ? sp.start + i : sp.tail0 + (i - sp.nh);
         a = fmaxf(a, fabsf(grad_at(sg, e)));
     }
@@ -94,16 +95,16 @@ __device__ __forceinline__ float span_absmax(const Seg& sg, const GSpan& sp)
 }
 
 __device__ __forceinline__ void span_bins(const Seg& sg, const GSpan& sp, float a, double half_nb,
-                                          int nbins, uint32_t* h)
+                                          int nbins, uint32_t* h, int tid, int stride)
 {
 #pragma unroll 2
-    for (int64_t v = sp.vb + threadIdx.x; v < sp.ve; v += kThreads) {
+    for (int64_t v = sp.vb + tid; v < sp.ve; v += stride) {
         float g[4];
         grad4_at(sg, v, g);
 #pragma unroll
         for (int c = 0; c < 4; ++c) atomicAdd(&h[bin_of(g[c], a, half_nb, nbins)], 1u);
     }
-    for (int64_t i = threadIdx.x; i < sp.nh + sp.nt; i += kThreads) {
+    for (int64_t i = tid; i < sp.nh + sp.nt; i += stride) {
         const int64_t e = i < sp.nh ? sp.start + i : sp.tail0 + (i - sp.nh);
         atomicAdd(&h[bin_of(grad_at(sg, e), a, half_nb, nbins)], 1u);
     }
@@ -132,7 +133,7 @@ __global__ __launch_bounds__(kThreads) void k_hist_h_absmax(const Tile* __restri
     const Tile tl = tiles[blockIdx.x];
     const HTile ht = htiles[blockIdx.x];
     const Seg sg = segs[tl.seg];
-    float a = span_absmax(sg, grad_span(sg, tl.elem0, tl.nelem));
+    float a = span_absmax(sg, grad_span(sg, tl.elem0, tl.nelem), threadIdx.x, kThreads);
     for (int off = 1; off < 64; off <<= 1) a = fmaxf(a, __shfl_xor(a, off));
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = a;
     __syncthreads();
@@ -152,7 +153,6 @@ __global__ __launch_bounds__(kThreads) void k_histogram(const Tile* __restrict__
                                                         uint64_t* __restrict__ hist)
 {
     __shared__ uint32_t h[kMaxBins];
-    __shared__ float red[kThreads / 64];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
@@ -160,15 +160,19 @@ __global__ __launch_bounds__(kThreads) void k_histogram(const Tile* __restrict__
     __syncthreads();
     const double half_nb = 0.5 * static_cast<double>(nbins);
 
-    for (int64_t ti = blockIdx.x; ti < n_tiles; ti += gridDim.x) {
+    // Every wave takes its own tiles (wave-strided persistent loop) and reduces within
+    // itself, so no barrier is needed until the flush.
+    constexpr int kWaves = kThreads / 64;
+    for (int64_t ti = static_cast<int64_t>(blockIdx.x) * kWaves + wave; ti < n_tiles;
+         ti += static_cast<int64_t>(gridDim.x) * kWaves) {
         const Tile tl = tiles[ti];
         const Seg sg = segs[tl.seg];
         const int kind = tile_kind[ti];
         if (kind == KIND_L) {
             // one lane per small block
-            if (tid < tl.nblk) {
+            for (int bi = lane; bi < tl.nblk; bi += 64) {
                 int64_t start, len;
-                tile_block(sg, tl, tid, start, len);
+                tile_block(sg, tl, bi, start, len);
                 float a = 0.0f;
                 for (int64_t i = 0; i < len; ++i) a = fmaxf(a, fabsf(grad_at(sg, start + i)));
                 if (a > 0.0f)
@@ -179,32 +183,19 @@ __global__ __launch_bounds__(kThreads) void k_histogram(const Tile* __restrict__
             // one chunk of a huge block: block absmax from the chunk maxima
             const HTile ht = htiles[ti];
             float a = 0.0f;
-            for (int c = 0; c < ht.nchunk; ++c) a = fmaxf(a, am_partials[ht.first + c]);
-            if (a > 0.0f) span_bins(sg, grad_span(sg, tl.elem0, tl.nelem), a, half_nb, nbins, h);
-        } else if (tl.nblk == 1) {
-            // the whole workgroup on one block
-            int64_t start, len;
-            tile_block(sg, tl, 0, start, len);
-            const GSpan sp = grad_span(sg, start, len);
-            float a = span_absmax(sg, sp);
+            for (int c = lane; c < ht.nchunk; c += 64) a = fmaxf(a, am_partials[ht.first + c]);
             for (int off = 1; off < 64; off <<= 1) a = fmaxf(a, __shfl_xor(a, off));
-            if (lane == 0) red[wave] = a;
-            __syncthreads();
-            a = red[0];
-            for (int w = 1; w < kThreads / 64; ++w) a = fmaxf(a, red[w]);
-            if (a > 0.0f) span_bins(sg, sp, a, half_nb, nbins, h);
-            __syncthreads();   // red[] is reused by the next tile
+            if (a > 0.0f)
+                span_bins(sg, grad_span(sg, tl.elem0, tl.nelem), a, half_nb, nbins, h, lane, 64);
         } else {
-            // one wave per block
-            for (int bi = wave; bi < tl.nblk; bi += kThreads / 64) {
+            // the tile's blocks one after another, each by the whole wave
+            for (int bi = 0; bi < tl.nblk; ++bi) {
                 int64_t start, len;
                 tile_block(sg, tl, bi, start, len);
-                float a = 0.0f;
-                for (int64_t i = lane; i < len; i += 64) a = fmaxf(a, fabsf(grad_at(sg, start + i)));
+                const GSpan sp = grad_span(sg, start, len);
+                float a = span_absmax(sg, sp, lane, 64);
                 for (int off = 1; off < 64; off <<= 1) a = fmaxf(a, __shfl_xor(a, off));
-                if (a > 0.0f)
-                    for (int64_t i = lane; i < len; i += 64)
-                        atomicAdd(&h[bin_of(grad_at(sg, start + i), a, half_nb, nbins)], 1u);
+                if (a > 0.0f) span_bins(sg, sp, a, half_nb, nbins, h, lane, 64);
             }
         }
     }
@@ -496,7 +487,8 @@ hipError_t launch_histogram(const Tile* tiles, int64_t n_tiles, const int32_t* t
                             int32_t nbins, uint64_t* hist, hipStream_t stream)
 {
     if (n_tiles <= 0) return hipSuccess;
-    const int64_t g = n_tiles < 4096 ? n_tiles : 4096;
+    const int64_t w = (n_tiles + kThreads / 64 - 1) / (kThreads / 64);
+    const int64_t g = w < 4096 ? w : 4096;
     hipLaunchKernelGGL(k_histogram, dim3(static_cast<unsigned>(g)), dim3(kThreads), 0, stream,
                        tiles, n_tiles, tile_kind, htiles, am_partials, segs, nbins, hist);
     return hipGetLastError();
