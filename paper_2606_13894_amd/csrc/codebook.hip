@@ -214,10 +214,16 @@ __global__ __launch_bounds__(kThreads) void k_histogram(const Tile* __restrict__
 //   Z0,Z1,Z2,cnt,ctr   double[NB + 1] each (1-based, index 0 = 0)
 //   D      double[(k + 1) * (NB + 1)]   D[j][r]
 //   split  uint16[(k + 1) * (NB + 1)]
+//   pv, pa double / int32 [2][NB + 1][kDpMaxChunks]: per-chunk partial minima of a level
 // ---------------------------------------------------------------------------------
 struct DpLayout {
-    size_t hdr, z0, z1, z2, cnt, ctr, d, split, total;
+    size_t hdr, z0, z1, z2, cnt, ctr, d, split, pv, pa, total;
 };
+
+constexpr int kDpThreads = 1024;
+constexpr int kDpRows = kDpThreads / 64;                        // rows r per workgroup
+constexpr int kDpChunk = 1024;                                  // l values per workgroup
+constexpr int kDpMaxChunks = (kMaxBins + kDpChunk - 1) / kDpChunk;
 
 __host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
@@ -234,6 +240,8 @@ __host__ __device__ inline DpLayout dp_layout(int32_t nbins, int32_t k)
     L.ctr = o; o += align256(row * sizeof(double));
     L.d = o; o += align256(static_cast<size_t>(k + 1) * row * sizeof(double));
     L.split = o; o += align256(static_cast<size_t>(k + 1) * row * sizeof(uint16_t));
+    L.pv = o; o += align256(2 * row * kDpMaxChunks * sizeof(double));
+    L.pa = o; o += align256(2 * row * kDpMaxChunks * sizeof(int32_t));
     L.total = o;
     return L;
 }
@@ -290,18 +298,44 @@ __global__ __launch_bounds__(kThreads) void k_dp_prep(const uint64_t* __restrict
     hdr[2] = r >= k ? 0 : 1;
 }
 
-// One DP level j: D[j][r] = min_{l in [j, r]} D[j-1][l-1] + C(l, r, j), ties to the
-// smallest l. A workgroup owns kDpRows consecutive right boundaries r, one per wave; it
-// stages the prefix sums and row j-1 of D over the index range it needs in LDS, so the
-// O(b) candidates per r read LDS instead of L2. Lanes stride over l keeping their first
-// minimum; a shuffle reduction then picks the smallest (value, l).
-constexpr int kDpThreads = 1024;
-constexpr int kDpRows = kDpThreads / 64;
+// ---------------------------------------------------------------------------------
+// DP level j: D[j][r] = min over l of D[j-1][l-1] + C(l, r), argmin to the smallest l.
+// Workgroup (x, y) takes rows r0 .. r0 + 15 (one wave each) and the candidates l of
+// chunk y, [j + 1024 y, j + 1024 y + 1023], staging Z[l-1] and D[j-1][l-1] for that
+// chunk in LDS (32 KB), so every workgroup does at most 16 x 1024 evaluations. It writes
+// a partial (min, argmin) per row and chunk (double-buffered by level parity); level
+// j + 1 rebuilds D[j][.] from them while staging, in chunk order with ties to the
+// smaller l, and its last row of workgroups (whose chunks cover every l) stores the
+// final D[j][.] and split[j][.] rows for the backtrack. k_dp_final reduces the last
+// level.
+// ---------------------------------------------------------------------------------
+__device__ __forceinline__ int dp_chunks(int jj, int r)
+{
+    const int hi = jj == 1 ? 1 : r;
+    return hi < jj ? 0 : (hi - jj) / kDpChunk + 1;
+}
+
+__device__ __forceinline__ void dp_reduce(const double* __restrict__ pv,
+                                          const int32_t* __restrict__ pa, int jj, int r,
+                                          double& v, int& a)
+{
+    v = INFINITY;
+    a = 0x7fffffff;
+    const int nc = dp_chunks(jj, r);
+    for (int c = 0; c < nc; ++c) {
+        const double x = pv[static_cast<size_t>(r) * kDpMaxChunks + c];
+        const int y = pa[static_cast<size_t>(r) * kDpMaxChunks + c];
+        if (x < v || (x == v && y < a)) {
+            v = x;
+            a = y;
+        }
+    }
+}
 
 __global__ __launch_bounds__(kDpThreads) void k_dp_level(int32_t nbins, int32_t k, int32_t j,
                                                          void* ws)
 {
-    __shared__ double sh[4 * (kMaxBins + 1)];
+    __shared__ double sZ0[kDpChunk], sZ1[kDpChunk], sZ2[kDpChunk], sD[kDpChunk];
     const DpLayout L = dp_layout(nbins, k);
     const int32_t* hdr = at<int32_t>(ws, L.hdr);
     const int b = hdr[0];
@@ -316,39 +350,54 @@ __global__ __launch_bounds__(kDpThreads) void k_dp_level(int32_t nbins, int32_t 
         if (r0 > b) return;
         r1 = r0 + kDpRows - 1 < b ? r0 + kDpRows - 1 : b;
     }
+    const int hi_max = j == 1 ? 1 : r1;
+    const int l0 = j + static_cast<int>(blockIdx.y) * kDpChunk;
+    if (l0 > hi_max) return;
+    const int l1 = l0 + kDpChunk - 1 < hi_max ? l0 + kDpChunk - 1 : hi_max;
     const double* Z0 = at<double>(ws, L.z0);
     const double* Z1 = at<double>(ws, L.z1);
     const double* Z2 = at<double>(ws, L.z2);
     const size_t row = static_cast<size_t>(nbins) + 1;
     double* D = at<double>(ws, L.d);
     uint16_t* split = at<uint16_t>(ws, L.split);
-    const double* Dprev = D + static_cast<size_t>(j - 1) * row;
-    // indices base .. r1 of Z0, Z1, Z2 and base .. r1 - 1 of D[j-1]
-    const int base = j - 1;
-    const int span = r1 - base + 1;
-    double* sZ0 = sh;
-    double* sZ1 = sh + span;
-    double* sZ2 = sh + 2 * span;
-    double* sD = sh + 3 * span;
-    for (int i = threadIdx.x; i < span; i += kDpThreads) {
-        sZ0[i] = Z0[base + i];
-        sZ1[i] = Z1[base + i];
-        sZ2[i] = Z2[base + i];
-        sD[i] = base + i <= r1 - 1 ? Dprev[base + i] : 0.0;
+    const size_t pstride = row * kDpMaxChunks;
+    const double* pv_prev = at<double>(ws, L.pv) + ((j - 1) & 1) * pstride;
+    const int32_t* pa_prev = at<int32_t>(ws, L.pa) + ((j - 1) & 1) * pstride;
+    double* pv_cur = at<double>(ws, L.pv) + (j & 1) * pstride;
+    int32_t* pa_cur = at<int32_t>(ws, L.pa) + (j & 1) * pstride;
+    const bool last_rows = j == keff || static_cast<int>(blockIdx.x) == (b - j) / kDpRows;
+    for (int i = threadIdx.x; i <= l1 - l0; i += kDpThreads) {
+        const int l = l0 + i;
+        sZ0[i] = Z0[l - 1];
+        sZ1[i] = Z1[l - 1];
+        sZ2[i] = Z2[l - 1];
+        double dv;
+        if (j == 1) {
+            dv = l == 1 ? 0.0 : INFINITY;   // D[0][l-1]
+        } else {
+            int da;
+            dp_reduce(pv_prev, pa_prev, j - 1, l - 1, dv, da);
+            if (last_rows) {
+                D[static_cast<size_t>(j - 1) * row + (l - 1)] = dv;
+                split[static_cast<size_t>(j - 1) * row + (l - 1)] = static_cast<uint16_t>(da);
+            }
+        }
+        sD[i] = dv;
     }
     __syncthreads();
     const int r = r0 + static_cast<int>(threadIdx.x >> 6);
     if (r > r1) return;
     const int lane = threadIdx.x & 63;
-    const double zr0 = sZ0[r - base], zr1 = sZ1[r - base], zr2 = sZ2[r - base];
+    const double zr0 = Z0[r], zr1 = Z1[r], zr2 = Z2[r];
+    const int hi = j == 1 ? 1 : r;
     double best = INFINITY;
     int arg = 0x7fffffff;
-    const int hi = j == 1 ? 1 : r;   // level 1 can only start at bin 1 (D[0][l-1] = inf otherwise)
-    for (int l = j + lane; l <= hi; l += 64) {
-        const int o = l - 1 - base;
-        const double S0 = zr0 - sZ0[o];
-        const double S1 = zr1 - sZ1[o];
-        const double S2 = zr2 - sZ2[o];
+    for (int i = lane; i <= l1 - l0; i += 64) {   // increasing l: first minimum kept
+        const int l = l0 + i;
+        if (l > hi) break;
+        const double S0 = zr0 - sZ0[i];
+        const double S1 = zr1 - sZ1[i];
+        const double S2 = zr2 - sZ2[i];
         double c;
         if (j == 1 || j == keff) {
             const double a = j == 1 ? -1.0 : 1.0;
@@ -356,7 +405,7 @@ __global__ __launch_bounds__(kDpThreads) void k_dp_level(int32_t nbins, int32_t 
         } else {
             c = S2 - S1 * S1 / S0;
         }
-        const double cand = sD[o] + c;
+        const double cand = sD[i] + c;
         if (cand < best) {
             best = cand;
             arg = l;
@@ -371,9 +420,28 @@ __global__ __launch_bounds__(kDpThreads) void k_dp_level(int32_t nbins, int32_t 
         }
     }
     if (lane == 0) {
-        D[static_cast<size_t>(j) * row + r] = best;
-        split[static_cast<size_t>(j) * row + r] = static_cast<uint16_t>(arg);
+        pv_cur[static_cast<size_t>(r) * kDpMaxChunks + blockIdx.y] = best;
+        pa_cur[static_cast<size_t>(r) * kDpMaxChunks + blockIdx.y] = arg;
     }
+}
+
+// The last level's result for r = b.
+__global__ void k_dp_final(int32_t nbins, int32_t k, void* ws)
+{
+    if (threadIdx.x != 0) return;
+    const DpLayout L = dp_layout(nbins, k);
+    const int32_t* hdr = at<int32_t>(ws, L.hdr);
+    const int b = hdr[0];
+    const int keff = hdr[1];
+    if (keff < 2) return;
+    const size_t row = static_cast<size_t>(nbins) + 1;
+    const size_t pstride = row * kDpMaxChunks;
+    double v;
+    int a;
+    dp_reduce(at<double>(ws, L.pv) + (keff & 1) * pstride,
+              at<int32_t>(ws, L.pa) + (keff & 1) * pstride, keff, b, v, a);
+    at<double>(ws, L.d)[static_cast<size_t>(keff) * row + b] = v;
+    at<uint16_t>(ws, L.split)[static_cast<size_t>(keff) * row + b] = static_cast<uint16_t>(a);
 }
 
 // Backtracking (one thread): entry j is -1, +1 or the weighted mean of its interval;
@@ -499,9 +567,11 @@ hipError_t launch_dp(const uint64_t* hist, int32_t nbins, int32_t k, void* ws,
                      hipStream_t stream)
 {
     hipLaunchKernelGGL(k_dp_prep, dim3(1), dim3(kThreads), 0, stream, hist, nbins, k, ws);
-    const unsigned grid = (static_cast<unsigned>(nbins) + kDpRows - 1) / kDpRows;
+    const dim3 grid((static_cast<unsigned>(nbins) + kDpRows - 1) / kDpRows,
+                    (static_cast<unsigned>(nbins) + kDpChunk - 1) / kDpChunk);
     for (int j = 1; j <= k; ++j)
-        hipLaunchKernelGGL(k_dp_level, dim3(grid), dim3(kDpThreads), 0, stream, nbins, k, j, ws);
+        hipLaunchKernelGGL(k_dp_level, grid, dim3(kDpThreads), 0, stream, nbins, k, j, ws);
+    hipLaunchKernelGGL(k_dp_final, dim3(1), dim3(64), 0, stream, nbins, k, ws);
     hipLaunchKernelGGL(k_dp_backtrack, dim3(1), dim3(64), 0, stream, nbins, k, ws,
                        codebook_out, cost_out, status_out);
     return hipGetLastError();
