@@ -40,7 +40,7 @@ METRIC = "optimizer-step Gparams/s and achieved HBM GB/s (% of MI355X peak), 1 G
 
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
-    for name in ("step.hip", "gefen_internal.h"):
+    for name in ("step.hip", "step_device.h", "gefen_internal.h"):
         with open(os.path.join(ROOT, "paper_2606_13894_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]

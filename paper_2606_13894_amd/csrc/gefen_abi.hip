@@ -3,6 +3,7 @@
 // partition.hip); this file decides which kernel processes which part of which tensor.
 #include "gefen.h"
 #include "gefen_internal.h"
+#include "muon_internal.h"
 
 #include <rocblas/rocblas.h>
 

@@ -1,9 +1,10 @@
-// Gefen-Muon (appendix "Gefen-Muon"), the parts around the orthogonalisation: the
-// Frobenius norm of each momentum matrix, its normalised bfloat16 copy in the wide
-// orientation (the Newton-Schulz input), and the parameter update from the result.
-// The momentum codec itself lives with the step kernels; the Newton-Schulz matrix
-// products are plain bfloat16 GEMMs (rocBLAS), driven from the host.
-#include "gefen_internal.h"
+// Gefen-Muon (appendix "Gefen-Muon") on the device: the codec that keeps Muon's
+// momentum in Gefen's quantized form, the Frobenius norm of each momentum matrix, its
+// normalised bfloat16 copy in the wide orientation (the Newton-Schulz input), and the
+// parameter update from the orthogonalised result. The Newton-Schulz matrix products
+// are plain bfloat16 GEMMs (rocBLAS), driven from the host.
+#include "muon_internal.h"
+#include "step_device.h"
 
 namespace gefen {
 namespace {
@@ -39,6 +40,183 @@ __global__ __launch_bounds__(256) void k_muon_norm(const float* __restrict__ til
     if (threadIdx.x == 0) {
         const float nv = bf16_val(to_bf16(static_cast<float>(sqrt(red[0]))));
         norm[t] = fmaxf(nv, eps_bf16);
+    }
+}
+
+// ---------------------------------------------------------------------------------
+// Gefen-Muon codec (appendix "Gefen-Muon"): Muon's momentum held in Gefen's quantized
+// form. Per block: m = mu * c_dec[q] * s + (1 - mu) * g, s' = max |m|,
+// q' = nearest(c_enc, m / s'); the matrix handed to the orthogonalisation is
+// u = nesterov ? (1 - mu) * g + mu * m : m, written as bfloat16 at the code index of
+// each element, and each tile's sum of u^2 (of the bfloat16 values) goes to tile_ss.
+// Tile mode in Tile::vpl: 0 = the workgroup on one block, 1 = one lane per block,
+// 2 = one wave per block.
+// ---------------------------------------------------------------------------------
+struct MuonOut {
+    uint16_t* u;
+    float mu, one_minus_mu;
+    int nesterov;
+};
+
+// One element of the output pass: encode, write u, return u^2 (of the bfloat16 value).
+template <int CB>
+__device__ __forceinline__ float muon_elem_out(const LdsTables& L, uint8_t* __restrict__ codes,
+                                               int64_t j, float g, float s_old, float s_new,
+                                               float inv_s, const StepScalars& sc,
+                                               const MuonOut& mo, float half_ng, int ng_m1)
+{
+    const int q0 = code_ld<CB>(codes, j);
+    const float mm = momentum(L, q0, s_old, g, sc);
+    const int q = s_new > 0.0f ? encode(L, mm * inv_s, half_ng, ng_m1) : 0;
+    code_st<CB>(codes, j, q0, q);
+    const float uu = mo.nesterov ? fmaf(mo.mu, mm, mo.one_minus_mu * g) : mm;
+    const uint16_t ub = to_bf16(uu);
+    mo.u[j] = ub;
+    const float ur = __uint_as_float(static_cast<uint32_t>(ub) << 16);
+    return ur * ur;
+}
+
+// Both passes of a block by BS threads (a wave or the workgroup; tid = index among them)
+// over the Span layout of the streamed step: 4-element vectors over the aligned body
+// (16- or 8-byte gradient loads, one code word, one 8-byte store of four bfloat16 u),
+// elements at the head and tail. absmax_pass returns the thread's max |m|.
+template <int GDT, int BS, int CB>
+__device__ __forceinline__ float muon_absmax_pass(const LdsTables& L, const Seg& sg,
+                                                  const uint8_t* __restrict__ codes,
+                                                  const Span& sp, float s_old,
+                                                  const StepScalars& sc, int tid)
+{
+    const int64_t cj = sg.code_off;
+    float am = 0.0f;
+#pragma unroll 2
+    for (int64_t v = sp.vb + tid; v < sp.ve; v += BS) {
+        float g[4];
+        load_grad4<GDT>(sg, v, g);
+        const uint32_t q4 = code_ld4<CB>(codes, cj + 4 * v);
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+            am = fmaxf(am, fabsf(momentum(L, code_get<CB>(q4, c), s_old, g[c], sc)));
+    }
+    for (int64_t i = tid; i < sp.nh + sp.nt; i += BS) {
+        const int64_t e = i < sp.nh ? sp.start + i : sp.tail0 + (i - sp.nh);
+        const float g = load_grad(sg.grad, e, GDT);
+        am = fmaxf(am, fabsf(momentum(L, code_ld<CB>(codes, cj + e), s_old, g, sc)));
+    }
+    return am;
+}
+
+template <int GDT, int BS, int CB>
+__device__ __forceinline__ float muon_out_pass(const LdsTables& L, const Seg& sg,
+                                               uint8_t* __restrict__ codes, const Span& sp,
+                                               float s_old, float s_new, const StepScalars& sc,
+                                               const MuonOut& mo, float half_ng, int ng_m1,
+                                               int tid)
+{
+    const int64_t cj = sg.code_off;
+    const float inv_s = s_new > 0.0f ? 1.0f / s_new : 0.0f;
+    float uss = 0.0f;
+#pragma unroll 2
+    for (int64_t v = sp.vb + tid; v < sp.ve; v += BS) {
+        float g[4];
+        load_grad4<GDT>(sg, v, g);
+        const uint32_t q4 = code_ld4<CB>(codes, cj + 4 * v);
+        uint32_t packed = 0;
+        uint32_t ub[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const float mm = momentum(L, code_get<CB>(q4, c), s_old, g[c], sc);
+            const int q = s_new > 0.0f ? encode(L, mm * inv_s, half_ng, ng_m1) : 0;
+            packed |= static_cast<uint32_t>(q) << (CB * c);
+            const float uu = mo.nesterov ? fmaf(mo.mu, mm, mo.one_minus_mu * g[c]) : mm;
+            ub[c] = to_bf16(uu);
+            const float ur = __uint_as_float(ub[c] << 16);
+            uss = fmaf(ur, ur, uss);
+        }
+        code_st4<CB>(codes, cj + 4 * v, packed);
+        const u32x2 w = {ub[0] | (ub[1] << 16), ub[2] | (ub[3] << 16)};
+        *glw<u32x2>(mo.u + cj + 4 * v) = w;
+    }
+    for (int64_t i = tid; i < sp.nh + sp.nt; i += BS) {
+        const int64_t e = i < sp.nh ? sp.start + i : sp.tail0 + (i - sp.nh);
+        uss += muon_elem_out<CB>(L, codes, cj + e, load_grad(sg.grad, e, GDT), s_old, s_new,
+                                 inv_s, sc, mo, half_ng, ng_m1);
+    }
+    return uss;
+}
+
+template <int GDT, int CB>
+__global__ __launch_bounds__(kThreads) void k_muon_codec(const Tile* __restrict__ tiles,
+                                                         const Seg* __restrict__ segs,
+                                                         uint8_t* __restrict__ codes,
+                                                         float* __restrict__ scale,
+                                                         CodebookDev cbd, StepScalars sc,
+                                                         MuonOut mo, float* __restrict__ tile_ss)
+{
+    __shared__ LdsTables L;
+    const Tile tl = tiles[blockIdx.x];
+    const Seg sg = segs[tl.seg];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    load_tables<kThreads>(L, cbd);
+    __syncthreads();
+    const float half_ng = 0.5f * static_cast<float>(cbd.ng);
+    const int ng_m1 = cbd.ng - 1;
+    float uss = 0.0f;
+    if (tl.vpl == 0) {
+        int64_t start, len;
+        block_range(sg, tl, 0, start, len);
+        const float s_old = scale[tl.blk0];
+        const Span sp = make_span<GDT>(sg, start, len);
+        float am = muon_absmax_pass<GDT, kThreads, CB>(L, sg, codes, sp, s_old, sc, tid);
+        for (int off = 1; off < 64; off <<= 1) am = fmaxf(am, __shfl_xor(am, off));
+        if (lane == 0) L.red_am[wave] = am;
+        __syncthreads();
+        am = L.red_am[0];
+        for (int w = 1; w < kThreads / 64; ++w) am = fmaxf(am, L.red_am[w]);
+        if (tid == 0) scale[tl.blk0] = am;
+        uss = muon_out_pass<GDT, kThreads, CB>(L, sg, codes, sp, s_old, am, sc, mo, half_ng,
+                                               ng_m1, tid);
+    } else if (tl.vpl == 1) {
+        if (tid < tl.nblk) {
+            int64_t start, len;
+            block_range(sg, tl, tid, start, len);
+            const int64_t blk = tl.blk0 + tid;
+            const float s_old = scale[blk];
+            const int64_t cj = sg.code_off + start;
+            float am = 0.0f;
+            for (int64_t i = 0; i < len; ++i) {
+                const float g = load_grad(sg.grad, start + i, GDT);
+                am = fmaxf(am, fabsf(momentum(L, code_ld<CB>(codes, cj + i), s_old, g, sc)));
+            }
+            scale[blk] = am;
+            const float inv_s = am > 0.0f ? 1.0f / am : 0.0f;
+            for (int64_t i = 0; i < len; ++i)
+                uss += muon_elem_out<CB>(L, codes, cj + i, load_grad(sg.grad, start + i, GDT),
+                                         s_old, am, inv_s, sc, mo, half_ng, ng_m1);
+        }
+    } else {
+        if (wave < tl.nblk) {
+            int64_t start, len;
+            block_range(sg, tl, wave, start, len);
+            const int64_t blk = tl.blk0 + wave;
+            const float s_old = scale[blk];
+            const Span sp = make_span<GDT>(sg, start, len);
+            float am = muon_absmax_pass<GDT, 64, CB>(L, sg, codes, sp, s_old, sc, lane);
+            for (int off = 1; off < 64; off <<= 1) am = fmaxf(am, __shfl_xor(am, off));
+            if (lane == 0) scale[blk] = am;
+            uss = muon_out_pass<GDT, 64, CB>(L, sg, codes, sp, s_old, am, sc, mo, half_ng, ng_m1,
+                                             lane);
+        }
+    }
+    // the tile's sum of u^2, fixed order (red_ss is not used above)
+    for (int off = 1; off < 64; off <<= 1) uss += __shfl_xor(uss, off);
+    if (lane == 0) L.red_ss[wave] = uss;
+    __syncthreads();
+    if (tid == 0) {
+        float t = L.red_ss[0];
+        for (int w = 1; w < kThreads / 64; ++w) t += L.red_ss[w];
+        tile_ss[blockIdx.x] = t;
     }
 }
 
@@ -301,6 +479,32 @@ hipError_t launch_muon_ns_vec(uint16_t* x, int32_t batch, int64_t n, int32_t ste
     if (batch <= 0 || steps <= 0) return hipSuccess;
     hipLaunchKernelGGL(k_muon_ns_vec, dim3(static_cast<unsigned>(batch)), dim3(256), 0, stream,
                        x, n, steps, a, b, c);
+    return hipGetLastError();
+}
+
+hipError_t launch_muon_codec(int code_bits, int gdtype, const Tile* tiles, int64_t n_tiles,
+                             const Seg* segs,
+                             uint8_t* codes, float* scale, CodebookDev cb, float mu,
+                             float one_minus_mu, int nesterov, uint16_t* u, float* tile_ss,
+                             hipStream_t stream)
+{
+    if (n_tiles <= 0) return hipSuccess;
+    if (n_tiles > 0x7fffffffLL) return hipErrorInvalidValue;
+    StepScalars sc{};
+    sc.beta1 = mu;
+    sc.one_minus_beta1 = one_minus_mu;
+    MuonOut mo{u, mu, one_minus_mu, nesterov};
+    const dim3 grid(static_cast<unsigned>(n_tiles));
+#define GEFEN_MC(G, C)                                                                      \
+    hipLaunchKernelGGL((k_muon_codec<G, C>), grid, dim3(kThreads), 0, stream, tiles, segs,  \
+                       codes, scale, cb, sc, mo, tile_ss)
+    if (code_bits != 8 && code_bits != 4) return hipErrorInvalidValue;
+    if (gdtype == DT_F32) {
+        if (code_bits == 8) GEFEN_MC(DT_F32, 8); else GEFEN_MC(DT_F32, 4);
+    } else {
+        if (code_bits == 8) GEFEN_MC(DT_BF16, 8); else GEFEN_MC(DT_BF16, 4);
+    }
+#undef GEFEN_MC
     return hipGetLastError();
 }
 

@@ -14,142 +14,10 @@
 // (one byte per bucket of [-1, 1] giving the number of midpoints below the bucket) plus
 // a short scan over the midpoints that fall inside the bucket (at most one for codebooks
 // whose entries are at least a bucket apart, as the DP's are).
-#include "gefen_internal.h"
+#include "step_device.h"
 
 namespace gefen {
 namespace {
-
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-
-// Pointers read from the tensor table are generic to the compiler, which then emits
-// flat accesses (counted against both the memory and the LDS wait counters); these
-// casts state that they point to global memory.
-#define GEFEN_GLOBAL __attribute__((address_space(1)))
-template <typename T>
-__device__ __forceinline__ const GEFEN_GLOBAL T* gl(const void* p)
-{
-    return (const GEFEN_GLOBAL T*)p;
-}
-template <typename T>
-__device__ __forceinline__ GEFEN_GLOBAL T* glw(void* p)
-{
-    return (GEFEN_GLOBAL T*)p;
-}
-
-struct LdsTables {
-    float cb[kMaxK];                  // decode entries
-    float mid[kMaxK];                 // encode midpoints
-    uint8_t guide[16 * kMaxK + 16];   // ng + 1 bytes (padded)
-    float red_ss[kMaxThreads / 64];
-    float red_am[kMaxThreads / 64];
-};
-
-template <int BS = kThreads>
-__device__ __forceinline__ void load_tables(LdsTables& L, const CodebookDev& cb)
-{
-    const int t = threadIdx.x;
-    if (t < cb.k) {
-        L.cb[t] = cb.dec[t];
-        L.mid[t] = cb.enc_mid[t];
-    }
-    const int words = (cb.ng + 1 + 3) >> 2;   // the global guide is padded to 16 bytes
-    const uint32_t* src = reinterpret_cast<const uint32_t*>(cb.enc_guide);
-    uint32_t* dst = reinterpret_cast<uint32_t*>(L.guide);
-    for (int i = t; i < words; i += BS) dst[i] = src[i];
-}
-
-// Nearest codebook entry of x (ties to the lower index) = number of midpoints < x.
-__device__ __forceinline__ int encode(const LdsTables& L, float x, float half_ng, int ng_m1)
-{
-    x = fminf(fmaxf(x, -1.0f), 1.0f);
-    int b = static_cast<int>((x + 1.0f) * half_ng);
-    b = min(b, ng_m1);
-    int q = L.guide[b];
-    const int hi = L.guide[b + 1];
-    while (q < hi && L.mid[q] < x) ++q;
-    return q;
-}
-
-__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
-
-// Momentum codes of CB bits (8 or 4), addressed by code index j = the tensor's code
-// offset + element index. CB = 8: byte j. CB = 4: nibble j, i.e. byte j / 2, low half
-// for even j, so four consecutive codes from j % 4 == 0 form one 16-bit word.
-template <int CB>
-__device__ __forceinline__ int code_ld(const uint8_t* codes, int64_t j)
-{
-    if (CB == 8) return codes[j];
-    return (codes[j >> 1] >> (4 * (j & 1))) & 0xf;
-}
-
-// Scalar store of code j whose current value is `old`. With 4-bit codes the byte can be
-// shared with a neighbouring block that another lane or workgroup updates at the same
-// time, so the nibble changes by one atomic XOR (old ^ q) of its 32-bit word, which
-// leaves every other nibble of the word as it is.
-template <int CB>
-__device__ __forceinline__ void code_st(uint8_t* codes, int64_t j, int old, int q)
-{
-    if (CB == 8) {
-        codes[j] = static_cast<uint8_t>(q);
-    } else if (old != q) {
-        atomicXor(reinterpret_cast<unsigned int*>(codes) + (j >> 3),
-                  static_cast<unsigned int>(old ^ q) << (4 * (j & 7)));
-    }
-}
-
-// Codes j .. j + 3 (j % 4 == 0) packed CB bits apiece, lowest index in the lowest bits.
-template <int CB>
-__device__ __forceinline__ uint32_t code_ld4(const uint8_t* codes, int64_t j)
-{
-    if (CB == 8) return *gl<uint32_t>(codes + j);
-    return *gl<uint16_t>(codes + (j >> 1));
-}
-
-template <int CB>
-__device__ __forceinline__ void code_st4(uint8_t* codes, int64_t j, uint32_t w)
-{
-    if (CB == 8)
-        __builtin_nontemporal_store(w, glw<uint32_t>(codes + j));
-    else
-        __builtin_nontemporal_store(static_cast<uint16_t>(w), glw<uint16_t>(codes + (j >> 1)));
-}
-
-template <int CB>
-__device__ __forceinline__ int code_get(uint32_t w, int c)
-{
-    return static_cast<int>((w >> (CB * c)) & ((1u << CB) - 1));
-}
-
-__device__ __forceinline__ float momentum(const LdsTables& L, int q, float s_old, float g,
-                                          const StepScalars& sc)
-{
-    return fmaf(sc.beta1, L.cb[q] * s_old, sc.one_minus_beta1 * g);
-}
-
-__device__ __forceinline__ float load_grad(const void* base, int64_t i, int gdt)
-{
-    if (gdt == DT_F32) return static_cast<const float*>(base)[i];
-    return __uint_as_float(static_cast<uint32_t>(static_cast<const uint16_t*>(base)[i]) << 16);
-}
-
-// Block-local scalars after the reductions.
-struct BlockOut {
-    float s_new, v_new, r, inv_s;
-};
-
-__device__ __forceinline__ BlockOut finish_block(float ss, float am, float v_old, float count,
-                                                 const StepScalars& sc)
-{
-    BlockOut o;
-    o.s_new = am;
-    o.v_new = fmaf(sc.beta2, v_old, sc.one_minus_beta2 * (ss / count));
-    const float denom = sqrtf(o.v_new * sc.inv_bc2) + sc.eps;
-    o.r = sc.step_size / denom;
-    o.inv_s = am > 0.0f ? 1.0f / am : 0.0f;
-    return o;
-}
 
 // ---------------------------------------------------------------------------------
 // KIND_U: uniform blocks of p elements (p % 4 == 0, p <= 8192). A group of
@@ -293,22 +161,6 @@ __device__ __forceinline__ void step_u_body(LdsTables& L, const Tile& tl, const 
             }
             code_st4<CB>(codes, cj0 + o, packed);
         }
-    }
-}
-
-// ---------------------------------------------------------------------------------
-// Block range of block `bi` of a tile (tensor-relative start, length).
-// ---------------------------------------------------------------------------------
-__device__ __forceinline__ void block_range(const Seg& sg, const Tile& tl, int bi,
-                                            int64_t& start, int64_t& len)
-{
-    if (sg.period > 0) {
-        start = tl.elem0 + static_cast<int64_t>(bi) * sg.period;
-        len = sg.period;
-    } else {
-        const int64_t local = tl.blk0 + bi - sg.blk_begin;
-        start = sg.csr[local];
-        len = sg.csr[local + 1] - start;
     }
 }
 
@@ -493,62 +345,10 @@ __global__ __launch_bounds__(BS) void k_step_u(const Tile* __restrict__ tiles,
         step_u_body<GDT, VPL, BS, false, CB>(L, tl, sg, codes, scale, vmom, cbd, sc);
 }
 
-// ---------------------------------------------------------------------------------
-// Streaming passes over an element range [start, start + len) of one block (KIND_G:
-// the whole block; KIND_H: one chunk). When the tensor's parameter and gradient
-// pointers allow it, the 4-element-aligned body of the range moves with 128-bit
-// (parameters, fp32 gradients), 64-bit (bf16 gradients) and 32-bit (4 codes) accesses;
-// the head and tail (at most 3 elements each) go element by element. The reduce pass
-// uses ordinary loads so that the update pass finds gradient and code lines in cache.
-// Both passes evaluate the momentum with the same operations, so they agree bit for bit.
-// ---------------------------------------------------------------------------------
-template <int GDT>
-__device__ __forceinline__ bool vector_ok(const Seg& sg)
-{
-    const uintptr_t galign = GDT == DT_F32 ? 15 : 7;
-    return ((reinterpret_cast<uintptr_t>(sg.theta) & 15) == 0) &&
-           ((reinterpret_cast<uintptr_t>(sg.grad) & galign) == 0);
-}
-
-template <int GDT>
-__device__ __forceinline__ void load_grad4(const Seg& sg, int64_t v, float g[4])
-{
-    if (GDT == DT_F32) {
-        const f32x4 x = gl<f32x4>(sg.grad)[v];
-        g[0] = x.x; g[1] = x.y; g[2] = x.z; g[3] = x.w;
-    } else {
-        const u32x2 x = gl<u32x2>(sg.grad)[v];
-        g[0] = bf16_lo(x.x); g[1] = bf16_hi(x.x); g[2] = bf16_lo(x.y); g[3] = bf16_hi(x.y);
-    }
-}
-
-struct Span {
-    int64_t vb, ve;   // vector body [vb, ve) in vector units (4 elements)
-    int64_t start, nh, hb_end, tail0, nt;
-};
-
-template <int GDT>
-__device__ __forceinline__ Span make_span(const Seg& sg, int64_t start, int64_t len)
-{
-    const int64_t end = start + len;
-    int64_t b = end, e = end;
-    if (vector_ok<GDT>(sg)) {
-        b = (start + 3) & ~int64_t(3);
-        e = end & ~int64_t(3);
-        if (b > end) b = end;
-        if (e < b) e = b;
-    }
-    Span sp;
-    sp.vb = b >> 2;
-    sp.ve = e >> 2;
-    sp.start = start;
-    sp.nh = b - start;
-    sp.tail0 = e;
-    sp.nt = end - e;
-    sp.hb_end = b;
-    return sp;
-}
-
+// Streaming passes over the Span of one block (KIND_G: the whole block; KIND_H: one
+// chunk). The reduce pass uses ordinary loads so that the update pass finds gradient and
+// code lines in cache. Both passes evaluate the momentum with the same operations, so
+// they agree bit for bit.
 template <int GDT, int BS, int CB>
 __device__ __forceinline__ void pass_reduce(const LdsTables& L, const Seg& sg,
                                             const uint8_t* __restrict__ codes, const Span& sp,
@@ -821,188 +621,6 @@ hipError_t launch_u(int vpl, int bs, dim3 grid, const Tile* tiles, const Seg* se
     return hipErrorInvalidValue;
 }
 
-// ---------------------------------------------------------------------------------
-// Gefen-Muon codec (appendix "Gefen-Muon"): Muon's momentum held in Gefen's quantized
-// form. Per block: m = mu * c_dec[q] * s + (1 - mu) * g, s' = max |m|,
-// q' = nearest(c_enc, m / s'); the matrix handed to the orthogonalisation is
-// u = nesterov ? (1 - mu) * g + mu * m : m, written as bfloat16 at the code index of
-// each element, and each tile's sum of u^2 (of the bfloat16 values) goes to tile_ss.
-// Tile mode in Tile::vpl: 0 = the workgroup on one block, 1 = one lane per block,
-// 2 = one wave per block.
-// ---------------------------------------------------------------------------------
-__device__ __forceinline__ uint16_t bf16_rne(float x)
-{
-    const uint32_t b = __float_as_uint(x);
-    return static_cast<uint16_t>((b + 0x7FFFu + ((b >> 16) & 1u)) >> 16);
-}
-
-struct MuonOut {
-    uint16_t* u;
-    float mu, one_minus_mu;
-    int nesterov;
-};
-
-// One element of the output pass: encode, write u, return u^2 (of the bfloat16 value).
-template <int CB>
-__device__ __forceinline__ float muon_elem_out(const LdsTables& L, uint8_t* __restrict__ codes,
-                                               int64_t j, float g, float s_old, float s_new,
-                                               float inv_s, const StepScalars& sc,
-                                               const MuonOut& mo, float half_ng, int ng_m1)
-{
-    const int q0 = code_ld<CB>(codes, j);
-    const float mm = momentum(L, q0, s_old, g, sc);
-    const int q = s_new > 0.0f ? encode(L, mm * inv_s, half_ng, ng_m1) : 0;
-    code_st<CB>(codes, j, q0, q);
-    const float uu = mo.nesterov ? fmaf(mo.mu, mm, mo.one_minus_mu * g) : mm;
-    const uint16_t ub = bf16_rne(uu);
-    mo.u[j] = ub;
-    const float ur = __uint_as_float(static_cast<uint32_t>(ub) << 16);
-    return ur * ur;
-}
-
-// Both passes of a block by BS threads (a wave or the workgroup; tid = index among them)
-// over the Span layout of the streamed step: 4-element vectors over the aligned body
-// (16- or 8-byte gradient loads, one code word, one 8-byte store of four bfloat16 u),
-// elements at the head and tail. absmax_pass returns the thread's max |m|.
-template <int GDT, int BS, int CB>
-__device__ __forceinline__ float muon_absmax_pass(const LdsTables& L, const Seg& sg,
-                                                  const uint8_t* __restrict__ codes,
-                                                  const Span& sp, float s_old,
-                                                  const StepScalars& sc, int tid)
-{
-    const int64_t cj = sg.code_off;
-    float am = 0.0f;
-#pragma unroll 2
-    for (int64_t v = sp.vb + tid; v < sp.ve; v += BS) {
-        float g[4];
-        load_grad4<GDT>(sg, v, g);
-        const uint32_t q4 = code_ld4<CB>(codes, cj + 4 * v);
-#pragma unroll
-        for (int c = 0; c < 4; ++c)
-            am = fmaxf(am, fabsf(momentum(L, code_get<CB>(q4, c), s_old, g[c], sc)));
-    }
-    for (int64_t i = tid; i < sp.nh + sp.nt; i += BS) {
-        const int64_t e = i < sp.nh ? sp.start + i : sp.tail0 + (i - sp.nh);
-        const float g = load_grad(sg.grad, e, GDT);
-        am = fmaxf(am, fabsf(momentum(L, code_ld<CB>(codes, cj + e), s_old, g, sc)));
-    }
-    return am;
-}
-
-template <int GDT, int BS, int CB>
-__device__ __forceinline__ float muon_out_pass(const LdsTables& L, const Seg& sg,
-                                               uint8_t* __restrict__ codes, const Span& sp,
-                                               float s_old, float s_new, const StepScalars& sc,
-                                               const MuonOut& mo, float half_ng, int ng_m1,
-                                               int tid)
-{
-    const int64_t cj = sg.code_off;
-    const float inv_s = s_new > 0.0f ? 1.0f / s_new : 0.0f;
-    float uss = 0.0f;
-#pragma unroll 2
-    for (int64_t v = sp.vb + tid; v < sp.ve; v += BS) {
-        float g[4];
-        load_grad4<GDT>(sg, v, g);
-        const uint32_t q4 = code_ld4<CB>(codes, cj + 4 * v);
-        uint32_t packed = 0;
-        uint32_t ub[4];
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            const float mm = momentum(L, code_get<CB>(q4, c), s_old, g[c], sc);
-            const int q = s_new > 0.0f ? encode(L, mm * inv_s, half_ng, ng_m1) : 0;
-            packed |= static_cast<uint32_t>(q) << (CB * c);
-            const float uu = mo.nesterov ? fmaf(mo.mu, mm, mo.one_minus_mu * g[c]) : mm;
-            ub[c] = bf16_rne(uu);
-            const float ur = __uint_as_float(ub[c] << 16);
-            uss = fmaf(ur, ur, uss);
-        }
-        code_st4<CB>(codes, cj + 4 * v, packed);
-        const u32x2 w = {ub[0] | (ub[1] << 16), ub[2] | (ub[3] << 16)};
-        *glw<u32x2>(mo.u + cj + 4 * v) = w;
-    }
-    for (int64_t i = tid; i < sp.nh + sp.nt; i += BS) {
-        const int64_t e = i < sp.nh ? sp.start + i : sp.tail0 + (i - sp.nh);
-        uss += muon_elem_out<CB>(L, codes, cj + e, load_grad(sg.grad, e, GDT), s_old, s_new,
-                                 inv_s, sc, mo, half_ng, ng_m1);
-    }
-    return uss;
-}
-
-template <int GDT, int CB>
-__global__ __launch_bounds__(kThreads) void k_muon_codec(const Tile* __restrict__ tiles,
-                                                         const Seg* __restrict__ segs,
-                                                         uint8_t* __restrict__ codes,
-                                                         float* __restrict__ scale,
-                                                         CodebookDev cbd, StepScalars sc,
-                                                         MuonOut mo, float* __restrict__ tile_ss)
-{
-    __shared__ LdsTables L;
-    const Tile tl = tiles[blockIdx.x];
-    const Seg sg = segs[tl.seg];
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = tid >> 6;
-    load_tables<kThreads>(L, cbd);
-    __syncthreads();
-    const float half_ng = 0.5f * static_cast<float>(cbd.ng);
-    const int ng_m1 = cbd.ng - 1;
-    float uss = 0.0f;
-    if (tl.vpl == 0) {
-        int64_t start, len;
-        block_range(sg, tl, 0, start, len);
-        const float s_old = scale[tl.blk0];
-        const Span sp = make_span<GDT>(sg, start, len);
-        float am = muon_absmax_pass<GDT, kThreads, CB>(L, sg, codes, sp, s_old, sc, tid);
-        for (int off = 1; off < 64; off <<= 1) am = fmaxf(am, __shfl_xor(am, off));
-        if (lane == 0) L.red_am[wave] = am;
-        __syncthreads();
-        am = L.red_am[0];
-        for (int w = 1; w < kThreads / 64; ++w) am = fmaxf(am, L.red_am[w]);
-        if (tid == 0) scale[tl.blk0] = am;
-        uss = muon_out_pass<GDT, kThreads, CB>(L, sg, codes, sp, s_old, am, sc, mo, half_ng,
-                                               ng_m1, tid);
-    } else if (tl.vpl == 1) {
-        if (tid < tl.nblk) {
-            int64_t start, len;
-            block_range(sg, tl, tid, start, len);
-            const int64_t blk = tl.blk0 + tid;
-            const float s_old = scale[blk];
-            const int64_t cj = sg.code_off + start;
-            float am = 0.0f;
-            for (int64_t i = 0; i < len; ++i) {
-                const float g = load_grad(sg.grad, start + i, GDT);
-                am = fmaxf(am, fabsf(momentum(L, code_ld<CB>(codes, cj + i), s_old, g, sc)));
-            }
-            scale[blk] = am;
-            const float inv_s = am > 0.0f ? 1.0f / am : 0.0f;
-            for (int64_t i = 0; i < len; ++i)
-                uss += muon_elem_out<CB>(L, codes, cj + i, load_grad(sg.grad, start + i, GDT),
-                                         s_old, am, inv_s, sc, mo, half_ng, ng_m1);
-        }
-    } else {
-        if (wave < tl.nblk) {
-            int64_t start, len;
-            block_range(sg, tl, wave, start, len);
-            const int64_t blk = tl.blk0 + wave;
-            const float s_old = scale[blk];
-            const Span sp = make_span<GDT>(sg, start, len);
-            float am = muon_absmax_pass<GDT, 64, CB>(L, sg, codes, sp, s_old, sc, lane);
-            for (int off = 1; off < 64; off <<= 1) am = fmaxf(am, __shfl_xor(am, off));
-            if (lane == 0) scale[blk] = am;
-            uss = muon_out_pass<GDT, 64, CB>(L, sg, codes, sp, s_old, am, sc, mo, half_ng, ng_m1,
-                                             lane);
-        }
-    }
-    // the tile's sum of u^2, fixed order (red_ss is not used above)
-    for (int off = 1; off < 64; off <<= 1) uss += __shfl_xor(uss, off);
-    if (lane == 0) L.red_ss[wave] = uss;
-    __syncthreads();
-    if (tid == 0) {
-        float t = L.red_ss[0];
-        for (int w = 1; w < kThreads / 64; ++w) t += L.red_ss[w];
-        tile_ss[blockIdx.x] = t;
-    }
-}
 
 template <int GDT, int CB>
 hipError_t launch_h(dim3 grid, const Tile* tiles, const HTile* htiles, const Seg* segs,
@@ -1092,30 +710,5 @@ hipError_t launch_step(int kind, int gdtype, int code_bits, int vpl, int bs, con
                                          cb, sc, stream);
 }
 
-hipError_t launch_muon_codec(int code_bits, int gdtype, const Tile* tiles, int64_t n_tiles,
-                             const Seg* segs,
-                             uint8_t* codes, float* scale, CodebookDev cb, float mu,
-                             float one_minus_mu, int nesterov, uint16_t* u, float* tile_ss,
-                             hipStream_t stream)
-{
-    if (n_tiles <= 0) return hipSuccess;
-    if (n_tiles > 0x7fffffffLL) return hipErrorInvalidValue;
-    StepScalars sc{};
-    sc.beta1 = mu;
-    sc.one_minus_beta1 = one_minus_mu;
-    MuonOut mo{u, mu, one_minus_mu, nesterov};
-    const dim3 grid(static_cast<unsigned>(n_tiles));
-#define GEFEN_MC(G, C)                                                                      \
-    hipLaunchKernelGGL((k_muon_codec<G, C>), grid, dim3(kThreads), 0, stream, tiles, segs,  \
-                       codes, scale, cb, sc, mo, tile_ss)
-    if (code_bits != 8 && code_bits != 4) return hipErrorInvalidValue;
-    if (gdtype == DT_F32) {
-        if (code_bits == 8) GEFEN_MC(DT_F32, 8); else GEFEN_MC(DT_F32, 4);
-    } else {
-        if (code_bits == 8) GEFEN_MC(DT_BF16, 8); else GEFEN_MC(DT_BF16, 4);
-    }
-#undef GEFEN_MC
-    return hipGetLastError();
-}
 
 }  // namespace gefen
