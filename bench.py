@@ -196,6 +196,39 @@ def bench_muon(args, torch, w, dev):
     gb = 2 if w.grad_dtype == "bf16" else 4
     codec_bytes = w.numel * (gb + (2 if args.code_bits == 8 else 1) + 2)
     persistent, workspace = st.state_bytes()
+    out = {
+        "metric": METRIC + " (Gefen-Muon)",
+        "value": round(w.numel / (ms * 1e-3) / 1e9, 3),
+        "unit": "Gparams/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "optimizer": "gefen_muon", "params": w.numel,
+                   "tensors": len(w.tensors), "grad_dtype": w.grad_dtype,
+                   "code_bits": args.code_bits, "ns_steps": ns_steps, "nesterov": True},
+        "phases_ms": {"codec": round(codec_ms, 4), "newton_schulz": round(ns_ms, 4),
+                      "prep_update": round(prof["rest_ms"] / max(1, prof["steps"]), 4)},
+        "roofline": {"bound": "mfma", "achieved": None, "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": None, "traffic": None,
+                     "kernel": "Newton-Schulz bf16 GEMMs (rocBLAS)", "flops_per_step": flops},
+        "codec": {"bytes_per_step": codec_bytes,
+                  "gbps": round(codec_bytes / (codec_ms * 1e-3) / 1e9, 1)},
+        "memory": {"gefen_muon_persistent_bytes": persistent,
+                   "gefen_muon_workspace_bytes": workspace},
+        "init_s": round(init_s, 3),
+    }
+    achieved = flops / (ns_ms * 1e-3) / 1e12
+    out["roofline"]["achieved"] = round(achieved, 1)
+    out["roofline"]["frac"] = round(achieved / PEAK_BF16_TFLOPS, 4)
+    if args.no_torch_muon:
+        out["torch_muon"] = None
+        return out
     # torch.optim.Muon on the same matrices
     ps = [torch.nn.Parameter(p.detach().clone().view(r, p.numel() // r))
           for p, r in zip(params, rows)]
@@ -220,38 +253,10 @@ def bench_muon(args, torch, w, dev):
     m1.record()
     torch.cuda.synchronize()
     muon_ms = m0.elapsed_time(m1) / reps
-    achieved = flops / (ns_ms * 1e-3) / 1e12
-    return {
-        "metric": METRIC + " (Gefen-Muon)",
-        "value": round(w.numel / (ms * 1e-3) / 1e9, 3),
-        "unit": "Gparams/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(ms, 4),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16",
-        "data": "synthetic",
-        "config": {"workload": w.name, "optimizer": "gefen_muon", "params": w.numel,
-                   "tensors": len(w.tensors), "grad_dtype": w.grad_dtype,
-                   "code_bits": args.code_bits, "ns_steps": ns_steps, "nesterov": True},
-        "phases_ms": {"codec": round(codec_ms, 4), "newton_schulz": round(ns_ms, 4),
-                      "prep_update": round(prof["rest_ms"] / max(1, prof["steps"]), 4)},
-        "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": None, "kernel": "Newton-Schulz bf16 GEMMs (rocBLAS)",
-                     "flops_per_step": flops},
-        "codec": {"bytes_per_step": codec_bytes,
-                  "gbps": round(codec_bytes / (codec_ms * 1e-3) / 1e9, 1)},
-        "torch_muon": {"ms_per_step": round(muon_ms, 4), "state_bytes": muon_state,
-                       "gefen_muon_persistent_bytes": persistent,
-                       "gefen_muon_workspace_bytes": workspace,
-                       "state_ratio": round(muon_state / persistent, 3),
-                       "gefen_speedup": round(muon_ms / ms, 3)},
-        "init_s": round(init_s, 3),
-    }
+    out["torch_muon"] = {"ms_per_step": round(muon_ms, 4), "state_bytes": muon_state,
+                         "state_ratio": round(muon_state / persistent, 3),
+                         "gefen_speedup": round(muon_ms / ms, 3)}
+    return out
 
 
 def copy_ceiling(torch, dev, nbytes: int = 4 << 30, reps: int = 10):
@@ -294,6 +299,8 @@ def main():
                          "with Newton-Schulz; default workload gpt2_125m)")
     ap.add_argument("--no-adamw", action="store_true",
                     help="skip the torch AdamW comparison (always skipped for explicit blocks)")
+    ap.add_argument("--no-torch-muon", action="store_true",
+                    help="skip the torch.optim.Muon comparison of --optimizer gefen_muon")
     ap.add_argument("--cpu-sample-elems", type=int, default=100_000_000)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain device-to-device copy of a known byte count "

@@ -257,6 +257,8 @@ int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, voi
  *   ns_steps times: A = X X^T; B = ns_b A + ns_c A A; X = ns_a X + B X
  *       (bfloat16 matrices, float32 accumulation, as Muon's PyTorch implementation)
  *   theta = theta * (1 - lr * weight_decay) - lr * sqrt(max(1, rows / cols)) * X^(T)
+ * (The transpose is mathematical only: X lives in the tensor's own row-major layout,
+ * which the column-major matrix products read as X or X^T.)
  *  params, grads  as for gefen_step; momentum in [0, 1); ns_steps in [0, 100];
  *  ns_eps > 0. Muon's defaults: ns_steps 5, (ns_a, ns_b, ns_c) =
  *  (3.4445, -4.7750, 2.0315), ns_eps 1e-7, nesterov 1.
@@ -272,7 +274,7 @@ int gefen_muon_step(gefen_state* st, const gefen_tensor* params, const gefen_ten
 
 /* Measurement of Gefen-Muon steps (after gefen_muon_init and gefen_profile_begin):
  * sums over the profiled steps of the codec time (codec and norms), the Newton-Schulz
- * GEMM time (all shape groups) and the rest (normalise/transpose and update kernels),
+ * GEMM time (all shape groups) and the rest (normalise and update kernels),
  * in milliseconds, from HIP events on the step's stream; then disarms like
  * gefen_profile_end. */
 int gefen_muon_profile_end(gefen_state* st, int32_t* steps, double* codec_ms, double* ns_ms,

@@ -131,10 +131,20 @@ struct gefen_state {
 
     // Gefen-Muon (gefen_muon_init): codec tiles over every block, the bfloat16 momentum
     // matrix per code index, tensors grouped by shape for batched Newton-Schulz GEMMs.
-    struct MuonGroup {
+    struct MuonPart {           // tensors of one rows x cols shape inside a group
         int64_t rows, cols;
+        int32_t first, count;   // batch entries [first, first + count) of the group
+        bool transposed;        // rows > cols > 1: X = U^T
+    };
+    struct MuonGroup {
+        // wide matrices X (m x n, m = min(rows, cols)) in row-major layout with leading
+        // dimension ldx; the products run over ldx columns. A tall part's X is U^T with
+        // its columns n .. ldx - 1 zero (ldx: n rounded up to a multiple of 8, or of
+        // 8 * splits for a split Gram product); otherwise X is U itself and ldx = n.
+        int64_t m, n, ldx;
         int32_t first, count;   // muon_tensor_of[first .. first + count)
         int32_t splits;         // K-chunks of the Gram product (1 = one GEMM)
+        std::vector<MuonPart> parts;
     };
     bool muon_ready = false;
     Tile* muon_tiles = nullptr;
@@ -1326,34 +1336,37 @@ hipStream_t rocblas_get_stream_for(gefen_state* st)
     return s;
 }
 
-// One Newton-Schulz iteration on a batch of wide m x n row-major matrices (m <= n):
-// A = X X^T; B = b A + c A A; X' = a X + B X, all bfloat16 with float32 accumulation.
-// rocBLAS is column-major: the row-major m x n X is the column-major n x m X^T.
+// One Newton-Schulz iteration X <- a X + (b A + c A^2) X, A = X X^T, on the m x n wide
+// row-major matrices X (leading dimension ldx) of a shape group, bfloat16 products with
+// float32 accumulation. rocBLAS is column-major, so it sees each X as X^T (n x m, leading
+// dimension ldx): A = (X^T)^T X^T and the new X^T = a X^T + X^T B (B is symmetric). Both
+// operands of the Gram product run along K contiguously, the layout rocBLAS is fastest on.
 int ns_iteration(gefen_state* st, const gefen_state::MuonGroup& g, const uint16_t* x,
                  uint16_t* xo, float a, float b, float c)
 {
-    const int64_t m = std::min(g.rows, g.cols), n = std::max(g.rows, g.cols);
+    const int64_t m = g.m, n = g.ldx;   // zero columns beyond g.n add nothing
     const rocblas_int mi = static_cast<rocblas_int>(m), ni = static_cast<rocblas_int>(n);
-    const rocblas_stride sx = m * n, sa = m * m;
+    const rocblas_int ldx = static_cast<rocblas_int>(g.ldx);
+    const rocblas_stride sx = m * g.ldx, sa = m * m;
     const float one = 1.0f, zero = 0.0f;
     const rocblas_datatype bf = rocblas_datatype_bf16_r, f32 = rocblas_datatype_f32_r;
     if (g.splits > 1) {
         // tall-skinny Gram product (one matrix, long K): float32 partial products of
-        // K-chunks, summed in chunk order and rounded once
+        // K-chunks (column blocks of X), summed in chunk order and rounded once
         const int64_t kc = (n + g.splits - 1) / g.splits;
         const int64_t full = n / kc;               // chunks of length kc
         const int64_t rest = n - full * kc;
         if (full > 0)
             GEFEN_BLAS(rocblas_gemm_strided_batched_ex(
                 st->blas, rocblas_operation_transpose, rocblas_operation_none, mi, mi,
-                static_cast<rocblas_int>(kc), &one, x, bf, ni, kc, x, bf, ni, kc, &zero,
+                static_cast<rocblas_int>(kc), &one, x, bf, ldx, kc, x, bf, ldx, kc, &zero,
                 st->muon_partial, f32, mi, sa, st->muon_partial, f32, mi, sa,
                 static_cast<rocblas_int>(full), f32, rocblas_gemm_algo_standard, 0, 0));
         if (rest > 0)
             GEFEN_BLAS(rocblas_gemm_ex(
                 st->blas, rocblas_operation_transpose, rocblas_operation_none, mi, mi,
-                static_cast<rocblas_int>(rest), &one, x + full * kc, bf, ni, x + full * kc, bf,
-                ni, &zero, st->muon_partial + full * sa, f32, mi, st->muon_partial + full * sa,
+                static_cast<rocblas_int>(rest), &one, x + full * kc, bf, ldx, x + full * kc, bf,
+                ldx, &zero, st->muon_partial + full * sa, f32, mi, st->muon_partial + full * sa,
                 f32, mi, f32, rocblas_gemm_algo_standard, 0, 0));
         GEFEN_HIP(launch_muon_splitk_sum(st->muon_partial,
                                          static_cast<int32_t>(full + (rest > 0 ? 1 : 0)), sa,
@@ -1361,7 +1374,7 @@ int ns_iteration(gefen_state* st, const gefen_state::MuonGroup& g, const uint16_
     } else {
         GEFEN_BLAS(rocblas_gemm_strided_batched_ex(
             st->blas, rocblas_operation_transpose, rocblas_operation_none, mi, mi, ni, &one, x,
-            bf, ni, sx, x, bf, ni, sx, &zero, st->muon_a, bf, mi, sa, st->muon_a, bf, mi, sa,
+            bf, ldx, sx, x, bf, ldx, sx, &zero, st->muon_a, bf, mi, sa, st->muon_a, bf, mi, sa,
             g.count, f32, rocblas_gemm_algo_standard, 0, 0));
     }
     GEFEN_BLAS(rocblas_gemm_strided_batched_ex(
@@ -1369,8 +1382,8 @@ int ns_iteration(gefen_state* st, const gefen_state::MuonGroup& g, const uint16_
         mi, sa, st->muon_a, bf, mi, sa, &b, st->muon_a, bf, mi, sa, st->muon_b, bf, mi, sa,
         g.count, f32, rocblas_gemm_algo_standard, 0, 0));
     GEFEN_BLAS(rocblas_gemm_strided_batched_ex(
-        st->blas, rocblas_operation_none, rocblas_operation_none, ni, mi, mi, &one, x, bf, ni, sx,
-        st->muon_b, bf, mi, sa, &a, x, bf, ni, sx, xo, bf, ni, sx, g.count, f32,
+        st->blas, rocblas_operation_none, rocblas_operation_none, ni, mi, mi, &one, x, bf, ldx,
+        sx, st->muon_b, bf, mi, sa, &a, x, bf, ldx, sx, xo, bf, ldx, sx, g.count, f32,
         rocblas_gemm_algo_standard, 0, 0));
     return GEFEN_OK;
 }
@@ -1439,40 +1452,67 @@ int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, voi
         if (pass == 0) st->muon_dt_first[1] = static_cast<int64_t>(tiles.size());
     }
 
-    // shape groups, in order of first appearance
+    // Shape groups: tensors whose wide matrices and X layouts agree share one batch of
+    // Newton-Schulz products (so a tall R x C tensor joins the C x R ones); inside a
+    // group, parts of one R x C shape share the normalise and update launches. Groups and
+    // parts in order of first appearance.
     std::vector<int32_t> order;
     st->muon_groups.clear();
+    struct Shape {
+        int64_t rows, cols, m, n, ldx;
+        bool transposed;
+    };
+    std::vector<Shape> shp(n);
     for (int32_t t = 0; t < n; ++t) {
-        const int64_t R = rows[t], C = st->numel[t] / rows[t];
-        bool found = false;
-        for (const auto& g : st->muon_groups) found = found || (g.rows == R && g.cols == C);
-        if (found) continue;
-        gefen_state::MuonGroup g{R, C, static_cast<int32_t>(order.size()), 0, 1};
-        for (int32_t u = t; u < n; ++u)
-            if (rows[u] == R && st->numel[u] / rows[u] == C) {
-                order.push_back(u);
-                ++g.count;
-            }
+        Shape& sh = shp[t];
+        sh.rows = rows[t];
+        sh.cols = st->numel[t] / rows[t];
+        sh.m = std::min(sh.rows, sh.cols);
+        sh.n = std::max(sh.rows, sh.cols);
+        if (sh.n > 0x7ffff000LL)
+            return fail(GEFEN_EINVAL, "a matrix side exceeds 2^31 - 4096");
+        sh.transposed = sh.rows > sh.cols && sh.cols > 1;
+        sh.ldx = sh.transposed ? (sh.n + 7) / 8 * 8 : sh.n;
+    }
+    std::vector<char> placed(static_cast<size_t>(n), 0);
+    for (int32_t t = 0; t < n; ++t) {
+        if (placed[t]) continue;
+        gefen_state::MuonGroup g{};
+        g.m = shp[t].m;
+        g.n = shp[t].n;
+        g.ldx = shp[t].ldx;
+        g.first = static_cast<int32_t>(order.size());
+        g.splits = 1;
+        for (int32_t u = t; u < n; ++u) {
+            if (placed[u] || shp[u].m != g.m || shp[u].n != g.n || shp[u].ldx != g.ldx) continue;
+            gefen_state::MuonPart pt{shp[u].rows, shp[u].cols, g.count, 0, shp[u].transposed};
+            for (int32_t v = u; v < n; ++v)
+                if (!placed[v] && shp[v].rows == pt.rows && shp[v].cols == pt.cols) {
+                    placed[v] = 1;
+                    order.push_back(v);
+                    ++pt.count;
+                    ++g.count;
+                }
+            g.parts.push_back(pt);
+        }
         st->muon_groups.push_back(g);
     }
     // Split the Gram product of a lone tall-skinny matrix over K when its m x m output
-    // has too few 128 x 128 tiles to occupy the GPU.
-    int64_t max_partial = 0;
+    // has too few 128 x 128 tiles to occupy the GPU. A transposed X gets zero columns up
+    // to a multiple of 8 * splits, so that the chunks are equal and one batched call
+    // covers them.
+    int64_t max_partial = 0, max_x = 0, max_a = 0;
     for (auto& g : st->muon_groups) {
-        const int64_t m = std::min(g.rows, g.cols), n = std::max(g.rows, g.cols);
+        const int64_t m = g.m;
         const int64_t tiles = ((m + 127) / 128) * ((m + 127) / 128);
-        if (g.count == 1 && m > 1 && tiles < 128 && n >= 8 * m) {
-            g.splits = static_cast<int32_t>(std::min<int64_t>(16, n / (4 * m)));
+        if (g.count == 1 && m > 1 && tiles < 128 && g.n >= 8 * m) {
+            g.splits = static_cast<int32_t>(std::min<int64_t>(16, g.n / (4 * m)));
             if (g.splits < 2) g.splits = 1;
         }
+        if (g.splits > 1 && g.parts[0].transposed)
+            g.ldx = (g.n + 8 * g.splits - 1) / (8 * g.splits) * (8 * g.splits);
         if (g.splits > 1) max_partial = std::max(max_partial, g.splits * m * m);
-    }
-    int64_t max_x = 0, max_a = 0;
-    for (const auto& g : st->muon_groups) {
-        const int64_t m = std::min(g.rows, g.cols);
-        if (std::max(g.rows, g.cols) > 0x7fffffffLL)
-            return fail(GEFEN_EINVAL, "a matrix side exceeds 2^31 - 1");
-        max_x = std::max(max_x, g.count * g.rows * g.cols);
+        max_x = std::max(max_x, g.count * m * g.ldx);
         max_a = std::max(max_a, g.count * m * m);
     }
     // Shape groups above kMuonMaxGroup elements are refused: a state of that size (the
@@ -1510,7 +1550,7 @@ int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, voi
     st->workspace_bytes += static_cast<int64_t>(kBlasWorkspace);
     GEFEN_HIP(fill_zero(st->muon_x[0], 2 * static_cast<size_t>(max_x), stream));
     for (const auto& g : st->muon_groups)
-        if (std::min(g.rows, g.cols) > 1 &&
+        if (g.m > 1 &&
             (rc = ns_iteration(st, g, st->muon_x[0], st->muon_x[1], 1.0f, 1.0f, 1.0f)))
             return rc;
     GEFEN_HIP(hipStreamSynchronize(stream));
@@ -1555,15 +1595,23 @@ int gefen_muon_step(gefen_state* st, const gefen_tensor* params, const gefen_ten
     const float decay = static_cast<float>(1.0 - lr * weight_decay);
     for (size_t gi = 0; gi < st->muon_groups.size(); ++gi) {
         const auto& g = st->muon_groups[gi];
-        GEFEN_HIP(launch_muon_prep(st->muon_u, st->segs, st->muon_tensor_of + g.first, g.count,
-                                   st->muon_norm, g.rows, g.cols, st->muon_x[0], stream));
+        const int64_t xs = g.m * g.ldx;   // elements per batch entry of X
+        for (const auto& pt : g.parts) {
+            const int32_t* tof = st->muon_tensor_of + g.first + pt.first;
+            uint16_t* xb = st->muon_x[0] + pt.first * xs;
+            if (pt.transposed)
+                GEFEN_HIP(launch_muon_prep_t(st->muon_u, st->segs, tof, pt.count, st->muon_norm,
+                                             pt.rows, pt.cols, g.ldx, xb, stream));
+            else
+                GEFEN_HIP(launch_muon_prep(st->muon_u, st->segs, tof, pt.count, st->muon_norm,
+                                           pt.rows * pt.cols, xb, stream));
+        }
         if (prof) GEFEN_HIP(hipEventRecord(ev[2 + 2 * gi], stream));
         int cur = 0;
-        if (std::min(g.rows, g.cols) == 1) {
-            GEFEN_HIP(launch_muon_ns_vec(st->muon_x[0], g.count, std::max(g.rows, g.cols),
-                                         ns_steps, static_cast<float>(ns_a),
-                                         static_cast<float>(ns_b), static_cast<float>(ns_c),
-                                         stream));
+        if (g.m == 1) {
+            GEFEN_HIP(launch_muon_ns_vec(st->muon_x[0], g.count, g.n, ns_steps,
+                                         static_cast<float>(ns_a), static_cast<float>(ns_b),
+                                         static_cast<float>(ns_c), stream));
         } else {
             for (int32_t it = 0; it < ns_steps; ++it) {
                 if ((rc = ns_iteration(st, g, st->muon_x[cur], st->muon_x[1 - cur],
@@ -1574,10 +1622,18 @@ int gefen_muon_step(gefen_state* st, const gefen_tensor* params, const gefen_ten
             }
         }
         if (prof) GEFEN_HIP(hipEventRecord(ev[3 + 2 * gi], stream));
-        const double scale = std::sqrt(std::max(1.0, static_cast<double>(g.rows) / g.cols));
-        GEFEN_HIP(launch_muon_update(st->muon_x[cur], st->segs, st->muon_tensor_of + g.first,
-                                     g.count, g.rows, g.cols, decay,
-                                     static_cast<float>(lr * scale), stream));
+        for (const auto& pt : g.parts) {
+            const int32_t* tof = st->muon_tensor_of + g.first + pt.first;
+            const uint16_t* ob = st->muon_x[cur] + pt.first * xs;
+            const double scale = std::sqrt(std::max(1.0, static_cast<double>(pt.rows) / pt.cols));
+            const float step = static_cast<float>(lr * scale);
+            if (pt.transposed)
+                GEFEN_HIP(launch_muon_update_t(ob, st->segs, tof, pt.count, pt.rows, pt.cols,
+                                               g.ldx, decay, step, stream));
+            else
+                GEFEN_HIP(launch_muon_update(ob, st->segs, tof, pt.count, pt.rows * pt.cols,
+                                             decay, step, stream));
+        }
     }
     if (prof) {
         GEFEN_HIP(hipEventRecord(ev[st->muon_prof_stride() - 1], stream));

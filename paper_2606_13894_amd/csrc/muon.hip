@@ -1,7 +1,7 @@
 // Gefen-Muon (appendix "Gefen-Muon") on the device: the codec that keeps Muon's
 // momentum in Gefen's quantized form, the Frobenius norm of each momentum matrix, its
-// normalised bfloat16 copy in the wide orientation (the Newton-Schulz input), and the
-// parameter update from the orthogonalised result. The Newton-Schulz matrix products
+// normalised bfloat16 copy (the Newton-Schulz input), and the parameter update from the
+// orthogonalised result. The Newton-Schulz matrix products
 // are plain bfloat16 GEMMs (rocBLAS), driven from the host.
 #include "muon_internal.h"
 #include "step_device.h"
@@ -220,51 +220,10 @@ __global__ __launch_bounds__(kThreads) void k_muon_codec(const Tile* __restrict_
     }
 }
 
-constexpr int kT = 64;   // transpose tile edge
-
-// X[batch] (m x n row-major, m = min(R, C)) = bf16(U_t / norm_t), with U_t the tensor's
-// R x C momentum matrix; transposed when R > C. 64 x 64 tiles through LDS so both the
-// read and the write are coalesced.
-__global__ __launch_bounds__(256) void k_muon_prep(const uint16_t* __restrict__ u,
-                                                   const Seg* __restrict__ segs,
-                                                   const int32_t* __restrict__ tensor_of,
-                                                   const float* __restrict__ norm, int64_t R,
-                                                   int64_t C, int transposed,
-                                                   uint16_t* __restrict__ x)
-{
-    __shared__ uint16_t tile[kT][kT + 2];
-    const int b = blockIdx.z;
-    const int t = tensor_of[b];
-    const uint16_t* __restrict__ src = u + segs[t].code_off;
-    uint16_t* __restrict__ dst = x + static_cast<int64_t>(b) * R * C;
-    const float nrm = norm[t];
-    const int64_t r0 = static_cast<int64_t>(blockIdx.y) * kT;
-    const int64_t c0 = static_cast<int64_t>(blockIdx.x) * kT;
-    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-    for (int i = ty; i < kT; i += 4) {
-        const int64_t r = r0 + i, c = c0 + tx;
-        uint16_t v = 0;
-        if (r < R && c < C) v = to_bf16(bf16_val(src[r * C + c]) / nrm);
-        tile[i][tx] = v;
-    }
-    __syncthreads();
-    if (!transposed) {
-        for (int i = ty; i < kT; i += 4) {
-            const int64_t r = r0 + i, c = c0 + tx;
-            if (r < R && c < C) dst[r * C + c] = tile[i][tx];
-        }
-    } else {
-        // X is C x R: X[c][r] = U[r][c]
-        for (int i = ty; i < kT; i += 4) {
-            const int64_t c = c0 + i, r = r0 + tx;
-            if (r < R && c < C) dst[c * R + r] = tile[tx][i];
-        }
-    }
-}
-
-// Untransposed orientation (R <= C): the same copy and update as flat element loops,
-// eight bfloat16 (prep) or four parameters (update) per thread where sizes and pointers
-// are aligned, element by element otherwise.
+// Newton-Schulz input and update for a matrix that is not tall (R <= C, or C = 1): X has
+// the tensor's own row-major layout, so both are flat element loops, eight bfloat16
+// (prep) or four parameters (update) per thread where sizes and pointers are aligned,
+// element by element otherwise.
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
 typedef float f32x4v __attribute__((ext_vector_type(4)));
@@ -324,37 +283,132 @@ __global__ __launch_bounds__(256) void k_muon_update_flat(const uint16_t* __rest
     }
 }
 
-// theta_t (R x C) = theta_t * decay - step * O, O the orthogonalised matrix of batch
-// entry b (m x n row-major, transposed back when R > C).
-__global__ __launch_bounds__(256) void k_muon_update(const uint16_t* __restrict__ o,
+// Tall matrices (R > C > 1) are orthogonalised as their wide transpose X = U^T (C x R,
+// rows padded to ldx, a multiple of 8). A lane moves an 8 x 8 block and transposes it in
+// registers; lane l of a wave takes rows 8 (l / 8) .. + 7 and columns 8 (l % 8) .. + 7 of
+// a 64 x 64 tile, so each of its eight 16-byte row loads and eight 16-byte column stores
+// joins those of seven neighbouring lanes into 128 contiguous bytes. A workgroup holds 4
+// tiles along R. Blocks on the matrix edge, or of tensors whose rows are not 16-byte
+// aligned, go element by element.
+constexpr int kTile = 64;
+constexpr int kTilesPerGroup = 4;
+
+struct TBlock {
+    int64_t r0, c0;
+    bool full;
+};
+
+__device__ __forceinline__ TBlock t_block(int64_t R, int64_t C)
+{
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    TBlock tb;
+    tb.r0 = (static_cast<int64_t>(blockIdx.y) * kTilesPerGroup + wave) * kTile + 8 * (lane >> 3);
+    tb.c0 = static_cast<int64_t>(blockIdx.x) * kTile + 8 * (lane & 7);
+    tb.full = tb.r0 + 8 <= R && tb.c0 + 8 <= C;
+    return tb;
+}
+
+// Element j (0..7) of eight packed bfloat16.
+__device__ __forceinline__ uint32_t bf16_at(const u32x4& w, int j)
+{
+    const uint32_t v = w[j >> 1];
+    return (j & 1) ? (v >> 16) : (v & 0xffffu);
+}
+
+// x[b] (C x ldx) = bf16(U^T / norm), U the R x C momentum matrix of tensor tensor_of[b],
+// and zero in columns R .. ldx - 1 (the grid covers ldx rows of U)
+__global__ __launch_bounds__(256) void k_muon_prep_t(const uint16_t* __restrict__ u,
                                                      const Seg* __restrict__ segs,
                                                      const int32_t* __restrict__ tensor_of,
-                                                     int64_t R, int64_t C, int transposed,
-                                                     float decay, float step)
+                                                     const float* __restrict__ norm, int64_t R,
+                                                     int64_t C, int64_t ldx,
+                                                     uint16_t* __restrict__ x)
 {
-    __shared__ uint16_t tile[kT][kT + 2];
+    const int b = blockIdx.z;
+    const int t = tensor_of[b];
+    const uint16_t* __restrict__ src = u + segs[t].code_off;
+    uint16_t* __restrict__ dst = x + static_cast<int64_t>(b) * C * ldx;
+    const float nrm = norm[t];
+    const TBlock tb = t_block(R, C);
+    if (tb.r0 >= ldx || tb.c0 >= C) return;
+    if (tb.r0 >= R) {   // zero columns of X (tb.r0 + 8 <= ldx, as ldx % 8 == 0)
+        const u32x4 z = {0u, 0u, 0u, 0u};
+        for (int k = 0; k < 8; ++k)
+            if (tb.c0 + k < C) *reinterpret_cast<u32x4*>(dst + (tb.c0 + k) * ldx + tb.r0) = z;
+        return;
+    }
+    if (tb.full && (C & 7) == 0) {
+        u32x4 w[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            w[j] = *reinterpret_cast<const u32x4*>(src + (tb.r0 + j) * C + tb.c0);
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const uint32_t lo = to_bf16(bf16_val(static_cast<uint16_t>(w[j][q] & 0xffffu)) / nrm);
+                const uint32_t hi = to_bf16(bf16_val(static_cast<uint16_t>(w[j][q] >> 16)) / nrm);
+                w[j][q] = lo | (hi << 16);
+            }
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            u32x4 o;
+#pragma unroll
+            for (int p = 0; p < 4; ++p) o[p] = bf16_at(w[2 * p], k) | (bf16_at(w[2 * p + 1], k) << 16);
+            *reinterpret_cast<u32x4*>(dst + (tb.c0 + k) * ldx + tb.r0) = o;
+        }
+    } else {
+        for (int j = 0; j < 8; ++j)
+            for (int k = 0; k < 8; ++k) {
+                const int64_t r = tb.r0 + j, c = tb.c0 + k;
+                if (c >= C || r >= ldx) continue;
+                dst[c * ldx + r] = r < R ? to_bf16(bf16_val(src[r * C + c]) / nrm) : 0;
+            }
+    }
+}
+
+// theta of tensor_of[b] (R x C) = theta * decay - step * O^T, O = o[b] (C x ldx)
+__global__ __launch_bounds__(256) void k_muon_update_t(const uint16_t* __restrict__ o,
+                                                       const Seg* __restrict__ segs,
+                                                       const int32_t* __restrict__ tensor_of,
+                                                       int64_t R, int64_t C, int64_t ldx,
+                                                       float decay, float step)
+{
     const int b = blockIdx.z;
     const int t = tensor_of[b];
     float* __restrict__ th = segs[t].theta;
-    const uint16_t* __restrict__ src = o + static_cast<int64_t>(b) * R * C;
-    const int64_t r0 = static_cast<int64_t>(blockIdx.y) * kT;
-    const int64_t c0 = static_cast<int64_t>(blockIdx.x) * kT;
-    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-    if (transposed) {
-        // O is C x R: stage O[c0 .. c0 + 64)[r0 .. r0 + 64) with coalesced reads along r
-        for (int i = ty; i < kT; i += 4) {
-            const int64_t c = c0 + i, r = r0 + tx;
-            tile[i][tx] = (r < R && c < C) ? src[c * R + r] : 0;
+    const uint16_t* __restrict__ src = o + static_cast<int64_t>(b) * C * ldx;
+    const TBlock tb = t_block(R, C);
+    if (tb.r0 >= R || tb.c0 >= C) return;
+    if (tb.full && (C & 3) == 0 && (reinterpret_cast<uintptr_t>(th) & 15) == 0) {
+        u32x4 w[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k)
+            w[k] = *reinterpret_cast<const u32x4*>(src + (tb.c0 + k) * ldx + tb.r0);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            f32x4v* row = reinterpret_cast<f32x4v*>(th + (tb.r0 + j) * C + tb.c0);
+            f32x4v t0 = row[0], t1 = row[1];
+            t0.x = fmaf(-step, bf16_val(static_cast<uint16_t>(bf16_at(w[0], j))), t0.x * decay);
+            t0.y = fmaf(-step, bf16_val(static_cast<uint16_t>(bf16_at(w[1], j))), t0.y * decay);
+            t0.z = fmaf(-step, bf16_val(static_cast<uint16_t>(bf16_at(w[2], j))), t0.z * decay);
+            t0.w = fmaf(-step, bf16_val(static_cast<uint16_t>(bf16_at(w[3], j))), t0.w * decay);
+            t1.x = fmaf(-step, bf16_val(static_cast<uint16_t>(bf16_at(w[4], j))), t1.x * decay);
+            t1.y = fmaf(-step, bf16_val(static_cast<uint16_t>(bf16_at(w[5], j))), t1.y * decay);
+            t1.z = fmaf(-step, bf16_val(static_cast<uint16_t>(bf16_at(w[6], j))), t1.z * decay);
+            t1.w = fmaf(-step, bf16_val(static_cast<uint16_t>(bf16_at(w[7], j))), t1.w * decay);
+            row[0] = t0;
+            row[1] = t1;
         }
-        __syncthreads();
-    }
-    for (int i = ty; i < kT; i += 4) {
-        const int64_t r = r0 + i, c = c0 + tx;
-        if (r < R && c < C) {
-            const uint16_t ob = transposed ? tile[tx][i] : src[r * C + c];
-            const int64_t e = r * C + c;
-            th[e] = fmaf(-step, bf16_val(ob), th[e] * decay);
-        }
+    } else {
+        for (int j = 0; j < 8; ++j)
+            for (int k = 0; k < 8; ++k) {
+                const int64_t r = tb.r0 + j, c = tb.c0 + k;
+                if (r < R && c < C) {
+                    const int64_t e = r * C + c;
+                    th[e] = fmaf(-step, bf16_val(src[c * ldx + r]), th[e] * decay);
+                }
+            }
     }
 }
 
@@ -414,12 +468,6 @@ hipError_t launch_muon_norm(const float* tile_ss, const int64_t* tile_range, int
     return hipGetLastError();
 }
 
-static dim3 tile_grid(int64_t R, int64_t C, int batch)
-{
-    return dim3(static_cast<unsigned>((C + kT - 1) / kT), static_cast<unsigned>((R + kT - 1) / kT),
-                static_cast<unsigned>(batch));
-}
-
 static dim3 flat_grid(int64_t n, int batch)
 {
     int64_t g = (n + 2047) / 2048;
@@ -429,36 +477,57 @@ static dim3 flat_grid(int64_t n, int batch)
 }
 
 hipError_t launch_muon_prep(const uint16_t* u, const Seg* segs, const int32_t* tensor_of,
-                            int32_t batch, const float* norm, int64_t R, int64_t C,
-                            uint16_t* x, hipStream_t stream)
+                            int32_t batch, const float* norm, int64_t n, uint16_t* x,
+                            hipStream_t stream)
 {
-    if (batch <= 0) return hipSuccess;
+    if (batch <= 0 || n <= 0) return hipSuccess;
     if (batch > 65535) return hipErrorInvalidValue;
-    if (R <= C) {
-        hipLaunchKernelGGL(k_muon_prep_flat, flat_grid(R * C, batch), dim3(256), 0, stream, u,
-                           segs, tensor_of, norm, R * C, x);
-        return hipGetLastError();
-    }
-    if ((R + kT - 1) / kT > 65535 || batch > 65535) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_muon_prep, tile_grid(R, C, batch), dim3(256), 0, stream, u, segs,
-                       tensor_of, norm, R, C, R > C ? 1 : 0, x);
+    hipLaunchKernelGGL(k_muon_prep_flat, flat_grid(n, batch), dim3(256), 0, stream, u, segs,
+                       tensor_of, norm, n, x);
     return hipGetLastError();
 }
 
 hipError_t launch_muon_update(const uint16_t* o, const Seg* segs, const int32_t* tensor_of,
-                              int32_t batch, int64_t R, int64_t C, float decay, float step,
+                              int32_t batch, int64_t n, float decay, float step,
                               hipStream_t stream)
 {
-    if (batch <= 0) return hipSuccess;
+    if (batch <= 0 || n <= 0) return hipSuccess;
     if (batch > 65535) return hipErrorInvalidValue;
-    if (R <= C) {
-        hipLaunchKernelGGL(k_muon_update_flat, flat_grid(R * C, batch), dim3(256), 0, stream, o,
-                           segs, tensor_of, R * C, decay, step);
-        return hipGetLastError();
-    }
-    if ((R + kT - 1) / kT > 65535 || batch > 65535) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_muon_update, tile_grid(R, C, batch), dim3(256), 0, stream, o, segs,
-                       tensor_of, R, C, R > C ? 1 : 0, decay, step);
+    hipLaunchKernelGGL(k_muon_update_flat, flat_grid(n, batch), dim3(256), 0, stream, o, segs,
+                       tensor_of, n, decay, step);
+    return hipGetLastError();
+}
+
+static bool t_grid(int64_t R, int64_t C, int32_t batch, dim3& grid)
+{
+    const int64_t gx = (C + kTile - 1) / kTile;
+    const int64_t gy = (R + kTile * kTilesPerGroup - 1) / (kTile * kTilesPerGroup);
+    if (gx > 0x7fffffffLL || gy > 65535 || batch > 65535) return false;
+    grid = dim3(static_cast<unsigned>(gx), static_cast<unsigned>(gy), static_cast<unsigned>(batch));
+    return true;
+}
+
+hipError_t launch_muon_prep_t(const uint16_t* u, const Seg* segs, const int32_t* tensor_of,
+                              int32_t batch, const float* norm, int64_t R, int64_t C,
+                              int64_t ldx, uint16_t* x, hipStream_t stream)
+{
+    if (batch <= 0 || R <= 0 || C <= 0) return hipSuccess;
+    dim3 grid;
+    if (ldx < R || (ldx & 7) != 0 || !t_grid(ldx, C, batch, grid)) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_muon_prep_t, grid, dim3(256), 0, stream, u, segs, tensor_of, norm, R,
+                       C, ldx, x);
+    return hipGetLastError();
+}
+
+hipError_t launch_muon_update_t(const uint16_t* o, const Seg* segs, const int32_t* tensor_of,
+                                int32_t batch, int64_t R, int64_t C, int64_t ldx, float decay,
+                                float step, hipStream_t stream)
+{
+    if (batch <= 0 || R <= 0 || C <= 0) return hipSuccess;
+    dim3 grid;
+    if (ldx < R || (ldx & 7) != 0 || !t_grid(R, C, batch, grid)) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_muon_update_t, grid, dim3(256), 0, stream, o, segs, tensor_of, R, C,
+                       ldx, decay, step);
     return hipGetLastError();
 }
 

@@ -122,7 +122,15 @@ SHAPES = [[(64, 192)], [(192, 64)], [(128, 128)], [(1, 300)], [(300, 1)], [(3, 5
           [(64, 128), (128, 64), (64, 128), (1, 77), (64, 128), (128, 64), (96, 96)],
           # lone tall-skinny matrices: the Gram product is split over K (even chunks; a
           # remainder chunk)
-          [(64, 4096)], [(5000, 48)]]
+          [(64, 4096)], [(5000, 48)],
+          # tall matrices with ragged edges (rows not a multiple of 8 or of the 64-row
+          # tile; columns not a multiple of 8), two of one shape batched together
+          [(1003, 40), (77, 9), (1003, 40), (130, 129)],
+          # tall and wide tensors of one wide shape share a batch (1008 x 40 is stored
+          # transposed, 40 x 1008 as it is); 1 x n and n x 1 share the vector kernel
+          [(1008, 40), (40, 1008), (1, 50), (50, 1), (1008, 40)],
+          # lone wide tall-skinny matrix whose K does not split evenly (remainder chunk)
+          [(48, 5000)]]
 
 
 @pytest.mark.parametrize("shapes", SHAPES, ids=lambda s: "+".join(f"{r}x{c}" for r, c in s))
