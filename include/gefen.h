@@ -280,6 +280,24 @@ int gefen_muon_step(gefen_state* st, const gefen_tensor* params, const gefen_ten
 int gefen_muon_profile_end(gefen_state* st, int32_t* steps, double* codec_ms, double* ns_ms,
                            double* rest_ms);
 
+/* ------------------------------------------------------------------------------
+ * gefen_stream_mix -- measurement support: the practical HBM ceiling for the step's
+ * access mix. One pass over n elements that reads and writes `theta` (float32), reads
+ * `grad` (GEFEN_F32 or GEFEN_BF16) and reads and writes `codes` (one byte per element),
+ * with none of the optimizer's arithmetic (two lanes of each theta vector gain the
+ * gradient, every code byte flips its low bit). It uses the tile shape that moves this
+ * mix fastest: one-shot tiles of 1024 elements, 256 threads, one 16-byte parameter
+ * vector per thread, non-temporal accesses.
+ * Bytes moved: n * (8 + 4 or 2 + 2), the step's per-element algorithmic bytes.
+ *  theta, grad, codes  caller-owned device arrays of n elements; modified in place
+ *                      (theta and codes). theta 16-byte aligned, grad 16 (F32) or 8
+ *                      (BF16) byte aligned, codes 4-byte aligned.
+ * Asynchronous on `stream`. n = 0 is a no-op.
+ * Errors: EINVAL (n < 0, NULL array, misaligned pointer), EDTYPE, EHIP.
+ * ---------------------------------------------------------------------------- */
+int gefen_stream_mix(float* theta, const void* grad, int32_t grad_dtype, uint8_t* codes,
+                     int64_t n, void* stream);
+
 /* Free the state and every device buffer it owns. NULL is a no-op. */
 void gefen_destroy(gefen_state* st);
 

@@ -34,7 +34,7 @@ SYMBOLS = [
     "gefen_read_state", "gefen_write_state", "gefen_get_fit_info", "gefen_state_bytes",
     "gefen_checkpoint_bytes", "gefen_export", "gefen_import", "gefen_profile_begin",
     "gefen_profile_end", "gefen_destroy", "gefen_last_error", "gefen_muon_init",
-    "gefen_muon_step", "gefen_muon_profile_end",
+    "gefen_muon_step", "gefen_muon_profile_end", "gefen_stream_mix",
 ]
 
 
@@ -92,6 +92,7 @@ def load_library(path: str = LIB_PATH):
     lib.gefen_muon_step.argtypes = [vp, P(gefen_tensor), P(gefen_tensor), i32, f64, f64, f64,
                                     i32, i32, f64, f64, f64, f64, vp]
     lib.gefen_muon_profile_end.argtypes = [vp, P(i32), P(f64), P(f64), P(f64)]
+    lib.gefen_stream_mix.argtypes = [vp, vp, i32, vp, i64, vp]
     lib.gefen_destroy.argtypes = [vp]
     lib.gefen_destroy.restype = None
     lib.gefen_last_error.argtypes = []
@@ -359,6 +360,20 @@ def dp_codebook(hist, k: int, stream=None):
                                  ctypes.c_void_p(cb.data_ptr()), ctypes.c_void_p(cost.data_ptr()),
                                  ctypes.c_void_p(st.data_ptr()), _stream(stream)))
     return cb, float(cost.item()), int(st.item())
+
+
+def stream_mix(theta, grad, codes, stream=None):
+    """One pass of the step's byte mix (theta fp32 read + write, grad read, one code byte
+    read + write per element) with no optimizer arithmetic: the streaming ceiling."""
+    lib = load_library()
+    torch = _torch()
+    n = theta.numel()
+    if grad.numel() != n or codes.numel() != n or codes.dtype != torch.uint8:
+        raise ValueError("theta, grad and codes must have the same numel; codes uint8")
+    gdt = F32 if grad.dtype == torch.float32 else BF16
+    _check(lib.gefen_stream_mix(ctypes.c_void_p(theta.data_ptr()),
+                                ctypes.c_void_p(grad.data_ptr()), gdt,
+                                ctypes.c_void_p(codes.data_ptr()), n, _stream(stream)))
 
 
 class Gefen:

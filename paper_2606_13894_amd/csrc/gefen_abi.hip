@@ -4,6 +4,7 @@
 #include "gefen.h"
 #include "gefen_internal.h"
 #include "muon_internal.h"
+#include "measure_internal.h"
 
 #include <rocblas/rocblas.h>
 
@@ -565,12 +566,34 @@ int plan_tiles(gefen_state* st, const std::vector<std::vector<int64_t>>& starts)
                 int64_t e = 0;
                 for (const Tile& tl : lists[i]) e += tl.nelem;
                 if (e > fold_max) continue;
-                for (Tile tl : lists[i]) {
+                // Uniform small-block tiles are cut to kThreads / lpb blocks, lpb = p
+                // rounded up to a power of two: the generic kernel gives each block a
+                // group of lpb lanes and covers such a tile in one pass.
+                for (size_t j = 0; j < lists[i].size(); ++j) {
+                    Tile tl = lists[i][j];
+                    const int32_t kd = tile_kinds[i][j];
                     tl.vpl = 0;
                     tl.lpb_log2 = 0;
-                    front.push_back(tl);
+                    const int64_t p = st->explicit_blocks ? 0 : st->period[tl.seg];
+                    if (kd == KIND_L && p > 0) {
+                        int64_t lpb = 1;
+                        while (lpb < p) lpb <<= 1;
+                        const int64_t per = kThreads / lpb;
+                        for (int64_t b = 0; b < tl.nblk; b += per) {
+                            Tile sub = tl;
+                            const int64_t nb = std::min<int64_t>(per, tl.nblk - b);
+                            sub.elem0 = tl.elem0 + b * p;
+                            sub.blk0 = tl.blk0 + b;
+                            sub.nblk = static_cast<int16_t>(nb);
+                            sub.nelem = nb * p;
+                            front.push_back(sub);
+                            front_kinds.push_back(kd);
+                        }
+                    } else {
+                        front.push_back(tl);
+                        front_kinds.push_back(kd);
+                    }
                 }
-                front_kinds.insert(front_kinds.end(), tile_kinds[i].begin(), tile_kinds[i].end());
                 any_dtype = keys[i].gdtype;
                 lists[i].clear();
                 tile_kinds[i].clear();
@@ -1298,6 +1321,26 @@ int gefen_profile_end(gefen_state* st, int32_t cap, int32_t* n_classes, int32_t*
         if (bytes_per_launch) bytes_per_launch[c] = k.bytes;
     }
     st->prof_free();
+    return GEFEN_OK;
+}
+
+int gefen_stream_mix(float* theta, const void* grad, int32_t grad_dtype, uint8_t* codes,
+                     int64_t n, void* stream)
+{
+    g_err.clear();
+    if (n < 0) return fail(GEFEN_EINVAL, "n must be >= 0");
+    if (grad_dtype != GEFEN_F32 && grad_dtype != GEFEN_BF16)
+        return fail(GEFEN_EDTYPE, "grad_dtype %d is not F32 or BF16", grad_dtype);
+    if (n == 0) return GEFEN_OK;
+    if (!theta || !grad || !codes) return fail(GEFEN_EINVAL, "NULL array");
+    const uintptr_t ga = grad_dtype == GEFEN_F32 ? 15 : 7;
+    if ((reinterpret_cast<uintptr_t>(theta) & 15) || (reinterpret_cast<uintptr_t>(grad) & ga) ||
+        (reinterpret_cast<uintptr_t>(codes) & 3))
+        return fail(GEFEN_EINVAL, "theta must be 16-byte, grad %d-byte, codes 4-byte aligned",
+                    static_cast<int>(ga + 1));
+    const hipError_t e = launch_stream_mix(theta, grad, grad_dtype == GEFEN_F32 ? DT_F32 : DT_BF16,
+                                           codes, n, as_stream(stream));
+    if (e != hipSuccess) return fail(GEFEN_EHIP, "stream mix launch: %s", hipGetErrorString(e));
     return GEFEN_OK;
 }
 

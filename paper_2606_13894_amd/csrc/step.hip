@@ -230,8 +230,53 @@ __device__ void foreign_tile(LdsTables& L, const Tile& tl, const Seg& sg,
         }
         return;
     }
-    if (sg.period > 0 ? sg.period <= kSmallBlock : true) {
-        // small blocks (uniform p <= 32, or an explicit small-block tile): lane per block
+    if (sg.period > 0 && sg.period <= kSmallBlock) {
+        // small uniform blocks: a group of lpb = 2^ceil(log2 p) consecutive lanes per
+        // block, one element per lane, so every access of a wave is contiguous; block
+        // sums by shuffles inside the group. The planner sizes these tiles to one pass
+        // (nblk * lpb <= BS); longer tiles take several.
+        const int p = static_cast<int>(sg.period);
+        int lpb = 1;
+        while (lpb < p) lpb <<= 1;
+        const int li = tid & (lpb - 1);
+        for (int b0 = 0; b0 < tl.nblk; b0 += BS / lpb) {
+            const int bi = b0 + tid / lpb;
+            const bool okb = bi < tl.nblk;
+            const bool ok = okb && li < p;
+            const int64_t e = tl.elem0 + static_cast<int64_t>(bi) * p + li;
+            const int64_t blk = tl.blk0 + bi;
+            float g = 0.0f, tv = 0.0f, s_old = 0.0f, v_old = 0.0f;
+            int q0 = 0;
+            if (ok) {
+                g = load_grad(sg.grad, e, gdt);
+                q0 = code_ld<CB>(codes, sg.code_off + e);
+                tv = sg.theta[e];
+            }
+            if (okb) {
+                s_old = scale[blk];
+                v_old = vmom[blk];
+            }
+            const float mm = ok ? momentum(L, q0, s_old, g, sc) : 0.0f;
+            float ss = g * g, am = fabsf(mm);
+            for (int off = 1; off < lpb; off <<= 1) {
+                ss += __shfl_xor(ss, off);
+                am = fmaxf(am, __shfl_xor(am, off));
+            }
+            const BlockOut bo = finish_block(ss, am, v_old, static_cast<float>(p), sc);
+            if (okb && li == 0) {
+                scale[blk] = bo.s_new;
+                vmom[blk] = bo.v_new;
+            }
+            if (ok) {
+                const int q = bo.s_new > 0.0f ? encode(L, mm * bo.inv_s, half_ng, ng_m1) : 0;
+                sg.theta[e] = fmaf(-bo.r, mm, tv * sc.decay);
+                code_st<CB>(codes, sg.code_off + e, q0, q);
+            }
+        }
+        return;
+    }
+    if (sg.period == 0) {
+        // explicit small-block tile: lane per block
         for (int bi = tid; bi < tl.nblk; bi += BS) {
             int64_t start, len;
             block_range(sg, tl, bi, start, len);
@@ -240,23 +285,37 @@ __device__ void foreign_tile(LdsTables& L, const Tile& tl, const Seg& sg,
             const float v_old = vmom[blk];
             float* __restrict__ th = sg.theta + start;
             const int64_t cj = sg.code_off + start;
+            // len <= kSmallBlock: the block stays in registers. Every load is issued
+            // unconditionally (past the block's end it re-reads its first element), so
+            // the loads of a pass go out together instead of one guarded load at a time.
+            float g[kSmallBlock], m[kSmallBlock], tv[kSmallBlock];
+            int q0[kSmallBlock];
+#pragma unroll
+            for (int i = 0; i < kSmallBlock; ++i) {
+                const int64_t ii = i < len ? i : 0;
+                g[i] = load_grad(sg.grad, start + ii, gdt);
+                q0[i] = code_ld<CB>(codes, cj + ii);
+                tv[i] = th[ii];
+            }
             float ss = 0.0f, am = 0.0f;
-            for (int64_t i = 0; i < len; ++i) {
-                const float g = load_grad(sg.grad, start + i, gdt);
-                const float mm = momentum(L, code_ld<CB>(codes, cj + i), s_old, g, sc);
-                ss = fmaf(g, g, ss);
-                am = fmaxf(am, fabsf(mm));
+#pragma unroll
+            for (int i = 0; i < kSmallBlock; ++i) {
+                const bool ok = i < len;
+                m[i] = ok ? momentum(L, q0[i], s_old, g[i], sc) : 0.0f;
+                ss = ok ? fmaf(g[i], g[i], ss) : ss;
+                am = fmaxf(am, fabsf(m[i]));
             }
             const BlockOut bo = finish_block(ss, am, v_old, static_cast<float>(len), sc);
             scale[blk] = bo.s_new;
             vmom[blk] = bo.v_new;
-            for (int64_t i = 0; i < len; ++i) {
-                const float g = load_grad(sg.grad, start + i, gdt);
-                const int q0 = code_ld<CB>(codes, cj + i);
-                const float mm = momentum(L, q0, s_old, g, sc);
-                const int q = bo.s_new > 0.0f ? encode(L, mm * bo.inv_s, half_ng, ng_m1) : 0;
-                th[i] = fmaf(-bo.r, mm, th[i] * sc.decay);
-                code_st<CB>(codes, cj + i, q0, q);
+#pragma unroll
+            for (int i = 0; i < kSmallBlock; ++i) {
+                if (i < len) {
+                    const int q = bo.s_new > 0.0f ? encode(L, m[i] * bo.inv_s, half_ng, ng_m1)
+                                                  : 0;
+                    th[i] = fmaf(-bo.r, m[i], tv[i] * sc.decay);
+                    code_st<CB>(codes, cj + i, q0[i], q);
+                }
             }
         }
         return;
@@ -349,7 +408,7 @@ __global__ __launch_bounds__(BS) void k_step_u(const Tile* __restrict__ tiles,
 // chunk). The reduce pass uses ordinary loads so that the update pass finds gradient and
 // code lines in cache. Both passes evaluate the momentum with the same operations, so
 // they agree bit for bit.
-template <int GDT, int BS, int CB>
+template <int GDT, int BS, int CB, int UNR = 2>
 __device__ __forceinline__ void pass_reduce(const LdsTables& L, const Seg& sg,
                                             const uint8_t* __restrict__ codes, const Span& sp,
                                             float s_old, const StepScalars& sc, float& ss,
@@ -357,16 +416,30 @@ __device__ __forceinline__ void pass_reduce(const LdsTables& L, const Seg& sg,
 {
     const int tid = threadIdx.x;
     const int64_t cj = sg.code_off;
-#pragma unroll 2
-    for (int64_t v = sp.vb + tid; v < sp.ve; v += BS) {
-        float g[4];
-        load_grad4<GDT>(sg, v, g);
-        const uint32_t q4 = code_ld4<CB>(codes, cj + 4 * v);
+    // batches of UNR vectors per thread, every load of a batch issued before its use
+    for (int64_t v0 = sp.vb + tid; v0 < sp.ve; v0 += static_cast<int64_t>(BS) * UNR) {
+        float g[UNR][4];
+        uint32_t q4[UNR];
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            const float mm = momentum(L, code_get<CB>(q4, c), s_old, g[c], sc);
-            ss = fmaf(g[c], g[c], ss);
-            am = fmaxf(am, fabsf(mm));
+        for (int u = 0; u < UNR; ++u) {
+            const int64_t v = v0 + static_cast<int64_t>(u) * BS;
+            q4[u] = 0;
+            g[u][0] = g[u][1] = g[u][2] = g[u][3] = 0.0f;
+            if (v < sp.ve) {
+                load_grad4<GDT>(sg, v, g[u]);
+                q4[u] = code_ld4<CB>(codes, cj + 4 * v);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) {
+            const bool ok = v0 + static_cast<int64_t>(u) * BS < sp.ve;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const float mm = ok ? momentum(L, code_get<CB>(q4[u], c), s_old, g[u][c], sc)
+                                    : 0.0f;
+                ss = fmaf(g[u][c], g[u][c], ss);
+                am = fmaxf(am, fabsf(mm));
+            }
         }
     }
     for (int64_t i = tid; i < sp.nh + sp.nt; i += BS) {
@@ -378,7 +451,7 @@ __device__ __forceinline__ void pass_reduce(const LdsTables& L, const Seg& sg,
     }
 }
 
-template <int GDT, int BS, int CB>
+template <int GDT, int BS, int CB, int UNR = 2>
 __device__ __forceinline__ void pass_update(const LdsTables& L, const Seg& sg,
                                             uint8_t* __restrict__ codes, const Span& sp,
                                             float s_old, const BlockOut& bo,
@@ -387,25 +460,38 @@ __device__ __forceinline__ void pass_update(const LdsTables& L, const Seg& sg,
     const int tid = threadIdx.x;
     float* __restrict__ th = sg.theta;
     const int64_t cj = sg.code_off;
-#pragma unroll 2
-    for (int64_t v = sp.vb + tid; v < sp.ve; v += BS) {
-        float g[4];
-        load_grad4<GDT>(sg, v, g);
-        const uint32_t q4 = code_ld4<CB>(codes, cj + 4 * v);
-        const f32x4 t4 = __builtin_nontemporal_load(gl<f32x4>(th) + v);
-        const float tv[4] = {t4.x, t4.y, t4.z, t4.w};
-        float out[4];
-        uint32_t packed = 0;
+    for (int64_t v0 = sp.vb + tid; v0 < sp.ve; v0 += static_cast<int64_t>(BS) * UNR) {
+        float g[UNR][4];
+        uint32_t q4[UNR];
+        f32x4 t4[UNR];
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            const float mm = momentum(L, code_get<CB>(q4, c), s_old, g[c], sc);
-            const int q = bo.s_new > 0.0f ? encode(L, mm * bo.inv_s, half_ng, ng_m1) : 0;
-            packed |= static_cast<uint32_t>(q) << (CB * c);
-            out[c] = fmaf(-bo.r, mm, tv[c] * sc.decay);
+        for (int u = 0; u < UNR; ++u) {
+            const int64_t v = v0 + static_cast<int64_t>(u) * BS;
+            if (v < sp.ve) {
+                load_grad4<GDT>(sg, v, g[u]);
+                q4[u] = code_ld4<CB>(codes, cj + 4 * v);
+                t4[u] = __builtin_nontemporal_load(gl<f32x4>(th) + v);
+            }
         }
-        const f32x4 o4 = {out[0], out[1], out[2], out[3]};
-        __builtin_nontemporal_store(o4, glw<f32x4>(th) + v);
-        code_st4<CB>(codes, cj + 4 * v, packed);
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) {
+            const int64_t v = v0 + static_cast<int64_t>(u) * BS;
+            if (v < sp.ve) {
+                const float tv[4] = {t4[u].x, t4[u].y, t4[u].z, t4[u].w};
+                float out[4];
+                uint32_t packed = 0;
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const float mm = momentum(L, code_get<CB>(q4[u], c), s_old, g[u][c], sc);
+                    const int q = bo.s_new > 0.0f ? encode(L, mm * bo.inv_s, half_ng, ng_m1) : 0;
+                    packed |= static_cast<uint32_t>(q) << (CB * c);
+                    out[c] = fmaf(-bo.r, mm, tv[c] * sc.decay);
+                }
+                const f32x4 o4 = {out[0], out[1], out[2], out[3]};
+                __builtin_nontemporal_store(o4, glw<f32x4>(th) + v);
+                code_st4<CB>(codes, cj + 4 * v, packed);
+            }
+        }
     }
     for (int64_t i = tid; i < sp.nh + sp.nt; i += BS) {
         const int64_t e = i < sp.nh ? sp.start + i : sp.tail0 + (i - sp.nh);

@@ -118,3 +118,17 @@ def test_stress_block_recipe():
     seq = W.stress_block_offsets(n=10_000_000, variant="sequential")
     s2 = np.diff(seq)
     assert seq[-1] == 10_000_000 and s2[:-1].min() >= 64 and s2.max() <= 65536
+
+
+def test_stream_mix_argument_errors(lib):
+    """The measurement pass checks its arguments before any device call."""
+    a16, a8 = 0x10000, 0x10008
+    assert lib.gefen_stream_mix(a16, a16, 0, a16, -1, None) == -1
+    assert lib.gefen_stream_mix(a16, a16, 9, a16, 16, None) == -2
+    assert lib.gefen_stream_mix(None, a16, 0, a16, 16, None) == -1
+    assert lib.gefen_stream_mix(a16 + 4, a16, 0, a16, 16, None) == -1      # theta 16 B
+    assert lib.gefen_stream_mix(a16, a8, 0, a16, 16, None) == -1           # fp32 grad 16 B
+    assert lib.gefen_stream_mix(a16, a16 + 2, 1, a16, 16, None) == -1      # bf16 grad 8 B
+    assert lib.gefen_stream_mix(a16, a16, 0, a16 + 1, 16, None) == -1      # codes 4 B
+    assert b"aligned" in lib.gefen_last_error()
+    assert lib.gefen_stream_mix(None, None, 0, None, 0, None) == 0         # n = 0: no-op

@@ -137,3 +137,28 @@ def test_dp_from_gradient_histogram():
     assert st == st_ref == 0
     np.testing.assert_array_equal(cb.cpu().numpy(), cb_ref)
     assert cost == cost_ref
+
+
+@pytest.mark.parametrize("gdtype", [torch.float32, torch.bfloat16])
+def test_stream_mix_moves_every_byte(gdtype):
+    """The streaming-ceiling pass (measurement support) touches every element: in each
+    full 4-element vector lanes 0 and 3 gain the gradient, the ragged tail gains it
+    element by element, and every code byte flips its low bit."""
+    dev = _dev()
+    n = 3 * 1024 + 4 * 77 + 3
+    rng = np.random.default_rng(5)
+    th0 = rng.standard_normal(n).astype(np.float32)
+    g = torch.from_numpy(rng.standard_normal(n).astype(np.float32)).to(gdtype)
+    c0 = rng.integers(0, 256, n, dtype=np.uint8)
+    theta = torch.from_numpy(th0).to(dev)
+    codes = torch.from_numpy(c0).to(dev)
+    gf.stream_mix(theta, g.to(dev), codes)
+    torch.cuda.synchronize()
+    gd = g.float().numpy()
+    ref = th0.copy()
+    full = n // 4 * 4
+    ref[0:full:4] += gd[0:full:4]
+    ref[3:full:4] += gd[3:full:4]
+    ref[full:] += gd[full:]
+    np.testing.assert_array_equal(theta.cpu().numpy(), ref)
+    np.testing.assert_array_equal(codes.cpu().numpy(), c0 ^ 1)
