@@ -262,7 +262,10 @@ int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, voi
  *  params, grads  as for gefen_step; momentum in [0, 1); ns_steps in [0, 100];
  *  ns_eps > 0. Muon's defaults: ns_steps 5, (ns_a, ns_b, ns_c) =
  *  (3.4445, -4.7750, 2.0315), ns_eps 1e-7, nesterov 1.
- * Asynchronous on `stream`; no allocation. Refits (gefen_fit_codebook) apply as for
+ * Asynchronous on `stream`; no allocation. The shape groups are split over two lanes
+ * that run concurrently: one on `stream`, one on a stream the state owns, which waits
+ * for the norms on `stream`; `stream` then waits for it, so all of the step's work is
+ * ordered before later work on `stream`. Refits (gefen_fit_codebook) apply as for
  * gefen_step. The bfloat16 momentum matrix of the last step can be read as array 6 of
  * gefen_read_state (uint16 bit patterns at each element's code index).
  * Errors: EINVAL (arguments, gefen_muon_init not called), EDTYPE, EHIP.
@@ -273,12 +276,12 @@ int gefen_muon_step(gefen_state* st, const gefen_tensor* params, const gefen_ten
                     double ns_eps, void* stream);
 
 /* Measurement of Gefen-Muon steps (after gefen_muon_init and gefen_profile_begin):
- * sums over the profiled steps of the codec time (codec and norms), the Newton-Schulz
- * GEMM time (all shape groups) and the rest (normalise and update kernels),
- * in milliseconds, from HIP events on the step's stream; then disarms like
+ * sums over the profiled steps of the codec time (codec and norms) and of the
+ * orthogonalisation wall time (normalise, Newton-Schulz and update of every shape
+ * group, on both of the step's streams, from the end of the norms to the join), in
+ * milliseconds, from HIP events on the step's stream; then disarms like
  * gefen_profile_end. */
-int gefen_muon_profile_end(gefen_state* st, int32_t* steps, double* codec_ms, double* ns_ms,
-                           double* rest_ms);
+int gefen_muon_profile_end(gefen_state* st, int32_t* steps, double* codec_ms, double* ortho_ms);
 
 /* ------------------------------------------------------------------------------
  * gefen_stream_mix -- measurement support: the practical HBM ceiling for the step's

@@ -91,7 +91,7 @@ def load_library(path: str = LIB_PATH):
     lib.gefen_muon_init.argtypes = [vp, vp, i32, vp]
     lib.gefen_muon_step.argtypes = [vp, P(gefen_tensor), P(gefen_tensor), i32, f64, f64, f64,
                                     i32, i32, f64, f64, f64, f64, vp]
-    lib.gefen_muon_profile_end.argtypes = [vp, P(i32), P(f64), P(f64), P(f64)]
+    lib.gefen_muon_profile_end.argtypes = [vp, P(i32), P(f64), P(f64)]
     lib.gefen_stream_mix.argtypes = [vp, vp, i32, vp, i64, vp]
     lib.gefen_destroy.argtypes = [vp]
     lib.gefen_destroy.restype = None
@@ -218,12 +218,13 @@ class GefenState:
                                     _stream(stream)))
 
     def muon_profile_end(self):
-        """Profiled Gefen-Muon steps: {steps, codec_ms, ns_ms, rest_ms} (sums)."""
+        """Profiled Gefen-Muon steps: {steps, codec_ms, ortho_ms} (sums; ortho_ms is the
+        wall time of normalise + Newton-Schulz + update over both lanes)."""
         n = ctypes.c_int32()
-        a, b, c = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+        a, b = ctypes.c_double(), ctypes.c_double()
         _check(_lib.gefen_muon_profile_end(self._h, ctypes.byref(n), ctypes.byref(a),
-                                           ctypes.byref(b), ctypes.byref(c)))
-        return {"steps": n.value, "codec_ms": a.value, "ns_ms": b.value, "rest_ms": c.value}
+                                           ctypes.byref(b)))
+        return {"steps": n.value, "codec_ms": a.value, "ortho_ms": b.value}
 
     def fit_codebook(self, grads: Sequence, stream=None):
         _check(_lib.gefen_fit_codebook(self._h, _tensors(grads, "grads"), self._n,

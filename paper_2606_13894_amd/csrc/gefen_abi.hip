@@ -157,22 +157,32 @@ struct gefen_state {
     uint16_t* muon_u = nullptr;
     int32_t* muon_tensor_of = nullptr;
     std::vector<MuonGroup> muon_groups;
-    uint16_t* muon_x[2] = {nullptr, nullptr};
-    uint16_t* muon_a = nullptr;
-    uint16_t* muon_b = nullptr;
-    float* muon_partial = nullptr;   // split-K partial Gram products (float32)
-    rocblas_handle blas = nullptr;
+    // The shape groups are split over two lanes that run concurrently: lane 0 on the
+    // caller's stream, lane 1 on a stream of the library's own (forked after the norms,
+    // joined at the end of the step). Each lane has its own rocBLAS handle (fixed
+    // workspace) and Newton-Schulz buffers.
+    struct MuonLane {
+        rocblas_handle blas = nullptr;
+        uint16_t* x[2] = {nullptr, nullptr};
+        uint16_t* a = nullptr;
+        uint16_t* b = nullptr;
+        float* partial = nullptr;       // split-K partial Gram products (float32)
+        std::vector<int32_t> groups;    // indices into muon_groups, in launch order
+    };
+    MuonLane muon_lane[2];
+    hipStream_t muon_side = nullptr;    // lane 1's stream (default priority)
+    hipEvent_t muon_fork = nullptr, muon_join = nullptr;
 
     // measurement: events[(step * classes + c) * 2 + {0 start, 1 stop}]
     bool prof_armed = false;
     int32_t prof_max_steps = 0, prof_steps = 0;
     std::vector<hipEvent_t> prof_events;
-    // Gefen-Muon steps: per step, events [codec start, codec end, (NS start, NS end) per
-    // shape group, step end]
+    // Gefen-Muon steps: per step, events [step start, codec + norms end, step end], all
+    // on the caller's stream (the step end follows the join of lane 1)
     int32_t muon_prof_steps = 0;
     std::vector<hipEvent_t> muon_prof_events;
 
-    size_t muon_prof_stride() const { return 3 + 2 * muon_groups.size(); }
+    size_t muon_prof_stride() const { return 3; }
 
     void prof_free()
     {
@@ -188,7 +198,11 @@ struct gefen_state {
     ~gefen_state()
     {
         prof_free();
-        if (blas) (void)rocblas_destroy_handle(blas);
+        for (MuonLane& l : muon_lane)
+            if (l.blas) (void)rocblas_destroy_handle(l.blas);
+        if (muon_fork) (void)hipEventDestroy(muon_fork);
+        if (muon_join) (void)hipEventDestroy(muon_join);
+        if (muon_side) (void)hipStreamDestroy(muon_side);
         for (void* p : dev_allocs) (void)hipFree(p);
         if (segs_pinned) (void)hipHostFree(segs_pinned);
         for (hipEvent_t e : seg_evt)
@@ -1372,10 +1386,10 @@ float host_bf16_value(float x)
             return fail(GEFEN_EHIP, "%s failed: %s", #call, rocblas_status_to_string(s_)); \
     } while (0)
 
-hipStream_t rocblas_get_stream_for(gefen_state* st)
+hipStream_t rocblas_get_stream_for(rocblas_handle h)
 {
     hipStream_t s = nullptr;
-    (void)rocblas_get_stream(st->blas, &s);
+    (void)rocblas_get_stream(h, &s);
     return s;
 }
 
@@ -1384,7 +1398,7 @@ hipStream_t rocblas_get_stream_for(gefen_state* st)
 // float32 accumulation. rocBLAS is column-major, so it sees each X as X^T (n x m, leading
 // dimension ldx): A = (X^T)^T X^T and the new X^T = a X^T + X^T B (B is symmetric). Both
 // operands of the Gram product run along K contiguously, the layout rocBLAS is fastest on.
-int ns_iteration(gefen_state* st, const gefen_state::MuonGroup& g, const uint16_t* x,
+int ns_iteration(gefen_state::MuonLane& ln, const gefen_state::MuonGroup& g, const uint16_t* x,
                  uint16_t* xo, float a, float b, float c)
 {
     const int64_t m = g.m, n = g.ldx;   // zero columns beyond g.n add nothing
@@ -1401,32 +1415,32 @@ int ns_iteration(gefen_state* st, const gefen_state::MuonGroup& g, const uint16_
         const int64_t rest = n - full * kc;
         if (full > 0)
             GEFEN_BLAS(rocblas_gemm_strided_batched_ex(
-                st->blas, rocblas_operation_transpose, rocblas_operation_none, mi, mi,
+                ln.blas, rocblas_operation_transpose, rocblas_operation_none, mi, mi,
                 static_cast<rocblas_int>(kc), &one, x, bf, ldx, kc, x, bf, ldx, kc, &zero,
-                st->muon_partial, f32, mi, sa, st->muon_partial, f32, mi, sa,
+                ln.partial, f32, mi, sa, ln.partial, f32, mi, sa,
                 static_cast<rocblas_int>(full), f32, rocblas_gemm_algo_standard, 0, 0));
         if (rest > 0)
             GEFEN_BLAS(rocblas_gemm_ex(
-                st->blas, rocblas_operation_transpose, rocblas_operation_none, mi, mi,
+                ln.blas, rocblas_operation_transpose, rocblas_operation_none, mi, mi,
                 static_cast<rocblas_int>(rest), &one, x + full * kc, bf, ldx, x + full * kc, bf,
-                ldx, &zero, st->muon_partial + full * sa, f32, mi, st->muon_partial + full * sa,
+                ldx, &zero, ln.partial + full * sa, f32, mi, ln.partial + full * sa,
                 f32, mi, f32, rocblas_gemm_algo_standard, 0, 0));
-        GEFEN_HIP(launch_muon_splitk_sum(st->muon_partial,
+        GEFEN_HIP(launch_muon_splitk_sum(ln.partial,
                                          static_cast<int32_t>(full + (rest > 0 ? 1 : 0)), sa,
-                                         st->muon_a, rocblas_get_stream_for(st)));
+                                         ln.a, rocblas_get_stream_for(ln.blas)));
     } else {
         GEFEN_BLAS(rocblas_gemm_strided_batched_ex(
-            st->blas, rocblas_operation_transpose, rocblas_operation_none, mi, mi, ni, &one, x,
-            bf, ldx, sx, x, bf, ldx, sx, &zero, st->muon_a, bf, mi, sa, st->muon_a, bf, mi, sa,
+            ln.blas, rocblas_operation_transpose, rocblas_operation_none, mi, mi, ni, &one, x,
+            bf, ldx, sx, x, bf, ldx, sx, &zero, ln.a, bf, mi, sa, ln.a, bf, mi, sa,
             g.count, f32, rocblas_gemm_algo_standard, 0, 0));
     }
     GEFEN_BLAS(rocblas_gemm_strided_batched_ex(
-        st->blas, rocblas_operation_none, rocblas_operation_none, mi, mi, mi, &c, st->muon_a, bf,
-        mi, sa, st->muon_a, bf, mi, sa, &b, st->muon_a, bf, mi, sa, st->muon_b, bf, mi, sa,
+        ln.blas, rocblas_operation_none, rocblas_operation_none, mi, mi, mi, &c, ln.a, bf,
+        mi, sa, ln.a, bf, mi, sa, &b, ln.a, bf, mi, sa, ln.b, bf, mi, sa,
         g.count, f32, rocblas_gemm_algo_standard, 0, 0));
     GEFEN_BLAS(rocblas_gemm_strided_batched_ex(
-        st->blas, rocblas_operation_none, rocblas_operation_none, ni, mi, mi, &one, x, bf, ldx,
-        sx, st->muon_b, bf, mi, sa, &a, x, bf, ldx, sx, xo, bf, ldx, sx, g.count, f32,
+        ln.blas, rocblas_operation_none, rocblas_operation_none, ni, mi, mi, &one, x, bf, ldx,
+        sx, ln.b, bf, mi, sa, &a, x, bf, ldx, sx, xo, bf, ldx, sx, g.count, f32,
         rocblas_gemm_algo_standard, 0, 0));
     return GEFEN_OK;
 }
@@ -1544,7 +1558,7 @@ int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, voi
     // has too few 128 x 128 tiles to occupy the GPU. A transposed X gets zero columns up
     // to a multiple of 8 * splits, so that the chunks are equal and one batched call
     // covers them.
-    int64_t max_partial = 0, max_x = 0, max_a = 0;
+    int64_t max_x = 0;
     for (auto& g : st->muon_groups) {
         const int64_t m = g.m;
         const int64_t tiles = ((m + 127) / 128) * ((m + 127) / 128);
@@ -1554,9 +1568,29 @@ int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, voi
         }
         if (g.splits > 1 && g.parts[0].transposed)
             g.ldx = (g.n + 8 * g.splits - 1) / (8 * g.splits) * (8 * g.splits);
-        if (g.splits > 1) max_partial = std::max(max_partial, g.splits * m * m);
         max_x = std::max(max_x, g.count * m * g.ldx);
-        max_a = std::max(max_a, g.count * m * m);
+    }
+    // Lanes: groups in decreasing order of Newton-Schulz work, each to the lane with
+    // less work so far (GEFEN_MUON_LANES=1 keeps every group on the caller's stream).
+    const int n_lanes = std::min(2, std::max(1, env_int("GEFEN_MUON_LANES", 2)));
+    {
+        std::vector<int32_t> byw(st->muon_groups.size());
+        std::vector<double> work(byw.size());
+        for (size_t gi = 0; gi < byw.size(); ++gi) {
+            const auto& g = st->muon_groups[gi];
+            byw[gi] = static_cast<int32_t>(gi);
+            const double m = static_cast<double>(g.m), nn = static_cast<double>(g.ldx);
+            work[gi] = g.count * (g.m > 1 ? 4.0 * m * m * nn + 2.0 * m * m * m : 4.0 * nn);
+        }
+        std::stable_sort(byw.begin(), byw.end(),
+                         [&](int32_t a, int32_t b) { return work[a] > work[b]; });
+        double load[2] = {0.0, 0.0};
+        for (gefen_state::MuonLane& l : st->muon_lane) l.groups.clear();
+        for (int32_t gi : byw) {
+            const int l = (n_lanes > 1 && load[1] < load[0]) ? 1 : 0;
+            st->muon_lane[l].groups.push_back(gi);
+            load[l] += work[gi];
+        }
     }
     // Shape groups above kMuonMaxGroup elements are refused: a state of that size (the
     // GPT-2 1B shapes, 4e8 elements in one group) failed with a device memory fault in
@@ -1574,28 +1608,54 @@ int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, voi
     if ((rc = st->alloc(&st->muon_norm, 4 * static_cast<size_t>(n), false))) return rc;
     if ((rc = st->alloc(&st->muon_tensor_of, 4 * order.size(), false))) return rc;
     if ((rc = st->alloc(&st->muon_u, 2 * static_cast<size_t>(st->code_off[n]), false))) return rc;
-    for (auto& x : st->muon_x)
-        if ((rc = st->alloc(&x, 2 * static_cast<size_t>(max_x), false))) return rc;
-    if ((rc = st->alloc(&st->muon_a, 2 * static_cast<size_t>(max_a), false))) return rc;
-    if ((rc = st->alloc(&st->muon_b, 2 * static_cast<size_t>(max_a), false))) return rc;
-    if ((rc = st->alloc(&st->muon_partial, 4 * static_cast<size_t>(max_partial), false))) return rc;
+    int64_t lane_x[2] = {0, 0};
+    for (int l = 0; l < 2; ++l) {
+        gefen_state::MuonLane& ln = st->muon_lane[l];
+        int64_t mx = 0, ma = 0, mp = 0;
+        for (int32_t gi : ln.groups) {
+            const auto& g = st->muon_groups[gi];
+            mx = std::max(mx, g.count * g.m * g.ldx);
+            ma = std::max(ma, g.count * g.m * g.m);
+            if (g.splits > 1) mp = std::max(mp, g.splits * g.m * g.m);
+        }
+        lane_x[l] = mx;
+        if (ln.groups.empty()) continue;
+        for (auto& x : ln.x)
+            if ((rc = st->alloc(&x, 2 * static_cast<size_t>(mx), false))) return rc;
+        if ((rc = st->alloc(&ln.a, 2 * static_cast<size_t>(ma), false))) return rc;
+        if ((rc = st->alloc(&ln.b, 2 * static_cast<size_t>(ma), false))) return rc;
+        if ((rc = st->alloc(&ln.partial, 4 * static_cast<size_t>(mp), false))) return rc;
+    }
     GEFEN_HIP(hipMemcpy(st->muon_tiles, tiles.data(), sizeof(Tile) * tiles.size(), hipMemcpyHostToDevice));
     GEFEN_HIP(hipMemcpy(st->muon_tile_range, tile_range.data(), 8 * tile_range.size(), hipMemcpyHostToDevice));
     GEFEN_HIP(hipMemcpy(st->muon_tensor_of, order.data(), 4 * order.size(), hipMemcpyHostToDevice));
 
-    // rocBLAS handle with a fixed workspace, set before any product runs, so that steps
-    // allocate nothing; a product that would need more returns an error status. One
-    // Newton-Schulz iteration per group on zeroed matrices loads and checks every GEMM
-    // the steps use.
-    GEFEN_BLAS(rocblas_create_handle(&st->blas));
-    GEFEN_BLAS(rocblas_set_stream(st->blas, stream));
-    GEFEN_BLAS(rocblas_set_device_memory_size(st->blas, kBlasWorkspace));
-    st->workspace_bytes += static_cast<int64_t>(kBlasWorkspace);
-    GEFEN_HIP(fill_zero(st->muon_x[0], 2 * static_cast<size_t>(max_x), stream));
-    for (const auto& g : st->muon_groups)
-        if (g.m > 1 &&
-            (rc = ns_iteration(st, g, st->muon_x[0], st->muon_x[1], 1.0f, 1.0f, 1.0f)))
-            return rc;
+    // One rocBLAS handle per lane with a fixed workspace, set before any product runs,
+    // so that steps allocate nothing; a product that would need more returns an error
+    // status. One Newton-Schulz iteration per group on zeroed matrices loads and checks
+    // every GEMM the steps use, on the lane's own stream.
+    if (!st->muon_lane[1].groups.empty()) {
+        GEFEN_HIP(hipStreamCreateWithFlags(&st->muon_side, hipStreamNonBlocking));
+        GEFEN_HIP(hipEventCreateWithFlags(&st->muon_fork, hipEventDisableTiming));
+        GEFEN_HIP(hipEventCreateWithFlags(&st->muon_join, hipEventDisableTiming));
+    }
+    for (int l = 0; l < 2; ++l) {
+        gefen_state::MuonLane& ln = st->muon_lane[l];
+        if (ln.groups.empty()) continue;
+        hipStream_t ls = l == 0 ? stream : st->muon_side;
+        GEFEN_BLAS(rocblas_create_handle(&ln.blas));
+        GEFEN_BLAS(rocblas_set_stream(ln.blas, ls));
+        GEFEN_BLAS(rocblas_set_device_memory_size(ln.blas, kBlasWorkspace));
+        st->workspace_bytes += static_cast<int64_t>(kBlasWorkspace);
+        if (l == 1) GEFEN_HIP(hipStreamSynchronize(stream));   // allocations above
+        GEFEN_HIP(fill_zero(ln.x[0], 2 * static_cast<size_t>(lane_x[l]), ls));
+        for (int32_t gi : ln.groups) {
+            const auto& g = st->muon_groups[gi];
+            if (g.m > 1 && (rc = ns_iteration(ln, g, ln.x[0], ln.x[1], 1.0f, 1.0f, 1.0f)))
+                return rc;
+        }
+        GEFEN_HIP(hipStreamSynchronize(ls));
+    }
     GEFEN_HIP(hipStreamSynchronize(stream));
     st->muon_ready = true;
     return GEFEN_OK;
@@ -1618,7 +1678,7 @@ int gefen_muon_step(gefen_state* st, const gefen_tensor* params, const gefen_ten
     if (!finite_f(ns_eps) || ns_eps <= 0.0) return fail(GEFEN_EINVAL, "ns_eps must be finite and > 0");
     hipStream_t stream = as_stream(stream_);
     if ((rc = refresh_segs(st, params, grads, stream))) return rc;
-    GEFEN_BLAS(rocblas_set_stream(st->blas, stream));
+    GEFEN_BLAS(rocblas_set_stream(st->muon_lane[0].blas, stream));
     const bool prof = st->prof_armed && st->muon_prof_steps < st->prof_max_steps &&
                       !st->muon_prof_events.empty();
     hipEvent_t* ev = prof ? &st->muon_prof_events[st->muon_prof_steps * st->muon_prof_stride()]
@@ -1636,48 +1696,60 @@ int gefen_muon_step(gefen_state* st, const gefen_tensor* params, const gefen_ten
                                host_bf16_value(static_cast<float>(ns_eps)), st->muon_norm, stream));
     if (prof) GEFEN_HIP(hipEventRecord(ev[1], stream));
     const float decay = static_cast<float>(1.0 - lr * weight_decay);
-    for (size_t gi = 0; gi < st->muon_groups.size(); ++gi) {
-        const auto& g = st->muon_groups[gi];
+    // normalise, orthogonalise and update one shape group with a lane's resources
+    auto run_group = [&](gefen_state::MuonLane& ln, const gefen_state::MuonGroup& g,
+                         hipStream_t ls) -> int {
         const int64_t xs = g.m * g.ldx;   // elements per batch entry of X
         for (const auto& pt : g.parts) {
             const int32_t* tof = st->muon_tensor_of + g.first + pt.first;
-            uint16_t* xb = st->muon_x[0] + pt.first * xs;
+            uint16_t* xb = ln.x[0] + pt.first * xs;
             if (pt.transposed)
                 GEFEN_HIP(launch_muon_prep_t(st->muon_u, st->segs, tof, pt.count, st->muon_norm,
-                                             pt.rows, pt.cols, g.ldx, xb, stream));
+                                             pt.rows, pt.cols, g.ldx, xb, ls));
             else
                 GEFEN_HIP(launch_muon_prep(st->muon_u, st->segs, tof, pt.count, st->muon_norm,
-                                           pt.rows * pt.cols, xb, stream));
+                                           pt.rows * pt.cols, xb, ls));
         }
-        if (prof) GEFEN_HIP(hipEventRecord(ev[2 + 2 * gi], stream));
         int cur = 0;
         if (g.m == 1) {
-            GEFEN_HIP(launch_muon_ns_vec(st->muon_x[0], g.count, g.n, ns_steps,
+            GEFEN_HIP(launch_muon_ns_vec(ln.x[0], g.count, g.n, ns_steps,
                                          static_cast<float>(ns_a), static_cast<float>(ns_b),
-                                         static_cast<float>(ns_c), stream));
+                                         static_cast<float>(ns_c), ls));
         } else {
             for (int32_t it = 0; it < ns_steps; ++it) {
-                if ((rc = ns_iteration(st, g, st->muon_x[cur], st->muon_x[1 - cur],
-                                       static_cast<float>(ns_a), static_cast<float>(ns_b),
-                                       static_cast<float>(ns_c))))
-                    return rc;
+                const int r = ns_iteration(ln, g, ln.x[cur], ln.x[1 - cur],
+                                           static_cast<float>(ns_a), static_cast<float>(ns_b),
+                                           static_cast<float>(ns_c));
+                if (r) return r;
                 cur ^= 1;
             }
         }
-        if (prof) GEFEN_HIP(hipEventRecord(ev[3 + 2 * gi], stream));
         for (const auto& pt : g.parts) {
             const int32_t* tof = st->muon_tensor_of + g.first + pt.first;
-            const uint16_t* ob = st->muon_x[cur] + pt.first * xs;
+            const uint16_t* ob = ln.x[cur] + pt.first * xs;
             const double scale = std::sqrt(std::max(1.0, static_cast<double>(pt.rows) / pt.cols));
             const float step = static_cast<float>(lr * scale);
             if (pt.transposed)
                 GEFEN_HIP(launch_muon_update_t(ob, st->segs, tof, pt.count, pt.rows, pt.cols,
-                                               g.ldx, decay, step, stream));
+                                               g.ldx, decay, step, ls));
             else
                 GEFEN_HIP(launch_muon_update(ob, st->segs, tof, pt.count, pt.rows * pt.cols,
-                                             decay, step, stream));
+                                             decay, step, ls));
         }
+        return GEFEN_OK;
+    };
+    // lane 1 first (it starts as soon as the norms are done), then lane 0, then the join
+    gefen_state::MuonLane& l1 = st->muon_lane[1];
+    if (!l1.groups.empty()) {
+        GEFEN_HIP(hipEventRecord(st->muon_fork, stream));
+        GEFEN_HIP(hipStreamWaitEvent(st->muon_side, st->muon_fork, 0));
+        for (int32_t gi : l1.groups)
+            if ((rc = run_group(l1, st->muon_groups[gi], st->muon_side))) return rc;
+        GEFEN_HIP(hipEventRecord(st->muon_join, st->muon_side));
     }
+    for (int32_t gi : st->muon_lane[0].groups)
+        if ((rc = run_group(st->muon_lane[0], st->muon_groups[gi], stream))) return rc;
+    if (!l1.groups.empty()) GEFEN_HIP(hipStreamWaitEvent(stream, st->muon_join, 0));
     if (prof) {
         GEFEN_HIP(hipEventRecord(ev[st->muon_prof_stride() - 1], stream));
         ++st->muon_prof_steps;
@@ -1686,29 +1758,21 @@ int gefen_muon_step(gefen_state* st, const gefen_tensor* params, const gefen_ten
     return GEFEN_OK;
 }
 
-int gefen_muon_profile_end(gefen_state* st, int32_t* steps, double* codec_ms, double* ns_ms,
-                           double* rest_ms)
+int gefen_muon_profile_end(gefen_state* st, int32_t* steps, double* codec_ms, double* ortho_ms)
 {
-    if (!st || !steps || !codec_ms || !ns_ms || !rest_ms) return fail(GEFEN_EINVAL, "NULL argument");
+    if (!st || !steps || !codec_ms || !ortho_ms) return fail(GEFEN_EINVAL, "NULL argument");
     *steps = 0;
-    *codec_ms = *ns_ms = *rest_ms = 0.0;
+    *codec_ms = *ortho_ms = 0.0;
     const size_t k = st->muon_prof_stride();
     if (st->prof_armed && st->muon_prof_steps > 0) {
         GEFEN_HIP(hipEventSynchronize(st->muon_prof_events[st->muon_prof_steps * k - 1]));
         for (int32_t s = 0; s < st->muon_prof_steps; ++s) {
             hipEvent_t* ev = &st->muon_prof_events[s * k];
-            float a = 0.0f, total = 0.0f;
+            float a = 0.0f, o = 0.0f;
             GEFEN_HIP(hipEventElapsedTime(&a, ev[0], ev[1]));
-            GEFEN_HIP(hipEventElapsedTime(&total, ev[0], ev[k - 1]));
-            double ns = 0.0;
-            for (size_t gi = 0; gi < st->muon_groups.size(); ++gi) {
-                float b = 0.0f;
-                GEFEN_HIP(hipEventElapsedTime(&b, ev[2 + 2 * gi], ev[3 + 2 * gi]));
-                ns += b;
-            }
+            GEFEN_HIP(hipEventElapsedTime(&o, ev[1], ev[2]));
             *codec_ms += a;
-            *ns_ms += ns;
-            *rest_ms += total - a - ns;
+            *ortho_ms += o;
         }
         *steps = st->muon_prof_steps;
     }
