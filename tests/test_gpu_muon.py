@@ -178,6 +178,31 @@ def test_muon_gpt2_mlp_shape():
     print("worst O deviation (max, mean) / max|O|:", w)
 
 
+def test_muon_two_lanes_match_one_stream(monkeypatch):
+    """The shape groups split over two concurrent streams compute exactly what one
+    stream computes: every group's kernels and products are the same, only their order
+    across groups changes. Bitwise, over several steps, including the split-K Gram, the
+    vector kernel, tall and wide parts and groups on both lanes."""
+    dev = _dev()
+    shapes = [(5000, 48), (64, 128), (128, 64), (1, 77), (96, 96), (300, 1), (64, 128),
+              (768, 3072), (3072, 768)]
+    params = {}
+    for lanes in ("1", "2"):
+        monkeypatch.setenv("GEFEN_MUON_LANES", lanes)
+        torch.manual_seed(21)
+        ps = [torch.randn(r * c, device=dev) * 0.02 for r, c in shapes]
+        gs = [[_grad(r, c, 100 * t + i, torch.bfloat16, dev) for i, (r, c) in enumerate(shapes)]
+              for t in range(4)]
+        st = gf.GefenState(gs[0])
+        st.muon_init([r for r, _ in shapes])
+        for t in range(4):
+            st.muon_step(ps, gs[t], 0.02, 0.95, 0.01, True)
+        torch.cuda.synchronize()
+        params[lanes] = [p.clone() for p in ps]
+    for i, (a, b) in enumerate(zip(params["1"], params["2"])):
+        assert torch.equal(a, b), f"tensor {i} {shapes[i]}"
+
+
 def test_muon_lossless_block_size_one_matches_torch_muon():
     """Block size 1: the stored momentum is exact, so Gefen-Muon is Muon; free-running
     against torch.optim.Muon on the GPU (both bfloat16 Newton-Schulz)."""
