@@ -158,14 +158,93 @@ __global__ __launch_bounds__(kThreads) void k_muon_codec(const Tile* __restrict_
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
+
+    // Register path for a block of whole, aligned 4-element vectors: the workgroup
+    // (mode 0, up to 4 * kRegV * kThreads elements) or one wave (mode 2, up to
+    // 4 * kRegV * 64) holds it, every load issued before the tables are staged, so the
+    // gradient and the codes are read once. Other blocks take the two streaming passes.
+    constexpr int kRegV = 4;
+    const bool wg_mode = tl.vpl == 0;
+    const int bi = wg_mode ? 0 : wave;
+    const int ti = wg_mode ? tid : lane;      // index within the block's threads
+    const int bs = wg_mode ? kThreads : 64;   // threads per block
+    int64_t start = 0, len = 0;
+    bool reg = false;
+    if ((wg_mode || tl.vpl == 2) && bi < tl.nblk) {
+        block_range(sg, tl, bi, start, len);
+        reg = ((start | len) & 3) == 0 && len <= 4LL * kRegV * bs && vector_ok<GDT>(sg);
+    }
+    float g[kRegV][4];
+    uint32_t cq[kRegV];
+    const int64_t v0 = start >> 2;
+    const int nv = static_cast<int>(len >> 2);
+    if (reg) {
+#pragma unroll
+        for (int j = 0; j < kRegV; ++j) {
+            const int v = ti + j * bs;
+            cq[j] = 0;
+            g[j][0] = g[j][1] = g[j][2] = g[j][3] = 0.0f;
+            if (v < nv) {
+                load_grad4<GDT>(sg, v0 + v, g[j]);
+                cq[j] = code_ld4<CB>(codes, sg.code_off + 4 * (v0 + v));
+            }
+        }
+    }
     load_tables<kThreads>(L, cbd);
     __syncthreads();
     const float half_ng = 0.5f * static_cast<float>(cbd.ng);
     const int ng_m1 = cbd.ng - 1;
     float uss = 0.0f;
-    if (tl.vpl == 0) {
-        int64_t start, len;
-        block_range(sg, tl, 0, start, len);
+    if (reg) {   // uniform over the workgroup in mode 0, over the wave in mode 2
+        const int64_t blk = tl.blk0 + bi;
+        const float s_old = scale[blk];
+        // momentum (kept in g), u = nesterov ? mu m + (1 - mu) g : m as packed bfloat16
+        // (it does not depend on the new scale), and the block's max |m|
+        uint32_t up[kRegV][2];
+        float am = 0.0f;
+#pragma unroll
+        for (int j = 0; j < kRegV; ++j) {
+            const bool ok = ti + j * bs < nv;
+            uint32_t ub[4];
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const float mm = ok ? momentum(L, code_get<CB>(cq[j], c), s_old, g[j][c], sc)
+                                    : 0.0f;
+                const float uu = mo.nesterov ? fmaf(mo.mu, mm, mo.one_minus_mu * g[j][c]) : mm;
+                ub[c] = ok ? to_bf16(uu) : 0u;
+                const float ur = __uint_as_float(ub[c] << 16);
+                uss = fmaf(ur, ur, uss);
+                am = fmaxf(am, fabsf(mm));
+                g[j][c] = mm;
+            }
+            up[j][0] = ub[0] | (ub[1] << 16);
+            up[j][1] = ub[2] | (ub[3] << 16);
+        }
+        for (int off = 1; off < 64; off <<= 1) am = fmaxf(am, __shfl_xor(am, off));
+        if (wg_mode) {
+            if (lane == 0) L.red_am[wave] = am;
+            __syncthreads();
+            am = L.red_am[0];
+            for (int w = 1; w < kThreads / 64; ++w) am = fmaxf(am, L.red_am[w]);
+        }
+        if (ti == 0) scale[blk] = am;
+        const float inv_s = am > 0.0f ? 1.0f / am : 0.0f;
+#pragma unroll
+        for (int j = 0; j < kRegV; ++j) {
+            const int v = ti + j * bs;
+            if (v < nv) {
+                uint32_t packed = 0;
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const int q = am > 0.0f ? encode(L, g[j][c] * inv_s, half_ng, ng_m1) : 0;
+                    packed |= static_cast<uint32_t>(q) << (CB * c);
+                }
+                code_st4<CB>(codes, sg.code_off + 4 * (v0 + v), packed);
+                const u32x2 w = {up[j][0], up[j][1]};
+                *glw<u32x2>(mo.u + sg.code_off + 4 * (v0 + v)) = w;
+            }
+        }
+    } else if (wg_mode) {
         const float s_old = scale[tl.blk0];
         const Span sp = make_span<GDT>(sg, start, len);
         float am = muon_absmax_pass<GDT, kThreads, CB>(L, sg, codes, sp, s_old, sc, tid);
@@ -195,10 +274,8 @@ __global__ __launch_bounds__(kThreads) void k_muon_codec(const Tile* __restrict_
                 uss += muon_elem_out<CB>(L, codes, cj + i, load_grad(sg.grad, start + i, GDT),
                                          s_old, am, inv_s, sc, mo, half_ng, ng_m1);
         }
-    } else {
+    } else if (tl.vpl == 2) {
         if (wave < tl.nblk) {
-            int64_t start, len;
-            block_range(sg, tl, wave, start, len);
             const int64_t blk = tl.blk0 + wave;
             const float s_old = scale[blk];
             const Span sp = make_span<GDT>(sg, start, len);
