@@ -154,20 +154,25 @@ def test_gpt2_125m_full_coverage():
     _free()
 
 
-@pytest.mark.parametrize("name", ["gpt2_1b", "llama3_1p5b"])
-def test_large_shapes_sampled(name):
+@pytest.mark.parametrize("name,code_bits", [("gpt2_1b", 8), ("llama3_1p5b", 8),
+                                            ("llama3_1p5b", 4)])
+def test_large_shapes_sampled(name, code_bits):
+    """Whole-model steps at full size; the 4-bit case checks two codes per byte at the
+    Llama-3 shape (its periods are those of the 8-bit case, checked there)."""
     dev = _dev()
     w = W.get(name)
     fields = W.scale_fields(w)
     params = W.init_params(w, dev)
     g1 = W.make_grads(w, fields, 1, dev)
-    st = gf.GefenState(g1, eps_part=w.eps)
+    st = gf.GefenState(g1, eps_part=w.eps, code_bits=code_bits)
     periods = st.periods
-    n_layer = 12 if name == "gpt2_1b" else 9
-    first = list(range(2, 2 + n_layer)) if name == "gpt2_1b" else list(range(1, 1 + n_layer))
-    last = list(range(len(w.tensors) - 2 - n_layer, len(w.tensors) - 2))
-    norms = [i for i, t in enumerate(w.tensors) if t.kind in ("norm", "bias")]
-    _check_periods(w, g1, periods, sorted(set(first + last + norms)))
+    if code_bits == 8:
+        n_layer = 12 if name == "gpt2_1b" else 9
+        first = (list(range(2, 2 + n_layer)) if name == "gpt2_1b"
+                 else list(range(1, 1 + n_layer)))
+        last = list(range(len(w.tensors) - 2 - n_layer, len(w.tensors) - 2))
+        norms = [i for i, t in enumerate(w.tensors) if t.kind in ("norm", "bias")]
+        _check_periods(w, g1, periods, sorted(set(first + last + norms)))
     offsets = _uniform_offsets(params, periods)
     smp = Sampled(st, params, offsets, _sample_uniform(offsets, 0.002, seed=w.index))
     hp = (w.lr, w.betas, w.eps, w.wd)
@@ -175,7 +180,7 @@ def test_large_shapes_sampled(name):
     for t in (1, 2):
         if t > 1:
             g = W.make_grads(w, fields, t, dev)
-        rep = smp.step(g, *hp, t, where=f"{name} t={t}")
+        rep = smp.step(g, *hp, t, where=f"{name} cb{code_bits} t={t}")
         assert rep["codes"] > 1_000_000
     del st, params, g1, g, smp
     _free()
