@@ -10,7 +10,8 @@
   follows: a seeded random 1 % of blocks, every block under 128 elements, the first and
   last 100 blocks and the 100 largest; two steps, a codebook refit (histogram checked
   exactly, DP codebook bit-identical), and the step after the refit (decode with the
-  old codebook, encode with the new one).
+  old codebook, encode with the new one). The other reading of its block sizes
+  (log-uniform sizes drawn until 4e9 is covered) is checked the same way over two steps.
 
 Blocks are independent in the step, so a sample checks its blocks completely.
 """
@@ -233,5 +234,30 @@ def test_stress_4b_sampled_with_refit():
     rep = smp.step(g2, *hp, 3, where="stress t=3 (after refit)")
     assert rep["codes"] > 10_000_000
     np.testing.assert_array_equal(st.read(gf.STATE_CB_DEC64).cpu().numpy(), cb_ref)
+    del st, params, g2, smp
+    _free()
+
+
+def test_stress_sequential_variant_sampled():
+    """The other reading of the stress block sizes: log-uniform [64, 65536] drawn until
+    4e9 elements are covered (about 4.2e5 blocks, the largest at 65536, a short last
+    block). Two teacher-forced steps on the same kind of sample."""
+    dev = _dev()
+    w = W.get("stress_4b")
+    offs = W.stress_block_offsets(w.numel, variant="sequential")
+    nb = offs.size - 1
+    assert 400_000 < nb < 450_000 and np.diff(offs).max() <= 65536
+    bsc = W.stress_block_scales(nb)
+    params = W.init_params(w, dev)
+    g1 = W.make_grads(w, W.scale_fields(w), 1, dev, block_scales=bsc, offsets=offs)
+    st = gf.GefenState(g1, block_offsets=offs, eps_part=w.eps)
+    smp = Sampled(st, params, [offs], [_stress_sample(offs, seed=7)])
+    hp = (w.lr, w.betas, w.eps, w.wd)
+    smp.step(g1, *hp, 1, where="stress sequential t=1")
+    del g1
+    _free()
+    g2 = W.make_grads(w, W.scale_fields(w), 2, dev, block_scales=bsc, offsets=offs)
+    rep = smp.step(g2, *hp, 2, where="stress sequential t=2")
+    assert rep["codes"] > 10_000_000
     del st, params, g2, smp
     _free()
