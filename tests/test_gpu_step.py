@@ -351,3 +351,40 @@ def test_mixed_tensors_share_one_launch():
     st.step(params, gr(4), 1e-3, (0.9, 0.999), 1e-8, 0.1, 4)
     kinds = [c["kind"] for c in st.profile_end()]
     assert kinds.count("uniform_registers") == 1 and "split_block" in kinds, kinds
+
+
+DEGENERATE = [
+    # (lr, betas, eps, wd, first t): no momentum memory (m = g); no second-moment memory
+    # (v = mean g^2 of this step); a pure decay step (lr = 0 leaves theta unchanged and
+    # still updates codes, scales and v); eps = 0 with bias corrections at 1 (large t);
+    # strong decay and balanced betas
+    (1e-3, (0.0, 0.999), 1e-8, 0.1, 1),
+    (1e-3, (0.9, 0.0), 1e-8, 0.0, 1),
+    (0.0, (0.9, 0.999), 1e-8, 0.1, 1),
+    (1e-2, (0.99, 0.9999), 0.0, 0.0, 1_000_000),
+    (1e-3, (0.5, 0.5), 1e-3, 1.0, 1),
+]
+
+
+@pytest.mark.parametrize("lr,betas,eps,wd,t0", DEGENERATE)
+def test_degenerate_hyperparameters(lr, betas, eps, wd, t0):
+    """Edge settings of the step on every kernel class, one state per class so that
+    nothing is folded into the leftover launch: register blocks (p = 64 and 2048),
+    streamed (p = 33), lane per block (p = 5), split blocks (p = 70000), and the leftover
+    launch (small classes beside a register class)."""
+    from parity import Run
+    dev = _dev()
+    cases = [[(64, 300), (2048, 12)], [(33, 200)], [(5, 400)], [(70000, 2)],
+             [(2048, 40), (33, 20), (5, 30)]]
+    for ci, specs in enumerate(cases):
+        params = [torch.randn(p * nb, device=dev) * 0.02 for p, nb in specs]
+        gr = lambda t: [_grad(p * nb, 1000 * ci + 50 * i + t, torch.bfloat16, rows=nb, dev=dev)
+                        for i, (p, nb) in enumerate(specs)]
+        run = Run(params, gr(0), period_override=[p for p, _ in specs])
+        before = [p.clone() for p in params]
+        for t in range(t0, t0 + 3):
+            run.teacher_forced_step(gr(t), lr, betas, eps, wd, t,
+                                    where=f"case {ci} lr={lr} b={betas} t={t}")
+        if lr == 0.0:
+            for a, b in zip(params, before):
+                assert torch.equal(a, b)
