@@ -108,15 +108,18 @@ def cpu_baseline(w, params, grads, st, sample_elems: int):
 
 
 def adamw_comparator(torch, w, params, grads, steps: int, gefen_state_bytes: int,
-                     gefen_ms: float):
+                     gefen_peak_bytes: int, gefen_ms: float):
     """torch.optim.AdamW (fused) on the same parameters and gradients: step time, state
-    bytes and algorithmic bytes per element (parameter read + write 8, fp32 gradient 4,
-    m and v read + write 16). Fused AdamW takes gradients in the parameter dtype, so
-    bf16 gradients are widened to fp32 once, outside the timed loop."""
+    bytes (after the first step), peak bytes above parameters and gradients over its
+    steps, and algorithmic bytes per element (parameter read + write 8, fp32 gradient
+    4, m and v read + write 16). Fused AdamW takes gradients in the parameter dtype, so
+    bf16 gradients are widened to fp32 once, outside the timed loop. Gefen's peak is
+    its persistent state plus its workspace: the library allocates nothing in a step."""
     ps = [torch.nn.Parameter(p.detach().clone()) for p in params]
     g32 = [[g.float() for g in gs] for gs in grads]
     torch.cuda.synchronize()
     base = torch.cuda.memory_allocated()
+    torch.cuda.reset_peak_memory_stats()
     opt = torch.optim.AdamW(ps, lr=w.lr, betas=w.betas, eps=w.eps, weight_decay=w.wd,
                             fused=True)
     for p, g in zip(ps, g32[0]):
@@ -133,15 +136,17 @@ def adamw_comparator(torch, w, params, grads, steps: int, gefen_state_bytes: int
         opt.step()
     e1.record()
     torch.cuda.synchronize()
+    peak_bytes = torch.cuda.max_memory_allocated() - base
     ms = e0.elapsed_time(e1) / steps
     n = w.numel
     bytes_step = 28 * n
     out = {"optimizer": "torch.optim.AdamW(fused=True)", "ms_per_step": round(ms, 4),
            "gparams_per_s": round(n / (ms * 1e-3) / 1e9, 3),
            "hbm_gbps": round(bytes_step / (ms * 1e-3) / 1e9, 1),
-           "bytes_per_elem": 28, "state_bytes": state_bytes,
-           "gefen_state_bytes": gefen_state_bytes,
+           "bytes_per_elem": 28, "state_bytes": state_bytes, "peak_bytes": peak_bytes,
+           "gefen_state_bytes": gefen_state_bytes, "gefen_peak_bytes": gefen_peak_bytes,
            "state_ratio": round(state_bytes / gefen_state_bytes, 3),
+           "peak_ratio": round(peak_bytes / gefen_peak_bytes, 3),
            "gefen_speedup": round(ms / gefen_ms, 3)}
     del opt, ps, g32
     torch.cuda.empty_cache()
@@ -467,7 +472,7 @@ def main():
     }
     if not args.no_adamw and not w.n_blocks:
         line["adamw"] = adamw_comparator(torch, w, params, grads, min(args.steps, 20),
-                                         persistent, ms_per_step)
+                                         persistent, persistent + workspace, ms_per_step)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, params, grads[t % 2], st, args.cpu_sample_elems)
     print(json.dumps(line), flush=True)
