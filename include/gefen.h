@@ -26,6 +26,17 @@
  *  - The state and every device buffer inside it are owned by the library: allocated
  *    by gefen_init, freed by gefen_destroy. gefen_step allocates nothing.
  *  - Calls on one state must be ordered (same stream, or externally synchronised).
+ *
+ * Environment variables (measurement and debugging only; defaults are the tuned
+ * choices):
+ *  GEFEN_U_THREADS   256, 512 or 1024: preferred workgroup size of the register-resident
+ *                    step kernel (read by gefen_init; default 1024).
+ *  GEFEN_U_VPL       1-8: force that kernel's vectors per lane (default 0: chosen).
+ *  GEFEN_FOLD        0: keep every small kernel class as its own launch instead of one
+ *                    leftover launch (default 1).
+ *  GEFEN_MUON_LANES  1: run every Gefen-Muon shape group on the caller's stream instead
+ *                    of two concurrent lanes (read by gefen_muon_init; default 2).
+ *  GEFEN_DEBUG_SYNC  set: gefen_step synchronises its stream and reports kernel errors.
  */
 #ifndef GEFEN_H
 #define GEFEN_H
