@@ -1630,9 +1630,8 @@ int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, voi
     GEFEN_HIP(hipMemcpy(st->muon_tile_range, tile_range.data(), 8 * tile_range.size(), hipMemcpyHostToDevice));
     GEFEN_HIP(hipMemcpy(st->muon_tensor_of, order.data(), 4 * order.size(), hipMemcpyHostToDevice));
 
-    // One rocBLAS handle per lane with a fixed workspace, set before any product runs,
-    // so that steps allocate nothing; a product that would need more returns an error
-    // status. One Newton-Schulz iteration per group on zeroed matrices loads and checks
+    // One rocBLAS handle per lane with a fixed workspace that the state owns, handed to
+    // rocBLAS before any product runs, so that steps allocate nothing. One Newton-Schulz iteration per group on zeroed matrices loads and checks
     // every GEMM the steps use, on the lane's own stream.
     if (!st->muon_lane[1].groups.empty()) {
         GEFEN_HIP(hipStreamCreateWithFlags(&st->muon_side, hipStreamNonBlocking));
@@ -1643,10 +1642,11 @@ int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, voi
         gefen_state::MuonLane& ln = st->muon_lane[l];
         if (ln.groups.empty()) continue;
         hipStream_t ls = l == 0 ? stream : st->muon_side;
+        void* ws = nullptr;
+        if ((rc = st->alloc(&ws, kBlasWorkspace, false))) return rc;
         GEFEN_BLAS(rocblas_create_handle(&ln.blas));
         GEFEN_BLAS(rocblas_set_stream(ln.blas, ls));
-        GEFEN_BLAS(rocblas_set_device_memory_size(ln.blas, kBlasWorkspace));
-        st->workspace_bytes += static_cast<int64_t>(kBlasWorkspace);
+        GEFEN_BLAS(rocblas_set_workspace(ln.blas, ws, kBlasWorkspace));
         if (l == 1) GEFEN_HIP(hipStreamSynchronize(stream));   // allocations above
         GEFEN_HIP(fill_zero(ln.x[0], 2 * static_cast<size_t>(lane_x[l]), ls));
         for (int32_t gi : ln.groups) {
