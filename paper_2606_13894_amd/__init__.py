@@ -409,3 +409,40 @@ class Gefen:
         self.t += 1
         self.state.step(self.params, grads, self.lr, self.betas, self.eps, self.weight_decay,
                         self.t)
+
+
+class GefenMuon:
+    """``torch.optim.Muon``-style front end for Gefen-Muon (appendix "Gefen-Muon"):
+    ``GefenMuon(params, lr, weight_decay, momentum, nesterov, ns_coefficients, eps,
+    ns_steps)`` with Muon's defaults. Parameter i is the matrix shape[0] x (numel /
+    shape[0]) (a 1-D parameter is 1 x numel). The first ``step()`` infers the blocks and
+    fits the codebook from the current gradients (Alg. 1), then steps with them.
+    Parameters must be fp32 device tensors; gradients fp32 or bf16.
+    """
+
+    def __init__(self, params, lr: float = 1e-3, weight_decay: float = 0.1,
+                 momentum: float = 0.95, nesterov: bool = True,
+                 ns_coefficients=MUON_NS_COEFFS, eps: float = 1e-7, ns_steps: int = 5,
+                 code_bits: int = 8, eps_part: float = 1e-8):
+        self.params = [p for p in params]
+        self.lr, self.weight_decay, self.momentum = lr, weight_decay, momentum
+        self.nesterov, self.ns_coefficients = nesterov, tuple(ns_coefficients)
+        self.eps, self.ns_steps = eps, ns_steps
+        self.code_bits, self.eps_part = code_bits, eps_part
+        self.state: Optional[GefenState] = None
+
+    def zero_grad(self, set_to_none: bool = True):
+        for p in self.params:
+            if p.grad is not None:
+                if set_to_none:
+                    p.grad = None
+                else:
+                    p.grad.zero_()
+
+    def step(self):
+        grads = [p.grad.contiguous() for p in self.params]
+        if self.state is None:
+            self.state = GefenState(grads, code_bits=self.code_bits, eps_part=self.eps_part)
+            self.state.muon_init([p.shape[0] if p.dim() >= 2 else 1 for p in self.params])
+        self.state.muon_step(self.params, grads, self.lr, self.momentum, self.weight_decay,
+                             self.nesterov, self.ns_steps, self.ns_coefficients, self.eps)

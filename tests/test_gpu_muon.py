@@ -283,3 +283,27 @@ def test_muon_refuses_groups_over_the_limit():
     st = gf.GefenState(gs, period_override=[8192] * 3)
     with pytest.raises(gf.GefenError, match="per group"):
         st.muon_init([8192] * 3)
+
+
+def test_gefen_muon_front_end_matches_the_state_calls():
+    """The optimizer-style front end makes exactly the calls of the state API: init from
+    the first gradients, muon_init with each parameter's rows, then muon_step."""
+    dev = _dev()
+    shapes = [(64, 96), (96, 64), (77,)]
+    torch.manual_seed(4)
+    p0 = [torch.randn(*s, device=dev) * 0.02 for s in shapes]
+    gs = [[torch.randn(*s, device=dev) for s in shapes] for _ in range(3)]
+    ps = [torch.nn.Parameter(p.clone()) for p in p0]
+    opt = gf.GefenMuon(ps, lr=0.02, weight_decay=0.01)
+    for g in gs:
+        for p, gi in zip(ps, g):
+            p.grad = gi
+        opt.step()
+    ref = [p.clone().reshape(-1) for p in p0]
+    st = gf.GefenState([g.reshape(-1) for g in gs[0]])
+    st.muon_init([s[0] if len(s) == 2 else 1 for s in shapes])
+    for g in gs:
+        st.muon_step(ref, [gi.reshape(-1) for gi in g], 0.02, 0.95, 0.01, True)
+    torch.cuda.synchronize()
+    for a, b in zip(ps, ref):
+        assert torch.equal(a.detach().reshape(-1), b)
