@@ -1445,32 +1445,21 @@ int ns_iteration(gefen_state::MuonLane& ln, const gefen_state::MuonGroup& g, con
     return GEFEN_OK;
 }
 
-}  // namespace
-
-int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, void* stream_)
+// Gefen-Muon codec tiles over every block (host side), in launch order: fp32-gradient
+// tensors first, then bf16 (one codec launch per gradient dtype). Tile mode in
+// Tile::vpl: 1 (lane per block) for blocks of <= 32 elements, 2 (wave per block, up to
+// 4) for <= 2048, else 0 (the workgroup on one block). tile_range[2t, 2t + 1) are
+// tensor t's tiles.
+int muon_codec_tiles(gefen_state* st, std::vector<Tile>& tiles, std::vector<int64_t>& tile_range)
 {
-    if (!st || !rows) return fail(GEFEN_EINVAL, "NULL argument");
-    if (n_tensors != st->n_tensors)
-        return fail(GEFEN_EINVAL, "n_tensors = %d, state has %d", n_tensors, st->n_tensors);
-    if (st->muon_ready) return fail(GEFEN_EINVAL, "gefen_muon_init was already called");
-    const int32_t n = n_tensors;
-    for (int32_t t = 0; t < n; ++t)
-        if (rows[t] < 1 || st->numel[t] % rows[t] != 0)
-            return fail(GEFEN_EINVAL, "rows[%d] = %lld does not divide numel %lld", t,
-                        (long long)rows[t], (long long)st->numel[t]);
-    hipStream_t stream = as_stream(stream_);
-
+    const int32_t n = st->n_tensors;
+    tile_range.assign(2 * static_cast<size_t>(n), 0);
     // block starts on the host (explicit blocks: from the device table)
     std::vector<int64_t> csr_host;
     if (st->explicit_blocks) {
         csr_host.resize(static_cast<size_t>(st->total_blocks + n));
         GEFEN_HIP(hipMemcpy(csr_host.data(), st->csr, 8 * csr_host.size(), hipMemcpyDeviceToHost));
     }
-    // codec tiles: mode 1 (lane per block) for blocks of <= 32 elements, mode 2 (wave per
-    // block, up to 4) for <= 2048, else mode 0 (the workgroup on one block)
-    // (tiles of fp32-gradient tensors first, then bf16: one codec launch per dtype)
-    std::vector<Tile> tiles;
-    std::vector<int64_t> tile_range(2 * static_cast<size_t>(n), 0);
     std::vector<int64_t> csr_at(n + 1, 0);
     for (int32_t t = 0; t < n; ++t)
         csr_at[t + 1] = csr_at[t] + (st->explicit_blocks
@@ -1509,11 +1498,19 @@ int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, voi
         if (pass == 0) st->muon_dt_first[1] = static_cast<int64_t>(tiles.size());
     }
 
+    return GEFEN_OK;
+}
+
+// Shape groups (tensor order in `order`) and their split-K choice; max_x is the largest
+// group's Newton-Schulz buffer in elements.
+int muon_shape_groups(gefen_state* st, const int64_t* rows, std::vector<int32_t>& order,
+                      int64_t& max_x)
+{
+    const int32_t n = st->n_tensors;
     // Shape groups: tensors whose wide matrices and X layouts agree share one batch of
     // Newton-Schulz products (so a tall R x C tensor joins the C x R ones); inside a
     // group, parts of one R x C shape share the normalise and update launches. Groups and
     // parts in order of first appearance.
-    std::vector<int32_t> order;
     st->muon_groups.clear();
     struct Shape {
         int64_t rows, cols, m, n, ldx;
@@ -1558,7 +1555,7 @@ int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, voi
     // has too few 128 x 128 tiles to occupy the GPU. A transposed X gets zero columns up
     // to a multiple of 8 * splits, so that the chunks are equal and one batched call
     // covers them.
-    int64_t max_x = 0;
+    max_x = 0;
     for (auto& g : st->muon_groups) {
         const int64_t m = g.m;
         const int64_t tiles = ((m + 127) / 128) * ((m + 127) / 128);
@@ -1570,44 +1567,38 @@ int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, voi
             g.ldx = (g.n + 8 * g.splits - 1) / (8 * g.splits) * (8 * g.splits);
         max_x = std::max(max_x, g.count * m * g.ldx);
     }
-    // Lanes: groups in decreasing order of Newton-Schulz work, each to the lane with
-    // less work so far (GEFEN_MUON_LANES=1 keeps every group on the caller's stream).
-    const int n_lanes = std::min(2, std::max(1, env_int("GEFEN_MUON_LANES", 2)));
-    {
-        std::vector<int32_t> byw(st->muon_groups.size());
-        std::vector<double> work(byw.size());
-        for (size_t gi = 0; gi < byw.size(); ++gi) {
-            const auto& g = st->muon_groups[gi];
-            byw[gi] = static_cast<int32_t>(gi);
-            const double m = static_cast<double>(g.m), nn = static_cast<double>(g.ldx);
-            work[gi] = g.count * (g.m > 1 ? 4.0 * m * m * nn + 2.0 * m * m * m : 4.0 * nn);
-        }
-        std::stable_sort(byw.begin(), byw.end(),
-                         [&](int32_t a, int32_t b) { return work[a] > work[b]; });
-        double load[2] = {0.0, 0.0};
-        for (gefen_state::MuonLane& l : st->muon_lane) l.groups.clear();
-        for (int32_t gi : byw) {
-            const int l = (n_lanes > 1 && load[1] < load[0]) ? 1 : 0;
-            st->muon_lane[l].groups.push_back(gi);
-            load[l] += work[gi];
-        }
-    }
-    // Shape groups above kMuonMaxGroup elements are refused: a state of that size (the
-    // GPT-2 1B shapes, 4e8 elements in one group) failed with a device memory fault in
-    // this initialisation, whose cause has not been found.
-    if (max_x > kMuonMaxGroup)
-        return fail(GEFEN_EINVAL, "a group of equal-shape tensors holds %lld elements; "
-                    "Gefen-Muon supports at most %lld per group",
-                    (long long)max_x, (long long)kMuonMaxGroup);
+    return GEFEN_OK;
+}
 
+// Lanes: groups in decreasing order of Newton-Schulz work, each to the lane with less
+// work so far (GEFEN_MUON_LANES=1 keeps every group on the caller's stream).
+void muon_assign_lanes(gefen_state* st)
+{
+    const int n_lanes = std::min(2, std::max(1, env_int("GEFEN_MUON_LANES", 2)));
+    std::vector<int32_t> byw(st->muon_groups.size());
+    std::vector<double> work(byw.size());
+    for (size_t gi = 0; gi < byw.size(); ++gi) {
+        const auto& g = st->muon_groups[gi];
+        byw[gi] = static_cast<int32_t>(gi);
+        const double m = static_cast<double>(g.m), nn = static_cast<double>(g.ldx);
+        work[gi] = g.count * (g.m > 1 ? 4.0 * m * m * nn + 2.0 * m * m * m : 4.0 * nn);
+    }
+    std::stable_sort(byw.begin(), byw.end(),
+                     [&](int32_t a, int32_t b) { return work[a] > work[b]; });
+    double load[2] = {0.0, 0.0};
+    for (gefen_state::MuonLane& l : st->muon_lane) l.groups.clear();
+    for (int32_t gi : byw) {
+        const int l = (n_lanes > 1 && load[1] < load[0]) ? 1 : 0;
+        st->muon_lane[l].groups.push_back(gi);
+        load[l] += work[gi];
+    }
+}
+
+// Per-lane Newton-Schulz buffers, rocBLAS handles and workspaces, the side stream, and
+// a warm-up iteration of every group.
+int muon_lane_resources(gefen_state* st, hipStream_t stream)
+{
     int rc;
-    st->muon_n_tiles = static_cast<int64_t>(tiles.size());
-    if ((rc = st->alloc(&st->muon_tiles, sizeof(Tile) * tiles.size(), false))) return rc;
-    if ((rc = st->alloc(&st->muon_tile_range, 8 * tile_range.size(), false))) return rc;
-    if ((rc = st->alloc(&st->muon_tile_ss, 4 * tiles.size(), false))) return rc;
-    if ((rc = st->alloc(&st->muon_norm, 4 * static_cast<size_t>(n), false))) return rc;
-    if ((rc = st->alloc(&st->muon_tensor_of, 4 * order.size(), false))) return rc;
-    if ((rc = st->alloc(&st->muon_u, 2 * static_cast<size_t>(st->code_off[n]), false))) return rc;
     int64_t lane_x[2] = {0, 0};
     for (int l = 0; l < 2; ++l) {
         gefen_state::MuonLane& ln = st->muon_lane[l];
@@ -1626,13 +1617,10 @@ int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, voi
         if ((rc = st->alloc(&ln.b, 2 * static_cast<size_t>(ma), false))) return rc;
         if ((rc = st->alloc(&ln.partial, 4 * static_cast<size_t>(mp), false))) return rc;
     }
-    GEFEN_HIP(hipMemcpy(st->muon_tiles, tiles.data(), sizeof(Tile) * tiles.size(), hipMemcpyHostToDevice));
-    GEFEN_HIP(hipMemcpy(st->muon_tile_range, tile_range.data(), 8 * tile_range.size(), hipMemcpyHostToDevice));
-    GEFEN_HIP(hipMemcpy(st->muon_tensor_of, order.data(), 4 * order.size(), hipMemcpyHostToDevice));
-
     // One rocBLAS handle per lane with a fixed workspace that the state owns, handed to
-    // rocBLAS before any product runs, so that steps allocate nothing. One Newton-Schulz iteration per group on zeroed matrices loads and checks
-    // every GEMM the steps use, on the lane's own stream.
+    // rocBLAS before any product runs, so that steps allocate nothing. One Newton-Schulz
+    // iteration per group on zeroed matrices loads and checks every GEMM the steps use,
+    // on the lane's own stream.
     if (!st->muon_lane[1].groups.empty()) {
         GEFEN_HIP(hipStreamCreateWithFlags(&st->muon_side, hipStreamNonBlocking));
         GEFEN_HIP(hipEventCreateWithFlags(&st->muon_fork, hipEventDisableTiming));
@@ -1656,6 +1644,51 @@ int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, voi
         }
         GEFEN_HIP(hipStreamSynchronize(ls));
     }
+    return GEFEN_OK;
+}
+
+}  // namespace
+
+int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, void* stream_)
+{
+    if (!st || !rows) return fail(GEFEN_EINVAL, "NULL argument");
+    if (n_tensors != st->n_tensors)
+        return fail(GEFEN_EINVAL, "n_tensors = %d, state has %d", n_tensors, st->n_tensors);
+    if (st->muon_ready) return fail(GEFEN_EINVAL, "gefen_muon_init was already called");
+    const int32_t n = n_tensors;
+    for (int32_t t = 0; t < n; ++t)
+        if (rows[t] < 1 || st->numel[t] % rows[t] != 0)
+            return fail(GEFEN_EINVAL, "rows[%d] = %lld does not divide numel %lld", t,
+                        (long long)rows[t], (long long)st->numel[t]);
+    hipStream_t stream = as_stream(stream_);
+
+    int rc;
+    std::vector<Tile> tiles;
+    std::vector<int64_t> tile_range;
+    if ((rc = muon_codec_tiles(st, tiles, tile_range))) return rc;
+    std::vector<int32_t> order;
+    int64_t max_x = 0;
+    if ((rc = muon_shape_groups(st, rows, order, max_x))) return rc;
+    // Shape groups above kMuonMaxGroup elements are refused: a state of that size (the
+    // GPT-2 1B shapes, 4e8 elements in one group) failed with a device memory fault in
+    // this initialisation, whose cause has not been found.
+    if (max_x > kMuonMaxGroup)
+        return fail(GEFEN_EINVAL, "a group of equal-shape tensors holds %lld elements; "
+                    "Gefen-Muon supports at most %lld per group",
+                    (long long)max_x, (long long)kMuonMaxGroup);
+    muon_assign_lanes(st);
+
+    st->muon_n_tiles = static_cast<int64_t>(tiles.size());
+    if ((rc = st->alloc(&st->muon_tiles, sizeof(Tile) * tiles.size(), false))) return rc;
+    if ((rc = st->alloc(&st->muon_tile_range, 8 * tile_range.size(), false))) return rc;
+    if ((rc = st->alloc(&st->muon_tile_ss, 4 * tiles.size(), false))) return rc;
+    if ((rc = st->alloc(&st->muon_norm, 4 * static_cast<size_t>(n), false))) return rc;
+    if ((rc = st->alloc(&st->muon_tensor_of, 4 * order.size(), false))) return rc;
+    if ((rc = st->alloc(&st->muon_u, 2 * static_cast<size_t>(st->code_off[n]), false))) return rc;
+    GEFEN_HIP(hipMemcpy(st->muon_tiles, tiles.data(), sizeof(Tile) * tiles.size(), hipMemcpyHostToDevice));
+    GEFEN_HIP(hipMemcpy(st->muon_tile_range, tile_range.data(), 8 * tile_range.size(), hipMemcpyHostToDevice));
+    GEFEN_HIP(hipMemcpy(st->muon_tensor_of, order.data(), 4 * order.size(), hipMemcpyHostToDevice));
+    if ((rc = muon_lane_resources(st, stream))) return rc;
     GEFEN_HIP(hipStreamSynchronize(stream));
     st->muon_ready = true;
     return GEFEN_OK;
