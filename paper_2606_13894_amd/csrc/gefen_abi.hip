@@ -379,285 +379,298 @@ UShape choose_u(int64_t p)
     return UShape{8, kMaxVpl, 256};
 }
 
-// Tensor-relative block starts of tensor i (explicit blocks), size n_blocks_i + 1.
-int plan_tiles(gefen_state* st, const std::vector<std::vector<int64_t>>& starts)
-{
+// Tiles per kernel class while planning: one list per class key, with the split-block
+// bookkeeping and the kind of every tile (the histogram's view of it) kept parallel.
+struct TilePlan {
     struct Key {
         int32_t kind, gdtype, vpl, bs;
     };
-    std::vector<std::vector<Tile>> lists;
     std::vector<Key> keys;
-    auto list_for = [&](int32_t kind, int32_t gdt, int32_t vpl,
-                        int32_t bs = kThreads) -> std::vector<Tile>& {
+    std::vector<std::vector<Tile>> lists;
+    std::vector<std::vector<HTile>> hlists;
+    std::vector<std::vector<int32_t>> kinds;
+
+    size_t index(int32_t kind, int32_t gdt, int32_t vpl, int32_t bs = kThreads)
+    {
         for (size_t i = 0; i < keys.size(); ++i)
             if (keys[i].kind == kind && keys[i].gdtype == gdt && keys[i].vpl == vpl &&
                 keys[i].bs == bs)
-                return lists[i];
+                return i;
         keys.push_back({kind, gdt, vpl, bs});
         lists.emplace_back();
-        return lists.back();
-    };
-    // huge blocks: chunk tiles, bookkeeping completed once tiles are concatenated
-    std::vector<std::vector<HTile>> hlists;   // parallel to lists
-    auto add_huge = [&](int32_t t, int32_t gdt, int64_t start, int64_t len, int64_t blk) {
-        std::vector<Tile>& L = list_for(KIND_H, gdt, 0);
-        hlists.resize(lists.size());
-        size_t li = 0;
-        while (&lists[li] != &L) ++li;
-        std::vector<HTile>& H = hlists[li];
-        const int64_t nchunk = (len + kHChunk - 1) / kHChunk;
-        const int64_t first_rel = static_cast<int64_t>(L.size());
-        for (int64_t c = 0; c < nchunk; ++c) {
-            Tile tl{};
-            tl.elem0 = start + c * kHChunk;
-            tl.blk0 = blk;
-            tl.nelem = std::min(kHChunk, len - c * kHChunk);
-            tl.seg = t;
-            tl.nblk = 1;
-            L.push_back(tl);
-            HTile ht{};
-            ht.blk_len = len;
-            ht.first = first_rel;   // made absolute below
-            ht.nchunk = static_cast<int32_t>(nchunk);
-            ht.chunk = static_cast<int32_t>(c);
-            ht.hb = static_cast<int32_t>(st->n_hblocks);
-            H.push_back(ht);
-        }
-        ++st->n_hblocks;
-    };
-    st->n_hblocks = 0;
-    // Register-resident shapes: each eligible tensor's own best shape, then every tensor
-    // that fits the dominant shape's kernel (its vectors per lane and workgroup size; the
-    // kernel masks vectors past a block's end and reads lanes-per-block from the tile)
-    // is re-planned onto it, so one launch covers them on the fast path.
+        hlists.emplace_back();
+        kinds.emplace_back();
+        return keys.size() - 1;
+    }
+    void add(size_t i, const Tile& tl)
+    {
+        lists[i].push_back(tl);
+        kinds[i].push_back(keys[i].kind);
+    }
+    int64_t elems(size_t i) const
+    {
+        int64_t e = 0;
+        for (const Tile& tl : lists[i]) e += tl.nelem;
+        return e;
+    }
+};
+
+// Register-resident shapes: each eligible tensor's own best shape, then every tensor
+// that fits the dominant shape's kernel (its vectors per lane and workgroup size; the
+// kernel masks vectors past a block's end and reads lanes-per-block from the tile) is
+// re-planned onto it, so one launch covers them on the fast path. lpb_log2 < 0: not
+// register-resident.
+std::vector<UShape> plan_u_shapes(const gefen_state* st)
+{
     std::vector<UShape> ushape(st->n_tensors, UShape{-1, 0, 0});
-    {
-        std::vector<std::pair<std::pair<int, int>, int64_t>> tally;
-        for (int32_t t = 0; t < st->n_tensors; ++t) {
-            const int64_t p = st->period[t];
-            if (st->explicit_blocks || p % 4 != 0 || p > kUMaxPeriod) continue;
-            ushape[t] = choose_u(p);
-            const std::pair<int, int> key{ushape[t].vpl, ushape[t].bs};
-            bool found = false;
-            for (auto& e : tally)
-                if (e.first == key) {
-                    e.second += st->numel[t];
-                    found = true;
-                }
-            if (!found) tally.push_back({key, st->numel[t]});
-        }
-        int dom_vpl = 0, dom_bs = 0;
-        int64_t best = -1;
-        for (auto& e : tally)
-            if (e.second > best) {
-                best = e.second;
-                dom_vpl = e.first.first;
-                dom_bs = e.first.second;
-            }
-        if (best >= 0 && env_int("GEFEN_FOLD", 1)) {
-            for (int32_t t = 0; t < st->n_tensors; ++t) {
-                if (ushape[t].lpb_log2 < 0) continue;
-                if (ushape[t].vpl == dom_vpl && ushape[t].bs == dom_bs) continue;
-                const int64_t nv = st->period[t] / 4;
-                const int64_t need = (nv + dom_vpl - 1) / dom_vpl;
-                int l2 = 0;
-                while ((int64_t(1) << l2) < need) ++l2;
-                if ((1 << l2) <= dom_bs) ushape[t] = UShape{l2, dom_vpl, dom_bs};
-            }
-        }
-    }
+    std::vector<std::pair<std::pair<int, int>, int64_t>> tally;
     for (int32_t t = 0; t < st->n_tensors; ++t) {
-        const int32_t gdt = st->gdtype[t];
-        const int64_t bb = st->blk_begin[t];
-        if (st->explicit_blocks) {
-            const std::vector<int64_t>& s = starts[t];
-            const int64_t nb = static_cast<int64_t>(s.size()) - 1;
-            int64_t b = 0;
-            while (b < nb) {
-                const int64_t len = s[b + 1] - s[b];
-                if (len > kHugeBlock) {
-                    add_huge(t, gdt, s[b], len, bb + b);
-                    ++b;
-                } else if (len <= kSmallBlock) {
-                    Tile tl{};
-                    tl.elem0 = s[b];
-                    tl.blk0 = bb + b;
-                    tl.seg = t;
-                    int n = 0;
-                    while (b < nb && n < kThreads && s[b + 1] - s[b] <= kSmallBlock) {
-                        ++n;
-                        ++b;
-                    }
-                    tl.nblk = static_cast<int16_t>(n);
-                    tl.nelem = s[b] - tl.elem0;
-                    list_for(KIND_L, gdt, 0).push_back(tl);
-                } else {
-                    Tile tl{};
-                    tl.elem0 = s[b];
-                    tl.blk0 = bb + b;
-                    tl.nelem = len;
-                    tl.seg = t;
-                    tl.nblk = 1;
-                    list_for(KIND_G, gdt, 0).push_back(tl);
-                    ++b;
-                }
-            }
-            continue;
-        }
         const int64_t p = st->period[t];
-        const int64_t nb = st->numel[t] / p;
-        if (ushape[t].lpb_log2 >= 0) {
-            const UShape u = ushape[t];
-            const int l2 = u.lpb_log2, vpl = u.vpl, bs = u.bs;
-            const int64_t bpw = bs >> l2;
-            std::vector<Tile>& L = list_for(KIND_U, gdt, vpl, bs);
-            for (int64_t b = 0; b < nb; b += bpw) {
-                Tile tl{};
-                const int64_t n = std::min(bpw, nb - b);
-                tl.elem0 = b * p;
-                tl.blk0 = bb + b;
-                tl.nelem = n * p;
-                tl.seg = t;
-                tl.nblk = static_cast<int16_t>(n);
-                tl.vpl = static_cast<uint8_t>(vpl);
-                tl.lpb_log2 = static_cast<uint8_t>(l2);
-                L.push_back(tl);
+        if (st->explicit_blocks || p % 4 != 0 || p > kUMaxPeriod) continue;
+        ushape[t] = choose_u(p);
+        const std::pair<int, int> key{ushape[t].vpl, ushape[t].bs};
+        bool found = false;
+        for (auto& e : tally)
+            if (e.first == key) {
+                e.second += st->numel[t];
+                found = true;
             }
-        } else if (p <= kSmallBlock) {
-            std::vector<Tile>& L = list_for(KIND_L, gdt, 0);
-            for (int64_t b = 0; b < nb; b += kThreads) {
-                Tile tl{};
-                const int64_t n = std::min<int64_t>(kThreads, nb - b);
-                tl.elem0 = b * p;
-                tl.blk0 = bb + b;
-                tl.nelem = n * p;
-                tl.seg = t;
-                tl.nblk = static_cast<int16_t>(n);
-                L.push_back(tl);
-            }
-        } else if (p > kHugeBlock || (p > kUMaxPeriod && nb < kMinStreamedBlocks)) {
-            for (int64_t b = 0; b < nb; ++b) add_huge(t, gdt, b * p, p, bb + b);
-        } else {
-            std::vector<Tile>& L = list_for(KIND_G, gdt, 0);
-            for (int64_t b = 0; b < nb; ++b) {
-                Tile tl{};
-                tl.elem0 = b * p;
-                tl.blk0 = bb + b;
-                tl.nelem = p;
-                tl.seg = t;
-                tl.nblk = 1;
-                L.push_back(tl);
-            }
+        if (!found) tally.push_back({key, st->numel[t]});
+    }
+    int dom_vpl = 0, dom_bs = 0;
+    int64_t best = -1;
+    for (auto& e : tally)
+        if (e.second > best) {
+            best = e.second;
+            dom_vpl = e.first.first;
+            dom_bs = e.first.second;
+        }
+    if (best >= 0 && env_int("GEFEN_FOLD", 1)) {
+        for (int32_t t = 0; t < st->n_tensors; ++t) {
+            if (ushape[t].lpb_log2 < 0) continue;
+            if (ushape[t].vpl == dom_vpl && ushape[t].bs == dom_bs) continue;
+            const int64_t nv = st->period[t] / 4;
+            const int64_t need = (nv + dom_vpl - 1) / dom_vpl;
+            int l2 = 0;
+            while ((int64_t(1) << l2) < need) ++l2;
+            if ((1 << l2) <= dom_bs) ushape[t] = UShape{l2, dom_vpl, dom_bs};
         }
     }
-    hlists.resize(lists.size());
-    // Fold the small classes other than the largest register-resident one (and the
-    // split huge-block classes, which need two kernels) into one generic launch
-    // (KIND_ANY, tile.vpl = 0). Tile kinds are kept for the histogram kernel.
-    std::vector<std::vector<int32_t>> tile_kinds(lists.size());
-    for (size_t i = 0; i < lists.size(); ++i) tile_kinds[i].assign(lists[i].size(), keys[i].kind);
-    {
-        int dom = -1;
-        int64_t dom_elems = -1;
-        for (size_t i = 0; i < lists.size(); ++i) {
-            if (keys[i].kind != KIND_U) continue;
-            int64_t e = 0;
-            for (const Tile& tl : lists[i]) e += tl.nelem;
-            if (e > dom_elems) {
-                dom_elems = e;
-                dom = static_cast<int>(i);
-            }
-        }
-        if (dom >= 0 && env_int("GEFEN_FOLD", 1)) {
-            // only small classes: a folded tile runs the slower generic path
-            const int64_t fold_max = std::max<int64_t>(int64_t(1) << 21, dom_elems / 64);
-            std::vector<Tile> front;
-            std::vector<int32_t> front_kinds;
-            int32_t any_dtype = -1;
-            for (size_t i = 0; i < lists.size(); ++i) {
-                if (static_cast<int>(i) == dom || keys[i].kind == KIND_H || lists[i].empty())
-                    continue;
-                int64_t e = 0;
-                for (const Tile& tl : lists[i]) e += tl.nelem;
-                if (e > fold_max) continue;
-                // Uniform small-block tiles are cut to kThreads / lpb blocks, lpb = p
-                // rounded up to a power of two: the generic kernel gives each block a
-                // group of lpb lanes and covers such a tile in one pass.
-                for (size_t j = 0; j < lists[i].size(); ++j) {
-                    Tile tl = lists[i][j];
-                    const int32_t kd = tile_kinds[i][j];
-                    tl.vpl = 0;
-                    tl.lpb_log2 = 0;
-                    const int64_t p = st->explicit_blocks ? 0 : st->period[tl.seg];
-                    if (kd == KIND_L && p > 0) {
-                        int64_t lpb = 1;
-                        while (lpb < p) lpb <<= 1;
-                        const int64_t per = kThreads / lpb;
-                        for (int64_t b = 0; b < tl.nblk; b += per) {
-                            Tile sub = tl;
-                            const int64_t nb = std::min<int64_t>(per, tl.nblk - b);
-                            sub.elem0 = tl.elem0 + b * p;
-                            sub.blk0 = tl.blk0 + b;
-                            sub.nblk = static_cast<int16_t>(nb);
-                            sub.nelem = nb * p;
-                            front.push_back(sub);
-                            front_kinds.push_back(kd);
-                        }
-                    } else {
-                        front.push_back(tl);
-                        front_kinds.push_back(kd);
-                    }
+    return ushape;
+}
+
+// A huge block as chunk tiles (KIND_H); the chunk bookkeeping is made absolute when
+// the classes are concatenated.
+void plan_huge(gefen_state* st, TilePlan& P, int32_t t, int32_t gdt, int64_t start,
+               int64_t len, int64_t blk)
+{
+    const size_t li = P.index(KIND_H, gdt, 0);
+    const int64_t nchunk = (len + kHChunk - 1) / kHChunk;
+    const int64_t first_rel = static_cast<int64_t>(P.lists[li].size());
+    for (int64_t c = 0; c < nchunk; ++c) {
+        Tile tl{};
+        tl.elem0 = start + c * kHChunk;
+        tl.blk0 = blk;
+        tl.nelem = std::min(kHChunk, len - c * kHChunk);
+        tl.seg = t;
+        tl.nblk = 1;
+        P.add(li, tl);
+        HTile ht{};
+        ht.blk_len = len;
+        ht.first = first_rel;
+        ht.nchunk = static_cast<int32_t>(nchunk);
+        ht.chunk = static_cast<int32_t>(c);
+        ht.hb = static_cast<int32_t>(st->n_hblocks);
+        P.hlists[li].push_back(ht);
+    }
+    ++st->n_hblocks;
+}
+
+// One block per workgroup (KIND_G).
+void plan_single(TilePlan& P, int32_t t, int32_t gdt, int64_t start, int64_t len, int64_t blk)
+{
+    Tile tl{};
+    tl.elem0 = start;
+    tl.blk0 = blk;
+    tl.nelem = len;
+    tl.seg = t;
+    tl.nblk = 1;
+    P.add(P.index(KIND_G, gdt, 0), tl);
+}
+
+// The tiles of tensor t: explicit blocks by their length; uniform blocks by the period
+// (registers, lane per block, split, or streamed).
+void plan_tensor(gefen_state* st, TilePlan& P, int32_t t, const UShape& u,
+                 const std::vector<int64_t>& s)
+{
+    const int32_t gdt = st->gdtype[t];
+    const int64_t bb = st->blk_begin[t];
+    if (st->explicit_blocks) {
+        const int64_t nb = static_cast<int64_t>(s.size()) - 1;
+        int64_t b = 0;
+        while (b < nb) {
+            const int64_t len = s[b + 1] - s[b];
+            if (len > kHugeBlock) {
+                plan_huge(st, P, t, gdt, s[b], len, bb + b);
+                ++b;
+            } else if (len <= kSmallBlock) {
+                Tile tl{};
+                tl.elem0 = s[b];
+                tl.blk0 = bb + b;
+                tl.seg = t;
+                int n = 0;
+                while (b < nb && n < kThreads && s[b + 1] - s[b] <= kSmallBlock) {
+                    ++n;
+                    ++b;
                 }
-                any_dtype = keys[i].gdtype;
-                lists[i].clear();
-                tile_kinds[i].clear();
-            }
-            if (!front.empty()) {
-                std::vector<Tile>& A = list_for(KIND_ANY, any_dtype, 0);
-                A.insert(A.end(), front.begin(), front.end());
-                hlists.resize(lists.size());
-                tile_kinds.resize(lists.size());
-                tile_kinds.back().insert(tile_kinds.back().end(), front_kinds.begin(),
-                                         front_kinds.end());
+                tl.nblk = static_cast<int16_t>(n);
+                tl.nelem = s[b] - tl.elem0;
+                P.add(P.index(KIND_L, gdt, 0), tl);
+            } else {
+                plan_single(P, t, gdt, s[b], len, bb + b);
+                ++b;
             }
         }
+        return;
     }
+    const int64_t p = st->period[t];
+    const int64_t nb = st->numel[t] / p;
+    if (u.lpb_log2 >= 0) {
+        const int64_t bpw = u.bs >> u.lpb_log2;
+        const size_t li = P.index(KIND_U, gdt, u.vpl, u.bs);
+        for (int64_t b = 0; b < nb; b += bpw) {
+            Tile tl{};
+            const int64_t n = std::min(bpw, nb - b);
+            tl.elem0 = b * p;
+            tl.blk0 = bb + b;
+            tl.nelem = n * p;
+            tl.seg = t;
+            tl.nblk = static_cast<int16_t>(n);
+            tl.vpl = static_cast<uint8_t>(u.vpl);
+            tl.lpb_log2 = static_cast<uint8_t>(u.lpb_log2);
+            P.add(li, tl);
+        }
+    } else if (p <= kSmallBlock) {
+        const size_t li = P.index(KIND_L, gdt, 0);
+        for (int64_t b = 0; b < nb; b += kThreads) {
+            Tile tl{};
+            const int64_t n = std::min<int64_t>(kThreads, nb - b);
+            tl.elem0 = b * p;
+            tl.blk0 = bb + b;
+            tl.nelem = n * p;
+            tl.seg = t;
+            tl.nblk = static_cast<int16_t>(n);
+            P.add(li, tl);
+        }
+    } else if (p > kHugeBlock || (p > kUMaxPeriod && nb < kMinStreamedBlocks)) {
+        for (int64_t b = 0; b < nb; ++b) plan_huge(st, P, t, gdt, b * p, p, bb + b);
+    } else {
+        for (int64_t b = 0; b < nb; ++b) plan_single(P, t, gdt, b * p, p, bb + b);
+    }
+}
+
+// Fold the small classes other than the largest register-resident one (and the split
+// huge-block classes, which need two kernels) into one generic launch (KIND_ANY,
+// tile.vpl = 0); a folded tile runs the slower generic path, so only small classes go.
+// The folded tiles keep their kinds for the histogram kernel.
+void fold_small_classes(const gefen_state* st, TilePlan& P)
+{
+    int dom = -1;
+    int64_t dom_elems = -1;
+    for (size_t i = 0; i < P.lists.size(); ++i) {
+        if (P.keys[i].kind != KIND_U) continue;
+        const int64_t e = P.elems(i);
+        if (e > dom_elems) {
+            dom_elems = e;
+            dom = static_cast<int>(i);
+        }
+    }
+    if (dom < 0 || !env_int("GEFEN_FOLD", 1)) return;
+    const int64_t fold_max = std::max<int64_t>(int64_t(1) << 21, dom_elems / 64);
+    std::vector<Tile> front;
+    std::vector<int32_t> front_kinds;
+    int32_t any_dtype = -1;
+    for (size_t i = 0; i < P.lists.size(); ++i) {
+        if (static_cast<int>(i) == dom || P.keys[i].kind == KIND_H || P.lists[i].empty())
+            continue;
+        if (P.elems(i) > fold_max) continue;
+        // Uniform small-block tiles are cut to kThreads / lpb blocks, lpb = p rounded up
+        // to a power of two: the generic kernel gives each block a group of lpb lanes and
+        // covers such a tile in one pass.
+        for (size_t j = 0; j < P.lists[i].size(); ++j) {
+            Tile tl = P.lists[i][j];
+            const int32_t kd = P.kinds[i][j];
+            tl.vpl = 0;
+            tl.lpb_log2 = 0;
+            const int64_t p = st->explicit_blocks ? 0 : st->period[tl.seg];
+            if (kd == KIND_L && p > 0) {
+                int64_t lpb = 1;
+                while (lpb < p) lpb <<= 1;
+                const int64_t per = kThreads / lpb;
+                for (int64_t b = 0; b < tl.nblk; b += per) {
+                    Tile sub = tl;
+                    const int64_t nb = std::min<int64_t>(per, tl.nblk - b);
+                    sub.elem0 = tl.elem0 + b * p;
+                    sub.blk0 = tl.blk0 + b;
+                    sub.nblk = static_cast<int16_t>(nb);
+                    sub.nelem = nb * p;
+                    front.push_back(sub);
+                    front_kinds.push_back(kd);
+                }
+            } else {
+                front.push_back(tl);
+                front_kinds.push_back(kd);
+            }
+        }
+        any_dtype = P.keys[i].gdtype;
+        P.lists[i].clear();
+        P.kinds[i].clear();
+    }
+    if (front.empty()) return;
+    const size_t ai = P.index(KIND_ANY, any_dtype, 0);
+    P.lists[ai].insert(P.lists[ai].end(), front.begin(), front.end());
+    P.kinds[ai].insert(P.kinds[ai].end(), front_kinds.begin(), front_kinds.end());
+}
+
+// Concatenate the classes (the small generic class first: it is short and leaves the
+// machine to the long launches after it, which measured faster than running it beside
+// them on a second stream, whose fork and join cost more than it saves), record each
+// class's launch range and algorithmic bytes, and upload the tables.
+int upload_plan(gefen_state* st, TilePlan& P)
+{
     std::vector<Tile> all;
     std::vector<int32_t> kinds;
     std::vector<HTile> hall;
     st->classes.clear();
-    // The small generic class launches first: it is short and leaves the machine to the
-    // long launches after it (measured faster than running it beside them on a second
-    // stream, whose fork and join cost more than it saves).
     std::vector<size_t> order;
-    for (size_t i = 0; i < lists.size(); ++i)
-        if (keys[i].kind == KIND_ANY) order.push_back(i);
-    for (size_t i = 0; i < lists.size(); ++i)
-        if (keys[i].kind != KIND_ANY) order.push_back(i);
+    for (size_t i = 0; i < P.lists.size(); ++i)
+        if (P.keys[i].kind == KIND_ANY) order.push_back(i);
+    for (size_t i = 0; i < P.lists.size(); ++i)
+        if (P.keys[i].kind != KIND_ANY) order.push_back(i);
     for (size_t i : order) {
-        if (lists[i].empty()) continue;
+        if (P.lists[i].empty()) continue;
         const int64_t base = static_cast<int64_t>(all.size());
-        if (keys[i].kind == KIND_H) {
-            for (HTile h : hlists[i]) {
+        if (P.keys[i].kind == KIND_H) {
+            for (HTile h : P.hlists[i]) {
                 h.first += base;
                 hall.push_back(h);
             }
         } else {
-            hall.insert(hall.end(), lists[i].size(), HTile{});
+            hall.insert(hall.end(), P.lists[i].size(), HTile{});
         }
-        Class c{keys[i].kind, keys[i].gdtype, keys[i].vpl, keys[i].bs,
-                static_cast<int64_t>(all.size()), static_cast<int64_t>(lists[i].size()), 0, 0};
-        for (size_t j = 0; j < lists[i].size(); ++j) {
-            const Tile& tl = lists[i][j];
+        Class c{P.keys[i].kind, P.keys[i].gdtype, P.keys[i].vpl, P.keys[i].bs, base,
+                static_cast<int64_t>(P.lists[i].size()), 0, 0};
+        for (size_t j = 0; j < P.lists[i].size(); ++j) {
+            const Tile& tl = P.lists[i][j];
             const int64_t per_elem =
                 8 + (st->gdtype[tl.seg] == DT_F32 ? 4 : 2) + (st->code_bits == 4 ? 1 : 2);
             c.elems += tl.nelem;
             c.bytes += tl.nelem * per_elem + 16 * int64_t(tl.nblk);
-            if (tile_kinds[i][j] == KIND_L && st->explicit_blocks) c.bytes += 8 * int64_t(tl.nblk);
+            if (P.kinds[i][j] == KIND_L && st->explicit_blocks) c.bytes += 8 * int64_t(tl.nblk);
         }
         st->classes.push_back(c);
-        all.insert(all.end(), lists[i].begin(), lists[i].end());
-        kinds.insert(kinds.end(), tile_kinds[i].begin(), tile_kinds[i].end());
+        all.insert(all.end(), P.lists[i].begin(), P.lists[i].end());
+        kinds.insert(kinds.end(), P.kinds[i].begin(), P.kinds[i].end());
     }
     st->n_tiles = static_cast<int64_t>(all.size());
     int rc = st->alloc(&st->tiles, sizeof(Tile) * all.size(), false);
@@ -676,6 +689,19 @@ int plan_tiles(gefen_state* st, const std::vector<std::vector<int64_t>>& starts)
                             hipMemcpyHostToDevice));
     }
     return GEFEN_OK;
+}
+
+// Tensor-relative block starts of tensor i (explicit blocks), size n_blocks_i + 1.
+int plan_tiles(gefen_state* st, const std::vector<std::vector<int64_t>>& starts)
+{
+    st->n_hblocks = 0;
+    const std::vector<UShape> ushape = plan_u_shapes(st);
+    TilePlan P;
+    static const std::vector<int64_t> kNone;
+    for (int32_t t = 0; t < st->n_tensors; ++t)
+        plan_tensor(st, P, t, ushape[t], st->explicit_blocks ? starts[t] : kNone);
+    fold_small_classes(st, P);
+    return upload_plan(st, P);
 }
 
 // Alg. 2 for a list of tensors. Writes one period per tensor (host), and optionally the
