@@ -104,7 +104,25 @@ def cpu_baseline(w, params, grads, st, sample_elems: int):
     return {"value": n / dt / 1e9, "unit": "Gparams/s", "cores": 1, "kind": "oracle",
             "sample": f"oracle step (float64, single thread) on {n} of {w.numel} elements: "
                       f"whole blocks from the start of the {len(jobs)} largest tensors",
-            "seconds": dt}
+            "seconds": dt, "host": host_cpu()}
+
+
+def host_cpu():
+    """The host's CPU model and the logical CPUs this process may use."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        ncpu = len(os.sched_getaffinity(0))
+    except AttributeError:
+        ncpu = os.cpu_count()
+    return {"cpu_model": model, "cpus_available": ncpu}
 
 
 def adamw_comparator(torch, w, params, grads, steps: int, gefen_state_bytes: int,
