@@ -307,3 +307,33 @@ def test_gefen_muon_front_end_matches_the_state_calls():
     torch.cuda.synchronize()
     for a, b in zip(ps, ref):
         assert torch.equal(a.detach().reshape(-1), b)
+
+
+def test_steps_on_a_side_stream_match_the_default_stream():
+    """Everything the library enqueues follows the caller's stream: the Gefen step and
+    Gefen-Muon (whose second lane forks from that stream and joins back) on a
+    non-default torch stream give bitwise the results of the default stream."""
+    dev = _dev()
+    shapes = [(64, 96), (96, 64), (77, 1), (128, 128)]
+    gs = [[_grad(r, c, 40 * t + i, torch.bfloat16, dev) for i, (r, c) in enumerate(shapes)]
+          for t in range(3)]
+    out = {}
+    side = torch.cuda.Stream()
+    for name, stream in (("default", None), ("side", side)):
+        torch.manual_seed(12)
+        p_step = [torch.randn(r * c, device=dev) * 0.02 for r, c in shapes]
+        p_muon = [p.clone() for p in p_step]
+        torch.cuda.synchronize()
+        ctx = torch.cuda.stream(stream) if stream is not None else torch.cuda.stream(
+            torch.cuda.current_stream())
+        with ctx:
+            a = gf.GefenState(gs[0])
+            b = gf.GefenState(gs[0])
+            b.muon_init([r for r, _ in shapes])
+            for t in range(3):
+                a.step(p_step, gs[t], 1e-3, (0.9, 0.999), 1e-8, 0.1, t + 1)
+                b.muon_step(p_muon, gs[t], 0.02, 0.95, 0.01, True)
+        torch.cuda.synchronize()
+        out[name] = [p.clone() for p in p_step + p_muon]
+    for i, (x, y) in enumerate(zip(out["default"], out["side"])):
+        assert torch.equal(x, y), i
