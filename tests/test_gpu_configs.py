@@ -261,3 +261,25 @@ def test_stress_sequential_variant_sampled():
     assert rep["codes"] > 10_000_000
     del st, params, g2, smp
     _free()
+
+
+@pytest.mark.parametrize("code_bits", [8, 4])
+def test_gpt2_125m_persistent_state_accounting(code_bits):
+    """The library's persistent state on the GPT-2 125M shapes, with the periods it
+    infers: exactly codes + 8 bytes per block + two codebook slots, and, at 8 bits, the
+    x0.25 of parameter memory that the paper's memory table prints
+    (tests/golden/optimizer_state_memory.txt)."""
+    from test_memory_accounting import _golden, codebook_bytes
+    dev = _dev()
+    w = W.get("gpt2_125m")
+    g1 = W.make_grads(w, W.scale_fields(w), 1, dev)
+    st = gf.GefenState(g1, eps_part=w.eps, code_bits=code_bits)
+    lay = st.layout()
+    persistent, _ = st.state_bytes()
+    codes = sum((t.numel + 31) // 32 * 32 for t in w.tensors) * code_bits // 8
+    assert lay["code_bytes"] == codes
+    assert persistent == codes + 8 * lay["total_blocks"] + codebook_bytes(1 << code_bits)
+    if code_bits == 8:
+        assert round(persistent / (4 * w.numel), 2) == _golden()["gpt2_125m_gefen_persistent"][0]
+    del st, g1
+    _free()

@@ -5,16 +5,25 @@ printed divisor-count maxima, brute-force divisor lists and scores, and a closed
 case whose scores and chosen period follow from the score equation by hand.
 """
 import itertools
+import os
 
 import numpy as np
 import pytest
 
 
+def _golden_tau_maxima():
+    path = os.path.join(os.path.dirname(__file__), "golden", "divisor_count_maxima.txt")
+    rows = [ln.split() for ln in open(path) if ln.strip() and not ln.startswith("#")]
+    return [(int(a), int(b), int(c)) for a, b, c in rows]
+
+
 def test_divisor_counts_printed_in_paper(oracle):
-    # Sec. 5.1 prints the maximum of tau(n) over [0.9e6, 1.1e6] (256) and over
-    # [0.9e9, 1.1e9] (1344). The maximisers are 1,081,080 and 931,170,240.
-    assert oracle.divisors(1081080).size == 256
-    assert oracle.divisors(931170240).size == 1344
+    # Sec. 5.1 prints the maximum of tau(n) over [0.9e6, 1.1e6] and [0.9e9, 1.1e9]
+    # (tests/golden/divisor_count_maxima.txt). The maximisers are 1,081,080 and
+    # 931,170,240; the first interval is swept in full below.
+    golden = {(lo, hi): m for lo, hi, m in _golden_tau_maxima()}
+    assert oracle.divisors(1081080).size == golden[(900_000, 1_100_000)]
+    assert oracle.divisors(931170240).size == golden[(900_000_000, 1_100_000_000)]
 
 
 def test_divisor_count_maximum_over_interval_by_sieve(oracle):
@@ -23,7 +32,8 @@ def test_divisor_count_maximum_over_interval_by_sieve(oracle):
     tau = np.zeros(hi + 1, dtype=np.int32)
     for d in range(1, hi + 1):
         tau[d::d] += 1
-    assert int(tau[lo:hi + 1].max()) == 256
+    assert int(tau[lo:hi + 1].max()) == dict(((a, b), c) for a, b, c in _golden_tau_maxima())[
+        (lo, hi)]
     # spot-check the oracle's count on a few numbers of the interval
     rng = np.random.default_rng(3)
     for n in rng.integers(lo, hi + 1, size=20):
