@@ -47,6 +47,11 @@ def test_reduction_per_billion_parameters():
     assert round(lo, 1) == g[0] and round(hi, 1) == g[0]
 
 
+def test_adamw_state_of_a_13b_model():
+    g = _golden()["adamw_13b_params"]
+    assert g[1] == "GiB" and round(13e9 * 8 / 2**30) == g[0]
+
+
 def test_llama3_state_sizes():
     g = _golden()
     w = W.get("llama3_1p5b")
