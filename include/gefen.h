@@ -54,9 +54,11 @@ typedef enum {
     GEFEN_EDTYPE = -2,      /* unsupported dtype, or dtype differs from the one at init */
     GEFEN_EHIP = -3,        /* a HIP runtime call failed; the message names it */
     GEFEN_ENOMEM = -4,      /* device or host allocation failed */
-    GEFEN_EDEGENERATE = -5  /* codebook fit saw fewer non-empty histogram bins than
-                               codebook entries; a valid fallback codebook was still
-                               installed (see gefen_fit_codebook) */
+    GEFEN_EDEGENERATE = -5  /* reserved, returned by no call: a fit that sees fewer
+                               non-empty histogram bins than codebook entries is not an
+                               error; it installs a valid fallback codebook and
+                               gefen_get_fit_info reports status 1 (fits are
+                               asynchronous, so no call could return it in time) */
 } gefen_status;
 
 typedef enum { GEFEN_F32 = 0, GEFEN_BF16 = 1 } gefen_dtype;
