@@ -388,3 +388,47 @@ def test_degenerate_hyperparameters(lr, betas, eps, wd, t0):
         if lr == 0.0:
             for a, b in zip(params, before):
                 assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("code_bits", [8, 4])
+def test_degenerate_codebook_fit(code_bits):
+    """A first gradient whose block-normalised values fill only a few histogram bins
+    (each block holds +-its absmax and a few fixed fractions of it): the init fit sees
+    b < k non-empty bins, reports status 1, and installs the oracle's fallback codebook
+    bit for bit: the DP over max(b, 2) entries, strictly increasing from -1 to +1, then
+    padded with +1 (App. D has no feasible k-entry solution here). Steps with it, and
+    after a refit on ordinary gradients, match the oracle."""
+    from parity import Run, grad_bits
+    dev = _dev()
+    p, nb = 64, 200
+    n = p * nb
+    levels = torch.tensor([-1.0, -0.5, 0.25, 1.0], device=dev)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(5)
+    pick = torch.randint(0, 4, (n,), generator=gen, device=dev)
+    pick.view(nb, p)[:, 0] = 3     # every block reaches its absmax
+    scales = torch.exp(torch.empty(nb, device=dev).uniform_(-5, 0, generator=gen))
+    g0 = (levels[pick].view(nb, p) * scales[:, None]).reshape(-1).contiguous()
+    theta = torch.randn(n, device=dev) * 0.02
+    run = Run([theta], [g0], period_override=[p], code_bits=code_bits)
+    k = run.k
+    cost, status = run.state.fit_info()
+    h = np.zeros(16 * k, dtype=np.uint64)
+    oracle.histogram_blocks(grad_bits(g0), run.offsets[0], 16 * k, h)
+    assert int((h > 0).sum()) < k
+    cb_ref, cost_ref, _, st_ref = oracle.dp_codebook(h, k)
+    assert status == st_ref == 1 and cost == cost_ref
+    cb = run.state.read(gf.STATE_CB_DEC64).cpu().numpy()
+    np.testing.assert_array_equal(cb, cb_ref)
+    b = int((h > 0).sum())
+    head = cb[:max(b, 2)]
+    assert head[0] == -1.0 and head[-1] == 1.0 and (np.diff(head) > 0).all()
+    assert (cb[max(b, 2):] == 1.0).all()
+    hp = (1e-3, (0.9, 0.999), 1e-8, 0.1)
+    run.teacher_forced_step([g0], *hp, 1, where="degenerate fit t=1")
+    g2 = _grad(n, 77, torch.float32, rows=nb, dev=dev)
+    run.teacher_forced_step([g2], *hp, 2, where="degenerate fit t=2")
+    run.state.fit_codebook([g2])
+    _, status2 = run.state.fit_info()
+    assert status2 == 0
+    run.teacher_forced_step([g2], *hp, 3, where="after refit t=3")
