@@ -337,3 +337,64 @@ def test_steps_on_a_side_stream_match_the_default_stream():
         out[name] = [p.clone() for p in p_step + p_muon]
     for i, (x, y) in enumerate(zip(out["default"], out["side"])):
         assert torch.equal(x, y), i
+
+
+
+# Kept as the record of a removed experiment; see the skip reason.
+SKIP_TUNE = pytest.mark.skip(
+    reason="the rocBLAS solution search for the Newton-Schulz products (gefen_muon_tune) "
+           "was removed: its one GPU run took an illegal memory access inside a library "
+           "solution it timed, whose cause was not found")
+
+
+@SKIP_TUNE
+def test_muon_tuned_products_match_oracle():
+    """Steps after gefen_muon_tune (rocBLAS solutions chosen by timing) still match the
+    oracle, teacher-forced: a batched wide group holding tall and wide GPT-2 MLP
+    matrices, a square group and a lone 256 x 4096 matrix whose Gram product is split
+    over K. The search never reports a chosen time above the library's."""
+    dev = _dev()
+    mr = MuonRun([(768, 3072), (3072, 768), (768, 768), (256, 4096)], torch.float32, dev,
+                 seed=31)
+    res = mr.st.muon_tune()
+    assert 0.0 < res["tuned_us"] <= res["default_us"], res
+    for t in (1, 2):
+        w = mr.step(t, where=f"tuned t={t}")
+    print("tuned products (us):", res, "worst O deviation:", w)
+
+
+@SKIP_TUNE
+def test_muon_tuned_steps_are_deterministic():
+    """With the tuned solutions fixed, the same state and inputs give bitwise the same
+    parameters (no solution that accumulates with atomics): three steps, a checkpoint
+    restore, the same three steps again."""
+    dev = _dev()
+    shapes = [(768, 3072), (3072, 768), (768, 768), (256, 4096)]
+    torch.manual_seed(41)
+    p0 = [torch.randn(r * c, device=dev) * 0.02 for r, c in shapes]
+    gs = [[_grad(r, c, 100 * t + i, torch.bfloat16, dev) for i, (r, c) in enumerate(shapes)]
+          for t in range(3)]
+    st = gf.GefenState(gs[0])
+    st.muon_init([r for r, _ in shapes])
+    st.muon_tune()
+    ckpt = st.export()
+    out = []
+    for rep in range(2):
+        if rep:
+            st.import_(ckpt)
+        ps = [p.clone() for p in p0]
+        for t in range(3):
+            st.muon_step(ps, gs[t], 0.02, 0.95, 0.01, True)
+        torch.cuda.synchronize()
+        out.append(ps)
+    for i, (a, b) in enumerate(zip(*out)):
+        assert torch.equal(a, b), f"tensor {i} {shapes[i]}"
+
+
+@SKIP_TUNE
+def test_muon_tune_before_init_is_refused():
+    dev = _dev()
+    g = torch.randn(1024, device=dev)
+    st = gf.GefenState([g])
+    with pytest.raises(gf.GefenError, match="gefen_muon_init"):
+        st.muon_tune()
