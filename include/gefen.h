@@ -199,8 +199,9 @@ int gefen_read_state(const gefen_state* st, int32_t which, void* dst, int64_t by
                      void* stream);
 
 /* Overwrite a state array from `src` (host or device), same `which` and sizes as
- * gefen_read_state, except 5. Writing 3 or 4 installs a codebook (float[k],
- * strictly increasing, first -1, last +1; EINVAL otherwise) into that slot. */
+ * gefen_read_state, except 5 and 6. Writing 3 or 4 installs a codebook (float[k]:
+ * finite, first -1, last +1, never decreasing -- a degenerate fit repeats +1 at the
+ * end; EINVAL otherwise) into that slot. */
 int gefen_write_state(gefen_state* st, int32_t which, const void* src, int64_t bytes,
                       void* stream);
 
@@ -216,7 +217,10 @@ int gefen_state_bytes(const gefen_state* st, int64_t* persistent, int64_t* works
 /* Checkpoint: serialise the whole mutable state (codes, scales, second moments,
  * both codebook slots, slot indices) into `dst` (host or device) of exactly
  * gefen_checkpoint_bytes() bytes; gefen_import restores it into a state created
- * with the same tensors and blocks. Stream-ordered; synchronises for host memory. */
+ * with the same tensors and blocks. Stream-ordered; synchronises for host memory.
+ * gefen_import checks the header and the codebooks of the slots in use (decode and
+ * encode; as gefen_write_state does) before it writes anything: on EINVAL the state
+ * is unchanged. */
 int gefen_checkpoint_bytes(const gefen_state* st, int64_t* bytes);
 int gefen_export(const gefen_state* st, void* dst, int64_t bytes, void* stream);
 int gefen_import(gefen_state* st, const void* src, int64_t bytes, void* stream);

@@ -853,6 +853,18 @@ CkptLayout ckpt_layout(const gefen_state* st)
     return L;
 }
 
+// A codebook the encode and decode tables accept: finite, first entry -1, last +1, never
+// decreasing. A degenerate fit pads its DP solution with repeated +1 entries; equal
+// entries give equal midpoints, which the encoder resolves to the lower index.
+template <typename T>
+bool valid_codebook(const T* cb, int32_t k)
+{
+    if (k < 2 || cb[0] != T(-1) || cb[k - 1] != T(1)) return false;
+    for (int32_t i = 1; i < k; ++i)
+        if (!(cb[i] >= cb[i - 1]) || !std::isfinite(static_cast<double>(cb[i]))) return false;
+    return true;
+}
+
 bool is_host_ptr(const void* p)
 {
     hipPointerAttribute_t a;
@@ -1206,10 +1218,9 @@ int gefen_write_state(gefen_state* st, int32_t which, const void* src, int64_t b
         std::vector<float> cb(st->k);
         GEFEN_HIP(hipMemcpyAsync(cb.data(), src, need, hipMemcpyDefault, stream));
         GEFEN_HIP(hipStreamSynchronize(stream));
-        if (cb[0] != -1.0f || cb[st->k - 1] != 1.0f)
-            return fail(GEFEN_EINVAL, "codebook must start at -1 and end at +1");
-        for (int i = 1; i < st->k; ++i)
-            if (!(cb[i] > cb[i - 1])) return fail(GEFEN_EINVAL, "codebook must increase strictly");
+        if (!valid_codebook(cb.data(), st->k))
+            return fail(GEFEN_EINVAL, "a codebook must be finite, start at -1, end at +1 and "
+                        "never decrease");
         const int slot = which == 3 ? st->dec_slot : st->enc_slot;
         float* staging = nullptr;
         GEFEN_HIP(hipMallocAsync(reinterpret_cast<void**>(&staging), need, stream));
@@ -1283,19 +1294,28 @@ int gefen_import(gefen_state* st, const void* src, int64_t bytes, void* stream_)
     if (bytes != L.total) return fail(GEFEN_EINVAL, "checkpoint needs %lld bytes", (long long)L.total);
     hipStream_t stream = as_stream(stream_);
     const char* s = static_cast<const char*>(src);
+    // header and both codebooks are checked before anything of the state is touched
     int64_t hdr[8];
+    std::vector<double> cbs(2 * static_cast<size_t>(st->k));
     GEFEN_HIP(hipMemcpyAsync(hdr, s + L.header, sizeof hdr, hipMemcpyDefault, stream));
+    GEFEN_HIP(hipMemcpyAsync(cbs.data(), s + L.cb0, 16 * st->k, hipMemcpyDefault, stream));
     GEFEN_HIP(hipStreamSynchronize(stream));
     if (hdr[0] != (kCkptMagic | (int64_t(1) << 32)) || hdr[1] != st->n_tensors ||
         hdr[2] != st->k || hdr[3] != st->code_bytes || hdr[4] != st->total_blocks ||
         hdr[5] < 0 || hdr[5] > 1 || hdr[6] < 0 || hdr[6] > 1)
         return fail(GEFEN_EINVAL, "checkpoint does not match this state");
+    // the slots in use: decode and encode (one slot until the first refit; the other
+    // holds whatever it was allocated with)
+    for (int64_t slot : {hdr[5], hdr[6]})
+        if (!valid_codebook(cbs.data() + slot * st->k, st->k))
+            return fail(GEFEN_EINVAL, "checkpoint codebook %d is not valid (finite, -1 first, "
+                        "+1 last, never decreasing)", static_cast<int>(slot));
     GEFEN_HIP(hipMemcpyAsync(st->codes, s + L.codes, st->code_bytes, hipMemcpyDefault, stream));
     GEFEN_HIP(hipMemcpyAsync(st->scale, s + L.scale, 4 * st->total_blocks, hipMemcpyDefault, stream));
     GEFEN_HIP(hipMemcpyAsync(st->vmom, s + L.vmom, 4 * st->total_blocks, hipMemcpyDefault, stream));
     double* staging = nullptr;
     GEFEN_HIP(hipMallocAsync(reinterpret_cast<void**>(&staging), 16 * st->k, stream));
-    GEFEN_HIP(hipMemcpyAsync(staging, s + L.cb0, 16 * st->k, hipMemcpyDefault, stream));
+    GEFEN_HIP(hipMemcpyAsync(staging, cbs.data(), 16 * st->k, hipMemcpyHostToDevice, stream));
     for (int slot = 0; slot < 2; ++slot) {
         hipError_t e = launch_install_codebook(staging + slot * st->k, st->k, st->ng,
                                                st->cb32[slot], st->cb64[slot], st->mid[slot],

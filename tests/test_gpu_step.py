@@ -424,6 +424,12 @@ def test_degenerate_codebook_fit(code_bits):
     head = cb[:max(b, 2)]
     assert head[0] == -1.0 and head[-1] == 1.0 and (np.diff(head) > 0).all()
     assert (cb[max(b, 2):] == 1.0).all()
+    # such a codebook (repeated +1 entries) round-trips through write and a checkpoint
+    cb32 = run.state.read(gf.STATE_CB_DEC).clone()
+    run.state.write(gf.STATE_CB_DEC, cb32)
+    assert torch.equal(run.state.read(gf.STATE_CB_DEC), cb32)
+    run.state.import_(run.state.export())
+    np.testing.assert_array_equal(run.state.read(gf.STATE_CB_DEC64).cpu().numpy(), cb_ref)
     hp = (1e-3, (0.9, 0.999), 1e-8, 0.1)
     run.teacher_forced_step([g0], *hp, 1, where="degenerate fit t=1")
     g2 = _grad(n, 77, torch.float32, rows=nb, dev=dev)
@@ -432,3 +438,36 @@ def test_degenerate_codebook_fit(code_bits):
     _, status2 = run.state.fit_info()
     assert status2 == 0
     run.teacher_forced_step([g2], *hp, 3, where="after refit t=3")
+
+
+def test_import_refuses_bad_checkpoints_and_leaves_the_state():
+    """A checkpoint whose codebook decreases (two entries swapped), or whose header does
+    not match the state, is refused before anything is written: the state exports the
+    same bytes afterwards."""
+    dev = _dev()
+    cpu = torch.device("cpu")
+    w = W.get("tiny")
+    fields = W.scale_fields(w)
+    hp = (w.lr, w.betas, w.eps, w.wd)
+    pa = W.init_params(w, dev)
+    st = gf.GefenState(W.make_grads(w, fields, 1, dev))
+    for t in range(1, 4):
+        st.step(pa, W.make_grads(w, fields, t, dev), *hp, t)
+    good = st.export(device=cpu).numpy()
+    k = st.k
+    cb = st.read(gf.STATE_CB_DEC64, device=cpu).numpy()
+    off = good.tobytes().find(cb.tobytes())
+    assert off >= 0
+    bad = good.copy()
+    vals = bad[off:off + 8 * k].view(np.float64)
+    vals[[1, 2]] = vals[[2, 1]]
+    with pytest.raises(gf.GefenError, match="codebook"):
+        st.import_(torch.from_numpy(bad).to(dev))
+    assert np.array_equal(st.export(device=cpu).numpy(), good)
+    bad = good.copy()
+    bad[8] ^= 1                       # n_tensors in the header
+    with pytest.raises(gf.GefenError, match="does not match"):
+        st.import_(torch.from_numpy(bad).to(dev))
+    assert np.array_equal(st.export(device=cpu).numpy(), good)
+    st.import_(torch.from_numpy(good).to(dev))
+    assert np.array_equal(st.export(device=cpu).numpy(), good)
