@@ -132,3 +132,39 @@ def test_stream_mix_argument_errors(lib):
     assert lib.gefen_stream_mix(a16, a16, 0, a16 + 1, 16, None) == -1      # codes 4 B
     assert b"aligned" in lib.gefen_last_error()
     assert lib.gefen_stream_mix(None, None, 0, None, 0, None) == 0         # n = 0: no-op
+
+
+def test_header_is_c99_and_links(lib, tmp_path):
+    """include/gefen.h compiles as strict C99 (no C++ in the ABI), every declared function
+    resolves when a C program links libgefen.so, and a call that fails its argument
+    checks returns GEFEN_EINVAL with a message, without touching the device."""
+    import shutil
+    import subprocess
+    import paper_2606_13894_amd as gf
+    cc = shutil.which("gcc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    names = _declared()
+    src = tmp_path / "abi.c"
+    src.write_text(
+        '#include "gefen.h"\n#include <stdio.h>\n'
+        "typedef void (*fn)(void);\n"
+        "static const fn table[] = {\n"
+        + "".join(f"    (fn){n},\n" for n in names)
+        + "};\n"
+        "int main(void)\n{\n"
+        "    gefen_state* st = 0;\n"
+        "    int rc = gefen_init(NULL, 1, NULL, NULL, 0, 8, 1e-8, NULL, &st);\n"
+        "    const char* msg = gefen_last_error();\n"
+        '    printf("%d %d %s\\n", rc, (int)(sizeof table / sizeof table[0]), msg);\n'
+        "    return rc == GEFEN_EINVAL && msg && msg[0] && st == 0 ? 0 : 1;\n}\n")
+    exe = tmp_path / "abi"
+    libdir = os.path.dirname(gf.LIB_PATH)
+    subprocess.run([cc, "-std=c99", "-Wall", "-Wextra", "-pedantic", "-Werror",
+                    "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe),
+                    "-L", libdir, "-lgefen", f"-Wl,-rpath,{libdir}"],
+                   check=True, capture_output=True, text=True)
+    out = subprocess.run([str(exe)], capture_output=True, text=True, timeout=60)
+    assert out.returncode == 0, out.stdout + out.stderr
+    rc, count, _ = out.stdout.split(" ", 2)
+    assert int(rc) == -1 and int(count) == len(names)
