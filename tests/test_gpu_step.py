@@ -471,3 +471,42 @@ def test_import_refuses_bad_checkpoints_and_leaves_the_state():
     assert np.array_equal(st.export(device=cpu).numpy(), good)
     st.import_(torch.from_numpy(good).to(dev))
     assert np.array_equal(st.export(device=cpu).numpy(), good)
+
+
+@pytest.mark.parametrize("code_bits", [8, 4])
+def test_explicit_blocks_are_deterministic(code_bits):
+    """Explicit irregular blocks take every kernel class (one lane per small block, one
+    workgroup per block, a huge block split over workgroups; with 4-bit codes, nibbles
+    shared across blocks and stored by atomic XOR). From one checkpoint, a refit and two
+    steps give bitwise the same parameters, codes, scales and second moments twice."""
+    dev = _dev()
+    rng = np.random.default_rng(17)
+    sizes = np.concatenate([[1, 3, 33, 70000, 9000], rng.integers(1, 40, size=200),
+                            rng.integers(40, 5000, size=80)])
+    rng.shuffle(sizes)
+    n = int(sizes.sum())
+    n1 = int(sizes[:150].sum())
+    offs = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    gr = lambda t: [_grad(n1, 300 + t, torch.bfloat16, dev=dev),
+                    _grad(n - n1, 400 + t, torch.bfloat16, dev=dev)]
+    p0 = [torch.randn(n1, device=dev) * 0.02, torch.randn(n - n1, device=dev) * 0.02]
+    st = gf.GefenState(gr(1), block_offsets=offs, code_bits=code_bits)
+    ps = [p.clone() for p in p0]
+    for t in range(1, 4):
+        st.step(ps, gr(t), 1e-3, (0.9, 0.999), 1e-8, 0.1, t)
+    ck = st.export()
+    p_ck = [p.clone() for p in ps]
+    outs = []
+    for _ in range(2):
+        st.import_(ck)
+        for a, b in zip(ps, p_ck):
+            a.copy_(b)
+        st.fit_codebook(gr(4))
+        for t in (4, 5):
+            st.step(ps, gr(t), 1e-3, (0.9, 0.999), 1e-8, 0.1, t)
+        torch.cuda.synchronize()
+        outs.append([p.clone() for p in ps] +
+                    [st.read(w).clone() for w in (gf.STATE_CODES, gf.STATE_SCALE, gf.STATE_V,
+                                                  gf.STATE_CB_DEC)])
+    for i, (x, y) in enumerate(zip(*outs)):
+        assert torch.equal(x, y), i
