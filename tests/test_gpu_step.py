@@ -510,3 +510,21 @@ def test_explicit_blocks_are_deterministic(code_bits):
                                                   gf.STATE_CB_DEC)])
     for i, (x, y) in enumerate(zip(*outs)):
         assert torch.equal(x, y), i
+
+
+@pytest.mark.parametrize("code_bits", [8, 4])
+def test_explicit_block_class_edges(code_bits):
+    """Explicit blocks at the edges of the kernel classes: 32 and 33 elements (one lane
+    per block against one workgroup per block), 65536 and 65537 (one workgroup against a
+    block split over workgroups), with odd neighbours so that 4-bit codes share bytes
+    across every edge. Teacher-forced parity against the oracle over three steps."""
+    from parity import Run
+    dev = _dev()
+    sizes = np.array([32, 33, 65536, 1, 65537, 31, 33, 32, 4097, 65536, 7, 65537, 3],
+                     dtype=np.int64)
+    n = int(sizes.sum())
+    offs = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    params = [torch.randn(n, device=dev) * 0.02]
+    gr = lambda t: [_grad(n, 500 + t, torch.bfloat16, dev=dev)]
+    run = Run(params, gr(1), block_offsets=offs, code_bits=code_bits)
+    _run_steps(run, gr, 3, where=f"class edges {code_bits}-bit")
