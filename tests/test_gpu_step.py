@@ -528,3 +528,20 @@ def test_explicit_block_class_edges(code_bits):
     gr = lambda t: [_grad(n, 500 + t, torch.bfloat16, dev=dev)]
     run = Run(params, gr(1), block_offsets=offs, code_bits=code_bits)
     _run_steps(run, gr, 3, where=f"class edges {code_bits}-bit")
+
+
+def test_uniform_long_period_streamed():
+    """A uniform period just above the register kernel's limit with enough blocks
+    (4096) to stay in the one-workgroup-per-block kernel rather than being split: every
+    block of an 8196 x 4096 tensor, teacher-forced against the oracle."""
+    from parity import Run
+    dev = _dev()
+    p, nb = 8196, 4096
+    n = p * nb
+    params = [torch.randn(n, device=dev) * 0.02]
+    gr = lambda t: [_grad(n, 700 + t, torch.bfloat16, rows=nb, dev=dev)]
+    run = Run(params, gr(1), period_override=[p])
+    _run_steps(run, gr, 2, where="p=8196 x 4096")
+    run.state.profile_begin(1)
+    run.state.step(params, gr(3), HP["lr"], HP["betas"], HP["eps"], HP["wd"], 3)
+    assert [k["kind"] for k in run.state.profile_end()] == ["streamed_block"]
