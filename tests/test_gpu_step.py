@@ -545,3 +545,22 @@ def test_uniform_long_period_streamed():
     run.state.profile_begin(1)
     run.state.step(params, gr(3), HP["lr"], HP["betas"], HP["eps"], HP["wd"], 3)
     assert [k["kind"] for k in run.state.profile_end()] == ["streamed_block"]
+
+
+def test_tiny_tensors_inferred():
+    """Tensors of 1 to 12 elements (a scalar parameter, primes, small composites) beside a
+    normal matrix, both gradient dtypes, periods inferred on the GPU: each period equals
+    the oracle's Alg. 2 result on the same bits, and three steps match the oracle."""
+    from parity import Run, grad_bits
+    dev = _dev()
+    sizes = [1, 2, 3, 5, 7, 4, 6, 12, 2048 * 6]
+    dts = [torch.float32, torch.bfloat16] * 4 + [torch.bfloat16]
+    params = [torch.randn(n, device=dev) * 0.02 for n in sizes]
+    gr = lambda t: [_grad(n, 900 + 7 * i + t, dt, rows=6 if n > 12 else None, dev=dev)
+                    for i, (n, dt) in enumerate(zip(sizes, dts))]
+    g1 = gr(1)
+    run = Run(params, g1)
+    for i, g in enumerate(g1):
+        _, _, per = oracle.partition(grad_bits(g), 1e-8)
+        assert run.periods[i] == per, (sizes[i], run.periods[i], per)
+    _run_steps(run, gr, 3, where="tiny tensors")
