@@ -283,3 +283,45 @@ def test_gpt2_125m_persistent_state_accounting(code_bits):
         assert round(persistent / (4 * w.numel), 2) == _golden()["gpt2_125m_gefen_persistent"][0]
     del st, g1
     _free()
+
+
+def test_uniform_tensor_beyond_2p31_elements_sampled():
+    """One bf16 tensor of 2048 x 1,048,600 elements (2^31 + 49,152) with period 2048, so
+    the register kernel and the state tables index past 2^31 elements (the init
+    histogram and fit run over all of them too). Two steps; sampled blocks (the first two, the last 100, those around element 2^31,
+    and a seeded random 0.01 %) checked completely against the oracle."""
+    dev = _dev()
+    p, nb = 2048, 1_048_600
+    n = p * nb
+    assert n > 2 ** 31
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(71)
+    params = [torch.randn(n, device=dev, generator=gen) * 0.02]
+    row_scale = torch.exp(torch.empty(nb, device=dev).uniform_(np.log(1e-3), 0, generator=gen))
+
+    def grads(t):
+        g = torch.empty(n, device=dev, dtype=torch.bfloat16)
+        gen.manual_seed(1000 + t)
+        for r0 in range(0, nb, 1 << 17):      # in slices, to bound the float32 temporary
+            r1 = min(nb, r0 + (1 << 17))
+            x = torch.randn((r1 - r0) * p, device=dev, generator=gen)
+            g[r0 * p:r1 * p] = (x.view(r1 - r0, p) * row_scale[r0:r1, None]).reshape(-1).bfloat16()
+        return [g]
+
+    g1 = grads(1)
+    st = gf.GefenState(g1, period_override=[p])
+    offs = _uniform_offsets(params, [p])
+    mid = 2 ** 31 // p
+    rng = np.random.default_rng(5)
+    pick = set(range(2)) | set(range(nb - 100, nb)) | set(range(mid - 3, mid + 3))
+    pick |= set(rng.choice(nb, size=nb // 10000, replace=False).tolist())
+    blocks = [np.array(sorted(pick), dtype=np.int64)]
+    smp = Sampled(st, params, offs, blocks)
+    hp = (1e-3, (0.9, 0.999), 1e-8, 0.1)
+    smp.step(g1, *hp, 1, where="2^31+ t=1")
+    del g1
+    _free()
+    smp.step(grads(2), *hp, 2, where="2^31+ t=2")
+    st.close()
+    del params, smp
+    _free()
