@@ -285,7 +285,8 @@ def test_gpt2_125m_persistent_state_accounting(code_bits):
     _free()
 
 
-def test_uniform_tensor_beyond_2p31_elements_sampled():
+@pytest.mark.parametrize("code_bits", [8, 4])
+def test_uniform_tensor_beyond_2p31_elements_sampled(code_bits):
     """One bf16 tensor of 2048 x 1,048,600 elements (2^31 + 49,152) with period 2048, so
     the register kernel and the state tables index past 2^31 elements (the init
     histogram and fit run over all of them too). Two steps; sampled blocks (the first two, the last 100, those around element 2^31,
@@ -309,7 +310,7 @@ def test_uniform_tensor_beyond_2p31_elements_sampled():
         return [g]
 
     g1 = grads(1)
-    st = gf.GefenState(g1, period_override=[p])
+    st = gf.GefenState(g1, period_override=[p], code_bits=code_bits)
     offs = _uniform_offsets(params, [p])
     mid = 2 ** 31 // p
     rng = np.random.default_rng(5)
