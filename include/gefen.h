@@ -167,7 +167,9 @@ int gefen_histogram(gefen_state* st, const gefen_tensor* grads, int32_t n_tensor
  * uint64[nbins]) into k sorted entries with the first forced to -1 and the last to
  * +1. Outputs: codebook_out device double[k], cost_out device double[1],
  * status_out device int32[1] (0 ok, 1 degenerate: fewer non-empty bins than k, the
- * DP then uses max(b, 2) entries and pads with +1). Asynchronous. */
+ * DP then uses max(b, 2) entries and pads with +1). Asynchronous; its workspace is
+ * allocated and freed stream-ordered on `stream`.
+ * Errors: EINVAL (NULL pointer, k outside [2, 256], nbins outside [1, 4096]), EHIP. */
 int gefen_dp_codebook(const uint64_t* hist, int32_t nbins, int32_t k, double* codebook_out,
                       double* cost_out, int32_t* status_out, void* stream);
 
@@ -175,7 +177,8 @@ int gefen_dp_codebook(const uint64_t* hist, int32_t nbins, int32_t k, double* co
  * Queries, state access and checkpointing.
  * ---------------------------------------------------------------------------- */
 
-/* Periods per tensor (0 for tensors under explicit blocks). Host int64[n_tensors]. */
+/* Periods per tensor (0 for tensors under explicit blocks). Host int64[n_tensors].
+ * Errors: EINVAL (NULL). */
 int gefen_get_periods(const gefen_state* st, int64_t* periods_out);
 
 /* Layout of the state buffers (host int64 arrays of n_tensors + 1 entries each):
@@ -184,7 +187,7 @@ int gefen_get_periods(const gefen_state* st, int64_t* periods_out);
  * code j is byte j of the codes buffer; with 4-bit codes it is the low (j even) or high
  * (j odd) nibble of byte j / 2. Tensor i's blocks are global block indices
  * [block_index[i], block_index[i+1]). total_code_bytes is the codes buffer's size.
- * Any output pointer may be NULL. */
+ * Any output pointer may be NULL. Errors: EINVAL (NULL state). */
 int gefen_get_layout(const gefen_state* st, int64_t* code_offsets, int64_t* block_index,
                      int64_t* total_code_bytes, int64_t* total_blocks, int32_t* k);
 
@@ -194,7 +197,8 @@ int gefen_get_layout(const gefen_state* st, int64_t* code_offsets, int64_t* bloc
  * 4 = encode codebook (float[k]), 5 = decode codebook in double (double[k]),
  * 6 = the Gefen-Muon bfloat16 momentum matrix (uint16[code index count], after
  * gefen_muon_init; read-only, as is 5).
- * `bytes` must equal the array size. Synchronises `stream` when dst is host memory. */
+ * `bytes` must equal the array size. Synchronises `stream` when dst is host memory.
+ * Errors: EINVAL (NULL, unknown `which`, 6 before gefen_muon_init, size mismatch), EHIP. */
 int gefen_read_state(const gefen_state* st, int32_t which, void* dst, int64_t bytes,
                      void* stream);
 
@@ -206,7 +210,8 @@ int gefen_write_state(gefen_state* st, int32_t which, const void* src, int64_t b
                       void* stream);
 
 /* Result of the last codebook fit (init or gefen_fit_codebook): DP cost and
- * status (0 ok, 1 degenerate). Synchronises `stream`. */
+ * status (0 ok, 1 degenerate). Either output may be NULL. Synchronises `stream`.
+ * Errors: EINVAL (NULL state), EHIP. */
 int gefen_get_fit_info(const gefen_state* st, double* cost_out, int32_t* status_out,
                        void* stream);
 
@@ -240,6 +245,8 @@ int gefen_import(gefen_state* st, const void* src, int64_t bytes, void* stream);
  * and write; per
  * block: 16 for scale and second moment read and write, plus 8 for an explicit block
  * offset read by the small-block kernel). It then disarms and frees the events.
+ * Errors: EINVAL (NULL state or n_classes, max_steps < 1, cap below the class count),
+ * EHIP (event creation or timing).
  * ---------------------------------------------------------------------------- */
 int gefen_profile_begin(gefen_state* st, int32_t max_steps);
 int gefen_profile_end(gefen_state* st, int32_t cap, int32_t* n_classes, int32_t* kind,
@@ -297,7 +304,7 @@ int gefen_muon_step(gefen_state* st, const gefen_tensor* params, const gefen_ten
  * orthogonalisation wall time (normalise, Newton-Schulz and update of every shape
  * group, on both of the step's streams, from the end of the norms to the join), in
  * milliseconds, from HIP events on the step's stream; then disarms like
- * gefen_profile_end. */
+ * gefen_profile_end. Errors: EINVAL (NULL), EHIP. */
 int gefen_muon_profile_end(gefen_state* st, int32_t* steps, double* codec_ms, double* ortho_ms);
 
 /* ------------------------------------------------------------------------------
