@@ -34,6 +34,9 @@
  *  GEFEN_U_VPL       1-8: force that kernel's vectors per lane (default 0: chosen).
  *  GEFEN_FOLD        0: keep every small kernel class as its own launch instead of one
  *                    leftover launch (default 1).
+ *  GEFEN_G_RUNS      0: explicit blocks of 33-2042 elements take one workgroup each
+ *                    instead of being packed into register runs (8-bit codes; read by
+ *                    gefen_init; default 1).
  *  GEFEN_MUON_LANES  1: run every Gefen-Muon shape group on the caller's stream instead
  *                    of two concurrent lanes (read by gefen_muon_init; default 2).
  *  GEFEN_DEBUG_SYNC  set: gefen_step synchronises its stream and reports kernel errors.
@@ -234,7 +237,8 @@ int gefen_import(gefen_state* st, const void* src, int64_t bytes, void* stream);
  * Measurement support. gefen_profile_begin arms per-launch timing for the next
  * `max_steps` calls of gefen_step: a pair of HIP events is recorded on the step's
  * stream around every step-kernel launch (one launch per kernel class: KIND 0 =
- * uniform blocks in registers, 1 = one streamed block per workgroup, 2 = one small
+ * uniform blocks in registers, 1 = one streamed block per workgroup (or, with 8-bit
+ * codes, a run of consecutive explicit blocks of 33-2042 elements in registers), 2 = one small
  * block per lane, 3 = blocks over 65536 elements split across workgroups (two
  * kernels, timed together), 4 = the leftover small tiles of all other classes in one
  * generic launch). gefen_profile_end synchronises those events and returns, for each

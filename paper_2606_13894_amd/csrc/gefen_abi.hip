@@ -5,6 +5,7 @@
 #include "gefen_internal.h"
 #include "muon_internal.h"
 #include "measure_internal.h"
+#include "run_internal.h"
 
 #include <rocblas/rocblas.h>
 
@@ -507,10 +508,29 @@ void plan_tensor(gefen_state* st, TilePlan& P, int32_t t, const UShape& u,
     const int64_t bb = st->blk_begin[t];
     if (st->explicit_blocks) {
         const int64_t nb = static_cast<int64_t>(s.size()) - 1;
+        static const bool runs = env_int("GEFEN_G_RUNS", 1) != 0;
+        auto run_block = [](int64_t len) { return len >= kRunMinBlock && len <= kRunMaxElems; };
         int64_t b = 0;
         while (b < nb) {
             const int64_t len = s[b + 1] - s[b];
-            if (len > kHugeBlock) {
+            if (st->code_bits == 8 && runs && run_block(len)) {
+                // consecutive short blocks held in registers by one KIND_G workgroup
+                const int64_t b0 = b;
+                int cnt = 0;
+                while (b < nb && cnt < kRunMaxBlocks && run_block(s[b + 1] - s[b]) &&
+                       s[b + 1] - s[b0] <= kRunMaxElems) {
+                    ++cnt;
+                    ++b;
+                }
+                Tile tl{};
+                tl.elem0 = s[b0];
+                tl.blk0 = bb + b0;
+                tl.nelem = s[b] - s[b0];
+                tl.seg = t;
+                tl.nblk = static_cast<int16_t>(cnt);
+                tl.vpl = 1;
+                P.add(P.index(KIND_G, gdt, 0), tl);
+            } else if (len > kHugeBlock) {
                 plan_huge(st, P, t, gdt, s[b], len, bb + b);
                 ++b;
             } else if (len <= kSmallBlock) {
@@ -667,6 +687,14 @@ int upload_plan(gefen_state* st, TilePlan& P)
             c.elems += tl.nelem;
             c.bytes += tl.nelem * per_elem + 16 * int64_t(tl.nblk);
             if (P.kinds[i][j] == KIND_L && st->explicit_blocks) c.bytes += 8 * int64_t(tl.nblk);
+            if (P.kinds[i][j] == KIND_G && tl.vpl == 1) {
+                // a register run: the kernel's fixed register and LDS capacity
+                const int64_t nvec = ((tl.elem0 + tl.nelem + 3) >> 2) - (tl.elem0 >> 2);
+                if (nvec > kRunMaxVec || tl.nblk < 1 || tl.nblk > kRunMaxBlocks)
+                    return fail(GEFEN_EINVAL, "internal: run tile of %lld vectors, %d blocks",
+                                (long long)nvec, int(tl.nblk));
+                c.bytes += 8 * (int64_t(tl.nblk) + 1);
+            }
         }
         st->classes.push_back(c);
         all.insert(all.end(), P.lists[i].begin(), P.lists[i].end());

@@ -14,6 +14,7 @@
 // (one byte per bucket of [-1, 1] giving the number of midpoints below the bucket) plus
 // a short scan over the midpoints that fall inside the bucket (at most one for codebooks
 // whose entries are at least a bucket apart, as the DP's are).
+#include "run_internal.h"
 #include "step_device.h"
 
 namespace gefen {
@@ -526,7 +527,178 @@ __device__ __forceinline__ void wg_reduce(float& ss, float& am, LdsTables& L)
     __syncthreads();
 }
 
-// KIND_G: one block per workgroup, any size and alignment: reduce pass, update pass.
+// Register runs inside the KIND_G launch (tile.vpl == 1): consecutive explicit blocks of
+// kRunMinBlock .. kRunMaxElems elements, at most kRunMaxElems in all, taken by one
+// workgroup with every element in registers (two 4-element vectors per thread, loaded
+// before anything else), so nothing is read twice. A vector meets at most two blocks, so
+// it keeps one partial (sum g^2, max |m|) for the block of its first element and one
+// for the next; one wave per block then reduces them in a fixed order. Edge vectors
+// (shared with neighbouring tiles) are loaded and stored element by element.
+struct RunLds {
+    int64_t start[kRunMaxBlocks + 1];   // tensor-relative block starts; start[nblk] = end
+    float s_old[kRunMaxBlocks], v_old[kRunMaxBlocks];
+    float s_new[kRunMaxBlocks], r[kRunMaxBlocks], inv_s[kRunMaxBlocks];
+    float part[kRunMaxVec][4];
+};
+
+template <int GDT>
+__device__ __forceinline__ void run_tile(LdsTables& L, RunLds& R, const Tile& tl, const Seg& sg,
+                                         uint8_t* __restrict__ codes, float* __restrict__ scale,
+                                         float* __restrict__ vmom, const CodebookDev& cbd,
+                                         const StepScalars& sc)
+{
+    const int tid = threadIdx.x;
+    const int64_t e_lo = tl.elem0, e_hi = tl.elem0 + tl.nelem;
+    const int64_t va = e_lo >> 2;
+    const int nvec = static_cast<int>(((e_hi + 3) >> 2) - va);   // <= kRunMaxVec (planner)
+    const int nb = tl.nblk;                                       // <= kRunMaxBlocks
+    const bool aligned = vector_ok<GDT>(sg);
+    float* __restrict__ th = sg.theta;
+    const int64_t cj = sg.code_off;
+    float tv[kRunVpl][4], gv[kRunVpl][4];
+    uint32_t cq[kRunVpl];
+#pragma unroll
+    for (int j = 0; j < kRunVpl; ++j) {
+        const int i = tid + j * kThreads;
+        cq[j] = 0;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) { tv[j][c] = 0.0f; gv[j][c] = 0.0f; }
+        if (i < nvec) {
+            const int64_t v = va + i;
+            const int64_t e = 4 * v;
+            if (aligned && e >= e_lo && e + 4 <= e_hi) {
+                const f32x4 t4 = __builtin_nontemporal_load(gl<f32x4>(th) + v);
+                tv[j][0] = t4.x; tv[j][1] = t4.y; tv[j][2] = t4.z; tv[j][3] = t4.w;
+                load_grad4<GDT>(sg, v, gv[j]);
+                cq[j] = *gl<uint32_t>(codes + cj + e);
+            } else {
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const int64_t x = e + c;
+                    if (x >= e_lo && x < e_hi) {
+                        tv[j][c] = th[x];
+                        gv[j][c] = load_grad(sg.grad, x, GDT);
+                        cq[j] |= static_cast<uint32_t>(codes[cj + x]) << (8 * c);
+                    }
+                }
+            }
+        }
+    }
+    const int64_t local0 = tl.blk0 - sg.blk_begin;
+    for (int k = tid; k <= nb; k += kThreads) R.start[k] = sg.csr[local0 + k];
+    for (int k = tid; k < nb; k += kThreads) {
+        R.s_old[k] = scale[tl.blk0 + k];
+        R.v_old[k] = vmom[tl.blk0 + k];
+    }
+    load_tables(L, cbd);
+    __syncthreads();
+    int kb[kRunVpl];
+#pragma unroll
+    for (int j = 0; j < kRunVpl; ++j) {
+        const int i = tid + j * kThreads;
+        kb[j] = 0;
+        if (i < nvec) {
+            const int64_t e = 4 * (va + i);
+            const int64_t first = e > e_lo ? e : e_lo;
+            int lo = 0, hi = nb - 1;   // last block whose start <= first
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (R.start[mid] <= first) lo = mid; else hi = mid - 1;
+            }
+            kb[j] = lo;
+            const int64_t next = R.start[lo + 1];
+            float ssa = 0.0f, ama = 0.0f, ssb = 0.0f, amb = 0.0f;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const int64_t x = e + c;
+                if (x >= e_lo && x < e_hi) {
+                    const bool second = x >= next;   // then lo + 1 < nb
+                    const float g = gv[j][c];
+                    const float m = momentum(L, code_get<8>(cq[j], c),
+                                             R.s_old[lo + (second ? 1 : 0)], g, sc);
+                    gv[j][c] = m;
+                    if (second) {
+                        ssb = fmaf(g, g, ssb);
+                        amb = fmaxf(amb, fabsf(m));
+                    } else {
+                        ssa = fmaf(g, g, ssa);
+                        ama = fmaxf(ama, fabsf(m));
+                    }
+                }
+            }
+            R.part[i][0] = ssa;
+            R.part[i][1] = ama;
+            R.part[i][2] = ssb;
+            R.part[i][3] = amb;
+        }
+    }
+    __syncthreads();
+    const int wave = tid >> 6, lane = tid & 63;
+    for (int k = wave; k < nb; k += kThreads / 64) {
+        const int64_t bs = R.start[k], be = R.start[k + 1];
+        const int i0 = static_cast<int>((bs >> 2) - va);
+        const int i1 = static_cast<int>(((be - 1) >> 2) - va);
+        float ss = 0.0f, am = 0.0f;
+        for (int i = i0 + lane; i <= i1; i += 64) {
+            const int64_t e = 4 * (va + i);
+            const bool own_first = (e > e_lo ? e : e_lo) >= bs;
+            ss += own_first ? R.part[i][0] : R.part[i][2];
+            am = fmaxf(am, own_first ? R.part[i][1] : R.part[i][3]);
+        }
+        for (int off = 1; off < 64; off <<= 1) {
+            ss += __shfl_xor(ss, off);
+            am = fmaxf(am, __shfl_xor(am, off));
+        }
+        if (lane == 0) {
+            const BlockOut bo = finish_block(ss, am, R.v_old[k], static_cast<float>(be - bs), sc);
+            scale[tl.blk0 + k] = bo.s_new;
+            vmom[tl.blk0 + k] = bo.v_new;
+            R.s_new[k] = bo.s_new;
+            R.r[k] = bo.r;
+            R.inv_s[k] = bo.inv_s;
+        }
+    }
+    __syncthreads();
+    const float half_ng = 0.5f * static_cast<float>(cbd.ng);
+    const int ng_m1 = cbd.ng - 1;
+#pragma unroll
+    for (int j = 0; j < kRunVpl; ++j) {
+        const int i = tid + j * kThreads;
+        if (i >= nvec) continue;
+        const int64_t v = va + i;
+        const int64_t e = 4 * v;
+        const int lo = kb[j];
+        const int64_t next = R.start[lo + 1];
+        uint32_t packed = 0;
+        float out[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const int k = lo + (e + c >= next ? 1 : 0);
+            const int kk = k < nb ? k : nb - 1;   // lanes outside the run: any valid block
+            const float m = gv[j][c];
+            const int q = R.s_new[kk] > 0.0f ? encode(L, m * R.inv_s[kk], half_ng, ng_m1) : 0;
+            packed |= static_cast<uint32_t>(q) << (8 * c);
+            out[c] = fmaf(-R.r[kk], m, tv[j][c] * sc.decay);
+        }
+        if (aligned && e >= e_lo && e + 4 <= e_hi) {
+            const f32x4 o4 = {out[0], out[1], out[2], out[3]};
+            __builtin_nontemporal_store(o4, glw<f32x4>(th) + v);
+            code_st4<8>(codes, cj + e, packed);
+        } else {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const int64_t x = e + c;
+                if (x >= e_lo && x < e_hi) {
+                    th[x] = out[c];
+                    codes[cj + x] = static_cast<uint8_t>(packed >> (8 * c));
+                }
+            }
+        }
+    }
+}
+
+// KIND_G: one block per workgroup, any size and alignment: reduce pass, update pass;
+// or a register run of short explicit blocks (tile.vpl == 1, 8-bit codes).
 template <int GDT, int CB>
 __global__ __launch_bounds__(kThreads) void k_step_g(const Tile* __restrict__ tiles,
                                                      const Seg* __restrict__ segs,
@@ -536,8 +708,13 @@ __global__ __launch_bounds__(kThreads) void k_step_g(const Tile* __restrict__ ti
                                                      StepScalars sc)
 {
     __shared__ LdsTables L;
+    __shared__ RunLds R;
     const Tile tl = tiles[blockIdx.x];
     const Seg sg = segs[tl.seg];
+    if (CB == 8 && tl.vpl == 1) {   // a register run (8-bit codes only)
+        run_tile<GDT>(L, R, tl, sg, codes, scale, vmom, cbd, sc);
+        return;
+    }
     const int64_t blk = tl.blk0;
     const Span sp = make_span<GDT>(sg, tl.elem0, tl.nelem);
     const float s_old = scale[blk];
