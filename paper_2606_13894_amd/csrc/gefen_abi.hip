@@ -693,7 +693,6 @@ int upload_plan(gefen_state* st, TilePlan& P)
                 if (nvec > kRunMaxVec || tl.nblk < 1 || tl.nblk > kRunMaxBlocks)
                     return fail(GEFEN_EINVAL, "internal: run tile of %lld vectors, %d blocks",
                                 (long long)nvec, int(tl.nblk));
-                c.bytes += 8 * (int64_t(tl.nblk) + 1);
             }
         }
         st->classes.push_back(c);
