@@ -240,26 +240,51 @@ def to_bf16(x):
     return r.astype(np.uint32).view(np.float32).astype(np.float64)
 
 
+def ns_normalise(u, rows, cols, eps=MUON_EPS, bf16=True):
+    """First stage of Muon's orthogonalisation: the wide orientation of the rows x cols
+    matrix (transposed when rows > cols), divided by its Frobenius norm (at least eps).
+    With bf16 the input, the norm, eps and the quotient are bfloat16 values."""
+    r = to_bf16 if bf16 else (lambda z: np.asarray(z, dtype=np.float64))
+    x = r(np.asarray(u, dtype=np.float64).reshape(rows, cols))
+    if rows > cols:
+        x = x.T
+    norm = float(r(np.array([np.sqrt(np.sum(x * x))]))[0])
+    return r(x / max(norm, float(r(np.array([eps]))[0])))
+
+
+def ns_gram(x, bf16=True):
+    """A = X X^T, one rounding of the exact product (a float32 accumulator rounded to
+    bfloat16 with bf16)."""
+    r = to_bf16 if bf16 else (lambda z: np.asarray(z, dtype=np.float64))
+    return r(x @ x.T)
+
+
+def ns_poly(gram, b, c, bf16=True):
+    """B = b A + c A A, one rounding of the whole expression (a matrix product whose
+    epilogue adds the scaled input before the result is rounded)."""
+    r = to_bf16 if bf16 else (lambda z: np.asarray(z, dtype=np.float64))
+    return r(b * gram + c * (gram @ gram))
+
+
+def ns_combine(x, poly, a, bf16=True):
+    """X' = a X + B X, one rounding of the whole expression."""
+    r = to_bf16 if bf16 else (lambda z: np.asarray(z, dtype=np.float64))
+    return r(a * x + poly @ x)
+
+
 def newton_schulz(u, rows, cols, steps=MUON_NS_STEPS, coeffs=MUON_NS_COEFFS, eps=MUON_EPS,
                   bf16=True):
     """Muon's orthogonalisation of a rows x cols matrix: work on the wide orientation
     (transpose when rows > cols), divide by the Frobenius norm (at least eps), then
     `steps` times X <- a X + (b A + c A^2) X with A = X X^T; transpose back.
     With bf16, the input, the norm and every matrix result are rounded to bfloat16,
-    as the implementation the paper uses does. Returns a float64 rows x cols array."""
+    as the implementation the paper uses does (three rounded products per iteration:
+    A, then b A + c A A, then a X + B X). Returns a float64 rows x cols array."""
     a, b, c = coeffs
-    r = to_bf16 if bf16 else (lambda z: np.asarray(z, dtype=np.float64))
-    x = r(np.asarray(u, dtype=np.float64).reshape(rows, cols))
-    transposed = rows > cols
-    if transposed:
-        x = x.T
-    norm = float(r(np.array([np.sqrt(np.sum(x * x))]))[0])
-    x = r(x / max(norm, float(r(np.array([eps]))[0])))
+    x = ns_normalise(u, rows, cols, eps, bf16)
     for _ in range(steps):
-        gram = r(x @ x.T)
-        poly = r(b * gram + c * (gram @ gram))
-        x = r(a * x + poly @ x)
-    return np.ascontiguousarray(x.T if transposed else x)
+        x = ns_combine(x, ns_poly(ns_gram(x, bf16), b, c, bf16), a, bf16)
+    return np.ascontiguousarray(x.T if rows > cols else x)
 
 
 def muon_lr_scale(rows, cols):

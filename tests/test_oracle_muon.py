@@ -12,12 +12,18 @@
   (the step's codes are pinned separately).
 * Whole step with lossless codes against torch.optim.Muon (CPU), within bfloat16
   rounding of the orthogonalised update.
+* bfloat16 Newton-Schulz against torch's own implementation (the one torch.optim.Muon
+  runs), on the CPU: each of the three products of an iteration, given torch's inputs,
+  rounds where torch rounds (bit-equal except rare one-step flips from float32
+  accumulation order); one whole iteration from the normalisation on; five iterations
+  within the spread that accumulation order alone produces.
 """
 import numpy as np
 import pytest
 import torch
 
 import oracle
+from torch.optim._muon import _zeropower_via_newtonschulz as torch_newton_schulz
 
 
 def test_bf16_rounding_matches_torch():
@@ -141,3 +147,110 @@ def test_lossless_step_matches_torch_muon(rows, cols):
     # round differently (accumulation order and width), measured up to 0.8 % of one step
     assert np.abs(theta - ref).max() < 0.02 * scale
     assert np.abs(theta - theta0).max() > 10 * np.abs(theta - ref).max()
+
+
+# ------------------------------------------------------------------ bf16 Newton-Schulz
+NS_SHAPES = [(64, 256), (96, 96), (128, 384), (32, 1000), (200, 600)]
+FLIP_FRACTION = 2e-3   # measured at most 1e-3 (4 of 4096 elements) per product here
+
+
+def _torch_products(x, coeffs):
+    """One iteration in torch's bfloat16 form: the products the Muon implementation calls."""
+    a, b, c = coeffs
+    gram = x @ x.T
+    poly = torch.addmm(gram, gram, gram, beta=b, alpha=c)
+    return gram, poly, torch.addmm(x, poly, x, beta=a)
+
+
+def _check_product(got, ref, mag, k, what):
+    """got, ref: bfloat16 values (float64 arrays). They may differ where a float32 sum of
+    k terms of total magnitude `mag`, taken in another order, rounds to the neighbouring
+    bfloat16 value: one step of 2^-7 relative at most, or the sum's own error where the
+    terms cancel. Such flips must stay rare."""
+    d = np.abs(got - ref)
+    bound = 2.0 ** -7 * np.abs(ref) + k * 2.0 ** -24 * mag
+    assert (d <= bound).all(), (what, (d / np.maximum(bound, 1e-300)).max())
+    frac = np.count_nonzero(d) / d.size
+    assert frac <= FLIP_FRACTION, (what, frac)
+    return frac
+
+
+def _normalised_bf16(u):
+    x = torch.from_numpy(u).bfloat16()
+    return x / x.norm().clamp(min=oracle.MUON_EPS)
+
+
+@pytest.mark.parametrize("m,n", NS_SHAPES)
+def test_ns_products_round_as_torch(m, n):
+    """Teacher-forced: every product of five iterations, fed torch's own operands."""
+    a, b, c = oracle.MUON_NS_COEFFS
+    rng = np.random.default_rng(m * 7 + n)
+    x = _normalised_bf16(rng.standard_normal((m, n)).astype(np.float32))
+    for _ in range(5):
+        gram, poly, xn = _torch_products(x, oracle.MUON_NS_COEFFS)
+        xd, gd, pd = (t.double().numpy() for t in (x, gram, poly))
+        _check_product(oracle.ns_gram(xd), gd, np.abs(xd) @ np.abs(xd).T, n, "gram")
+        _check_product(oracle.ns_poly(gd, b, c), pd,
+                       abs(b) * np.abs(gd) + abs(c) * (np.abs(gd) @ np.abs(gd)), m, "poly")
+        _check_product(oracle.ns_combine(xd, pd, a), xn.double().numpy(),
+                       abs(a) * np.abs(xd) + np.abs(pd) @ np.abs(xd), m, "combine")
+        x = xn
+
+
+def test_ns_product_pin_catches_rounding_slips():
+    """The product pin is sharp enough to see a misplaced rounding: each variant below
+    rounds one intermediate that torch keeps in float32, and differs from torch in far
+    more elements than the pin allows."""
+    a, b, c = oracle.MUON_NS_COEFFS
+    r = oracle.to_bf16
+    rng = np.random.default_rng(11)
+    x = _normalised_bf16(rng.standard_normal((128, 384)).astype(np.float32))
+    for _ in range(2):   # the second iteration's operands are no longer near-orthogonal
+        gram, poly, xn = _torch_products(x, oracle.MUON_NS_COEFFS)
+        x = xn
+    xd, gd, pd = (t.double().numpy() for t in (x, gram, poly))
+    gram2, poly2, xn2 = (t.double().numpy() for t in _torch_products(x, oracle.MUON_NS_COEFFS))
+    slips = {
+        "A A rounded before scaling": (r(b * gram2 + r(c * r(gram2 @ gram2))), poly2),
+        "b A rounded before the sum": (r(r(b * gram2) + c * (gram2 @ gram2)), poly2),
+        "B X rounded before a X is added": (r(r(a * xd) + r(poly2 @ xd)), xn2),
+    }
+    for what, (got, ref) in slips.items():
+        frac = np.count_nonzero(got != ref) / got.size
+        assert frac > 10 * FLIP_FRACTION, (what, frac)
+
+
+@pytest.mark.parametrize("rows,cols", [(64, 256), (256, 64), (96, 96), (40, 1000)])
+def test_ns_one_iteration_matches_torch(rows, cols):
+    """From the float32 input on: orientation, bfloat16 norm, division, one iteration."""
+    rng = np.random.default_rng(rows + 3 * cols)
+    u = rng.standard_normal((rows, cols)).astype(np.float32)
+    got = oracle.newton_schulz(u, rows, cols, steps=1)
+    ref = torch_newton_schulz(torch.from_numpy(u), oracle.MUON_NS_COEFFS, 1,
+                              oracle.MUON_EPS).double().numpy()
+    assert got.shape == ref.shape
+    m, n = min(rows, cols), max(rows, cols)
+    x = oracle.ns_normalise(u, rows, cols)
+    gram = oracle.ns_gram(x)
+    a, b, c = oracle.MUON_NS_COEFFS
+    poly = oracle.ns_poly(gram, b, c)
+    mag = abs(a) * np.abs(x) + np.abs(poly) @ np.abs(x)
+    _check_product(got if rows <= cols else got.T, ref if rows <= cols else ref.T,
+                   (1 + 8 * m * 2.0 ** -7) * mag, n, "iteration")
+
+
+@pytest.mark.parametrize("rows,cols", [(64, 256), (256, 64), (96, 96), (200, 600), (48, 1000)])
+def test_ns_five_iterations_match_torch(rows, cols):
+    """Muon's default five iterations: the rare flips of each product spread through the
+    later products, so the results differ in many elements, but only by the amount that
+    float32 accumulation order alone produces (torch against itself on a column-permuted
+    input reaches 0.47 % in Frobenius norm and 1.6 % of the largest entry on 200 x 600)."""
+    rng = np.random.default_rng(rows * cols)
+    u = rng.standard_normal((rows, cols)).astype(np.float32)
+    got = oracle.newton_schulz(u, rows, cols)
+    ref = torch_newton_schulz(torch.from_numpy(u), oracle.MUON_NS_COEFFS, 5,
+                              oracle.MUON_EPS).double().numpy()
+    fro = np.sqrt(np.sum((got - ref) ** 2) / np.sum(ref ** 2))
+    assert fro <= 1e-2, fro
+    assert np.abs(got - ref).max() <= 3e-2 * np.abs(ref).max()
+    assert np.all(got == oracle.to_bf16(got))
