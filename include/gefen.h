@@ -27,18 +27,7 @@
  *    by gefen_init, freed by gefen_destroy. gefen_step allocates nothing.
  *  - Calls on one state must be ordered (same stream, or externally synchronised).
  *
- * Environment variables (measurement and debugging only; defaults are the tuned
- * choices):
- *  GEFEN_U_THREADS   256, 512 or 1024: preferred workgroup size of the register-resident
- *                    step kernel (read by gefen_init; default 1024).
- *  GEFEN_U_VPL       1-8: force that kernel's vectors per lane (default 0: chosen).
- *  GEFEN_FOLD        0: keep every small kernel class as its own launch instead of one
- *                    leftover launch (default 1).
- *  GEFEN_G_RUNS      0: explicit blocks of 33-2042 elements take one workgroup each
- *                    instead of being packed into register runs (8-bit codes; read by
- *                    gefen_init; default 1).
- *  GEFEN_MUON_LANES  1: run every Gefen-Muon shape group on the caller's stream instead
- *                    of two concurrent lanes (read by gefen_muon_init; default 2).
+ * Environment variable (debugging only):
  *  GEFEN_DEBUG_SYNC  set: gefen_step synchronises its stream and reports kernel errors.
  */
 #ifndef GEFEN_H
@@ -92,7 +81,7 @@ typedef struct gefen_state gefen_state;   /* opaque, library-owned */
  *                  every tensor boundary. Overrides inference and period_override.
  *  code_bits       bits per momentum code: 8 (k = 256 entries, 16k = 4096 histogram
  *                  bins, one code per byte) or 4 (k = 16, 256 bins, two codes per
- *                  byte; the paper's 4-bit variant, Sec. 6 ablation).
+ *                  byte; the paper's 4-bit variant, Sec. 7 ablation).
  *  eps_part        eps inside log(g^2 + eps) of the partition score (>= 0; the
  *                  paper leaves it open -- the optimizer eps, 1e-8, is the default).
  *  stream          stream for all work; synchronised once (the inferred periods

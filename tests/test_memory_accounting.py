@@ -59,8 +59,14 @@ def test_llama3_state_sizes():
     assert g["llama3_1p5b_adamw"][1] == "GiB"
     assert round(adamw / 2**30, 1) == g["llama3_1p5b_adamw"][0]
     gefen = gefen_persistent_bytes(w)
-    assert g["llama3_1p5b_gefen"][1] == "GB"
-    assert round(gefen / 1e9, 1) == g["llama3_1p5b_gefen"][0]
+    printed, unit = g["llama3_1p5b_gefen"]
+    assert unit == "GiB"
+    # Recorded discrepancy: the paper prints 1.5 GiB, the layout holds 1.40 GiB. The
+    # printed figure is the byte count in decimal gigabytes (1.50 GB); no reading of the
+    # state (one byte per parameter, 8 bytes per block) reaches 1.5 GiB.
+    assert round(gefen / 2**30, 2) == 1.40
+    assert round(gefen / 1e9, 1) == printed
+    assert round(gefen / 2**30, 1) != printed
     assert 7.9 < adamw / gefen < 8.0
 
 
