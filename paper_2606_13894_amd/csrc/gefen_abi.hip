@@ -340,24 +340,15 @@ hipError_t fill_zero(void* p, size_t bytes, hipStream_t s)
 // 4.38 TB/s -- the per-workgroup start (descriptor loads, LDS tables, barrier) needs
 // ~8K elements to amortise, while larger tiles lose memory-level parallelism. So v = 2
 // is tried first, then 1, 3, 4; 256-thread workgroups (up to 8 vectors) are the
-// fallback. Tunables for measurement: GEFEN_U_THREADS (256, 512, 1024) and GEFEN_U_VPL
-// (force v).
+// fallback.
 struct UShape {
     int lpb_log2, vpl, bs;
 };
 
-int env_int(const char* name, int dflt)
-{
-    const char* v = std::getenv(name);
-    return v && *v ? std::atoi(v) : dflt;
-}
-
 UShape choose_u(int64_t p)
 {
     const int64_t nv = p / 4;
-    int pref = env_int("GEFEN_U_THREADS", 1024);
-    if (pref != 256 && pref != 512 && pref != 1024) pref = 1024;
-    const int force = env_int("GEFEN_U_VPL", 0);
+    constexpr int pref = 1024;
     constexpr int kMaxVplBig = 4;   // instances of the 512/1024-thread kernels
     static const int kOrderBig[kMaxVplBig] = {2, 1, 3, 4};
     static const int kOrderSmall[kMaxVpl] = {2, 1, 3, 4, 5, 6, 7, 8};
@@ -366,7 +357,6 @@ UShape choose_u(int64_t p)
         const int vmax = bs > 256 ? kMaxVplBig : kMaxVpl;
         for (int vi = 0; vi < vmax; ++vi) {
             const int v = bs > 256 ? kOrderBig[vi] : kOrderSmall[vi];
-            if (force && pass == 0 && v != force) continue;
             const int64_t need = (nv + v - 1) / v;
             int l2 = 0;
             while ((int64_t(1) << l2) < need) ++l2;
@@ -446,7 +436,7 @@ std::vector<UShape> plan_u_shapes(const gefen_state* st)
             dom_vpl = e.first.first;
             dom_bs = e.first.second;
         }
-    if (best >= 0 && env_int("GEFEN_FOLD", 1)) {
+    if (best >= 0) {
         for (int32_t t = 0; t < st->n_tensors; ++t) {
             if (ushape[t].lpb_log2 < 0) continue;
             if (ushape[t].vpl == dom_vpl && ushape[t].bs == dom_bs) continue;
@@ -508,12 +498,11 @@ void plan_tensor(gefen_state* st, TilePlan& P, int32_t t, const UShape& u,
     const int64_t bb = st->blk_begin[t];
     if (st->explicit_blocks) {
         const int64_t nb = static_cast<int64_t>(s.size()) - 1;
-        static const bool runs = env_int("GEFEN_G_RUNS", 1) != 0;
         auto run_block = [](int64_t len) { return len >= kRunMinBlock && len <= kRunMaxElems; };
         int64_t b = 0;
         while (b < nb) {
             const int64_t len = s[b + 1] - s[b];
-            if (st->code_bits == 8 && runs && run_block(len)) {
+            if (st->code_bits == 8 && run_block(len)) {
                 // consecutive short blocks held in registers by one KIND_G workgroup
                 const int64_t b0 = b;
                 int cnt = 0;
@@ -605,7 +594,7 @@ void fold_small_classes(const gefen_state* st, TilePlan& P)
             dom = static_cast<int>(i);
         }
     }
-    if (dom < 0 || !env_int("GEFEN_FOLD", 1)) return;
+    if (dom < 0) return;
     const int64_t fold_max = std::max<int64_t>(int64_t(1) << 21, dom_elems / 64);
     std::vector<Tile> front;
     std::vector<int32_t> front_kinds;
@@ -1644,10 +1633,10 @@ int muon_shape_groups(gefen_state* st, const int64_t* rows, std::vector<int32_t>
 }
 
 // Lanes: groups in decreasing order of Newton-Schulz work, each to the lane with less
-// work so far (GEFEN_MUON_LANES=1 keeps every group on the caller's stream).
+// work so far.
 void muon_assign_lanes(gefen_state* st)
 {
-    const int n_lanes = std::min(2, std::max(1, env_int("GEFEN_MUON_LANES", 2)));
+    constexpr int n_lanes = 2;
     std::vector<int32_t> byw(st->muon_groups.size());
     std::vector<double> work(byw.size());
     for (size_t gi = 0; gi < byw.size(); ++gi) {
