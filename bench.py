@@ -21,7 +21,8 @@ Prints one JSON line. ``roofline`` describes the dominant kernel class: algorith
 bytes per launch over its mean launch time, from HIP events recorded on the step's
 stream. ``traffic`` comes from committed rocprofv3 counter summaries when they were
 taken on the current kernel source, else null. ``cpu_baseline`` is the float64 oracle
-(single thread, as it stands) timed on a bounded sample of the same workload.
+(as it stands) timed on a bounded sample of the same workload, over one process per
+available core (at most 16), with the one-core rate beside it.
 """
 from __future__ import annotations
 
@@ -62,12 +63,12 @@ def read_traffic(workload: str, kind: str, vpl: int, gdt: str, code_bits: int = 
     return None if ent is None else ent.get("bytes_per_launch")
 
 
-def cpu_baseline(w, params, grads, st, sample_elems: int):
-    """Time the oracle's step on a bounded sample: whole blocks taken from the start
-    of every tensor in turn until `sample_elems` elements are covered."""
+def _baseline_jobs(w, params, grads, st, sample_elems: int):
+    """A bounded sample of the workload for the oracle: whole blocks from the start of
+    every tensor in turn (largest first) until `sample_elems` elements are covered, with
+    the state the GPU holds for them. Each job is (theta, grad bits, codes, s, v, block
+    offsets relative to the job)."""
     import numpy as np
-    import torch
-    import oracle
     import paper_2606_13894_amd as gf
     sys.path.insert(0, os.path.join(ROOT, "tests"))
     from parity import grad_bits, unpack_codes
@@ -77,7 +78,10 @@ def cpu_baseline(w, params, grads, st, sample_elems: int):
     codes = unpack_codes(st.read(gf.STATE_CODES).cpu().numpy(), st.k)
     scale = st.read(gf.STATE_SCALE).cpu().numpy().astype(np.float64)
     vm = st.read(gf.STATE_V).cpu().numpy().astype(np.float64)
-    cb = st.read(gf.STATE_CB_DEC).cpu().numpy().astype(np.float64)
+    explicit = None
+    if any(p == 0 for p in periods):
+        import workloads as W
+        explicit = W.stress_block_offsets(w.numel, w.n_blocks)
     jobs = []
     left = sample_elems
     order = sorted(range(len(params)), key=lambda i: -params[i].numel())
@@ -85,26 +89,141 @@ def cpu_baseline(w, params, grads, st, sample_elems: int):
     for i in order:
         if left <= 0:
             break
-        p = periods[i] if periods[i] > 0 else params[i].numel()
-        take = min(params[i].numel(), max(p, (min(per_tensor, left) // p) * p))
-        nb = take // p
+        want = min(per_tensor, left)
+        if periods[i] > 0:
+            p = periods[i]
+            take = min(params[i].numel(), max(p, (want // p) * p))
+            offs = np.arange(0, take + 1, p, dtype=np.int64)
+        else:
+            # explicit blocks (one tensor spans the whole table): the first whole blocks
+            nb = int(np.searchsorted(explicit, want, side="right")) - 1
+            nb = max(1, nb)
+            offs = np.ascontiguousarray(explicit[:nb + 1], dtype=np.int64)
+            take = int(offs[-1])
+        nb = offs.size - 1
         th = params[i].detach().reshape(-1)[:take].double().cpu().numpy()
         g = grad_bits(grads[i].reshape(-1)[:take])
         c0 = lay["code_offsets"][i]
         b0 = lay["block_index"][i]
         jobs.append((th, g, codes[c0:c0 + take].copy(), scale[b0:b0 + nb].copy(),
-                     vm[b0:b0 + nb].copy(), np.arange(0, take + 1, p, dtype=np.int64)))
+                     vm[b0:b0 + nb].copy(), offs))
         left -= take
+    return jobs
+
+
+def _cpu_worker(job_dir: str, idx: int):
+    """--cpu-worker: run the oracle's step over this worker's share of the sample
+    (disjoint whole-block ranges written by cpu_baseline), write the results back and
+    print the wall-clock interval of the oracle calls. Touches no GPU."""
+    import numpy as np
+    import oracle
+    with open(os.path.join(job_dir, "hp.json")) as f:
+        hp = json.load(f)
+    cb = np.load(os.path.join(job_dir, "cb.npy"))
+    pieces = hp["shares"][idx]
+    arrays = []
+    for name in pieces:
+        base = os.path.join(job_dir, name)
+        arrays.append([np.load(f"{base}.{k}.npy") for k in ("th", "g", "c", "s", "v", "o")])
+    t0 = time.time()
+    for th, g, c, s_, v, o in arrays:
+        oracle.step_blocks(th, g, c, s_, v, o, cb, cb, hp["lr"], hp["b1"], hp["b2"], hp["eps"],
+                           hp["wd"], hp["t"])
+    t1 = time.time()
+    for name, (th, g, c, s_, v, o) in zip(pieces, arrays):
+        np.save(os.path.join(job_dir, f"{name}.out.npy"), th)
+    print(json.dumps({"t0": t0, "t1": t1, "elems": int(sum(a[0].size for a in arrays))}),
+          flush=True)
+
+
+def time_oracle(jobs, cb, hp: dict, ncpu: int):
+    """Time the oracle's step over `jobs` (see _baseline_jobs) once on one core and once
+    over disjoint whole-block ranges in `ncpu` worker processes, each running the same
+    oracle routine. The all-core parameters must equal the one-core ones bit for bit.
+    Returns (elements, all-core seconds, one-core seconds, pieces, processes)."""
+    import shutil
+    import subprocess
+    import tempfile
+    import numpy as np
+    import oracle
+
     n = sum(j[0].size for j in jobs)
-    t0 = time.perf_counter()
-    for th, g, cq, s, v, offs in jobs:
-        oracle.step_blocks(th, g, cq, s, v, offs, cb, cb, w.lr, w.betas[0], w.betas[1], w.eps,
-                           w.wd, 5)
-    dt = time.perf_counter() - t0
-    return {"value": n / dt / 1e9, "unit": "Gparams/s", "cores": 1, "kind": "oracle",
-            "sample": f"oracle step (float64, single thread) on {n} of {w.numel} elements: "
-                      f"whole blocks from the start of the {len(jobs)} largest tensors",
-            "seconds": dt, "host": host_cpu()}
+    job_dir = tempfile.mkdtemp(prefix="gefen_cpu_", dir="/dev/shm" if os.path.isdir("/dev/shm")
+                               else None)
+    try:
+        np.save(os.path.join(job_dir, "cb.npy"), cb)
+        pieces = []   # (name, job index, first element, end element, size)
+        target = max(1, n // (4 * ncpu))
+        for ji, (th, g, c, s_, v, offs) in enumerate(jobs):
+            b = 0
+            nb = offs.size - 1
+            while b < nb:
+                e = int(np.searchsorted(offs, offs[b] + target, side="right")) - 1
+                e = min(nb, max(b + 1, e))
+                lo, hi = int(offs[b]), int(offs[e])
+                name = f"j{ji}_b{b}"
+                base = os.path.join(job_dir, name)
+                for k, a in (("th", th[lo:hi]), ("g", g[lo:hi]), ("c", c[lo:hi]),
+                             ("s", s_[b:e]), ("v", v[b:e]), ("o", offs[b:e + 1] - lo)):
+                    np.save(f"{base}.{k}.npy", np.ascontiguousarray(a))
+                pieces.append((name, ji, lo, hi, hi - lo))
+                b = e
+        shares = [[] for _ in range(ncpu)]
+        load = [0] * ncpu
+        for name, _, _, _, sz in sorted(pieces, key=lambda q: -q[4]):
+            k = load.index(min(load))
+            shares[k].append(name)
+            load[k] += sz
+        with open(os.path.join(job_dir, "hp.json"), "w") as f:
+            json.dump(dict(hp, shares=shares), f)
+        procs = [subprocess.Popen([sys.executable, os.path.abspath(__file__), "--cpu-worker",
+                                   job_dir, str(k)], stdout=subprocess.PIPE, text=True)
+                 for k in range(ncpu) if shares[k]]
+        outs = [p.communicate()[0] for p in procs]
+        if any(p.returncode for p in procs):
+            raise RuntimeError("an oracle worker failed")
+        spans = [json.loads(o.strip().splitlines()[-1]) for o in outs]
+        par_dt = max(x["t1"] for x in spans) - min(x["t0"] for x in spans)
+        if sum(x["elems"] for x in spans) != n:
+            raise RuntimeError("the workers did not cover the sample")
+
+        t0 = time.perf_counter()
+        for th, g, c, s_, v, offs in jobs:
+            oracle.step_blocks(th, g, c, s_, v, offs, cb, cb, hp["lr"], hp["b1"], hp["b2"],
+                               hp["eps"], hp["wd"], hp["t"])
+        one_dt = time.perf_counter() - t0
+        for name, ji, lo, hi, _ in pieces:
+            got = np.load(os.path.join(job_dir, f"{name}.out.npy"))
+            if not np.array_equal(got, jobs[ji][0][lo:hi]):
+                raise RuntimeError("the all-core oracle run differs from the one-core run")
+    finally:
+        shutil.rmtree(job_dir, ignore_errors=True)
+    return n, par_dt, one_dt, len(pieces), len(procs)
+
+
+def cpu_baseline(w, params, grads, st, sample_elems: int, t: int):
+    """The oracle's step (float64, as it stands) on a bounded sample of the workload, on
+    one core and on every available core (at most 16 processes). The rate is the
+    sample's, extrapolated to the workload (the step costs the same per element
+    everywhere)."""
+    import numpy as np
+    import paper_2606_13894_amd as gf
+
+    jobs = _baseline_jobs(w, params, grads, st, sample_elems)
+    cb = st.read(gf.STATE_CB_DEC).cpu().numpy().astype(np.float64)
+    hp = {"lr": w.lr, "b1": w.betas[0], "b2": w.betas[1], "eps": w.eps, "wd": w.wd, "t": t}
+    ncpu = min(16, host_cpu()["cpus_available"] or 1)
+    n, par_dt, one_dt, npieces, nproc = time_oracle(jobs, cb, hp, ncpu)
+    kind = ("explicit blocks from the start of the block table" if any(
+        p == 0 for p in st.periods) else f"whole blocks from the start of the {len(jobs)} "
+        "largest tensors")
+    return {"value": n / par_dt / 1e9, "unit": "Gparams/s", "cores": nproc, "kind": "oracle",
+            "sample": f"oracle step (float64) on {n} of {w.numel} elements ({kind}), "
+                      f"{npieces} disjoint block ranges over {nproc} processes; "
+                      "rate extrapolated from the sample",
+            "seconds": par_dt,
+            "single_thread": {"value": n / one_dt / 1e9, "cores": 1, "seconds": one_dt},
+            "host": host_cpu()}
 
 
 def host_cpu():
@@ -333,6 +452,9 @@ def mix_ceiling(torch, gf, dev, grad_dtype: str, n: int = 1_500_000_000, reps: i
 
 
 def main():
+    if len(sys.argv) == 4 and sys.argv[1] == "--cpu-worker":
+        _cpu_worker(sys.argv[2], int(sys.argv[3]))
+        return
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
@@ -492,7 +614,8 @@ def main():
         line["adamw"] = adamw_comparator(torch, w, params, grads, min(args.steps, 20),
                                          persistent, persistent + workspace, ms_per_step)
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(w, params, grads[t % 2], st, args.cpu_sample_elems)
+        line["cpu_baseline"] = cpu_baseline(w, params, grads[t % 2], st, args.cpu_sample_elems,
+                                            t + 1)
     print(json.dumps(line), flush=True)
 
 

@@ -43,3 +43,31 @@ def test_newton_schulz_flops_of_gpt2_small():
     per_iter = sum(4 * min(a, b) ** 2 * max(a, b) + 2 * min(a, b) ** 3 for a, b in mats)
     per_iter += sum(4 * n + 2 for n in vecs)
     assert bench.muon_ns_flops(W.get("gpt2_125m"), 5) == 5 * per_iter
+
+
+def test_all_core_oracle_baseline_equals_one_core():
+    """The all-core CPU baseline deals disjoint whole-block ranges to worker processes
+    that run the unchanged oracle; their parameters must equal the one-core run's bit
+    for bit (time_oracle raises otherwise), and every element is counted once."""
+    import numpy as np
+    import oracle
+    rng = np.random.default_rng(5)
+    h = np.zeros(4096, dtype=np.uint64)
+    g0 = rng.standard_normal(4096).astype(np.float32)
+    oracle.histogram_uniform(g0, 64, 4096, h)
+    cb, _, _, _ = oracle.dp_codebook(h, 256)
+    jobs = []
+    for p, nb in ((64, 300), (100, 7), (1, 50)):
+        n = p * nb
+        jobs.append((rng.standard_normal(n) * 0.02, rng.standard_normal(n).astype(np.float32),
+                     rng.integers(0, 256, n).astype(np.uint8), rng.uniform(0, 1, nb),
+                     rng.uniform(0, 1, nb), np.arange(0, n + 1, p, dtype=np.int64)))
+    ref = [j[0].copy() for j in jobs]
+    for (th0, g, c, s, v, offs), r in zip([tuple(a.copy() for a in j) for j in jobs], ref):
+        oracle.step_blocks(r, g, c, s, v, offs, cb, cb, 1e-3, 0.9, 0.999, 1e-8, 0.1, 3)
+    hp = {"lr": 1e-3, "b1": 0.9, "b2": 0.999, "eps": 1e-8, "wd": 0.1, "t": 3}
+    n, par_dt, one_dt, pieces, procs = bench.time_oracle(jobs, cb, hp, 3)
+    assert n == sum(j[0].size for j in jobs)
+    assert procs == 3 and pieces >= 3 and par_dt > 0 and one_dt > 0
+    for j, r in zip(jobs, ref):
+        np.testing.assert_array_equal(j[0], r)
