@@ -24,6 +24,7 @@ from __future__ import annotations
 import numpy as np
 import torch
 
+import gates
 import oracle
 import paper_2606_13894_amd as gf
 
@@ -112,65 +113,16 @@ class Run:
         return ref
 
     def check(self, pre, post, ref, grads, lr, betas, eps, wd, t, where=""):
-        """Apply the gates; returns a small report, raises AssertionError on a breach."""
-        b1 = betas[0]
-        rep = {"code_ties": 0, "codes": 0, "max_rel_theta": 0.0, "max_theta_gate": 0.0,
-               "max_rel_v": 0.0}
-        cb = pre["cb_enc"]
+        """Apply the gates (tests/gates.py) to every tensor; returns a small report,
+        raises AssertionError on a breach."""
+        rep = gates.empty_report()
         for i in range(len(self.params)):
-            offs = self.offsets[i]
-            sizes = np.diff(offs)
-            g = np.abs(grad_f64(grads[i]))
-            gmax = np.maximum.reduceat(g, offs[:-1]) if g.size else g
-            s_prev = pre["s"][i]
-            s_ref, s_gpu = ref["s"][i], post["s"][i]
-            floor = b1 * s_prev + (1 - b1) * gmax
-            bad = np.abs(s_gpu - s_ref) > 1e-6 * s_ref + 1e-6 * floor
-            assert not bad.any(), f"{where} tensor {i}: scale mismatch at blocks {np.nonzero(bad)[0][:5]}"
-            v_ref, v_gpu = ref["v"][i], post["v"][i]
-            relv = np.abs(v_gpu - v_ref) / np.maximum(np.abs(v_ref), 1e-300)
-            relv[(v_ref == 0) & (v_gpu == 0)] = 0.0
-            rep["max_rel_v"] = max(rep["max_rel_v"], float(relv.max(initial=0.0)))
-            assert (relv <= 4e-6).all(), f"{where} tensor {i}: v mismatch {relv.max()}"
-            # codes
-            c_ref, c_gpu = ref["codes"][i].astype(np.int64), post["codes"][i].astype(np.int64)
-            diff = c_ref != c_gpu
-            rep["codes"] += c_ref.size
-            if diff.any():
-                idx = np.nonzero(diff)[0]
-                blk = np.searchsorted(offs, idx, side="right") - 1
-                sr = s_ref[blk]
-                assert (sr > 0).all(), f"{where} tensor {i}: code differs in a zero-scale block"
-                x = ref["m"][i][idx] / sr
-                a = np.minimum(c_ref[idx], c_gpu[idx])
-                bb = np.maximum(c_ref[idx], c_gpu[idx])
-                assert (bb - a == 1).all(), f"{where} tensor {i}: non-adjacent code mismatch"
-                midp = 0.5 * (cb[a] + cb[bb])
-                delta = 1e-6 * np.maximum(1.0, floor[blk] / sr)
-                ok = np.abs(x - midp) <= delta
-                assert ok.all(), (f"{where} tensor {i}: {int((~ok).sum())} code mismatches "
-                                  f"outside the tie window (first at {idx[~ok][:3]})")
-                rep["code_ties"] += int(idx.size)
-            # parameters
-            th_ref, th_gpu = ref["theta"][i], post["theta"][i]
-            elem_blk = np.repeat(np.arange(sizes.size), sizes)
-            dq = pre["cb_dec"][pre["codes"][i].astype(np.int64)] * s_prev[elem_blk]
-            terms = b1 * np.abs(dq) + (1 - b1) * g
-            bc1 = 1.0 - b1 ** t
-            vhat = v_ref[elem_blk] / (1.0 - betas[1] ** t)
-            u_scale = terms / bc1 / (np.sqrt(vhat) + eps) + abs(wd) * np.abs(pre["theta"][i])
-            gate = 1e-5 * np.abs(th_ref) + 1e-5 * abs(lr) * u_scale + 1e-30
-            err = np.abs(th_gpu - th_ref)
-            ratio = err / gate
-            rep["max_theta_gate"] = max(rep["max_theta_gate"], float(ratio.max(initial=0)))
-            rel = err / np.maximum(np.abs(th_ref), 1e-30)
-            rep["max_rel_theta"] = max(rep["max_rel_theta"], float(rel.max(initial=0)))
-            if not (err <= gate).all():
-                j = int(ratio.argmax())
-                raise AssertionError(
-                    f"{where} tensor {i}: theta gate exceeded ({ratio[j]:.3g}x) at element {j}: "
-                    f"theta_pre={pre['theta'][i][j]:.9g} ref={th_ref[j]:.9g} gpu={th_gpu[j]:.9g} "
-                    f"m_ref={ref['m'][i][j]:.6g} terms={terms[j]:.6g} u_scale={u_scale[j]:.6g}")
+            gates.merge(rep, gates.check_tensor(
+                pre["theta"][i], pre["codes"][i], pre["s"][i],
+                post["theta"][i], post["codes"][i], post["s"][i], post["v"][i],
+                ref["theta"][i], ref["codes"][i], ref["s"][i], ref["v"][i], ref["m"][i],
+                grad_f64(grads[i]), self.offsets[i], pre["cb_dec"], pre["cb_enc"],
+                lr, betas, eps, wd, t, f"{where} tensor {i}"))
         return rep
 
     def teacher_forced_step(self, grads, lr, betas, eps, wd, t, where=""):
