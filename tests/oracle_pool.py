@@ -71,14 +71,17 @@ def run(job_dir: str, meta: dict, tasks: list, sizes: list, nproc: int, timeout:
              for k in range(len(shares))]
     results = []
     errors = []
-    t_end = time.time() + timeout
-    for p in procs:
+    t0 = time.time()
+    t_end = t0 + timeout
+    for k, p in enumerate(procs):
         try:
             out, err = p.communicate(timeout=max(1.0, t_end - time.time()))
         except subprocess.TimeoutExpired:
             for q in procs:
                 q.kill()
             raise RuntimeError("oracle workers timed out")
+        print(f"  oracle worker {k + 1}/{len(procs)} done after {time.time() - t0:.1f} s",
+              flush=True)
         if p.returncode != 0:
             errors.append(err[-2000:])
             continue
