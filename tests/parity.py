@@ -3,18 +3,9 @@
 Test infrastructure. Before every step the oracle is loaded with the library's state
 after the previous step (parameters, codes, scales, second moments, both codebooks,
 widened exactly to float64), gets the same gradient bits, and every output of the
-step is compared element by element:
-
-* codes: equal, or adjacent where the oracle's x = m / s' lies within
-  delta = 1e-6 * max(1, (beta1*s + (1-beta1)*max|g|) / s') of the two entries' midpoint
-  (a tie decided by fp32 rounding);
-* scale s': |diff| <= 1e-6 * s' + 1e-6 * (beta1*s + (1-beta1)*max|g|);
-* second moment v': relative error <= 4e-6 (fp32 tree sum of up to 2^16 terms);
-* parameters: |diff| <= 1e-5 * |theta_ref| + 1e-5 * lr * u_scale, where u_scale is the
-  magnitude of the update's operands, (beta1*|c[q]*s| + (1-beta1)*|g|) / (1 - beta1^t)
-  / (sqrt(v_hat) + eps) + wd*|theta| >= |u_ref|: relative 1e-5 in fp32, with a floor
-  for parameters near zero and for momenta that cancel (the fp32 error of
-  m = beta1*c[q]*s + (1-beta1)*g is relative to its summands, not to m).
+step is compared element by element with the gates of tests/gates.py (codes equal up
+to ties decided by rounding, scales and second moments to 1e-6 and 4e-6 relative,
+parameters to 1e-5 relative with floors for values near zero and cancelled momenta).
 
 Teacher forcing is needed because a legitimate tie flip changes the next momentum by a
 codebook gap times the scale, which a free-running comparison would accumulate.

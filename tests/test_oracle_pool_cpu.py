@@ -95,3 +95,41 @@ def test_pool_partition_tasks(tmp_path):
         _, scores, per = oracle.partition(gi, 1e-8)
         assert r["result"]["period"] == per
         np.testing.assert_array_equal(np.array(r["result"]["scores"]), scores)
+
+
+def test_code_gate_accepts_rounding_ties_and_refuses_other_codes():
+    """The code gate of tests/gates.py: a block of one element whose momentum cancels
+    exactly in real arithmetic (bf16 gradients, g_2 = -0.9 g_1, beta1 = 0.9) holds
+    rounding noise on both sides, so either end code is a tie; a far code for a
+    well-conditioned element is refused."""
+    import gates
+    import pytest
+    cb = np.linspace(-1.0, 1.0, 256)
+    b1 = 0.9
+    g1, g2 = 0.205078125, -0.1845703125          # bf16 values, g2 = -0.9 g1 exactly
+    s_pre = np.array([abs(np.float32(0.1) * np.float32(g1))], dtype=np.float64)
+    codes_pre = np.array([255], dtype=np.uint8)
+    th = np.array([0.5])
+    cq, s, v = codes_pre.copy(), s_pre.copy(), np.array([0.01])
+    m = np.zeros(1)
+    offs = np.array([0, 1], dtype=np.int64)
+    g = np.array([g2], dtype=np.float32)
+    oracle.step_blocks(th, g, cq, s, v, offs, cb, cb, 1e-3, b1, 0.999, 1e-8, 0.0, 2, m_out=m)
+    assert abs(m[0]) < 1e-15                      # float64 noise of an exact zero
+    post_codes = np.array([255 - int(cq[0])], dtype=np.uint8)   # the other end
+    post_s = np.array([1e-10])
+    args = (np.array([0.5]), codes_pre, s_pre, th.copy(), post_codes, post_s, v.copy(),
+            th, cq, s, v, m, g.astype(np.float64), offs, cb, cb, 1e-3, (b1, 0.999), 1e-8,
+            0.0, 2)
+    rep = gates.check_tensor(*args)
+    assert rep["code_ties"] == 1
+    # a well-conditioned element: a code two entries away is refused
+    g = np.array([0.3], dtype=np.float32)
+    th = np.array([0.5])
+    cq, s, v, m = codes_pre.copy(), s_pre.copy(), np.array([0.01]), np.zeros(1)
+    oracle.step_blocks(th, g, cq, s, v, offs, cb, cb, 1e-3, b1, 0.999, 1e-8, 0.0, 2, m_out=m)
+    bad = np.array([int(cq[0]) - 2], dtype=np.uint8)
+    with pytest.raises(AssertionError, match="outside the tie window"):
+        gates.check_tensor(np.array([0.5]), codes_pre, s_pre, th.copy(), bad, s.copy(),
+                           v.copy(), th, cq, s, v, m, g.astype(np.float64), offs, cb, cb,
+                           1e-3, (b1, 0.999), 1e-8, 0.0, 2)
