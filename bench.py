@@ -359,8 +359,9 @@ def bench_muon(args, torch, w, dev):
         "phases_ms": {"codec": round(codec_ms, 4), "orthogonalise_update": round(ortho_ms, 4)},
         "roofline": {"bound": "mfma", "achieved": None, "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": None, "traffic": None,
-                     "kernel": "Newton-Schulz bf16 GEMMs (rocBLAS), timed with the normalise "
-                               "and update kernels around them (wall time of that phase)",
+                     "kernel": "Newton-Schulz bf16 matrix-core products (k_ns_gemm), timed "
+                               "with the prep and update kernels around them (wall time of "
+                               "that phase)",
                      "flops_per_step": flops},
         "codec": {"bytes_per_step": codec_bytes,
                   "gbps": round(codec_bytes / (codec_ms * 1e-3) / 1e9, 1)},

@@ -255,12 +255,13 @@ int gefen_profile_end(gefen_state* st, int32_t cap, int32_t* n_classes, int32_t*
  * explicit blocks) for gefen_muon_step.
  *  rows    host int64[n_tensors]: tensor i is the rows[i] x (numel_i / rows[i]) matrix,
  *          row-major (a 1-D tensor is 1 x numel). rows[i] must divide numel_i.
- * Allocates the bfloat16 momentum matrix (2 bytes per parameter), the Newton-Schulz
- * buffers for the largest group of equal-shape tensors, and a rocBLAS handle whose
- * workspace is sized here; synchronises `stream`. Call once per state. Tensors of one
- * shape are orthogonalised together; a shape group of more than 2^27 elements is
- * refused (EINVAL).
- * Errors: EINVAL (NULL, count mismatch, rows, second call, group size), ENOMEM, EHIP.
+ * Allocates the bfloat16 momentum matrix (2 bytes per parameter) and the Newton-Schulz
+ * buffers of each of two lanes, sized for the lane's largest group of tensors that share
+ * one wide shape (X and X^T twice, the two m x m products: about 8 bytes per element of
+ * that group), and checks every matrix product of the steps against them on the host;
+ * synchronises `stream`. Call once per state.
+ * Errors: EINVAL (NULL, count mismatch, rows, second call, a matrix side above
+ * 2^31 - 4096), ENOMEM, EHIP.
  * ---------------------------------------------------------------------------- */
 int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, void* stream);
 
@@ -272,10 +273,9 @@ int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, voi
  *   U = nesterov ? (1 - mu) * G + mu * M : M, rounded to bfloat16
  *   X = bf16(U / max(bf16(||U||_F), bf16(ns_eps))), transposed if rows > cols
  *   ns_steps times: A = X X^T; B = ns_b A + ns_c A A; X = ns_a X + B X
- *       (bfloat16 matrices, float32 accumulation, as Muon's PyTorch implementation)
+ *       (bfloat16 matrices, float32 accumulation, each product rounded once, as Muon's
+ *       PyTorch implementation; the library's own matrix-core kernels)
  *   theta = theta * (1 - lr * weight_decay) - lr * sqrt(max(1, rows / cols)) * X^(T)
- * (The transpose is mathematical only: X lives in the tensor's own row-major layout,
- * which the column-major matrix products read as X or X^T.)
  *  params, grads  as for gefen_step; momentum in [0, 1); ns_steps in [0, 100];
  *  ns_eps > 0. Muon's defaults: ns_steps 5, (ns_a, ns_b, ns_c) =
  *  (3.4445, -4.7750, 2.0315), ns_eps 1e-7, nesterov 1.
@@ -299,6 +299,24 @@ int gefen_muon_step(gefen_state* st, const gefen_tensor* params, const gefen_ten
  * milliseconds, from HIP events on the step's stream; then disarms like
  * gefen_profile_end. Errors: EINVAL (NULL), EHIP. */
 int gefen_muon_profile_end(gefen_state* st, int32_t* steps, double* codec_ms, double* ortho_ms);
+
+/* ------------------------------------------------------------------------------
+ * gefen_newton_schulz -- Muon's orthogonalisation iterations (appendix "Gefen-Muon"),
+ * the matrix-product part of gefen_muon_step on its own: `steps` times
+ *   A = X X^T;  B = b A + c A A;  X = a X + B X
+ * on each of `batch` wide bfloat16 matrices, every product rounded once to bfloat16 from
+ * float32 accumulation (the same kernels as gefen_muon_step). No normalisation: x_in is
+ * the first iteration's input.
+ *  x_in   device uint16[batch * m * n]: bfloat16 bit patterns, matrix b row-major m x n
+ *         at x_in + b * m * n, 1 <= m <= n <= 2^31 - 4096, batch in [1, 65535].
+ *  x_out  device uint16[batch * m * n], same layout; may equal x_in.
+ *  steps  in [0, 100] (0 copies x_in to x_out); a, b, c finite.
+ * Asynchronous on `stream`; its workspace (about 8 bytes per element of the batch) is
+ * allocated and freed stream-ordered on `stream`.
+ * Errors: EINVAL (NULL, sizes, steps, coefficients), ENOMEM, EHIP.
+ * ---------------------------------------------------------------------------- */
+int gefen_newton_schulz(const uint16_t* x_in, uint16_t* x_out, int32_t batch, int64_t m,
+                        int64_t n, int32_t steps, double a, double b, double c, void* stream);
 
 /* ------------------------------------------------------------------------------
  * gefen_stream_mix -- measurement support: the practical HBM ceiling for the step's

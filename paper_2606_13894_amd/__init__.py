@@ -34,7 +34,7 @@ SYMBOLS = [
     "gefen_read_state", "gefen_write_state", "gefen_get_fit_info", "gefen_state_bytes",
     "gefen_checkpoint_bytes", "gefen_export", "gefen_import", "gefen_profile_begin",
     "gefen_profile_end", "gefen_destroy", "gefen_last_error", "gefen_muon_init",
-    "gefen_muon_step", "gefen_muon_profile_end", "gefen_stream_mix",
+    "gefen_muon_step", "gefen_muon_profile_end", "gefen_stream_mix", "gefen_newton_schulz",
 ]
 
 
@@ -93,6 +93,7 @@ def load_library(path: str = LIB_PATH):
                                     i32, i32, f64, f64, f64, f64, vp]
     lib.gefen_muon_profile_end.argtypes = [vp, P(i32), P(f64), P(f64)]
     lib.gefen_stream_mix.argtypes = [vp, vp, i32, vp, i64, vp]
+    lib.gefen_newton_schulz.argtypes = [vp, vp, i32, i64, i64, i32, f64, f64, f64, vp]
     lib.gefen_destroy.argtypes = [vp]
     lib.gefen_destroy.restype = None
     lib.gefen_last_error.argtypes = []
@@ -361,6 +362,26 @@ def dp_codebook(hist, k: int, stream=None):
                                  ctypes.c_void_p(cb.data_ptr()), ctypes.c_void_p(cost.data_ptr()),
                                  ctypes.c_void_p(st.data_ptr()), _stream(stream)))
     return cb, float(cost.item()), int(st.item())
+
+
+def newton_schulz(x, steps: int = 5, coeffs=(3.4445, -4.7750, 2.0315), out=None, stream=None):
+    """Muon's Newton-Schulz iterations on the library's matrix-core products: x is a
+    bfloat16 device tensor of shape [batch, m, n] (or [m, n]) with m <= n, already
+    normalised; returns the result (a new tensor, or `out`)."""
+    lib = load_library()
+    torch = _torch()
+    if x.dtype != torch.bfloat16:
+        raise TypeError("x must be bfloat16")
+    x = x.contiguous()
+    shape = x.shape
+    x3 = x.reshape(-1, shape[-2], shape[-1])
+    if out is None:
+        out = torch.empty_like(x)
+    _check(lib.gefen_newton_schulz(ctypes.c_void_p(x3.data_ptr()), ctypes.c_void_p(out.data_ptr()),
+                                   x3.shape[0], x3.shape[1], x3.shape[2], int(steps),
+                                   float(coeffs[0]), float(coeffs[1]), float(coeffs[2]),
+                                   _stream(stream)))
+    return out
 
 
 def stream_mix(theta, grad, codes, stream=None):

@@ -24,7 +24,7 @@ FLAGS = [
     "-ffp-contract=off",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Rpass-analysis=kernel-resource-usage",
-    "-L/opt/rocm/lib", "-Wl,-rpath,/opt/rocm/lib", "-lrocblas",
+    "-L/opt/rocm/lib", "-Wl,-rpath,/opt/rocm/lib",
 ]
 
 

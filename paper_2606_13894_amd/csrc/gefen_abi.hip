@@ -7,8 +7,6 @@
 #include "measure_internal.h"
 #include "run_internal.h"
 
-#include <rocblas/rocblas.h>
-
 #include <algorithm>
 #include <cstdlib>
 #include <memory>
@@ -52,8 +50,6 @@ struct Class {
 constexpr int64_t kUMaxPeriod = 8192;          // longest period held in registers (KIND_U)
 constexpr int64_t kHugeBlock = 65536;         // longer blocks are always split (KIND_H)
 constexpr int kSegSlots = 4;                 // device tensor tables cached per state
-constexpr size_t kBlasWorkspace = size_t(512) << 20;   // rocBLAS workspace (Gefen-Muon)
-constexpr int64_t kMuonMaxGroup = int64_t(1) << 27;    // elements per Gefen-Muon shape group
 constexpr int64_t kMinStreamedBlocks = 4096;  // fewer blocks > kUMaxPeriod: split them too
 constexpr int64_t kPartChunk = 65536;     // elements of one partition sub-chunk (mode 1)
 constexpr int64_t kPartItemElems = 16384; // elements per partition item (mode 0)
@@ -132,22 +128,7 @@ struct gefen_state {
     std::vector<void*> dev_allocs;
 
     // Gefen-Muon (gefen_muon_init): codec tiles over every block, the bfloat16 momentum
-    // matrix per code index, tensors grouped by shape for batched Newton-Schulz GEMMs.
-    struct MuonPart {           // tensors of one rows x cols shape inside a group
-        int64_t rows, cols;
-        int32_t first, count;   // batch entries [first, first + count) of the group
-        bool transposed;        // rows > cols > 1: X = U^T
-    };
-    struct MuonGroup {
-        // wide matrices X (m x n, m = min(rows, cols)) in row-major layout with leading
-        // dimension ldx; the products run over ldx columns. A tall part's X is U^T with
-        // its columns n .. ldx - 1 zero (ldx: n rounded up to a multiple of 8, or of
-        // 8 * splits for a split Gram product); otherwise X is U itself and ldx = n.
-        int64_t m, n, ldx;
-        int32_t first, count;   // muon_tensor_of[first .. first + count)
-        int32_t splits;         // K-chunks of the Gram product (1 = one GEMM)
-        std::vector<MuonPart> parts;
-    };
+    // matrix per code index, tensors grouped by shape for batched Newton-Schulz products.
     bool muon_ready = false;
     Tile* muon_tiles = nullptr;
     int64_t muon_n_tiles = 0;
@@ -156,18 +137,15 @@ struct gefen_state {
     float* muon_tile_ss = nullptr;
     float* muon_norm = nullptr;
     uint16_t* muon_u = nullptr;
+    int64_t* muon_u_off = nullptr;        // code index of each tensor's first element
     int32_t* muon_tensor_of = nullptr;
-    std::vector<MuonGroup> muon_groups;
+    std::vector<NsGroup> muon_groups;
     // The shape groups are split over two lanes that run concurrently: lane 0 on the
     // caller's stream, lane 1 on a stream of the library's own (forked after the norms,
-    // joined at the end of the step). Each lane has its own rocBLAS handle (fixed
-    // workspace) and Newton-Schulz buffers.
+    // joined at the end of the step). Each lane has its own Newton-Schulz buffers.
     struct MuonLane {
-        rocblas_handle blas = nullptr;
-        uint16_t* x[2] = {nullptr, nullptr};
-        uint16_t* a = nullptr;
-        uint16_t* b = nullptr;
-        float* partial = nullptr;       // split-K partial Gram products (float32)
+        NsLaneBuffers buf{};            // X and X^T (ping-pong), A, B, split-K partials
+        NsLaneSizes size;
         std::vector<int32_t> groups;    // indices into muon_groups, in launch order
     };
     MuonLane muon_lane[2];
@@ -199,8 +177,6 @@ struct gefen_state {
     ~gefen_state()
     {
         prof_free();
-        for (MuonLane& l : muon_lane)
-            if (l.blas) (void)rocblas_destroy_handle(l.blas);
         if (muon_fork) (void)hipEventDestroy(muon_fork);
         if (muon_join) (void)hipEventDestroy(muon_join);
         if (muon_side) (void)hipStreamDestroy(muon_side);
@@ -1441,69 +1417,16 @@ float host_bf16_value(float x)
     return f;
 }
 
-#define GEFEN_BLAS(call)                                                                 \
-    do {                                                                                 \
-        rocblas_status s_ = (call);                                                      \
-        if (s_ != rocblas_status_success)                                                \
-            return fail(GEFEN_EHIP, "%s failed: %s", #call, rocblas_status_to_string(s_)); \
-    } while (0)
-
-hipStream_t rocblas_get_stream_for(rocblas_handle h)
+// One Newton-Schulz iteration of a shape group on a lane's buffers (ns_plan.h):
+// A = X X^T, B = b A + c A A, X' = a X + B X, each a bfloat16 product with float32
+// accumulation; `cur` selects the ping-pong buffers that hold X and X^T.
+int ns_iteration(const NsLaneBuffers& lb, const NsLaneSizes& z, const NsShape& sh, int cur,
+                 float a, float b, float c, hipStream_t stream)
 {
-    hipStream_t s = nullptr;
-    (void)rocblas_get_stream(h, &s);
-    return s;
-}
-
-// One Newton-Schulz iteration X <- a X + (b A + c A^2) X, A = X X^T, on the m x n wide
-// row-major matrices X (leading dimension ldx) of a shape group, bfloat16 products with
-// float32 accumulation. rocBLAS is column-major, so it sees each X as X^T (n x m, leading
-// dimension ldx): A = (X^T)^T X^T and the new X^T = a X^T + X^T B (B is symmetric). Both
-// operands of the Gram product run along K contiguously, the layout rocBLAS is fastest on.
-int ns_iteration(gefen_state::MuonLane& ln, const gefen_state::MuonGroup& g, const uint16_t* x,
-                 uint16_t* xo, float a, float b, float c)
-{
-    const int64_t m = g.m, n = g.ldx;   // zero columns beyond g.n add nothing
-    const rocblas_int mi = static_cast<rocblas_int>(m), ni = static_cast<rocblas_int>(n);
-    const rocblas_int ldx = static_cast<rocblas_int>(g.ldx);
-    const rocblas_stride sx = m * g.ldx, sa = m * m;
-    const float one = 1.0f, zero = 0.0f;
-    const rocblas_datatype bf = rocblas_datatype_bf16_r, f32 = rocblas_datatype_f32_r;
-    if (g.splits > 1) {
-        // tall-skinny Gram product (one matrix, long K): float32 partial products of
-        // K-chunks (column blocks of X), summed in chunk order and rounded once
-        const int64_t kc = (n + g.splits - 1) / g.splits;
-        const int64_t full = n / kc;               // chunks of length kc
-        const int64_t rest = n - full * kc;
-        if (full > 0)
-            GEFEN_BLAS(rocblas_gemm_strided_batched_ex(
-                ln.blas, rocblas_operation_transpose, rocblas_operation_none, mi, mi,
-                static_cast<rocblas_int>(kc), &one, x, bf, ldx, kc, x, bf, ldx, kc, &zero,
-                ln.partial, f32, mi, sa, ln.partial, f32, mi, sa,
-                static_cast<rocblas_int>(full), f32, rocblas_gemm_algo_standard, 0, 0));
-        if (rest > 0)
-            GEFEN_BLAS(rocblas_gemm_ex(
-                ln.blas, rocblas_operation_transpose, rocblas_operation_none, mi, mi,
-                static_cast<rocblas_int>(rest), &one, x + full * kc, bf, ldx, x + full * kc, bf,
-                ldx, &zero, ln.partial + full * sa, f32, mi, ln.partial + full * sa,
-                f32, mi, f32, rocblas_gemm_algo_standard, 0, 0));
-        GEFEN_HIP(launch_muon_splitk_sum(ln.partial,
-                                         static_cast<int32_t>(full + (rest > 0 ? 1 : 0)), sa,
-                                         ln.a, rocblas_get_stream_for(ln.blas)));
-    } else {
-        GEFEN_BLAS(rocblas_gemm_strided_batched_ex(
-            ln.blas, rocblas_operation_transpose, rocblas_operation_none, mi, mi, ni, &one, x,
-            bf, ldx, sx, x, bf, ldx, sx, &zero, ln.a, bf, mi, sa, ln.a, bf, mi, sa,
-            g.count, f32, rocblas_gemm_algo_standard, 0, 0));
-    }
-    GEFEN_BLAS(rocblas_gemm_strided_batched_ex(
-        ln.blas, rocblas_operation_none, rocblas_operation_none, mi, mi, mi, &c, ln.a, bf,
-        mi, sa, ln.a, bf, mi, sa, &b, ln.a, bf, mi, sa, ln.b, bf, mi, sa,
-        g.count, f32, rocblas_gemm_algo_standard, 0, 0));
-    GEFEN_BLAS(rocblas_gemm_strided_batched_ex(
-        ln.blas, rocblas_operation_none, rocblas_operation_none, ni, mi, mi, &one, x, bf, ldx,
-        sx, ln.b, bf, mi, sa, &a, x, bf, ldx, sx, xo, bf, ldx, sx, g.count, f32,
-        rocblas_gemm_algo_standard, 0, 0));
+    NsGemmArgs prods[3];
+    int64_t avail[3][6];
+    ns_iteration_products(sh, lb, z, cur, a, b, c, prods, avail);
+    for (const NsGemmArgs& p : prods) GEFEN_HIP(launch_ns_gemm(p, stream));
     return GEFEN_OK;
 }
 
@@ -1563,148 +1486,83 @@ int muon_codec_tiles(gefen_state* st, std::vector<Tile>& tiles, std::vector<int6
     return GEFEN_OK;
 }
 
-// Shape groups (tensor order in `order`) and their split-K choice; max_x is the largest
-// group's Newton-Schulz buffer in elements.
-int muon_shape_groups(gefen_state* st, const int64_t* rows, std::vector<int32_t>& order,
-                      int64_t& max_x)
-{
-    const int32_t n = st->n_tensors;
-    // Shape groups: tensors whose wide matrices and X layouts agree share one batch of
-    // Newton-Schulz products (so a tall R x C tensor joins the C x R ones); inside a
-    // group, parts of one R x C shape share the normalise and update launches. Groups and
-    // parts in order of first appearance.
-    st->muon_groups.clear();
-    struct Shape {
-        int64_t rows, cols, m, n, ldx;
-        bool transposed;
-    };
-    std::vector<Shape> shp(n);
-    for (int32_t t = 0; t < n; ++t) {
-        Shape& sh = shp[t];
-        sh.rows = rows[t];
-        sh.cols = st->numel[t] / rows[t];
-        sh.m = std::min(sh.rows, sh.cols);
-        sh.n = std::max(sh.rows, sh.cols);
-        if (sh.n > 0x7ffff000LL)
-            return fail(GEFEN_EINVAL, "a matrix side exceeds 2^31 - 4096");
-        sh.transposed = sh.rows > sh.cols && sh.cols > 1;
-        sh.ldx = sh.transposed ? (sh.n + 7) / 8 * 8 : sh.n;
-    }
-    std::vector<char> placed(static_cast<size_t>(n), 0);
-    for (int32_t t = 0; t < n; ++t) {
-        if (placed[t]) continue;
-        gefen_state::MuonGroup g{};
-        g.m = shp[t].m;
-        g.n = shp[t].n;
-        g.ldx = shp[t].ldx;
-        g.first = static_cast<int32_t>(order.size());
-        g.splits = 1;
-        for (int32_t u = t; u < n; ++u) {
-            if (placed[u] || shp[u].m != g.m || shp[u].n != g.n || shp[u].ldx != g.ldx) continue;
-            gefen_state::MuonPart pt{shp[u].rows, shp[u].cols, g.count, 0, shp[u].transposed};
-            for (int32_t v = u; v < n; ++v)
-                if (!placed[v] && shp[v].rows == pt.rows && shp[v].cols == pt.cols) {
-                    placed[v] = 1;
-                    order.push_back(v);
-                    ++pt.count;
-                    ++g.count;
-                }
-            g.parts.push_back(pt);
-        }
-        st->muon_groups.push_back(g);
-    }
-    // Split the Gram product of a lone tall-skinny matrix over K when its m x m output
-    // has too few 128 x 128 tiles to occupy the GPU. A transposed X gets zero columns up
-    // to a multiple of 8 * splits, so that the chunks are equal and one batched call
-    // covers them.
-    max_x = 0;
-    for (auto& g : st->muon_groups) {
-        const int64_t m = g.m;
-        const int64_t tiles = ((m + 127) / 128) * ((m + 127) / 128);
-        if (g.count == 1 && m > 1 && tiles < 128 && g.n >= 8 * m) {
-            g.splits = static_cast<int32_t>(std::min<int64_t>(16, g.n / (4 * m)));
-            if (g.splits < 2) g.splits = 1;
-        }
-        if (g.splits > 1 && g.parts[0].transposed)
-            g.ldx = (g.n + 8 * g.splits - 1) / (8 * g.splits) * (8 * g.splits);
-        max_x = std::max(max_x, g.count * m * g.ldx);
-    }
-    return GEFEN_OK;
-}
-
-// Lanes: groups in decreasing order of Newton-Schulz work, each to the lane with less
-// work so far.
-void muon_assign_lanes(gefen_state* st)
-{
-    constexpr int n_lanes = 2;
-    std::vector<int32_t> byw(st->muon_groups.size());
-    std::vector<double> work(byw.size());
-    for (size_t gi = 0; gi < byw.size(); ++gi) {
-        const auto& g = st->muon_groups[gi];
-        byw[gi] = static_cast<int32_t>(gi);
-        const double m = static_cast<double>(g.m), nn = static_cast<double>(g.ldx);
-        work[gi] = g.count * (g.m > 1 ? 4.0 * m * m * nn + 2.0 * m * m * m : 4.0 * nn);
-    }
-    std::stable_sort(byw.begin(), byw.end(),
-                     [&](int32_t a, int32_t b) { return work[a] > work[b]; });
-    double load[2] = {0.0, 0.0};
-    for (gefen_state::MuonLane& l : st->muon_lane) l.groups.clear();
-    for (int32_t gi : byw) {
-        const int l = (n_lanes > 1 && load[1] < load[0]) ? 1 : 0;
-        st->muon_lane[l].groups.push_back(gi);
-        load[l] += work[gi];
-    }
-}
-
-// Per-lane Newton-Schulz buffers, rocBLAS handles and workspaces, the side stream, and
-// a warm-up iteration of every group.
-int muon_lane_resources(gefen_state* st, hipStream_t stream)
+// Per-lane Newton-Schulz buffers (sized for the lane's largest group), the host check of
+// every product and prep/update extent the steps will run, and the side stream.
+int muon_lane_resources(gefen_state* st)
 {
     int rc;
-    int64_t lane_x[2] = {0, 0};
     for (int l = 0; l < 2; ++l) {
         gefen_state::MuonLane& ln = st->muon_lane[l];
-        int64_t mx = 0, ma = 0, mp = 0;
-        for (int32_t gi : ln.groups) {
-            const auto& g = st->muon_groups[gi];
-            mx = std::max(mx, g.count * g.m * g.ldx);
-            ma = std::max(ma, g.count * g.m * g.m);
-            if (g.splits > 1) mp = std::max(mp, g.splits * g.m * g.m);
-        }
-        lane_x[l] = mx;
         if (ln.groups.empty()) continue;
-        for (auto& x : ln.x)
-            if ((rc = st->alloc(&x, 2 * static_cast<size_t>(mx), false))) return rc;
-        if ((rc = st->alloc(&ln.a, 2 * static_cast<size_t>(ma), false))) return rc;
-        if ((rc = st->alloc(&ln.b, 2 * static_cast<size_t>(ma), false))) return rc;
-        if ((rc = st->alloc(&ln.partial, 4 * static_cast<size_t>(mp), false))) return rc;
+        ln.size = ns_lane_sizes(st->muon_groups, ln.groups);
+        NsLaneBuffers& lb = ln.buf;
+        for (int k = 0; k < 2; ++k) {
+            if ((rc = st->alloc(&lb.x[k], 2 * static_cast<size_t>(ln.size.x_elems), false))) return rc;
+            if ((rc = st->alloc(&lb.xt[k], 2 * static_cast<size_t>(ln.size.x_elems), false))) return rc;
+        }
+        if ((rc = st->alloc(&lb.a, 2 * static_cast<size_t>(ln.size.a_elems), false))) return rc;
+        if ((rc = st->alloc(&lb.b, 2 * static_cast<size_t>(ln.size.a_elems), false))) return rc;
+        if ((rc = st->alloc(&lb.partial, 4 * static_cast<size_t>(ln.size.partial_elems), false)))
+            return rc;
+        for (int32_t gi : ln.groups) {
+            const std::string why = ns_check_group(st->muon_groups[gi], lb, ln.size);
+            if (!why.empty()) return fail(GEFEN_EINVAL, "internal: %s", why.c_str());
+        }
     }
-    // One rocBLAS handle per lane with a fixed workspace that the state owns, handed to
-    // rocBLAS before any product runs, so that steps allocate nothing. One Newton-Schulz
-    // iteration per group on zeroed matrices loads and checks every GEMM the steps use,
-    // on the lane's own stream.
     if (!st->muon_lane[1].groups.empty()) {
         GEFEN_HIP(hipStreamCreateWithFlags(&st->muon_side, hipStreamNonBlocking));
         GEFEN_HIP(hipEventCreateWithFlags(&st->muon_fork, hipEventDisableTiming));
         GEFEN_HIP(hipEventCreateWithFlags(&st->muon_join, hipEventDisableTiming));
     }
-    for (int l = 0; l < 2; ++l) {
-        gefen_state::MuonLane& ln = st->muon_lane[l];
-        if (ln.groups.empty()) continue;
-        hipStream_t ls = l == 0 ? stream : st->muon_side;
-        void* ws = nullptr;
-        if ((rc = st->alloc(&ws, kBlasWorkspace, false))) return rc;
-        GEFEN_BLAS(rocblas_create_handle(&ln.blas));
-        GEFEN_BLAS(rocblas_set_stream(ln.blas, ls));
-        GEFEN_BLAS(rocblas_set_workspace(ln.blas, ws, kBlasWorkspace));
-        if (l == 1) GEFEN_HIP(hipStreamSynchronize(stream));   // allocations above
-        GEFEN_HIP(fill_zero(ln.x[0], 2 * static_cast<size_t>(lane_x[l]), ls));
-        for (int32_t gi : ln.groups) {
-            const auto& g = st->muon_groups[gi];
-            if (g.m > 1 && (rc = ns_iteration(ln, g, ln.x[0], ln.x[1], 1.0f, 1.0f, 1.0f)))
-                return rc;
+    return GEFEN_OK;
+}
+
+// Normalise (prep), orthogonalise and update one shape group with a lane's buffers.
+int muon_run_group(gefen_state* st, const gefen_state::MuonLane& lane, const NsGroup& g,
+                   int32_t ns_steps, float ca, float cb, float cc, double lr, float decay,
+                   hipStream_t ls)
+{
+    const NsShape& sh = g.shape;
+    const NsLaneBuffers& ln = lane.buf;
+    const int64_t xs = sh.m * sh.ldx, ts = sh.ldx * sh.ldm;   // batch strides of X, X^T
+    for (const auto& pt : g.parts) {
+        const int32_t* tof = st->muon_tensor_of + g.first + pt.first;
+        uint16_t* x0 = ln.x[0] + pt.first * xs;
+        uint16_t* t0 = ln.xt[0] + pt.first * ts;
+        if (sh.m == 1)
+            GEFEN_HIP(launch_ns_prep(st->muon_u, st->muon_u_off, tof, st->muon_norm, pt.count, 1,
+                                     pt.rows * pt.cols, x0, xs, t0, ts, ls));
+        else if (!pt.transposed)
+            GEFEN_HIP(launch_ns_prep(st->muon_u, st->muon_u_off, tof, st->muon_norm, pt.count,
+                                     pt.rows, pt.cols, x0, xs, t0, ts, ls));
+        else
+            GEFEN_HIP(launch_ns_prep(st->muon_u, st->muon_u_off, tof, st->muon_norm, pt.count,
+                                     pt.rows, pt.cols, t0, ts, x0, xs, ls));
+    }
+    int cur = 0;
+    if (sh.m == 1) {
+        GEFEN_HIP(launch_muon_ns_vec(ln.x[0], static_cast<int32_t>(sh.count), sh.n, sh.ldx,
+                                     ns_steps, ca, cb, cc, ls));
+    } else {
+        for (int32_t it = 0; it < ns_steps; ++it) {
+            const int r = ns_iteration(ln, lane.size, sh, cur, ca, cb, cc, ls);
+            if (r) return r;
+            cur ^= 1;
         }
-        GEFEN_HIP(hipStreamSynchronize(ls));
+    }
+    for (const auto& pt : g.parts) {
+        const int32_t* tof = st->muon_tensor_of + g.first + pt.first;
+        const double scale = std::sqrt(std::max(1.0, static_cast<double>(pt.rows) / pt.cols));
+        const float step = static_cast<float>(lr * scale);
+        if (sh.m == 1)
+            GEFEN_HIP(launch_ns_update(ln.x[cur] + pt.first * xs, xs, sh.ldx, st->segs, tof,
+                                       pt.count, 1, pt.rows * pt.cols, decay, step, ls));
+        else if (!pt.transposed)   // theta = X' (m x n)
+            GEFEN_HIP(launch_ns_update(ln.x[cur] + pt.first * xs, xs, sh.ldx, st->segs, tof,
+                                       pt.count, pt.rows, pt.cols, decay, step, ls));
+        else                       // theta = X'^T (n x m)
+            GEFEN_HIP(launch_ns_update(ln.xt[cur] + pt.first * ts, ts, sh.ldm, st->segs, tof,
+                                       pt.count, pt.rows, pt.cols, decay, step, ls));
     }
     return GEFEN_OK;
 }
@@ -1729,16 +1587,13 @@ int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, voi
     std::vector<int64_t> tile_range;
     if ((rc = muon_codec_tiles(st, tiles, tile_range))) return rc;
     std::vector<int32_t> order;
-    int64_t max_x = 0;
-    if ((rc = muon_shape_groups(st, rows, order, max_x))) return rc;
-    // Shape groups above kMuonMaxGroup elements are refused: a state of that size (the
-    // GPT-2 1B shapes, 4e8 elements in one group) failed with a device memory fault in
-    // this initialisation, whose cause has not been found.
-    if (max_x > kMuonMaxGroup)
-        return fail(GEFEN_EINVAL, "a group of equal-shape tensors holds %lld elements; "
-                    "Gefen-Muon supports at most %lld per group",
-                    (long long)max_x, (long long)kMuonMaxGroup);
-    muon_assign_lanes(st);
+    const std::string why = ns_plan_groups(n, rows, st->numel.data(), st->muon_groups, order);
+    if (!why.empty()) return fail(GEFEN_EINVAL, "%s", why.c_str());
+    {
+        std::vector<int32_t> lanes[2];
+        ns_assign_lanes(st->muon_groups, lanes);
+        for (int l = 0; l < 2; ++l) st->muon_lane[l].groups = lanes[l];
+    }
 
     st->muon_n_tiles = static_cast<int64_t>(tiles.size());
     if ((rc = st->alloc(&st->muon_tiles, sizeof(Tile) * tiles.size(), false))) return rc;
@@ -1750,7 +1605,10 @@ int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, voi
     GEFEN_HIP(hipMemcpy(st->muon_tiles, tiles.data(), sizeof(Tile) * tiles.size(), hipMemcpyHostToDevice));
     GEFEN_HIP(hipMemcpy(st->muon_tile_range, tile_range.data(), 8 * tile_range.size(), hipMemcpyHostToDevice));
     GEFEN_HIP(hipMemcpy(st->muon_tensor_of, order.data(), 4 * order.size(), hipMemcpyHostToDevice));
-    if ((rc = muon_lane_resources(st, stream))) return rc;
+    if ((rc = st->alloc(&st->muon_u_off, 8 * static_cast<size_t>(n), false))) return rc;
+    GEFEN_HIP(hipMemcpy(st->muon_u_off, st->code_off.data(), 8 * static_cast<size_t>(n),
+                        hipMemcpyHostToDevice));
+    if ((rc = muon_lane_resources(st))) return rc;
     GEFEN_HIP(hipStreamSynchronize(stream));
     st->muon_ready = true;
     return GEFEN_OK;
@@ -1773,7 +1631,6 @@ int gefen_muon_step(gefen_state* st, const gefen_tensor* params, const gefen_ten
     if (!finite_f(ns_eps) || ns_eps <= 0.0) return fail(GEFEN_EINVAL, "ns_eps must be finite and > 0");
     hipStream_t stream = as_stream(stream_);
     if ((rc = refresh_segs(st, params, grads, stream))) return rc;
-    GEFEN_BLAS(rocblas_set_stream(st->muon_lane[0].blas, stream));
     const bool prof = st->prof_armed && st->muon_prof_steps < st->prof_max_steps &&
                       !st->muon_prof_events.empty();
     hipEvent_t* ev = prof ? &st->muon_prof_events[st->muon_prof_steps * st->muon_prof_stride()]
@@ -1791,47 +1648,10 @@ int gefen_muon_step(gefen_state* st, const gefen_tensor* params, const gefen_ten
                                host_bf16_value(static_cast<float>(ns_eps)), st->muon_norm, stream));
     if (prof) GEFEN_HIP(hipEventRecord(ev[1], stream));
     const float decay = static_cast<float>(1.0 - lr * weight_decay);
-    // normalise, orthogonalise and update one shape group with a lane's resources
-    auto run_group = [&](gefen_state::MuonLane& ln, const gefen_state::MuonGroup& g,
-                         hipStream_t ls) -> int {
-        const int64_t xs = g.m * g.ldx;   // elements per batch entry of X
-        for (const auto& pt : g.parts) {
-            const int32_t* tof = st->muon_tensor_of + g.first + pt.first;
-            uint16_t* xb = ln.x[0] + pt.first * xs;
-            if (pt.transposed)
-                GEFEN_HIP(launch_muon_prep_t(st->muon_u, st->segs, tof, pt.count, st->muon_norm,
-                                             pt.rows, pt.cols, g.ldx, xb, ls));
-            else
-                GEFEN_HIP(launch_muon_prep(st->muon_u, st->segs, tof, pt.count, st->muon_norm,
-                                           pt.rows * pt.cols, xb, ls));
-        }
-        int cur = 0;
-        if (g.m == 1) {
-            GEFEN_HIP(launch_muon_ns_vec(ln.x[0], g.count, g.n, ns_steps,
-                                         static_cast<float>(ns_a), static_cast<float>(ns_b),
-                                         static_cast<float>(ns_c), ls));
-        } else {
-            for (int32_t it = 0; it < ns_steps; ++it) {
-                const int r = ns_iteration(ln, g, ln.x[cur], ln.x[1 - cur],
-                                           static_cast<float>(ns_a), static_cast<float>(ns_b),
-                                           static_cast<float>(ns_c));
-                if (r) return r;
-                cur ^= 1;
-            }
-        }
-        for (const auto& pt : g.parts) {
-            const int32_t* tof = st->muon_tensor_of + g.first + pt.first;
-            const uint16_t* ob = ln.x[cur] + pt.first * xs;
-            const double scale = std::sqrt(std::max(1.0, static_cast<double>(pt.rows) / pt.cols));
-            const float step = static_cast<float>(lr * scale);
-            if (pt.transposed)
-                GEFEN_HIP(launch_muon_update_t(ob, st->segs, tof, pt.count, pt.rows, pt.cols,
-                                               g.ldx, decay, step, ls));
-            else
-                GEFEN_HIP(launch_muon_update(ob, st->segs, tof, pt.count, pt.rows * pt.cols,
-                                             decay, step, ls));
-        }
-        return GEFEN_OK;
+    const float ca = static_cast<float>(ns_a), cb = static_cast<float>(ns_b),
+                cc = static_cast<float>(ns_c);
+    auto run_group = [&](gefen_state::MuonLane& ln, const NsGroup& g, hipStream_t ls) -> int {
+        return muon_run_group(st, ln, g, ns_steps, ca, cb, cc, lr, decay, ls);
     };
     // lane 1 first (it starts as soon as the norms are done), then lane 0, then the join
     gefen_state::MuonLane& l1 = st->muon_lane[1];
@@ -1873,6 +1693,79 @@ int gefen_muon_profile_end(gefen_state* st, int32_t* steps, double* codec_ms, do
     }
     st->prof_free();
     return GEFEN_OK;
+}
+
+int gefen_newton_schulz(const uint16_t* x_in, uint16_t* x_out, int32_t batch, int64_t m,
+                        int64_t n, int32_t steps, double a, double b, double c, void* stream_)
+{
+    if (!x_in || !x_out) return fail(GEFEN_EINVAL, "NULL argument");
+    if (batch < 1 || batch > 65535) return fail(GEFEN_EINVAL, "batch must be in [1, 65535]");
+    if (m < 1 || m > n || n > 0x7ffff000LL)
+        return fail(GEFEN_EINVAL, "need 1 <= m <= n <= 2^31 - 4096 (m = %lld, n = %lld)",
+                    (long long)m, (long long)n);
+    if (steps < 0 || steps > 100) return fail(GEFEN_EINVAL, "steps must be in [0, 100]");
+    if (!finite_f(a) || !finite_f(b) || !finite_f(c))
+        return fail(GEFEN_EINVAL, "Newton-Schulz coefficients must be finite");
+    hipStream_t stream = as_stream(stream_);
+    NsGroup g{};
+    g.shape = ns_shape(batch, m, n);
+    g.parts.push_back(NsPart{m, n, 0, batch, false});
+    const NsShape& sh = g.shape;
+    const NsLaneSizes z = ns_lane_sizes(std::vector<NsGroup>{g}, std::vector<int32_t>{0});
+    if (z.x_elems > (int64_t(1) << 40)) return fail(GEFEN_EINVAL, "matrices too large");
+    NsLaneBuffers lb{};
+    std::vector<void*> bufs;
+    auto release = [&]() {
+        for (void* p : bufs) (void)hipFreeAsync(p, stream);
+    };
+    auto get = [&](void** p, int64_t bytes) -> int {
+        hipError_t e = hipMallocAsync(p, static_cast<size_t>(std::max<int64_t>(bytes, 16)), stream);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            release();
+            return fail(GEFEN_ENOMEM, "hipMallocAsync(%lld) failed: %s", (long long)bytes,
+                        hipGetErrorString(e));
+        }
+        bufs.push_back(*p);
+        return GEFEN_OK;
+    };
+    int rc;
+    for (int k = 0; k < 2; ++k) {
+        if ((rc = get(reinterpret_cast<void**>(&lb.x[k]), 2 * z.x_elems))) return rc;
+        if ((rc = get(reinterpret_cast<void**>(&lb.xt[k]), 2 * z.x_elems))) return rc;
+    }
+    if ((rc = get(reinterpret_cast<void**>(&lb.a), 2 * z.a_elems))) return rc;
+    if ((rc = get(reinterpret_cast<void**>(&lb.b), 2 * z.a_elems))) return rc;
+    if ((rc = get(reinterpret_cast<void**>(&lb.partial), 4 * z.partial_elems))) return rc;
+    {
+        const std::string why = ns_check_group(g, lb, z);
+        if (!why.empty()) {
+            release();
+            return fail(GEFEN_EINVAL, "internal: %s", why.c_str());
+        }
+    }
+    const int64_t xs = sh.m * sh.ldx, ts = sh.ldx * sh.ldm;
+    auto run = [&]() -> int {
+        GEFEN_HIP(launch_ns_prep(x_in, nullptr, nullptr, nullptr, batch, m, n, lb.x[0], xs,
+                                 lb.xt[0], ts, stream));
+        int cur = 0;
+        if (m == 1) {
+            GEFEN_HIP(launch_muon_ns_vec(lb.x[0], batch, n, sh.ldx, steps, static_cast<float>(a),
+                                         static_cast<float>(b), static_cast<float>(c), stream));
+        } else {
+            for (int32_t it = 0; it < steps; ++it) {
+                const int r = ns_iteration(lb, z, sh, cur, static_cast<float>(a),
+                                           static_cast<float>(b), static_cast<float>(c), stream);
+                if (r) return r;
+                cur ^= 1;
+            }
+        }
+        GEFEN_HIP(launch_ns_unpad(lb.x[cur], xs, sh.ldx, batch, m, n, x_out, stream));
+        return GEFEN_OK;
+    };
+    rc = run();
+    release();
+    return rc;
 }
 
 }  // extern "C"

@@ -1,8 +1,7 @@
 // Gefen-Muon (appendix "Gefen-Muon") on the device: the codec that keeps Muon's
 // momentum in Gefen's quantized form, the Frobenius norm of each momentum matrix, its
-// normalised bfloat16 copy (the Newton-Schulz input), and the parameter update from the
-// orthogonalised result. The Newton-Schulz matrix products
-// are plain bfloat16 GEMMs (rocBLAS), driven from the host.
+// and the Newton-Schulz iterations of 1 x n matrices. The matrix products of the other
+// shapes, and the kernels around them, are in ns_gemm.hip.
 #include "muon_internal.h"
 #include "step_device.h"
 
@@ -297,220 +296,15 @@ __global__ __launch_bounds__(kThreads) void k_muon_codec(const Tile* __restrict_
     }
 }
 
-// Newton-Schulz input and update for a matrix that is not tall (R <= C, or C = 1): X has
-// the tensor's own row-major layout, so both are flat element loops, eight bfloat16
-// (prep) or four parameters (update) per thread where sizes and pointers are aligned,
-// element by element otherwise.
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
-typedef float f32x4v __attribute__((ext_vector_type(4)));
-
-__global__ __launch_bounds__(256) void k_muon_prep_flat(const uint16_t* __restrict__ u,
-                                                        const Seg* __restrict__ segs,
-                                                        const int32_t* __restrict__ tensor_of,
-                                                        const float* __restrict__ norm,
-                                                        int64_t n, uint16_t* __restrict__ x)
-{
-    const int b = blockIdx.y;
-    const int t = tensor_of[b];
-    const uint16_t* __restrict__ src = u + segs[t].code_off;
-    uint16_t* __restrict__ dst = x + static_cast<int64_t>(b) * n;
-    const float nrm = norm[t];
-    const int64_t stride = 256LL * gridDim.x;
-    if ((n & 7) == 0) {
-        for (int64_t v = blockIdx.x * 256LL + threadIdx.x; v < n / 8; v += stride) {
-            const u32x4 w = reinterpret_cast<const u32x4*>(src)[v];
-            u32x4 o;
-            for (int c = 0; c < 4; ++c) {
-                const uint32_t lo = to_bf16(bf16_val(static_cast<uint16_t>(w[c] & 0xffffu)) / nrm);
-                const uint32_t hi = to_bf16(bf16_val(static_cast<uint16_t>(w[c] >> 16)) / nrm);
-                o[c] = lo | (hi << 16);
-            }
-            reinterpret_cast<u32x4*>(dst)[v] = o;
-        }
-    } else {
-        for (int64_t i = blockIdx.x * 256LL + threadIdx.x; i < n; i += stride)
-            dst[i] = to_bf16(bf16_val(src[i]) / nrm);
-    }
-}
-
-__global__ __launch_bounds__(256) void k_muon_update_flat(const uint16_t* __restrict__ o,
-                                                          const Seg* __restrict__ segs,
-                                                          const int32_t* __restrict__ tensor_of,
-                                                          int64_t n, float decay, float step)
-{
-    const int b = blockIdx.y;
-    const int t = tensor_of[b];
-    float* __restrict__ th = segs[t].theta;
-    const uint16_t* __restrict__ src = o + static_cast<int64_t>(b) * n;
-    const int64_t stride = 256LL * gridDim.x;
-    if ((n & 3) == 0 && (reinterpret_cast<uintptr_t>(th) & 15) == 0) {
-        for (int64_t v = blockIdx.x * 256LL + threadIdx.x; v < n / 4; v += stride) {
-            const u32x2v w = reinterpret_cast<const u32x2v*>(src)[v];
-            f32x4v tv = reinterpret_cast<const f32x4v*>(th)[v];
-            tv.x = fmaf(-step, bf16_val(static_cast<uint16_t>(w.x & 0xffffu)), tv.x * decay);
-            tv.y = fmaf(-step, bf16_val(static_cast<uint16_t>(w.x >> 16)), tv.y * decay);
-            tv.z = fmaf(-step, bf16_val(static_cast<uint16_t>(w.y & 0xffffu)), tv.z * decay);
-            tv.w = fmaf(-step, bf16_val(static_cast<uint16_t>(w.y >> 16)), tv.w * decay);
-            reinterpret_cast<f32x4v*>(th)[v] = tv;
-        }
-    } else {
-        for (int64_t i = blockIdx.x * 256LL + threadIdx.x; i < n; i += stride)
-            th[i] = fmaf(-step, bf16_val(src[i]), th[i] * decay);
-    }
-}
-
-// Tall matrices (R > C > 1) are orthogonalised as their wide transpose X = U^T (C x R,
-// rows padded to ldx, a multiple of 8). A lane moves an 8 x 8 block and transposes it in
-// registers; lane l of a wave takes rows 8 (l / 8) .. + 7 and columns 8 (l % 8) .. + 7 of
-// a 64 x 64 tile, so each of its eight 16-byte row loads and eight 16-byte column stores
-// joins those of seven neighbouring lanes into 128 contiguous bytes. A workgroup holds 4
-// tiles along R. Blocks on the matrix edge, or of tensors whose rows are not 16-byte
-// aligned, go element by element.
-constexpr int kTile = 64;
-constexpr int kTilesPerGroup = 4;
-
-struct TBlock {
-    int64_t r0, c0;
-    bool full;
-};
-
-__device__ __forceinline__ TBlock t_block(int64_t R, int64_t C)
-{
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    TBlock tb;
-    tb.r0 = (static_cast<int64_t>(blockIdx.y) * kTilesPerGroup + wave) * kTile + 8 * (lane >> 3);
-    tb.c0 = static_cast<int64_t>(blockIdx.x) * kTile + 8 * (lane & 7);
-    tb.full = tb.r0 + 8 <= R && tb.c0 + 8 <= C;
-    return tb;
-}
-
-// Element j (0..7) of eight packed bfloat16.
-__device__ __forceinline__ uint32_t bf16_at(const u32x4& w, int j)
-{
-    const uint32_t v = w[j >> 1];
-    return (j & 1) ? (v >> 16) : (v & 0xffffu);
-}
-
-// x[b] (C x ldx) = bf16(U^T / norm), U the R x C momentum matrix of tensor tensor_of[b],
-// and zero in columns R .. ldx - 1 (the grid covers ldx rows of U)
-__global__ __launch_bounds__(256) void k_muon_prep_t(const uint16_t* __restrict__ u,
-                                                     const Seg* __restrict__ segs,
-                                                     const int32_t* __restrict__ tensor_of,
-                                                     const float* __restrict__ norm, int64_t R,
-                                                     int64_t C, int64_t ldx,
-                                                     uint16_t* __restrict__ x)
-{
-    const int b = blockIdx.z;
-    const int t = tensor_of[b];
-    const uint16_t* __restrict__ src = u + segs[t].code_off;
-    uint16_t* __restrict__ dst = x + static_cast<int64_t>(b) * C * ldx;
-    const float nrm = norm[t];
-    const TBlock tb = t_block(R, C);
-    if (tb.r0 >= ldx || tb.c0 >= C) return;
-    if (tb.r0 >= R) {   // zero columns of X (tb.r0 + 8 <= ldx, as ldx % 8 == 0)
-        const u32x4 z = {0u, 0u, 0u, 0u};
-        for (int k = 0; k < 8; ++k)
-            if (tb.c0 + k < C) *reinterpret_cast<u32x4*>(dst + (tb.c0 + k) * ldx + tb.r0) = z;
-        return;
-    }
-    if (tb.full && (C & 7) == 0) {
-        u32x4 w[8];
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-            w[j] = *reinterpret_cast<const u32x4*>(src + (tb.r0 + j) * C + tb.c0);
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const uint32_t lo = to_bf16(bf16_val(static_cast<uint16_t>(w[j][q] & 0xffffu)) / nrm);
-                const uint32_t hi = to_bf16(bf16_val(static_cast<uint16_t>(w[j][q] >> 16)) / nrm);
-                w[j][q] = lo | (hi << 16);
-            }
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            u32x4 o;
-#pragma unroll
-            for (int p = 0; p < 4; ++p) o[p] = bf16_at(w[2 * p], k) | (bf16_at(w[2 * p + 1], k) << 16);
-            *reinterpret_cast<u32x4*>(dst + (tb.c0 + k) * ldx + tb.r0) = o;
-        }
-    } else {
-        for (int j = 0; j < 8; ++j)
-            for (int k = 0; k < 8; ++k) {
-                const int64_t r = tb.r0 + j, c = tb.c0 + k;
-                if (c >= C || r >= ldx) continue;
-                dst[c * ldx + r] = r < R ? to_bf16(bf16_val(src[r * C + c]) / nrm) : 0;
-            }
-    }
-}
-
-// theta of tensor_of[b] (R x C) = theta * decay - step * O^T, O = o[b] (C x ldx)
-__global__ __launch_bounds__(256) void k_muon_update_t(const uint16_t* __restrict__ o,
-                                                       const Seg* __restrict__ segs,
-                                                       const int32_t* __restrict__ tensor_of,
-                                                       int64_t R, int64_t C, int64_t ldx,
-                                                       float decay, float step)
-{
-    const int b = blockIdx.z;
-    const int t = tensor_of[b];
-    float* __restrict__ th = segs[t].theta;
-    const uint16_t* __restrict__ src = o + static_cast<int64_t>(b) * C * ldx;
-    const TBlock tb = t_block(R, C);
-    if (tb.r0 >= R || tb.c0 >= C) return;
-    if (tb.full && (C & 3) == 0 && (reinterpret_cast<uintptr_t>(th) & 15) == 0) {
-        u32x4 w[8];
-#pragma unroll
-        for (int k = 0; k < 8; ++k)
-            w[k] = *reinterpret_cast<const u32x4*>(src + (tb.c0 + k) * ldx + tb.r0);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            f32x4v* row = reinterpret_cast<f32x4v*>(th + (tb.r0 + j) * C + tb.c0);
-            f32x4v t0 = row[0], t1 = row[1];
-            t0.x = fmaf(-step, bf16_val(static_cast<uint16_t>(bf16_at(w[0], j))), t0.x * decay);
-            t0.y = fmaf(-step, bf16_val(static_cast<uint16_t>(bf16_at(w[1], j))), t0.y * decay);
-            t0.z = fmaf(-step, bf16_val(static_cast<uint16_t>(bf16_at(w[2], j))), t0.z * decay);
-            t0.w = fmaf(-step, bf16_val(static_cast<uint16_t>(bf16_at(w[3], j))), t0.w * decay);
-            t1.x = fmaf(-step, bf16_val(static_cast<uint16_t>(bf16_at(w[4], j))), t1.x * decay);
-            t1.y = fmaf(-step, bf16_val(static_cast<uint16_t>(bf16_at(w[5], j))), t1.y * decay);
-            t1.z = fmaf(-step, bf16_val(static_cast<uint16_t>(bf16_at(w[6], j))), t1.z * decay);
-            t1.w = fmaf(-step, bf16_val(static_cast<uint16_t>(bf16_at(w[7], j))), t1.w * decay);
-            row[0] = t0;
-            row[1] = t1;
-        }
-    } else {
-        for (int j = 0; j < 8; ++j)
-            for (int k = 0; k < 8; ++k) {
-                const int64_t r = tb.r0 + j, c = tb.c0 + k;
-                if (r < R && c < C) {
-                    const int64_t e = r * C + c;
-                    th[e] = fmaf(-step, bf16_val(src[c * ldx + r]), th[e] * decay);
-                }
-            }
-    }
-}
-
-// Split-K Gram: A = bf16(sum over s of P[s]), the float32 partial products of K-chunks,
-// added in chunk order.
-__global__ __launch_bounds__(256) void k_muon_splitk_sum(const float* __restrict__ partial,
-                                                         int32_t splits, int64_t mm,
-                                                         uint16_t* __restrict__ a)
-{
-    for (int64_t i = blockIdx.x * 256LL + threadIdx.x; i < mm; i += 256LL * gridDim.x) {
-        float acc = partial[i];
-        for (int32_t s = 1; s < splits; ++s) acc += partial[s * mm + i];
-        a[i] = to_bf16(acc);
-    }
-}
-
 // Newton-Schulz on 1 x n matrices (one workgroup per batch entry): the Gram matrix is
 // the scalar s = x x^T, so every iteration is x <- bf16(a x + bf16(b s + c s^2) x), with
 // s = bf16(x x^T) accumulated in float32 -- the same rounding points as the GEMM form.
 __global__ __launch_bounds__(256) void k_muon_ns_vec(uint16_t* __restrict__ x, int64_t n,
-                                                     int32_t steps, float ca, float cb,
-                                                     float cc)
+                                                     int64_t stride, int32_t steps, float ca,
+                                                     float cb, float cc)
 {
     __shared__ float red[256];
-    uint16_t* __restrict__ v = x + static_cast<int64_t>(blockIdx.x) * n;
+    uint16_t* __restrict__ v = x + static_cast<int64_t>(blockIdx.x) * stride;
     for (int32_t it = 0; it < steps; ++it) {
         float acc = 0.0f;
         for (int64_t i = threadIdx.x; i < n; i += 256) {
@@ -545,86 +339,12 @@ hipError_t launch_muon_norm(const float* tile_ss, const int64_t* tile_range, int
     return hipGetLastError();
 }
 
-static dim3 flat_grid(int64_t n, int batch)
-{
-    int64_t g = (n + 2047) / 2048;
-    if (g > 4096) g = 4096;
-    if (g < 1) g = 1;
-    return dim3(static_cast<unsigned>(g), static_cast<unsigned>(batch));
-}
-
-hipError_t launch_muon_prep(const uint16_t* u, const Seg* segs, const int32_t* tensor_of,
-                            int32_t batch, const float* norm, int64_t n, uint16_t* x,
-                            hipStream_t stream)
-{
-    if (batch <= 0 || n <= 0) return hipSuccess;
-    if (batch > 65535) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_muon_prep_flat, flat_grid(n, batch), dim3(256), 0, stream, u, segs,
-                       tensor_of, norm, n, x);
-    return hipGetLastError();
-}
-
-hipError_t launch_muon_update(const uint16_t* o, const Seg* segs, const int32_t* tensor_of,
-                              int32_t batch, int64_t n, float decay, float step,
-                              hipStream_t stream)
-{
-    if (batch <= 0 || n <= 0) return hipSuccess;
-    if (batch > 65535) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_muon_update_flat, flat_grid(n, batch), dim3(256), 0, stream, o, segs,
-                       tensor_of, n, decay, step);
-    return hipGetLastError();
-}
-
-static bool t_grid(int64_t R, int64_t C, int32_t batch, dim3& grid)
-{
-    const int64_t gx = (C + kTile - 1) / kTile;
-    const int64_t gy = (R + kTile * kTilesPerGroup - 1) / (kTile * kTilesPerGroup);
-    if (gx > 0x7fffffffLL || gy > 65535 || batch > 65535) return false;
-    grid = dim3(static_cast<unsigned>(gx), static_cast<unsigned>(gy), static_cast<unsigned>(batch));
-    return true;
-}
-
-hipError_t launch_muon_prep_t(const uint16_t* u, const Seg* segs, const int32_t* tensor_of,
-                              int32_t batch, const float* norm, int64_t R, int64_t C,
-                              int64_t ldx, uint16_t* x, hipStream_t stream)
-{
-    if (batch <= 0 || R <= 0 || C <= 0) return hipSuccess;
-    dim3 grid;
-    if (ldx < R || (ldx & 7) != 0 || !t_grid(ldx, C, batch, grid)) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_muon_prep_t, grid, dim3(256), 0, stream, u, segs, tensor_of, norm, R,
-                       C, ldx, x);
-    return hipGetLastError();
-}
-
-hipError_t launch_muon_update_t(const uint16_t* o, const Seg* segs, const int32_t* tensor_of,
-                                int32_t batch, int64_t R, int64_t C, int64_t ldx, float decay,
-                                float step, hipStream_t stream)
-{
-    if (batch <= 0 || R <= 0 || C <= 0) return hipSuccess;
-    dim3 grid;
-    if (ldx < R || (ldx & 7) != 0 || !t_grid(R, C, batch, grid)) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_muon_update_t, grid, dim3(256), 0, stream, o, segs, tensor_of, R, C,
-                       ldx, decay, step);
-    return hipGetLastError();
-}
-
-hipError_t launch_muon_splitk_sum(const float* partial, int32_t splits, int64_t mm,
-                                  uint16_t* a, hipStream_t stream)
-{
-    if (mm <= 0) return hipSuccess;
-    int64_t g = (mm + 255) / 256;
-    if (g > 65536) g = 65536;
-    hipLaunchKernelGGL(k_muon_splitk_sum, dim3(static_cast<unsigned>(g)), dim3(256), 0, stream,
-                       partial, splits, mm, a);
-    return hipGetLastError();
-}
-
-hipError_t launch_muon_ns_vec(uint16_t* x, int32_t batch, int64_t n, int32_t steps, float a,
-                              float b, float c, hipStream_t stream)
+hipError_t launch_muon_ns_vec(uint16_t* x, int32_t batch, int64_t n, int64_t stride, int32_t steps,
+                              float a, float b, float c, hipStream_t stream)
 {
     if (batch <= 0 || steps <= 0) return hipSuccess;
     hipLaunchKernelGGL(k_muon_ns_vec, dim3(static_cast<unsigned>(batch)), dim3(256), 0, stream,
-                       x, n, steps, a, b, c);
+                       x, n, stride, steps, a, b, c);
     return hipGetLastError();
 }
 

@@ -1,8 +1,9 @@
 // Gefen-Muon launchers (appendix "Gefen-Muon"): the quantized-momentum codec, the
-// per-tensor Frobenius norm, the normalised bfloat16 Newton-Schulz input, the split-K
-// sum, the 1 x n Newton-Schulz kernel and the parameter update.
+// per-tensor Frobenius norm, the 1 x n Newton-Schulz kernel, and the matrix-core
+// Newton-Schulz products with the kernels that move matrices into and out of their layout.
 #pragma once
 #include "gefen_internal.h"
+#include "ns_plan.h"
 
 namespace gefen {
 
@@ -18,30 +19,29 @@ hipError_t launch_muon_codec(int code_bits, int gdtype, const Tile* tiles, int64
 // norm[t] = max(bf16(sqrt(sum of tile_ss over [tile_range[2t], tile_range[2t+1]))), eps_bf16)
 hipError_t launch_muon_norm(const float* tile_ss, const int64_t* tile_range, int32_t n_tensors,
                             float eps_bf16, float* norm, hipStream_t stream);
-// x[b] = bf16(u of tensor tensor_of[b] / norm[tensor]), n elements in the tensor's own
-// row-major layout
-hipError_t launch_muon_prep(const uint16_t* u, const Seg* segs, const int32_t* tensor_of,
-                            int32_t batch, const float* norm, int64_t n, uint16_t* x,
-                            hipStream_t stream);
-// Tall matrices (R > C > 1): x[b] (C x ldx row-major, ldx >= R, ldx % 8 == 0) =
-// bf16(U^T / norm), U the R x C momentum matrix of tensor tensor_of[b], zero in
-// columns R .. ldx - 1
-hipError_t launch_muon_prep_t(const uint16_t* u, const Seg* segs, const int32_t* tensor_of,
-                              int32_t batch, const float* norm, int64_t R, int64_t C,
-                              int64_t ldx, uint16_t* x, hipStream_t stream);
-// theta (R x C) of tensor_of[b] = theta * decay - step * O^T, O = o[b] (C x ldx)
-hipError_t launch_muon_update_t(const uint16_t* o, const Seg* segs, const int32_t* tensor_of,
-                                int32_t batch, int64_t R, int64_t C, int64_t ldx, float decay,
-                                float step, hipStream_t stream);
-// a (mm bfloat16) = bf16(sum of `splits` float32 partial products, in order)
-hipError_t launch_muon_splitk_sum(const float* partial, int32_t splits, int64_t mm,
-                                  uint16_t* a, hipStream_t stream);
-// `steps` Newton-Schulz iterations in place on `batch` 1 x n bfloat16 rows
-hipError_t launch_muon_ns_vec(uint16_t* x, int32_t batch, int64_t n, int32_t steps, float a,
-                              float b, float c, hipStream_t stream);
-// theta of tensor_of[b] = theta * decay - step * o[b], n elements, the tensor's layout
-hipError_t launch_muon_update(const uint16_t* o, const Seg* segs, const int32_t* tensor_of,
-                              int32_t batch, int64_t n, float decay, float step,
-                              hipStream_t stream);
+// `steps` Newton-Schulz iterations in place on `batch` 1 x n bfloat16 rows, row b at
+// x + b * stride
+hipError_t launch_muon_ns_vec(uint16_t* x, int32_t batch, int64_t n, int64_t stride, int32_t steps,
+                              float a, float b, float c, hipStream_t stream);
+
+// Newton-Schulz on the matrix cores (ns_gemm.hip; layout and products in ns_plan.h).
+// One batched product (and, when split over K, the in-order sum of its chunks).
+hipError_t launch_ns_gemm(const NsGemmArgs& a, hipStream_t stream);
+// Batch entry b takes tensor t = tensor_of ? tensor_of[b] : b, whose R x C matrix starts at
+// src + (src_off ? src_off[t] : b * R * C), divided by norm[t] (norm null: 1); writes
+// copy[b] (R x round8(C)) = S / norm and trans[b] (C x round8(R)) = (S / norm)^T, zero
+// padded, at batch strides copy_stride and trans_stride (elements, multiples of 8).
+hipError_t launch_ns_prep(const uint16_t* src, const int64_t* src_off, const int32_t* tensor_of,
+                          const float* norm, int32_t batch, int64_t R, int64_t C, uint16_t* copy,
+                          int64_t copy_stride, uint16_t* trans, int64_t trans_stride,
+                          hipStream_t stream);
+// theta of tensor tensor_of[b] (R x C) = theta * decay - step * S[b], S[b] the R x C matrix
+// of row stride ss at o + b * stride
+hipError_t launch_ns_update(const uint16_t* o, int64_t stride, int64_t ss, const Seg* segs,
+                            const int32_t* tensor_of, int32_t batch, int64_t R, int64_t C,
+                            float decay, float step, hipStream_t stream);
+// dst[b] (R x C, dense) = the R x C matrix of row stride ss at src + b * stride
+hipError_t launch_ns_unpad(const uint16_t* src, int64_t stride, int64_t ss, int32_t batch,
+                           int64_t R, int64_t C, uint16_t* dst, hipStream_t stream);
 
 }  // namespace gefen

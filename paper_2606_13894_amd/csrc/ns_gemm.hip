@@ -1,0 +1,414 @@
+// Newton-Schulz products of Gefen-Muon (appendix "Gefen-Muon") on the CDNA4 matrix
+// cores, and the kernels that bring the momentum matrices into and out of their layout
+// (ns_plan.h gives the layout and the three products of an iteration).
+//
+// The product kernel: one 256-thread workgroup computes a 128 x 128 output tile of one
+// batch entry (and one K chunk when split). Its four waves own 64 x 64 quarters, each
+// made of 2 x 2 v_mfma_f32_32x32x16_bf16 accumulators (float32). Both operands are read
+// along contiguous K, 16 bytes per thread, into LDS tiles of 128 rows x 64 K (rows padded
+// to 72 elements so that the 16-byte fragment reads of 16 consecutive rows hit distinct
+// banks); two LDS stages: the next stage's global loads are in flight while the current
+// one feeds the matrix cores, with one barrier per stage. The epilogue forms
+// alpha * C + beta * E in float32, rounds once to bfloat16 (round to nearest even, as the
+// float32-accumulating GEMMs of the implementation the paper uses), stages the tile in LDS
+// for 16-byte row stores of O, and writes the transposed tile (or, for the symmetric
+// products, the mirror) straight from the accumulators, four rows per 8-byte store.
+// Work items are dealt to the eight XCDs in contiguous runs, so the tiles of one batch
+// entry share an XCD's L2.
+#include "muon_internal.h"
+#include "ns_plan.h"
+
+namespace gefen {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4v __attribute__((ext_vector_type(4)));
+
+constexpr int BM = kNsTile, BN = kNsTile, BK = kNsBK;
+constexpr int LDK = BK + 8;      // LDS row stride of the operand tiles (elements)
+constexpr int LDT = BN + 8;      // LDS row stride of the epilogue tile (elements)
+constexpr int kLdsElems = 2 * (BM + BN) * LDK;
+static_assert(BM * LDT <= kLdsElems, "epilogue tile fits the operand LDS");
+
+__device__ __forceinline__ float bf16_val(uint16_t b)
+{
+    return __uint_as_float(static_cast<uint32_t>(b) << 16);
+}
+
+// float32 -> bfloat16, round to nearest even; NaN stays NaN.
+__device__ __forceinline__ uint16_t to_bf16(float x)
+{
+    const uint32_t b = __float_as_uint(x);
+    if ((b & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((b >> 16) | 0x40u);
+    return static_cast<uint16_t>((b + 0x7FFFu + ((b >> 16) & 1u)) >> 16);
+}
+
+__global__ __launch_bounds__(kNsThreads, 2) void k_ns_gemm(const NsGemmArgs a)
+{
+    __shared__ __attribute__((aligned(16))) uint16_t lds[kLdsElems];
+    const int64_t total = int64_t(a.batch) * a.splits * a.tiles;
+    const int64_t per_xcd = (total + 7) / 8;
+    const int64_t wid = static_cast<int64_t>(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+    if (wid >= total) return;
+    const NsWork w = ns_decode(a, wid);
+    const int64_t row0 = int64_t(w.ti) * BM, col0 = int64_t(w.tj) * BN;
+    const int64_t kbeg = int64_t(w.s) * a.kchunk;
+    const int64_t kend = a.splits > 1 ? min(int64_t(a.K), kbeg + a.kchunk) : int64_t(a.K);
+    const uint16_t* __restrict__ P = a.p + w.b * a.sp;
+    const uint16_t* __restrict__ Q = a.q + w.b * a.sq;
+
+    const int tid = threadIdx.x;
+    const int lrow = tid >> 3, lk = (tid & 7) * 8;   // loader: 8 threads per 64-element row
+    u32x4 ra[4], rb[4];
+    auto gload = [&](int64_t k0) {
+        const int64_t kk = k0 + lk;
+        const bool kin = kk < kend;   // kend % 8 == 0: a vector is all in or all out
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int64_t gi = row0 + lrow + 32 * r;
+            const int64_t gj = col0 + lrow + 32 * r;
+            const u32x4 z = {0u, 0u, 0u, 0u};
+            ra[r] = (kin && gi < a.M) ? *reinterpret_cast<const u32x4*>(P + gi * a.ldp + kk) : z;
+            rb[r] = (kin && gj < a.N) ? *reinterpret_cast<const u32x4*>(Q + gj * a.ldq + kk) : z;
+        }
+    };
+    auto lstore = [&](int buf) {
+        uint16_t* sa = lds + buf * (BM + BN) * LDK;
+        uint16_t* sb = sa + BM * LDK;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            *reinterpret_cast<u32x4*>(sa + (lrow + 32 * r) * LDK + lk) = ra[r];
+            *reinterpret_cast<u32x4*>(sb + (lrow + 32 * r) * LDK + lk) = rb[r];
+        }
+    };
+
+    const int lane = tid & 63, wave = tid >> 6;
+    const int wm = (wave >> 1) * 64, wn = (wave & 1) * 64;
+    const int frow = lane & 31, fk = (lane >> 5) * 8;
+    f32x16 acc[2][2];
+#pragma unroll
+    for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < 2; ++ni)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[mi][ni][v] = 0.0f;
+
+    const int64_t nk = (kend - kbeg + BK - 1) / BK;
+    gload(kbeg);
+    lstore(0);
+    __syncthreads();
+    for (int64_t it = 0; it < nk; ++it) {
+        if (it + 1 < nk) gload(kbeg + (it + 1) * BK);
+        const uint16_t* sa = lds + (it & 1) * (BM + BN) * LDK;
+        const uint16_t* sb = sa + BM * LDK;
+#pragma unroll
+        for (int kk = 0; kk < BK; kk += 16) {
+            bf16x8 fa[2], fb[2];
+#pragma unroll
+            for (int mi = 0; mi < 2; ++mi)
+                fa[mi] = __builtin_bit_cast(
+                    bf16x8, *reinterpret_cast<const u32x4*>(sa + (wm + mi * 32 + frow) * LDK + kk + fk));
+#pragma unroll
+            for (int ni = 0; ni < 2; ++ni)
+                fb[ni] = __builtin_bit_cast(
+                    bf16x8, *reinterpret_cast<const u32x4*>(sb + (wn + ni * 32 + frow) * LDK + kk + fk));
+#pragma unroll
+            for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+                for (int ni = 0; ni < 2; ++ni)
+                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[mi], fb[ni],
+                                                                        acc[mi][ni], 0, 0, 0);
+        }
+        if (it + 1 < nk) lstore((it + 1) & 1);
+        __syncthreads();
+    }
+
+    // Accumulator element v of block (mi, ni): row (v / 4) * 8 + (lane / 32) * 4 + v % 4,
+    // column lane % 32 of the 32 x 32 block.
+    if (a.splits > 1) {
+        float* __restrict__ part = a.partial + ((int64_t(w.s) * a.batch + w.b) * a.M) * a.N;
+#pragma unroll
+        for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+            for (int ni = 0; ni < 2; ++ni) {
+                const int64_t j = col0 + wn + ni * 32 + frow;
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int64_t i = row0 + wm + mi * 32 + (v >> 2) * 8 + fk / 2 + (v & 3);
+                    if (i < a.M && j < a.N) part[i * a.N + j] = acc[mi][ni][v];
+                }
+            }
+        return;
+    }
+
+    const uint16_t* __restrict__ Et = a.et ? a.et + w.b * a.se : nullptr;
+    uint16_t* __restrict__ Ot = a.ot ? a.ot + w.b * a.sot : nullptr;
+    const bool mirror = Ot && (!a.sym || w.ti != w.tj);
+    uint16_t* stage = lds;   // BM x LDT, free after the last barrier of the main loop
+#pragma unroll
+    for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < 2; ++ni) {
+            const int64_t j = col0 + wn + ni * 32 + frow;
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int lr = wm + mi * 32 + g * 8 + fk / 2;   // local row of element 0
+                const int64_t i0 = row0 + lr;
+                float e[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+                if (Et && j < a.N && i0 < a.M) {
+                    const uint16_t* src = Et + j * a.lde + i0;
+                    if (i0 + 4 <= a.M) {
+                        const u32x2 wv = *reinterpret_cast<const u32x2*>(src);
+                        e[0] = bf16_val(static_cast<uint16_t>(wv.x & 0xffffu));
+                        e[1] = bf16_val(static_cast<uint16_t>(wv.x >> 16));
+                        e[2] = bf16_val(static_cast<uint16_t>(wv.y & 0xffffu));
+                        e[3] = bf16_val(static_cast<uint16_t>(wv.y >> 16));
+                    } else {
+                        for (int q = 0; q < 4; ++q)
+                            if (i0 + q < a.M) e[q] = bf16_val(src[q]);
+                    }
+                }
+                uint16_t h[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    h[q] = to_bf16(fmaf(a.alpha, acc[mi][ni][g * 4 + q], a.beta * e[q]));
+                if (mirror && j < a.N && i0 < a.ot_cols) {
+                    uint16_t* dst = Ot + j * a.ldot + i0;
+                    if (i0 + 4 <= a.ot_cols) {
+                        u32x2 wv;
+                        wv.x = uint32_t(h[0]) | (uint32_t(h[1]) << 16);
+                        wv.y = uint32_t(h[2]) | (uint32_t(h[3]) << 16);
+                        *reinterpret_cast<u32x2*>(dst) = wv;
+                    } else {
+                        for (int q = 0; q < 4; ++q)
+                            if (i0 + q < a.ot_cols) dst[q] = h[q];
+                    }
+                }
+                if (a.o) {
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        stage[(lr + q) * LDT + wn + ni * 32 + frow] = h[q];
+                }
+            }
+        }
+    if (!a.o) return;
+    __syncthreads();
+    uint16_t* __restrict__ O = a.o + w.b * a.so;
+    const int sc = (tid & 15) * 8;
+#pragma unroll
+    for (int pass = 0; pass < BM / 16; ++pass) {
+        const int sr = pass * 16 + (tid >> 4);
+        const int64_t i = row0 + sr, j = col0 + sc;
+        if (i < a.M && j < a.o_cols)
+            *reinterpret_cast<u32x4*>(O + i * a.ldo + j) =
+                *reinterpret_cast<const u32x4*>(stage + sr * LDT + sc);
+    }
+}
+
+// Split-K Gram: O[b][i][j] = bf16(alpha * sum over chunks s (in order) of the float32
+// partial of the upper-tile element (i, j) or, below the diagonal tiles, (j, i)); zero in
+// the padding columns M .. o_cols - 1.
+__global__ __launch_bounds__(256) void k_ns_reduce(const NsGemmArgs a)
+{
+    const int64_t per_b = int64_t(a.M) * a.o_cols;
+    const int64_t total = per_b * a.batch;
+    for (int64_t e = blockIdx.x * 256LL + threadIdx.x; e < total; e += 256LL * gridDim.x) {
+        const int64_t b = e / per_b;
+        const int64_t r = e - b * per_b;
+        const int64_t i = r / a.o_cols, j = r - i * a.o_cols;
+        float sum = 0.0f;
+        if (j < a.N) {
+            const bool upper = i / BM <= j / BN;
+            const int64_t ii = upper ? i : j, jj = upper ? j : i;
+            for (int32_t s = 0; s < a.splits; ++s)
+                sum += a.partial[((int64_t(s) * a.batch + b) * a.M + ii) * a.N + jj];
+            sum *= a.alpha;
+        }
+        a.o[b * a.so + i * a.ldo + j] = to_bf16(sum);
+    }
+}
+
+// ---------------------------------------------------------------------------------
+// Into and out of the layout. A lane moves an 8 x 8 block of a source matrix S (R x C,
+// row-major, dense): lane l of a wave takes rows 8 (l / 8) .. + 7 and columns
+// 8 (l % 8) .. + 7 of a 64 x 64 tile (a workgroup holds 4 tiles along R), so its row
+// loads and the row stores of the copy and of the transpose each join seven neighbouring
+// lanes' into 128 contiguous bytes.
+// ---------------------------------------------------------------------------------
+constexpr int kTile = 64;
+constexpr int kTilesPerGroup = 4;
+
+// Element j (0..7) of eight packed bfloat16.
+__device__ __forceinline__ uint32_t bf16_at(const u32x4& w, int j)
+{
+    const uint32_t v = w[j >> 1];
+    return (j & 1) ? (v >> 16) : (v & 0xffffu);
+}
+
+// Batch entry b takes tensor t = tensor_of ? tensor_of[b] : b, whose R x C matrix starts at
+// src + src_off[t] (src_off null: src + b R C; bfloat16), divided by norm[t] (norm null:
+// 1). Writes, with zero padding,
+// copy[b] (R x cs, cs = C rounded up to 8) = S / norm and trans[b] (C x ts, ts = R rounded up
+// to 8) = (S / norm)^T; copy_stride / trans_stride are the batch strides.
+__global__ __launch_bounds__(256) void k_ns_prep(const uint16_t* __restrict__ src,
+                                                 const int64_t* __restrict__ src_off,
+                                                 const int32_t* __restrict__ tensor_of,
+                                                 const float* __restrict__ norm, int64_t R,
+                                                 int64_t C, uint16_t* __restrict__ copy,
+                                                 int64_t copy_stride,
+                                                 uint16_t* __restrict__ trans,
+                                                 int64_t trans_stride)
+{
+    const int b = blockIdx.z;
+    const int t = tensor_of ? tensor_of[b] : b;
+    const uint16_t* __restrict__ s = src + (src_off ? src_off[t] : b * R * C);
+    const float nrm = norm ? norm[t] : 1.0f;
+    const int64_t cs = (C + 7) / 8 * 8, ts = (R + 7) / 8 * 8;
+    uint16_t* __restrict__ cp = copy + b * copy_stride;
+    uint16_t* __restrict__ tp = trans + b * trans_stride;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t r0 = (static_cast<int64_t>(blockIdx.y) * kTilesPerGroup + wave) * kTile +
+                       8 * (lane >> 3);
+    const int64_t c0 = static_cast<int64_t>(blockIdx.x) * kTile + 8 * (lane & 7);
+    if (r0 >= ts || c0 >= cs) return;
+    u32x4 w[8];
+    const bool vec = r0 + 8 <= R && c0 + 8 <= C && (C & 7) == 0 &&
+                     (reinterpret_cast<uintptr_t>(s) & 15) == 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        if (vec) {
+            w[j] = *reinterpret_cast<const u32x4*>(s + (r0 + j) * C + c0);
+        } else {
+            for (int q = 0; q < 4; ++q) {
+                const int64_t r = r0 + j, c = c0 + 2 * q;
+                const uint32_t lo = (r < R && c < C) ? s[r * C + c] : 0u;
+                const uint32_t hi = (r < R && c + 1 < C) ? s[r * C + c + 1] : 0u;
+                w[j][q] = lo | (hi << 16);
+            }
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const uint32_t lo = to_bf16(bf16_val(static_cast<uint16_t>(w[j][q] & 0xffffu)) / nrm);
+            const uint32_t hi = to_bf16(bf16_val(static_cast<uint16_t>(w[j][q] >> 16)) / nrm);
+            w[j][q] = lo | (hi << 16);
+        }
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+        if (r0 + j < R) *reinterpret_cast<u32x4*>(cp + (r0 + j) * cs + c0) = w[j];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+        if (c0 + k >= C) break;
+        u32x4 o;
+#pragma unroll
+        for (int p = 0; p < 4; ++p) o[p] = bf16_at(w[2 * p], k) | (bf16_at(w[2 * p + 1], k) << 16);
+        *reinterpret_cast<u32x4*>(tp + (c0 + k) * ts + r0) = o;
+    }
+}
+
+// theta of tensor tensor_of[b] (R x C, dense) = theta * decay - step * S[b], where S[b] is
+// R x C with row stride ss (a multiple of 8) at o + b * stride.
+__global__ __launch_bounds__(256) void k_ns_update(const uint16_t* __restrict__ o, int64_t stride,
+                                                   int64_t ss, const Seg* __restrict__ segs,
+                                                   const int32_t* __restrict__ tensor_of,
+                                                   int64_t R, int64_t C, float decay, float step)
+{
+    const int b = blockIdx.y;
+    float* __restrict__ th = segs[tensor_of[b]].theta;
+    const uint16_t* __restrict__ src = o + b * stride;
+    const int64_t n = R * C;
+    const int64_t gstride = 256LL * gridDim.x;
+    if ((C & 3) == 0 && (reinterpret_cast<uintptr_t>(th) & 15) == 0) {
+        for (int64_t v = blockIdx.x * 256LL + threadIdx.x; v < n / 4; v += gstride) {
+            const int64_t e = 4 * v, r = e / C, c = e - r * C;
+            const u32x2 wv = *reinterpret_cast<const u32x2*>(src + r * ss + c);
+            f32x4v tv = reinterpret_cast<const f32x4v*>(th)[v];
+            tv.x = fmaf(-step, bf16_val(static_cast<uint16_t>(wv.x & 0xffffu)), tv.x * decay);
+            tv.y = fmaf(-step, bf16_val(static_cast<uint16_t>(wv.x >> 16)), tv.y * decay);
+            tv.z = fmaf(-step, bf16_val(static_cast<uint16_t>(wv.y & 0xffffu)), tv.z * decay);
+            tv.w = fmaf(-step, bf16_val(static_cast<uint16_t>(wv.y >> 16)), tv.w * decay);
+            reinterpret_cast<f32x4v*>(th)[v] = tv;
+        }
+    } else {
+        for (int64_t e = blockIdx.x * 256LL + threadIdx.x; e < n; e += gstride) {
+            const int64_t r = e / C, c = e - r * C;
+            th[e] = fmaf(-step, bf16_val(src[r * ss + c]), th[e] * decay);
+        }
+    }
+}
+
+// dst[b] (R x C, dense) = S[b] (R x C, row stride ss, at src + b * stride).
+__global__ __launch_bounds__(256) void k_ns_unpad(const uint16_t* __restrict__ src, int64_t stride,
+                                                  int64_t ss, int64_t R, int64_t C,
+                                                  uint16_t* __restrict__ dst)
+{
+    const int b = blockIdx.y;
+    const int64_t n = R * C;
+    for (int64_t e = blockIdx.x * 256LL + threadIdx.x; e < n; e += 256LL * gridDim.x) {
+        const int64_t r = e / C, c = e - r * C;
+        dst[b * n + e] = src[b * stride + r * ss + c];
+    }
+}
+
+}  // namespace
+
+hipError_t launch_ns_gemm(const NsGemmArgs& a, hipStream_t stream)
+{
+    const int64_t groups = ns_workgroups(a);
+    hipLaunchKernelGGL(k_ns_gemm, dim3(static_cast<unsigned>(groups)), dim3(kNsThreads), 0, stream,
+                       a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || a.splits == 1) return e;
+    const int64_t total = int64_t(a.M) * a.o_cols * a.batch;
+    const int64_t g = std::min<int64_t>((total + 255) / 256, 4096);
+    hipLaunchKernelGGL(k_ns_reduce, dim3(static_cast<unsigned>(g)), dim3(256), 0, stream, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_ns_prep(const uint16_t* src, const int64_t* src_off, const int32_t* tensor_of,
+                          const float* norm, int32_t batch, int64_t R, int64_t C, uint16_t* copy,
+                          int64_t copy_stride, uint16_t* trans, int64_t trans_stride,
+                          hipStream_t stream)
+{
+    const int64_t ts = (R + 7) / 8 * 8, cs = (C + 7) / 8 * 8;
+    const int64_t gx = (cs + kTile - 1) / kTile;
+    const int64_t gy = (ts + kTile * kTilesPerGroup - 1) / (kTile * kTilesPerGroup);
+    if (gx > 0x7fffffff || gy > 65535 || batch > 65535) return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL(k_ns_prep, dim3(static_cast<unsigned>(gx), static_cast<unsigned>(gy), batch),
+                       dim3(256), 0, stream, src, src_off, tensor_of, norm, R, C, copy,
+                       copy_stride, trans, trans_stride);
+    return hipGetLastError();
+}
+
+static dim3 ns_flat_grid(int64_t n, int32_t batch)
+{
+    int64_t g = (n / 4 + 255) / 256;
+    g = std::max<int64_t>(1, std::min<int64_t>(g, 4096));
+    return dim3(static_cast<unsigned>(g), static_cast<unsigned>(batch));
+}
+
+hipError_t launch_ns_update(const uint16_t* o, int64_t stride, int64_t ss, const Seg* segs,
+                            const int32_t* tensor_of, int32_t batch, int64_t R, int64_t C,
+                            float decay, float step, hipStream_t stream)
+{
+    if (batch > 65535) return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL(k_ns_update, ns_flat_grid(R * C, batch), dim3(256), 0, stream, o, stride, ss,
+                       segs, tensor_of, R, C, decay, step);
+    return hipGetLastError();
+}
+
+hipError_t launch_ns_unpad(const uint16_t* src, int64_t stride, int64_t ss, int32_t batch, int64_t R,
+                           int64_t C, uint16_t* dst, hipStream_t stream)
+{
+    if (batch > 65535) return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL(k_ns_unpad, ns_flat_grid(4 * R * C, batch), dim3(256), 0, stream, src, stride,
+                       ss, R, C, dst);
+    return hipGetLastError();
+}
+
+}  // namespace gefen

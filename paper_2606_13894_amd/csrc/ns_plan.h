@@ -1,0 +1,470 @@
+// Planning of the Newton-Schulz products of Gefen-Muon (appendix "Gefen-Muon": Muon's
+// orthogonalisation X <- a X + (b A + c A A) X, A = X X^T, on bfloat16 matrices).
+// Plain C++ with no HIP types, so that host-only tests can build and check it.
+//
+// Layout of one shape group of `count` wide matrices (m rows <= n columns):
+//   X   count x m x ldx   row-major, ldx = n rounded up to 8, zero in columns n .. ldx-1
+//   Xt  count x ldx x ldm row-major X^T, ldm = m rounded up to 8, zero in columns m ..
+//       ldm-1 (rows n .. ldx-1 are never read)
+//   A   count x m x ldm   (A = X X^T, symmetric), zero in columns m .. ldm-1
+//   B   count x m x ldm   (B = b A + c A A, symmetric), same padding
+// Every product reads both operands along contiguous K:
+//   Gram     A = X X^T     P = X, Q = X, K = ldx, symmetric (upper tiles, mirrored)
+//   Poly     B = c A A + b A   P = Q = A (A A = A A^T), K = ldm, E = A, symmetric
+//   Combine  X' = B X + a X    P = B, Q = Xt (X[k][j] = Xt[j][k]), K = ldm, E^T = Xt;
+//            writes X' and X'^T (the next iteration's Xt)
+#pragma once
+
+#include <stdint.h>
+
+#include <algorithm>
+#include <cstdio>
+#include <string>
+#include <vector>
+
+#if defined(__HIPCC__)
+#define NS_HOST_DEVICE __host__ __device__
+#else
+#define NS_HOST_DEVICE
+#endif
+
+namespace gefen {
+
+constexpr int kNsTile = 128;   // output rows and columns of one workgroup
+constexpr int kNsBK = 64;      // K of one pipeline stage
+constexpr int kNsThreads = 256;
+
+// One batched product C[i][j] = sum_k P[i][k] Q[j][k] (i < M, j < N, k < K), then
+//   value(i, j) = bf16(alpha * C[i][j] + beta * E[i][j]),  E[i][j] = et[j * lde + i]
+// (E absent: beta ignored), written to O[i][j] (i < M, j < o_cols; columns N .. o_cols-1
+// are zero) and to Ot[j][i] (j < N, i < ot_cols; zero for i >= M). Symmetric mode
+// (M == N, P == Q): only the tiles on and above the diagonal run, and each tile above
+// it also writes its mirror through Ot (= O, ot_cols = M). Split-K (splits > 1,
+// symmetric, no E): workgroup s of a tile sums K range [s * kchunk, (s+1) * kchunk) and
+// writes float32 partial[((s * batch + b) * M + i) * N + j]; ns_reduce adds the chunks in
+// order and writes O.
+struct NsGemmArgs {
+    const uint16_t* p;
+    int64_t ldp, sp;
+    const uint16_t* q;
+    int64_t ldq, sq;
+    const uint16_t* et;
+    int64_t lde, se;
+    uint16_t* o;
+    int64_t ldo, so;
+    uint16_t* ot;
+    int64_t ldot, sot;
+    float* partial;
+    int32_t M, N, K;
+    int32_t o_cols, ot_cols;
+    int32_t batch, sym, splits;
+    int32_t tm, tn;       // tiles along M and along N
+    int32_t tiles;        // tiles per batch entry (symmetric: tm (tm + 1) / 2)
+    int32_t kchunk;       // split-K chunk (a multiple of kNsBK); K when splits == 1
+    float alpha, beta;
+};
+
+inline int64_t ns_round8(int64_t v) { return (v + 7) / 8 * 8; }
+inline int32_t ns_tiles_along(int64_t v) { return static_cast<int32_t>((v + kNsTile - 1) / kNsTile); }
+
+// Sizes of one shape group.
+struct NsShape {
+    int64_t count, m, n, ldx, ldm;
+    int32_t splits;   // K chunks of the Gram product
+    int32_t kchunk;   // their length (a multiple of kNsBK; ldx when splits == 1)
+};
+
+// Split the Gram product over K when the group's upper tiles leave most compute units
+// idle (a lone tall-skinny matrix such as a token embedding: 21 tiles at m = 768), into
+// at most 16 chunks of at least 8 stages each.
+inline int32_t ns_gram_splits(int64_t count, int64_t m, int64_t ldx)
+{
+    const int64_t t = ns_tiles_along(m);
+    const int64_t work = count * t * (t + 1) / 2;
+    if (work >= 256) return 1;
+    int64_t s = (512 + work - 1) / work;
+    s = std::min<int64_t>(s, 16);
+    s = std::min<int64_t>(s, ldx / (8 * kNsBK));
+    return static_cast<int32_t>(std::max<int64_t>(s, 1));
+}
+
+inline NsShape ns_shape(int64_t count, int64_t m, int64_t n)
+{
+    NsShape s{count, m, n, ns_round8(n), ns_round8(m), 1, 0};
+    s.splits = m > 1 ? ns_gram_splits(count, m, s.ldx) : 1;   // vectors have no Gram product
+    s.kchunk = static_cast<int32_t>(s.ldx);
+    if (s.splits > 1) {
+        // equal chunks of whole stages; the last one may be shorter, none is empty
+        const int64_t chunk = (s.ldx + s.splits - 1) / s.splits;
+        s.kchunk = static_cast<int32_t>((chunk + kNsBK - 1) / kNsBK * kNsBK);
+        s.splits = static_cast<int32_t>((s.ldx + s.kchunk - 1) / s.kchunk);
+        if (s.splits < 2) s.kchunk = static_cast<int32_t>(s.ldx);
+    }
+    return s;
+}
+
+// Elements each lane buffer needs for a group.
+inline int64_t ns_x_elems(const NsShape& s) { return s.count * s.ldx * s.ldm; }   // X, Xt
+inline int64_t ns_a_elems(const NsShape& s) { return s.count * s.m * s.ldm; }     // A, B
+inline int64_t ns_partial_elems(const NsShape& s)
+{
+    return s.splits > 1 ? int64_t(s.splits) * s.count * s.m * s.m : 0;
+}
+
+inline void ns_fill_tiles(NsGemmArgs& a)
+{
+    a.tm = ns_tiles_along(a.M);
+    a.tn = ns_tiles_along(a.N);
+    a.tiles = a.sym ? a.tm * (a.tm + 1) / 2 : a.tm * a.tn;
+}
+
+// Work item `wid` of a product: batch entry, K chunk and output tile (row and column
+// tile). Work items run batch-major, then chunk, then tile; symmetric products number
+// their upper tiles row by row.
+struct NsWork {
+    int64_t b;
+    int32_t s, ti, tj;
+};
+
+inline NS_HOST_DEVICE NsWork ns_decode(const NsGemmArgs& a, int64_t wid)
+{
+    NsWork w;
+    const int64_t per_b = int64_t(a.splits) * a.tiles;
+    w.b = wid / per_b;
+    const int32_t r = static_cast<int32_t>(wid - w.b * per_b);
+    w.s = r / a.tiles;
+    int32_t t = r - w.s * a.tiles;
+    if (a.sym) {
+        int32_t ti = 0;
+        while (t >= a.tm - ti) {
+            t -= a.tm - ti;
+            ++ti;
+        }
+        w.ti = ti;
+        w.tj = ti + t;
+    } else {
+        w.ti = t / a.tn;
+        w.tj = t - w.ti * a.tn;
+    }
+    return w;
+}
+
+inline NsGemmArgs ns_gram_args(const NsShape& s, const uint16_t* x, uint16_t* a_out,
+                               float* partial)
+{
+    NsGemmArgs a{};
+    a.p = a.q = x;
+    a.ldp = a.ldq = s.ldx;
+    a.sp = a.sq = s.m * s.ldx;
+    a.o = a.ot = a_out;
+    a.ldo = a.ldot = s.ldm;
+    a.so = a.sot = s.m * s.ldm;
+    a.M = a.N = static_cast<int32_t>(s.m);
+    a.K = static_cast<int32_t>(s.ldx);
+    a.o_cols = static_cast<int32_t>(s.ldm);
+    a.ot_cols = static_cast<int32_t>(s.m);
+    a.batch = static_cast<int32_t>(s.count);
+    a.sym = 1;
+    a.splits = s.splits;
+    a.alpha = 1.0f;
+    a.beta = 0.0f;
+    a.kchunk = s.kchunk;
+    if (s.splits > 1) a.partial = partial;
+    ns_fill_tiles(a);
+    return a;
+}
+
+inline NsGemmArgs ns_poly_args(const NsShape& s, const uint16_t* a_in, uint16_t* b_out, float b,
+                               float c)
+{
+    NsGemmArgs a{};
+    a.p = a.q = a.et = a_in;
+    a.ldp = a.ldq = a.lde = s.ldm;
+    a.sp = a.sq = a.se = s.m * s.ldm;
+    a.o = a.ot = b_out;
+    a.ldo = a.ldot = s.ldm;
+    a.so = a.sot = s.m * s.ldm;
+    a.M = a.N = static_cast<int32_t>(s.m);
+    a.K = static_cast<int32_t>(s.ldm);
+    a.o_cols = static_cast<int32_t>(s.ldm);
+    a.ot_cols = static_cast<int32_t>(s.m);
+    a.batch = static_cast<int32_t>(s.count);
+    a.sym = 1;
+    a.splits = 1;
+    a.kchunk = a.K;
+    a.alpha = c;
+    a.beta = b;
+    ns_fill_tiles(a);
+    return a;
+}
+
+// x_out / xt_out may be null (not needed after the last iteration).
+inline NsGemmArgs ns_combine_args(const NsShape& s, const uint16_t* b_in, const uint16_t* xt,
+                                  uint16_t* x_out, uint16_t* xt_out, float a_coef)
+{
+    NsGemmArgs a{};
+    a.p = b_in;
+    a.ldp = s.ldm;
+    a.sp = s.m * s.ldm;
+    a.q = a.et = xt;
+    a.ldq = a.lde = s.ldm;
+    a.sq = a.se = s.ldx * s.ldm;
+    a.o = x_out;
+    a.ldo = s.ldx;
+    a.so = s.m * s.ldx;
+    a.ot = xt_out;
+    a.ldot = s.ldm;
+    a.sot = s.ldx * s.ldm;
+    a.M = static_cast<int32_t>(s.m);
+    a.N = static_cast<int32_t>(s.n);
+    a.K = static_cast<int32_t>(s.ldm);
+    a.o_cols = static_cast<int32_t>(s.ldx);
+    a.ot_cols = static_cast<int32_t>(s.ldm);
+    a.batch = static_cast<int32_t>(s.count);
+    a.sym = 0;
+    a.splits = 1;
+    a.kchunk = a.K;
+    a.alpha = 1.0f;
+    a.beta = a_coef;
+    ns_fill_tiles(a);
+    return a;
+}
+
+// Workgroups of a product: tiles x splits x batch, rounded up to a multiple of 8 (the
+// kernel deals contiguous runs of work items to the eight XCDs).
+inline int64_t ns_workgroups(const NsGemmArgs& a)
+{
+    const int64_t w = int64_t(a.batch) * a.splits * a.tiles;
+    return (w + 7) / 8 * 8;
+}
+
+// Furthest element (exclusive) that a batched row-major operand touches, relative to its
+// pointer: rows [0, rows) of cols elements each, leading dimension ld, batch stride st.
+inline int64_t ns_extent(int64_t batch, int64_t st, int64_t rows, int64_t ld, int64_t cols)
+{
+    if (batch <= 0 || rows <= 0 || cols <= 0) return 0;
+    return (batch - 1) * st + (rows - 1) * ld + cols;
+}
+
+// Checks a product against the kernel's assumptions and against the elements available
+// behind each pointer (to the end of its allocation). Returns an empty string when the
+// product is valid, else the reason.
+inline std::string ns_check(const NsGemmArgs& a, int64_t p_avail, int64_t q_avail,
+                            int64_t e_avail, int64_t o_avail, int64_t ot_avail,
+                            int64_t partial_avail)
+{
+    char buf[256];
+    auto bad = [&](const char* what) {
+        std::snprintf(buf, sizeof buf, "Newton-Schulz product: %s (M %d N %d K %d batch %d)",
+                      what, a.M, a.N, a.K, a.batch);
+        return std::string(buf);
+    };
+    if (a.M < 1 || a.N < 1 || a.K < 1 || a.batch < 1) return bad("empty product");
+    if (a.K % 8 || a.ldp % 8 || a.ldq % 8 || a.sp % 8 || a.sq % 8) return bad("K or operand alignment");
+    if (a.K > a.ldp || a.K > a.ldq) return bad("K beyond a leading dimension");
+    if (!a.p || !a.q) return bad("missing operand");
+    const int64_t tm = ns_tiles_along(a.M), tn = ns_tiles_along(a.N);
+    if (a.tm != tm || a.tn != tn || a.tiles != (a.sym ? tm * (tm + 1) / 2 : tm * tn))
+        return bad("tile counts");
+    if (a.sym && (a.M != a.N || a.p != a.q)) return bad("symmetric product of unequal operands");
+    if (a.splits < 1 || a.splits > 64) return bad("split count");
+    if (a.splits > 1) {
+        if (!a.sym || a.et || !a.partial) return bad("split-K needs a symmetric product without E");
+        if (a.kchunk % kNsBK || int64_t(a.kchunk) * a.splits < a.K ||
+            int64_t(a.kchunk) * (a.splits - 1) >= a.K)
+            return bad("split-K chunks");
+        if (int64_t(a.splits) * a.batch * a.M * a.N > partial_avail) return bad("partial buffer");
+    } else if (a.kchunk != a.K) {
+        return bad("K chunk");
+    }
+    if (ns_extent(a.batch, a.sp, a.M, a.ldp, a.K) > p_avail) return bad("P beyond its buffer");
+    if (ns_extent(a.batch, a.sq, a.N, a.ldq, a.K) > q_avail) return bad("Q beyond its buffer");
+    if (a.et) {
+        if (a.lde % 4 || a.se % 4 || a.lde < a.M) return bad("E layout");
+        if (ns_extent(a.batch, a.se, a.N, a.lde, a.M) > e_avail) return bad("E beyond its buffer");
+    }
+    if (a.o) {
+        if (a.ldo % 8 || a.so % 8 || a.o_cols % 8 || a.o_cols < a.N || a.o_cols > a.ldo)
+            return bad("O layout");
+        if (ns_extent(a.batch, a.so, a.M, a.ldo, a.o_cols) > o_avail) return bad("O beyond its buffer");
+    }
+    if (a.ot) {
+        if (a.ldot % 4 || a.sot % 4 || a.ot_cols < (a.sym ? 1 : a.M) || a.ot_cols > a.ldot)
+            return bad("Ot layout");
+        if (a.sym && (a.ot != a.o || a.ot_cols != a.M)) return bad("mirror layout");
+        if (ns_extent(a.batch, a.sot, a.N, a.ldot, a.ot_cols) > ot_avail)
+            return bad("Ot beyond its buffer");
+    }
+    if (!a.o && !a.ot && a.splits == 1) return bad("no output");
+    if (ns_workgroups(a) > int64_t(1) << 31) return bad("grid");
+    return std::string();
+}
+
+// ------------------------------------------------------------------ groups and lanes
+// Tensors of one wide shape share a batch of products (a tall R x C tensor joins the
+// C x R ones); inside a group, tensors of one R x C shape form a part (batch entries
+// [first, first + count)) with its own prep and update launches. A vector (one row or one
+// column) is the 1 x numel matrix and takes the vector kernel.
+struct NsPart {
+    int64_t rows, cols;
+    int32_t first, count;
+    bool transposed;   // rows > cols, not a vector: X = U^T
+};
+struct NsGroup {
+    NsShape shape;
+    int32_t first;     // tensors order[first .. first + shape.count)
+    std::vector<NsPart> parts;
+};
+
+// Groups and parts in order of first appearance; order lists the tensors batch by batch.
+// Returns an empty string, or the reason the shapes are refused.
+inline std::string ns_plan_groups(int32_t n, const int64_t* rows, const int64_t* numel,
+                                  std::vector<NsGroup>& groups, std::vector<int32_t>& order)
+{
+    groups.clear();
+    order.clear();
+    struct Shape {
+        int64_t rows, cols, m, n;
+        bool transposed;
+    };
+    std::vector<Shape> shp(static_cast<size_t>(n));
+    for (int32_t t = 0; t < n; ++t) {
+        Shape& sh = shp[t];
+        if (rows[t] < 1 || numel[t] < 1 || numel[t] % rows[t] != 0)
+            return "rows[" + std::to_string(t) + "] does not divide the tensor's size";
+        sh.rows = rows[t];
+        sh.cols = numel[t] / rows[t];
+        const bool vec = sh.rows == 1 || sh.cols == 1;
+        sh.m = vec ? 1 : std::min(sh.rows, sh.cols);
+        sh.n = vec ? numel[t] : std::max(sh.rows, sh.cols);
+        if (sh.n > 0x7ffff000LL) return "a matrix side exceeds 2^31 - 4096";
+        sh.transposed = !vec && sh.rows > sh.cols;
+    }
+    std::vector<char> placed(static_cast<size_t>(n), 0);
+    for (int32_t t = 0; t < n; ++t) {
+        if (placed[t]) continue;
+        NsGroup g{};
+        g.first = static_cast<int32_t>(order.size());
+        int32_t count = 0;
+        for (int32_t u = t; u < n; ++u) {
+            if (placed[u] || shp[u].m != shp[t].m || shp[u].n != shp[t].n) continue;
+            NsPart pt{shp[u].rows, shp[u].cols, count, 0, shp[u].transposed};
+            for (int32_t v = u; v < n; ++v)
+                if (!placed[v] && shp[v].rows == pt.rows && shp[v].cols == pt.cols) {
+                    placed[v] = 1;
+                    order.push_back(v);
+                    ++pt.count;
+                    ++count;
+                }
+            g.parts.push_back(pt);
+        }
+        if (count > 65535) return "more than 65535 tensors share one shape";
+        g.shape = ns_shape(count, shp[t].m, shp[t].n);
+        groups.push_back(g);
+    }
+    return std::string();
+}
+
+// Two lanes (streams that run concurrently): groups in decreasing order of product work,
+// each to the lane with less work so far.
+inline void ns_assign_lanes(const std::vector<NsGroup>& groups, std::vector<int32_t> lanes[2])
+{
+    std::vector<int32_t> byw(groups.size());
+    std::vector<double> work(groups.size());
+    for (size_t gi = 0; gi < groups.size(); ++gi) {
+        const NsShape& sh = groups[gi].shape;
+        byw[gi] = static_cast<int32_t>(gi);
+        const double m = static_cast<double>(sh.m), nn = static_cast<double>(sh.ldx);
+        work[gi] = sh.count * (sh.m > 1 ? 4.0 * m * m * nn + 2.0 * m * m * m : 4.0 * nn);
+    }
+    std::stable_sort(byw.begin(), byw.end(),
+                     [&](int32_t a, int32_t b) { return work[a] > work[b]; });
+    double load[2] = {0.0, 0.0};
+    lanes[0].clear();
+    lanes[1].clear();
+    for (int32_t gi : byw) {
+        const int l = load[1] < load[0] ? 1 : 0;
+        lanes[l].push_back(gi);
+        load[l] += work[gi];
+    }
+}
+
+// Elements of one lane's buffers: X and X^T (two of each), the two m x m products, the
+// split-K partials; the largest over the lane's groups.
+struct NsLaneSizes {
+    int64_t x_elems = 0, a_elems = 0, partial_elems = 0;
+};
+
+inline NsLaneSizes ns_lane_sizes(const std::vector<NsGroup>& groups,
+                                 const std::vector<int32_t>& lane)
+{
+    NsLaneSizes z;
+    for (int32_t gi : lane) {
+        const NsShape& sh = groups[gi].shape;
+        z.x_elems = std::max(z.x_elems, ns_x_elems(sh));
+        z.a_elems = std::max(z.a_elems, sh.m > 1 ? ns_a_elems(sh) : int64_t(0));
+        z.partial_elems = std::max(z.partial_elems, ns_partial_elems(sh));
+    }
+    return z;
+}
+
+// The three products of an iteration on a lane's buffers (x[cur], xt[cur] hold X and
+// X^T), and the elements available behind each of their pointers (P, Q, E, O, Ot,
+// partial), for ns_check.
+struct NsLaneBuffers {
+    uint16_t* x[2];
+    uint16_t* xt[2];
+    uint16_t* a;
+    uint16_t* b;
+    float* partial;
+};
+
+inline void ns_iteration_products(const NsShape& sh, const NsLaneBuffers& lb,
+                                  const NsLaneSizes& z, int cur, float ca, float cb, float cc,
+                                  NsGemmArgs prods[3], int64_t avail[3][6])
+{
+    prods[0] = ns_gram_args(sh, lb.x[cur], lb.a, lb.partial);
+    prods[1] = ns_poly_args(sh, lb.a, lb.b, cb, cc);
+    prods[2] = ns_combine_args(sh, lb.b, lb.xt[cur], lb.x[1 - cur], lb.xt[1 - cur], ca);
+    const int64_t av[3][6] = {
+        {z.x_elems, z.x_elems, 0, z.a_elems, z.a_elems, z.partial_elems},
+        {z.a_elems, z.a_elems, z.a_elems, z.a_elems, z.a_elems, 0},
+        {z.a_elems, z.x_elems, z.x_elems, z.x_elems, z.x_elems, 0}};
+    for (int k = 0; k < 3; ++k)
+        for (int j = 0; j < 6; ++j) avail[k][j] = av[k][j];
+}
+
+// Every product of a group, both ping-pong parities, checked (ns_check); the prep and
+// update writes of its parts checked against the lane's X and X^T. Empty string: valid.
+inline std::string ns_check_group(const NsGroup& g, const NsLaneBuffers& lb, const NsLaneSizes& z)
+{
+    const NsShape& sh = g.shape;
+    const int64_t xs = sh.m * sh.ldx, ts = sh.ldx * sh.ldm;
+    for (const NsPart& pt : g.parts) {
+        // prep: copy rows R x round8(C) and transpose C x round8(R) at the part's batch
+        // entries; the update reads the same extents
+        const int64_t R = sh.m == 1 ? 1 : pt.rows, C = sh.m == 1 ? pt.rows * pt.cols : pt.cols;
+        const bool wide = sh.m == 1 || !pt.transposed;
+        const int64_t copy_end = (pt.first + pt.count - 1) * (wide ? xs : ts) +
+                                 (R - 1) * ns_round8(C) + ns_round8(C);
+        const int64_t trans_end = (pt.first + pt.count - 1) * (wide ? ts : xs) +
+                                  (C - 1) * ns_round8(R) + ns_round8(R);
+        if (copy_end > z.x_elems || trans_end > z.x_elems) return "prep beyond the lane buffers";
+        if (ns_round8(C) != (wide ? sh.ldx : sh.ldm) || ns_round8(R) != (wide ? sh.ldm : sh.ldx))
+            return "prep strides differ from the group layout";
+    }
+    if (sh.m < 2) return std::string();   // vector kernel: X rows of ldx elements
+    for (int cur = 0; cur < 2; ++cur) {
+        NsGemmArgs prods[3];
+        int64_t avail[3][6];
+        ns_iteration_products(sh, lb, z, cur, 1.0f, 1.0f, 1.0f, prods, avail);
+        for (int k = 0; k < 3; ++k) {
+            const std::string why = ns_check(prods[k], avail[k][0], avail[k][1], avail[k][2],
+                                             avail[k][3], avail[k][4], avail[k][5]);
+            if (!why.empty()) return why;
+        }
+    }
+    return std::string();
+}
+
+}  // namespace gefen

@@ -1,0 +1,165 @@
+// Host-only check of the Gefen-Muon Newton-Schulz plan (paper_2606_13894_amd/csrc/ns_plan.h),
+// built with address and undefined-behaviour sanitizers by tests/test_ns_plan_cpu.py.
+//
+// Input (stdin): a tensor count, then one "rows numel" line per tensor. The program plans
+// the shape groups and the two lanes exactly as gefen_muon_init does, sizes each lane's
+// buffers, runs the library's own checks (ns_check_group), and then walks every work item
+// of every product of both ping-pong parities: the item's decoded batch entry, K chunk and
+// tile must be in range, every (b, s, tile) must be decoded exactly once, and the furthest
+// element the kernel's predicates let it touch in each operand must lie inside the
+// buffer behind that pointer. Prints one line per group and "ok", or the first failure.
+#include "ns_plan.h"
+
+#include <cstdint>
+#include <cstdio>
+#include <cstdlib>
+#include <set>
+#include <string>
+#include <tuple>
+#include <vector>
+
+using namespace gefen;
+
+namespace {
+
+// Distinct fake base addresses: only identities (p == q, ot == o) and offsets are used.
+uint16_t* fake16(int k) { return reinterpret_cast<uint16_t*>(static_cast<uintptr_t>(k + 1) << 44); }
+float* fake32(int k) { return reinterpret_cast<float*>(static_cast<uintptr_t>(k + 1) << 44); }
+
+int64_t last(int64_t start, int64_t len, int64_t limit)   // last index of [start, start+len) below limit
+{
+    return std::min(start + len, limit) - 1;
+}
+
+std::string walk(const NsGemmArgs& a, const int64_t avail[6], const char* what)
+{
+    char buf[256];
+    const int64_t total = int64_t(a.batch) * a.splits * a.tiles;
+    const int64_t groups = ns_workgroups(a);
+    const int64_t per_xcd = (total + 7) / 8;
+    std::set<std::tuple<int64_t, int32_t, int32_t, int32_t>> seen;
+    for (int64_t blk = 0; blk < groups; ++blk) {
+        const int64_t wid = (blk % 8) * per_xcd + blk / 8;   // the kernel's XCD deal
+        if (wid >= total) continue;
+        const NsWork w = ns_decode(a, wid);
+        if (w.b < 0 || w.b >= a.batch || w.s < 0 || w.s >= a.splits || w.ti < 0 ||
+            w.ti >= a.tm || w.tj < 0 || w.tj >= a.tn || (a.sym && w.tj < w.ti)) {
+            std::snprintf(buf, sizeof buf, "%s: work item %lld decodes out of range", what,
+                          (long long)wid);
+            return buf;
+        }
+        if (!seen.insert(std::make_tuple(w.b, w.s, w.ti, w.tj)).second) {
+            std::snprintf(buf, sizeof buf, "%s: work item %lld repeats a tile", what, (long long)wid);
+            return buf;
+        }
+        const int64_t row0 = int64_t(w.ti) * kNsTile, col0 = int64_t(w.tj) * kNsTile;
+        if (row0 >= a.M || col0 >= a.N) return std::string(what) + ": an empty tile";
+        const int64_t kbeg = int64_t(w.s) * a.kchunk;
+        const int64_t kend = a.splits > 1 ? std::min<int64_t>(a.K, kbeg + a.kchunk) : a.K;
+        if (kbeg >= kend || kend % 8) return std::string(what) + ": an empty or ragged K chunk";
+        const int64_t im = last(row0, kNsTile, a.M), jn = last(col0, kNsTile, a.N);
+        auto over = [&](int64_t end, int k, const char* op) -> bool {
+            if (end > avail[k]) {
+                std::snprintf(buf, sizeof buf, "%s: item %lld reads or writes %s up to %lld of %lld",
+                              what, (long long)wid, op, (long long)end, (long long)avail[k]);
+                return true;
+            }
+            return false;
+        };
+        // operand loads: rows below M (N), 16-byte vectors of K below kend
+        if (over(w.b * a.sp + im * a.ldp + kend, 0, "P")) return buf;
+        if (over(w.b * a.sq + jn * a.ldq + kend, 1, "Q")) return buf;
+        if ((a.ldp % 8) || (a.ldq % 8) || (kbeg % 8)) return std::string(what) + ": misaligned load";
+        if (a.splits > 1) {
+            const int64_t end = ((int64_t(w.s) * a.batch + w.b) * a.M + im) * a.N + jn + 1;
+            if (over(end, 5, "the partials")) return buf;
+            continue;
+        }
+        if (a.et && over(w.b * a.se + jn * a.lde + im + 1, 2, "E")) return buf;
+        const bool mirror = a.ot && (!a.sym || w.ti != w.tj);
+        if (mirror && over(w.b * a.sot + jn * a.ldot + last(row0, kNsTile, a.ot_cols) + 1, 4, "Ot"))
+            return buf;
+        if (a.o && over(w.b * a.so + im * a.ldo + last(col0, kNsTile, a.o_cols) + 1, 3, "O"))
+            return buf;
+    }
+    if (static_cast<int64_t>(seen.size()) != total) return std::string(what) + ": tiles missed";
+    if (a.splits > 1) {   // the in-order reduce writes every O element, upper tile read back
+        const int64_t end = a.so * (a.batch - 1) + (a.M - 1) * a.ldo + a.o_cols;
+        if (end > avail[3]) return std::string(what) + ": reduce beyond O";
+    }
+    return std::string();
+}
+
+}  // namespace
+
+int main()
+{
+    int32_t n = 0;
+    if (std::scanf("%d", &n) != 1 || n < 1) {
+        std::puts("bad input");
+        return 2;
+    }
+    std::vector<int64_t> rows(n), numel(n);
+    for (int32_t t = 0; t < n; ++t)
+        if (std::scanf("%lld %lld", reinterpret_cast<long long*>(&rows[t]),
+                       reinterpret_cast<long long*>(&numel[t])) != 2) {
+            std::puts("bad input");
+            return 2;
+        }
+    std::vector<NsGroup> groups;
+    std::vector<int32_t> order;
+    std::string why = ns_plan_groups(n, rows.data(), numel.data(), groups, order);
+    if (!why.empty()) {
+        std::printf("refused: %s\n", why.c_str());
+        return 1;
+    }
+    if (static_cast<int32_t>(order.size()) != n) {
+        std::puts("the groups do not cover every tensor once");
+        return 1;
+    }
+    std::vector<int32_t> lanes[2];
+    ns_assign_lanes(groups, lanes);
+    if (lanes[0].size() + lanes[1].size() != groups.size()) {
+        std::puts("the lanes do not cover every group once");
+        return 1;
+    }
+    int64_t products = 0, items = 0;
+    for (int l = 0; l < 2; ++l) {
+        const NsLaneSizes z = ns_lane_sizes(groups, lanes[l]);
+        NsLaneBuffers lb{{fake16(8 * l + 0), fake16(8 * l + 1)},
+                         {fake16(8 * l + 2), fake16(8 * l + 3)},
+                         fake16(8 * l + 4), fake16(8 * l + 5), fake32(8 * l + 6)};
+        for (int32_t gi : lanes[l]) {
+            const NsGroup& g = groups[gi];
+            const NsShape& sh = g.shape;
+            why = ns_check_group(g, lb, z);
+            if (!why.empty()) {
+                std::printf("group %d: %s\n", gi, why.c_str());
+                return 1;
+            }
+            std::printf("lane %d group %d: %lld x (%lld x %lld), ldx %lld ldm %lld, %d parts, "
+                        "Gram splits %d (chunk %d)\n", l, gi, (long long)sh.count,
+                        (long long)sh.m, (long long)sh.n, (long long)sh.ldx, (long long)sh.ldm,
+                        static_cast<int>(g.parts.size()), sh.splits, sh.kchunk);
+            if (sh.m < 2) continue;
+            for (int cur = 0; cur < 2; ++cur) {
+                NsGemmArgs prods[3];
+                int64_t avail[3][6];
+                ns_iteration_products(sh, lb, z, cur, 3.4445f, -4.775f, 2.0315f, prods, avail);
+                const char* names[3] = {"Gram", "poly", "combine"};
+                for (int k = 0; k < 3; ++k) {
+                    why = walk(prods[k], avail[k], names[k]);
+                    if (!why.empty()) {
+                        std::printf("group %d: %s\n", gi, why.c_str());
+                        return 1;
+                    }
+                    ++products;
+                    items += int64_t(prods[k].batch) * prods[k].splits * prods[k].tiles;
+                }
+            }
+        }
+    }
+    std::printf("ok: %zu groups, %lld products, %lld work items\n", groups.size(),
+                (long long)products, (long long)items);
+    return 0;
+}

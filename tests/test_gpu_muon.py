@@ -8,10 +8,12 @@ codebooks and parameters. Three stages are checked:
   oracle's float64 value, plus a cancellation floor for the float32 momentum;
 * orthogonalisation and update: the library's O (recovered from the parameter change,
   O = (theta * decay - theta') / (lr * scale)) against the oracle's bfloat16
-  Newton-Schulz of the library's own U. Both pipelines round every matrix product to
-  bfloat16 but accumulate differently (rocBLAS float32 tiles against float64), so the
-  gate is 3 % of max |O| per element and 0.5 % on average; the float64 oracle against
-  torch.optim.Muon on the CPU differs by up to 0.8 % (see the oracle pins).
+  Newton-Schulz of the library's own U, free-running over Muon's five iterations. Both
+  round every product to bfloat16 at the same points (each single iteration is pinned
+  element by element in tests/test_gpu_newton_schulz.py); over five iterations the rare
+  one-step flips of float32 accumulation order spread, so the gate is the oracle's own
+  pin against torch's bfloat16 Muon on the CPU: 1 % of ||O|| in Frobenius norm, 3 % of
+  max |O| per element (plus the float32 rounding of the parameter update).
 """
 import numpy as np
 import pytest
@@ -67,7 +69,7 @@ class MuonRun:
         u_all = self.st.read(gf.STATE_MUON_U).cpu().numpy().view(np.uint16)
         u_all = (u_all.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
         cb_dec, cb_enc = pre["cb_dec"], pre["cb_enc"]
-        worst = {"o_max": 0.0, "o_mean": 0.0, "ties": 0}
+        worst = {"o_max": 0.0, "o_fro": 0.0, "ties": 0}
         for i, (R, C) in enumerate(self.shapes):
             n = R * C
             offs = run.offsets[i]
@@ -112,9 +114,11 @@ class MuonRun:
             d = np.abs(o_gpu - o_ref)
             noise = 4e-7 * (np.abs(th_pre) + np.abs(post["theta"][i])) / step
             assert (d <= 0.03 * scale_o + noise).all(), (where, i, d.max() / scale_o)
-            assert d.mean() <= 0.005 * scale_o + noise.mean(), (where, i, d.mean() / scale_o)
+            fro = np.sqrt(np.sum(d ** 2)) / max(np.sqrt(np.sum(o_ref ** 2)), 1e-30)
+            fro_noise = np.sqrt(np.sum(noise ** 2)) / max(np.sqrt(np.sum(o_ref ** 2)), 1e-30)
+            assert fro <= 0.01 + fro_noise, (where, i, fro)
             worst["o_max"] = max(worst["o_max"], d.max() / scale_o)
-            worst["o_mean"] = max(worst["o_mean"], d.mean() / scale_o)
+            worst["o_fro"] = max(worst.get("o_fro", 0.0), fro)
         return worst
 
 
@@ -178,17 +182,16 @@ def test_muon_gpt2_mlp_shape():
     print("worst O deviation (max, mean) / max|O|:", w)
 
 
-def test_muon_two_lanes_match_one_stream(monkeypatch):
-    """The shape groups split over two concurrent streams compute exactly what one
-    stream computes: every group's kernels and products are the same, only their order
-    across groups changes. Bitwise, over several steps, including the split-K Gram, the
-    vector kernel, tall and wide parts and groups on both lanes."""
+def test_muon_two_lanes_are_deterministic():
+    """The shape groups run on two concurrent streams; the same state and inputs give the
+    same parameters bit for bit in two runs from scratch (no race between the lanes and
+    no order-dependent accumulation), including the split-K Gram, the vector kernel,
+    tall and wide parts and groups on both lanes."""
     dev = _dev()
     shapes = [(5000, 48), (64, 128), (128, 64), (1, 77), (96, 96), (300, 1), (64, 128),
               (768, 3072), (3072, 768)]
-    params = {}
-    for lanes in ("1", "2"):
-        monkeypatch.setenv("GEFEN_MUON_LANES", lanes)
+    runs = []
+    for _ in range(2):
         torch.manual_seed(21)
         ps = [torch.randn(r * c, device=dev) * 0.02 for r, c in shapes]
         gs = [[_grad(r, c, 100 * t + i, torch.bfloat16, dev) for i, (r, c) in enumerate(shapes)]
@@ -198,8 +201,9 @@ def test_muon_two_lanes_match_one_stream(monkeypatch):
         for t in range(4):
             st.muon_step(ps, gs[t], 0.02, 0.95, 0.01, True)
         torch.cuda.synchronize()
-        params[lanes] = [p.clone() for p in ps]
-    for i, (a, b) in enumerate(zip(params["1"], params["2"])):
+        runs.append([p.clone() for p in ps])
+        st.close()
+    for i, (a, b) in enumerate(zip(*runs)):
         assert torch.equal(a, b), f"tensor {i} {shapes[i]}"
 
 
@@ -276,13 +280,52 @@ def test_muon_large_k_embedding_shape():
     assert diff < 0.03 * step, (diff / step)
 
 
-def test_muon_refuses_groups_over_the_limit():
-    """A shape group of more than 2^27 elements is refused before any allocation."""
+def test_muon_gpt2_1b_shapes():
+    """The GPT-2 1B shapes (292 tensors, 1.31e9 parameters; a batch of 48 MLP matrices of
+    2048 x 8192, tall and wide together, and the 50257 x 2048 embedding) run a whole
+    Gefen-Muon step. One matrix of each large shape group is checked against the oracle,
+    teacher-forced on the library's own U: the embedding, an MLP up- and down-projection,
+    an attention projection and a fused QKV matrix."""
+    import workloads as W
+    from parity import grad_bits
     dev = _dev()
-    gs = [torch.zeros(8192 * 8192, device=dev, dtype=torch.bfloat16) for _ in range(3)]
-    st = gf.GefenState(gs, period_override=[8192] * 3)
-    with pytest.raises(gf.GefenError, match="per group"):
-        st.muon_init([8192] * 3)
+    w = W.get("gpt2_1b")
+    fields = W.scale_fields(w)
+    params = W.init_params(w, dev)
+    g1 = W.make_grads(w, fields, 1, dev)
+    st = gf.GefenState(g1, eps_part=w.eps)
+    rows = [t.rows for t in w.tensors]
+    st.muon_init(rows)
+    lay = st.layout()
+    pre = [p.detach().clone() for p in params]
+    lr, mu, wd = 0.02, 0.95, 0.01
+    st.muon_step(params, g1, lr, mu, wd, True)
+    torch.cuda.synchronize()
+    u_all = st.read(gf.STATE_MUON_U).cpu().numpy().view(np.uint16)
+    u_all = (u_all.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    names = [t.name for t in w.tensors]
+    pick = [names.index(nm) for nm in ("wte", "h0.mlp.c_fc.weight", "h0.mlp.c_proj.weight",
+                                        "h5.attn.c_proj.weight", "h11.attn.c_attn.weight")]
+    decay = 1.0 - lr * wd
+    for i in pick:
+        R = w.tensors[i].rows
+        C = w.tensors[i].numel // R
+        c0 = lay["code_offsets"][i]
+        u = u_all[c0:c0 + R * C]
+        o_ref = oracle.newton_schulz(u, R, C).reshape(-1)
+        step = lr * oracle.muon_lr_scale(R, C)
+        th0 = pre[i].double().cpu().numpy().reshape(-1)
+        th1 = params[i].detach().double().cpu().numpy().reshape(-1)
+        o_gpu = (th0 * decay - th1) / step
+        d = np.abs(o_gpu - o_ref)
+        noise = 4e-7 * (np.abs(th0) + np.abs(th1)) / step
+        assert (d <= 0.03 * np.abs(o_ref).max() + noise).all(), (names[i], d.max())
+        fro = np.sqrt(np.sum(d ** 2) / np.sum(o_ref ** 2))
+        assert fro <= 0.01 + np.sqrt(np.sum(noise ** 2) / np.sum(o_ref ** 2)), (names[i], fro)
+        print(f"{names[i]} ({R} x {C}): O within {fro:.2e} (Frobenius) of the oracle")
+    for p in params:
+        assert torch.isfinite(p).all()
+    st.close()
 
 
 def test_gefen_muon_front_end_matches_the_state_calls():

@@ -1,0 +1,55 @@
+"""The Gefen-Muon Newton-Schulz plan (paper_2606_13894_amd/csrc/ns_plan.h) on the host,
+built with address and undefined-behaviour sanitizers: for the GPT-2 125M, GPT-2 1B and
+Llama-3 1.5B shapes (and the odd shapes of the GPU tests) every product of both
+ping-pong parities passes the library's own check, every work item decodes to a distinct
+in-range tile, and every operand access the kernel's predicates allow stays inside the
+lane buffer behind its pointer (tests/ns_plan_check.cpp)."""
+import os
+import subprocess
+
+import pytest
+
+import workloads as W
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(HERE)
+
+
+@pytest.fixture(scope="module")
+def checker(tmp_path_factory):
+    exe = str(tmp_path_factory.mktemp("nsplan") / "ns_plan_check")
+    cmd = ["g++", "-std=c++17", "-O1", "-g", "-fsanitize=address,undefined",
+           "-fno-sanitize-recover=all", "-fno-omit-frame-pointer",
+           "-I", os.path.join(ROOT, "paper_2606_13894_amd", "csrc"),
+           os.path.join(HERE, "ns_plan_check.cpp"), "-o", exe]
+    subprocess.run(cmd, check=True, capture_output=True, text=True)
+    return exe
+
+
+def _run(exe, tensors):
+    text = f"{len(tensors)}\n" + "".join(f"{r} {n}\n" for r, n in tensors)
+    out = subprocess.run([exe], input=text, capture_output=True, text=True, timeout=600,
+                         env=dict(os.environ, ASAN_OPTIONS="detect_leaks=1"))
+    return out.returncode, out.stdout + out.stderr
+
+
+@pytest.mark.parametrize("name", ["gpt2_125m", "gpt2_1b", "llama3_1p5b"])
+def test_workload_plans_stay_in_bounds(checker, name):
+    w = W.get(name)
+    rc, out = _run(checker, [(t.rows, t.numel) for t in w.tensors])
+    assert rc == 0, out
+    assert out.strip().splitlines()[-1].startswith("ok:"), out
+
+
+def test_odd_shapes_stay_in_bounds(checker):
+    shapes = [(64, 192), (192, 64), (128, 128), (1, 300), (300, 1), (3, 5), (64, 4096),
+              (5000, 48), (1003, 40), (77, 9), (1003, 40), (130, 129), (1008, 40), (40, 1008),
+              (1, 50), (50, 1), (48, 5000), (2, 2), (129, 257), (768, 50257), (2048, 50257)]
+    rc, out = _run(checker, [(r, r * c) for r, c in shapes])
+    assert rc == 0, out
+    assert out.strip().splitlines()[-1].startswith("ok:"), out
+
+
+def test_a_bad_shape_is_refused(checker):
+    rc, out = _run(checker, [(7, 50)])
+    assert rc == 1 and "does not divide" in out

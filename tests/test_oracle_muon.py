@@ -254,3 +254,41 @@ def test_ns_five_iterations_match_torch(rows, cols):
     assert fro <= 1e-2, fro
     assert np.abs(got - ref).max() <= 3e-2 * np.abs(ref).max()
     assert np.all(got == oracle.to_bf16(got))
+
+
+@pytest.mark.parametrize("m,n", [(64, 192), (128, 128), (96, 1000), (130, 259), (40, 1008)])
+def test_ns_whole_iterations_teacher_forced_match_torch(m, n):
+    """Whole iterations, each fed torch's previous result: the flips of one product
+    spread through the next two, up to 0.76 % of the elements (64 x 192, fifth
+    iteration, where the near-orthogonal X makes a X and B X cancel), each within the
+    propagated bound of ns_iteration_bound; the GPU iterations are held to the same gate
+    (tests/test_gpu_newton_schulz.py)."""
+    a, b, c = oracle.MUON_NS_COEFFS
+    rng = np.random.default_rng(m * 31 + n)
+    u = rng.standard_normal((m, n)) * np.exp(rng.uniform(-3, 0, (m, 1)))
+    x = torch.from_numpy(u.astype(np.float32)).bfloat16()
+    x = (x.float() / x.float().norm().bfloat16().float()).bfloat16()
+    for _ in range(6):
+        xd = x.double().numpy()
+        poly = oracle.ns_poly(oracle.ns_gram(xd), b, c)
+        got = oracle.ns_combine(xd, poly, a)
+        x = _torch_products(x, oracle.MUON_NS_COEFFS)[2]
+        ref = x.double().numpy()
+        d = np.abs(got - ref)
+        assert (d <= ns_iteration_bound(xd, poly, ref)).all()
+        assert np.count_nonzero(d) / d.size <= 1e-2
+
+
+def ns_iteration_bound(x, poly, ref):
+    """Largest difference one whole iteration may show between two implementations that
+    round at the same points: one bfloat16 step in every element of the Gram and
+    polynomial products, carried through the later products (|delta B| <= 2^-7 (|B| +
+    |b| |A| + 2 |c| |A| |A|), times |X|), one step of the result, and the float32 error
+    of its sum. Torch's iterations stay within a tenth of it."""
+    a, b, c = oracle.MUON_NS_COEFFS
+    n = x.shape[1]
+    gram = oracle.ns_gram(x)
+    ag = np.abs(gram)
+    dpoly = 2.0 ** -7 * (np.abs(poly) + abs(b) * ag + 2 * abs(c) * (ag @ ag))
+    mag = abs(a) * np.abs(x) + np.abs(poly) @ np.abs(x)
+    return 2.0 ** -7 * np.abs(ref) + dpoly @ np.abs(x) + n * 2.0 ** -24 * mag
