@@ -144,90 +144,156 @@ __global__ __launch_bounds__(kNsThreads, 2) void k_ns_gemm(const NsGemmArgs a)
         return;
     }
 
+    // Epilogue through LDS, so that every global access is a 16-byte row segment:
+    // region A holds the E^T tile (rows j, columns i, as E^T is stored), later the O tile;
+    // region B holds the O^T tile. 16 threads cover a 128-element row, 16 rows a pass.
     const uint16_t* __restrict__ Et = a.et ? a.et + w.b * a.se : nullptr;
     uint16_t* __restrict__ Ot = a.ot ? a.ot + w.b * a.sot : nullptr;
     const bool mirror = Ot && (!a.sym || w.ti != w.tj);
-    uint16_t* stage = lds;   // BM x LDT, free after the last barrier of the main loop
+    uint16_t* sA = lds;
+    uint16_t* sB = lds + BM * LDT;
+    const int srow = tid >> 4, scol = (tid & 15) * 8;
+    if (Et) {
+#pragma unroll
+        for (int pass = 0; pass < BN / 16; ++pass) {
+            const int r = pass * 16 + srow;
+            const int64_t j = col0 + r, i = row0 + scol;
+            const u32x4 z = {0u, 0u, 0u, 0u};
+            // E^T rows are zero beyond M up to lde (a multiple of 8)
+            *reinterpret_cast<u32x4*>(sA + r * LDT + scol) =
+                (j < a.N && i < a.lde) ? *reinterpret_cast<const u32x4*>(Et + j * a.lde + i) : z;
+        }
+        __syncthreads();
+    }
+    u32x2 hp[2][2][4];   // bfloat16 results, rows (g * 8 + fk / 2) .. + 3 of each block
 #pragma unroll
     for (int mi = 0; mi < 2; ++mi)
 #pragma unroll
         for (int ni = 0; ni < 2; ++ni) {
-            const int64_t j = col0 + wn + ni * 32 + frow;
+            const int lc = wn + ni * 32 + frow;
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
-                const int lr = wm + mi * 32 + g * 8 + fk / 2;   // local row of element 0
-                const int64_t i0 = row0 + lr;
+                const int lr = wm + mi * 32 + g * 8 + fk / 2;
                 float e[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-                if (Et && j < a.N && i0 < a.M) {
-                    const uint16_t* src = Et + j * a.lde + i0;
-                    if (i0 + 4 <= a.M) {
-                        const u32x2 wv = *reinterpret_cast<const u32x2*>(src);
-                        e[0] = bf16_val(static_cast<uint16_t>(wv.x & 0xffffu));
-                        e[1] = bf16_val(static_cast<uint16_t>(wv.x >> 16));
-                        e[2] = bf16_val(static_cast<uint16_t>(wv.y & 0xffffu));
-                        e[3] = bf16_val(static_cast<uint16_t>(wv.y >> 16));
-                    } else {
-                        for (int q = 0; q < 4; ++q)
-                            if (i0 + q < a.M) e[q] = bf16_val(src[q]);
-                    }
+                if (Et) {
+                    const u32x2 ev = *reinterpret_cast<const u32x2*>(sA + lc * LDT + lr);
+                    e[0] = bf16_val(static_cast<uint16_t>(ev.x & 0xffffu));
+                    e[1] = bf16_val(static_cast<uint16_t>(ev.x >> 16));
+                    e[2] = bf16_val(static_cast<uint16_t>(ev.y & 0xffffu));
+                    e[3] = bf16_val(static_cast<uint16_t>(ev.y >> 16));
                 }
-                uint16_t h[4];
+                uint32_t h[4];
 #pragma unroll
                 for (int q = 0; q < 4; ++q)
                     h[q] = to_bf16(fmaf(a.alpha, acc[mi][ni][g * 4 + q], a.beta * e[q]));
-                if (mirror && j < a.N && i0 < a.ot_cols) {
-                    uint16_t* dst = Ot + j * a.ldot + i0;
-                    if (i0 + 4 <= a.ot_cols) {
-                        u32x2 wv;
-                        wv.x = uint32_t(h[0]) | (uint32_t(h[1]) << 16);
-                        wv.y = uint32_t(h[2]) | (uint32_t(h[3]) << 16);
-                        *reinterpret_cast<u32x2*>(dst) = wv;
-                    } else {
-                        for (int q = 0; q < 4; ++q)
-                            if (i0 + q < a.ot_cols) dst[q] = h[q];
-                    }
-                }
-                if (a.o) {
-#pragma unroll
-                    for (int q = 0; q < 4; ++q)
-                        stage[(lr + q) * LDT + wn + ni * 32 + frow] = h[q];
-                }
+                hp[mi][ni][g].x = h[0] | (h[1] << 16);
+                hp[mi][ni][g].y = h[2] | (h[3] << 16);
+                if (mirror) *reinterpret_cast<u32x2*>(sB + lc * LDT + lr) = hp[mi][ni][g];
             }
         }
-    if (!a.o) return;
-    __syncthreads();
-    uint16_t* __restrict__ O = a.o + w.b * a.so;
-    const int sc = (tid & 15) * 8;
+    if (a.o) {
+        if (Et) __syncthreads();   // every E^T read is done before region A takes O
 #pragma unroll
-    for (int pass = 0; pass < BM / 16; ++pass) {
-        const int sr = pass * 16 + (tid >> 4);
-        const int64_t i = row0 + sr, j = col0 + sc;
-        if (i < a.M && j < a.o_cols)
-            *reinterpret_cast<u32x4*>(O + i * a.ldo + j) =
-                *reinterpret_cast<const u32x4*>(stage + sr * LDT + sc);
+        for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+            for (int ni = 0; ni < 2; ++ni) {
+                const int lc = wn + ni * 32 + frow;
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const int lr = wm + mi * 32 + g * 8 + fk / 2;
+                    const u32x2 v = hp[mi][ni][g];
+                    sA[(lr + 0) * LDT + lc] = static_cast<uint16_t>(v.x & 0xffffu);
+                    sA[(lr + 1) * LDT + lc] = static_cast<uint16_t>(v.x >> 16);
+                    sA[(lr + 2) * LDT + lc] = static_cast<uint16_t>(v.y & 0xffffu);
+                    sA[(lr + 3) * LDT + lc] = static_cast<uint16_t>(v.y >> 16);
+                }
+            }
+    }
+    if (!a.o && !mirror) return;
+    __syncthreads();
+    if (a.o) {
+        uint16_t* __restrict__ O = a.o + w.b * a.so;
+#pragma unroll
+        for (int pass = 0; pass < BM / 16; ++pass) {
+            const int r = pass * 16 + srow;
+            const int64_t i = row0 + r, j = col0 + scol;
+            if (i < a.M && j < a.o_cols)
+                *reinterpret_cast<u32x4*>(O + i * a.ldo + j) =
+                    *reinterpret_cast<const u32x4*>(sA + r * LDT + scol);
+        }
+    }
+    if (mirror) {
+#pragma unroll
+        for (int pass = 0; pass < BN / 16; ++pass) {
+            const int r = pass * 16 + srow;
+            const int64_t j = col0 + r, i = row0 + scol;
+            if (j < a.N && i < a.ot_cols)
+                *reinterpret_cast<u32x4*>(Ot + j * a.ldot + i) =
+                    *reinterpret_cast<const u32x4*>(sB + r * LDT + scol);
+        }
     }
 }
 
-// Split-K Gram: O[b][i][j] = bf16(alpha * sum over chunks s (in order) of the float32
-// partial of the upper-tile element (i, j) or, below the diagonal tiles, (j, i)); zero in
-// the padding columns M .. o_cols - 1.
+// Split-K Gram: O[b][i][j] = bf16(alpha * the sum over the chunks s, in order, of the
+// float32 partials of (i, j)), zero in the padding columns N .. o_cols - 1, and the mirror
+// O[b][j][i] for tiles above the diagonal. A workgroup takes 16 rows of one upper tile:
+// each thread sums 8 consecutive partials of a row (two 16-byte loads per chunk) and
+// stores them as one 16-byte row segment; the mirror goes through an LDS transpose.
+constexpr int kReduceRows = 16;
+
 __global__ __launch_bounds__(256) void k_ns_reduce(const NsGemmArgs a)
 {
-    const int64_t per_b = int64_t(a.M) * a.o_cols;
-    const int64_t total = per_b * a.batch;
-    for (int64_t e = blockIdx.x * 256LL + threadIdx.x; e < total; e += 256LL * gridDim.x) {
-        const int64_t b = e / per_b;
-        const int64_t r = e - b * per_b;
-        const int64_t i = r / a.o_cols, j = r - i * a.o_cols;
-        float sum = 0.0f;
-        if (j < a.N) {
-            const bool upper = i / BM <= j / BN;
-            const int64_t ii = upper ? i : j, jj = upper ? j : i;
-            for (int32_t s = 0; s < a.splits; ++s)
-                sum += a.partial[((int64_t(s) * a.batch + b) * a.M + ii) * a.N + jj];
-            sum *= a.alpha;
+    __shared__ __attribute__((aligned(16))) uint16_t t[kReduceRows * LDT];
+    const int64_t slices = BM / kReduceRows;
+    const int64_t total = int64_t(a.batch) * a.tiles * slices;
+    const int64_t wid = blockIdx.x;
+    if (wid >= total) return;
+    NsGemmArgs one = a;
+    one.splits = 1;
+    const NsWork w = ns_decode(one, wid / slices);
+    const int slice = static_cast<int>(wid % slices);
+    const int64_t row0 = int64_t(w.ti) * BM + slice * kReduceRows, col0 = int64_t(w.tj) * BN;
+    const int tid = threadIdx.x, r = tid >> 4, scol = (tid & 15) * 8;
+    const int64_t plane = int64_t(a.batch) * a.M * a.N;
+    const int64_t i = row0 + r, j0 = col0 + scol;
+    float v[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+    if (i < a.M && j0 < a.N) {
+        const float* __restrict__ src = a.partial + (w.b * a.M + i) * a.N + j0;
+        // 16-byte loads when the row segment is whole and aligned (N % 4 == 0)
+        const bool vec = j0 + 8 <= a.N && (a.N & 3) == 0;
+        for (int32_t sp = 0; sp < a.splits; ++sp) {
+            const float* row = src + sp * plane;
+            if (vec) {
+                const f32x4v lo = *reinterpret_cast<const f32x4v*>(row);
+                const f32x4v hi = *reinterpret_cast<const f32x4v*>(row + 4);
+                v[0] += lo.x; v[1] += lo.y; v[2] += lo.z; v[3] += lo.w;
+                v[4] += hi.x; v[5] += hi.y; v[6] += hi.z; v[7] += hi.w;
+            } else {
+                for (int c = 0; c < 8; ++c)
+                    if (j0 + c < a.N) v[c] += row[c];
+            }
         }
-        a.o[b * a.so + i * a.ldo + j] = to_bf16(sum);
+    }
+    u32x4 h;
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+        h[c] = uint32_t(to_bf16(a.alpha * v[2 * c])) |
+               (uint32_t(to_bf16(a.alpha * v[2 * c + 1])) << 16);
+    if (i < a.M && j0 < a.o_cols)
+        *reinterpret_cast<u32x4*>(a.o + w.b * a.so + i * a.ldo + j0) = h;
+    if (w.ti == w.tj) return;
+    *reinterpret_cast<u32x4*>(t + r * LDT + scol) = h;
+    __syncthreads();
+    // mirror: row j = col0 + jr of O takes this slice's 16 rows as columns
+    const int jr = tid >> 1, half = (tid & 1) * 8;
+    const int64_t j = col0 + jr, ic = row0 + half;
+    if (j < a.N && ic < a.ot_cols) {
+        u32x4 m;
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+            m[c] = uint32_t(t[(half + 2 * c) * LDT + jr]) |
+                   (uint32_t(t[(half + 2 * c + 1) * LDT + jr]) << 16);
+        *reinterpret_cast<u32x4*>(a.ot + w.b * a.sot + j * a.ldot + ic) = m;
     }
 }
 
@@ -364,9 +430,9 @@ hipError_t launch_ns_gemm(const NsGemmArgs& a, hipStream_t stream)
                        a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.splits == 1) return e;
-    const int64_t total = int64_t(a.M) * a.o_cols * a.batch;
-    const int64_t g = std::min<int64_t>((total + 255) / 256, 4096);
-    hipLaunchKernelGGL(k_ns_reduce, dim3(static_cast<unsigned>(g)), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(k_ns_reduce,
+                       dim3(static_cast<unsigned>(int64_t(a.batch) * a.tiles * (BM / kReduceRows))),
+                       dim3(256), 0, stream, a);
     return hipGetLastError();
 }
 

@@ -36,10 +36,12 @@ constexpr int kNsThreads = 256;
 
 // One batched product C[i][j] = sum_k P[i][k] Q[j][k] (i < M, j < N, k < K), then
 //   value(i, j) = bf16(alpha * C[i][j] + beta * E[i][j]),  E[i][j] = et[j * lde + i]
-// (E absent: beta ignored), written to O[i][j] (i < M, j < o_cols; columns N .. o_cols-1
-// are zero) and to Ot[j][i] (j < N, i < ot_cols; zero for i >= M). Symmetric mode
-// (M == N, P == Q): only the tiles on and above the diagonal run, and each tile above
-// it also writes its mirror through Ot (= O, ot_cols = M). Split-K (splits > 1,
+// (E absent: beta ignored; E^T rows are read up to lde and must be zero from M on),
+// written to O[i][j] (i < M, j < o_cols; columns N .. o_cols-1 are zero) and to Ot[j][i]
+// (j < N, i < ot_cols; zero for i >= M). Symmetric mode (M == N, P == Q): only the tiles
+// on and above the diagonal run, and each tile above it also writes its mirror through
+// Ot (= O, ot_cols = o_cols). Every E load and O or Ot store is a 16-byte row segment:
+// the column counts, leading dimensions and batch strides are multiples of 8. Split-K (splits > 1,
 // symmetric, no E): workgroup s of a tile sums K range [s * kchunk, (s+1) * kchunk) and
 // writes float32 partial[((s * batch + b) * M + i) * N + j]; ns_reduce adds the chunks in
 // order and writes O.
@@ -74,18 +76,30 @@ struct NsShape {
     int32_t kchunk;   // their length (a multiple of kNsBK; ldx when splits == 1)
 };
 
-// Split the Gram product over K when the group's upper tiles leave most compute units
-// idle (a lone tall-skinny matrix such as a token embedding: 21 tiles at m = 768), into
-// at most 16 chunks of at least 8 stages each.
+// Split the Gram product over K so that its workgroups (count x t (t + 1) / 2 upper
+// tiles, times the split) fill their rounds on the GPU -- 256 compute units, two resident
+// workgroups each, so rounds of 512: the smallest split whose rounds are at least 90 %
+// full, else the fullest, with chunks of at least 8 stages and at most 32 chunks. A lone
+// tall-skinny matrix (a token embedding: 21 tiles at m = 768) splits 22 ways; a batch
+// that already fills its rounds (the GPT-2 MLP group: 504 tiles) does not split.
 inline int32_t ns_gram_splits(int64_t count, int64_t m, int64_t ldx)
 {
+    constexpr int64_t kSlots = 512;
     const int64_t t = ns_tiles_along(m);
     const int64_t work = count * t * (t + 1) / 2;
-    if (work >= 256) return 1;
-    int64_t s = (512 + work - 1) / work;
-    s = std::min<int64_t>(s, 16);
-    s = std::min<int64_t>(s, ldx / (8 * kNsBK));
-    return static_cast<int32_t>(std::max<int64_t>(s, 1));
+    const int64_t smax = std::max<int64_t>(1, std::min<int64_t>(32, ldx / (8 * kNsBK)));
+    int64_t best = 1;
+    double best_fill = 0.0;
+    for (int64_t s = 1; s <= smax; ++s) {
+        const int64_t groups = work * s;
+        const double fill = double(groups) / double((groups + kSlots - 1) / kSlots * kSlots);
+        if (fill >= 0.9) return static_cast<int32_t>(s);
+        if (fill > best_fill + 1e-12) {
+            best = s;
+            best_fill = fill;
+        }
+    }
+    return static_cast<int32_t>(best);
 }
 
 inline NsShape ns_shape(int64_t count, int64_t m, int64_t n)
@@ -162,7 +176,7 @@ inline NsGemmArgs ns_gram_args(const NsShape& s, const uint16_t* x, uint16_t* a_
     a.M = a.N = static_cast<int32_t>(s.m);
     a.K = static_cast<int32_t>(s.ldx);
     a.o_cols = static_cast<int32_t>(s.ldm);
-    a.ot_cols = static_cast<int32_t>(s.m);
+    a.ot_cols = static_cast<int32_t>(s.ldm);
     a.batch = static_cast<int32_t>(s.count);
     a.sym = 1;
     a.splits = s.splits;
@@ -187,7 +201,7 @@ inline NsGemmArgs ns_poly_args(const NsShape& s, const uint16_t* a_in, uint16_t*
     a.M = a.N = static_cast<int32_t>(s.m);
     a.K = static_cast<int32_t>(s.ldm);
     a.o_cols = static_cast<int32_t>(s.ldm);
-    a.ot_cols = static_cast<int32_t>(s.m);
+    a.ot_cols = static_cast<int32_t>(s.ldm);
     a.batch = static_cast<int32_t>(s.count);
     a.sym = 1;
     a.splits = 1;
@@ -280,8 +294,8 @@ inline std::string ns_check(const NsGemmArgs& a, int64_t p_avail, int64_t q_avai
     if (ns_extent(a.batch, a.sp, a.M, a.ldp, a.K) > p_avail) return bad("P beyond its buffer");
     if (ns_extent(a.batch, a.sq, a.N, a.ldq, a.K) > q_avail) return bad("Q beyond its buffer");
     if (a.et) {
-        if (a.lde % 4 || a.se % 4 || a.lde < a.M) return bad("E layout");
-        if (ns_extent(a.batch, a.se, a.N, a.lde, a.M) > e_avail) return bad("E beyond its buffer");
+        if (a.lde % 8 || a.se % 8 || a.lde < a.M) return bad("E layout");
+        if (ns_extent(a.batch, a.se, a.N, a.lde, a.lde) > e_avail) return bad("E beyond its buffer");
     }
     if (a.o) {
         if (a.ldo % 8 || a.so % 8 || a.o_cols % 8 || a.o_cols < a.N || a.o_cols > a.ldo)
@@ -289,9 +303,9 @@ inline std::string ns_check(const NsGemmArgs& a, int64_t p_avail, int64_t q_avai
         if (ns_extent(a.batch, a.so, a.M, a.ldo, a.o_cols) > o_avail) return bad("O beyond its buffer");
     }
     if (a.ot) {
-        if (a.ldot % 4 || a.sot % 4 || a.ot_cols < (a.sym ? 1 : a.M) || a.ot_cols > a.ldot)
+        if (a.ldot % 8 || a.sot % 8 || a.ot_cols % 8 || a.ot_cols < a.M || a.ot_cols > a.ldot)
             return bad("Ot layout");
-        if (a.sym && (a.ot != a.o || a.ot_cols != a.M)) return bad("mirror layout");
+        if (a.sym && (a.ot != a.o || a.ot_cols != a.o_cols)) return bad("mirror layout");
         if (ns_extent(a.batch, a.sot, a.N, a.ldot, a.ot_cols) > ot_avail)
             return bad("Ot beyond its buffer");
     }

@@ -75,7 +75,8 @@ std::string walk(const NsGemmArgs& a, const int64_t avail[6], const char* what)
             if (over(end, 5, "the partials")) return buf;
             continue;
         }
-        if (a.et && over(w.b * a.se + jn * a.lde + im + 1, 2, "E")) return buf;
+        if (a.et && over(w.b * a.se + jn * a.lde + last(row0, kNsTile, a.lde) + 1, 2, "E"))
+            return buf;
         const bool mirror = a.ot && (!a.sym || w.ti != w.tj);
         if (mirror && over(w.b * a.sot + jn * a.ldot + last(row0, kNsTile, a.ot_cols) + 1, 4, "Ot"))
             return buf;
@@ -83,9 +84,20 @@ std::string walk(const NsGemmArgs& a, const int64_t avail[6], const char* what)
             return buf;
     }
     if (static_cast<int64_t>(seen.size()) != total) return std::string(what) + ": tiles missed";
-    if (a.splits > 1) {   // the in-order reduce writes every O element, upper tile read back
-        const int64_t end = a.so * (a.batch - 1) + (a.M - 1) * a.ldo + a.o_cols;
-        if (end > avail[3]) return std::string(what) + ": reduce beyond O";
+    if (a.splits > 1) {   // the reduce: one upper tile per workgroup, direct and mirror rows
+        for (int64_t wid = 0; wid < int64_t(a.batch) * a.tiles; ++wid) {
+            NsGemmArgs one = a;
+            one.splits = 1;
+            const NsWork w = ns_decode(one, wid);
+            const int64_t row0 = int64_t(w.ti) * kNsTile, col0 = int64_t(w.tj) * kNsTile;
+            const int64_t im = last(row0, kNsTile, a.M);
+            if (w.b * a.so + im * a.ldo + last(col0, kNsTile, a.o_cols) + 1 > avail[3] ||
+                ((int64_t(a.splits) - 1) * a.batch * a.M + w.b * a.M + im) * a.N +
+                        last(col0, kNsTile, a.N) + 1 > avail[5] ||
+                (w.ti != w.tj && w.b * a.sot + last(col0, kNsTile, a.N) * a.ldot +
+                                         last(row0, kNsTile, a.ot_cols) + 1 > avail[4]))
+                return std::string(what) + ": reduce beyond its buffers";
+        }
     }
     return std::string();
 }
