@@ -165,6 +165,22 @@ int gefen_histogram(gefen_state* st, const gefen_tensor* grads, int32_t n_tensor
 int gefen_dp_codebook(const uint64_t* hist, int32_t nbins, int32_t k, double* codebook_out,
                       double* cost_out, int32_t* status_out, void* stream);
 
+/* gefen_dp_codebook_static -- gefen_dp_codebook for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same DP, the same kernels and the same results, with its workspace in
+ * one fixed array per GPU that the library holds until the process ends (11 MiB; enough
+ * for the largest DP, 4096 bins and 256 entries). It calls no hipMalloc, hipFree or other
+ * allocating routine. Arguments, outputs and errors as gefen_dp_codebook; a DP larger
+ * than the fixed workspace is refused with EINVAL. The first call on a device looks up
+ * that device's array (EHIP if the runtime cannot). Every call on one GPU shares that
+ * GPU's array: calls that overlap on one GPU (different streams, or threads without
+ * ordering) race and give undefined results; calls ordered on one stream do not. The
+ * workspace needs no clearing: the DP writes every entry before reading it.
+ * Asynchronous on `stream`. */
+int gefen_dp_codebook_static(const uint64_t* hist, int32_t nbins, int32_t k,
+                             double* codebook_out, double* cost_out, int32_t* status_out,
+                             void* stream);
+
 /* ------------------------------------------------------------------------------
  * Queries, state access and checkpointing.
  * ---------------------------------------------------------------------------- */

@@ -35,6 +35,7 @@ SYMBOLS = [
     "gefen_checkpoint_bytes", "gefen_export", "gefen_import", "gefen_profile_begin",
     "gefen_profile_end", "gefen_destroy", "gefen_last_error", "gefen_muon_init",
     "gefen_muon_step", "gefen_muon_profile_end", "gefen_stream_mix", "gefen_newton_schulz",
+    "gefen_dp_codebook_static",
 ]
 
 
@@ -77,6 +78,7 @@ def load_library(path: str = LIB_PATH):
     lib.gefen_partition_scores.argtypes = [P(gefen_tensor), f64, vp, vp, i32, P(i32), P(i64), vp]
     lib.gefen_histogram.argtypes = [vp, P(gefen_tensor), i32, vp, vp]
     lib.gefen_dp_codebook.argtypes = [vp, i32, i32, vp, vp, vp, vp]
+    lib.gefen_dp_codebook_static.argtypes = [vp, i32, i32, vp, vp, vp, vp]
     lib.gefen_get_periods.argtypes = [vp, vp]
     lib.gefen_get_layout.argtypes = [vp, vp, vp, P(i64), P(i64), P(i32)]
     lib.gefen_read_state.argtypes = [vp, i32, vp, i64, vp]
@@ -382,6 +384,25 @@ def newton_schulz(x, steps: int = 5, coeffs=(3.4445, -4.7750, 2.0315), out=None,
                                    float(coeffs[0]), float(coeffs[1]), float(coeffs[2]),
                                    _stream(stream)))
     return out
+
+
+def dp_codebook_static(hist, k: int, out=None, stream=None):
+    """gefen_dp_codebook_static: the DP with the library's fixed workspace (no allocation
+    in the library). `out` = (codebook float64 [k], cost float64 [1], status int32 [1])
+    device tensors to write, else new ones. Returns the three tensors."""
+    lib = load_library()
+    torch = _torch()
+    hist = hist.contiguous()
+    if out is None:
+        out = (torch.empty(k, dtype=torch.float64, device=hist.device),
+               torch.empty(1, dtype=torch.float64, device=hist.device),
+               torch.empty(1, dtype=torch.int32, device=hist.device))
+    cb, cost, st = out
+    _check(lib.gefen_dp_codebook_static(ctypes.c_void_p(hist.data_ptr()), hist.numel(), int(k),
+                                        ctypes.c_void_p(cb.data_ptr()),
+                                        ctypes.c_void_p(cost.data_ptr()),
+                                        ctypes.c_void_p(st.data_ptr()), _stream(stream)))
+    return cb, cost, st
 
 
 def stream_mix(theta, grad, codes, stream=None):

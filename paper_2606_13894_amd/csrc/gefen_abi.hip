@@ -10,6 +10,7 @@
 #include <algorithm>
 #include <cstdlib>
 #include <memory>
+#include <mutex>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -869,6 +870,41 @@ bool is_host_ptr(const void* p)
 
 }  // namespace
 
+// ------------------------------------------------------------------ fixed DP workspace
+// The workspace of gefen_dp_codebook_static: one array per GPU, for the process's
+// lifetime, large enough for the largest DP (16 * 256 bins, 256 entries: 11,088,896
+// bytes). Host code never passes `scratch` itself to a kernel (in host code it is a
+// stand-in, not a device address): the first call on each device asks the runtime for
+// that device's copy and keeps the address.
+constexpr size_t kDpScratchBytes = size_t(11) << 20;
+static __device__ __align__(256) unsigned char scratch[kDpScratchBytes];
+
+namespace {
+
+std::mutex g_scratch_mu;
+std::vector<void*> g_scratch_ptr;   // per device ordinal; null until its first call
+
+int dp_scratch(void** out)
+{
+    int dev = 0;
+    GEFEN_HIP(hipGetDevice(&dev));
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (dev >= static_cast<int>(g_scratch_ptr.size())) g_scratch_ptr.resize(dev + 1, nullptr);
+    if (!g_scratch_ptr[dev]) {
+        if (dp_workspace_bytes(16 * kMaxK, kMaxK) > kDpScratchBytes)
+            return fail(GEFEN_EHIP, "internal: the fixed DP workspace is too small");
+        void* p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return fail(GEFEN_EHIP, "hipGetSymbolAddress(scratch) failed: %s", hipGetErrorString(e));
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return GEFEN_OK;
+}
+
+}  // namespace
+
 // ------------------------------------------------------------------ ABI
 extern "C" {
 
@@ -1139,6 +1175,27 @@ int gefen_dp_codebook(const uint64_t* hist, int32_t nbins, int32_t k, double* co
     GEFEN_HIP(hipMallocAsync(&ws, dp_workspace_bytes(nbins, k), stream));
     hipError_t e = launch_dp(hist, nbins, k, ws, codebook_out, cost_out, status_out, stream);
     (void)hipFreeAsync(ws, stream);
+    if (e != hipSuccess) return fail(GEFEN_EHIP, "DP launch failed: %s", hipGetErrorString(e));
+    return GEFEN_OK;
+}
+
+int gefen_dp_codebook_static(const uint64_t* hist, int32_t nbins, int32_t k, double* codebook_out,
+                             double* cost_out, int32_t* status_out, void* stream_)
+{
+    g_err.clear();
+    if (!hist || !codebook_out || !cost_out || !status_out)
+        return fail(GEFEN_EINVAL, "NULL argument");
+    if (k < 2 || k > kMaxK) return fail(GEFEN_EINVAL, "k must be in [2, %d]", kMaxK);
+    if (nbins < 1 || nbins > 16 * kMaxK) return fail(GEFEN_EINVAL, "nbins must be in [1, %d]", 16 * kMaxK);
+    const size_t need = dp_workspace_bytes(nbins, k);
+    if (need > kDpScratchBytes)
+        return fail(GEFEN_EINVAL, "a DP of %d bins and %d entries needs %zu bytes of workspace; "
+                    "the fixed workspace holds %zu", nbins, k, need, kDpScratchBytes);
+    void* ws = nullptr;
+    int rc = dp_scratch(&ws);
+    if (rc) return rc;
+    hipError_t e = launch_dp(hist, nbins, k, ws, codebook_out, cost_out, status_out,
+                             as_stream(stream_));
     if (e != hipSuccess) return fail(GEFEN_EHIP, "DP launch failed: %s", hipGetErrorString(e));
     return GEFEN_OK;
 }
