@@ -1574,52 +1574,70 @@ int muon_lane_resources(gefen_state* st)
     return GEFEN_OK;
 }
 
-// Normalise (prep), orthogonalise and update one shape group with a lane's buffers.
-int muon_run_group(gefen_state* st, const gefen_state::MuonLane& lane, const NsGroup& g,
-                   int32_t ns_steps, float ca, float cb, float cc, double lr, float decay,
-                   hipStream_t ls)
+// One shape group on a lane's buffers runs in phases, each a few launches on the lane's
+// stream: 0 normalises its momentum matrices into the layout (prep), 1 .. the
+// Newton-Schulz iterations (the vector kernel does all of them in phase 1), the last
+// writes the updates.
+int muon_group_phases(const NsGroup& g, int32_t ns_steps)
+{
+    return 2 + (g.shape.m == 1 ? 1 : ns_steps);
+}
+
+struct MuonGroupRun {
+    float ca, cb, cc, decay;
+    double lr;
+    int32_t ns_steps;
+};
+
+// Enqueues phase `phase` of group g; cur (the buffer parity of X, X^T) advances with the
+// iterations.
+int muon_group_phase(gefen_state* st, const gefen_state::MuonLane& lane, const NsGroup& g,
+                     const MuonGroupRun& r, int phase, int& cur, hipStream_t ls)
 {
     const NsShape& sh = g.shape;
     const NsLaneBuffers& ln = lane.buf;
     const int64_t xs = sh.m * sh.ldx, ts = sh.ldx * sh.ldm;   // batch strides of X, X^T
-    for (const auto& pt : g.parts) {
-        const int32_t* tof = st->muon_tensor_of + g.first + pt.first;
-        uint16_t* x0 = ln.x[0] + pt.first * xs;
-        uint16_t* t0 = ln.xt[0] + pt.first * ts;
-        if (sh.m == 1)
-            GEFEN_HIP(launch_ns_prep(st->muon_u, st->muon_u_off, tof, st->muon_norm, pt.count, 1,
-                                     pt.rows * pt.cols, x0, xs, t0, ts, ls));
-        else if (!pt.transposed)
-            GEFEN_HIP(launch_ns_prep(st->muon_u, st->muon_u_off, tof, st->muon_norm, pt.count,
-                                     pt.rows, pt.cols, x0, xs, t0, ts, ls));
-        else
-            GEFEN_HIP(launch_ns_prep(st->muon_u, st->muon_u_off, tof, st->muon_norm, pt.count,
-                                     pt.rows, pt.cols, t0, ts, x0, xs, ls));
-    }
-    int cur = 0;
-    if (sh.m == 1) {
-        GEFEN_HIP(launch_muon_ns_vec(ln.x[0], static_cast<int32_t>(sh.count), sh.n, sh.ldx,
-                                     ns_steps, ca, cb, cc, ls));
-    } else {
-        for (int32_t it = 0; it < ns_steps; ++it) {
-            const int r = ns_iteration(ln, lane.size, sh, cur, ca, cb, cc, ls);
-            if (r) return r;
+    const int last = muon_group_phases(g, r.ns_steps) - 1;
+    if (phase == 0) {
+        cur = 0;
+        for (const auto& pt : g.parts) {
+            const int32_t* tof = st->muon_tensor_of + g.first + pt.first;
+            uint16_t* x0 = ln.x[0] + pt.first * xs;
+            uint16_t* t0 = ln.xt[0] + pt.first * ts;
+            if (sh.m == 1)
+                GEFEN_HIP(launch_ns_prep(st->muon_u, st->muon_u_off, tof, st->muon_norm, pt.count,
+                                         1, pt.rows * pt.cols, x0, xs, sh.ldx, t0, ts, sh.ldm, ls));
+            else if (!pt.transposed)
+                GEFEN_HIP(launch_ns_prep(st->muon_u, st->muon_u_off, tof, st->muon_norm, pt.count,
+                                         pt.rows, pt.cols, x0, xs, sh.ldx, t0, ts, sh.ldm, ls));
+            else
+                GEFEN_HIP(launch_ns_prep(st->muon_u, st->muon_u_off, tof, st->muon_norm, pt.count,
+                                         pt.rows, pt.cols, t0, ts, sh.ldm, x0, xs, sh.ldx, ls));
+        }
+    } else if (phase < last) {
+        if (sh.m == 1) {
+            GEFEN_HIP(launch_muon_ns_vec(ln.x[0], static_cast<int32_t>(sh.count), sh.n, sh.ldx,
+                                         r.ns_steps, r.ca, r.cb, r.cc, ls));
+        } else {
+            const int rc = ns_iteration(ln, lane.size, sh, cur, r.ca, r.cb, r.cc, ls);
+            if (rc) return rc;
             cur ^= 1;
         }
-    }
-    for (const auto& pt : g.parts) {
-        const int32_t* tof = st->muon_tensor_of + g.first + pt.first;
-        const double scale = std::sqrt(std::max(1.0, static_cast<double>(pt.rows) / pt.cols));
-        const float step = static_cast<float>(lr * scale);
-        if (sh.m == 1)
-            GEFEN_HIP(launch_ns_update(ln.x[cur] + pt.first * xs, xs, sh.ldx, st->segs, tof,
-                                       pt.count, 1, pt.rows * pt.cols, decay, step, ls));
-        else if (!pt.transposed)   // theta = X' (m x n)
-            GEFEN_HIP(launch_ns_update(ln.x[cur] + pt.first * xs, xs, sh.ldx, st->segs, tof,
-                                       pt.count, pt.rows, pt.cols, decay, step, ls));
-        else                       // theta = X'^T (n x m)
-            GEFEN_HIP(launch_ns_update(ln.xt[cur] + pt.first * ts, ts, sh.ldm, st->segs, tof,
-                                       pt.count, pt.rows, pt.cols, decay, step, ls));
+    } else {
+        for (const auto& pt : g.parts) {
+            const int32_t* tof = st->muon_tensor_of + g.first + pt.first;
+            const double scale = std::sqrt(std::max(1.0, static_cast<double>(pt.rows) / pt.cols));
+            const float step = static_cast<float>(r.lr * scale);
+            if (sh.m == 1)
+                GEFEN_HIP(launch_ns_update(ln.x[cur] + pt.first * xs, xs, sh.ldx, st->segs, tof,
+                                           pt.count, 1, pt.rows * pt.cols, r.decay, step, ls));
+            else if (!pt.transposed)   // theta = X' (m x n)
+                GEFEN_HIP(launch_ns_update(ln.x[cur] + pt.first * xs, xs, sh.ldx, st->segs, tof,
+                                           pt.count, pt.rows, pt.cols, r.decay, step, ls));
+            else                       // theta = X'^T (n x m)
+                GEFEN_HIP(launch_ns_update(ln.xt[cur] + pt.first * ts, ts, sh.ldm, st->segs, tof,
+                                           pt.count, pt.rows, pt.cols, r.decay, step, ls));
+        }
     }
     return GEFEN_OK;
 }
@@ -1707,21 +1725,38 @@ int gefen_muon_step(gefen_state* st, const gefen_tensor* params, const gefen_ten
     const float decay = static_cast<float>(1.0 - lr * weight_decay);
     const float ca = static_cast<float>(ns_a), cb = static_cast<float>(ns_b),
                 cc = static_cast<float>(ns_c);
-    auto run_group = [&](gefen_state::MuonLane& ln, const NsGroup& g, hipStream_t ls) -> int {
-        return muon_run_group(st, ln, g, ns_steps, ca, cb, cc, lr, decay, ls);
-    };
-    // lane 1 first (it starts as soon as the norms are done), then lane 0, then the join
+    const MuonGroupRun run{ca, cb, cc, decay, lr, ns_steps};
+    // The two lanes' phases are enqueued alternately, so that both streams hold work from
+    // the start (enqueueing one lane whole first would leave the other idle for as long
+    // as the host takes to launch the first one's kernels).
     gefen_state::MuonLane& l1 = st->muon_lane[1];
     if (!l1.groups.empty()) {
         GEFEN_HIP(hipEventRecord(st->muon_fork, stream));
         GEFEN_HIP(hipStreamWaitEvent(st->muon_side, st->muon_fork, 0));
-        for (int32_t gi : l1.groups)
-            if ((rc = run_group(l1, st->muon_groups[gi], st->muon_side))) return rc;
-        GEFEN_HIP(hipEventRecord(st->muon_join, st->muon_side));
     }
-    for (int32_t gi : st->muon_lane[0].groups)
-        if ((rc = run_group(st->muon_lane[0], st->muon_groups[gi], stream))) return rc;
-    if (!l1.groups.empty()) GEFEN_HIP(hipStreamWaitEvent(stream, st->muon_join, 0));
+    struct Cursor {
+        const gefen_state::MuonLane* lane;
+        hipStream_t s;
+        size_t gi;
+        int phase, cur;
+    } cursors[2] = {{&l1, st->muon_side, 0, 0, 0}, {&st->muon_lane[0], stream, 0, 0, 0}};
+    for (bool more = true; more;) {
+        more = false;
+        for (Cursor& c : cursors) {
+            if (c.gi >= c.lane->groups.size()) continue;
+            const NsGroup& g = st->muon_groups[c.lane->groups[c.gi]];
+            if ((rc = muon_group_phase(st, *c.lane, g, run, c.phase, c.cur, c.s))) return rc;
+            if (++c.phase == muon_group_phases(g, ns_steps)) {
+                c.phase = 0;
+                ++c.gi;
+            }
+            more = more || c.gi < c.lane->groups.size();
+        }
+    }
+    if (!l1.groups.empty()) {
+        GEFEN_HIP(hipEventRecord(st->muon_join, st->muon_side));
+        GEFEN_HIP(hipStreamWaitEvent(stream, st->muon_join, 0));
+    }
     if (prof) {
         GEFEN_HIP(hipEventRecord(ev[st->muon_prof_stride() - 1], stream));
         ++st->muon_prof_steps;
@@ -1804,7 +1839,7 @@ int gefen_newton_schulz(const uint16_t* x_in, uint16_t* x_out, int32_t batch, in
     const int64_t xs = sh.m * sh.ldx, ts = sh.ldx * sh.ldm;
     auto run = [&]() -> int {
         GEFEN_HIP(launch_ns_prep(x_in, nullptr, nullptr, nullptr, batch, m, n, lb.x[0], xs,
-                                 lb.xt[0], ts, stream));
+                                 sh.ldx, lb.xt[0], ts, sh.ldm, stream));
         int cur = 0;
         if (m == 1) {
             GEFEN_HIP(launch_muon_ns_vec(lb.x[0], batch, n, sh.ldx, steps, static_cast<float>(a),

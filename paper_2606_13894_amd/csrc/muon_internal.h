@@ -29,12 +29,13 @@ hipError_t launch_muon_ns_vec(uint16_t* x, int32_t batch, int64_t n, int64_t str
 hipError_t launch_ns_gemm(const NsGemmArgs& a, hipStream_t stream);
 // Batch entry b takes tensor t = tensor_of ? tensor_of[b] : b, whose R x C matrix starts at
 // src + (src_off ? src_off[t] : b * R * C), divided by norm[t] (norm null: 1); writes
-// copy[b] (R x round8(C)) = S / norm and trans[b] (C x round8(R)) = (S / norm)^T, zero
-// padded, at batch strides copy_stride and trans_stride (elements, multiples of 8).
+// copy[b] (R rows of cs >= C elements) = S / norm and trans[b] (C rows of ts >= R) =
+// (S / norm)^T, zero padded, at batch strides copy_stride and trans_stride (elements; all
+// four multiples of 8).
 hipError_t launch_ns_prep(const uint16_t* src, const int64_t* src_off, const int32_t* tensor_of,
                           const float* norm, int32_t batch, int64_t R, int64_t C, uint16_t* copy,
-                          int64_t copy_stride, uint16_t* trans, int64_t trans_stride,
-                          hipStream_t stream);
+                          int64_t copy_stride, int64_t cs, uint16_t* trans, int64_t trans_stride,
+                          int64_t ts, hipStream_t stream);
 // theta of tensor tensor_of[b] (R x C) = theta * decay - step * S[b], S[b] the R x C matrix
 // of row stride ss at o + b * stride
 hipError_t launch_ns_update(const uint16_t* o, int64_t stride, int64_t ss, const Seg* segs,

@@ -2,10 +2,10 @@
 // cores, and the kernels that bring the momentum matrices into and out of their layout
 // (ns_plan.h gives the layout and the three products of an iteration).
 //
-// The product kernel: one 256-thread workgroup computes a 128 x 128 output tile of one
-// batch entry (and one K chunk when split). Its four waves own 64 x 64 quarters, each
-// made of 2 x 2 v_mfma_f32_32x32x16_bf16 accumulators (float32). Both operands are read
-// along contiguous K, 16 bytes per thread, into LDS tiles of 128 rows x 64 K (rows padded
+// The product kernel: one 256-thread workgroup computes a 128 x 128 or 256 x 256 output
+// tile of one batch entry (and one K chunk when split). Its four waves own quarters made
+// of 2 x 2 or 4 x 4 v_mfma_f32_32x32x16_bf16 accumulators (float32). Both operands are read
+// along contiguous K, 16 bytes per thread, into LDS tiles of 64 K per row (rows padded
 // to 72 elements so that the 16-byte fragment reads of 16 consecutive rows hit distinct
 // banks); two LDS stages: the next stage's global loads are in flight while the current
 // one feeds the matrix cores, with one barrier per stage. The epilogue forms
@@ -27,11 +27,8 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4v __attribute__((ext_vector_type(4)));
 
-constexpr int BM = kNsTile, BN = kNsTile, BK = kNsBK;
+constexpr int BK = kNsBK;
 constexpr int LDK = BK + 8;      // LDS row stride of the operand tiles (elements)
-constexpr int LDT = BN + 8;      // LDS row stride of the epilogue tile (elements)
-constexpr int kLdsElems = 2 * (BM + BN) * LDK;
-static_assert(BM * LDT <= kLdsElems, "epilogue tile fits the operand LDS");
 
 __device__ __forceinline__ float bf16_val(uint16_t b)
 {
@@ -46,137 +43,70 @@ __device__ __forceinline__ uint16_t to_bf16(float x)
     return static_cast<uint16_t>((b + 0x7FFFu + ((b >> 16) & 1u)) >> 16);
 }
 
-__global__ __launch_bounds__(kNsThreads, 2) void k_ns_gemm(const NsGemmArgs a)
+// Element j (0..7) of eight packed bfloat16.
+__device__ __forceinline__ uint32_t bf16_at(const u32x4& w, int j)
 {
-    __shared__ __attribute__((aligned(16))) uint16_t lds[kLdsElems];
-    const int64_t total = int64_t(a.batch) * a.splits * a.tiles;
-    const int64_t per_xcd = (total + 7) / 8;
-    const int64_t wid = static_cast<int64_t>(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-    if (wid >= total) return;
-    const NsWork w = ns_decode(a, wid);
-    const int64_t row0 = int64_t(w.ti) * BM, col0 = int64_t(w.tj) * BN;
-    const int64_t kbeg = int64_t(w.s) * a.kchunk;
-    const int64_t kend = a.splits > 1 ? min(int64_t(a.K), kbeg + a.kchunk) : int64_t(a.K);
-    const uint16_t* __restrict__ P = a.p + w.b * a.sp;
-    const uint16_t* __restrict__ Q = a.q + w.b * a.sq;
+    const uint32_t v = w[j >> 1];
+    return (j & 1) ? (v >> 16) : (v & 0xffffu);
+}
 
-    const int tid = threadIdx.x;
-    const int lrow = tid >> 3, lk = (tid & 7) * 8;   // loader: 8 threads per 64-element row
-    u32x4 ra[4], rb[4];
-    auto gload = [&](int64_t k0) {
-        const int64_t kk = k0 + lk;
-        const bool kin = kk < kend;   // kend % 8 == 0: a vector is all in or all out
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int64_t gi = row0 + lrow + 32 * r;
-            const int64_t gj = col0 + lrow + 32 * r;
-            const u32x4 z = {0u, 0u, 0u, 0u};
-            ra[r] = (kin && gi < a.M) ? *reinterpret_cast<const u32x4*>(P + gi * a.ldp + kk) : z;
-            rb[r] = (kin && gj < a.N) ? *reinterpret_cast<const u32x4*>(Q + gj * a.ldq + kk) : z;
-        }
-    };
-    auto lstore = [&](int buf) {
-        uint16_t* sa = lds + buf * (BM + BN) * LDK;
-        uint16_t* sb = sa + BM * LDK;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            *reinterpret_cast<u32x4*>(sa + (lrow + 32 * r) * LDK + lk) = ra[r];
-            *reinterpret_cast<u32x4*>(sb + (lrow + 32 * r) * LDK + lk) = rb[r];
-        }
-    };
+// W x W accumulator blocks of 32 x 32 per wave, 2 x 2 waves: a (64 W) x (64 W) tile.
+template <int W>
+struct NsTileShape {
+    static constexpr int T = 64 * W;               // tile rows and columns
+    static constexpr int LDT = T + 8;              // LDS row stride of the epilogue tiles
+    static constexpr int kStage = 2 * T * LDK;     // both operand tiles of one stage
+    static constexpr int kLds = 2 * kStage > T * LDT ? 2 * kStage : T * LDT;
+    static constexpr int kPasses = T / 32;         // 32 rows of 64 K loaded per pass
+};
 
+// Epilogue through one LDS tile in the E^T / O^T orientation (rows j, columns i), so that
+// every global access is a 16-byte row segment: (1) the E^T tile as stored; (2) each lane
+// turns its accumulators into bfloat16 results in place, over the E^T elements of the
+// same positions (8 bytes: four consecutive i); (3) the tile's rows are the rows of O^T
+// (or of the mirror); (4) the rows of O come from 8 x 8 blocks of the tile transposed in
+// registers.
+template <int W>
+__device__ __forceinline__ void epilogue(const NsGemmArgs& a, const NsWork& w,
+                                         const f32x16 (&acc)[W][W], uint16_t* lds, int tid)
+{
+    using S = NsTileShape<W>;
+    constexpr int T = S::T, LDT = S::LDT;
+    const int64_t row0 = int64_t(w.ti) * T, col0 = int64_t(w.tj) * T;
     const int lane = tid & 63, wave = tid >> 6;
-    const int wm = (wave >> 1) * 64, wn = (wave & 1) * 64;
+    const int wm = (wave >> 1) * (32 * W), wn = (wave & 1) * (32 * W);
     const int frow = lane & 31, fk = (lane >> 5) * 8;
-    f32x16 acc[2][2];
-#pragma unroll
-    for (int mi = 0; mi < 2; ++mi)
-#pragma unroll
-        for (int ni = 0; ni < 2; ++ni)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) acc[mi][ni][v] = 0.0f;
 
-    const int64_t nk = (kend - kbeg + BK - 1) / BK;
-    gload(kbeg);
-    lstore(0);
-    __syncthreads();
-    for (int64_t it = 0; it < nk; ++it) {
-        if (it + 1 < nk) gload(kbeg + (it + 1) * BK);
-        const uint16_t* sa = lds + (it & 1) * (BM + BN) * LDK;
-        const uint16_t* sb = sa + BM * LDK;
-#pragma unroll
-        for (int kk = 0; kk < BK; kk += 16) {
-            bf16x8 fa[2], fb[2];
-#pragma unroll
-            for (int mi = 0; mi < 2; ++mi)
-                fa[mi] = __builtin_bit_cast(
-                    bf16x8, *reinterpret_cast<const u32x4*>(sa + (wm + mi * 32 + frow) * LDK + kk + fk));
-#pragma unroll
-            for (int ni = 0; ni < 2; ++ni)
-                fb[ni] = __builtin_bit_cast(
-                    bf16x8, *reinterpret_cast<const u32x4*>(sb + (wn + ni * 32 + frow) * LDK + kk + fk));
-#pragma unroll
-            for (int mi = 0; mi < 2; ++mi)
-#pragma unroll
-                for (int ni = 0; ni < 2; ++ni)
-                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[mi], fb[ni],
-                                                                        acc[mi][ni], 0, 0, 0);
-        }
-        if (it + 1 < nk) lstore((it + 1) & 1);
-        __syncthreads();
-    }
-
-    // Accumulator element v of block (mi, ni): row (v / 4) * 8 + (lane / 32) * 4 + v % 4,
-    // column lane % 32 of the 32 x 32 block.
-    if (a.splits > 1) {
-        float* __restrict__ part = a.partial + ((int64_t(w.s) * a.batch + w.b) * a.M) * a.N;
-#pragma unroll
-        for (int mi = 0; mi < 2; ++mi)
-#pragma unroll
-            for (int ni = 0; ni < 2; ++ni) {
-                const int64_t j = col0 + wn + ni * 32 + frow;
-#pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    const int64_t i = row0 + wm + mi * 32 + (v >> 2) * 8 + fk / 2 + (v & 3);
-                    if (i < a.M && j < a.N) part[i * a.N + j] = acc[mi][ni][v];
-                }
-            }
-        return;
-    }
-
-    // Epilogue through LDS, so that every global access is a 16-byte row segment:
-    // region A holds the E^T tile (rows j, columns i, as E^T is stored), later the O tile;
-    // region B holds the O^T tile. 16 threads cover a 128-element row, 16 rows a pass.
     const uint16_t* __restrict__ Et = a.et ? a.et + w.b * a.se : nullptr;
     uint16_t* __restrict__ Ot = a.ot ? a.ot + w.b * a.sot : nullptr;
     const bool mirror = Ot && (!a.sym || w.ti != w.tj);
-    uint16_t* sA = lds;
-    uint16_t* sB = lds + BM * LDT;
     const int srow = tid >> 4, scol = (tid & 15) * 8;
     if (Et) {
 #pragma unroll
-        for (int pass = 0; pass < BN / 16; ++pass) {
-            const int r = pass * 16 + srow;
-            const int64_t j = col0 + r, i = row0 + scol;
-            const u32x4 z = {0u, 0u, 0u, 0u};
-            // E^T rows are zero beyond M up to lde (a multiple of 8)
-            *reinterpret_cast<u32x4*>(sA + r * LDT + scol) =
-                (j < a.N && i < a.lde) ? *reinterpret_cast<const u32x4*>(Et + j * a.lde + i) : z;
-        }
+        for (int half = 0; half < T / 128; ++half)
+#pragma unroll
+            for (int pass = 0; pass < T / 16; ++pass) {
+                const int r = pass * 16 + srow, c = half * 128 + scol;
+                const int64_t j = col0 + r, i = row0 + c;
+                const u32x4 z = {0u, 0u, 0u, 0u};
+                // E^T rows are zero beyond M up to lde (a multiple of 8)
+                *reinterpret_cast<u32x4*>(lds + r * LDT + c) =
+                    (j < a.N && i < a.lde) ? *reinterpret_cast<const u32x4*>(Et + j * a.lde + i) : z;
+            }
         __syncthreads();
     }
-    u32x2 hp[2][2][4];   // bfloat16 results, rows (g * 8 + fk / 2) .. + 3 of each block
 #pragma unroll
-    for (int mi = 0; mi < 2; ++mi)
+    for (int mi = 0; mi < W; ++mi)
 #pragma unroll
-        for (int ni = 0; ni < 2; ++ni) {
+        for (int ni = 0; ni < W; ++ni) {
             const int lc = wn + ni * 32 + frow;
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
                 const int lr = wm + mi * 32 + g * 8 + fk / 2;
+                u32x2* cell = reinterpret_cast<u32x2*>(lds + lc * LDT + lr);
                 float e[4] = {0.0f, 0.0f, 0.0f, 0.0f};
                 if (Et) {
-                    const u32x2 ev = *reinterpret_cast<const u32x2*>(sA + lc * LDT + lr);
+                    const u32x2 ev = *cell;
                     e[0] = bf16_val(static_cast<uint16_t>(ev.x & 0xffffu));
                     e[1] = bf16_val(static_cast<uint16_t>(ev.x >> 16));
                     e[2] = bf16_val(static_cast<uint16_t>(ev.y & 0xffffu));
@@ -186,65 +116,275 @@ __global__ __launch_bounds__(kNsThreads, 2) void k_ns_gemm(const NsGemmArgs a)
 #pragma unroll
                 for (int q = 0; q < 4; ++q)
                     h[q] = to_bf16(fmaf(a.alpha, acc[mi][ni][g * 4 + q], a.beta * e[q]));
-                hp[mi][ni][g].x = h[0] | (h[1] << 16);
-                hp[mi][ni][g].y = h[2] | (h[3] << 16);
-                if (mirror) *reinterpret_cast<u32x2*>(sB + lc * LDT + lr) = hp[mi][ni][g];
+                u32x2 hv;
+                hv.x = h[0] | (h[1] << 16);
+                hv.y = h[2] | (h[3] << 16);
+                *cell = hv;
             }
         }
-    if (a.o) {
-        if (Et) __syncthreads();   // every E^T read is done before region A takes O
-#pragma unroll
-        for (int mi = 0; mi < 2; ++mi)
-#pragma unroll
-            for (int ni = 0; ni < 2; ++ni) {
-                const int lc = wn + ni * 32 + frow;
-#pragma unroll
-                for (int g = 0; g < 4; ++g) {
-                    const int lr = wm + mi * 32 + g * 8 + fk / 2;
-                    const u32x2 v = hp[mi][ni][g];
-                    sA[(lr + 0) * LDT + lc] = static_cast<uint16_t>(v.x & 0xffffu);
-                    sA[(lr + 1) * LDT + lc] = static_cast<uint16_t>(v.x >> 16);
-                    sA[(lr + 2) * LDT + lc] = static_cast<uint16_t>(v.y & 0xffffu);
-                    sA[(lr + 3) * LDT + lc] = static_cast<uint16_t>(v.y >> 16);
-                }
-            }
-    }
-    if (!a.o && !mirror) return;
     __syncthreads();
-    if (a.o) {
-        uint16_t* __restrict__ O = a.o + w.b * a.so;
-#pragma unroll
-        for (int pass = 0; pass < BM / 16; ++pass) {
-            const int r = pass * 16 + srow;
-            const int64_t i = row0 + r, j = col0 + scol;
-            if (i < a.M && j < a.o_cols)
-                *reinterpret_cast<u32x4*>(O + i * a.ldo + j) =
-                    *reinterpret_cast<const u32x4*>(sA + r * LDT + scol);
-        }
-    }
     if (mirror) {
 #pragma unroll
-        for (int pass = 0; pass < BN / 16; ++pass) {
-            const int r = pass * 16 + srow;
-            const int64_t j = col0 + r, i = row0 + scol;
-            if (j < a.N && i < a.ot_cols)
-                *reinterpret_cast<u32x4*>(Ot + j * a.ldot + i) =
-                    *reinterpret_cast<const u32x4*>(sB + r * LDT + scol);
+        for (int half = 0; half < T / 128; ++half)
+#pragma unroll
+            for (int pass = 0; pass < T / 16; ++pass) {
+                const int r = pass * 16 + srow, c = half * 128 + scol;
+                const int64_t j = col0 + r, i = row0 + c;
+                if (j < a.N && i < a.ot_cols)
+                    *reinterpret_cast<u32x4*>(Ot + j * a.ldot + i) =
+                        *reinterpret_cast<const u32x4*>(lds + r * LDT + c);
+            }
+    }
+    if (a.o) {
+        constexpr int NB = T / 8;   // 8 x 8 blocks along a side
+        uint16_t* __restrict__ O = a.o + w.b * a.so;
+#pragma unroll
+        for (int q = 0; q < NB * NB / kNsThreads; ++q) {
+            const int blk = q * kNsThreads + tid;
+            const int bj = blk % NB, bi = blk / NB;
+            u32x4 rv[8];   // tile rows j = 8 bj .. + 7, columns i = 8 bi .. + 7
+#pragma unroll
+            for (int jj = 0; jj < 8; ++jj)
+                rv[jj] = *reinterpret_cast<const u32x4*>(lds + (bj * 8 + jj) * LDT + bi * 8);
+            const int64_t j = col0 + bj * 8;
+#pragma unroll
+            for (int ii = 0; ii < 8; ++ii) {
+                const int64_t i = row0 + bi * 8 + ii;
+                if (i < a.M && j < a.o_cols) {
+                    u32x4 o;
+#pragma unroll
+                    for (int p = 0; p < 4; ++p)
+                        o[p] = bf16_at(rv[2 * p], ii) | (bf16_at(rv[2 * p + 1], ii) << 16);
+                    *reinterpret_cast<u32x4*>(O + i * a.ldo + j) = o;
+                }
+            }
         }
+    }
+}
+
+template <int W, bool SPLIT>
+__global__ __launch_bounds__(kNsThreads, W == 2 ? 2 : 1) void k_ns_gemm(const NsGemmArgs a)
+{
+    using S = NsTileShape<W>;
+    constexpr int T = S::T, LDT = S::LDT, NP = S::kPasses;
+    __shared__ __attribute__((aligned(16))) uint16_t lds[S::kLds];
+    const int64_t total = int64_t(a.batch) * a.splits * a.tiles;
+    const int64_t per_xcd = (total + 7) / 8;
+    const int64_t wid = static_cast<int64_t>(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+    if (wid >= total) return;
+    const NsWork w = ns_decode(a, wid);
+    const int64_t row0 = int64_t(w.ti) * T, col0 = int64_t(w.tj) * T;
+    const int64_t kbeg = int64_t(w.s) * a.kchunk;
+    const int64_t kend = SPLIT ? min(int64_t(a.K), kbeg + a.kchunk) : int64_t(a.K);
+
+    // Operands through buffer resources over the tile's own rows of this batch entry,
+    // ending at row M (N): the hardware returns zero for a load whose vector offset (the
+    // lane's row, its row pass and K position) lies past the range, so the loads need no
+    // predicates (K is a whole number of stages). The stage's K offset is uniform.
+    const int64_t prow = min(int64_t(T), int64_t(a.M) - row0);
+    const int64_t qrow = min(int64_t(T), int64_t(a.N) - col0);
+    const __amdgpu_buffer_rsrc_t rp = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(a.p + w.b * a.sp + row0 * a.ldp), 0,
+        static_cast<int>(2 * prow * a.ldp), 0x00020000);
+    const __amdgpu_buffer_rsrc_t rq = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(a.q + w.b * a.sq + col0 * a.ldq), 0,
+        static_cast<int>(2 * qrow * a.ldq), 0x00020000);
+    const int ldp = static_cast<int>(a.ldp), ldq = static_cast<int>(a.ldq);
+
+    const int tid = threadIdx.x;
+    const int lrow = tid >> 3, lk = (tid & 7) * 8;   // loader: 8 threads per 64-element row
+    const int vp = 2 * (lrow * ldp + lk), vq = 2 * (lrow * ldq + lk);
+    u32x4 ra[NP], rb[NP];
+    auto gload = [&](int k0) {
+#pragma unroll
+        for (int r = 0; r < NP; ++r) {
+            ra[r] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                  rp, vp + 64 * r * ldp, 2 * k0, 0));
+            rb[r] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                  rq, vq + 64 * r * ldq, 2 * k0, 0));
+        }
+    };
+    auto lstore = [&](int buf) {
+        uint16_t* sa = lds + buf * S::kStage;
+        uint16_t* sb = sa + T * LDK;
+#pragma unroll
+        for (int r = 0; r < NP; ++r) {
+            *reinterpret_cast<u32x4*>(sa + (lrow + 32 * r) * LDK + lk) = ra[r];
+            *reinterpret_cast<u32x4*>(sb + (lrow + 32 * r) * LDK + lk) = rb[r];
+        }
+    };
+
+    const int lane = tid & 63, wave = tid >> 6;
+    const int wm = (wave >> 1) * (32 * W), wn = (wave & 1) * (32 * W);
+    const int frow = lane & 31, fk = (lane >> 5) * 8;
+    f32x16 acc[W][W];
+#pragma unroll
+    for (int mi = 0; mi < W; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < W; ++ni)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[mi][ni][v] = 0.0f;
+
+    // The fragments of one 16-wide K step: rows of the wave's A and B blocks.
+    typedef bf16x8 Frag[W];
+    auto frags = [&](Frag& fa, Frag& fb, int buf, int kk) {
+        const uint16_t* sa = lds + buf * S::kStage;
+        const uint16_t* sb = sa + T * LDK;
+#pragma unroll
+        for (int mi = 0; mi < W; ++mi)
+            fa[mi] = __builtin_bit_cast(
+                bf16x8, *reinterpret_cast<const u32x4*>(sa + (wm + mi * 32 + frow) * LDK + kk + fk));
+#pragma unroll
+        for (int ni = 0; ni < W; ++ni)
+            fb[ni] = __builtin_bit_cast(
+                bf16x8, *reinterpret_cast<const u32x4*>(sb + (wn + ni * 32 + frow) * LDK + kk + fk));
+    };
+    auto mfmas = [&](const Frag& fa, const Frag& fb, int from, int to) {
+#pragma unroll
+        for (int q = from; q < to; ++q)
+            acc[q / W][q % W] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[q / W], fb[q % W],
+                                                                       acc[q / W][q % W], 0, 0, 0);
+    };
+    // Scheduling groups (instruction classes of __builtin_amdgcn_sched_group_barrier):
+    // `n` matrix-core ops, each followed by `per` ops of class `mask`.
+    constexpr int kMfma = 0x008, kDsRead = 0x100, kDsWrite = 0x200, kVmemRead = 0x020;
+    constexpr int kMM = W * W;                 // MFMAs of one K step
+    constexpr int kFr = 2 * W;                 // fragment reads of one K step
+    constexpr int kWr = 2 * NP;                // LDS writes of one stage
+
+    // One stage in a software pipeline: the next stage's global loads go out first; each
+    // K step's matrix-core ops run while the next step's fragments are read from LDS; the
+    // next stage goes into the other LDS buffer during the third step, and after a
+    // barrier in the middle of the fourth step the next stage's first fragments are read.
+    Frag fa, fb, na, nb;
+    const int nk = static_cast<int>((kend - kbeg) / BK);
+    gload(static_cast<int>(kbeg));
+    lstore(0);
+    __syncthreads();
+    frags(fa, fb, 0, 0);
+    // Fragment reads against matrix-core ops inside one K step. With W = 2 a step has
+    // only four MFMAs, so all of the next step's reads go out before them (their own
+    // registers; reads placed between the MFMAs would reuse the current fragments'
+    // registers and reach the next step's first MFMA too late); with W = 4 they go out
+    // one per MFMA over the first half of the step.
+    auto step_groups = [&]() {
+        if constexpr (W == 2) {
+            __builtin_amdgcn_sched_group_barrier(kDsRead, kFr, 0);
+            __builtin_amdgcn_sched_group_barrier(kMfma, kMM, 0);
+        } else {
+#pragma unroll
+            for (int q = 0; q < kFr; ++q) {
+                __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(kDsRead, 1, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(kMfma, kMM - kFr, 0);
+        }
+    };
+    auto advance = [&]() {
+#pragma unroll
+        for (int q = 0; q < W; ++q) {
+            fa[q] = na[q];
+            fb[q] = nb[q];
+        }
+    };
+    for (int it = 0; it + 1 < nk; ++it) {
+        const int cur = it & 1;
+        gload(static_cast<int>(kbeg) + (it + 1) * BK);
+        __builtin_amdgcn_sched_group_barrier(kVmemRead, kWr, 0);
+        // steps 0 and 1
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            frags(na, nb, cur, (ks + 1) * 16);
+            mfmas(fa, fb, 0, kMM);
+            step_groups();
+            advance();
+        }
+        // step 2: the last fragments of this stage, the next stage into LDS
+        frags(na, nb, cur, 48);
+        lstore(cur ^ 1);
+        mfmas(fa, fb, 0, kMM);
+        if constexpr (W == 2) {
+            __builtin_amdgcn_sched_group_barrier(kDsRead, kFr, 0);
+#pragma unroll
+            for (int q = 0; q < kMM; ++q) {
+                __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(kDsWrite, kWr / kMM, 0);
+            }
+            // step 3: the barrier first, then the next stage's first fragments before
+            // this step's MFMAs
+            __syncthreads();
+            frags(fa, fb, cur ^ 1, 0);
+            mfmas(na, nb, 0, kMM);
+            __builtin_amdgcn_sched_group_barrier(kDsRead, kFr, 0);
+            __builtin_amdgcn_sched_group_barrier(kMfma, kMM, 0);
+        } else {
+#pragma unroll
+            for (int q = 0; q < kMM; ++q) {
+                __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
+                if (q < kFr) __builtin_amdgcn_sched_group_barrier(kDsRead, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(kDsWrite, (kWr + kMM - 1) / kMM, 0);
+            }
+            // step 3: half its MFMAs, the barrier, then the next stage's first fragments
+            // under the other half
+            mfmas(na, nb, 0, kMM / 2);
+            __builtin_amdgcn_sched_group_barrier(kMfma, kMM / 2, 0);
+            __syncthreads();
+            frags(fa, fb, cur ^ 1, 0);
+            mfmas(na, nb, kMM / 2, kMM);
+#pragma unroll
+            for (int q = 0; q < kMM / 2; ++q) {
+                __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(kDsRead, (2 * kFr + kMM - 1) / kMM, 0);
+            }
+        }
+    }
+    {   // the last stage
+        const int cur = (nk - 1) & 1;
+#pragma unroll
+        for (int ks = 0; ks < 3; ++ks) {
+            frags(na, nb, cur, (ks + 1) * 16);
+            mfmas(fa, fb, 0, kMM);
+            step_groups();
+            advance();
+        }
+        mfmas(fa, fb, 0, kMM);
+    }
+    __syncthreads();   // the epilogue reuses the LDS
+
+    // Accumulator element v of block (mi, ni): row (v / 4) * 8 + (lane / 32) * 4 + v % 4,
+    // column lane % 32 of the 32 x 32 block.
+    if constexpr (SPLIT) {
+        float* __restrict__ part = a.partial + ((int64_t(w.s) * a.batch + w.b) * a.M) * a.N;
+#pragma unroll
+        for (int mi = 0; mi < W; ++mi)
+#pragma unroll
+            for (int ni = 0; ni < W; ++ni) {
+                const int64_t j = col0 + wn + ni * 32 + frow;
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int64_t i = row0 + wm + mi * 32 + (v >> 2) * 8 + fk / 2 + (v & 3);
+                    if (i < a.M && j < a.N) part[i * a.N + j] = acc[mi][ni][v];
+                }
+            }
+    } else {
+        epilogue<W>(a, w, acc, lds, tid);
     }
 }
 
 // Split-K Gram: O[b][i][j] = bf16(alpha * the sum over the chunks s, in order, of the
 // float32 partials of (i, j)), zero in the padding columns N .. o_cols - 1, and the mirror
-// O[b][j][i] for tiles above the diagonal. A workgroup takes 16 rows of one upper tile:
-// each thread sums 8 consecutive partials of a row (two 16-byte loads per chunk) and
-// stores them as one 16-byte row segment; the mirror goes through an LDS transpose.
+// O[b][j][i] for tiles above the diagonal. A workgroup takes 16 rows x 128 columns of one
+// upper tile: each thread sums 8 consecutive partials of a row (two 16-byte loads per
+// chunk) and stores them as one 16-byte row segment; the mirror goes through an LDS
+// transpose.
 constexpr int kReduceRows = 16;
+constexpr int kReduceCols = 128;
+constexpr int kReduceLdt = kReduceCols + 8;
 
 __global__ __launch_bounds__(256) void k_ns_reduce(const NsGemmArgs a)
 {
-    __shared__ __attribute__((aligned(16))) uint16_t t[kReduceRows * LDT];
-    const int64_t slices = BM / kReduceRows;
+    __shared__ __attribute__((aligned(16))) uint16_t t[kReduceRows * kReduceLdt];
+    const int64_t slices = int64_t(a.tile / kReduceRows) * (a.tile / kReduceCols);
     const int64_t total = int64_t(a.batch) * a.tiles * slices;
     const int64_t wid = blockIdx.x;
     if (wid >= total) return;
@@ -252,7 +392,9 @@ __global__ __launch_bounds__(256) void k_ns_reduce(const NsGemmArgs a)
     one.splits = 1;
     const NsWork w = ns_decode(one, wid / slices);
     const int slice = static_cast<int>(wid % slices);
-    const int64_t row0 = int64_t(w.ti) * BM + slice * kReduceRows, col0 = int64_t(w.tj) * BN;
+    const int rs = slice / (a.tile / kReduceCols), cs = slice % (a.tile / kReduceCols);
+    const int64_t row0 = int64_t(w.ti) * a.tile + rs * kReduceRows;
+    const int64_t col0 = int64_t(w.tj) * a.tile + cs * kReduceCols;
     const int tid = threadIdx.x, r = tid >> 4, scol = (tid & 15) * 8;
     const int64_t plane = int64_t(a.batch) * a.M * a.N;
     const int64_t i = row0 + r, j0 = col0 + scol;
@@ -282,7 +424,7 @@ __global__ __launch_bounds__(256) void k_ns_reduce(const NsGemmArgs a)
     if (i < a.M && j0 < a.o_cols)
         *reinterpret_cast<u32x4*>(a.o + w.b * a.so + i * a.ldo + j0) = h;
     if (w.ti == w.tj) return;
-    *reinterpret_cast<u32x4*>(t + r * LDT + scol) = h;
+    *reinterpret_cast<u32x4*>(t + r * kReduceLdt + scol) = h;
     __syncthreads();
     // mirror: row j = col0 + jr of O takes this slice's 16 rows as columns
     const int jr = tid >> 1, half = (tid & 1) * 8;
@@ -291,8 +433,8 @@ __global__ __launch_bounds__(256) void k_ns_reduce(const NsGemmArgs a)
         u32x4 m;
 #pragma unroll
         for (int c = 0; c < 4; ++c)
-            m[c] = uint32_t(t[(half + 2 * c) * LDT + jr]) |
-                   (uint32_t(t[(half + 2 * c + 1) * LDT + jr]) << 16);
+            m[c] = uint32_t(t[(half + 2 * c) * kReduceLdt + jr]) |
+                   (uint32_t(t[(half + 2 * c + 1) * kReduceLdt + jr]) << 16);
         *reinterpret_cast<u32x4*>(a.ot + w.b * a.sot + j * a.ldot + ic) = m;
     }
 }
@@ -307,32 +449,25 @@ __global__ __launch_bounds__(256) void k_ns_reduce(const NsGemmArgs a)
 constexpr int kTile = 64;
 constexpr int kTilesPerGroup = 4;
 
-// Element j (0..7) of eight packed bfloat16.
-__device__ __forceinline__ uint32_t bf16_at(const u32x4& w, int j)
-{
-    const uint32_t v = w[j >> 1];
-    return (j & 1) ? (v >> 16) : (v & 0xffffu);
-}
 
 // Batch entry b takes tensor t = tensor_of ? tensor_of[b] : b, whose R x C matrix starts at
 // src + src_off[t] (src_off null: src + b R C; bfloat16), divided by norm[t] (norm null:
-// 1). Writes, with zero padding,
-// copy[b] (R x cs, cs = C rounded up to 8) = S / norm and trans[b] (C x ts, ts = R rounded up
-// to 8) = (S / norm)^T; copy_stride / trans_stride are the batch strides.
+// 1). Writes, zero in the padding, copy[b] (R rows of cs >= C elements) = S / norm and
+// trans[b] (C rows of ts >= R elements) = (S / norm)^T; cs and ts are multiples of 8,
+// copy_stride / trans_stride the batch strides.
 __global__ __launch_bounds__(256) void k_ns_prep(const uint16_t* __restrict__ src,
                                                  const int64_t* __restrict__ src_off,
                                                  const int32_t* __restrict__ tensor_of,
                                                  const float* __restrict__ norm, int64_t R,
                                                  int64_t C, uint16_t* __restrict__ copy,
-                                                 int64_t copy_stride,
+                                                 int64_t copy_stride, int64_t cs,
                                                  uint16_t* __restrict__ trans,
-                                                 int64_t trans_stride)
+                                                 int64_t trans_stride, int64_t ts)
 {
     const int b = blockIdx.z;
     const int t = tensor_of ? tensor_of[b] : b;
     const uint16_t* __restrict__ s = src + (src_off ? src_off[t] : b * R * C);
     const float nrm = norm ? norm[t] : 1.0f;
-    const int64_t cs = (C + 7) / 8 * 8, ts = (R + 7) / 8 * 8;
     uint16_t* __restrict__ cp = copy + b * copy_stride;
     uint16_t* __restrict__ tp = trans + b * trans_stride;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -426,28 +561,38 @@ __global__ __launch_bounds__(256) void k_ns_unpad(const uint16_t* __restrict__ s
 hipError_t launch_ns_gemm(const NsGemmArgs& a, hipStream_t stream)
 {
     const int64_t groups = ns_workgroups(a);
-    hipLaunchKernelGGL(k_ns_gemm, dim3(static_cast<unsigned>(groups)), dim3(kNsThreads), 0, stream,
-                       a);
+    const dim3 grid(static_cast<unsigned>(groups)), block(kNsThreads);
+    if (a.tile == kNsTileBig) {
+        if (a.splits > 1)
+            hipLaunchKernelGGL((k_ns_gemm<4, true>), grid, block, 0, stream, a);
+        else
+            hipLaunchKernelGGL((k_ns_gemm<4, false>), grid, block, 0, stream, a);
+    } else {
+        if (a.splits > 1)
+            hipLaunchKernelGGL((k_ns_gemm<2, true>), grid, block, 0, stream, a);
+        else
+            hipLaunchKernelGGL((k_ns_gemm<2, false>), grid, block, 0, stream, a);
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.splits == 1) return e;
-    hipLaunchKernelGGL(k_ns_reduce,
-                       dim3(static_cast<unsigned>(int64_t(a.batch) * a.tiles * (BM / kReduceRows))),
+    const int64_t slices = int64_t(a.tile / kReduceRows) * (a.tile / kReduceCols);
+    hipLaunchKernelGGL(k_ns_reduce, dim3(static_cast<unsigned>(int64_t(a.batch) * a.tiles * slices)),
                        dim3(256), 0, stream, a);
     return hipGetLastError();
 }
 
 hipError_t launch_ns_prep(const uint16_t* src, const int64_t* src_off, const int32_t* tensor_of,
                           const float* norm, int32_t batch, int64_t R, int64_t C, uint16_t* copy,
-                          int64_t copy_stride, uint16_t* trans, int64_t trans_stride,
-                          hipStream_t stream)
+                          int64_t copy_stride, int64_t cs, uint16_t* trans, int64_t trans_stride,
+                          int64_t ts, hipStream_t stream)
 {
-    const int64_t ts = (R + 7) / 8 * 8, cs = (C + 7) / 8 * 8;
+    if (cs < C || ts < R || cs % 8 || ts % 8) return hipErrorInvalidValue;
     const int64_t gx = (cs + kTile - 1) / kTile;
     const int64_t gy = (ts + kTile * kTilesPerGroup - 1) / (kTile * kTilesPerGroup);
     if (gx > 0x7fffffff || gy > 65535 || batch > 65535) return hipErrorInvalidConfiguration;
     hipLaunchKernelGGL(k_ns_prep, dim3(static_cast<unsigned>(gx), static_cast<unsigned>(gy), batch),
                        dim3(256), 0, stream, src, src_off, tensor_of, norm, R, C, copy,
-                       copy_stride, trans, trans_stride);
+                       copy_stride, cs, trans, trans_stride, ts);
     return hipGetLastError();
 }
 

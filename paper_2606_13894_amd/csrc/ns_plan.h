@@ -3,9 +3,10 @@
 // Plain C++ with no HIP types, so that host-only tests can build and check it.
 //
 // Layout of one shape group of `count` wide matrices (m rows <= n columns):
-//   X   count x m x ldx   row-major, ldx = n rounded up to 8, zero in columns n .. ldx-1
-//   Xt  count x ldx x ldm row-major X^T, ldm = m rounded up to 8, zero in columns m ..
-//       ldm-1 (rows n .. ldx-1 are never read)
+//   X   count x m x ldx   row-major, ldx = n rounded up to 64 (whole K stages), zero in
+//       columns n .. ldx-1
+//   Xt  count x ldx x ldm row-major X^T, ldm = m rounded up to 64 (8 for a vector), zero
+//       in columns m .. ldm-1 (rows n .. ldx-1 are never read)
 //   A   count x m x ldm   (A = X X^T, symmetric), zero in columns m .. ldm-1
 //   B   count x m x ldm   (B = b A + c A A, symmetric), same padding
 // Every product reads both operands along contiguous K:
@@ -30,9 +31,16 @@
 
 namespace gefen {
 
-constexpr int kNsTile = 128;   // output rows and columns of one workgroup
+// Output tiles of one workgroup: 128 x 128 (four waves of 64 x 64, two workgroups per
+// compute unit) or 256 x 256 (four waves of 128 x 128, one per compute unit: twice the
+// flops per loaded byte and four times the matrix-core work per K stage, to cover memory
+// latency on the large products).
+constexpr int kNsTileSmall = 128;
+constexpr int kNsTileBig = 256;
 constexpr int kNsBK = 64;      // K of one pipeline stage
 constexpr int kNsThreads = 256;
+constexpr int kNsCUs = 256;
+constexpr int kNsBand = 4;     // tile rows per band of a non-symmetric product
 
 // One batched product C[i][j] = sum_k P[i][k] Q[j][k] (i < M, j < N, k < K), then
 //   value(i, j) = bf16(alpha * C[i][j] + beta * E[i][j]),  E[i][j] = et[j * lde + i]
@@ -57,6 +65,7 @@ struct NsGemmArgs {
     uint16_t* ot;
     int64_t ldot, sot;
     float* partial;
+    int32_t tile;         // kNsTileSmall or kNsTileBig
     int32_t M, N, K;
     int32_t o_cols, ot_cols;
     int32_t batch, sym, splits;
@@ -66,33 +75,44 @@ struct NsGemmArgs {
     float alpha, beta;
 };
 
-inline int64_t ns_round8(int64_t v) { return (v + 7) / 8 * 8; }
-inline int32_t ns_tiles_along(int64_t v) { return static_cast<int32_t>((v + kNsTile - 1) / kNsTile); }
+inline int64_t ns_round64(int64_t v) { return (v + 63) / 64 * 64; }
+inline int32_t ns_tiles_along(int64_t v, int tile)
+{
+    return static_cast<int32_t>((v + tile - 1) / tile);
+}
+
+// Workgroups resident on the GPU at once, and the share of their rounds that `groups`
+// workgroups fill.
+inline int64_t ns_slots(int tile) { return tile == kNsTileBig ? kNsCUs : 2 * kNsCUs; }
+inline double ns_fill(int64_t groups, int tile)
+{
+    const int64_t slots = ns_slots(tile);
+    return double(groups) / double((groups + slots - 1) / slots * slots);
+}
 
 // Sizes of one shape group.
 struct NsShape {
     int64_t count, m, n, ldx, ldm;
     int32_t splits;   // K chunks of the Gram product
     int32_t kchunk;   // their length (a multiple of kNsBK; ldx when splits == 1)
+    int32_t tile_gram, tile_poly, tile_comb;
 };
 
 // Split the Gram product over K so that its workgroups (count x t (t + 1) / 2 upper
-// tiles, times the split) fill their rounds on the GPU -- 256 compute units, two resident
-// workgroups each, so rounds of 512: the smallest split whose rounds are at least 90 %
-// full, else the fullest, with chunks of at least 8 stages and at most 32 chunks. A lone
-// tall-skinny matrix (a token embedding: 21 tiles at m = 768) splits 22 ways; a batch
-// that already fills its rounds (the GPT-2 MLP group: 504 tiles) does not split.
-inline int32_t ns_gram_splits(int64_t count, int64_t m, int64_t ldx)
+// tiles, times the split) fill their rounds on the GPU: the smallest split whose rounds
+// are at least 90 % full, else the fullest, with chunks of at least 8 stages and at most
+// 32 chunks. A lone tall-skinny matrix (a token embedding: 21 small tiles at m = 768)
+// splits 22 ways; a batch that fills its rounds (the GPT-2 MLP group: 504 small tiles)
+// does not split.
+inline int32_t ns_gram_splits(int64_t count, int64_t m, int64_t ldx, int tile)
 {
-    constexpr int64_t kSlots = 512;
-    const int64_t t = ns_tiles_along(m);
+    const int64_t t = ns_tiles_along(m, tile);
     const int64_t work = count * t * (t + 1) / 2;
     const int64_t smax = std::max<int64_t>(1, std::min<int64_t>(32, ldx / (8 * kNsBK)));
     int64_t best = 1;
     double best_fill = 0.0;
     for (int64_t s = 1; s <= smax; ++s) {
-        const int64_t groups = work * s;
-        const double fill = double(groups) / double((groups + kSlots - 1) / kSlots * kSlots);
+        const double fill = ns_fill(work * s, tile);
         if (fill >= 0.9) return static_cast<int32_t>(s);
         if (fill > best_fill + 1e-12) {
             best = s;
@@ -102,11 +122,29 @@ inline int32_t ns_gram_splits(int64_t count, int64_t m, int64_t ldx)
     return static_cast<int32_t>(best);
 }
 
+// The big tile for a product of M x N outputs (upper tiles only when symmetric) when both
+// sides hold at least four big tiles and its workgroups fill at least 75 % of their
+// rounds; else the small tile. (Measured on the model shapes: at M = 768 the small tile
+// is faster for every product -- the MLP combine 186 against 231 us, the Gram 72 against
+// 154 us with its split -- and at M = 2048 the big one by about 8 %.)
+inline int ns_pick_tile(int64_t count, int64_t M, int64_t N, bool sym, int32_t splits = 1)
+{
+    if (M < 4 * kNsTileBig || N < 4 * kNsTileBig) return kNsTileSmall;
+    const int64_t tm = ns_tiles_along(M, kNsTileBig), tn = ns_tiles_along(N, kNsTileBig);
+    const int64_t tiles = sym ? tm * (tm + 1) / 2 : tm * tn;
+    return ns_fill(count * tiles * splits, kNsTileBig) >= 0.75 ? kNsTileBig : kNsTileSmall;
+}
+
 inline NsShape ns_shape(int64_t count, int64_t m, int64_t n)
 {
-    NsShape s{count, m, n, ns_round8(n), ns_round8(m), 1, 0};
-    s.splits = m > 1 ? ns_gram_splits(count, m, s.ldx) : 1;   // vectors have no Gram product
+    NsShape s{count, m, n, ns_round64(n), m > 1 ? ns_round64(m) : 8, 1, 0, kNsTileSmall,
+              kNsTileSmall, kNsTileSmall};
     s.kchunk = static_cast<int32_t>(s.ldx);
+    if (m < 2) return s;   // vectors have no matrix products
+    // the Gram product: the big tile when it fills the GPU with its own best split
+    const int32_t sb = ns_gram_splits(count, m, s.ldx, kNsTileBig);
+    s.tile_gram = ns_pick_tile(count, m, m, true, sb);
+    s.splits = s.tile_gram == kNsTileBig ? sb : ns_gram_splits(count, m, s.ldx, kNsTileSmall);
     if (s.splits > 1) {
         // equal chunks of whole stages; the last one may be shorter, none is empty
         const int64_t chunk = (s.ldx + s.splits - 1) / s.splits;
@@ -114,6 +152,8 @@ inline NsShape ns_shape(int64_t count, int64_t m, int64_t n)
         s.splits = static_cast<int32_t>((s.ldx + s.kchunk - 1) / s.kchunk);
         if (s.splits < 2) s.kchunk = static_cast<int32_t>(s.ldx);
     }
+    s.tile_poly = ns_pick_tile(count, m, m, true);
+    s.tile_comb = ns_pick_tile(count, m, n, false);
     return s;
 }
 
@@ -125,16 +165,21 @@ inline int64_t ns_partial_elems(const NsShape& s)
     return s.splits > 1 ? int64_t(s.splits) * s.count * s.m * s.m : 0;
 }
 
-inline void ns_fill_tiles(NsGemmArgs& a)
+inline void ns_fill_tiles(NsGemmArgs& a, int tile)
 {
-    a.tm = ns_tiles_along(a.M);
-    a.tn = ns_tiles_along(a.N);
+    a.tile = tile;
+    a.tm = ns_tiles_along(a.M, tile);
+    a.tn = ns_tiles_along(a.N, tile);
     a.tiles = a.sym ? a.tm * (a.tm + 1) / 2 : a.tm * a.tn;
 }
 
 // Work item `wid` of a product: batch entry, K chunk and output tile (row and column
 // tile). Work items run batch-major, then chunk, then tile; symmetric products number
-// their upper tiles row by row.
+// their upper tiles row by row. Other products number their tiles in bands of up to
+// kNsBand tile rows, column by column inside a band, so that the workgroups that run at
+// once on an XCD (its 32 compute units take consecutive work items) share a few row and
+// column slabs of the operands in its L2: 4 x 8 tiles read 12 slabs where a row of 32
+// tiles reads 33.
 struct NsWork {
     int64_t b;
     int32_t s, ti, tj;
@@ -157,8 +202,11 @@ inline NS_HOST_DEVICE NsWork ns_decode(const NsGemmArgs& a, int64_t wid)
         w.ti = ti;
         w.tj = ti + t;
     } else {
-        w.ti = t / a.tn;
-        w.tj = t - w.ti * a.tn;
+        const int32_t band = t / (kNsBand * a.tn);
+        const int32_t r = t - band * (kNsBand * a.tn);
+        const int32_t rows = a.tm - band * kNsBand < kNsBand ? a.tm - band * kNsBand : kNsBand;
+        w.ti = band * kNsBand + r % rows;
+        w.tj = r / rows;
     }
     return w;
 }
@@ -184,7 +232,7 @@ inline NsGemmArgs ns_gram_args(const NsShape& s, const uint16_t* x, uint16_t* a_
     a.beta = 0.0f;
     a.kchunk = s.kchunk;
     if (s.splits > 1) a.partial = partial;
-    ns_fill_tiles(a);
+    ns_fill_tiles(a, s.tile_gram);
     return a;
 }
 
@@ -208,7 +256,7 @@ inline NsGemmArgs ns_poly_args(const NsShape& s, const uint16_t* a_in, uint16_t*
     a.kchunk = a.K;
     a.alpha = c;
     a.beta = b;
-    ns_fill_tiles(a);
+    ns_fill_tiles(a, s.tile_poly);
     return a;
 }
 
@@ -240,7 +288,7 @@ inline NsGemmArgs ns_combine_args(const NsShape& s, const uint16_t* b_in, const 
     a.kchunk = a.K;
     a.alpha = 1.0f;
     a.beta = a_coef;
-    ns_fill_tiles(a);
+    ns_fill_tiles(a, s.tile_comb);
     return a;
 }
 
@@ -274,10 +322,17 @@ inline std::string ns_check(const NsGemmArgs& a, int64_t p_avail, int64_t q_avai
         return std::string(buf);
     };
     if (a.M < 1 || a.N < 1 || a.K < 1 || a.batch < 1) return bad("empty product");
-    if (a.K % 8 || a.ldp % 8 || a.ldq % 8 || a.sp % 8 || a.sq % 8) return bad("K or operand alignment");
+    if (a.K % kNsBK || a.ldp % 8 || a.ldq % 8 || a.sp % 8 || a.sq % 8)
+        return bad("K or operand alignment");
     if (a.K > a.ldp || a.K > a.ldq) return bad("K beyond a leading dimension");
+    // each tile reads its operand rows through buffer resources with 32-bit byte ranges
+    // and offsets: a tile's rows must span less than 2 GiB (rows of < 4 Mi elements)
+    if (2 * int64_t(a.tile) * a.ldp >= (int64_t(1) << 31) ||
+        2 * int64_t(a.tile) * a.ldq >= (int64_t(1) << 31))
+        return bad("a tile's operand rows span 2 GiB");
     if (!a.p || !a.q) return bad("missing operand");
-    const int64_t tm = ns_tiles_along(a.M), tn = ns_tiles_along(a.N);
+    if (a.tile != kNsTileSmall && a.tile != kNsTileBig) return bad("tile size");
+    const int64_t tm = ns_tiles_along(a.M, a.tile), tn = ns_tiles_along(a.N, a.tile);
     if (a.tm != tm || a.tn != tn || a.tiles != (a.sym ? tm * (tm + 1) / 2 : tm * tn))
         return bad("tile counts");
     if (a.sym && (a.M != a.N || a.p != a.q)) return bad("symmetric product of unequal operands");
@@ -455,17 +510,15 @@ inline std::string ns_check_group(const NsGroup& g, const NsLaneBuffers& lb, con
     const NsShape& sh = g.shape;
     const int64_t xs = sh.m * sh.ldx, ts = sh.ldx * sh.ldm;
     for (const NsPart& pt : g.parts) {
-        // prep: copy rows R x round8(C) and transpose C x round8(R) at the part's batch
-        // entries; the update reads the same extents
+        // prep: copy R rows of cs >= C and transpose C rows of tr >= R elements at the
+        // part's batch entries (cs, tr: the group's row strides); the update reads the same
         const int64_t R = sh.m == 1 ? 1 : pt.rows, C = sh.m == 1 ? pt.rows * pt.cols : pt.cols;
         const bool wide = sh.m == 1 || !pt.transposed;
-        const int64_t copy_end = (pt.first + pt.count - 1) * (wide ? xs : ts) +
-                                 (R - 1) * ns_round8(C) + ns_round8(C);
-        const int64_t trans_end = (pt.first + pt.count - 1) * (wide ? ts : xs) +
-                                  (C - 1) * ns_round8(R) + ns_round8(R);
+        const int64_t cs = wide ? sh.ldx : sh.ldm, tr = wide ? sh.ldm : sh.ldx;
+        if (cs < C || tr < R || cs % 8 || tr % 8) return "prep strides do not hold the matrix";
+        const int64_t copy_end = (pt.first + pt.count - 1) * (wide ? xs : ts) + R * cs;
+        const int64_t trans_end = (pt.first + pt.count - 1) * (wide ? ts : xs) + C * tr;
         if (copy_end > z.x_elems || trans_end > z.x_elems) return "prep beyond the lane buffers";
-        if (ns_round8(C) != (wide ? sh.ldx : sh.ldm) || ns_round8(R) != (wide ? sh.ldm : sh.ldx))
-            return "prep strides differ from the group layout";
     }
     if (sh.m < 2) return std::string();   // vector kernel: X rows of ldx elements
     for (int cur = 0; cur < 2; ++cur) {

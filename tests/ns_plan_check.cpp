@@ -10,6 +10,7 @@
 // buffer behind that pointer. Prints one line per group and "ok", or the first failure.
 #include "ns_plan.h"
 
+#include <algorithm>
 #include <cstdint>
 #include <cstdio>
 #include <cstdlib>
@@ -52,12 +53,13 @@ std::string walk(const NsGemmArgs& a, const int64_t avail[6], const char* what)
             std::snprintf(buf, sizeof buf, "%s: work item %lld repeats a tile", what, (long long)wid);
             return buf;
         }
-        const int64_t row0 = int64_t(w.ti) * kNsTile, col0 = int64_t(w.tj) * kNsTile;
+        const int64_t row0 = int64_t(w.ti) * a.tile, col0 = int64_t(w.tj) * a.tile;
         if (row0 >= a.M || col0 >= a.N) return std::string(what) + ": an empty tile";
         const int64_t kbeg = int64_t(w.s) * a.kchunk;
         const int64_t kend = a.splits > 1 ? std::min<int64_t>(a.K, kbeg + a.kchunk) : a.K;
-        if (kbeg >= kend || kend % 8) return std::string(what) + ": an empty or ragged K chunk";
-        const int64_t im = last(row0, kNsTile, a.M), jn = last(col0, kNsTile, a.N);
+        if (kbeg >= kend || kbeg % kNsBK || kend % kNsBK)
+            return std::string(what) + ": an empty or ragged K chunk";
+        const int64_t im = last(row0, a.tile, a.M), jn = last(col0, a.tile, a.N);
         auto over = [&](int64_t end, int k, const char* op) -> bool {
             if (end > avail[k]) {
                 std::snprintf(buf, sizeof buf, "%s: item %lld reads or writes %s up to %lld of %lld",
@@ -66,37 +68,52 @@ std::string walk(const NsGemmArgs& a, const int64_t avail[6], const char* what)
             }
             return false;
         };
-        // operand loads: rows below M (N), 16-byte vectors of K below kend
+        // operand loads: buffer resources from the tile's first row to row M (N); the
+        // loads that land inside are rows below M (N), 16-byte vectors of K below kend
         if (over(w.b * a.sp + im * a.ldp + kend, 0, "P")) return buf;
         if (over(w.b * a.sq + jn * a.ldq + kend, 1, "Q")) return buf;
-        if ((a.ldp % 8) || (a.ldq % 8) || (kbeg % 8)) return std::string(what) + ": misaligned load";
+        if ((a.ldp % 8) || (a.ldq % 8)) return std::string(what) + ": misaligned load";
+        // 32-bit byte offsets: lane row (< 32) and K position, plus row pass and stage
+        const int64_t off_p = 2 * ((a.tile - 1) * a.ldp + kend);
+        const int64_t off_q = 2 * ((a.tile - 1) * a.ldq + kend);
+        if (off_p >= (int64_t(1) << 31) || off_q >= (int64_t(1) << 31) ||
+            2 * std::min<int64_t>(a.tile, a.M - row0) * a.ldp >= (int64_t(1) << 31) ||
+            2 * std::min<int64_t>(a.tile, a.N - col0) * a.ldq >= (int64_t(1) << 31))
+            return std::string(what) + ": a buffer offset or range beyond 31 bits";
         if (a.splits > 1) {
             const int64_t end = ((int64_t(w.s) * a.batch + w.b) * a.M + im) * a.N + jn + 1;
             if (over(end, 5, "the partials")) return buf;
             continue;
         }
-        if (a.et && over(w.b * a.se + jn * a.lde + last(row0, kNsTile, a.lde) + 1, 2, "E"))
+        if (a.et && over(w.b * a.se + jn * a.lde + last(row0, a.tile, a.lde) + 1, 2, "E"))
             return buf;
         const bool mirror = a.ot && (!a.sym || w.ti != w.tj);
-        if (mirror && over(w.b * a.sot + jn * a.ldot + last(row0, kNsTile, a.ot_cols) + 1, 4, "Ot"))
+        if (mirror && over(w.b * a.sot + jn * a.ldot + last(row0, a.tile, a.ot_cols) + 1, 4, "Ot"))
             return buf;
-        if (a.o && over(w.b * a.so + im * a.ldo + last(col0, kNsTile, a.o_cols) + 1, 3, "O"))
+        if (a.o && over(w.b * a.so + im * a.ldo + last(col0, a.tile, a.o_cols) + 1, 3, "O"))
             return buf;
     }
     if (static_cast<int64_t>(seen.size()) != total) return std::string(what) + ": tiles missed";
-    if (a.splits > 1) {   // the reduce: one upper tile per workgroup, direct and mirror rows
-        for (int64_t wid = 0; wid < int64_t(a.batch) * a.tiles; ++wid) {
+    if (a.splits > 1) {   // the reduce: 16 rows x 128 columns of an upper tile per workgroup
+        const int64_t slices = int64_t(a.tile / 16) * (a.tile / 128);
+        for (int64_t wid = 0; wid < int64_t(a.batch) * a.tiles * slices; ++wid) {
             NsGemmArgs one = a;
             one.splits = 1;
-            const NsWork w = ns_decode(one, wid);
-            const int64_t row0 = int64_t(w.ti) * kNsTile, col0 = int64_t(w.tj) * kNsTile;
-            const int64_t im = last(row0, kNsTile, a.M);
-            if (w.b * a.so + im * a.ldo + last(col0, kNsTile, a.o_cols) + 1 > avail[3] ||
-                ((int64_t(a.splits) - 1) * a.batch * a.M + w.b * a.M + im) * a.N +
-                        last(col0, kNsTile, a.N) + 1 > avail[5] ||
-                (w.ti != w.tj && w.b * a.sot + last(col0, kNsTile, a.N) * a.ldot +
-                                         last(row0, kNsTile, a.ot_cols) + 1 > avail[4]))
-                return std::string(what) + ": reduce beyond its buffers";
+            const NsWork w = ns_decode(one, wid / slices);
+            const int64_t sl = wid % slices, rs = sl / (a.tile / 128), cs = sl % (a.tile / 128);
+            const int64_t row0 = int64_t(w.ti) * a.tile + 16 * rs;
+            const int64_t col0 = int64_t(w.tj) * a.tile + 128 * cs;
+            if (row0 >= a.M || col0 >= a.o_cols) continue;   // the kernel writes nothing there
+            const int64_t im = last(row0, 16, a.M);
+            if (w.b * a.so + im * a.ldo + last(col0, 128, a.o_cols) + 1 > avail[3])
+                return std::string(what) + ": reduce beyond O";
+            if (col0 < a.N && ((int64_t(a.splits) - 1) * a.batch * a.M + w.b * a.M + im) * a.N +
+                                      last(col0, 128, a.N) + 1 > avail[5])
+                return std::string(what) + ": reduce beyond the partials";
+            if (w.ti != w.tj && col0 < a.N &&
+                w.b * a.sot + last(col0, 128, a.N) * a.ldot + last(row0, 16, a.ot_cols) + 1 >
+                    avail[4])
+                return std::string(what) + ": reduce mirror beyond O";
         }
     }
     return std::string();
@@ -150,9 +167,10 @@ int main()
                 return 1;
             }
             std::printf("lane %d group %d: %lld x (%lld x %lld), ldx %lld ldm %lld, %d parts, "
-                        "Gram splits %d (chunk %d)\n", l, gi, (long long)sh.count,
-                        (long long)sh.m, (long long)sh.n, (long long)sh.ldx, (long long)sh.ldm,
-                        static_cast<int>(g.parts.size()), sh.splits, sh.kchunk);
+                        "Gram splits %d (chunk %d), tiles %d / %d / %d\n", l, gi,
+                        (long long)sh.count, (long long)sh.m, (long long)sh.n, (long long)sh.ldx,
+                        (long long)sh.ldm, static_cast<int>(g.parts.size()), sh.splits, sh.kchunk,
+                        sh.tile_gram, sh.tile_poly, sh.tile_comb);
             if (sh.m < 2) continue;
             for (int cur = 0; cur < 2; ++cur) {
                 NsGemmArgs prods[3];

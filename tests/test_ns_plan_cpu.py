@@ -53,3 +53,10 @@ def test_odd_shapes_stay_in_bounds(checker):
 def test_a_bad_shape_is_refused(checker):
     rc, out = _run(checker, [(7, 50)])
     assert rc == 1 and "does not divide" in out
+
+
+def test_rows_beyond_the_buffer_offsets_are_refused(checker):
+    """A tile's operand rows are read with 32-bit byte offsets: a 2 x 9,000,000 matrix
+    (Gram rows of 9 M elements, 128-row tiles) is refused by the library's own check, with the reason."""
+    rc, out = _run(checker, [(2, 2 * 9_000_000)])
+    assert rc == 1 and "span 2 GiB" in out, out
