@@ -534,9 +534,8 @@ def main():
     t = 0
     for _ in range(args.warmup):
         t += 1
-        st.step(params, grads[(t - 1) % 2], *hp, t)
-        if w.refit_every and t % w.refit_every == 0:
-            st.fit_codebook(grads[(t - 1) % 2])
+        st.step(params, grads[(t - 1) % 2], *hp, t,
+                fit=bool(w.refit_every and t % w.refit_every == 0))
     torch.cuda.synchronize()
 
     st.profile_begin(args.steps)
@@ -547,9 +546,11 @@ def main():
     marks[0].record()
     for i in range(args.steps):
         t += 1
-        st.step(params, grads[(t - 1) % 2], *hp, t)
-        if w.refit_every and t % w.refit_every == 0:
-            st.fit_codebook(grads[(t - 1) % 2])
+        refit = bool(w.refit_every and t % w.refit_every == 0)
+        # a refit step refits the codebook on its own gradients (gefen_step_fit: the
+        # histogram is taken inside the step kernels, then the DP)
+        st.step(params, grads[(t - 1) % 2], *hp, t, fit=refit)
+        if refit:
             refit_at.append(i)
         marks[i + 1].record()
     torch.cuda.synchronize()

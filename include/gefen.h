@@ -125,6 +125,20 @@ int gefen_step(gefen_state* st, const gefen_tensor* params, const gefen_tensor* 
                double weight_decay, int64_t t, void* stream);
 
 /* ------------------------------------------------------------------------------
+ * gefen_step_fit -- gefen_step, and the codebook refit (Alg. 3) on the same gradients:
+ * the result of gefen_step followed by gefen_fit_codebook(grads), bit for bit. The step
+ * kernels of explicit and irregular blocks take the histogram while they stream the
+ * gradients (each element is binned once its block's max |g| is known), so those blocks
+ * are not read a second time; the other tiles go through the histogram kernel. The
+ * new codebook ENCODES at the next step (this step decodes and encodes with the current
+ * one) and is used for both from the step after. The histogram stays readable as state
+ * array 7 until the next fit. Arguments, asynchrony and errors as gefen_step.
+ * ---------------------------------------------------------------------------- */
+int gefen_step_fit(gefen_state* st, const gefen_tensor* params, const gefen_tensor* grads,
+                   int32_t n_tensors, double lr, double beta1, double beta2, double eps,
+                   double weight_decay, int64_t t, void* stream);
+
+/* ------------------------------------------------------------------------------
  * gefen_fit_codebook -- refit the codebook (Alg. 3) on the gradients `grads`:
  * histogram of the block-absmax-normalised gradients (using the state's blocks),
  * then the exact DP on device. The new codebook is used to ENCODE at the next
@@ -204,14 +218,15 @@ int gefen_get_layout(const gefen_state* st, int64_t* code_offsets, int64_t* bloc
  * 2 = second moments (float[total_blocks]), 3 = decode codebook (float[k]),
  * 4 = encode codebook (float[k]), 5 = decode codebook in double (double[k]),
  * 6 = the Gefen-Muon bfloat16 momentum matrix (uint16[code index count], after
- * gefen_muon_init; read-only, as is 5).
+ * gefen_muon_init), 7 = the histogram of the last codebook fit (uint64[16 k]: init,
+ * gefen_fit_codebook or gefen_step_fit); 5, 6 and 7 are read-only.
  * `bytes` must equal the array size. Synchronises `stream` when dst is host memory.
  * Errors: EINVAL (NULL, unknown `which`, 6 before gefen_muon_init, size mismatch), EHIP. */
 int gefen_read_state(const gefen_state* st, int32_t which, void* dst, int64_t bytes,
                      void* stream);
 
 /* Overwrite a state array from `src` (host or device), same `which` and sizes as
- * gefen_read_state, except 5 and 6. Writing 3 or 4 installs a codebook (float[k]:
+ * gefen_read_state, except 5, 6 and 7. Writing 3 or 4 installs a codebook (float[k]:
  * finite, first -1, last +1, never decreasing -- a degenerate fit repeats +1 at the
  * end; EINVAL otherwise) into that slot. */
 int gefen_write_state(gefen_state* st, int32_t which, const void* src, int64_t bytes,

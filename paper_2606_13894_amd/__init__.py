@@ -29,7 +29,7 @@ F32, BF16 = 0, 1
 
 # symbols declared in include/gefen.h
 SYMBOLS = [
-    "gefen_init", "gefen_step", "gefen_fit_codebook", "gefen_partition_scores",
+    "gefen_init", "gefen_step", "gefen_step_fit", "gefen_fit_codebook", "gefen_partition_scores",
     "gefen_histogram", "gefen_dp_codebook", "gefen_get_periods", "gefen_get_layout",
     "gefen_read_state", "gefen_write_state", "gefen_get_fit_info", "gefen_state_bytes",
     "gefen_checkpoint_bytes", "gefen_export", "gefen_import", "gefen_profile_begin",
@@ -74,6 +74,8 @@ def load_library(path: str = LIB_PATH):
     lib.gefen_init.argtypes = [P(gefen_tensor), i32, vp, vp, i64, i32, f64, vp, P(vp)]
     lib.gefen_step.argtypes = [vp, P(gefen_tensor), P(gefen_tensor), i32, f64, f64, f64, f64,
                                f64, i64, vp]
+    lib.gefen_step_fit.argtypes = [vp, P(gefen_tensor), P(gefen_tensor), i32, f64, f64, f64,
+                                   f64, f64, i64, vp]
     lib.gefen_fit_codebook.argtypes = [vp, P(gefen_tensor), i32, vp]
     lib.gefen_partition_scores.argtypes = [P(gefen_tensor), f64, vp, vp, i32, P(i32), P(i64), vp]
     lib.gefen_histogram.argtypes = [vp, P(gefen_tensor), i32, vp, vp]
@@ -155,6 +157,7 @@ def _i64_array(vals):
 
 STATE_CODES, STATE_SCALE, STATE_V, STATE_CB_DEC, STATE_CB_ENC, STATE_CB_DEC64 = range(6)
 STATE_MUON_U = 6          # Gefen-Muon bfloat16 momentum matrix (after muon_init)
+STATE_HIST = 7            # histogram of the last codebook fit (uint64[16 k])
 MUON_NS_COEFFS = (3.4445, -4.7750, 2.0315)
 
 
@@ -197,12 +200,15 @@ class GefenState:
 
     # --------------------------------------------------------------- the path
     def step(self, params: Sequence, grads: Sequence, lr: float, betas=(0.9, 0.999),
-             eps: float = 1e-8, weight_decay: float = 0.0, t: int = 1, stream=None):
+             eps: float = 1e-8, weight_decay: float = 0.0, t: int = 1, stream=None,
+             fit: bool = False):
+        """One step; with fit=True also the codebook refit on these gradients
+        (gefen_step_fit: the same as step followed by fit_codebook(grads))."""
         pt = _tensors(params, "params")
         gt = _tensors(grads, "grads")
-        _check(_lib.gefen_step(self._h, pt, gt, self._n, float(lr), float(betas[0]),
-                               float(betas[1]), float(eps), float(weight_decay), int(t),
-                               _stream(stream)))
+        fn = _lib.gefen_step_fit if fit else _lib.gefen_step
+        _check(fn(self._h, pt, gt, self._n, float(lr), float(betas[0]), float(betas[1]),
+                  float(eps), float(weight_decay), int(t), _stream(stream)))
 
     def muon_init(self, rows: Sequence[int], stream=None):
         """Prepare Gefen-Muon steps; tensor i is rows[i] x (numel / rows[i])."""
@@ -270,7 +276,8 @@ class GefenState:
                 STATE_CB_DEC: (torch.float32, lay["k"]),
                 STATE_CB_ENC: (torch.float32, lay["k"]),
                 STATE_CB_DEC64: (torch.float64, lay["k"]),
-                STATE_MUON_U: (torch.int16, lay["code_offsets"][-1])}[which]
+                STATE_MUON_U: (torch.int16, lay["code_offsets"][-1]),
+                STATE_HIST: (torch.int64, 16 * lay["k"])}[which]
         dev = device if device is not None else torch.device("cuda", torch.cuda.current_device())
         out = torch.empty(spec[1], dtype=spec[0], device=dev)
         nbytes = out.numel() * out.element_size()

@@ -28,9 +28,7 @@ __device__ __forceinline__ float grad_at(const Seg& sg, int64_t i)
 
 __device__ __forceinline__ int bin_of(float g, float a, double half_nb, int nbins)
 {
-    const double x = static_cast<double>(g) / static_cast<double>(a);
-    int b = static_cast<int>((x + 1.0) * half_nb);
-    return b < nbins - 1 ? b : nbins - 1;
+    return hist_bin(g, a, half_nb, nbins);
 }
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));

@@ -1062,9 +1062,17 @@ int gefen_init(const gefen_tensor* grads0, int32_t n_tensors, const int64_t* per
     return GEFEN_OK;
 }
 
-int gefen_step(gefen_state* st, const gefen_tensor* params, const gefen_tensor* grads,
-               int32_t n_tensors, double lr, double beta1, double beta2, double eps,
-               double weight_decay, int64_t t, void* stream_)
+namespace {
+
+// One step (Alg. 1); with `fit`, the codebook fit (Alg. 3) on this step's gradients as
+// well: the KIND_G launches bin every element of their blocks on the way (the blocks'
+// max |g| come out of the same reduction as sum g^2), the other classes' tiles go through
+// the histogram kernel after their step launch, then the DP installs the new codebook
+// into the slot the next step encodes with -- the same result as gefen_step followed by
+// gefen_fit_codebook on the same gradients.
+int step_impl(gefen_state* st, const gefen_tensor* params, const gefen_tensor* grads,
+              int32_t n_tensors, double lr, double beta1, double beta2, double eps,
+              double weight_decay, int64_t t, void* stream_, bool fit)
 {
     int rc = check_against_state(st, params, n_tensors, true, "params");
     if (rc) return rc;
@@ -1091,27 +1099,67 @@ int gefen_step(gefen_state* st, const gefen_tensor* params, const gefen_tensor* 
     const CodebookDev cb = codebook_dev(st);
     const bool prof = st->prof_armed && st->prof_steps < st->prof_max_steps;
     const size_t ncls = st->classes.size();
+    if (fit) GEFEN_HIP(fill_zero(st->hist, sizeof(uint64_t) * st->nbins, stream));
     for (size_t ci = 0; ci < ncls; ++ci) {
         const Class& c = st->classes[ci];
+        const Tile* tiles = st->tiles + c.first;
         if (prof) GEFEN_HIP(hipEventRecord(st->prof_events[(st->prof_steps * ncls + ci) * 2], stream));
         hipError_t e =
             c.kind == KIND_H
-                ? launch_step_h(c.gdtype, st->code_bits, st->tiles + c.first, st->htiles + c.first, c.count,
+                ? launch_step_h(c.gdtype, st->code_bits, tiles, st->htiles + c.first, c.count,
                                 st->segs, st->codes, st->scale, st->vmom, cb, sc,
                                 st->h_partials, st->h_old, stream)
-                : launch_step(c.kind, c.gdtype, st->code_bits, c.vpl, c.bs, st->tiles + c.first, c.count,
+            : fit && c.kind == KIND_G
+                ? launch_step_g_hist(c.gdtype, st->code_bits, tiles, c.count, st->segs,
+                                     st->codes, st->scale, st->vmom, cb, sc, st->hist,
+                                     st->nbins, stream)
+                : launch_step(c.kind, c.gdtype, st->code_bits, c.vpl, c.bs, tiles, c.count,
                               st->segs, st->codes, st->scale, st->vmom, cb, sc, stream);
         if (e != hipSuccess)
             return fail(GEFEN_EHIP, "step launch (kind %d) failed: %s", c.kind, hipGetErrorString(e));
         if (prof) GEFEN_HIP(hipEventRecord(st->prof_events[(st->prof_steps * ncls + ci) * 2 + 1], stream));
+        if (fit && c.kind != KIND_G) {   // the gradients are read-only: any order is fine
+            if (c.kind == KIND_H)
+                GEFEN_HIP(launch_hist_h_absmax(tiles, st->htiles + c.first, c.count, st->segs,
+                                               st->h_absmax, stream));
+            GEFEN_HIP(launch_histogram(tiles, c.count, st->tile_kind + c.first,
+                                       st->htiles + c.first, st->h_absmax, st->segs, st->nbins,
+                                       st->hist, stream));
+        }
     }
     if (prof) ++st->prof_steps;
     st->dec_slot = st->enc_slot;
+    if (fit) {
+        const int slot = 1 - st->dec_slot;
+        GEFEN_HIP(launch_dp(st->hist, st->nbins, st->k, st->dp_ws, st->fit_cb64, st->fit_cost,
+                            st->fit_status, stream));
+        GEFEN_HIP(launch_install_codebook(st->fit_cb64, st->k, st->ng, st->cb32[slot],
+                                          st->cb64[slot], st->mid[slot], st->guide[slot], stream));
+        st->enc_slot = slot;
+    }
     if (std::getenv("GEFEN_DEBUG_SYNC")) {
         GEFEN_HIP(hipStreamSynchronize(stream));
         GEFEN_HIP(hipGetLastError());
     }
     return GEFEN_OK;
+}
+
+}  // namespace
+
+int gefen_step(gefen_state* st, const gefen_tensor* params, const gefen_tensor* grads,
+               int32_t n_tensors, double lr, double beta1, double beta2, double eps,
+               double weight_decay, int64_t t, void* stream)
+{
+    return step_impl(st, params, grads, n_tensors, lr, beta1, beta2, eps, weight_decay, t,
+                     stream, false);
+}
+
+int gefen_step_fit(gefen_state* st, const gefen_tensor* params, const gefen_tensor* grads,
+                   int32_t n_tensors, double lr, double beta1, double beta2, double eps,
+                   double weight_decay, int64_t t, void* stream)
+{
+    return step_impl(st, params, grads, n_tensors, lr, beta1, beta2, eps, weight_decay, t,
+                     stream, true);
 }
 
 int gefen_fit_codebook(gefen_state* st, const gefen_tensor* grads, int32_t n_tensors,
@@ -1228,6 +1276,7 @@ static int state_array(const gefen_state* st, int32_t which, void** ptr, int64_t
     case 3: *ptr = st->cb32[st->dec_slot]; *bytes = 4 * st->k; return GEFEN_OK;
     case 4: *ptr = st->cb32[st->enc_slot]; *bytes = 4 * st->k; return GEFEN_OK;
     case 5: *ptr = st->cb64[st->dec_slot]; *bytes = 8 * st->k; return GEFEN_OK;
+    case 7: *ptr = st->hist; *bytes = 8 * int64_t(st->nbins); return GEFEN_OK;
     case 6:
         if (!st->muon_ready) return fail(GEFEN_EINVAL, "array 6 needs gefen_muon_init");
         *ptr = st->muon_u;
@@ -1256,7 +1305,7 @@ int gefen_write_state(gefen_state* st, int32_t which, const void* src, int64_t b
                       void* stream_)
 {
     if (!st || !src) return fail(GEFEN_EINVAL, "NULL argument");
-    if (which == 5 || which == 6) return fail(GEFEN_EINVAL, "array %d is read-only", which);
+    if (which >= 5) return fail(GEFEN_EINVAL, "array %d is read-only", which);
     void* dst;
     int64_t need;
     int rc = state_array(st, which, &dst, &need);

@@ -90,6 +90,35 @@ struct CodebookDev {
     int32_t ng;
 };
 
+// Histogram bin (Alg. 3) of gradient g in a block whose largest |g| is a > 0: the bin of
+// x = g / a among nbins equal bins of [-1, 1], the last one closed; half_nb = nbins / 2.
+// The defining evaluation is in float64, b = trunc((g / a + 1) * half_nb) (these sources
+// are built with contraction off). Most elements take a float32 estimate instead,
+// t = fma(g * rcp(a), h, h) with h = half_nb: the reciprocal is within 1 ulp and each of
+// the two products rounds once, so |t - (g / a + 1) h| <= 2^-21.4 h, and float64 is within
+// 2^-50 h. When t lies more than 2^-18 h from every integer (eight times the bound), the
+// exact value and the float64 one share t's integer part, so the estimate's floor is
+// the bin; otherwise (about 2^-17 h of all elements: 1.6 % at h = 2048), and for tiny
+// or non-finite inputs, the float64 evaluation decides. Both histogram paths (the
+// histogram kernel and the step kernels that take the histogram on the way) call this.
+__device__ __forceinline__ int hist_bin(float g, float a, double half_nb, int nbins)
+{
+    const float h = static_cast<float>(half_nb);
+    if (a >= 0x1p-100f && a <= 0x1p100f) {
+        const float t = fmaf(g * __builtin_amdgcn_rcpf(a), h, h);
+        const float fl = floorf(t);
+        const float fr = t - fl;   // exact: t < 2^24
+        const float d = h * 0x1p-18f;
+        if (fr > d && fr < 1.0f - d) {
+            const int b = static_cast<int>(fl);
+            return b < nbins - 1 ? b : nbins - 1;
+        }
+    }
+    const double x = static_cast<double>(g) / static_cast<double>(a);
+    const int b = static_cast<int>((x + 1.0) * half_nb);
+    return b < nbins - 1 ? b : nbins - 1;
+}
+
 // Launchers (all enqueue on `stream` and return the launch status).
 // `bs` is the KIND_U workgroup size (256, 512 or 1024); other kinds use kThreads.
 // `code_bits` is 8 (one code per byte) or 4 (two codes per byte, low nibble first);
@@ -104,6 +133,14 @@ hipError_t launch_step_h(int gdtype, int code_bits, const Tile* tiles, const HTi
                          int64_t n_tiles, const Seg* segs, uint8_t* codes, float* scale,
                          float* vmom, CodebookDev cb, StepScalars sc, float2* partials,
                          float2* ws_old, hipStream_t stream);
+
+// The KIND_G step of launch_step that also adds every element of its blocks to `hist`
+// (uint64[nbins], accumulated into; Alg. 3 on this step's gradients). Persistent
+// workgroups, each flushing one LDS histogram at its end.
+hipError_t launch_step_g_hist(int gdtype, int code_bits, const Tile* tiles, int64_t n_tiles,
+                              const Seg* segs, uint8_t* codes, float* scale, float* vmom,
+                              CodebookDev cb, StepScalars sc, uint64_t* hist, int32_t nbins,
+                              hipStream_t stream);
 
 // Histogram over all tiles. KIND_H tiles need their block absmax first:
 // launch_hist_h_absmax over each KIND_H class range writes am_partials[first + chunk].

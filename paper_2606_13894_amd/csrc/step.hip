@@ -409,11 +409,12 @@ __global__ __launch_bounds__(BS) void k_step_u(const Tile* __restrict__ tiles,
 // chunk). The reduce pass uses ordinary loads so that the update pass finds gradient and
 // code lines in cache. Both passes evaluate the momentum with the same operations, so
 // they agree bit for bit.
-template <int GDT, int BS, int CB, int UNR = 2>
+// HG: also the block's max |g| into *ag (for the histogram).
+template <int GDT, int BS, int CB, int UNR = 2, bool HG = false>
 __device__ __forceinline__ void pass_reduce(const LdsTables& L, const Seg& sg,
                                             const uint8_t* __restrict__ codes, const Span& sp,
                                             float s_old, const StepScalars& sc, float& ss,
-                                            float& am)
+                                            float& am, float* ag = nullptr)
 {
     const int tid = threadIdx.x;
     const int64_t cj = sg.code_off;
@@ -440,6 +441,7 @@ __device__ __forceinline__ void pass_reduce(const LdsTables& L, const Seg& sg,
                                     : 0.0f;
                 ss = fmaf(g[u][c], g[u][c], ss);
                 am = fmaxf(am, fabsf(mm));
+                if constexpr (HG) *ag = fmaxf(*ag, fabsf(g[u][c]));
             }
         }
     }
@@ -449,14 +451,19 @@ __device__ __forceinline__ void pass_reduce(const LdsTables& L, const Seg& sg,
         const float mm = momentum(L, code_ld<CB>(codes, cj + e), s_old, g, sc);
         ss = fmaf(g, g, ss);
         am = fmaxf(am, fabsf(mm));
+        if constexpr (HG) *ag = fmaxf(*ag, fabsf(g));
     }
 }
 
-template <int GDT, int BS, int CB, int UNR = 2>
+// HG: also adds every element to the LDS histogram hl (block max |g| = ag; a block with
+// ag = 0 adds nothing).
+template <int GDT, int BS, int CB, int UNR = 2, bool HG = false>
 __device__ __forceinline__ void pass_update(const LdsTables& L, const Seg& sg,
                                             uint8_t* __restrict__ codes, const Span& sp,
                                             float s_old, const BlockOut& bo,
-                                            const StepScalars& sc, float half_ng, int ng_m1)
+                                            const StepScalars& sc, float half_ng, int ng_m1,
+                                            uint32_t* hl = nullptr, float ag = 0.0f,
+                                            double half_nb = 0.0, int nbins = 0)
 {
     const int tid = threadIdx.x;
     float* __restrict__ th = sg.theta;
@@ -487,6 +494,8 @@ __device__ __forceinline__ void pass_update(const LdsTables& L, const Seg& sg,
                     const int q = bo.s_new > 0.0f ? encode(L, mm * bo.inv_s, half_ng, ng_m1) : 0;
                     packed |= static_cast<uint32_t>(q) << (CB * c);
                     out[c] = fmaf(-bo.r, mm, tv[c] * sc.decay);
+                    if constexpr (HG)
+                        if (ag > 0.0f) atomicAdd(&hl[hist_bin(g[u][c], ag, half_nb, nbins)], 1u);
                 }
                 const f32x4 o4 = {out[0], out[1], out[2], out[3]};
                 __builtin_nontemporal_store(o4, glw<f32x4>(th) + v);
@@ -502,27 +511,34 @@ __device__ __forceinline__ void pass_update(const LdsTables& L, const Seg& sg,
         const int q = bo.s_new > 0.0f ? encode(L, mm * bo.inv_s, half_ng, ng_m1) : 0;
         th[e] = fmaf(-bo.r, mm, th[e] * sc.decay);
         code_st<CB>(codes, cj + e, q0, q);
+        if constexpr (HG)
+            if (ag > 0.0f) atomicAdd(&hl[hist_bin(g, ag, half_nb, nbins)], 1u);
     }
 }
 
-template <int BS>
-__device__ __forceinline__ void wg_reduce(float& ss, float& am, LdsTables& L)
+// HG: *ag (max |g|) is reduced too.
+template <int BS, bool HG = false>
+__device__ __forceinline__ void wg_reduce(float& ss, float& am, LdsTables& L, float* ag = nullptr)
 {
     for (int off = 1; off < 64; off <<= 1) {
         ss += __shfl_xor(ss, off);
         am = fmaxf(am, __shfl_xor(am, off));
+        if constexpr (HG) *ag = fmaxf(*ag, __shfl_xor(*ag, off));
     }
     const int wave = threadIdx.x >> 6;
     if ((threadIdx.x & 63) == 0) {
         L.red_ss[wave] = ss;
         L.red_am[wave] = am;
+        if constexpr (HG) L.red_ag[wave] = *ag;
     }
     __syncthreads();
     ss = L.red_ss[0];
     am = L.red_am[0];
+    if constexpr (HG) *ag = L.red_ag[0];
     for (int w = 1; w < BS / 64; ++w) {
         ss += L.red_ss[w];
         am = fmaxf(am, L.red_am[w]);
+        if constexpr (HG) *ag = fmaxf(*ag, L.red_ag[w]);
     }
     __syncthreads();
 }
@@ -534,18 +550,24 @@ __device__ __forceinline__ void wg_reduce(float& ss, float& am, LdsTables& L)
 // it keeps one partial (sum g^2, max |m|) for the block of its first element and one
 // for the next; one wave per block then reduces them in a fixed order. Edge vectors
 // (shared with neighbouring tiles) are loaded and stored element by element.
-struct RunLds {
+// HG (the step that also takes the histogram): the partials carry max |g| of both blocks
+// as well, and every element goes into the LDS histogram hl at the end.
+template <bool HG>
+struct RunLdsT {
     int64_t start[kRunMaxBlocks + 1];   // tensor-relative block starts; start[nblk] = end
     float s_old[kRunMaxBlocks], v_old[kRunMaxBlocks];
     float s_new[kRunMaxBlocks], r[kRunMaxBlocks], inv_s[kRunMaxBlocks];
-    float part[kRunMaxVec][4];
+    float ag[HG ? kRunMaxBlocks : 1];
+    float part[kRunMaxVec][HG ? 6 : 4];
 };
 
-template <int GDT>
-__device__ __forceinline__ void run_tile(LdsTables& L, RunLds& R, const Tile& tl, const Seg& sg,
-                                         uint8_t* __restrict__ codes, float* __restrict__ scale,
-                                         float* __restrict__ vmom, const CodebookDev& cbd,
-                                         const StepScalars& sc)
+template <int GDT, bool HG = false>
+__device__ __forceinline__ void run_tile(LdsTables& L, RunLdsT<HG>& R, const Tile& tl,
+                                         const Seg& sg, uint8_t* __restrict__ codes,
+                                         float* __restrict__ scale, float* __restrict__ vmom,
+                                         const CodebookDev& cbd, const StepScalars& sc,
+                                         uint32_t* hl = nullptr, double half_nb = 0.0,
+                                         int nbins = 0)
 {
     const int tid = threadIdx.x;
     const int64_t e_lo = tl.elem0, e_hi = tl.elem0 + tl.nelem;
@@ -593,10 +615,15 @@ __device__ __forceinline__ void run_tile(LdsTables& L, RunLds& R, const Tile& tl
     load_tables(L, cbd);
     __syncthreads();
     int kb[kRunVpl];
+    float gk[HG ? kRunVpl : 1][4];   // the gradients (gv becomes the momentum)
 #pragma unroll
     for (int j = 0; j < kRunVpl; ++j) {
         const int i = tid + j * kThreads;
         kb[j] = 0;
+        if constexpr (HG) {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) gk[j][c] = gv[j][c];
+        }
         if (i < nvec) {
             const int64_t e = 4 * (va + i);
             const int64_t first = e > e_lo ? e : e_lo;
@@ -607,7 +634,7 @@ __device__ __forceinline__ void run_tile(LdsTables& L, RunLds& R, const Tile& tl
             }
             kb[j] = lo;
             const int64_t next = R.start[lo + 1];
-            float ssa = 0.0f, ama = 0.0f, ssb = 0.0f, amb = 0.0f;
+            float ssa = 0.0f, ama = 0.0f, ssb = 0.0f, amb = 0.0f, aga = 0.0f, agb = 0.0f;
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
                 const int64_t x = e + c;
@@ -620,9 +647,11 @@ __device__ __forceinline__ void run_tile(LdsTables& L, RunLds& R, const Tile& tl
                     if (second) {
                         ssb = fmaf(g, g, ssb);
                         amb = fmaxf(amb, fabsf(m));
+                        agb = fmaxf(agb, fabsf(g));
                     } else {
                         ssa = fmaf(g, g, ssa);
                         ama = fmaxf(ama, fabsf(m));
+                        aga = fmaxf(aga, fabsf(g));
                     }
                 }
             }
@@ -630,6 +659,10 @@ __device__ __forceinline__ void run_tile(LdsTables& L, RunLds& R, const Tile& tl
             R.part[i][1] = ama;
             R.part[i][2] = ssb;
             R.part[i][3] = amb;
+            if constexpr (HG) {
+                R.part[i][4] = aga;
+                R.part[i][5] = agb;
+            }
         }
     }
     __syncthreads();
@@ -638,18 +671,21 @@ __device__ __forceinline__ void run_tile(LdsTables& L, RunLds& R, const Tile& tl
         const int64_t bs = R.start[k], be = R.start[k + 1];
         const int i0 = static_cast<int>((bs >> 2) - va);
         const int i1 = static_cast<int>(((be - 1) >> 2) - va);
-        float ss = 0.0f, am = 0.0f;
+        float ss = 0.0f, am = 0.0f, ag = 0.0f;
         for (int i = i0 + lane; i <= i1; i += 64) {
             const int64_t e = 4 * (va + i);
             const bool own_first = (e > e_lo ? e : e_lo) >= bs;
             ss += own_first ? R.part[i][0] : R.part[i][2];
             am = fmaxf(am, own_first ? R.part[i][1] : R.part[i][3]);
+            if constexpr (HG) ag = fmaxf(ag, own_first ? R.part[i][4] : R.part[i][5]);
         }
         for (int off = 1; off < 64; off <<= 1) {
             ss += __shfl_xor(ss, off);
             am = fmaxf(am, __shfl_xor(am, off));
+            if constexpr (HG) ag = fmaxf(ag, __shfl_xor(ag, off));
         }
         if (lane == 0) {
+            if constexpr (HG) R.ag[k] = ag;
             const BlockOut bo = finish_block(ss, am, R.v_old[k], static_cast<float>(be - bs), sc);
             scale[tl.blk0 + k] = bo.s_new;
             vmom[tl.blk0 + k] = bo.v_new;
@@ -679,6 +715,11 @@ __device__ __forceinline__ void run_tile(LdsTables& L, RunLds& R, const Tile& tl
             const int q = R.s_new[kk] > 0.0f ? encode(L, m * R.inv_s[kk], half_ng, ng_m1) : 0;
             packed |= static_cast<uint32_t>(q) << (8 * c);
             out[c] = fmaf(-R.r[kk], m, tv[j][c] * sc.decay);
+            if constexpr (HG) {
+                const int64_t x = e + c;
+                if (x >= e_lo && x < e_hi && R.ag[k] > 0.0f)
+                    atomicAdd(&hl[hist_bin(gk[j][c], R.ag[k], half_nb, nbins)], 1u);
+            }
         }
         if (aligned && e >= e_lo && e + 4 <= e_hi) {
             const f32x4 o4 = {out[0], out[1], out[2], out[3]};
@@ -699,38 +740,62 @@ __device__ __forceinline__ void run_tile(LdsTables& L, RunLds& R, const Tile& tl
 
 // KIND_G: one block per workgroup, any size and alignment: reduce pass, update pass;
 // or a register run of short explicit blocks (tile.vpl == 1, 8-bit codes).
-template <int GDT, int CB>
+// HIST: the step that also takes the histogram of this step's gradients (Alg. 3): a
+// persistent grid walks the tiles (tile blockIdx.x, + gridDim.x, ...), every element goes
+// into an LDS histogram once its block's max |g| is known, and each workgroup adds its
+// histogram to `hist` at the end (integer atomics: the sum does not depend on the order).
+template <int GDT, int CB, bool HIST = false>
 __global__ __launch_bounds__(kThreads) void k_step_g(const Tile* __restrict__ tiles,
                                                      const Seg* __restrict__ segs,
                                                      uint8_t* __restrict__ codes,
                                                      float* __restrict__ scale,
                                                      float* __restrict__ vmom, CodebookDev cbd,
-                                                     StepScalars sc)
+                                                     StepScalars sc, int64_t n_tiles,
+                                                     uint64_t* __restrict__ hist, int32_t nbins)
 {
     __shared__ LdsTables L;
-    __shared__ RunLds R;
-    const Tile tl = tiles[blockIdx.x];
-    const Seg sg = segs[tl.seg];
-    if (CB == 8 && tl.vpl == 1) {   // a register run (8-bit codes only)
-        run_tile<GDT>(L, R, tl, sg, codes, scale, vmom, cbd, sc);
-        return;
+    __shared__ RunLdsT<HIST> R;
+    __shared__ uint32_t H[HIST ? 16 * kMaxK : 1];
+    const double half_nb = 0.5 * static_cast<double>(nbins);
+    auto one = [&](const Tile& tl) {
+        const Seg sg = segs[tl.seg];
+        if (CB == 8 && tl.vpl == 1) {   // a register run (8-bit codes only)
+            run_tile<GDT, HIST>(L, R, tl, sg, codes, scale, vmom, cbd, sc, H, half_nb, nbins);
+            return;
+        }
+        const int64_t blk = tl.blk0;
+        const Span sp = make_span<GDT>(sg, tl.elem0, tl.nelem);
+        const float s_old = scale[blk];
+        const float v_old = vmom[blk];
+        load_tables(L, cbd);
+        __syncthreads();
+        float ss = 0.0f, am = 0.0f, ag = 0.0f;
+        pass_reduce<GDT, kThreads, CB, 2, HIST>(L, sg, codes, sp, s_old, sc, ss, am, &ag);
+        wg_reduce<kThreads, HIST>(ss, am, L, &ag);
+        const BlockOut bo = finish_block(ss, am, v_old, static_cast<float>(tl.nelem), sc);
+        if (threadIdx.x == 0) {
+            scale[blk] = bo.s_new;
+            vmom[blk] = bo.v_new;
+        }
+        pass_update<GDT, kThreads, CB, 2, HIST>(L, sg, codes, sp, s_old, bo, sc,
+                                                0.5f * static_cast<float>(cbd.ng), cbd.ng - 1,
+                                                H, ag, half_nb, nbins);
+    };
+    if constexpr (!HIST) {
+        one(tiles[blockIdx.x]);
+    } else {
+        for (int i = threadIdx.x; i < nbins; i += kThreads) H[i] = 0;
+        __syncthreads();
+        for (int64_t t = blockIdx.x; t < n_tiles; t += gridDim.x) {
+            one(tiles[t]);
+            __syncthreads();   // the next tile reuses the LDS
+        }
+        for (int i = threadIdx.x; i < nbins; i += kThreads) {
+            const uint32_t c = H[i];
+            if (c) atomicAdd(reinterpret_cast<unsigned long long*>(&hist[i]),
+                             static_cast<unsigned long long>(c));
+        }
     }
-    const int64_t blk = tl.blk0;
-    const Span sp = make_span<GDT>(sg, tl.elem0, tl.nelem);
-    const float s_old = scale[blk];
-    const float v_old = vmom[blk];
-    load_tables(L, cbd);
-    __syncthreads();
-    float ss = 0.0f, am = 0.0f;
-    pass_reduce<GDT, kThreads, CB>(L, sg, codes, sp, s_old, sc, ss, am);
-    wg_reduce<kThreads>(ss, am, L);
-    const BlockOut bo = finish_block(ss, am, v_old, static_cast<float>(tl.nelem), sc);
-    if (threadIdx.x == 0) {
-        scale[blk] = bo.s_new;
-        vmom[blk] = bo.v_new;
-    }
-    pass_update<GDT, kThreads, CB>(L, sg, codes, sp, s_old, bo, sc,
-                                   0.5f * static_cast<float>(cbd.ng), cbd.ng - 1);
 }
 
 // ---------------------------------------------------------------------------------
@@ -907,7 +972,8 @@ hipError_t launch_kind(int kind, int vpl, int bs, dim3 grid, const Tile* tiles,
         return launch_u<GDT, CB>(vpl, bs, grid, tiles, segs, codes, scale, vmom, cb, sc, stream);
     case KIND_G:
         hipLaunchKernelGGL((k_step_g<GDT, CB>), grid, dim3(kThreads), 0, stream, tiles, segs,
-                           codes, scale, vmom, cb, sc);
+                           codes, scale, vmom, cb, sc, int64_t(grid.x),
+                           static_cast<uint64_t*>(nullptr), 0);
         return hipGetLastError();
     case KIND_L:
         hipLaunchKernelGGL((k_step_l<GDT, CB>), grid, dim3(kThreads), 0, stream, tiles, segs,
@@ -941,6 +1007,41 @@ hipError_t launch_step_h(int gdtype, int code_bits, const Tile* tiles, const HTi
                    : launch_h<DT_BF16, 4>(grid, tiles, htiles, segs, codes, scale, vmom, cb, sc,
                                           partials, ws_old, stream);
     return hipErrorInvalidValue;
+}
+
+hipError_t launch_step_g_hist(int gdtype, int code_bits, const Tile* tiles, int64_t n_tiles,
+                              const Seg* segs, uint8_t* codes, float* scale, float* vmom,
+                              CodebookDev cb, StepScalars sc, uint64_t* hist, int32_t nbins,
+                              hipStream_t stream)
+{
+    if (n_tiles <= 0) return hipSuccess;
+    if (nbins < 1 || nbins > 16 * kMaxK || (code_bits != 8 && code_bits != 4))
+        return hipErrorInvalidValue;
+    // as many workgroups as are resident at once (each adds its 16 k bins at its end)
+#define GEFEN_GH(G, C)                                                                        \
+    do {                                                                                      \
+        static int resident = 0;                                                              \
+        if (resident == 0) {                                                                  \
+            int per_cu = 0, dev = 0, cus = 0;                                                 \
+            if (hipOccupancyMaxActiveBlocksPerMultiprocessor(                                 \
+                    &per_cu, k_step_g<G, C, true>, kThreads, 0) != hipSuccess ||              \
+                hipGetDevice(&dev) != hipSuccess ||                                           \
+                hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=    \
+                    hipSuccess)                                                               \
+                return hipErrorInvalidValue;                                                  \
+            resident = std::max(1, per_cu) * std::max(1, cus);                                \
+        }                                                                                     \
+        const dim3 grid(static_cast<unsigned>(std::min<int64_t>(n_tiles, resident)));         \
+        hipLaunchKernelGGL((k_step_g<G, C, true>), grid, dim3(kThreads), 0, stream, tiles,    \
+                           segs, codes, scale, vmom, cb, sc, n_tiles, hist, nbins);           \
+    } while (0)
+    if (code_bits == 8) {
+        if (gdtype == DT_F32) GEFEN_GH(DT_F32, 8); else GEFEN_GH(DT_BF16, 8);
+    } else {
+        if (gdtype == DT_F32) GEFEN_GH(DT_F32, 4); else GEFEN_GH(DT_BF16, 4);
+    }
+#undef GEFEN_GH
+    return hipGetLastError();
 }
 
 hipError_t launch_step(int kind, int gdtype, int code_bits, int vpl, int bs, const Tile* tiles,

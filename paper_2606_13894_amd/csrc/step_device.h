@@ -33,6 +33,7 @@ struct LdsTables {
     uint8_t guide[16 * kMaxK + 16];   // ng + 1 bytes (padded)
     float red_ss[kMaxThreads / 64];
     float red_am[kMaxThreads / 64];
+    float red_ag[kMaxThreads / 64];   // max |g| (the step that also takes the histogram)
 };
 
 template <int BS = kThreads>

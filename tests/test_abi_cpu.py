@@ -74,6 +74,8 @@ def test_step_and_queries_reject_null_state(lib):
     t = _tensor()
     assert lib.gefen_step(None, t, t, 1, 1e-3, 0.9, 0.999, 1e-8, 0.0, 1, None) == -1
     assert b"state" in lib.gefen_last_error()
+    assert lib.gefen_step_fit(None, t, t, 1, 1e-3, 0.9, 0.999, 1e-8, 0.0, 1, None) == -1
+    assert b"state" in lib.gefen_last_error()
     assert lib.gefen_fit_codebook(None, t, 1, None) == -1
     assert lib.gefen_get_periods(None, None) == -1
     n = ctypes.c_int64()

@@ -7,9 +7,10 @@
   and last two blocks of every tensor plus a seeded random 0.2 %).
 * ``stress_4b``: 4e9 elements (int64 indexing) in 1e6 explicit blocks, sampled as
   follows: a seeded random 1 % of blocks, every block under 128 elements, the first and
-  last 100 blocks and the 100 largest; two steps, a codebook refit (histogram checked
-  exactly, DP codebook bit-identical), and the step after the refit (decode with the
-  old codebook, encode with the new one). The other reading of its block sizes
+  last 100 blocks and the 100 largest; two steps, the second refitting the codebook on
+  its gradients inside the step (gefen_step_fit: the histogram the step kernels take is
+  checked exactly, as is the histogram kernel's, and the DP codebook bit-identical), and
+  the step after the refit (decode with the old codebook, encode with the new one). The other reading of its block sizes
   (log-uniform sizes drawn until 4e9 is covered) is checked the same way over two steps.
 
 Blocks are independent in the step, so a sample checks its blocks completely.
@@ -103,10 +104,10 @@ class Sampled:
                 ref[key].append(val)
         return ref
 
-    def step(self, grads, lr, betas, eps, wd, t, where):
+    def step(self, grads, lr, betas, eps, wd, t, where, fit=False):
         pre = self.snapshot()
         gs = self.grads_sample(grads)
-        self.st.step(self.params, grads, lr, betas, eps, wd, t)
+        self.st.step(self.params, grads, lr, betas, eps, wd, t, fit=fit)
         post = self.snapshot()
         ref = self.oracle(pre, gs, lr, betas, eps, wd, t)
         shim = type("S", (), {})()
@@ -205,9 +206,12 @@ def test_stress_4b_sampled_with_refit():
     del g1
     _free()
     g2 = W.make_grads(w, W.scale_fields(w), 2, dev, block_scales=bsc, offsets=offs)
-    smp.step(g2, *hp, 2, where="stress t=2")
-    # refit on g2: histogram exactly, DP codebook bit-identical (sampled histogram is not
-    # enough for the DP, so the oracle histogram is built over all blocks in chunks)
+    # step 2 refits on g2 inside the step (gefen_step_fit): the histogram the step kernels
+    # took equals the oracle's exactly, and so does the standalone histogram kernel's; the
+    # DP codebook is bit-identical (a sampled histogram is not enough for the DP, so the
+    # oracle histogram is built over all blocks in chunks)
+    smp.step(g2, *hp, 2, where="stress t=2 (refit inside the step)", fit=True)
+    h_fit = st.read(gf.STATE_HIST).cpu().numpy().view(np.uint64)
     h_gpu = st.histogram(g2).cpu().numpy().view(np.uint64)
     h_ref = np.zeros(16 * 256, dtype=np.uint64)
     chunk_blocks = 50_000
@@ -216,8 +220,8 @@ def test_stress_4b_sampled_with_refit():
         e0, e1 = int(offs[b0]), int(offs[b1])
         gb = grad_bits(g2[0][e0:e1])
         oracle.histogram_blocks(gb, offs[b0:b1 + 1] - e0, 16 * 256, h_ref)
+    np.testing.assert_array_equal(h_fit, h_ref)
     np.testing.assert_array_equal(h_gpu, h_ref)
-    st.fit_codebook(g2)
     cb_ref, _, _, _ = oracle.dp_codebook(h_ref, 256)
     torch.cuda.synchronize()
     enc = st.read(gf.STATE_CB_ENC).cpu().numpy()
