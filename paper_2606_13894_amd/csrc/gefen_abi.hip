@@ -5,7 +5,6 @@
 #include "gefen_internal.h"
 #include "muon_internal.h"
 #include "measure_internal.h"
-#include "run_internal.h"
 
 #include <algorithm>
 #include <cstdlib>
@@ -42,16 +41,9 @@ int fail(int code, const char* fmt, ...)
             return fail(GEFEN_EHIP, "%s failed: %s", #call, hipGetErrorString(e_));      \
     } while (0)
 
-struct Class {
-    int32_t kind, gdtype, vpl, bs;
-    int64_t first, count;
-    int64_t elems, bytes;   // per launch: elements and algorithmic HBM bytes
-};
+using Class = PlanClass;
 
-constexpr int64_t kUMaxPeriod = 8192;          // longest period held in registers (KIND_U)
-constexpr int64_t kHugeBlock = 65536;         // longer blocks are always split (KIND_H)
 constexpr int kSegSlots = 4;                 // device tensor tables cached per state
-constexpr int64_t kMinStreamedBlocks = 4096;  // fewer blocks > kUMaxPeriod: split them too
 constexpr int64_t kPartChunk = 65536;     // elements of one partition sub-chunk (mode 1)
 constexpr int64_t kPartItemElems = 16384; // elements per partition item (mode 0)
 constexpr int kPartMaxPairs = 2048;
@@ -308,393 +300,43 @@ hipError_t fill_zero(void* p, size_t bytes, hipStream_t s)
     return hipGetLastError();
 }
 
-// KIND_U shape for period p (p % 4 == 0, p <= kUMaxPeriod): vectors per lane v and a
-// power-of-two lane group per block leaving at most 1/8 of the lanes idle, in a
-// workgroup of `threads` lanes (threads / lanes blocks per workgroup). Measured on the
-// MI355X for the Llama-3 1.5B shape (p = 2048 and 8192, bf16 gradients): 1024 threads
-// with v = 2 (about 8K elements per workgroup) reach 5.76 TB/s; v = 1 (4K elements)
-// 4.82 TB/s, v = 4 (16K elements) 4.11 TB/s, 512 threads 4.55 TB/s, 256 threads
-// 4.38 TB/s -- the per-workgroup start (descriptor loads, LDS tables, barrier) needs
-// ~8K elements to amortise, while larger tiles lose memory-level parallelism. So v = 2
-// is tried first, then 1, 3, 4; 256-thread workgroups (up to 8 vectors) are the
-// fallback.
-struct UShape {
-    int lpb_log2, vpl, bs;
-};
-
-UShape choose_u(int64_t p)
+// Plan the tiles (tile_plan.h), check the plan against the kernels' assumptions and
+// upload the tables. starts[t]: tensor t's explicit block starts (n_blocks + 1).
+int plan_tiles(gefen_state* st, const std::vector<std::vector<int64_t>>& starts)
 {
-    const int64_t nv = p / 4;
-    constexpr int pref = 1024;
-    constexpr int kMaxVplBig = 4;   // instances of the 512/1024-thread kernels
-    static const int kOrderBig[kMaxVplBig] = {2, 1, 3, 4};
-    static const int kOrderSmall[kMaxVpl] = {2, 1, 3, 4, 5, 6, 7, 8};
-    for (int pass = 0; pass < 2; ++pass) {
-        const int bs = pass == 0 ? pref : 256;
-        const int vmax = bs > 256 ? kMaxVplBig : kMaxVpl;
-        for (int vi = 0; vi < vmax; ++vi) {
-            const int v = bs > 256 ? kOrderBig[vi] : kOrderSmall[vi];
-            const int64_t need = (nv + v - 1) / v;
-            int l2 = 0;
-            while ((int64_t(1) << l2) < need) ++l2;
-            if ((1 << l2) > bs) continue;
-            const int64_t waste = (int64_t(1) << l2) * v - nv;
-            if (8 * waste <= nv || v == vmax || (pass == 1 && v == kMaxVpl))
-                return UShape{l2, v, bs};
-        }
-    }
-    // not reached for p <= 8192: 256 lanes x 8 vectors x 4 = 8192
-    return UShape{8, kMaxVpl, 256};
-}
-
-// Tiles per kernel class while planning: one list per class key, with the split-block
-// bookkeeping and the kind of every tile (the histogram's view of it) kept parallel.
-struct TilePlan {
-    struct Key {
-        int32_t kind, gdtype, vpl, bs;
-    };
-    std::vector<Key> keys;
-    std::vector<std::vector<Tile>> lists;
-    std::vector<std::vector<HTile>> hlists;
-    std::vector<std::vector<int32_t>> kinds;
-
-    size_t index(int32_t kind, int32_t gdt, int32_t vpl, int32_t bs = kThreads)
-    {
-        for (size_t i = 0; i < keys.size(); ++i)
-            if (keys[i].kind == kind && keys[i].gdtype == gdt && keys[i].vpl == vpl &&
-                keys[i].bs == bs)
-                return i;
-        keys.push_back({kind, gdt, vpl, bs});
-        lists.emplace_back();
-        hlists.emplace_back();
-        kinds.emplace_back();
-        return keys.size() - 1;
-    }
-    void add(size_t i, const Tile& tl)
-    {
-        lists[i].push_back(tl);
-        kinds[i].push_back(keys[i].kind);
-    }
-    int64_t elems(size_t i) const
-    {
-        int64_t e = 0;
-        for (const Tile& tl : lists[i]) e += tl.nelem;
-        return e;
-    }
-};
-
-// Register-resident shapes: each eligible tensor's own best shape, then every tensor
-// that fits the dominant shape's kernel (its vectors per lane and workgroup size; the
-// kernel masks vectors past a block's end and reads lanes-per-block from the tile) is
-// re-planned onto it, so one launch covers them on the fast path. lpb_log2 < 0: not
-// register-resident.
-std::vector<UShape> plan_u_shapes(const gefen_state* st)
-{
-    std::vector<UShape> ushape(st->n_tensors, UShape{-1, 0, 0});
-    std::vector<std::pair<std::pair<int, int>, int64_t>> tally;
-    for (int32_t t = 0; t < st->n_tensors; ++t) {
-        const int64_t p = st->period[t];
-        if (st->explicit_blocks || p % 4 != 0 || p > kUMaxPeriod) continue;
-        ushape[t] = choose_u(p);
-        const std::pair<int, int> key{ushape[t].vpl, ushape[t].bs};
-        bool found = false;
-        for (auto& e : tally)
-            if (e.first == key) {
-                e.second += st->numel[t];
-                found = true;
-            }
-        if (!found) tally.push_back({key, st->numel[t]});
-    }
-    int dom_vpl = 0, dom_bs = 0;
-    int64_t best = -1;
-    for (auto& e : tally)
-        if (e.second > best) {
-            best = e.second;
-            dom_vpl = e.first.first;
-            dom_bs = e.first.second;
-        }
-    if (best >= 0) {
-        for (int32_t t = 0; t < st->n_tensors; ++t) {
-            if (ushape[t].lpb_log2 < 0) continue;
-            if (ushape[t].vpl == dom_vpl && ushape[t].bs == dom_bs) continue;
-            const int64_t nv = st->period[t] / 4;
-            const int64_t need = (nv + dom_vpl - 1) / dom_vpl;
-            int l2 = 0;
-            while ((int64_t(1) << l2) < need) ++l2;
-            if ((1 << l2) <= dom_bs) ushape[t] = UShape{l2, dom_vpl, dom_bs};
-        }
-    }
-    return ushape;
-}
-
-// A huge block as chunk tiles (KIND_H); the chunk bookkeeping is made absolute when
-// the classes are concatenated.
-void plan_huge(gefen_state* st, TilePlan& P, int32_t t, int32_t gdt, int64_t start,
-               int64_t len, int64_t blk)
-{
-    const size_t li = P.index(KIND_H, gdt, 0);
-    const int64_t nchunk = (len + kHChunk - 1) / kHChunk;
-    const int64_t first_rel = static_cast<int64_t>(P.lists[li].size());
-    for (int64_t c = 0; c < nchunk; ++c) {
-        Tile tl{};
-        tl.elem0 = start + c * kHChunk;
-        tl.blk0 = blk;
-        tl.nelem = std::min(kHChunk, len - c * kHChunk);
-        tl.seg = t;
-        tl.nblk = 1;
-        P.add(li, tl);
-        HTile ht{};
-        ht.blk_len = len;
-        ht.first = first_rel;
-        ht.nchunk = static_cast<int32_t>(nchunk);
-        ht.chunk = static_cast<int32_t>(c);
-        ht.hb = static_cast<int32_t>(st->n_hblocks);
-        P.hlists[li].push_back(ht);
-    }
-    ++st->n_hblocks;
-}
-
-// One block per workgroup (KIND_G).
-void plan_single(TilePlan& P, int32_t t, int32_t gdt, int64_t start, int64_t len, int64_t blk)
-{
-    Tile tl{};
-    tl.elem0 = start;
-    tl.blk0 = blk;
-    tl.nelem = len;
-    tl.seg = t;
-    tl.nblk = 1;
-    P.add(P.index(KIND_G, gdt, 0), tl);
-}
-
-// The tiles of tensor t: explicit blocks by their length; uniform blocks by the period
-// (registers, lane per block, split, or streamed).
-void plan_tensor(gefen_state* st, TilePlan& P, int32_t t, const UShape& u,
-                 const std::vector<int64_t>& s)
-{
-    const int32_t gdt = st->gdtype[t];
-    const int64_t bb = st->blk_begin[t];
-    if (st->explicit_blocks) {
-        const int64_t nb = static_cast<int64_t>(s.size()) - 1;
-        auto run_block = [](int64_t len) { return len >= kRunMinBlock && len <= kRunMaxElems; };
-        int64_t b = 0;
-        while (b < nb) {
-            const int64_t len = s[b + 1] - s[b];
-            if (st->code_bits == 8 && run_block(len)) {
-                // consecutive short blocks held in registers by one KIND_G workgroup
-                const int64_t b0 = b;
-                int cnt = 0;
-                while (b < nb && cnt < kRunMaxBlocks && run_block(s[b + 1] - s[b]) &&
-                       s[b + 1] - s[b0] <= kRunMaxElems) {
-                    ++cnt;
-                    ++b;
-                }
-                Tile tl{};
-                tl.elem0 = s[b0];
-                tl.blk0 = bb + b0;
-                tl.nelem = s[b] - s[b0];
-                tl.seg = t;
-                tl.nblk = static_cast<int16_t>(cnt);
-                tl.vpl = 1;
-                P.add(P.index(KIND_G, gdt, 0), tl);
-            } else if (len > kHugeBlock) {
-                plan_huge(st, P, t, gdt, s[b], len, bb + b);
-                ++b;
-            } else if (len <= kSmallBlock) {
-                Tile tl{};
-                tl.elem0 = s[b];
-                tl.blk0 = bb + b;
-                tl.seg = t;
-                int n = 0;
-                while (b < nb && n < kThreads && s[b + 1] - s[b] <= kSmallBlock) {
-                    ++n;
-                    ++b;
-                }
-                tl.nblk = static_cast<int16_t>(n);
-                tl.nelem = s[b] - tl.elem0;
-                P.add(P.index(KIND_L, gdt, 0), tl);
-            } else {
-                plan_single(P, t, gdt, s[b], len, bb + b);
-                ++b;
-            }
-        }
-        return;
-    }
-    const int64_t p = st->period[t];
-    const int64_t nb = st->numel[t] / p;
-    if (u.lpb_log2 >= 0) {
-        const int64_t bpw = u.bs >> u.lpb_log2;
-        const size_t li = P.index(KIND_U, gdt, u.vpl, u.bs);
-        for (int64_t b = 0; b < nb; b += bpw) {
-            Tile tl{};
-            const int64_t n = std::min(bpw, nb - b);
-            tl.elem0 = b * p;
-            tl.blk0 = bb + b;
-            tl.nelem = n * p;
-            tl.seg = t;
-            tl.nblk = static_cast<int16_t>(n);
-            tl.vpl = static_cast<uint8_t>(u.vpl);
-            tl.lpb_log2 = static_cast<uint8_t>(u.lpb_log2);
-            P.add(li, tl);
-        }
-    } else if (p <= kSmallBlock) {
-        const size_t li = P.index(KIND_L, gdt, 0);
-        for (int64_t b = 0; b < nb; b += kThreads) {
-            Tile tl{};
-            const int64_t n = std::min<int64_t>(kThreads, nb - b);
-            tl.elem0 = b * p;
-            tl.blk0 = bb + b;
-            tl.nelem = n * p;
-            tl.seg = t;
-            tl.nblk = static_cast<int16_t>(n);
-            P.add(li, tl);
-        }
-    } else if (p > kHugeBlock || (p > kUMaxPeriod && nb < kMinStreamedBlocks)) {
-        for (int64_t b = 0; b < nb; ++b) plan_huge(st, P, t, gdt, b * p, p, bb + b);
-    } else {
-        for (int64_t b = 0; b < nb; ++b) plan_single(P, t, gdt, b * p, p, bb + b);
-    }
-}
-
-// Fold the small classes other than the largest register-resident one (and the split
-// huge-block classes, which need two kernels) into one generic launch (KIND_ANY,
-// tile.vpl = 0); a folded tile runs the slower generic path, so only small classes go.
-// The folded tiles keep their kinds for the histogram kernel.
-void fold_small_classes(const gefen_state* st, TilePlan& P)
-{
-    int dom = -1;
-    int64_t dom_elems = -1;
-    for (size_t i = 0; i < P.lists.size(); ++i) {
-        if (P.keys[i].kind != KIND_U) continue;
-        const int64_t e = P.elems(i);
-        if (e > dom_elems) {
-            dom_elems = e;
-            dom = static_cast<int>(i);
-        }
-    }
-    if (dom < 0) return;
-    const int64_t fold_max = std::max<int64_t>(int64_t(1) << 21, dom_elems / 64);
-    std::vector<Tile> front;
-    std::vector<int32_t> front_kinds;
-    int32_t any_dtype = -1;
-    for (size_t i = 0; i < P.lists.size(); ++i) {
-        if (static_cast<int>(i) == dom || P.keys[i].kind == KIND_H || P.lists[i].empty())
-            continue;
-        if (P.elems(i) > fold_max) continue;
-        // Uniform small-block tiles are cut to kThreads / lpb blocks, lpb = p rounded up
-        // to a power of two: the generic kernel gives each block a group of lpb lanes and
-        // covers such a tile in one pass.
-        for (size_t j = 0; j < P.lists[i].size(); ++j) {
-            Tile tl = P.lists[i][j];
-            const int32_t kd = P.kinds[i][j];
-            tl.vpl = 0;
-            tl.lpb_log2 = 0;
-            const int64_t p = st->explicit_blocks ? 0 : st->period[tl.seg];
-            if (kd == KIND_L && p > 0) {
-                int64_t lpb = 1;
-                while (lpb < p) lpb <<= 1;
-                const int64_t per = kThreads / lpb;
-                for (int64_t b = 0; b < tl.nblk; b += per) {
-                    Tile sub = tl;
-                    const int64_t nb = std::min<int64_t>(per, tl.nblk - b);
-                    sub.elem0 = tl.elem0 + b * p;
-                    sub.blk0 = tl.blk0 + b;
-                    sub.nblk = static_cast<int16_t>(nb);
-                    sub.nelem = nb * p;
-                    front.push_back(sub);
-                    front_kinds.push_back(kd);
-                }
-            } else {
-                front.push_back(tl);
-                front_kinds.push_back(kd);
-            }
-        }
-        any_dtype = P.keys[i].gdtype;
-        P.lists[i].clear();
-        P.kinds[i].clear();
-    }
-    if (front.empty()) return;
-    const size_t ai = P.index(KIND_ANY, any_dtype, 0);
-    P.lists[ai].insert(P.lists[ai].end(), front.begin(), front.end());
-    P.kinds[ai].insert(P.kinds[ai].end(), front_kinds.begin(), front_kinds.end());
-}
-
-// Concatenate the classes (the small generic class first: it is short and leaves the
-// machine to the long launches after it, which measured faster than running it beside
-// them on a second stream, whose fork and join cost more than it saves), record each
-// class's launch range and algorithmic bytes, and upload the tables.
-int upload_plan(gefen_state* st, TilePlan& P)
-{
-    std::vector<Tile> all;
-    std::vector<int32_t> kinds;
-    std::vector<HTile> hall;
-    st->classes.clear();
-    std::vector<size_t> order;
-    for (size_t i = 0; i < P.lists.size(); ++i)
-        if (P.keys[i].kind == KIND_ANY) order.push_back(i);
-    for (size_t i = 0; i < P.lists.size(); ++i)
-        if (P.keys[i].kind != KIND_ANY) order.push_back(i);
-    for (size_t i : order) {
-        if (P.lists[i].empty()) continue;
-        const int64_t base = static_cast<int64_t>(all.size());
-        if (P.keys[i].kind == KIND_H) {
-            for (HTile h : P.hlists[i]) {
-                h.first += base;
-                hall.push_back(h);
-            }
-        } else {
-            hall.insert(hall.end(), P.lists[i].size(), HTile{});
-        }
-        Class c{P.keys[i].kind, P.keys[i].gdtype, P.keys[i].vpl, P.keys[i].bs, base,
-                static_cast<int64_t>(P.lists[i].size()), 0, 0};
-        for (size_t j = 0; j < P.lists[i].size(); ++j) {
-            const Tile& tl = P.lists[i][j];
-            const int64_t per_elem =
-                8 + (st->gdtype[tl.seg] == DT_F32 ? 4 : 2) + (st->code_bits == 4 ? 1 : 2);
-            c.elems += tl.nelem;
-            c.bytes += tl.nelem * per_elem + 16 * int64_t(tl.nblk);
-            if (P.kinds[i][j] == KIND_L && st->explicit_blocks) c.bytes += 8 * int64_t(tl.nblk);
-            if (P.kinds[i][j] == KIND_G && tl.vpl == 1) {
-                // a register run: the kernel's fixed register and LDS capacity
-                const int64_t nvec = ((tl.elem0 + tl.nelem + 3) >> 2) - (tl.elem0 >> 2);
-                if (nvec > kRunMaxVec || tl.nblk < 1 || tl.nblk > kRunMaxBlocks)
-                    return fail(GEFEN_EINVAL, "internal: run tile of %lld vectors, %d blocks",
-                                (long long)nvec, int(tl.nblk));
-            }
-        }
-        st->classes.push_back(c);
-        all.insert(all.end(), P.lists[i].begin(), P.lists[i].end());
-        kinds.insert(kinds.end(), P.kinds[i].begin(), P.kinds[i].end());
-    }
-    st->n_tiles = static_cast<int64_t>(all.size());
-    int rc = st->alloc(&st->tiles, sizeof(Tile) * all.size(), false);
+    PlanCtx ctx;
+    ctx.n_tensors = st->n_tensors;
+    ctx.code_bits = st->code_bits;
+    ctx.explicit_blocks = st->explicit_blocks;
+    ctx.numel = st->numel;
+    ctx.period = st->period;
+    ctx.blk_begin = st->blk_begin;
+    ctx.gdtype = st->gdtype;
+    Plan plan;
+    std::string why = build_plan(&ctx, starts, plan);
+    if (why.empty()) why = check_plan(ctx, starts, plan);
+    if (!why.empty()) return fail(GEFEN_EINVAL, "internal: tile plan: %s", why.c_str());
+    st->n_hblocks = ctx.n_hblocks;
+    st->classes = plan.classes;
+    st->n_tiles = static_cast<int64_t>(plan.tiles.size());
+    int rc = st->alloc(&st->tiles, sizeof(Tile) * plan.tiles.size(), false);
     if (rc) return rc;
-    rc = st->alloc(&st->tile_kind, sizeof(int32_t) * kinds.size(), false);
+    rc = st->alloc(&st->tile_kind, sizeof(int32_t) * plan.kinds.size(), false);
     if (rc) return rc;
-    GEFEN_HIP(hipMemcpy(st->tiles, all.data(), sizeof(Tile) * all.size(), hipMemcpyHostToDevice));
-    GEFEN_HIP(hipMemcpy(st->tile_kind, kinds.data(), sizeof(int32_t) * kinds.size(),
+    GEFEN_HIP(hipMemcpy(st->tiles, plan.tiles.data(), sizeof(Tile) * plan.tiles.size(),
+                        hipMemcpyHostToDevice));
+    GEFEN_HIP(hipMemcpy(st->tile_kind, plan.kinds.data(), sizeof(int32_t) * plan.kinds.size(),
                         hipMemcpyHostToDevice));
     if (st->n_hblocks > 0) {
-        if ((rc = st->alloc(&st->htiles, sizeof(HTile) * hall.size(), false))) return rc;
-        if ((rc = st->alloc(&st->h_partials, sizeof(float2) * all.size(), false))) return rc;
-        if ((rc = st->alloc(&st->h_absmax, sizeof(float) * all.size(), false))) return rc;
+        const size_t nt = plan.tiles.size();
+        if ((rc = st->alloc(&st->htiles, sizeof(HTile) * nt, false))) return rc;
+        if ((rc = st->alloc(&st->h_partials, sizeof(float2) * nt, false))) return rc;
+        if ((rc = st->alloc(&st->h_absmax, sizeof(float) * nt, false))) return rc;
         if ((rc = st->alloc(&st->h_old, sizeof(float2) * st->n_hblocks, false))) return rc;
-        GEFEN_HIP(hipMemcpy(st->htiles, hall.data(), sizeof(HTile) * hall.size(),
+        GEFEN_HIP(hipMemcpy(st->htiles, plan.htiles.data(), sizeof(HTile) * nt,
                             hipMemcpyHostToDevice));
     }
     return GEFEN_OK;
-}
-
-// Tensor-relative block starts of tensor i (explicit blocks), size n_blocks_i + 1.
-int plan_tiles(gefen_state* st, const std::vector<std::vector<int64_t>>& starts)
-{
-    st->n_hblocks = 0;
-    const std::vector<UShape> ushape = plan_u_shapes(st);
-    TilePlan P;
-    static const std::vector<int64_t> kNone;
-    for (int32_t t = 0; t < st->n_tensors; ++t)
-        plan_tensor(st, P, t, ushape[t], st->explicit_blocks ? starts[t] : kNone);
-    fold_small_classes(st, P);
-    return upload_plan(st, P);
 }
 
 // Alg. 2 for a list of tensors. Writes one period per tensor (host), and optionally the

@@ -4,54 +4,13 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "tile_plan.h"
+
 namespace gefen {
 
-// Gradient element types.
-enum : int32_t { DT_F32 = 0, DT_BF16 = 1 };
+// Kernel classes, tiles and the planner: tile_plan.h (host-only, shared with the
+// host tests).
 
-// Work classes of the step kernels. Every tile belongs to exactly one class.
-//  KIND_U  uniform blocks, p % 4 == 0, 16-byte aligned rows: groups of 2^lpb_log2 lanes
-//          own one block each, every lane holds `vpl` 4-element vectors in registers.
-//  KIND_G  any single block (irregular, unaligned, odd or very large p): the whole
-//          workgroup streams it twice (reduce pass, then update pass).
-//  KIND_L  up to 256 small blocks (<= 32 elements): one lane per block.
-//  KIND_H  one chunk of a huge block: a reduce kernel writes per-chunk partials, an
-//          update kernel combines the partials of the block (same fixed order in every
-//          chunk) and updates its chunk, so a huge block spreads over many workgroups.
-//  KIND_ANY small leftover tiles of any of the shapes above, one generic launch.
-enum : int32_t { KIND_U = 0, KIND_G = 1, KIND_L = 2, KIND_H = 3, KIND_ANY = 4 };
-
-constexpr int kThreads = 256;         // workgroup size of the streaming kernels
-constexpr int kMaxThreads = 1024;     // largest KIND_U workgroup
-constexpr int kMaxVpl = 8;            // max 4-element vectors per lane (KIND_U)
-constexpr int kMaxLpbLog2 = 10;       // KIND_U lanes per block up to 1024
-constexpr int kSmallBlock = 32;       // KIND_L blocks hold at most this many elements
-constexpr int kMaxK = 256;            // max codebook entries
-constexpr int64_t kHChunk = 8192;     // KIND_H chunk length
-
-// One tile = the work of one workgroup (32 bytes).
-struct Tile {
-    int64_t elem0;      // first element of the tile, relative to its tensor
-    int64_t blk0;       // global index of the tile's first block
-    int64_t nelem;      // elements in the tile
-    int32_t seg;        // tensor index
-    int16_t nblk;       // blocks in the tile
-    uint8_t vpl;        // KIND_U: vectors per lane
-    uint8_t lpb_log2;   // KIND_U: log2(lanes per block); workgroup size is a class property
-};
-static_assert(sizeof(Tile) == 32, "Tile layout");
-
-// KIND_H bookkeeping, one entry per tile (parallel to the tile array).
-struct HTile {
-    int64_t blk_len;     // elements of the whole block
-    int64_t first;       // absolute tile index of the block's chunk 0 (chunks are
-                         // consecutive tiles; partial arrays are indexed absolutely)
-    int32_t nchunk;      // chunks of the block
-    int32_t chunk;       // this tile's chunk index
-    int32_t hb;          // index of the block among huge blocks (workspace slot)
-    int32_t pad;
-};
-static_assert(sizeof(HTile) == 32, "HTile layout");
 
 // Per-tensor descriptor on device (64 bytes). Pointers are refreshed when the caller
 // passes different parameter or gradient buffers.

@@ -14,7 +14,7 @@
 // (one byte per bucket of [-1, 1] giving the number of midpoints below the bucket) plus
 // a short scan over the midpoints that fall inside the bucket (at most one for codebooks
 // whose entries are at least a bucket apart, as the DP's are).
-#include "run_internal.h"
+#include "tile_plan.h"
 #include "step_device.h"
 
 namespace gefen {
