@@ -51,28 +51,12 @@ struct CodebookDev {
 
 // Histogram bin (Alg. 3) of gradient g in a block whose largest |g| is a > 0: the bin of
 // x = g / a among nbins equal bins of [-1, 1], the last one closed; half_nb = nbins / 2.
-// The defining evaluation is in float64, b = trunc((g / a + 1) * half_nb) (these sources
-// are built with contraction off). Most elements take a float32 estimate instead,
-// t = fma(g * rcp(a), h, h) with h = half_nb: the reciprocal is within 1 ulp and each of
-// the two products rounds once, so |t - (g / a + 1) h| <= 2^-21.4 h, and float64 is within
-// 2^-50 h. When t lies more than 2^-18 h from every integer (eight times the bound), the
-// exact value and the float64 one share t's integer part, so the estimate's floor is
-// the bin; otherwise (about 2^-17 h of all elements: 1.6 % at h = 2048), and for tiny
-// or non-finite inputs, the float64 evaluation decides. Both histogram paths (the
-// histogram kernel and the step kernels that take the histogram on the way) call this.
+// Evaluated in float64 (these sources are built with contraction off), so that the
+// histogram kernel and the step kernels that take the histogram on the way bin every
+// element identically. (A float32 estimate with a float64 evaluation near bin edges
+// measured slower in both kernels: a wave almost always holds some lane near an edge.)
 __device__ __forceinline__ int hist_bin(float g, float a, double half_nb, int nbins)
 {
-    const float h = static_cast<float>(half_nb);
-    if (a >= 0x1p-100f && a <= 0x1p100f) {
-        const float t = fmaf(g * __builtin_amdgcn_rcpf(a), h, h);
-        const float fl = floorf(t);
-        const float fr = t - fl;   // exact: t < 2^24
-        const float d = h * 0x1p-18f;
-        if (fr > d && fr < 1.0f - d) {
-            const int b = static_cast<int>(fl);
-            return b < nbins - 1 ? b : nbins - 1;
-        }
-    }
     const double x = static_cast<double>(g) / static_cast<double>(a);
     const int b = static_cast<int>((x + 1.0) * half_nb);
     return b < nbins - 1 ? b : nbins - 1;

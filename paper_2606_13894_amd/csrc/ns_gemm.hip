@@ -5,16 +5,17 @@
 // The product kernel: one 256-thread workgroup computes a 128 x 128 or 256 x 256 output
 // tile of one batch entry (and one K chunk when split). Its four waves own quarters made
 // of 2 x 2 or 4 x 4 v_mfma_f32_32x32x16_bf16 accumulators (float32). Both operands are read
-// along contiguous K, 16 bytes per thread, into LDS tiles of 64 K per row (rows padded
-// to 72 elements so that the 16-byte fragment reads of 16 consecutive rows hit distinct
-// banks); two LDS stages: the next stage's global loads are in flight while the current
-// one feeds the matrix cores, with one barrier per stage. The epilogue forms
-// alpha * C + beta * E in float32, rounds once to bfloat16 (round to nearest even, as the
-// float32-accumulating GEMMs of the implementation the paper uses), stages the tile in LDS
-// for 16-byte row stores of O, and writes the transposed tile (or, for the symmetric
-// products, the mirror) straight from the accumulators, four rows per 8-byte store.
-// Work items are dealt to the eight XCDs in contiguous runs, so the tiles of one batch
-// entry share an XCD's L2.
+// along contiguous K through buffer resources, 16 bytes per thread, into LDS tiles of
+// 64 K per row (rows padded to 72 elements so that the 16-byte fragment reads of 16
+// consecutive rows hit distinct banks); two LDS stages in a software pipeline: the next
+// stage's global loads are in flight while the current one feeds the matrix cores, each
+// K step's fragments are read during the previous step's MFMAs, one barrier per stage.
+// The epilogue forms alpha * C + beta * E in float32 and rounds once to bfloat16 (round to
+// nearest even, as the float32-accumulating GEMMs of the implementation the paper uses),
+// through one LDS tile in the transposed orientation, so that E is read and O and the
+// transposed output (or, for the symmetric products, the mirror) are written as 16-byte
+// row segments. Work items are dealt to the eight XCDs in contiguous runs, so the tiles
+// of one batch entry share an XCD's L2.
 #include "muon_internal.h"
 #include "ns_plan.h"
 
