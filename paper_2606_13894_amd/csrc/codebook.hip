@@ -250,50 +250,87 @@ __device__ __forceinline__ T* at(void* ws, size_t off)
     return reinterpret_cast<T*>(static_cast<char*>(ws) + off);
 }
 
-// Compaction of non-empty bins and prefix sums, in increasing bin order (one thread,
-// so the summation order is the definition's; the histogram is staged in LDS first so
-// the sequential loop does not wait on global loads). Also clears row 0 of D.
+// Compaction of non-empty bins and prefix sums, in increasing bin order. The workgroup
+// compacts the non-empty bins (a prefix count over 16-bin runs) and forms each one's
+// centre, count and the two products c m and (c m) m in LDS; one thread then takes the
+// three running sums in increasing bin order, so the summation order is the
+// definition's, with nothing but three additions per bin on its path. The sums are
+// copied out by the whole workgroup. Also clears row 0 of D.
+constexpr int kPrepRun = kMaxBins / kThreads;   // bins per thread in the compaction
+
 __global__ __launch_bounds__(kThreads) void k_dp_prep(const uint64_t* __restrict__ hist,
                                                       int32_t nbins, int32_t k, void* ws)
 {
-    __shared__ uint64_t h[kMaxBins];
+    __shared__ double t0[kMaxBins + 1], t1[kMaxBins + 1], t2[kMaxBins + 1];   // c, c m, c m m
+    __shared__ int runs[kThreads];
+    __shared__ int nr;
+    const int tid = threadIdx.x;
     const DpLayout L = dp_layout(nbins, k);
     double* D = at<double>(ws, L.d);
-    const size_t row = static_cast<size_t>(nbins) + 1;
-    for (size_t r = threadIdx.x; r < row; r += blockDim.x) D[r] = r == 0 ? 0.0 : INFINITY;
-    for (int i = threadIdx.x; i < nbins; i += blockDim.x) h[i] = hist[i];
-    __syncthreads();
-    if (threadIdx.x != 0) return;
     double* Z0 = at<double>(ws, L.z0);
     double* Z1 = at<double>(ws, L.z1);
     double* Z2 = at<double>(ws, L.z2);
     double* cnt = at<double>(ws, L.cnt);
     double* ctr = at<double>(ws, L.ctr);
+    const size_t row = static_cast<size_t>(nbins) + 1;
+    for (size_t r = tid; r < row; r += blockDim.x) D[r] = r == 0 ? 0.0 : INFINITY;
     const double w = 2.0 / static_cast<double>(nbins);
-    double z0 = 0.0, z1 = 0.0, z2 = 0.0;
-    Z0[0] = 0.0;
-    Z1[0] = 0.0;
-    Z2[0] = 0.0;
-    int r = 0;
-    for (int i = 0; i < nbins; ++i) {
-        const uint64_t hv = h[i];
+    // thread tid owns bins [tid * kPrepRun, + kPrepRun): count, then scan the counts
+    const int i0 = tid * kPrepRun;
+    int mine = 0;
+    for (int i = i0; i < i0 + kPrepRun && i < nbins; ++i) mine += hist[i] != 0;
+    runs[tid] = mine;
+    __syncthreads();
+    if (tid == 0) {
+        int acc = 0;
+        for (int q = 0; q < kThreads; ++q) {
+            const int c = runs[q];
+            runs[q] = acc;
+            acc += c;
+        }
+        nr = acc;
+    }
+    __syncthreads();
+    int r = runs[tid];   // compacted slots before this thread's bins (0-based)
+    for (int i = i0; i < i0 + kPrepRun && i < nbins; ++i) {
+        const uint64_t hv = hist[i];
         if (hv == 0) continue;
         const double c = static_cast<double>(hv);
         const double m = -1.0 + (static_cast<double>(i) + 0.5) * w;
         ++r;
+        const double cm = c * m;
+        t0[r] = c;
+        t1[r] = cm;
+        t2[r] = cm * m;
         ctr[r] = m;
         cnt[r] = c;
-        z0 = z0 + c;
-        z1 = z1 + c * m;
-        z2 = z2 + c * m * m;
-        Z0[r] = z0;
-        Z1[r] = z1;
-        Z2[r] = z2;
     }
-    int32_t* hdr = at<int32_t>(ws, L.hdr);
-    hdr[0] = r;
-    hdr[1] = r >= k ? k : (r >= 2 ? r : 0);
-    hdr[2] = r >= k ? 0 : 1;
+    __syncthreads();
+    const int b = nr;
+    if (tid == 0) {
+        double z0 = 0.0, z1 = 0.0, z2 = 0.0;
+        t0[0] = 0.0;
+        t1[0] = 0.0;
+        t2[0] = 0.0;
+        for (int q = 1; q <= b; ++q) {
+            z0 = z0 + t0[q];
+            z1 = z1 + t1[q];
+            z2 = z2 + t2[q];
+            t0[q] = z0;
+            t1[q] = z1;
+            t2[q] = z2;
+        }
+        int32_t* hdr = at<int32_t>(ws, L.hdr);
+        hdr[0] = b;
+        hdr[1] = b >= k ? k : (b >= 2 ? b : 0);
+        hdr[2] = b >= k ? 0 : 1;
+    }
+    __syncthreads();
+    for (int q = tid; q <= b; q += blockDim.x) {
+        Z0[q] = t0[q];
+        Z1[q] = t1[q];
+        Z2[q] = t2[q];
+    }
 }
 
 // ---------------------------------------------------------------------------------

@@ -79,6 +79,24 @@ def test_each_iteration_teacher_forced(batch, m, n):
     print(f"{(batch, m, n)}: largest share of one-step flips {worst:.2e}")
 
 
+def test_big_tile_iterations():
+    """The 256 x 256 tile (one workgroup per CU, 4 x 4 accumulators per wave) and its
+    split Gram: six 1024 x 2048 matrices take the big tile in the Gram product (split 4
+    ways over K) and in the combine. Three iterations, teacher-forced, every batch entry."""
+    dev = _dev()
+    batch, m, n = 6, 1024, 2048
+    x = _x0(batch, m, n, seed=11, dev=dev)
+    worst = 0.0
+    for k in range(3):
+        y = gf.newton_schulz(x, steps=1)
+        torch.cuda.synchronize()
+        xi, yo = _f64(x), _f64(y)
+        for bi in range(batch):
+            worst = max(worst, _check_iteration(xi[bi], yo[bi], f"big tile it {k} b {bi}"))
+        x = y
+    print(f"big tile: largest share of one-step flips {worst:.2e}")
+
+
 def test_steps_chain_bitwise():
     """Five iterations in one call equal five calls of one iteration, bit for bit, and a
     repeated call gives the same bits (no order-dependent accumulation)."""

@@ -2,9 +2,10 @@
 
 Teacher-forced per step (see parity.py for the gates). Covers every kernel class:
 uniform blocks held in registers (p % 4 == 0, p <= 8192), the two-pass streaming kernel
-(odd, unaligned, irregular or large blocks) and the lane-per-block kernel (blocks of
-at most 32 elements), with fp32 and bf16 gradients, ragged last tiles, zero blocks,
-misaligned tensors, explicit block tables, codebook refits and checkpoints.
+(odd, unaligned, irregular or large blocks), register runs of short explicit blocks and
+the lane-per-block kernel (blocks of at most 32 elements), with fp32 and bf16
+gradients, ragged last tiles, zero blocks, misaligned tensors, explicit block tables,
+codebook refits and checkpoints.
 """
 import numpy as np
 import pytest
@@ -545,6 +546,48 @@ def test_uniform_long_period_streamed():
     run.state.profile_begin(1)
     run.state.step(params, gr(3), HP["lr"], HP["betas"], HP["eps"], HP["wd"], 3)
     assert [k["kind"] for k in run.state.profile_end()] == ["streamed_block"]
+
+
+def _single_block_sizes(seed):
+    """Explicit block sizes of one workgroup each (2043 to 32769 elements, with the
+    powers of two and their successors), register runs and small blocks around them."""
+    rng = np.random.default_rng(seed)
+    sizes = np.concatenate([[2043, 4096, 4097, 8192, 8193, 16384, 16385, 32768, 32769, 1, 5,
+                             33, 2042],
+                            rng.integers(2043, 32769, size=24), rng.integers(33, 2043, size=8)])
+    rng.shuffle(sizes)
+    return np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+
+
+@pytest.mark.parametrize("code_bits", [8, 4])
+@pytest.mark.parametrize("gdt", [torch.bfloat16, torch.float32])
+def test_single_blocks(gdt, code_bits):
+    """Explicit blocks of 2043 to 32769 elements, one per workgroup, beside register runs
+    and small blocks: three steps teacher-forced against the oracle."""
+    from parity import Run
+    dev = _dev()
+    offs = _single_block_sizes(41 + code_bits)
+    n = int(offs[-1])
+    params = [torch.randn(n, device=dev) * 0.02]
+    gr = lambda t: [_grad(n, 4100 + t, gdt, dev=dev)]
+    run = Run(params, gr(1), block_offsets=offs, code_bits=code_bits)
+    _run_steps(run, gr, 3, where=f"single blocks {code_bits}-bit {gdt}")
+
+
+@pytest.mark.parametrize("code_bits", [8, 4])
+def test_single_blocks_misaligned(code_bits):
+    """Explicit single blocks on parameter and gradient views at odd element offsets.
+    Teacher-forced, three steps."""
+    from parity import Run
+    dev = _dev()
+    offs = _single_block_sizes(7)[:12]
+    n = int(offs[-1])
+    pbuf = torch.randn(n + 3, device=dev) * 0.02
+    theta = pbuf[1:1 + n]
+    assert theta.data_ptr() % 16 != 0
+    gbufs = {t: _grad(n + 1, 4200 + t, torch.bfloat16, dev=dev) for t in range(1, 4)}
+    run = Run([theta], [gbufs[1][1:]], block_offsets=offs, code_bits=code_bits)
+    _run_steps(run, lambda t: [gbufs[t][1:]], 3, where=f"single blocks misaligned {code_bits}")
 
 
 def test_tiny_tensors_inferred():

@@ -44,7 +44,7 @@ def _explicit_offsets(seed):
     sizes = np.concatenate([[1, 3, 32, 33, 65536, 65537, 9000, 2042, 2043],
                             rng.integers(1, 33, size=150),      # one lane per block
                             rng.integers(33, 600, size=400),    # register runs
-                            rng.integers(600, 20000, size=40)])  # one workgroup per block
+                            rng.integers(600, 40000, size=40)])  # one workgroup per block
     rng.shuffle(sizes)
     return np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
 
