@@ -2,10 +2,13 @@
 // cores, and the kernels that bring the momentum matrices into and out of their layout
 // (ns_plan.h gives the layout and the three products of an iteration).
 //
-// The product kernel: one 256-thread workgroup computes a 128 x 128 or 256 x 256 output
-// tile of one batch entry (and one K chunk when split). Its four waves own quarters made
-// of 2 x 2 or 4 x 4 v_mfma_f32_32x32x16_bf16 accumulators (float32). Both operands are read
-// along contiguous K through buffer resources, 16 bytes per thread, into LDS tiles of
+// The product kernel: one workgroup computes a 128 x 128 or 256 x 256 output tile of one
+// batch entry (and one K chunk when split). At 128, four waves (two workgroups per CU)
+// own quarters of 2 x 2 v_mfma_f32_32x32x16_bf16 accumulators (float32); at 256, eight
+// waves (one workgroup per CU, two waves per SIMD) own eighths of 2 x 4 accumulators, which
+// needs 6 fragment reads per 8 matrix-core ops where a quarter of 4 x 4 per wave would
+// leave one wave per SIMD (measured 8-14 % slower on the model shapes). Both operands are
+// read along contiguous K through buffer resources, 16 bytes per thread, into LDS tiles of
 // 64 K per row (rows padded to 72 elements so that the 16-byte fragment reads of 16
 // consecutive rows hit distinct banks); two LDS stages in a software pipeline: the next
 // stage's global loads are in flight while the current one feeds the matrix cores, each
@@ -14,8 +17,8 @@
 // nearest even, as the float32-accumulating GEMMs of the implementation the paper uses),
 // through one LDS tile in the transposed orientation, so that E is read and O and the
 // transposed output (or, for the symmetric products, the mirror) are written as 16-byte
-// row segments. Work items are dealt to the eight XCDs in contiguous runs, so the tiles
-// of one batch entry share an XCD's L2.
+// row segments; the 128 tile loads its E rows during the last stage. Work items are dealt
+// to the eight XCDs in contiguous runs, so the tiles of one batch entry share an XCD's L2.
 #include "muon_internal.h"
 #include "ns_plan.h"
 
@@ -29,6 +32,7 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4v __attribute__((ext_vector_type(4)));
 
 constexpr int BK = kNsBK;
+constexpr int kNsBigWaves = 8;   // waves of the 256 x 256 tile's workgroup
 constexpr int LDK = BK + 8;      // LDS row stride of the operand tiles (elements)
 
 __device__ __forceinline__ float bf16_val(uint16_t b)
@@ -51,55 +55,94 @@ __device__ __forceinline__ uint32_t bf16_at(const u32x4& w, int j)
     return (j & 1) ? (v >> 16) : (v & 0xffffu);
 }
 
-// W x W accumulator blocks of 32 x 32 per wave, 2 x 2 waves: a (64 W) x (64 W) tile.
-template <int W>
+// A (64 W) x (64 W) output tile computed by NW waves (4 or 8) in a grid of NW / 2 x 2:
+// each wave owns MI x NI accumulator blocks of 32 x 32 (MI = NI = W with four waves;
+// MI = W / 2, NI = W with eight, so that a wave's fragment reads per matrix-core op drop
+// from 1 to 3/4 of a 16-byte read at the 256 tile and two waves share each SIMD).
+template <int W, int NW = 4>
 struct NsTileShape {
     static constexpr int T = 64 * W;               // tile rows and columns
+    static constexpr int kThreads = 64 * NW;
+    static constexpr int WR = NW / 2;              // wave rows (along M); two wave columns
+    static constexpr int MI = T / (32 * WR), NI = T / 64;
     static constexpr int LDT = T + 8;              // LDS row stride of the epilogue tiles
     static constexpr int kStage = 2 * T * LDK;     // both operand tiles of one stage
     static constexpr int kLds = 2 * kStage > T * LDT ? 2 * kStage : T * LDT;
-    static constexpr int kPasses = T / 32;         // 32 rows of 64 K loaded per pass
+    static constexpr int kRowsPerPass = kThreads / 8;   // 64-element rows loaded per pass
+    static constexpr int kPasses = T / kRowsPerPass;
+    static constexpr int kSRows = kThreads / 16;   // epilogue tile rows per pass
+    static constexpr int kEPasses = T / kSRows;
 };
+
+// The E^T tile rows a thread moves into the epilogue's LDS tile: pass p of half h is
+// tile row p * kSRows + tid / 16, columns h * 128 + (tid % 16) * 8 .. + 7 (zero beyond N
+// rows and lde columns; E^T rows are zero beyond M up to lde, a multiple of 8).
+template <int W, int NW>
+__device__ __forceinline__ void load_et(const NsGemmArgs& a, const NsWork& w, int tid,
+                                        u32x4 (&e)[W / 2][NsTileShape<W, NW>::kEPasses])
+{
+    using S = NsTileShape<W, NW>;
+    constexpr int T = S::T;
+    const int64_t row0 = int64_t(w.ti) * T, col0 = int64_t(w.tj) * T;
+    const uint16_t* __restrict__ Et = a.et + w.b * a.se;
+    const int srow = tid >> 4, scol = (tid & 15) * 8;
+#pragma unroll
+    for (int half = 0; half < T / 128; ++half)
+#pragma unroll
+        for (int pass = 0; pass < S::kEPasses; ++pass) {
+            const int64_t j = col0 + pass * S::kSRows + srow, i = row0 + half * 128 + scol;
+            const u32x4 z = {0u, 0u, 0u, 0u};
+            e[half][pass] =
+                (j < a.N && i < a.lde) ? *reinterpret_cast<const u32x4*>(Et + j * a.lde + i) : z;
+        }
+}
 
 // Epilogue through one LDS tile in the E^T / O^T orientation (rows j, columns i), so that
 // every global access is a 16-byte row segment: (1) the E^T tile as stored; (2) each lane
 // turns its accumulators into bfloat16 results in place, over the E^T elements of the
 // same positions (8 bytes: four consecutive i); (3) the tile's rows are the rows of O^T
 // (or of the mirror); (4) the rows of O come from 8 x 8 blocks of the tile transposed in
-// registers.
-template <int W>
-__device__ __forceinline__ void epilogue(const NsGemmArgs& a, const NsWork& w,
-                                         const f32x16 (&acc)[W][W], uint16_t* lds, int tid)
+// registers. pre: the E^T rows of this thread (load_et), loaded during the last stage;
+// null: loaded here.
+template <int W, int NW>
+__device__ __forceinline__ void epilogue(
+    const NsGemmArgs& a, const NsWork& w,
+    const f32x16 (&acc)[NsTileShape<W, NW>::MI][NsTileShape<W, NW>::NI], uint16_t* lds,
+    int tid, const u32x4 (*pre)[NsTileShape<W, NW>::kEPasses] = nullptr)
 {
-    using S = NsTileShape<W>;
-    constexpr int T = S::T, LDT = S::LDT;
+    using S = NsTileShape<W, NW>;
+    constexpr int T = S::T, LDT = S::LDT, MI = S::MI, NI = S::NI;
     const int64_t row0 = int64_t(w.ti) * T, col0 = int64_t(w.tj) * T;
     const int lane = tid & 63, wave = tid >> 6;
-    const int wm = (wave >> 1) * (32 * W), wn = (wave & 1) * (32 * W);
+    const int wm = (wave >> 1) * (32 * MI), wn = (wave & 1) * (32 * NI);
     const int frow = lane & 31, fk = (lane >> 5) * 8;
 
-    const uint16_t* __restrict__ Et = a.et ? a.et + w.b * a.se : nullptr;
+    const bool Et = a.et != nullptr;
     uint16_t* __restrict__ Ot = a.ot ? a.ot + w.b * a.sot : nullptr;
     const bool mirror = Ot && (!a.sym || w.ti != w.tj);
     const int srow = tid >> 4, scol = (tid & 15) * 8;
     if (Et) {
+        u32x4 e[W / 2][S::kEPasses];
+        if (pre) {
+#pragma unroll
+            for (int half = 0; half < T / 128; ++half)
+#pragma unroll
+                for (int pass = 0; pass < S::kEPasses; ++pass) e[half][pass] = pre[half][pass];
+        } else {
+            load_et<W, NW>(a, w, tid, e);
+        }
 #pragma unroll
         for (int half = 0; half < T / 128; ++half)
 #pragma unroll
-            for (int pass = 0; pass < T / 16; ++pass) {
-                const int r = pass * 16 + srow, c = half * 128 + scol;
-                const int64_t j = col0 + r, i = row0 + c;
-                const u32x4 z = {0u, 0u, 0u, 0u};
-                // E^T rows are zero beyond M up to lde (a multiple of 8)
-                *reinterpret_cast<u32x4*>(lds + r * LDT + c) =
-                    (j < a.N && i < a.lde) ? *reinterpret_cast<const u32x4*>(Et + j * a.lde + i) : z;
-            }
+            for (int pass = 0; pass < S::kEPasses; ++pass)
+                *reinterpret_cast<u32x4*>(lds + (pass * S::kSRows + srow) * LDT + half * 128 +
+                                          scol) = e[half][pass];
         __syncthreads();
     }
 #pragma unroll
-    for (int mi = 0; mi < W; ++mi)
+    for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
-        for (int ni = 0; ni < W; ++ni) {
+        for (int ni = 0; ni < NI; ++ni) {
             const int lc = wn + ni * 32 + frow;
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
@@ -128,8 +171,8 @@ __device__ __forceinline__ void epilogue(const NsGemmArgs& a, const NsWork& w,
 #pragma unroll
         for (int half = 0; half < T / 128; ++half)
 #pragma unroll
-            for (int pass = 0; pass < T / 16; ++pass) {
-                const int r = pass * 16 + srow, c = half * 128 + scol;
+            for (int pass = 0; pass < S::kEPasses; ++pass) {
+                const int r = pass * S::kSRows + srow, c = half * 128 + scol;
                 const int64_t j = col0 + r, i = row0 + c;
                 if (j < a.N && i < a.ot_cols)
                     *reinterpret_cast<u32x4*>(Ot + j * a.ldot + i) =
@@ -140,8 +183,8 @@ __device__ __forceinline__ void epilogue(const NsGemmArgs& a, const NsWork& w,
         constexpr int NB = T / 8;   // 8 x 8 blocks along a side
         uint16_t* __restrict__ O = a.o + w.b * a.so;
 #pragma unroll
-        for (int q = 0; q < NB * NB / kNsThreads; ++q) {
-            const int blk = q * kNsThreads + tid;
+        for (int q = 0; q < NB * NB / S::kThreads; ++q) {
+            const int blk = q * S::kThreads + tid;
             const int bj = blk % NB, bi = blk / NB;
             u32x4 rv[8];   // tile rows j = 8 bj .. + 7, columns i = 8 bi .. + 7
 #pragma unroll
@@ -163,11 +206,12 @@ __device__ __forceinline__ void epilogue(const NsGemmArgs& a, const NsWork& w,
     }
 }
 
-template <int W, bool SPLIT>
-__global__ __launch_bounds__(kNsThreads, W == 2 ? 2 : 1) void k_ns_gemm(const NsGemmArgs a)
+template <int W, bool SPLIT, int NW = 4>
+__global__ __launch_bounds__(64 * NW, W == 2 ? 2 : 1) void k_ns_gemm(const NsGemmArgs a)
 {
-    using S = NsTileShape<W>;
-    constexpr int T = S::T, LDT = S::LDT, NP = S::kPasses;
+    using S = NsTileShape<W, NW>;
+    constexpr int T = S::T, LDT = S::LDT, NP = S::kPasses, MI = S::MI, NI = S::NI;
+    constexpr int RP = S::kRowsPerPass;
     __shared__ __attribute__((aligned(16))) uint16_t lds[S::kLds];
     const int64_t total = int64_t(a.batch) * a.splits * a.tiles;
     const int64_t per_xcd = (total + 7) / 8;
@@ -200,9 +244,9 @@ __global__ __launch_bounds__(kNsThreads, W == 2 ? 2 : 1) void k_ns_gemm(const Ns
 #pragma unroll
         for (int r = 0; r < NP; ++r) {
             ra[r] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                                  rp, vp + 64 * r * ldp, 2 * k0, 0));
+                                                  rp, vp + 2 * RP * r * ldp, 2 * k0, 0));
             rb[r] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                                  rq, vq + 64 * r * ldq, 2 * k0, 0));
+                                                  rq, vq + 2 * RP * r * ldq, 2 * k0, 0));
         }
     };
     auto lstore = [&](int buf) {
@@ -210,54 +254,56 @@ __global__ __launch_bounds__(kNsThreads, W == 2 ? 2 : 1) void k_ns_gemm(const Ns
         uint16_t* sb = sa + T * LDK;
 #pragma unroll
         for (int r = 0; r < NP; ++r) {
-            *reinterpret_cast<u32x4*>(sa + (lrow + 32 * r) * LDK + lk) = ra[r];
-            *reinterpret_cast<u32x4*>(sb + (lrow + 32 * r) * LDK + lk) = rb[r];
+            *reinterpret_cast<u32x4*>(sa + (lrow + RP * r) * LDK + lk) = ra[r];
+            *reinterpret_cast<u32x4*>(sb + (lrow + RP * r) * LDK + lk) = rb[r];
         }
     };
 
     const int lane = tid & 63, wave = tid >> 6;
-    const int wm = (wave >> 1) * (32 * W), wn = (wave & 1) * (32 * W);
+    const int wm = (wave >> 1) * (32 * MI), wn = (wave & 1) * (32 * NI);
     const int frow = lane & 31, fk = (lane >> 5) * 8;
-    f32x16 acc[W][W];
+    f32x16 acc[MI][NI];
 #pragma unroll
-    for (int mi = 0; mi < W; ++mi)
+    for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
-        for (int ni = 0; ni < W; ++ni)
+        for (int ni = 0; ni < NI; ++ni)
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[mi][ni][v] = 0.0f;
 
     // The fragments of one 16-wide K step: rows of the wave's A and B blocks.
-    typedef bf16x8 Frag[W];
-    auto frags = [&](Frag& fa, Frag& fb, int buf, int kk) {
+    typedef bf16x8 FragA[MI];
+    typedef bf16x8 FragB[NI];
+    auto frags = [&](FragA& fa, FragB& fb, int buf, int kk) {
         const uint16_t* sa = lds + buf * S::kStage;
         const uint16_t* sb = sa + T * LDK;
 #pragma unroll
-        for (int mi = 0; mi < W; ++mi)
+        for (int mi = 0; mi < MI; ++mi)
             fa[mi] = __builtin_bit_cast(
                 bf16x8, *reinterpret_cast<const u32x4*>(sa + (wm + mi * 32 + frow) * LDK + kk + fk));
 #pragma unroll
-        for (int ni = 0; ni < W; ++ni)
+        for (int ni = 0; ni < NI; ++ni)
             fb[ni] = __builtin_bit_cast(
                 bf16x8, *reinterpret_cast<const u32x4*>(sb + (wn + ni * 32 + frow) * LDK + kk + fk));
     };
-    auto mfmas = [&](const Frag& fa, const Frag& fb, int from, int to) {
+    auto mfmas = [&](const FragA& fa, const FragB& fb, int from, int to) {
 #pragma unroll
         for (int q = from; q < to; ++q)
-            acc[q / W][q % W] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[q / W], fb[q % W],
-                                                                       acc[q / W][q % W], 0, 0, 0);
+            acc[q / NI][q % NI] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                fa[q / NI], fb[q % NI], acc[q / NI][q % NI], 0, 0, 0);
     };
     // Scheduling groups (instruction classes of __builtin_amdgcn_sched_group_barrier):
     // `n` matrix-core ops, each followed by `per` ops of class `mask`.
     constexpr int kMfma = 0x008, kDsRead = 0x100, kDsWrite = 0x200, kVmemRead = 0x020;
-    constexpr int kMM = W * W;                 // MFMAs of one K step
-    constexpr int kFr = 2 * W;                 // fragment reads of one K step
+    constexpr int kMM = MI * NI;               // MFMAs of one K step
+    constexpr int kFr = MI + NI;               // fragment reads of one K step
     constexpr int kWr = 2 * NP;                // LDS writes of one stage
 
     // One stage in a software pipeline: the next stage's global loads go out first; each
     // K step's matrix-core ops run while the next step's fragments are read from LDS; the
     // next stage goes into the other LDS buffer during the third step, and after a
     // barrier in the middle of the fourth step the next stage's first fragments are read.
-    Frag fa, fb, na, nb;
+    FragA fa, na;
+    FragB fb, nb;
     const int nk = static_cast<int>((kend - kbeg) / BK);
     gload(static_cast<int>(kbeg));
     lstore(0);
@@ -283,10 +329,9 @@ __global__ __launch_bounds__(kNsThreads, W == 2 ? 2 : 1) void k_ns_gemm(const Ns
     };
     auto advance = [&]() {
 #pragma unroll
-        for (int q = 0; q < W; ++q) {
-            fa[q] = na[q];
-            fb[q] = nb[q];
-        }
+        for (int q = 0; q < MI; ++q) fa[q] = na[q];
+#pragma unroll
+        for (int q = 0; q < NI; ++q) fb[q] = nb[q];
     };
     for (int it = 0; it + 1 < nk; ++it) {
         const int cur = it & 1;
@@ -339,8 +384,14 @@ __global__ __launch_bounds__(kNsThreads, W == 2 ? 2 : 1) void k_ns_gemm(const Ns
             }
         }
     }
+    // The 128 tile loads the epilogue's E^T rows during the last stage, so their latency
+    // hides behind its matrix-core ops (the 256 tile has no registers to spare for them).
+    constexpr bool kPrefetchE = !SPLIT && W == 2;
+    u32x4 epre[W / 2][S::kEPasses];
     {   // the last stage
         const int cur = (nk - 1) & 1;
+        if constexpr (kPrefetchE)
+            if (a.et) load_et<W, NW>(a, w, tid, epre);
 #pragma unroll
         for (int ks = 0; ks < 3; ++ks) {
             frags(na, nb, cur, (ks + 1) * 16);
@@ -357,9 +408,9 @@ __global__ __launch_bounds__(kNsThreads, W == 2 ? 2 : 1) void k_ns_gemm(const Ns
     if constexpr (SPLIT) {
         float* __restrict__ part = a.partial + ((int64_t(w.s) * a.batch + w.b) * a.M) * a.N;
 #pragma unroll
-        for (int mi = 0; mi < W; ++mi)
+        for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
-            for (int ni = 0; ni < W; ++ni) {
+            for (int ni = 0; ni < NI; ++ni) {
                 const int64_t j = col0 + wn + ni * 32 + frow;
 #pragma unroll
                 for (int v = 0; v < 16; ++v) {
@@ -368,7 +419,10 @@ __global__ __launch_bounds__(kNsThreads, W == 2 ? 2 : 1) void k_ns_gemm(const Ns
                 }
             }
     } else {
-        epilogue<W>(a, w, acc, lds, tid);
+        if constexpr (kPrefetchE)
+            epilogue<W, NW>(a, w, acc, lds, tid, a.et ? epre : nullptr);
+        else
+            epilogue<W, NW>(a, w, acc, lds, tid);
     }
 }
 
@@ -564,10 +618,12 @@ hipError_t launch_ns_gemm(const NsGemmArgs& a, hipStream_t stream)
     const int64_t groups = ns_workgroups(a);
     const dim3 grid(static_cast<unsigned>(groups)), block(kNsThreads);
     if (a.tile == kNsTileBig) {
+        constexpr int NW = kNsBigWaves;
+        const dim3 big(NsTileShape<4, NW>::kThreads);
         if (a.splits > 1)
-            hipLaunchKernelGGL((k_ns_gemm<4, true>), grid, block, 0, stream, a);
+            hipLaunchKernelGGL((k_ns_gemm<4, true, NW>), grid, big, 0, stream, a);
         else
-            hipLaunchKernelGGL((k_ns_gemm<4, false>), grid, block, 0, stream, a);
+            hipLaunchKernelGGL((k_ns_gemm<4, false, NW>), grid, big, 0, stream, a);
     } else {
         if (a.splits > 1)
             hipLaunchKernelGGL((k_ns_gemm<2, true>), grid, block, 0, stream, a);

@@ -32,9 +32,9 @@
 namespace gefen {
 
 // Output tiles of one workgroup: 128 x 128 (four waves of 64 x 64, two workgroups per
-// compute unit) or 256 x 256 (four waves of 128 x 128, one per compute unit: twice the
-// flops per loaded byte and four times the matrix-core work per K stage, to cover memory
-// latency on the large products).
+// compute unit) or 256 x 256 (eight waves of 64 x 128, one workgroup per compute unit:
+// twice the flops per loaded byte and four times the matrix-core work per K stage, to
+// cover memory latency on the large products). kNsThreads is the 128 tile's workgroup.
 constexpr int kNsTileSmall = 128;
 constexpr int kNsTileBig = 256;
 constexpr int kNsBK = 64;      // K of one pipeline stage
