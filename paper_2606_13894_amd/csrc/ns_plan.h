@@ -434,28 +434,50 @@ inline std::string ns_plan_groups(int32_t n, const int64_t* rows, const int64_t*
     return std::string();
 }
 
-// Two lanes (streams that run concurrently): groups in decreasing order of product work,
-// each to the lane with less work so far.
+// Estimated time of a group's Newton-Schulz iterations relative to the others': each
+// product launch costs its flops at the products' measured rate, but at least the
+// latency of a small launch (a product of a few dozen workgroups takes 10-50 us whatever
+// its flops), so that latency-bound groups such as a position embedding count for the
+// time they hold a lane rather than for their flops.
+inline double ns_group_cost(const NsShape& sh)
+{
+    constexpr double kFlopsPerUs = 6.0e8;   // ~600 TFLOP/s on the model shapes
+    constexpr double kLaunchUs = 15.0;
+    const double m = static_cast<double>(sh.m), n = static_cast<double>(sh.ldx);
+    const double c = static_cast<double>(sh.count);
+    if (sh.m < 2) return kLaunchUs;   // one vector kernel for all iterations
+    auto launch = [&](double flops) { return std::max(flops / kFlopsPerUs, kLaunchUs); };
+    double t = launch(c * 2.0 * m * m * n) + launch(c * 2.0 * m * m * m) +
+               launch(c * 2.0 * m * m * n);
+    if (sh.splits > 1) t += kLaunchUs;   // the Gram's split-K reduction
+    return t;
+}
+
+// Two lanes (streams that run concurrently): groups in decreasing order of estimated
+// time, each to the lane with less so far; then lane 0 runs its groups shortest first
+// and lane 1 longest first, so that the short, latency-bound groups of either lane run
+// beside a long group of the other rather than alone at the end of the phase (measured
+// on the GPT-2 125M shapes: the position-embedding group ran its 0.4 ms alone after the
+// other lane had finished).
 inline void ns_assign_lanes(const std::vector<NsGroup>& groups, std::vector<int32_t> lanes[2])
 {
     std::vector<int32_t> byw(groups.size());
-    std::vector<double> work(groups.size());
+    std::vector<double> cost(groups.size());
     for (size_t gi = 0; gi < groups.size(); ++gi) {
-        const NsShape& sh = groups[gi].shape;
         byw[gi] = static_cast<int32_t>(gi);
-        const double m = static_cast<double>(sh.m), nn = static_cast<double>(sh.ldx);
-        work[gi] = sh.count * (sh.m > 1 ? 4.0 * m * m * nn + 2.0 * m * m * m : 4.0 * nn);
+        cost[gi] = ns_group_cost(groups[gi].shape);
     }
     std::stable_sort(byw.begin(), byw.end(),
-                     [&](int32_t a, int32_t b) { return work[a] > work[b]; });
+                     [&](int32_t a, int32_t b) { return cost[a] > cost[b]; });
     double load[2] = {0.0, 0.0};
     lanes[0].clear();
     lanes[1].clear();
     for (int32_t gi : byw) {
         const int l = load[1] < load[0] ? 1 : 0;
         lanes[l].push_back(gi);
-        load[l] += work[gi];
+        load[l] += cost[gi];
     }
+    std::reverse(lanes[0].begin(), lanes[0].end());   // shortest first
 }
 
 // Elements of one lane's buffers: X and X^T (two of each), the two m x m products, the
