@@ -167,10 +167,10 @@ int main()
                 return 1;
             }
             std::printf("lane %d group %d: %lld x (%lld x %lld), ldx %lld ldm %lld, %d parts, "
-                        "Gram splits %d (chunk %d), tiles %d / %d / %d\n", l, gi,
+                        "Gram splits %d (chunk %d), tiles %d / %d / %d, cost %.3f\n", l, gi,
                         (long long)sh.count, (long long)sh.m, (long long)sh.n, (long long)sh.ldx,
                         (long long)sh.ldm, static_cast<int>(g.parts.size()), sh.splits, sh.kchunk,
-                        sh.tile_gram, sh.tile_poly, sh.tile_comb);
+                        sh.tile_gram, sh.tile_poly, sh.tile_comb, ns_group_cost(sh));
             if (sh.m < 2) continue;
             for (int cur = 0; cur < 2; ++cur) {
                 NsGemmArgs prods[3];

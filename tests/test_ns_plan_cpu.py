@@ -41,6 +41,30 @@ def test_workload_plans_stay_in_bounds(checker, name):
     assert out.strip().splitlines()[-1].startswith("ok:"), out
 
 
+@pytest.mark.parametrize("name", ["gpt2_125m", "gpt2_1b", "llama3_1p5b"])
+def test_lanes_balance_and_order(checker, name):
+    """The two lanes split the groups by estimated time (each group to the lane with less
+    so far, longest first: the lanes differ by at most the longest group), lane 0 runs
+    its groups shortest first and lane 1 longest first, and every group is on one lane."""
+    import re
+    w = W.get(name)
+    rc, out = _run(checker, [(t.rows, t.numel) for t in w.tensors])
+    assert rc == 0, out
+    lanes = {0: [], 1: []}
+    seen = set()
+    for line in out.splitlines():
+        m = re.match(r"lane (\d) group (\d+): .* cost ([0-9.]+)$", line)
+        if m:
+            lanes[int(m.group(1))].append(float(m.group(3)))
+            seen.add(int(m.group(2)))
+    n_groups = int(re.search(r"ok: (\d+) groups", out).group(1))
+    assert len(seen) == n_groups == len(lanes[0]) + len(lanes[1])
+    assert lanes[0] == sorted(lanes[0]), lanes[0]
+    assert lanes[1] == sorted(lanes[1], reverse=True), lanes[1]
+    longest = max(lanes[0] + lanes[1])
+    assert abs(sum(lanes[0]) - sum(lanes[1])) <= longest + 1e-9, lanes
+
+
 def test_odd_shapes_stay_in_bounds(checker):
     shapes = [(64, 192), (192, 64), (128, 128), (1, 300), (300, 1), (3, 5), (64, 4096),
               (5000, 48), (1003, 40), (77, 9), (1003, 40), (130, 129), (1008, 40), (40, 1008),
