@@ -458,6 +458,15 @@ inline std::string concat_plan(const PlanCtx* st, TilePlan& P, Plan& out)
         out.tiles.insert(out.tiles.end(), P.lists[i].begin(), P.lists[i].end());
         out.kinds.insert(out.kinds.end(), P.kinds[i].begin(), P.kinds[i].end());
     }
+    // Workspace slots of the huge blocks in tile order: the planner numbered them tensor
+    // by tensor, but each gradient type's huge blocks form a class of their own, so with
+    // both types the classes' concatenation interleaves that numbering.
+    int32_t hb = 0;
+    for (size_t t = 0; t < out.tiles.size(); ++t)
+        if (out.kinds[t] == KIND_H) {
+            HTile& h = out.htiles[t];
+            h.hb = h.chunk == 0 ? hb++ : out.htiles[static_cast<size_t>(h.first)].hb;
+        }
     return std::string();
 }
 

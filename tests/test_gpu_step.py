@@ -354,6 +354,29 @@ def test_mixed_tensors_share_one_launch():
     assert kinds.count("uniform_registers") == 1 and "split_block" in kinds, kinds
 
 
+@pytest.mark.parametrize("code_bits", [8, 4])
+def test_split_blocks_of_both_gradient_types(code_bits):
+    """Blocks split over workgroups (periods above 65536) in tensors of both gradient
+    types, interleaved: each type's split blocks form a launch of their own, so their
+    workspace slots are numbered in launch order (numbered tensor by tensor, such a state
+    used to be refused by the plan check). Teacher-forced, three steps, and every split
+    block in the profile's split class."""
+    from parity import Run
+    dev = _dev()
+    specs = [(70000, 3, torch.float32), (70001, 2, torch.bfloat16), (65540, 2, torch.float32),
+             (2048, 4, torch.bfloat16)]
+    params = [torch.randn(p * nb, device=dev) * 0.02 for p, nb, _ in specs]
+    gr = lambda t: [_grad(p * nb, 4400 + 10 * i + t, dt, dev=dev)
+                    for i, (p, nb, dt) in enumerate(specs)]
+    run = Run(params, gr(1), period_override=[p for p, _, _ in specs], code_bits=code_bits)
+    _run_steps(run, gr, 3, where=f"split blocks of both types {code_bits}-bit")
+    st = run.state
+    st.profile_begin(1)
+    st.step(params, gr(4), 1e-3, (0.9, 0.999), 1e-8, 0.1, 4)
+    split = [c for c in st.profile_end() if c["kind"] == "split_block"]
+    assert sorted(c["grad_dtype"] for c in split) == ["bf16", "f32"], split
+
+
 DEGENERATE = [
     # (lr, betas, eps, wd, first t): no momentum memory (m = g); no second-moment memory
     # (v = mean g^2 of this step); a pure decay step (lr = 0 leaves theta unchanged and

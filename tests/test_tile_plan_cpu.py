@@ -129,6 +129,39 @@ def test_edges_and_huge_tensors(checker, tmp_path):
     assert "class H" in out and "class U" in out
 
 
+@pytest.mark.parametrize("seed", range(12))
+def test_random_tables(checker, tmp_path, seed):
+    """Seeded random workloads: several tensors of either gradient type, each with explicit
+    blocks drawn from every class's range (1-32, 33-2042, 2043-65536, beyond 65536) or a
+    uniform period (divisors of a random size: small, register-held, streamed or split),
+    at both code widths; every plan passes the library's check."""
+    rng = np.random.default_rng(1000 + seed)
+    code_bits = int(rng.choice([8, 4]))
+    explicit = bool(rng.integers(2))
+    n_t = int(rng.integers(1, 6))
+    numels, periods, dts, starts = [], [], [], []
+    for _ in range(n_t):
+        if explicit:
+            ranges = [(1, 33), (33, 2043), (2043, 65537), (65537, 300000)]
+            sizes = []
+            for _ in range(int(rng.integers(1, 400))):
+                lo, hi = ranges[int(rng.choice(4, p=[0.3, 0.4, 0.25, 0.05]))]
+                sizes.append(int(rng.integers(lo, hi)))
+            offs = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+            numels.append(int(offs[-1]))
+            periods.append(0)
+            starts.append(offs)
+        else:
+            p = int(rng.choice([1, 3, 4, 20, 31, 32, 64, 768, 999, 2048, 8192, 8196, 70000]))
+            nb = int(rng.integers(1, 5000 if p < 8192 else 40))
+            numels.append(p * nb)
+            periods.append(p)
+        dts.append(int(rng.integers(2)))
+    path = tmp_path / "r.bin"
+    _write(path, numels, periods, dts, code_bits, starts=starts if explicit else None)
+    _assert_ok(*_run(checker, path))
+
+
 @pytest.mark.parametrize("corruption", [1, 2, 3, 4, 5])
 def test_check_refuses_planted_mistakes(checker, tmp_path, corruption):
     """The plan check is not vacuous: a repeated, shifted or dropped tile, a wrong chunk
