@@ -65,6 +65,35 @@ def test_lanes_balance_and_order(checker, name):
     assert abs(sum(lanes[0]) - sum(lanes[1])) <= longest + 1e-9, lanes
 
 
+@pytest.mark.parametrize("seed", range(10))
+def test_random_shapes_stay_in_bounds(checker, seed):
+    """Seeded random models: matrices of random sides (1 to 3000, some repeated so that
+    they batch, in both orientations), vectors, tiny and very tall or wide ones; every
+    product of every group passes the library's check and stays inside its buffers, and
+    the lanes cover every group once."""
+    import numpy as np
+    rng = np.random.default_rng(500 + seed)
+    shapes = []
+    for _ in range(int(rng.integers(1, 30))):
+        kind = int(rng.integers(6))
+        if kind == 0:
+            r, c = 1, int(rng.integers(1, 5000))
+        elif kind == 1:
+            r, c = int(rng.integers(1, 5000)), 1
+        elif kind == 2:
+            r, c = int(rng.integers(2, 40)), int(rng.integers(2, 40))
+        elif kind == 3:
+            r, c = int(rng.integers(2, 64)), int(rng.integers(2000, 60000))
+        else:
+            r, c = int(rng.integers(2, 3000)), int(rng.integers(2, 3000))
+        shapes += [(r, c)] * int(rng.integers(1, 4))
+        if rng.integers(2):
+            shapes.append((c, r))   # the other orientation of the same matrix
+    rc, out = _run(checker, [(r, r * c) for r, c in shapes])
+    assert rc == 0, out
+    assert out.strip().splitlines()[-1].startswith("ok:"), out
+
+
 def test_odd_shapes_stay_in_bounds(checker):
     shapes = [(64, 192), (192, 64), (128, 128), (1, 300), (300, 1), (3, 5), (64, 4096),
               (5000, 48), (1003, 40), (77, 9), (1003, 40), (130, 129), (1008, 40), (40, 1008),

@@ -129,7 +129,7 @@ def test_edges_and_huge_tensors(checker, tmp_path):
     assert "class H" in out and "class U" in out
 
 
-@pytest.mark.parametrize("seed", range(12))
+@pytest.mark.parametrize("seed", range(40))
 def test_random_tables(checker, tmp_path, seed):
     """Seeded random workloads: several tensors of either gradient type, each with explicit
     blocks drawn from every class's range (1-32, 33-2042, 2043-65536, beyond 65536) or a
