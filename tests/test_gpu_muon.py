@@ -146,6 +146,36 @@ def test_muon_parity_shapes(shapes, dtype):
         mr.step(t, where=f"t={t}")
 
 
+@pytest.mark.parametrize("seed", range(12))
+def test_muon_random_models(seed):
+    """Seeded random models: up to eight tensors of random sides (vectors, tiny, square,
+    tall and wide, with repeats and the other orientation of a shape, so that groups batch
+    tensors of both orientations and the lanes get several groups), either gradient type,
+    both code widths; two steps against the oracle."""
+    dev = _dev()
+    rng = np.random.default_rng(900 + seed)
+    shapes = []
+    for _ in range(int(rng.integers(1, 6))):
+        kind = int(rng.integers(5))
+        if kind == 0:
+            r, c = (1, int(rng.integers(2, 900))) if rng.integers(2) else (int(rng.integers(2, 900)), 1)
+        elif kind == 1:
+            r, c = int(rng.integers(2, 24)), int(rng.integers(2, 24))
+        elif kind == 2:
+            r, c = int(rng.integers(8, 64)), int(rng.integers(500, 3000))
+        else:
+            r, c = int(rng.integers(16, 400)), int(rng.integers(16, 400))
+        shapes += [(r, c)] * int(rng.integers(1, 3))
+        if rng.integers(2):
+            shapes.append((c, r))
+    shapes = shapes[:8]
+    dtype = torch.bfloat16 if rng.integers(2) else torch.float32
+    code_bits = int(rng.choice([8, 4]))
+    mr = MuonRun(shapes, dtype, dev, seed=seed, code_bits=code_bits)
+    for t in (1, 2):
+        mr.step(t, where=f"seed {seed} {shapes} {code_bits}-bit t={t}")
+
+
 @pytest.mark.parametrize("code_bits", [8, 4])
 @pytest.mark.parametrize("nesterov", [True, False])
 def test_muon_code_widths_and_nesterov(code_bits, nesterov):
