@@ -133,24 +133,25 @@ struct gefen_state {
     int64_t* muon_u_off = nullptr;        // code index of each tensor's first element
     int32_t* muon_tensor_of = nullptr;
     std::vector<NsGroup> muon_groups;
-    // The shape groups are split over two lanes that run concurrently: lane 0 on the
-    // caller's stream, lane 1 on a stream of the library's own (forked after the norms,
-    // joined at the end of the step). Each lane has its own Newton-Schulz buffers.
+    // The shape groups are split over lanes that run concurrently: lane 0 on the caller's
+    // stream, the others on streams of the library's own (forked after the norms, joined
+    // at the end of the step). Each lane has its own Newton-Schulz buffers.
     struct MuonLane {
         NsLaneBuffers buf{};            // X and X^T (ping-pong), A, B, split-K partials
         NsLaneSizes size;
         std::vector<int32_t> groups;    // indices into muon_groups, in launch order
     };
-    MuonLane muon_lane[2];
-    hipStream_t muon_side = nullptr;    // lane 1's stream (default priority)
-    hipEvent_t muon_fork = nullptr, muon_join = nullptr;
+    MuonLane muon_lane[kNsLanes];
+    hipStream_t muon_side[kNsLanes - 1] = {};   // lane l >= 1 runs on muon_side[l - 1]
+    hipEvent_t muon_fork = nullptr;              // (default priority streams)
+    hipEvent_t muon_join[kNsLanes - 1] = {};
 
     // measurement: events[(step * classes + c) * 2 + {0 start, 1 stop}]
     bool prof_armed = false;
     int32_t prof_max_steps = 0, prof_steps = 0;
     std::vector<hipEvent_t> prof_events;
     // Gefen-Muon steps: per step, events [step start, codec + norms end, step end], all
-    // on the caller's stream (the step end follows the join of lane 1)
+    // on the caller's stream (the step end follows the joins of the other lanes)
     int32_t muon_prof_steps = 0;
     std::vector<hipEvent_t> muon_prof_events;
 
@@ -171,8 +172,10 @@ struct gefen_state {
     {
         prof_free();
         if (muon_fork) (void)hipEventDestroy(muon_fork);
-        if (muon_join) (void)hipEventDestroy(muon_join);
-        if (muon_side) (void)hipStreamDestroy(muon_side);
+        for (hipEvent_t e : muon_join)
+            if (e) (void)hipEventDestroy(e);
+        for (hipStream_t s : muon_side)
+            if (s) (void)hipStreamDestroy(s);
         for (void* p : dev_allocs) (void)hipFree(p);
         if (segs_pinned) (void)hipHostFree(segs_pinned);
         for (hipEvent_t e : seg_evt)
@@ -1239,7 +1242,7 @@ int muon_codec_tiles(gefen_state* st, std::vector<Tile>& tiles, std::vector<int6
 int muon_lane_resources(gefen_state* st)
 {
     int rc;
-    for (int l = 0; l < 2; ++l) {
+    for (int l = 0; l < kNsLanes; ++l) {
         gefen_state::MuonLane& ln = st->muon_lane[l];
         if (ln.groups.empty()) continue;
         ln.size = ns_lane_sizes(st->muon_groups, ln.groups);
@@ -1257,10 +1260,12 @@ int muon_lane_resources(gefen_state* st)
             if (!why.empty()) return fail(GEFEN_EINVAL, "internal: %s", why.c_str());
         }
     }
-    if (!st->muon_lane[1].groups.empty()) {
-        GEFEN_HIP(hipStreamCreateWithFlags(&st->muon_side, hipStreamNonBlocking));
-        GEFEN_HIP(hipEventCreateWithFlags(&st->muon_fork, hipEventDisableTiming));
-        GEFEN_HIP(hipEventCreateWithFlags(&st->muon_join, hipEventDisableTiming));
+    for (int l = 1; l < kNsLanes; ++l) {
+        if (st->muon_lane[l].groups.empty()) continue;
+        if (!st->muon_fork)
+            GEFEN_HIP(hipEventCreateWithFlags(&st->muon_fork, hipEventDisableTiming));
+        GEFEN_HIP(hipStreamCreateWithFlags(&st->muon_side[l - 1], hipStreamNonBlocking));
+        GEFEN_HIP(hipEventCreateWithFlags(&st->muon_join[l - 1], hipEventDisableTiming));
     }
     return GEFEN_OK;
 }
@@ -1356,9 +1361,9 @@ int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, voi
     const std::string why = ns_plan_groups(n, rows, st->numel.data(), st->muon_groups, order);
     if (!why.empty()) return fail(GEFEN_EINVAL, "%s", why.c_str());
     {
-        std::vector<int32_t> lanes[2];
+        std::vector<int32_t> lanes[kNsLanes];
         ns_assign_lanes(st->muon_groups, lanes);
-        for (int l = 0; l < 2; ++l) st->muon_lane[l].groups = lanes[l];
+        for (int l = 0; l < kNsLanes; ++l) st->muon_lane[l].groups = lanes[l];
     }
 
     st->muon_n_tiles = static_cast<int64_t>(tiles.size());
@@ -1417,20 +1422,23 @@ int gefen_muon_step(gefen_state* st, const gefen_tensor* params, const gefen_ten
     const float ca = static_cast<float>(ns_a), cb = static_cast<float>(ns_b),
                 cc = static_cast<float>(ns_c);
     const MuonGroupRun run{ca, cb, cc, decay, lr, ns_steps};
-    // The two lanes' phases are enqueued alternately, so that both streams hold work from
-    // the start (enqueueing one lane whole first would leave the other idle for as long
-    // as the host takes to launch the first one's kernels).
-    gefen_state::MuonLane& l1 = st->muon_lane[1];
-    if (!l1.groups.empty()) {
-        GEFEN_HIP(hipEventRecord(st->muon_fork, stream));
-        GEFEN_HIP(hipStreamWaitEvent(st->muon_side, st->muon_fork, 0));
-    }
+    // The lanes' phases are enqueued in turn, so that every stream holds work from the
+    // start (enqueueing one lane whole first would leave the others idle for as long as
+    // the host takes to launch the first one's kernels).
+    if (st->muon_fork) GEFEN_HIP(hipEventRecord(st->muon_fork, stream));
     struct Cursor {
         const gefen_state::MuonLane* lane;
         hipStream_t s;
         size_t gi;
         int phase, cur;
-    } cursors[2] = {{&l1, st->muon_side, 0, 0, 0}, {&st->muon_lane[0], stream, 0, 0, 0}};
+    } cursors[kNsLanes];
+    for (int l = 1; l <= kNsLanes; ++l) {   // the side lanes, then lane 0
+        const int li = l % kNsLanes;
+        hipStream_t s = li == 0 ? stream : st->muon_side[li - 1];
+        if (li != 0 && !st->muon_lane[li].groups.empty())
+            GEFEN_HIP(hipStreamWaitEvent(s, st->muon_fork, 0));
+        cursors[l - 1] = Cursor{&st->muon_lane[li], s, 0, 0, 0};
+    }
     for (bool more = true; more;) {
         more = false;
         for (Cursor& c : cursors) {
@@ -1444,9 +1452,10 @@ int gefen_muon_step(gefen_state* st, const gefen_tensor* params, const gefen_ten
             more = more || c.gi < c.lane->groups.size();
         }
     }
-    if (!l1.groups.empty()) {
-        GEFEN_HIP(hipEventRecord(st->muon_join, st->muon_side));
-        GEFEN_HIP(hipStreamWaitEvent(stream, st->muon_join, 0));
+    for (int l = 1; l < kNsLanes; ++l) {
+        if (st->muon_lane[l].groups.empty()) continue;
+        GEFEN_HIP(hipEventRecord(st->muon_join[l - 1], st->muon_side[l - 1]));
+        GEFEN_HIP(hipStreamWaitEvent(stream, st->muon_join[l - 1], 0));
     }
     if (prof) {
         GEFEN_HIP(hipEventRecord(ev[st->muon_prof_stride() - 1], stream));

@@ -439,10 +439,12 @@ inline std::string ns_plan_groups(int32_t n, const int64_t* rows, const int64_t*
 // latency of a small launch (a product of a few dozen workgroups takes 10-50 us whatever
 // its flops), so that latency-bound groups such as a position embedding count for the
 // time they hold a lane rather than for their flops.
+constexpr double kNsLaunchUs = 15.0;
+
 inline double ns_group_cost(const NsShape& sh)
 {
     constexpr double kFlopsPerUs = 6.0e8;   // ~600 TFLOP/s on the model shapes
-    constexpr double kLaunchUs = 15.0;
+    constexpr double kLaunchUs = kNsLaunchUs;
     const double m = static_cast<double>(sh.m), n = static_cast<double>(sh.ldx);
     const double c = static_cast<double>(sh.count);
     if (sh.m < 2) return kLaunchUs;   // one vector kernel for all iterations
@@ -453,31 +455,49 @@ inline double ns_group_cost(const NsShape& sh)
     return t;
 }
 
-// Two lanes (streams that run concurrently): groups in decreasing order of estimated
-// time, each to the lane with less so far; then lane 0 runs its groups shortest first
-// and lane 1 longest first, so that the short, latency-bound groups of either lane run
-// beside a long group of the other rather than alone at the end of the phase (measured
-// on the GPT-2 125M shapes: the position-embedding group ran its 0.4 ms alone after the
-// other lane had finished).
-inline void ns_assign_lanes(const std::vector<NsGroup>& groups, std::vector<int32_t> lanes[2])
+// The estimated time of a group whose every launch takes the latency of a small launch:
+// the one vector kernel, or three products (four with the split-K reduction).
+inline double ns_group_floor(const NsShape& sh)
+{
+    if (sh.m < 2) return kNsLaunchUs;
+    return kNsLaunchUs * (sh.splits > 1 ? 4.0 : 3.0);
+}
+
+// Three lanes (streams that run concurrently). The latency-bound groups (estimated time
+// at the floor of their launches: vectors, small matrices such as a position embedding)
+// share lane 2, so that they run beside the long products from the start and hold
+// neither long lane; the others, in decreasing order of estimated time, each go to lane 0
+// or 1, whichever has less so far, and every lane runs its groups longest first. With
+// no long group at all, the latency-bound ones are split over lanes 0 and 1 the same way.
+// (Measured on the GPT-2 125M shapes: with two lanes, the short groups sharing a lane
+// with the MLP group waited for workgroup slots behind the other lane's long products
+// and held the MLP group back until the end of the phase.)
+constexpr int kNsLanes = 3;
+
+inline void ns_assign_lanes(const std::vector<NsGroup>& groups,
+                            std::vector<int32_t> (&lanes)[kNsLanes])
 {
     std::vector<int32_t> byw(groups.size());
     std::vector<double> cost(groups.size());
+    bool any_long = false;
     for (size_t gi = 0; gi < groups.size(); ++gi) {
         byw[gi] = static_cast<int32_t>(gi);
         cost[gi] = ns_group_cost(groups[gi].shape);
+        any_long = any_long || cost[gi] > ns_group_floor(groups[gi].shape);
     }
     std::stable_sort(byw.begin(), byw.end(),
                      [&](int32_t a, int32_t b) { return cost[a] > cost[b]; });
     double load[2] = {0.0, 0.0};
-    lanes[0].clear();
-    lanes[1].clear();
+    for (auto& l : lanes) l.clear();
     for (int32_t gi : byw) {
+        if (any_long && cost[gi] <= ns_group_floor(groups[gi].shape)) {
+            lanes[2].push_back(gi);
+            continue;
+        }
         const int l = load[1] < load[0] ? 1 : 0;
         lanes[l].push_back(gi);
         load[l] += cost[gi];
     }
-    std::reverse(lanes[0].begin(), lanes[0].end());   // shortest first
 }
 
 // Elements of one lane's buffers: X and X^T (two of each), the two m x m products, the

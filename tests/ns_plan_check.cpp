@@ -2,7 +2,7 @@
 // built with address and undefined-behaviour sanitizers by tests/test_ns_plan_cpu.py.
 //
 // Input (stdin): a tensor count, then one "rows numel" line per tensor. The program plans
-// the shape groups and the two lanes exactly as gefen_muon_init does, sizes each lane's
+// the shape groups and the lanes exactly as gefen_muon_init does, sizes each lane's
 // buffers, runs the library's own checks (ns_check_group), and then walks every work item
 // of every product of both ping-pong parities: the item's decoded batch entry, K chunk and
 // tile must be in range, every (b, s, tile) must be decoded exactly once, and the furthest
@@ -146,14 +146,16 @@ int main()
         std::puts("the groups do not cover every tensor once");
         return 1;
     }
-    std::vector<int32_t> lanes[2];
+    std::vector<int32_t> lanes[kNsLanes];
     ns_assign_lanes(groups, lanes);
-    if (lanes[0].size() + lanes[1].size() != groups.size()) {
+    size_t on_lanes = 0;
+    for (const auto& l : lanes) on_lanes += l.size();
+    if (on_lanes != groups.size()) {
         std::puts("the lanes do not cover every group once");
         return 1;
     }
     int64_t products = 0, items = 0;
-    for (int l = 0; l < 2; ++l) {
+    for (int l = 0; l < kNsLanes; ++l) {
         const NsLaneSizes z = ns_lane_sizes(groups, lanes[l]);
         NsLaneBuffers lb{{fake16(8 * l + 0), fake16(8 * l + 1)},
                          {fake16(8 * l + 2), fake16(8 * l + 3)},
@@ -167,10 +169,11 @@ int main()
                 return 1;
             }
             std::printf("lane %d group %d: %lld x (%lld x %lld), ldx %lld ldm %lld, %d parts, "
-                        "Gram splits %d (chunk %d), tiles %d / %d / %d, cost %.3f\n", l, gi,
+                        "Gram splits %d (chunk %d), tiles %d / %d / %d, floor %.3f, cost %.3f\n", l, gi,
                         (long long)sh.count, (long long)sh.m, (long long)sh.n, (long long)sh.ldx,
                         (long long)sh.ldm, static_cast<int>(g.parts.size()), sh.splits, sh.kchunk,
-                        sh.tile_gram, sh.tile_poly, sh.tile_comb, ns_group_cost(sh));
+                        sh.tile_gram, sh.tile_poly, sh.tile_comb, ns_group_floor(sh),
+                        ns_group_cost(sh));
             if (sh.m < 2) continue;
             for (int cur = 0; cur < 2; ++cur) {
                 NsGemmArgs prods[3];
