@@ -287,7 +287,7 @@ int gefen_profile_end(gefen_state* st, int32_t cap, int32_t* n_classes, int32_t*
  *  rows    host int64[n_tensors]: tensor i is the rows[i] x (numel_i / rows[i]) matrix,
  *          row-major (a 1-D tensor is 1 x numel). rows[i] must divide numel_i.
  * Allocates the bfloat16 momentum matrix (2 bytes per parameter) and the Newton-Schulz
- * buffers of each of two lanes, sized for the lane's largest group of tensors that share
+ * buffers of each of three lanes, sized for the lane's largest group of tensors that share
  * one wide shape (X and X^T twice, the two m x m products: about 8 bytes per element of
  * that group), and checks every matrix product of the steps against them on the host;
  * synchronises `stream`. Call once per state.
@@ -310,10 +310,10 @@ int gefen_muon_init(gefen_state* st, const int64_t* rows, int32_t n_tensors, voi
  *  params, grads  as for gefen_step; momentum in [0, 1); ns_steps in [0, 100];
  *  ns_eps > 0. Muon's defaults: ns_steps 5, (ns_a, ns_b, ns_c) =
  *  (3.4445, -4.7750, 2.0315), ns_eps 1e-7, nesterov 1.
- * Asynchronous on `stream`; no allocation. The shape groups are split over two lanes
- * that run concurrently: one on `stream`, one on a stream the state owns, which waits
- * for the norms on `stream`; `stream` then waits for it, so all of the step's work is
- * ordered before later work on `stream`. Refits (gefen_fit_codebook) apply as for
+ * Asynchronous on `stream`; no allocation. The shape groups are split over three lanes
+ * that run concurrently: one on `stream`, the others on streams the state owns, which
+ * wait for the norms on `stream`; `stream` then waits for them, so all of the step's
+ * work is ordered before later work on `stream`. Refits (gefen_fit_codebook) apply as for
  * gefen_step. The bfloat16 momentum matrix of the last step can be read as array 6 of
  * gefen_read_state (uint16 bit patterns at each element's code index).
  * Errors: EINVAL (arguments, gefen_muon_init not called), EDTYPE, EHIP.
@@ -326,7 +326,7 @@ int gefen_muon_step(gefen_state* st, const gefen_tensor* params, const gefen_ten
 /* Measurement of Gefen-Muon steps (after gefen_muon_init and gefen_profile_begin):
  * sums over the profiled steps of the codec time (codec and norms) and of the
  * orthogonalisation wall time (normalise, Newton-Schulz and update of every shape
- * group, on both of the step's streams, from the end of the norms to the join), in
+ * group, on all of the step's streams, from the end of the norms to the joins), in
  * milliseconds, from HIP events on the step's stream; then disarms like
  * gefen_profile_end. Errors: EINVAL (NULL), EHIP. */
 int gefen_muon_profile_end(gefen_state* st, int32_t* steps, double* codec_ms, double* ortho_ms);

@@ -228,7 +228,7 @@ class GefenState:
 
     def muon_profile_end(self):
         """Profiled Gefen-Muon steps: {steps, codec_ms, ortho_ms} (sums; ortho_ms is the
-        wall time of normalise + Newton-Schulz + update over both lanes)."""
+        wall time of normalise + Newton-Schulz + update over all lanes)."""
         n = ctypes.c_int32()
         a, b = ctypes.c_double(), ctypes.c_double()
         _check(_lib.gefen_muon_profile_end(self._h, ctypes.byref(n), ctypes.byref(a),

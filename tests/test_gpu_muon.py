@@ -212,11 +212,11 @@ def test_muon_gpt2_mlp_shape():
     print("worst O deviation (max, mean) / max|O|:", w)
 
 
-def test_muon_two_lanes_are_deterministic():
-    """The shape groups run on two concurrent streams; the same state and inputs give the
-    same parameters bit for bit in two runs from scratch (no race between the lanes and
-    no order-dependent accumulation), including the split-K Gram, the vector kernel,
-    tall and wide parts and groups on both lanes."""
+def test_muon_lanes_are_deterministic():
+    """The shape groups run on three concurrent streams; the same state and inputs give
+    the same parameters bit for bit in two runs from scratch (no race between the lanes
+    and no order-dependent accumulation), including the split-K Gram, the vector kernel,
+    tall and wide parts and groups on every lane."""
     dev = _dev()
     shapes = [(5000, 48), (64, 128), (128, 64), (1, 77), (96, 96), (300, 1), (64, 128),
               (768, 3072), (3072, 768)]
