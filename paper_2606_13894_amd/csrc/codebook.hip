@@ -342,7 +342,9 @@ __global__ __launch_bounds__(kThreads) void k_dp_prep(const uint64_t* __restrict
 // j + 1 rebuilds D[j][.] from them while staging, in chunk order with ties to the
 // smaller l, and its last row of workgroups (whose chunks cover every l) stores the
 // final D[j][.] and split[j][.] rows for the backtrack. k_dp_final reduces the last
-// level.
+// level. Level j < keff takes only the rows r <= b - (keff - j): a longer prefix leaves
+// too few bins for the entries still to come, so no path to D[keff][b] passes through
+// it (the rows it does take, and their candidates, are the ones the full scan has).
 // ---------------------------------------------------------------------------------
 __device__ __forceinline__ int dp_chunks(int jj, int r)
 {
@@ -381,9 +383,10 @@ __global__ __launch_bounds__(kDpThreads) void k_dp_level(int32_t nbins, int32_t 
         if (blockIdx.x != 0) return;
         r0 = r1 = b;
     } else {
+        const int rmax = b - keff + j;
         r0 = j + static_cast<int>(blockIdx.x) * kDpRows;
-        if (r0 > b) return;
-        r1 = r0 + kDpRows - 1 < b ? r0 + kDpRows - 1 : b;
+        if (r0 > rmax) return;
+        r1 = r0 + kDpRows - 1 < rmax ? r0 + kDpRows - 1 : rmax;
     }
     const int hi_max = j == 1 ? 1 : r1;
     const int l0 = j + static_cast<int>(blockIdx.y) * kDpChunk;
@@ -400,7 +403,7 @@ __global__ __launch_bounds__(kDpThreads) void k_dp_level(int32_t nbins, int32_t 
     const int32_t* pa_prev = at<int32_t>(ws, L.pa) + ((j - 1) & 1) * pstride;
     double* pv_cur = at<double>(ws, L.pv) + (j & 1) * pstride;
     int32_t* pa_cur = at<int32_t>(ws, L.pa) + (j & 1) * pstride;
-    const bool last_rows = j == keff || static_cast<int>(blockIdx.x) == (b - j) / kDpRows;
+    const bool last_rows = j == keff || static_cast<int>(blockIdx.x) == (b - keff) / kDpRows;
     for (int i = threadIdx.x; i <= l1 - l0; i += kDpThreads) {
         const int l = l0 + i;
         sZ0[i] = Z0[l - 1];
