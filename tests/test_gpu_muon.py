@@ -212,6 +212,20 @@ def test_muon_gpt2_mlp_shape():
     print("worst O deviation (max, mean) / max|O|:", w)
 
 
+def test_muon_three_lanes_against_the_oracle():
+    """A model whose groups fill all three lanes: four 1024 x 2048 matrices (three wide,
+    one tall; lane 0), four 768 x 2304 ones (lane 1), both long enough to count for more
+    than their launches and with split-K Grams, and the latency-bound small matrices and
+    vectors (lane 2). Every tensor against the oracle, teacher-forced, two steps."""
+    dev = _dev()
+    shapes = ([(1024, 2048)] * 3 + [(2048, 1024)] + [(768, 2304)] * 4 +
+              [(64, 128), (128, 64), (1, 300), (96, 96), (300, 1)])
+    mr = MuonRun(shapes, torch.bfloat16, dev, seed=31)
+    for t in (1, 2):
+        w = mr.step(t, where=f"three lanes t={t}")
+    print("worst O deviation (max, mean) / max|O|:", w)
+
+
 def test_muon_lanes_are_deterministic():
     """The shape groups run on three concurrent streams; the same state and inputs give
     the same parameters bit for bit in two runs from scratch (no race between the lanes
@@ -219,7 +233,8 @@ def test_muon_lanes_are_deterministic():
     tall and wide parts and groups on every lane."""
     dev = _dev()
     shapes = [(5000, 48), (64, 128), (128, 64), (1, 77), (96, 96), (300, 1), (64, 128),
-              (768, 3072), (3072, 768)]
+              (768, 3072), (3072, 768), (1024, 2048), (1024, 2048), (2048, 1024), (1024, 2048),
+              (768, 2304), (768, 2304), (768, 2304), (768, 2304)]
     runs = []
     for _ in range(2):
         torch.manual_seed(21)
